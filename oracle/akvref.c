@@ -1,0 +1,668 @@
+/*
+ * AnchorKV oracle: a plain, slow CPU reference of what the compression pass and
+ * the decode attention compute, written from the paper (arXiv 2608.02901,
+ * "AnchorKV: Anchor-Residual KV Cache Compression").
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing in the product library links, loads or
+ * calls this file; only the tests, the package's smoke check and the CPU
+ * baseline leg of the benchmark do.  It shares no code with the HIP path.
+ *
+ * Arithmetic conventions (the canonical forms both implementations follow so
+ * that every integer output -- anchor sets, anchor indices, coefficient bits,
+ * residual codes -- is unique):
+ *   - fp64 everywhere the paper gives a formula, except where a stored value
+ *     has a narrower type (coefficients, residuals, rotated residuals, codes).
+ *   - dot64(x, y): the fp64 products x_j*y_j (exact for fp32 and bf16 data)
+ *     summed sequentially for j = 0..D-1.  Built with -ffp-contract=off, so no
+ *     fused multiply-add ever merges a product into the running sum.
+ *   - fp32 steps are single IEEE roundings in the order written.
+ *   - bf16 conversion is round-to-nearest-even of the fp32 value.
+ *
+ * Parity status of each function (pins live in tests/test_oracle_*.py):
+ *   pinned   : splitmix64 (published first output), Hadamard (dense Sylvester
+ *              product, orthogonality), codec levels (Lloyd's iteration for a
+ *              unit Gaussian), byte budget (the worked example of App. A.1),
+ *              assignment (exhaustive search, closed-form special cases,
+ *              projection orthogonality), decode attention (all-anchor case
+ *              equals dense attention; output-error theorem of App. A.4),
+ *              selector (brute force on tiny inputs).
+ *   parity unpinned beyond self-consistency: the absmax scale readings of the
+ *              codec (Sec. 3.1 / App. A.1 leave the scale rule ambiguous) and
+ *              the utility values (Eq. utilities; the paper prints none) --
+ *              the utilities are additionally checked by a finite-difference
+ *              test of the two-channel expansion (Eq. channels).
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+/* ------------------------------------------------------------------------ */
+/* Primitives                                                                 */
+/* ------------------------------------------------------------------------ */
+
+/* SplitMix64 (Steele, Lea & Flood 2014): the first output of a generator
+ * whose state is x.  Used as a counter-based hash for the uniform anchor share
+ * (Sec. 3.2, anchor selection) and for the Hadamard sign pattern (App. A.1). */
+uint64_t akvref_splitmix64(uint64_t x) {
+  uint64_t z = x + 0x9E3779B97F4A7C15ULL;
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ULL;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBULL;
+  return z ^ (z >> 31);
+}
+
+/* Seeds derived from the user seed: one stream for anchor sampling, one for
+ * the sign pattern s of the randomized Hadamard rotation. */
+static uint64_t anchor_seed(uint64_t seed) { return akvref_splitmix64(seed ^ 1ULL); }
+static uint64_t sign_seed(uint64_t seed) { return akvref_splitmix64(seed ^ 2ULL); }
+
+static float bf16_rne(float f) {
+  uint32_t u;
+  memcpy(&u, &f, 4);
+  u = u + 0x7FFFu + ((u >> 16) & 1u);
+  u &= 0xFFFF0000u;
+  memcpy(&f, &u, 4);
+  return f;
+}
+
+/* Sequential fp64 dot product (canonical order). */
+static double dot64(const double* x, const double* y, int D) {
+  double s = 0.0;
+  for (int j = 0; j < D; ++j) s += x[j] * y[j];
+  return s;
+}
+
+/* Sign pattern s in {+1,-1}^D of the rotation U = H_D diag(s)/sqrt(D)
+ * (App. A.1, Eq. hadamard): s_j = -1 when the top bit of the hash of j is set. */
+void akvref_hadamard_signs(uint64_t seed, int D, float* s) {
+  uint64_t ss = sign_seed(seed);
+  for (int j = 0; j < D; ++j) s[j] = (akvref_splitmix64(ss ^ (uint64_t)j) >> 63) ? -1.0f : 1.0f;
+}
+
+/* Unnormalized fast Walsh-Hadamard transform in fp32, Sylvester ordering:
+ * stages h = 1, 2, 4, ..., D/2; in stage h every pair (i, i+h) with i & h == 0
+ * becomes (z_i + z_{i+h}, z_i - z_{i+h}).  Applying it twice multiplies by D. */
+void akvref_fwht(float* z, int D) {
+  for (int h = 1; h < D; h <<= 1)
+    for (int i = 0; i < D; ++i)
+      if ((i & h) == 0) {
+        float a = z[i], b = z[i + h];
+        z[i] = a + b;
+        z[i + h] = a - b;
+      }
+}
+
+/* ------------------------------------------------------------------------ */
+/* Residual codec (Sec. 3.1 "Residual quantization"; App. A.1 rotation and    */
+/* codebook).                                                                 */
+/* ------------------------------------------------------------------------ */
+
+/* Four-level Lloyd-Max quantizer for a unit Gaussian source (Lloyd 1957,
+ * Max 1960): reconstruction levels +-L0, +-L1 and decision threshold T. */
+#define AKV_LM_L0 0.4527800f
+#define AKV_LM_L1 1.5104176f
+#define AKV_LM_T 0.9815988f
+
+enum { SCALE_ABSMAX_OUTER = 0, SCALE_ABSMAX_LITERAL = 1, SCALE_RMS = 2 };
+
+/* Scale of one group of rotated coordinates: the Gaussian standard deviation
+ * the codebook is applied at.  The paper names a per-token absmax scale; the
+ * three readings of how the absmax enters are:
+ *   OUTER   : sigma = A / L1, so the largest coordinate lands on the outer level;
+ *   LITERAL : sigma = A (coordinates divided by the absmax, then quantized);
+ *   RMS     : sigma = sqrt(sum z^2 / G) (the marginal the rotation produces). */
+static float group_scale(const float* z, int G, int mode) {
+  if (mode == SCALE_RMS) {
+    float acc = 0.0f;
+    for (int j = 0; j < G; ++j) {
+      float sq = z[j] * z[j];
+      acc = acc + sq;
+    }
+    float ms = acc / (float)G;
+    return sqrtf(ms);
+  }
+  float A = 0.0f;
+  for (int j = 0; j < G; ++j) {
+    float m = fabsf(z[j]);
+    if (m > A) A = m;
+  }
+  if (mode == SCALE_ABSMAX_LITERAL) return A;
+  return A / AKV_LM_L1;
+}
+
+/* Encode one residual r[D] (fp32): z = FWHT(s * r); per group of G
+ * coordinates a scale sigma; code in {0,1,2,3} for levels {-L1,-L0,+L0,+L1};
+ * four codes per byte, coordinate j in byte j/4 at bits 2*(j%4)..2*(j%4)+1. */
+void akvref_codec_encode(const float* r, int D, int G, int mode, uint64_t seed,
+                         uint8_t* codes, float* scales) {
+  float* s = (float*)malloc(sizeof(float) * D);
+  float* z = (float*)malloc(sizeof(float) * D);
+  akvref_hadamard_signs(seed, D, s);
+  for (int j = 0; j < D; ++j) z[j] = s[j] * r[j];
+  akvref_fwht(z, D);
+  memset(codes, 0, (size_t)D / 4);
+  for (int g0 = 0; g0 < D; g0 += G) {
+    float sigma = group_scale(z + g0, G, mode);
+    scales[g0 / G] = sigma;
+    float T = sigma * AKV_LM_T;
+    for (int j = g0; j < g0 + G; ++j) {
+      int outer = fabsf(z[j]) > T;
+      int c = (z[j] < 0.0f) ? (outer ? 0 : 1) : (outer ? 3 : 2);
+      codes[j / 4] |= (uint8_t)(c << (2 * (j % 4)));
+    }
+  }
+  free(s);
+  free(z);
+}
+
+/* Decode: zhat_j = sigma * level(code_j); r~ = s * FWHT(zhat) / D, i.e.
+ * U^T applied to the dequantized rotated coordinates (App. A.1, Eq. arc-tuple). */
+void akvref_codec_decode(const uint8_t* codes, const float* scales, int D, int G,
+                         uint64_t seed, float* rt) {
+  static const float lev[4] = {-AKV_LM_L1, -AKV_LM_L0, AKV_LM_L0, AKV_LM_L1};
+  float* s = (float*)malloc(sizeof(float) * D);
+  akvref_hadamard_signs(seed, D, s);
+  for (int j = 0; j < D; ++j) {
+    int c = (codes[j / 4] >> (2 * (j % 4))) & 3;
+    rt[j] = scales[j / G] * lev[c];
+  }
+  akvref_fwht(rt, D);
+  float invD = 1.0f / (float)D;
+  for (int j = 0; j < D; ++j) rt[j] = (rt[j] * invD) * s[j];
+  free(s);
+}
+
+/* ------------------------------------------------------------------------ */
+/* Byte budget (Sec. 3.4, Eq. byte-budget; App. A.1, Eq. mfixed and Table of  */
+/* the layout).                                                              */
+/* ------------------------------------------------------------------------ */
+
+/* M_base of one layer: anchors (K and V, elem_bytes each), int64 anchor
+ * positions of the non-window anchors, per-side index (b_a = 2) and
+ * coefficient (b_gamma) for the P = S - W non-window positions, residual
+ * mask words and int32 prefix counts per side, head offsets, int32 position
+ * ids. */
+double akvref_base_bytes(int S, int H, int D, int W, int k, int elem_bytes, int b_gamma) {
+  double P = (double)(S - W);
+  double words = ceil(P / 64.0);
+  return (double)H * (2.0 * elem_bytes * k * D + 8.0 * (k - W) + 2.0 * P * (2.0 + b_gamma)) +
+         24.0 * H * words + 8.0 * (H + 1) + 4.0 * P;
+}
+
+/* N = max{0, floor((theta*M_full - M_base) / b_res)} with b_res the mean of
+ * the key residual cost c_K = D/4 + 4*(D/G) and the value residual cost
+ * c_V = c_K + 1 (one-byte chunk-local position). */
+int64_t akvref_theta_budget(int S, int H, int D, int W, int k, int G, int elem_bytes,
+                            int b_gamma, double theta) {
+  double Mfull = 2.0 * elem_bytes * (double)S * H * D;
+  double Mbase = akvref_base_bytes(S, H, D, W, k, elem_bytes, b_gamma);
+  double cK = D / 4.0 + 4.0 * (D / G);
+  double cV = cK + 1.0;
+  double bres = 0.5 * (cK + cV);
+  double n = floor((theta * Mfull - Mbase) / bres);
+  return n > 0 ? (int64_t)n : 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Observation window and anchor selection (Sec. 3.2; App. A.2 Eq.           */
+/* selector-score).                                                           */
+/* ------------------------------------------------------------------------ */
+
+/* Exact attention of the m = W*g observation rows of one KV head.  Row
+ * w = jj*W + i is query head jj of the group at window offset i, position
+ * S-W+i; it attends causally to t <= S-W+i.  Outputs the row max M_w of the
+ * logits l = q.k/sqrt(D), Z_w = sum_t exp(l - M_w), and y_w = sum_t alpha_wt v_t.
+ * Qg is [g][W][D]. */
+void akvref_obs_head(const double* Kh, const double* Vh, const double* Qg, int S, int D,
+                     int W, int g, double* M, double* Z, double* Y) {
+  int m = W * g;
+  double isd = 1.0 / sqrt((double)D);
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int w = 0; w < m; ++w) {
+    int i = w % W;
+    int last = S - W + i;
+    const double* q = Qg + (size_t)w * D;
+    double* l = (double*)malloc(sizeof(double) * (size_t)(last + 1));
+    double mx = -INFINITY;
+    for (int t = 0; t <= last; ++t) {
+      l[t] = dot64(q, Kh + (size_t)t * D, D) * isd;
+      if (l[t] > mx) mx = l[t];
+    }
+    double z = 0.0;
+    for (int t = 0; t <= last; ++t) z += exp(l[t] - mx);
+    double* y = Y + (size_t)w * D;
+    for (int j = 0; j < D; ++j) y[j] = 0.0;
+    for (int t = 0; t <= last; ++t) {
+      double a = exp(l[t] - mx) / z;
+      const double* v = Vh + (size_t)t * D;
+      for (int j = 0; j < D; ++j) y[j] += a * v[j];
+    }
+    M[w] = mx;
+    Z[w] = z;
+    free(l);
+  }
+}
+
+/* Attention weight alpha_{w,t} of observation row w on position t. */
+static double obs_alpha(const double* Kh, const double* Qg, const double* M, const double* Z,
+                        int S, int D, int W, int w, int t) {
+  int i = w % W;
+  if (t > S - W + i) return 0.0;
+  double l = dot64(Qg + (size_t)w * D, Kh + (size_t)t * D, D) / sqrt((double)D);
+  return exp(l - M[w]) / Z[w];
+}
+
+/* SnapKV-style score of every non-window position t in [0, P):
+ * sc(t) = (1/m) sum_w alpha_{w,t}, then average pooling of width kappa
+ * (odd), centred, zero padding outside [0, P), divided by kappa. */
+void akvref_selector_scores(const double* Kh, const double* Qg, const double* M,
+                            const double* Z, int S, int D, int W, int g, int kappa,
+                            double* sc, double* pooled) {
+  int m = W * g, P = S - W;
+#pragma omp parallel for schedule(static)
+  for (int t = 0; t < P; ++t) {
+    double s = 0.0;
+    for (int w = 0; w < m; ++w) s += obs_alpha(Kh, Qg, M, Z, S, D, W, w, t);
+    sc[t] = s / m;
+  }
+  int half = kappa / 2;
+  for (int t = 0; t < P; ++t) {
+    double s = 0.0;
+    for (int d = -half; d <= half; ++d) {
+      int u = t + d;
+      if (u >= 0 && u < P) s += sc[u];
+    }
+    pooled[t] = s / kappa;
+  }
+}
+
+typedef struct { double v; int t; } score_pos;
+static int by_score_desc(const void* a, const void* b) {
+  const score_pos* x = (const score_pos*)a;
+  const score_pos* y = (const score_pos*)b;
+  if (x->v > y->v) return -1;
+  if (x->v < y->v) return 1;
+  return (x->t > y->t) - (x->t < y->t);
+}
+typedef struct { uint64_t key; int t; } key_pos;
+static int by_key_asc(const void* a, const void* b) {
+  const key_pos* x = (const key_pos*)a;
+  const key_pos* y = (const key_pos*)b;
+  if (x->key < y->key) return -1;
+  if (x->key > y->key) return 1;
+  return (x->t > y->t) - (x->t < y->t);
+}
+static int int_asc(const void* a, const void* b) {
+  int x = *(const int*)a, y = *(const int*)b;
+  return (x > y) - (x < y);
+}
+
+/* Number of attention-scored anchors: floor(rho * (k - W)) in fp64. */
+int akvref_n_top(int k, int W, float rho) { return (int)floor((double)rho * (double)(k - W)); }
+
+/* Anchor set of one head (Algorithm 1, first step): the last W positions,
+ * the n_top best pooled scores among [0, P) (ties to the lower position),
+ * and the remaining k - W - n_top sampled uniformly without replacement from
+ * the rest of [0, P): the positions with the smallest hash
+ * splitmix64(anchor_seed ^ (h << 40) ^ t).  Output sorted ascending; the
+ * anchor index of a position is its rank in this list. */
+void akvref_select_anchors(const double* pooled, int S, int W, int k, float rho, uint64_t seed,
+                           int h, int* anchors) {
+  int P = S - W;
+  int n_top = akvref_n_top(k, W, rho);
+  int n_rand = k - W - n_top;
+  score_pos* sp = (score_pos*)malloc(sizeof(score_pos) * (size_t)(P > 0 ? P : 1));
+  for (int t = 0; t < P; ++t) { sp[t].v = pooled[t]; sp[t].t = t; }
+  qsort(sp, (size_t)P, sizeof(score_pos), by_score_desc);
+  char* taken = (char*)calloc((size_t)(P > 0 ? P : 1), 1);
+  int n = 0;
+  for (int i = 0; i < n_top; ++i) { taken[sp[i].t] = 1; anchors[n++] = sp[i].t; }
+  key_pos* kp = (key_pos*)malloc(sizeof(key_pos) * (size_t)(P > 0 ? P : 1));
+  int nk = 0;
+  uint64_t as = anchor_seed(seed);
+  for (int t = 0; t < P; ++t)
+    if (!taken[t]) {
+      kp[nk].key = akvref_splitmix64(as ^ ((uint64_t)h << 40) ^ (uint64_t)t);
+      kp[nk].t = t;
+      ++nk;
+    }
+  qsort(kp, (size_t)nk, sizeof(key_pos), by_key_asc);
+  for (int i = 0; i < n_rand; ++i) anchors[n++] = kp[i].t;
+  for (int t = P; t < S; ++t) anchors[n++] = t;
+  qsort(anchors, (size_t)k, sizeof(int), int_asc);
+  free(sp);
+  free(taken);
+  free(kp);
+}
+
+/* ------------------------------------------------------------------------ */
+/* Anchor-residual representation (Sec. 3.1, Eqs. nearest-anchor, projection, */
+/* reconstruction).                                                           */
+/* ------------------------------------------------------------------------ */
+
+/* Nearest anchor of one vector x among the k anchor vectors A[k][D] with
+ * squared norms nrm[k]: maximize c_a = d_a*d_a / n_a (d_a = dot64(x, A_a);
+ * c_a = -1 for a zero anchor), ties to the lowest index.  For fixed x this
+ * orders anchors like |cos(x, A_a)|.  Then gamma = d/n in fp64, rounded to
+ * fp32 and, for a bf16 cache, to bf16 (the stored coefficient). */
+static void nearest_anchor(const double* x, const double* A, const double* nrm, int k, int D,
+                           int bf16, int* a_out, double* g_out) {
+  int best = 0;
+  double bc = -INFINITY, bd = 0.0;
+  for (int a = 0; a < k; ++a) {
+    double d = dot64(x, A + (size_t)a * D, D);
+    double c = nrm[a] > 0.0 ? (d * d) / nrm[a] : -1.0;
+    if (c > bc) { bc = c; best = a; bd = d; }
+  }
+  double g64 = nrm[best] > 0.0 ? bd / nrm[best] : 0.0;
+  float g32 = (float)g64;
+  if (bf16) g32 = bf16_rne(g32);
+  *a_out = best;
+  *g_out = (double)g32;
+}
+
+/* Residual against the stored coefficient and anchor, in fp32:
+ * r_j = x_j - fp32(gamma * a_j). */
+static void residual(const double* x, const double* anc, double gamma, int D, float* r) {
+  float g = (float)gamma;
+  for (int j = 0; j < D; ++j) {
+    float p = g * (float)anc[j];
+    r[j] = (float)x[j] - p;
+  }
+}
+
+/* Assignment of an explicit list of tokens of one head against anchors at
+ * positions anchors[k] of X[S][D].  Anchor tokens keep their own index with
+ * gamma = 1 and a zero residual (the layout stores gamma = 1 on anchors). */
+void akvref_assign_tokens(const double* X, int S, int D, const int* anchors, int k, int bf16,
+                          const int* toks, int ntok, int* a_out, double* g_out, float* r_out) {
+  double* A = (double*)malloc(sizeof(double) * (size_t)k * D);
+  double* nrm = (double*)malloc(sizeof(double) * (size_t)k);
+  int* rank = (int*)malloc(sizeof(int) * (size_t)S);
+  for (int t = 0; t < S; ++t) rank[t] = -1;
+  for (int a = 0; a < k; ++a) {
+    memcpy(A + (size_t)a * D, X + (size_t)anchors[a] * D, sizeof(double) * D);
+    nrm[a] = dot64(A + (size_t)a * D, A + (size_t)a * D, D);
+    rank[anchors[a]] = a;
+  }
+#pragma omp parallel for schedule(dynamic, 16)
+  for (int i = 0; i < ntok; ++i) {
+    int t = toks[i];
+    float* r = r_out ? r_out + (size_t)i * D : NULL;
+    if (rank[t] >= 0) {
+      a_out[i] = rank[t];
+      g_out[i] = 1.0;
+      if (r) for (int j = 0; j < D; ++j) r[j] = 0.0f;
+      continue;
+    }
+    nearest_anchor(X + (size_t)t * D, A, nrm, k, D, bf16, &a_out[i], &g_out[i]);
+    if (r) residual(X + (size_t)t * D, A + (size_t)a_out[i] * D, g_out[i], D, r);
+  }
+  free(A);
+  free(nrm);
+  free(rank);
+}
+
+/* Nearest anchor of free vectors (appended tokens) against explicit anchor
+ * vectors A[k][D]. */
+void akvref_assign_vectors(const double* xs, int n, const double* A, int k, int D, int bf16,
+                           int* a_out, double* g_out) {
+  double* nrm = (double*)malloc(sizeof(double) * (size_t)k);
+  for (int a = 0; a < k; ++a) nrm[a] = dot64(A + (size_t)a * D, A + (size_t)a * D, D);
+  for (int i = 0; i < n; ++i) nearest_anchor(xs + (size_t)i * D, A, nrm, k, D, bf16, &a_out[i], &g_out[i]);
+  free(nrm);
+}
+
+/* ------------------------------------------------------------------------ */
+/* Attention-output-aware utilities (Sec. 3.3, Eq. utilities; App. A.3).      */
+/* ------------------------------------------------------------------------ */
+
+/* Utilities of listed non-anchor tokens of one head (R_t = I: no positional
+ * rotation on this path).  rK, rV are the fp32 residuals of those tokens.
+ *   uK_t = (1/m) sum_w alpha_wt^2 (q_w . rK_t)^2 / D * ||v_t - y_w||^2
+ *   uV_t = (1/m) sum_w alpha_wt^2 ||rV_t||^2 */
+void akvref_utilities(const double* Kh, const double* Vh, const double* Qg, const double* M,
+                      const double* Z, const double* Y, int S, int D, int W, int g,
+                      const int* toks, int ntok, const float* rK, const float* rV, double* uK,
+                      double* uV) {
+  int m = W * g;
+#pragma omp parallel for schedule(dynamic, 16)
+  for (int i = 0; i < ntok; ++i) {
+    int t = toks[i];
+    double* rk = (double*)malloc(sizeof(double) * D);
+    double* rv = (double*)malloc(sizeof(double) * D);
+    double* dv = (double*)malloc(sizeof(double) * D);
+    for (int j = 0; j < D; ++j) {
+      rk[j] = rK[(size_t)i * D + j];
+      rv[j] = rV[(size_t)i * D + j];
+    }
+    double rvn = dot64(rv, rv, D);
+    double sk = 0.0, sv = 0.0;
+    for (int w = 0; w < m; ++w) {
+      double a = obs_alpha(Kh, Qg, M, Z, S, D, W, w, t);
+      double a2 = a * a;
+      double qr = dot64(Qg + (size_t)w * D, rk, D);
+      for (int j = 0; j < D; ++j) dv[j] = Vh[(size_t)t * D + j] - Y[(size_t)w * D + j];
+      double vy = dot64(dv, dv, D);
+      sk += a2 * (qr * qr / D) * vy;
+      sv += a2 * rvn;
+    }
+    uK[i] = sk / m;
+    uV[i] = sv / m;
+    free(rk);
+    free(rv);
+    free(dv);
+  }
+}
+
+/* ------------------------------------------------------------------------ */
+/* Head-pooled residual budget (Sec. 3.4; Algorithm 1).                      */
+/* ------------------------------------------------------------------------ */
+
+typedef struct { double u; int h, t; } cand;
+static int cand_cmp(const void* a, const void* b) {
+  const cand* x = (const cand*)a;
+  const cand* y = (const cand*)b;
+  if (x->u > y->u) return -1;
+  if (x->u < y->u) return 1;
+  if (x->h != y->h) return x->h < y->h ? -1 : 1;
+  return (x->t > y->t) - (x->t < y->t);
+}
+
+/* Marks sel[h*S+t] = 1 for the N candidates of highest utility across all
+ * heads (candidates are entries with u >= 0; anchors carry u = -1), ties to
+ * the lower head, then the lower position.  Returns the number selected. */
+int64_t akvref_budget_select(const double* u, int H, int S, int64_t N, uint8_t* sel) {
+  cand* c = (cand*)malloc(sizeof(cand) * (size_t)H * S);
+  int64_t nc = 0;
+  for (int h = 0; h < H; ++h)
+    for (int t = 0; t < S; ++t) {
+      sel[(size_t)h * S + t] = 0;
+      double v = u[(size_t)h * S + t];
+      if (v >= 0.0) { c[nc].u = v; c[nc].h = h; c[nc].t = t; ++nc; }
+    }
+  qsort(c, (size_t)nc, sizeof(cand), cand_cmp);
+  int64_t n = N < nc ? N : nc;
+  for (int64_t i = 0; i < n; ++i) sel[(size_t)c[i].h * S + c[i].t] = 1;
+  free(c);
+  return n;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Whole compression pass of one request (Algorithm 1).                      */
+/* ------------------------------------------------------------------------ */
+
+enum { BUDGET_FRACTION = 0, BUDGET_THETA = 1, BUDGET_COUNT = 2 };
+
+/* K, V: [H][S][D]; Qobs: [Hq][W][D] (values exactly representable in the
+ * cache dtype).  anchor_override: [H][k] sorted positions or NULL.
+ * Outputs, all per head in position order:
+ *   anchors[H][k]; aK, aV [H][S] anchor index; gK, gV [H][S] stored gamma;
+ *   uK, uV [H][S] utilities (-1 on anchors); selK, selV [H][S] residual flags;
+ *   codesK, codesV [H][S][D/4]; scalesK, scalesV [H][S][D/G] (zero where the
+ *   position stores no residual); pooled [H][S-W] selector scores (may be NULL).
+ * nsel[2] receives the residual counts per side. */
+int akvref_encode(int H, int Hq, int D, int S, int W, int k, float rho, int kappa, int bf16,
+                  uint64_t seed, int budget_mode, double budget, int64_t budget_count, int G,
+                  int scale_mode, const double* K, const double* V, const double* Qobs,
+                  const int* anchor_override, int* anchors, int* aK, double* gK, int* aV,
+                  double* gV, double* uK, double* uV, uint8_t* selK, uint8_t* selV,
+                  uint8_t* codesK, float* scalesK, uint8_t* codesV, float* scalesV,
+                  double* pooled, int64_t* nsel) {
+  if (H <= 0 || Hq % H != 0 || D < 4 || (D & (D - 1)) || W < 0 || k < W || k > S ||
+      G <= 0 || D % G || G % 4 || kappa <= 0 || (kappa & 1) == 0)
+    return 1;
+  int g = Hq / H, m = W * g, P = S - W;
+  size_t SD = (size_t)S * D;
+  float* rK = (float*)calloc((size_t)H * SD, sizeof(float));
+  float* rV = (float*)calloc((size_t)H * SD, sizeof(float));
+  int* all = (int*)malloc(sizeof(int) * (size_t)S);
+  for (int t = 0; t < S; ++t) all[t] = t;
+  double* M = (double*)malloc(sizeof(double) * (size_t)(m > 0 ? m : 1));
+  double* Zs = (double*)malloc(sizeof(double) * (size_t)(m > 0 ? m : 1));
+  double* Y = (double*)malloc(sizeof(double) * (size_t)(m > 0 ? m : 1) * D);
+  double* sc = (double*)malloc(sizeof(double) * (size_t)(P > 0 ? P : 1));
+  double* pl = (double*)malloc(sizeof(double) * (size_t)(P > 0 ? P : 1));
+  for (int h = 0; h < H; ++h) {
+    const double* Kh = K + (size_t)h * SD;
+    const double* Vh = V + (size_t)h * SD;
+    const double* Qg = Qobs + (size_t)h * g * W * D;
+    int* anc = anchors + (size_t)h * k;
+    akvref_obs_head(Kh, Vh, Qg, S, D, W, g, M, Zs, Y);
+    if (anchor_override) {
+      memcpy(anc, anchor_override + (size_t)h * k, sizeof(int) * k);
+    } else {
+      akvref_selector_scores(Kh, Qg, M, Zs, S, D, W, g, kappa, sc, pl);
+      if (pooled) memcpy(pooled + (size_t)h * P, pl, sizeof(double) * P);
+      akvref_select_anchors(pl, S, W, k, rho, seed, h, anc);
+    }
+    float* rKh = rK + (size_t)h * SD;
+    float* rVh = rV + (size_t)h * SD;
+    akvref_assign_tokens(Kh, S, D, anc, k, bf16, all, S, aK + (size_t)h * S, gK + (size_t)h * S, rKh);
+    akvref_assign_tokens(Vh, S, D, anc, k, bf16, all, S, aV + (size_t)h * S, gV + (size_t)h * S, rVh);
+    char* isanc = (char*)calloc((size_t)S, 1);
+    for (int a = 0; a < k; ++a) isanc[anc[a]] = 1;
+    int* cand_t = (int*)malloc(sizeof(int) * (size_t)S);
+    int nc = 0;
+    for (int t = 0; t < S; ++t)
+      if (!isanc[t]) cand_t[nc++] = t;
+    float* crk = (float*)malloc(sizeof(float) * (size_t)(nc > 0 ? nc : 1) * D);
+    float* crv = (float*)malloc(sizeof(float) * (size_t)(nc > 0 ? nc : 1) * D);
+    double* cuk = (double*)malloc(sizeof(double) * (size_t)(nc > 0 ? nc : 1));
+    double* cuv = (double*)malloc(sizeof(double) * (size_t)(nc > 0 ? nc : 1));
+    for (int i = 0; i < nc; ++i) {
+      memcpy(crk + (size_t)i * D, rKh + (size_t)cand_t[i] * D, sizeof(float) * D);
+      memcpy(crv + (size_t)i * D, rVh + (size_t)cand_t[i] * D, sizeof(float) * D);
+    }
+    akvref_utilities(Kh, Vh, Qg, M, Zs, Y, S, D, W, g, cand_t, nc, crk, crv, cuk, cuv);
+    for (int t = 0; t < S; ++t) { uK[(size_t)h * S + t] = -1.0; uV[(size_t)h * S + t] = -1.0; }
+    for (int i = 0; i < nc; ++i) {
+      uK[(size_t)h * S + cand_t[i]] = cuk[i];
+      uV[(size_t)h * S + cand_t[i]] = cuv[i];
+    }
+    free(isanc); free(cand_t); free(crk); free(crv); free(cuk); free(cuv);
+  }
+  int64_t NK, NV;
+  if (budget_mode == BUDGET_THETA) {
+    int eb = bf16 ? 2 : 4;
+    int64_t N = akvref_theta_budget(S, H, D, W, k, G, eb, eb, budget);
+    NK = N / 2;
+    NV = N - NK;
+  } else if (budget_mode == BUDGET_COUNT) {
+    NK = NV = budget_count;
+  } else {
+    NK = NV = (int64_t)floor((double)(float)budget * (double)H * (double)S);
+  }
+  nsel[0] = akvref_budget_select(uK, H, S, NK, selK);
+  nsel[1] = akvref_budget_select(uV, H, S, NV, selV);
+  int nb = D / 4, ns = D / G;
+  memset(codesK, 0, (size_t)H * S * nb);
+  memset(codesV, 0, (size_t)H * S * nb);
+  memset(scalesK, 0, sizeof(float) * (size_t)H * S * ns);
+  memset(scalesV, 0, sizeof(float) * (size_t)H * S * ns);
+  for (int h = 0; h < H; ++h)
+    for (int t = 0; t < S; ++t) {
+      size_t e = (size_t)h * S + t;
+      if (selK[e]) akvref_codec_encode(rK + e * D, D, G, scale_mode, seed, codesK + e * nb, scalesK + e * ns);
+      if (selV[e]) akvref_codec_encode(rV + e * D, D, G, scale_mode, seed, codesV + e * nb, scalesV + e * ns);
+    }
+  free(rK); free(rV); free(all); free(M); free(Zs); free(Y); free(sc); free(pl);
+  return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Reconstruction (Eq. reconstruction) and decode attention (Eq.             */
+/* exact-attention over the reconstructed cache).                             */
+/* ------------------------------------------------------------------------ */
+
+/* Dense reconstruction of one side of one head, fp32:
+ *   anchor positions: the stored anchor vector;
+ *   others: p_j = fp32(gamma * abar_j); with a residual, x^_j = fp32(p_j + r~_j). */
+void akvref_reconstruct(const double* X, int S, int D, int G, uint64_t seed, const int* anchors,
+                        int k, const int* a, const double* gm, const uint8_t* sel,
+                        const uint8_t* codes, const float* scales, float* out) {
+  int* rank = (int*)malloc(sizeof(int) * (size_t)S);
+  for (int t = 0; t < S; ++t) rank[t] = -1;
+  for (int i = 0; i < k; ++i) rank[anchors[i]] = i;
+  float* rt = (float*)malloc(sizeof(float) * D);
+  for (int t = 0; t < S; ++t) {
+    float* o = out + (size_t)t * D;
+    if (rank[t] >= 0) {
+      for (int j = 0; j < D; ++j) o[j] = (float)X[(size_t)t * D + j];
+      continue;
+    }
+    const double* an = X + (size_t)anchors[a[t]] * D;
+    float g = (float)gm[t];
+    for (int j = 0; j < D; ++j) o[j] = g * (float)an[j];
+    if (sel[t]) {
+      akvref_codec_decode(codes + (size_t)t * (D / 4), scales + (size_t)t * (D / G), D, G, seed, rt);
+      for (int j = 0; j < D; ++j) o[j] = o[j] + rt[j];
+    }
+  }
+  free(rank);
+  free(rt);
+}
+
+/* Softmax attention of Hq query heads over T entries per KV head (query head
+ * j reads KV head j / (Hq/H)): Kt, Vt are [H][T][D] fp32, q is [Hq][D];
+ * logits dot64(q, k)*scale, softmax in fp64, output [Hq][D] fp64. */
+void akvref_attention(const float* Kt, const float* Vt, int H, int T, int D, const double* q,
+                      int Hq, double scale, double* out) {
+  int g = Hq / H;
+#pragma omp parallel for schedule(static)
+  for (int j = 0; j < Hq; ++j) {
+    int h = j / g;
+    double* l = (double*)malloc(sizeof(double) * (size_t)T);
+    double* kk = (double*)malloc(sizeof(double) * D);
+    double mx = -INFINITY;
+    for (int t = 0; t < T; ++t) {
+      const float* kr = Kt + ((size_t)h * T + t) * D;
+      for (int c = 0; c < D; ++c) kk[c] = kr[c];
+      l[t] = dot64(q + (size_t)j * D, kk, D) * scale;
+      if (l[t] > mx) mx = l[t];
+    }
+    double z = 0.0;
+    for (int t = 0; t < T; ++t) z += exp(l[t] - mx);
+    double* o = out + (size_t)j * D;
+    for (int c = 0; c < D; ++c) o[c] = 0.0;
+    for (int t = 0; t < T; ++t) {
+      double p = exp(l[t] - mx) / z;
+      const float* vr = Vt + ((size_t)h * T + t) * D;
+      for (int c = 0; c < D; ++c) o[c] += p * vr[c];
+    }
+    free(l);
+    free(kk);
+  }
+}
+
+int akvref_num_threads(void) {
+#ifdef _OPENMP
+  return omp_get_max_threads();
+#else
+  return 1;
+#endif
+}
