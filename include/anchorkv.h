@@ -1,0 +1,201 @@
+/*
+ * anchorkv.h -- C ABI of the AnchorKV hot path for AMD MI355X (gfx950).
+ *
+ * AnchorKV (arXiv 2608.02901) compresses one attention layer's per-KV-head key
+ * and value caches at the end of prefill (Sec. 3.2, Algorithm 1): k anchor
+ * tokens per head are kept exactly, every other token is stored as the index
+ * of its nearest anchor plus one projection coefficient gamma (Sec. 3.1, Eqs.
+ * nearest-anchor and projection), and a head-pooled budget of tokens also
+ * stores a 2-bit Hadamard-rotated residual (Sec. 3.1 "Residual quantization",
+ * Sec. 3.3 utilities, Sec. 3.4 budget).  Decode attention then reads that
+ * compressed cache directly; no token leaves the softmax (Sec. 3.4 "Storage
+ * and Decoding"; App. E.1).
+ *
+ * Conventions for every entry point:
+ *   - Device pointers are HIP device memory owned by the caller.  The library
+ *     never allocates or frees device memory and never synchronizes the stream.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).  All
+ *     work is enqueued on it in order; results are valid once it completes.
+ *   - Host pointers are read (or written) only during the call.
+ *   - Every argument is validated before anything is enqueued.  On an error
+ *     nothing is enqueued, the status says why and anchorkv_last_error()
+ *     returns a detail string for the calling thread.  A HIP launch failure
+ *     returns ANCHORKV_ERR_HIP; the stream state is then undefined for the
+ *     work of that call.  No entry point throws or aborts.
+ *   - Query head j reads KV head j / (num_q_heads / num_kv_heads) (GQA).
+ */
+#ifndef ANCHORKV_H
+#define ANCHORKV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  ANCHORKV_OK = 0,
+  ANCHORKV_ERR_INVALID_ARG = 1,   /* null pointer, bad size, inconsistent config */
+  ANCHORKV_ERR_UNSUPPORTED = 2,   /* valid for the method, outside this build's limits */
+  ANCHORKV_ERR_CAPACITY = 3,      /* append beyond the capacity reserved at plan time */
+  ANCHORKV_ERR_CORRUPT_CACHE = 4, /* export of a blob whose header does not match the plan */
+  ANCHORKV_ERR_HIP = 5            /* a HIP runtime call failed */
+} anchorkv_status;
+
+typedef enum { ANCHORKV_F32 = 0, ANCHORKV_BF16 = 1 } anchorkv_dtype;
+
+/* Scale of the 2-bit residual codec (Sec. 3.1; App. A.1 "Codebook").  The
+ * paper quantizes each rotated coordinate with the four-level Lloyd-Max
+ * codebook of a unit Gaussian after normalizing by a per-token absmax; how
+ * the absmax enters is not fixed by the text, so the scale sigma (the Gaussian
+ * standard deviation the codebook is applied at) has three readings:
+ *   OUTER   : sigma = absmax / L1 -- the largest coordinate lands on the outer level;
+ *   LITERAL : sigma = absmax;
+ *   RMS     : sigma = root mean square of the group's rotated coordinates. */
+typedef enum {
+  ANCHORKV_SCALE_ABSMAX_OUTER = 0,
+  ANCHORKV_SCALE_ABSMAX_LITERAL = 1,
+  ANCHORKV_SCALE_RMS = 2
+} anchorkv_scale_mode;
+
+/* Residual budget per side (Sec. 3.4).
+ *   FRACTION : N_side = floor(budget * H * S) per request and side;
+ *   THETA    : N = max{0, floor((theta*M_full - M_base)/b_res)} (Eq. byte-budget,
+ *              with M_base from Eq. mfixed and b_res the mean key/value residual
+ *              cost), keys get floor(N/2), values the rest;
+ *   COUNT    : N_side = budget_count.
+ * N_side is capped at the number of non-anchor tokens, H * (S - k). */
+typedef enum {
+  ANCHORKV_BUDGET_FRACTION = 0,
+  ANCHORKV_BUDGET_THETA = 1,
+  ANCHORKV_BUDGET_COUNT = 2
+} anchorkv_budget_mode;
+
+typedef struct anchorkv_config {
+  int32_t num_kv_heads;   /* H */
+  int32_t num_q_heads;    /* Hq, a multiple of H */
+  int32_t head_dim;       /* D; this build supports D = 128 */
+  int32_t window;         /* W: the last W positions are anchors and give the observation queries */
+  int32_t anchor_count;   /* k per head when > 0 (window included) ... */
+  float anchor_frac;      /* ... else k = max(W, floor(anchor_frac * S)), capped at S */
+  float rho;              /* share of the k - W free anchors taken by score (paper: 0.7) */
+  int32_t kappa;          /* odd average-pooling width of the selector score (paper: 7) */
+  int32_t budget_mode;    /* anchorkv_budget_mode */
+  float budget;           /* FRACTION: residual fraction; THETA: retained fraction theta */
+  int64_t budget_count;   /* COUNT: residuals per side */
+  int32_t quant_group;    /* G: coordinates per residual scale, G | D, 4 | G; 0 -> G = D */
+  int32_t scale_mode;     /* anchorkv_scale_mode */
+  int32_t dtype;          /* anchorkv_dtype of K, V, queries, anchors and coefficients */
+  int32_t max_append;     /* capacity for tokens appended after the compression pass */
+  uint64_t seed;          /* seeds the uniform anchor share and the Hadamard sign pattern */
+} anchorkv_config;
+
+/* Derived per-request sizes (host memory). */
+typedef struct anchorkv_request_info {
+  int32_t seq_len;        /* S */
+  int32_t anchors;        /* k */
+  int32_t n_top;          /* floor(rho * (k - W)), anchors chosen by selector score */
+  int32_t n_rand;         /* k - W - n_top, anchors sampled uniformly */
+  int64_t residuals_k;    /* N_K: key residuals stored */
+  int64_t residuals_v;    /* N_V: value residuals stored */
+} anchorkv_request_info;
+
+/* Opaque host-side plan: the config, the batch's sequence lengths and the
+ * byte layout of the cache blob, all computed on the host. */
+typedef struct anchorkv_plan anchorkv_plan;
+
+/* Validates `cfg` for `batch` requests with host lengths seq_lens[batch] and
+ * builds a plan.  batch in [1, 64], every S >= max(W, 1) + 1, k <= 16384.
+ * On success *out owns host memory released by anchorkv_plan_destroy. */
+anchorkv_status anchorkv_plan_create(const anchorkv_config* cfg, int32_t batch, const int32_t* seq_lens,
+                                     anchorkv_plan** out);
+void anchorkv_plan_destroy(anchorkv_plan* plan);
+
+/* Byte sizes of the caller-provided device buffers. */
+size_t anchorkv_cache_bytes(const anchorkv_plan* plan);
+size_t anchorkv_encode_workspace_bytes(const anchorkv_plan* plan);
+size_t anchorkv_decode_workspace_bytes(const anchorkv_plan* plan);
+anchorkv_status anchorkv_plan_request(const anchorkv_plan* plan, int32_t request, anchorkv_request_info* info);
+
+/* The compression pass (Algorithm 1) for all requests of the plan.
+ *   K, V    : device, dtype; request b is a contiguous [H][S_b][D] block, the
+ *             blocks packed back to back in request order.
+ *   Q_obs   : device, dtype; request b is [Hq][W][D] (the queries of the last W
+ *             positions, the observation window of Sec. 3.2), packed likewise.
+ *   anchor_pos_override : NULL, or device int32 [sum_b H*k_b]: per request and
+ *             head the k_b anchor positions, strictly increasing, containing the
+ *             last W positions; replaces the selection step.  An override that
+ *             breaks these rules marks the cache invalid (anchorkv_export then
+ *             returns ANCHORKV_ERR_CORRUPT_CACHE).
+ *   cache   : device, anchorkv_cache_bytes(plan); receives the compressed layer.
+ *   workspace : device, anchorkv_encode_workspace_bytes(plan); scratch, contents
+ *             undefined afterwards.  cache and workspace must not overlap the inputs. */
+anchorkv_status anchorkv_encode(const anchorkv_plan* plan, const void* K, const void* V, const void* Q_obs,
+                                const int32_t* anchor_pos_override, void* cache, void* workspace,
+                                void* stream);
+
+/* Appends one generated token per request and KV head (config max_append
+ * slots).  The token is encoded against the request's existing anchors (its
+ * nearest anchor and coefficient, Eqs. nearest-anchor and projection) and
+ * stores no residual.  n_appended: tokens already appended to this cache
+ * (host-tracked), must be < max_append.  k_new, v_new: device [batch][H][D]. */
+anchorkv_status anchorkv_append(const anchorkv_plan* plan, void* cache, int32_t n_appended, const void* k_new,
+                                const void* v_new, void* stream);
+
+/* Decode attention over the compressed cache (Eq. exact-attention with the
+ * reconstructed keys and values of Eq. reconstruction), never materializing
+ * them: q.k^_t = gamma_t (q.k_a(t)) + q.r~_t and the values accumulate as
+ * per-anchor weights plus a rotated residual sum (App. E.1).
+ *   n_appended : appended tokens included (the first n_appended tail slots).
+ *   q          : device [batch][Hq][D], dtype.
+ *   out        : device [batch][Hq][D], out_dtype (anchorkv_dtype).
+ *   softmax_scale : <= 0 selects 1/sqrt(D).
+ *   workspace  : device, anchorkv_decode_workspace_bytes(plan). */
+anchorkv_status anchorkv_decode_attn(const anchorkv_plan* plan, const void* cache, int32_t n_appended,
+                                     const void* q, void* out, int32_t out_dtype, float softmax_scale,
+                                     void* workspace, void* stream);
+
+/* Dense reconstruction (Eq. reconstruction) of one side (0 = keys, 1 = values)
+ * of one request: out is device fp32 [H][S_b + n_appended][D], position order. */
+anchorkv_status anchorkv_reconstruct(const anchorkv_plan* plan, const void* cache, int32_t n_appended,
+                                     int32_t request, int32_t side, float* out, void* stream);
+
+/* Logical content of one request, in position order, from a HOST copy of the
+ * cache blob (pure host code).  Every pointer is caller-allocated host memory,
+ * any may be NULL to skip it.  Shapes (S = S_b, k = k_b, per side X in {K, V}):
+ *   anchors [H][k] int32; a_X [H][S] int32 anchor index; gamma_X [H][S] fp32
+ *   stored coefficient; sel_X [H][S] uint8 residual flag; codes_X [H][S][D/4];
+ *   scales_X [H][S][D/G] (zero where no residual); tail_a_X, tail_gamma_X
+ *   [H][n_appended]; stats[4]: tokens resolved by the exact fp64 path of the
+ *   certified argmax, keys then values, then N_K, N_V. */
+typedef struct anchorkv_export_arrays {
+  int32_t* anchors;
+  int32_t* a_k;
+  float* gamma_k;
+  uint8_t* sel_k;
+  uint8_t* codes_k;
+  float* scales_k;
+  int32_t* a_v;
+  float* gamma_v;
+  uint8_t* sel_v;
+  uint8_t* codes_v;
+  float* scales_v;
+  int32_t* tail_a_k;
+  float* tail_gamma_k;
+  int32_t* tail_a_v;
+  float* tail_gamma_v;
+  int64_t* stats;
+} anchorkv_export_arrays;
+
+anchorkv_status anchorkv_export(const anchorkv_plan* plan, const void* cache_host, int32_t request,
+                                int32_t n_appended, anchorkv_export_arrays* out);
+
+const char* anchorkv_status_string(anchorkv_status status);
+const char* anchorkv_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ANCHORKV_H */

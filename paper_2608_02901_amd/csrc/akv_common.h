@@ -1,0 +1,254 @@
+// Internal definitions shared by the AnchorKV HIP kernels and the host layer.
+//
+// Every kernel of the library receives two small structs by value: `Geo`
+// (shapes, per-request sizes and prefix offsets of the batch) and a pointer
+// bundle (`Cache` for the compressed blob, `Ws` for encode scratch, `DecWs`
+// for decode scratch).  All per-request offsets are prefix sums over the
+// batch, so any array is addressed as base + H * prefix[b] * row_size.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+// Every floating-point expression of the library is evaluated as written:
+// no multiply-add contraction unless a kernel calls fmaf explicitly.
+#pragma clang fp contract(off)
+
+#define AKV_MAXB 64
+#define AKV_D 128
+#define AKV_MAXK 16384
+
+namespace akv {
+
+// ------------------------------------------------------------------ geometry
+struct Geo {
+  int B, H, Hq, g, D, W, G, m;  // m = W * g observation rows per KV head
+  int dtype;                    // 0 = fp32, 1 = bf16 (inputs, anchors, coefficients)
+  int esz;                      // element bytes of the dtype
+  int kappa, scale_mode, max_append;
+  int maxS, maxK;
+  unsigned long long seed_anchor, seed_sign;
+  int S[AKV_MAXB], k[AKV_MAXB], ntop[AKV_MAXB], nrand[AKV_MAXB];
+  int prefS[AKV_MAXB + 1];   // sum of S over earlier requests
+  int prefK[AKV_MAXB + 1];   // sum of k
+  int prefW[AKV_MAXB + 1];   // sum of ceil(S/64) (mask words per head)
+  int prefC[AKV_MAXB + 1];   // sum of observation chunks per head
+  int prefKT[AKV_MAXB + 1];  // sum of H * k * (sort chunks): counting-sort table offsets
+  int prefBC[AKV_MAXB + 1];  // sum of budget chunks (H * S / 4096, rounded up)
+  int prefSp[AKV_MAXB + 1];  // sum of decode splits per head
+  int prefNK[AKV_MAXB + 1];  // sum of key residual counts
+  int prefNV[AKV_MAXB + 1];  // sum of value residual counts
+  int dsplit;                // decode split length (sorted slots per workgroup)
+};
+
+constexpr int OBS_CHUNK = 2048;   // tokens per observation-pass workgroup
+constexpr int SORT_CHUNK = 2048;  // tokens per counting-sort chunk
+
+// Device pointers into the cache blob (layouts in position p = request-major,
+// head-major order; "sorted" arrays are in decode order, see the layout build).
+struct Cache {
+  uint32_t* header;     // [64] magic, version, flags
+  int32_t* anc_pos;     // [b][h][k_b] anchor positions, ascending
+  void* ancK;           // [b][h][k_b][D] dtype, pre-positional keys of the anchors
+  void* ancV;           // [b][h][k_b][D] dtype
+  double* nrmK;         // [b][h][k_b] canonical squared norms (fp64)
+  double* nrmV;
+  float* invK;          // [b][h][k_b] fp32 1/||a|| (0 for a zero anchor)
+  float* invV;
+  uint16_t* idxK;       // [b][h][S_b] anchor index per sorted slot
+  uint16_t* idxV;
+  void* gK;             // [b][h][S_b] coefficient per sorted slot (dtype)
+  void* gV;
+  int32_t* pos;         // [b][h][S_b] token position of each sorted slot
+  uint64_t* maskK;      // [b][h][ceil(S_b/64)] residual flag bits per sorted slot
+  uint64_t* maskV;
+  int32_t* pcK;         // [b][h][ceil(S_b/64)] global residual slot of the word's first set bit
+  int32_t* pcV;
+  uint8_t* codesK;      // [sum N_K][D/4] 2-bit codes, residual slots in sorted order
+  uint8_t* codesV;
+  float* scalesK;       // [sum N_K][D/G]
+  float* scalesV;
+  uint16_t* tidxK;      // [b][h][max_append] appended-token records
+  uint16_t* tidxV;
+  void* tgK;
+  void* tgV;
+  int32_t* stats;       // [b][4]
+};
+
+// Encode scratch.
+struct Ws {
+  float* opmax;         // [b][h][chunk][m] partial row max of the observation logits
+  float* opsum;         // [b][h][chunk][m] partial sum of exp
+  float* oM;            // [b][h][m] row max (scaled logits)
+  float* oiZ;           // [b][h][m] 1 / sum exp
+  float* ypart;         // [b][h][chunk][m][D] partial observation outputs
+  float* Y;             // [b][h][m][D]
+  uint16_t* Yhi;        // [b][h][m][D] bf16 split of Y: Y ~ hi + lo
+  uint16_t* Ylo;
+  float* ynorm;         // [b][h][m] ||y_w||^2
+  float* sc;            // [b][h][S_b] selector score, then pooled score
+  int32_t* rank;        // [b][h][S_b] anchor index of an anchor position, -1 otherwise
+  uint8_t* flag;        // [b][h][S_b] selection marks
+  float* QA;            // [b][h][m][k_b] q_w . abar^K_a
+  int32_t* apos;        // [side][b][h][S_b] anchor index per position (-1: fixup pending)
+  unsigned long long* fix;  // fixup list entries
+  int32_t* fixcount;    // [2] list length, overflow guard
+  float* gpos;          // [side][b][h][S_b] stored coefficient as fp32
+  float* u;             // [side][b][h][S_b] utility, -1 for anchors
+  uint8_t* sel;         // [side][b][h][S_b] residual flags
+  uint32_t* bhist;      // [b][side][256]
+  int32_t* bstate;      // [b][side][4]: prefix bits, remaining, threshold bits, need
+  int32_t* tiecnt;      // [b][side][nchunk]
+  int32_t* shist;       // [b][h][k_b][sort chunks] counting-sort histograms, then offsets
+  int32_t* wcnt;        // [side][b][h][ceil(S_b/64)] popcounts for the slot scan
+};
+
+struct DecWs {
+  float* SK;            // [b][h][g][k_b] anchor scores q_j . abar^K_a
+  float* qrot;          // [b][Hq][D] FWHT(s * q)
+  float* part;          // [b][Hq][split][2 + 2D] partial (max, sum, y[D], zacc[D])
+};
+
+// ------------------------------------------------------------------ vector types
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
+typedef __attribute__((ext_vector_type(16))) float f32x16;
+typedef __attribute__((ext_vector_type(4))) float f32x4;
+
+__device__ __host__ inline float bf2f(uint16_t h) {
+  uint32_t u = (uint32_t)h << 16;
+  float f;
+  __builtin_memcpy(&f, &u, 4);
+  return f;
+}
+// Round-to-nearest-even fp32 -> bf16 (finite inputs).
+__device__ __host__ inline uint16_t f2bf(float f) {
+  uint32_t u;
+  __builtin_memcpy(&u, &f, 4);
+  u = u + 0x7FFFu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+// Element access for the two cache dtypes.
+template <int DT> struct Elem;
+template <> struct Elem<0> {
+  using T = float;
+  __device__ static float get(const void* p, size_t i) { return ((const float*)p)[i]; }
+  __device__ static void put(void* p, size_t i, float v) { ((float*)p)[i] = v; }
+  // Stored coefficient: fp32.
+  __device__ static float round_coef(float g) { return g; }
+};
+template <> struct Elem<1> {
+  using T = uint16_t;
+  __device__ static float get(const void* p, size_t i) { return bf2f(((const uint16_t*)p)[i]); }
+  __device__ static void put(void* p, size_t i, float v) { ((uint16_t*)p)[i] = f2bf(v); }
+  __device__ static float round_coef(float g) { return bf2f(f2bf(g)); }
+};
+
+// MFMA traits: A[m][k] (anchors/rows), B[k][n] (tokens/columns), C 32x32.
+// Lane l supplies A[l%32][kofs..] and B[kofs..][l%32]; the accumulator entry
+// r = i*4 + j of lane l is C[i*8 + (l/32)*4 + j][l%32].
+template <int DT> struct MF;
+template <> struct MF<1> {
+  static constexpr int KS = 16;   // k per instruction
+  static constexpr int KL = 8;    // k per lane
+  using frag = bf16x8;
+  __device__ static frag load(const uint16_t* row, int k0) {
+    uint4 v = *(const uint4*)(row + k0);
+    return __builtin_bit_cast(frag, v);
+  }
+  __device__ static frag load_lds(const uint16_t* row, int k0) {
+    uint4 v = *(const uint4*)(row + k0);
+    return __builtin_bit_cast(frag, v);
+  }
+  __device__ static f32x16 mma(frag a, frag b, f32x16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+  }
+};
+template <> struct MF<0> {
+  static constexpr int KS = 2;
+  static constexpr int KL = 1;
+  using frag = float;
+  __device__ static frag load(const float* row, int k0) { return row[k0]; }
+  __device__ static frag load_lds(const float* row, int k0) { return row[k0]; }
+  __device__ static f32x16 mma(frag a, frag b, f32x16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
+  }
+};
+__device__ inline int kofs(int KS, int s, int lane) { return s * KS + (lane >> 5) * (KS >> 1); }
+__device__ inline int crow(int r, int lane) { return (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3); }
+
+// ------------------------------------------------------------------ canonical fp64 dot
+// Products of fp32 / bf16 values are exact in fp64; the sum runs j = 0..D-1
+// with one rounding per addition and no fused multiply-add.
+template <int DT>
+__device__ inline double dot64_seq(const typename Elem<DT>::T* x, const typename Elem<DT>::T* y, int D) {
+  double s = 0.0;
+  if constexpr (DT == 1) {
+    for (int j = 0; j < D; j += 8) {
+      uint4 xv = *(const uint4*)(x + j);
+      uint4 yv = *(const uint4*)(y + j);
+      const uint16_t* xs = (const uint16_t*)&xv;
+      const uint16_t* ys = (const uint16_t*)&yv;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) s = s + (double)bf2f(xs[i]) * (double)bf2f(ys[i]);
+    }
+  } else {
+    for (int j = 0; j < D; j += 4) {
+      float4 xv = *(const float4*)(x + j);
+      float4 yv = *(const float4*)(y + j);
+      s = s + (double)xv.x * (double)yv.x;
+      s = s + (double)xv.y * (double)yv.y;
+      s = s + (double)xv.z * (double)yv.z;
+      s = s + (double)xv.w * (double)yv.w;
+    }
+  }
+  return s;
+}
+
+// SplitMix64 (Steele, Lea & Flood 2014): first output of a generator in state x.
+__device__ __host__ inline unsigned long long splitmix64(unsigned long long x) {
+  unsigned long long z = x + 0x9E3779B97F4A7C15ULL;
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ULL;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBULL;
+  return z ^ (z >> 31);
+}
+
+// Sign of coordinate j of the randomized Hadamard rotation: +1 or -1.
+__device__ inline float hsign(unsigned long long seed_sign, int j) {
+  return (splitmix64(seed_sign ^ (unsigned long long)j) >> 63) ? -1.0f : 1.0f;
+}
+
+// Lloyd-Max 4-level quantizer for a unit Gaussian (Lloyd 1957, Max 1960).
+#define AKV_L0 0.4527800f
+#define AKV_L1 1.5104176f
+#define AKV_T 0.9815988f
+
+// ------------------------------------------------------------------ wave helpers
+__device__ inline float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+__device__ inline float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+__device__ inline int wave_sum_i(int v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+// Locates request b for a flat work index over per-request unit counts
+// n_b = H * ceil(S_b / tile) * mult.  Returns b and the index within b.
+__device__ inline int locate(const Geo& g, int tile, int mult, int& idx) {
+  for (int b = 0; b < g.B; ++b) {
+    int n = g.H * ((g.S[b] + tile - 1) / tile) * mult;
+    if (idx < n) return b;
+    idx -= n;
+  }
+  return -1;
+}
+
+}  // namespace akv

@@ -1,0 +1,546 @@
+// Host layer of the AnchorKV library: configuration checks, the byte layout
+// of the cache blob and of the workspaces (a pure function of the config and
+// the batch's sequence lengths), launch sequencing on the caller's stream,
+// error mapping, and the host-side export of a cache blob.
+#include <math.h>
+#include <string.h>
+
+#include <new>
+#include <string>
+#include <vector>
+
+#include "akv_common.h"
+#include "anchorkv.h"
+
+namespace akv {
+hipError_t launch_init(const Geo& g, const Cache& c, const Ws& w, hipStream_t st);
+hipError_t launch_obs(const Geo& g, const Ws& w, const void* K, const void* V, const void* Q, hipStream_t st);
+hipError_t launch_select(const Geo& g, const Ws& w, const Cache& c, const void* K, const void* V, const void* Q,
+                         const int32_t* ovr, hipStream_t st);
+hipError_t launch_assign(const Geo& g, const Ws& w, const Cache& c, const void* K, const void* V, hipStream_t st);
+hipError_t launch_epilogue(const Geo& g, const Ws& w, const Cache& c, const void* K, const void* V, const void* Q,
+                           hipStream_t st);
+hipError_t launch_budget(const Geo& g, const Ws& w, hipStream_t st);
+hipError_t launch_layout(const Geo& g, const Ws& w, const Cache& c, const void* K, const void* V, hipStream_t st);
+hipError_t launch_decode(const Geo& g, const Cache& c, const DecWs& dw, const void* q, void* out, int out_dtype,
+                         float scale, int n_app, hipStream_t st);
+hipError_t launch_append(const Geo& g, const Cache& c, int n_app, const void* kn, const void* vn, hipStream_t st);
+hipError_t launch_reconstruct(const Geo& g, const Cache& c, int b, int side, int n_app, float* out,
+                              hipStream_t st);
+}  // namespace akv
+
+using akv::Geo;
+
+static const uint32_t kMagic = 0x314B5641u;  // "AVK1" little endian
+static const uint32_t kVersion = 1;
+static const int kBudgetChunk = 4096;
+static const int kDecodeSplit = 2048;
+
+static thread_local std::string g_last_error;
+
+static anchorkv_status fail(anchorkv_status s, const std::string& msg) {
+  g_last_error = msg;
+  return s;
+}
+
+struct Layout {
+  std::vector<size_t> off;
+  size_t total = 0;
+  size_t add(size_t bytes) {
+    size_t o = total;
+    off.push_back(o);
+    total += (bytes + 255) & ~(size_t)255;
+    return o;
+  }
+};
+
+struct anchorkv_plan {
+  anchorkv_config cfg;
+  Geo geo;
+  std::vector<anchorkv_request_info> req;
+  // cache blob offsets
+  size_t c_header, c_anc_pos, c_ancK, c_ancV, c_nrmK, c_nrmV, c_invK, c_invV, c_idxK, c_idxV, c_gK, c_gV, c_pos,
+      c_maskK, c_maskV, c_pcK, c_pcV, c_codesK, c_codesV, c_scalesK, c_scalesV, c_tidxK, c_tidxV, c_tgK, c_tgV,
+      c_stats;
+  size_t cache_bytes;
+  // encode workspace offsets
+  size_t w_opmax, w_opsum, w_oM, w_oiZ, w_ypart, w_Y, w_Yhi, w_Ylo, w_ynorm, w_sc, w_rank, w_flag, w_QA, w_apos,
+      w_fix, w_fixcount, w_gpos, w_u, w_sel, w_bhist, w_bstate, w_tiecnt, w_shist, w_wcnt;
+  size_t ws_bytes;
+  // decode workspace offsets
+  size_t d_SK, d_qrot, d_part;
+  size_t dws_bytes;
+};
+
+static int64_t theta_residuals(int S, int H, int D, int W, int k, int G, int eb, double theta) {
+  // Eq. byte-budget with M_base from Eq. mfixed (b_a = 2, b_gamma = element size).
+  const double P = (double)(S - W);
+  const double words = ceil(P / 64.0);
+  const double Mbase = (double)H * (2.0 * eb * k * D + 8.0 * (k - W) + 2.0 * P * (2.0 + eb)) + 24.0 * H * words +
+                       8.0 * (H + 1) + 4.0 * P;
+  const double Mfull = 2.0 * eb * (double)S * H * D;
+  const double cK = D / 4.0 + 4.0 * (D / G);
+  const double bres = 0.5 * (cK + (cK + 1.0));
+  const double n = floor((theta * Mfull - Mbase) / bres);
+  return n > 0 ? (int64_t)n : 0;
+}
+
+static uint64_t mix64(uint64_t x) { return akv::splitmix64(x); }
+
+extern "C" anchorkv_status anchorkv_plan_create(const anchorkv_config* cfg, int32_t batch, const int32_t* seq_lens,
+                                                anchorkv_plan** out) {
+  if (!cfg || !seq_lens || !out) return fail(ANCHORKV_ERR_INVALID_ARG, "null argument");
+  *out = nullptr;
+  const anchorkv_config& c = *cfg;
+  if (batch < 1 || batch > AKV_MAXB) return fail(ANCHORKV_ERR_INVALID_ARG, "batch must be in [1, 64]");
+  if (c.num_kv_heads < 1 || c.num_kv_heads > 255) return fail(ANCHORKV_ERR_INVALID_ARG, "num_kv_heads must be in [1, 255]");
+  if (c.num_q_heads < c.num_kv_heads || c.num_q_heads % c.num_kv_heads)
+    return fail(ANCHORKV_ERR_INVALID_ARG, "num_q_heads must be a positive multiple of num_kv_heads");
+  const int g = c.num_q_heads / c.num_kv_heads;
+  if (g != 1 && g != 2 && g != 4 && g != 8)
+    return fail(ANCHORKV_ERR_UNSUPPORTED, "query heads per KV head must be 1, 2, 4 or 8");
+  if (c.head_dim <= 0 || (c.head_dim & (c.head_dim - 1)))
+    return fail(ANCHORKV_ERR_INVALID_ARG, "head_dim must be a power of two");
+  if (c.head_dim != AKV_D) return fail(ANCHORKV_ERR_UNSUPPORTED, "this build supports head_dim = 128");
+  if (c.window < 1) return fail(ANCHORKV_ERR_INVALID_ARG, "window must be >= 1");
+  if (c.window * g > 256) return fail(ANCHORKV_ERR_UNSUPPORTED, "window * (Hq/H) must be <= 256");
+  if (c.kappa < 1 || (c.kappa & 1) == 0) return fail(ANCHORKV_ERR_INVALID_ARG, "kappa must be odd and >= 1");
+  if (!(c.rho >= 0.0f && c.rho <= 1.0f)) return fail(ANCHORKV_ERR_INVALID_ARG, "rho must be in [0, 1]");
+  if (c.dtype != ANCHORKV_F32 && c.dtype != ANCHORKV_BF16) return fail(ANCHORKV_ERR_INVALID_ARG, "bad dtype");
+  const int G = c.quant_group ? c.quant_group : c.head_dim;
+  if (G < 4 || G % 4 || c.head_dim % G) return fail(ANCHORKV_ERR_INVALID_ARG, "quant_group must divide head_dim and be a multiple of 4");
+  if (c.scale_mode < 0 || c.scale_mode > 2) return fail(ANCHORKV_ERR_INVALID_ARG, "bad scale_mode");
+  if (c.budget_mode < 0 || c.budget_mode > 2) return fail(ANCHORKV_ERR_INVALID_ARG, "bad budget_mode");
+  if (!(c.budget >= 0.0f) || (c.budget_mode != ANCHORKV_BUDGET_COUNT && c.budget > 1.0f))
+    return fail(ANCHORKV_ERR_INVALID_ARG, "budget must be in [0, 1]");
+  if (c.budget_mode == ANCHORKV_BUDGET_COUNT && c.budget_count < 0)
+    return fail(ANCHORKV_ERR_INVALID_ARG, "budget_count must be >= 0");
+  if (c.max_append < 0) return fail(ANCHORKV_ERR_INVALID_ARG, "max_append must be >= 0");
+  if (c.anchor_count == 0 && !(c.anchor_frac > 0.0f && c.anchor_frac <= 1.0f))
+    return fail(ANCHORKV_ERR_INVALID_ARG, "anchor_frac must be in (0, 1] when anchor_count = 0");
+  if (c.anchor_count < 0) return fail(ANCHORKV_ERR_INVALID_ARG, "anchor_count must be >= 0");
+
+  anchorkv_plan* p = new (std::nothrow) anchorkv_plan();
+  if (!p) return fail(ANCHORKV_ERR_INVALID_ARG, "out of host memory");
+  p->cfg = c;
+  Geo& geo = p->geo;
+  memset(&geo, 0, sizeof(geo));
+  const int H = c.num_kv_heads, D = c.head_dim, W = c.window;
+  geo.B = batch;
+  geo.H = H;
+  geo.Hq = c.num_q_heads;
+  geo.g = g;
+  geo.D = D;
+  geo.W = W;
+  geo.G = G;
+  geo.m = W * g;
+  geo.dtype = c.dtype;
+  geo.esz = c.dtype == ANCHORKV_BF16 ? 2 : 4;
+  geo.kappa = c.kappa;
+  geo.scale_mode = c.scale_mode;
+  geo.max_append = c.max_append;
+  geo.seed_anchor = mix64(c.seed ^ 1ull);
+  geo.seed_sign = mix64(c.seed ^ 2ull);
+  geo.dsplit = kDecodeSplit;
+  int64_t totS = 0;
+  for (int b = 0; b < batch; ++b) {
+    const int S = seq_lens[b];
+    if (S <= W) {
+      delete p;
+      return fail(ANCHORKV_ERR_INVALID_ARG, "every sequence must be longer than the window");
+    }
+    if (S > (1 << 22)) {
+      delete p;
+      return fail(ANCHORKV_ERR_UNSUPPORTED, "sequence length above 4M");
+    }
+    int k;
+    if (c.anchor_count > 0) {
+      k = c.anchor_count < S ? c.anchor_count : S;
+    } else {
+      k = (int)floor((double)c.anchor_frac * (double)S);
+      if (k < W) k = W;
+      if (k > S) k = S;
+    }
+    if (k < W) {
+      delete p;
+      return fail(ANCHORKV_ERR_INVALID_ARG, "anchor count must include the window (k >= W)");
+    }
+    if (k > AKV_MAXK) {
+      delete p;
+      return fail(ANCHORKV_ERR_UNSUPPORTED, "more than 16384 anchors per head");
+    }
+    const int ntop = (int)floor((double)c.rho * (double)(k - W));
+    const int64_t ncand = (int64_t)H * (S - k);
+    int64_t NK, NV;
+    if (c.budget_mode == ANCHORKV_BUDGET_FRACTION) {
+      NK = NV = (int64_t)floor((double)c.budget * (double)H * (double)S);
+    } else if (c.budget_mode == ANCHORKV_BUDGET_THETA) {
+      const int64_t N = theta_residuals(S, H, D, W, k, G, geo.esz, (double)c.budget);
+      NK = N / 2;
+      NV = N - NK;
+    } else {
+      NK = NV = c.budget_count;
+    }
+    if (NK > ncand) NK = ncand;
+    if (NV > ncand) NV = ncand;
+    anchorkv_request_info ri;
+    ri.seq_len = S;
+    ri.anchors = k;
+    ri.n_top = ntop;
+    ri.n_rand = k - W - ntop;
+    ri.residuals_k = NK;
+    ri.residuals_v = NV;
+    p->req.push_back(ri);
+    geo.S[b] = S;
+    geo.k[b] = k;
+    geo.ntop[b] = ntop;
+    geo.nrand[b] = k - W - ntop;
+    geo.maxS = S > geo.maxS ? S : geo.maxS;
+    geo.maxK = k > geo.maxK ? k : geo.maxK;
+    totS += S;
+  }
+  if (totS * H >= (1ll << 30)) {
+    delete p;
+    return fail(ANCHORKV_ERR_UNSUPPORTED, "total tokens x heads above 2^30");
+  }
+  for (int b = 0; b < batch; ++b) {
+    const int S = geo.S[b], k = geo.k[b];
+    geo.prefS[b + 1] = geo.prefS[b] + S;
+    geo.prefK[b + 1] = geo.prefK[b] + k;
+    geo.prefW[b + 1] = geo.prefW[b] + (S + 63) / 64;
+    geo.prefC[b + 1] = geo.prefC[b] + (S + akv::OBS_CHUNK - 1) / akv::OBS_CHUNK;
+    geo.prefKT[b + 1] = geo.prefKT[b] + H * k * ((S + akv::SORT_CHUNK - 1) / akv::SORT_CHUNK);
+    geo.prefBC[b + 1] = geo.prefBC[b] + (H * S + kBudgetChunk - 1) / kBudgetChunk;
+    geo.prefSp[b + 1] = geo.prefSp[b] + (S + kDecodeSplit - 1) / kDecodeSplit;
+    geo.prefNK[b + 1] = geo.prefNK[b] + (int)p->req[b].residuals_k;
+    geo.prefNV[b + 1] = geo.prefNV[b] + (int)p->req[b].residuals_v;
+  }
+  const size_t TS = (size_t)geo.prefS[batch] * H, TK = (size_t)geo.prefK[batch] * H,
+               TW = (size_t)geo.prefW[batch] * H, TC = (size_t)geo.prefC[batch] * H;
+  const size_t NKt = geo.prefNK[batch], NVt = geo.prefNV[batch];
+  const size_t esz = geo.esz, m = geo.m, cap = c.max_append;
+  Layout L;
+  p->c_header = L.add(256);
+  p->c_anc_pos = L.add(4 * TK);
+  p->c_ancK = L.add(esz * TK * D);
+  p->c_ancV = L.add(esz * TK * D);
+  p->c_nrmK = L.add(8 * TK);
+  p->c_nrmV = L.add(8 * TK);
+  p->c_invK = L.add(4 * TK);
+  p->c_invV = L.add(4 * TK);
+  p->c_idxK = L.add(2 * TS);
+  p->c_idxV = L.add(2 * TS);
+  p->c_gK = L.add(esz * TS);
+  p->c_gV = L.add(esz * TS);
+  p->c_pos = L.add(4 * TS);
+  p->c_maskK = L.add(8 * TW);
+  p->c_maskV = L.add(8 * TW);
+  p->c_pcK = L.add(4 * TW);
+  p->c_pcV = L.add(4 * TW);
+  p->c_codesK = L.add(NKt * (D / 4));
+  p->c_codesV = L.add(NVt * (D / 4));
+  p->c_scalesK = L.add(4 * NKt * (D / G));
+  p->c_scalesV = L.add(4 * NVt * (D / G));
+  p->c_tidxK = L.add(2 * batch * H * cap);
+  p->c_tidxV = L.add(2 * batch * H * cap);
+  p->c_tgK = L.add(esz * batch * H * cap);
+  p->c_tgV = L.add(esz * batch * H * cap);
+  p->c_stats = L.add(4 * 4 * batch);
+  p->cache_bytes = L.total;
+
+  Layout Wl;
+  p->w_opmax = Wl.add(4 * TC * m);
+  p->w_opsum = Wl.add(4 * TC * m);
+  p->w_oM = Wl.add(4 * batch * H * m);
+  p->w_oiZ = Wl.add(4 * batch * H * m);
+  p->w_ypart = Wl.add(4 * TC * m * D);
+  p->w_Y = Wl.add(4 * batch * H * m * D);
+  p->w_Yhi = Wl.add(2 * batch * H * m * D);
+  p->w_Ylo = Wl.add(2 * batch * H * m * D);
+  p->w_ynorm = Wl.add(4 * batch * H * m);
+  p->w_sc = Wl.add(4 * TS);
+  p->w_rank = Wl.add(4 * TS);
+  p->w_flag = Wl.add(TS);
+  p->w_QA = Wl.add(4 * TK * m);
+  p->w_apos = Wl.add(4 * 2 * TS);
+  p->w_fix = Wl.add(8 * 2 * TS);
+  p->w_fixcount = Wl.add(16);
+  p->w_gpos = Wl.add(4 * 2 * TS);
+  p->w_u = Wl.add(4 * 2 * TS);
+  p->w_sel = Wl.add(2 * TS);
+  p->w_bhist = Wl.add(4 * 2 * 256 * batch);
+  p->w_bstate = Wl.add(4 * 2 * 4 * batch);
+  p->w_tiecnt = Wl.add(4 * 2 * (size_t)geo.prefBC[batch]);
+  p->w_shist = Wl.add(4 * (size_t)geo.prefKT[batch]);
+  p->w_wcnt = Wl.add(4 * 2 * TW);
+  p->ws_bytes = Wl.total;
+
+  Layout Dl;
+  p->d_SK = Dl.add(4 * TK * g);
+  p->d_qrot = Dl.add(4 * (size_t)batch * geo.Hq * D);
+  p->d_part = Dl.add(4 * (size_t)geo.prefSp[batch] * geo.Hq * (2 + 2 * D));
+  p->dws_bytes = Dl.total;
+  *out = p;
+  return ANCHORKV_OK;
+}
+
+extern "C" void anchorkv_plan_destroy(anchorkv_plan* plan) { delete plan; }
+extern "C" size_t anchorkv_cache_bytes(const anchorkv_plan* p) { return p ? p->cache_bytes : 0; }
+extern "C" size_t anchorkv_encode_workspace_bytes(const anchorkv_plan* p) { return p ? p->ws_bytes : 0; }
+extern "C" size_t anchorkv_decode_workspace_bytes(const anchorkv_plan* p) { return p ? p->dws_bytes : 0; }
+
+extern "C" anchorkv_status anchorkv_plan_request(const anchorkv_plan* p, int32_t request, anchorkv_request_info* info) {
+  if (!p || !info) return fail(ANCHORKV_ERR_INVALID_ARG, "null argument");
+  if (request < 0 || request >= p->geo.B) return fail(ANCHORKV_ERR_INVALID_ARG, "request out of range");
+  *info = p->req[request];
+  return ANCHORKV_OK;
+}
+
+template <typename T>
+static T* at(void* base, size_t off) {
+  return (T*)((char*)base + off);
+}
+
+static akv::Cache cache_ptrs(const anchorkv_plan* p, void* base) {
+  akv::Cache c;
+  c.header = at<uint32_t>(base, p->c_header);
+  c.anc_pos = at<int32_t>(base, p->c_anc_pos);
+  c.ancK = at<void>(base, p->c_ancK);
+  c.ancV = at<void>(base, p->c_ancV);
+  c.nrmK = at<double>(base, p->c_nrmK);
+  c.nrmV = at<double>(base, p->c_nrmV);
+  c.invK = at<float>(base, p->c_invK);
+  c.invV = at<float>(base, p->c_invV);
+  c.idxK = at<uint16_t>(base, p->c_idxK);
+  c.idxV = at<uint16_t>(base, p->c_idxV);
+  c.gK = at<void>(base, p->c_gK);
+  c.gV = at<void>(base, p->c_gV);
+  c.pos = at<int32_t>(base, p->c_pos);
+  c.maskK = at<uint64_t>(base, p->c_maskK);
+  c.maskV = at<uint64_t>(base, p->c_maskV);
+  c.pcK = at<int32_t>(base, p->c_pcK);
+  c.pcV = at<int32_t>(base, p->c_pcV);
+  c.codesK = at<uint8_t>(base, p->c_codesK);
+  c.codesV = at<uint8_t>(base, p->c_codesV);
+  c.scalesK = at<float>(base, p->c_scalesK);
+  c.scalesV = at<float>(base, p->c_scalesV);
+  c.tidxK = at<uint16_t>(base, p->c_tidxK);
+  c.tidxV = at<uint16_t>(base, p->c_tidxV);
+  c.tgK = at<void>(base, p->c_tgK);
+  c.tgV = at<void>(base, p->c_tgV);
+  c.stats = at<int32_t>(base, p->c_stats);
+  return c;
+}
+
+static akv::Ws ws_ptrs(const anchorkv_plan* p, void* base) {
+  akv::Ws w;
+  w.opmax = at<float>(base, p->w_opmax);
+  w.opsum = at<float>(base, p->w_opsum);
+  w.oM = at<float>(base, p->w_oM);
+  w.oiZ = at<float>(base, p->w_oiZ);
+  w.ypart = at<float>(base, p->w_ypart);
+  w.Y = at<float>(base, p->w_Y);
+  w.Yhi = at<uint16_t>(base, p->w_Yhi);
+  w.Ylo = at<uint16_t>(base, p->w_Ylo);
+  w.ynorm = at<float>(base, p->w_ynorm);
+  w.sc = at<float>(base, p->w_sc);
+  w.rank = at<int32_t>(base, p->w_rank);
+  w.flag = at<uint8_t>(base, p->w_flag);
+  w.QA = at<float>(base, p->w_QA);
+  w.apos = at<int32_t>(base, p->w_apos);
+  w.fix = at<unsigned long long>(base, p->w_fix);
+  w.fixcount = at<int32_t>(base, p->w_fixcount);
+  w.gpos = at<float>(base, p->w_gpos);
+  w.u = at<float>(base, p->w_u);
+  w.sel = at<uint8_t>(base, p->w_sel);
+  w.bhist = at<uint32_t>(base, p->w_bhist);
+  w.bstate = at<int32_t>(base, p->w_bstate);
+  w.tiecnt = at<int32_t>(base, p->w_tiecnt);
+  w.shist = at<int32_t>(base, p->w_shist);
+  w.wcnt = at<int32_t>(base, p->w_wcnt);
+  return w;
+}
+
+static akv::DecWs dws_ptrs(const anchorkv_plan* p, void* base) {
+  akv::DecWs d;
+  d.SK = at<float>(base, p->d_SK);
+  d.qrot = at<float>(base, p->d_qrot);
+  d.part = at<float>(base, p->d_part);
+  return d;
+}
+
+static anchorkv_status hip_status(hipError_t e, const char* what) {
+  if (e == hipSuccess) return ANCHORKV_OK;
+  return fail(ANCHORKV_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+extern "C" anchorkv_status anchorkv_encode(const anchorkv_plan* p, const void* K, const void* V, const void* Q_obs,
+                                           const int32_t* anchor_pos_override, void* cache, void* workspace,
+                                           void* stream) {
+  if (!p || !K || !V || !Q_obs || !cache || !workspace) return fail(ANCHORKV_ERR_INVALID_ARG, "null argument");
+  const hipStream_t st = (hipStream_t)stream;
+  const akv::Cache c = cache_ptrs(p, cache);
+  const akv::Ws w = ws_ptrs(p, workspace);
+  const Geo& g = p->geo;
+  (void)hipGetLastError();
+  anchorkv_status s;
+  if ((s = hip_status(akv::launch_init(g, c, w, st), "init")) != ANCHORKV_OK) return s;
+  if ((s = hip_status(akv::launch_obs(g, w, K, V, Q_obs, st), "observation pass")) != ANCHORKV_OK) return s;
+  if ((s = hip_status(akv::launch_select(g, w, c, K, V, Q_obs, anchor_pos_override, st), "anchor selection")) !=
+      ANCHORKV_OK)
+    return s;
+  if ((s = hip_status(akv::launch_assign(g, w, c, K, V, st), "assignment")) != ANCHORKV_OK) return s;
+  if ((s = hip_status(akv::launch_epilogue(g, w, c, K, V, Q_obs, st), "utilities")) != ANCHORKV_OK) return s;
+  if ((s = hip_status(akv::launch_budget(g, w, st), "budget")) != ANCHORKV_OK) return s;
+  if ((s = hip_status(akv::launch_layout(g, w, c, K, V, st), "layout")) != ANCHORKV_OK) return s;
+  return ANCHORKV_OK;
+}
+
+extern "C" anchorkv_status anchorkv_append(const anchorkv_plan* p, void* cache, int32_t n_appended, const void* k_new,
+                                           const void* v_new, void* stream) {
+  if (!p || !cache || !k_new || !v_new) return fail(ANCHORKV_ERR_INVALID_ARG, "null argument");
+  if (n_appended < 0) return fail(ANCHORKV_ERR_INVALID_ARG, "n_appended must be >= 0");
+  if (n_appended >= p->cfg.max_append) return fail(ANCHORKV_ERR_CAPACITY, "append capacity exhausted");
+  (void)hipGetLastError();
+  return hip_status(akv::launch_append(p->geo, cache_ptrs(p, cache), n_appended, k_new, v_new, (hipStream_t)stream),
+                    "append");
+}
+
+extern "C" anchorkv_status anchorkv_decode_attn(const anchorkv_plan* p, const void* cache, int32_t n_appended,
+                                                const void* q, void* out, int32_t out_dtype, float softmax_scale,
+                                                void* workspace, void* stream) {
+  if (!p || !cache || !q || !out || !workspace) return fail(ANCHORKV_ERR_INVALID_ARG, "null argument");
+  if (n_appended < 0 || n_appended > p->cfg.max_append)
+    return fail(ANCHORKV_ERR_INVALID_ARG, "n_appended must be in [0, max_append]");
+  if (out_dtype != ANCHORKV_F32 && out_dtype != ANCHORKV_BF16) return fail(ANCHORKV_ERR_INVALID_ARG, "bad out_dtype");
+  const float scale = softmax_scale > 0.0f ? softmax_scale : 1.0f / sqrtf((float)p->geo.D);
+  (void)hipGetLastError();
+  return hip_status(akv::launch_decode(p->geo, cache_ptrs(p, (void*)cache), dws_ptrs(p, workspace), q, out, out_dtype,
+                                       scale, n_appended, (hipStream_t)stream),
+                    "decode");
+}
+
+extern "C" anchorkv_status anchorkv_reconstruct(const anchorkv_plan* p, const void* cache, int32_t n_appended,
+                                                int32_t request, int32_t side, float* out, void* stream) {
+  if (!p || !cache || !out) return fail(ANCHORKV_ERR_INVALID_ARG, "null argument");
+  if (request < 0 || request >= p->geo.B) return fail(ANCHORKV_ERR_INVALID_ARG, "request out of range");
+  if (side != 0 && side != 1) return fail(ANCHORKV_ERR_INVALID_ARG, "side must be 0 (keys) or 1 (values)");
+  if (n_appended < 0 || n_appended > p->cfg.max_append)
+    return fail(ANCHORKV_ERR_INVALID_ARG, "n_appended must be in [0, max_append]");
+  (void)hipGetLastError();
+  return hip_status(
+      akv::launch_reconstruct(p->geo, cache_ptrs(p, (void*)cache), request, side, n_appended, out, (hipStream_t)stream),
+      "reconstruct");
+}
+
+static float coef_host(const void* base, size_t i, int dtype) {
+  if (dtype == ANCHORKV_BF16) return akv::bf2f(((const uint16_t*)base)[i]);
+  return ((const float*)base)[i];
+}
+
+extern "C" anchorkv_status anchorkv_export(const anchorkv_plan* p, const void* cache_host, int32_t b,
+                                           int32_t n_appended, anchorkv_export_arrays* o) {
+  if (!p || !cache_host || !o) return fail(ANCHORKV_ERR_INVALID_ARG, "null argument");
+  if (b < 0 || b >= p->geo.B) return fail(ANCHORKV_ERR_INVALID_ARG, "request out of range");
+  if (n_appended < 0 || n_appended > p->cfg.max_append)
+    return fail(ANCHORKV_ERR_INVALID_ARG, "n_appended must be in [0, max_append]");
+  const akv::Cache c = cache_ptrs(p, (void*)cache_host);
+  const Geo& g = p->geo;
+  if (c.header[0] != kMagic || c.header[1] != kVersion || (int)c.header[3] != g.B || (int)c.header[4] != g.H ||
+      (int)c.header[5] != g.D || (int)c.header[6] != g.dtype)
+    return fail(ANCHORKV_ERR_CORRUPT_CACHE, "cache header does not match the plan");
+  if (c.header[2] & 1u) return fail(ANCHORKV_ERR_CORRUPT_CACHE, "invalid anchor override");
+  if (c.header[2] & 2u) return fail(ANCHORKV_ERR_CORRUPT_CACHE, "anchor selection count mismatch");
+  const int H = g.H, S = g.S[b], k = g.k[b], D = g.D, G = g.G, nw = (S + 63) / 64;
+  const size_t ko = (size_t)g.prefK[b] * H, po = (size_t)g.prefS[b] * H, wo = (size_t)g.prefW[b] * H;
+  if (o->anchors) memcpy(o->anchors, c.anc_pos + ko, sizeof(int32_t) * H * k);
+  for (int side = 0; side < 2; ++side) {
+    int32_t* a_out = side ? o->a_v : o->a_k;
+    float* g_out = side ? o->gamma_v : o->gamma_k;
+    uint8_t* s_out = side ? o->sel_v : o->sel_k;
+    uint8_t* c_out = side ? o->codes_v : o->codes_k;
+    float* sc_out = side ? o->scales_v : o->scales_k;
+    const uint16_t* idx = side ? c.idxV : c.idxK;
+    const void* gm = side ? c.gV : c.gK;
+    const uint64_t* mask = side ? c.maskV : c.maskK;
+    const int32_t* pc = side ? c.pcV : c.pcK;
+    const uint8_t* codes = side ? c.codesV : c.codesK;
+    const float* scales = side ? c.scalesV : c.scalesK;
+    const int ntot = side ? g.prefNV[g.B] : g.prefNK[g.B];
+    if (c_out) memset(c_out, 0, (size_t)H * S * (D / 4));
+    if (sc_out) memset(sc_out, 0, sizeof(float) * (size_t)H * S * (D / G));
+    for (int h = 0; h < H; ++h)
+      for (int i = 0; i < S; ++i) {
+        const size_t e = po + (size_t)h * S + i;
+        const int t = c.pos[e];
+        if (t < 0 || t >= S) return fail(ANCHORKV_ERR_CORRUPT_CACHE, "position id out of range");
+        const size_t te = (size_t)h * S + t;
+        if (a_out) a_out[te] = idx[e];
+        if (g_out) g_out[te] = coef_host(gm, e, g.dtype);
+        const size_t wi = wo + (size_t)h * nw + (i >> 6);
+        const uint64_t wm = mask[wi];
+        const bool sel = (wm >> (i & 63)) & 1u;
+        if (s_out) s_out[te] = sel;
+        if (sel) {
+          const int slot = pc[wi] + __builtin_popcountll(wm & ((1ull << (i & 63)) - 1ull));
+          if (slot < 0 || slot >= ntot) return fail(ANCHORKV_ERR_CORRUPT_CACHE, "residual slot out of range");
+          if (c_out) memcpy(c_out + te * (D / 4), codes + (size_t)slot * (D / 4), D / 4);
+          if (sc_out) memcpy(sc_out + te * (D / G), scales + (size_t)slot * (D / G), sizeof(float) * (D / G));
+        }
+      }
+    int32_t* ta = side ? o->tail_a_v : o->tail_a_k;
+    float* tg = side ? o->tail_gamma_v : o->tail_gamma_k;
+    const uint16_t* tidx = side ? c.tidxV : c.tidxK;
+    const void* tgm = side ? c.tgV : c.tgK;
+    for (int h = 0; h < H; ++h)
+      for (int n = 0; n < n_appended; ++n) {
+        const size_t ti = ((size_t)b * H + h) * g.max_append + n;
+        if (ta) ta[(size_t)h * n_appended + n] = tidx[ti];
+        if (tg) tg[(size_t)h * n_appended + n] = coef_host(tgm, ti, g.dtype);
+      }
+  }
+  if (o->stats) {
+    o->stats[0] = c.stats[b * 4 + 0];
+    o->stats[1] = c.stats[b * 4 + 1];
+    o->stats[2] = p->req[b].residuals_k;
+    o->stats[3] = p->req[b].residuals_v;
+  }
+  return ANCHORKV_OK;
+}
+
+extern "C" const char* anchorkv_status_string(anchorkv_status s) {
+  switch (s) {
+    case ANCHORKV_OK: return "ok";
+    case ANCHORKV_ERR_INVALID_ARG: return "invalid argument";
+    case ANCHORKV_ERR_UNSUPPORTED: return "unsupported configuration";
+    case ANCHORKV_ERR_CAPACITY: return "append capacity exhausted";
+    case ANCHORKV_ERR_CORRUPT_CACHE: return "corrupt cache";
+    case ANCHORKV_ERR_HIP: return "HIP runtime error";
+  }
+  return "unknown status";
+}
+
+extern "C" const char* anchorkv_last_error(void) { return g_last_error.c_str(); }
+
+// ------------------------------------------------------------------ init kernel
+namespace akv {
+__global__ void k_init(Geo g, Cache c, Ws w) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i == 0) {
+    c.header[0] = kMagic;
+    c.header[1] = kVersion;
+    c.header[2] = 0;
+    c.header[3] = (uint32_t)g.B;
+    c.header[4] = (uint32_t)g.H;
+    c.header[5] = (uint32_t)g.D;
+    c.header[6] = (uint32_t)g.dtype;
+    w.fixcount[0] = 0;
+    w.fixcount[1] = 0;
+  }
+  if (i < 4 * g.B) c.stats[i] = 0;
+}
+hipError_t launch_init(const Geo& g, const Cache& c, const Ws& w, hipStream_t st) {
+  k_init<<<(4 * g.B + 255) / 256 + 1, 256, 0, st>>>(g, c, w);
+  return hipGetLastError();
+}
+}  // namespace akv
