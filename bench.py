@@ -1,0 +1,250 @@
+#!/usr/bin/env python3
+"""Benchmark of the AnchorKV hot path on one MI355X (gfx950).
+
+Workload (default): one Llama-3.1-8B attention layer shape at 128K context
+(8 KV heads, 32 query heads, head_dim 128, bf16; anchors 2 % of the tokens,
+residual budget 5 % per side), seeded synthetic clustered keys/values with 4
+outlier key channels.  A model has many such layers, and a single compressed
+layer (~25 MB) would sit in the 256 MB Infinity Cache, so the benchmark keeps
+L = 32 independently generated layers resident in HBM and one step is:
+
+  1. the compression pass (encode) of all L layers;
+  2. 64 decode steps; in each, every layer appends one generated token per KV
+     head (encoded against its anchors) and runs decode attention for the 32
+     query heads over its compressed cache;
+  3. one dense reconstruction (the debug API) of one layer's keys.
+
+Reported: value = decode throughput in GB/s = algorithmic bytes the decode
+attention must read per layer-step (records, residual flag words, residual
+codes and scales, anchor keys and values, query) x layer-steps / time of the
+decode phase (appends included); decode us per layer-step; encode Mtok/s
+(tokens compressed / encode-phase time).  Kernel durations come from HIP
+events the library records around the named kernels on their own stream.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--layers L]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "decode-attn HBM GB/s & µs/step on compressed cache; encode Mtok/s"
+HBM_PEAK_GBS = 8000.0
+BF16_PEAK_TFLOPS = 2500.0
+FP32_PEAK_TFLOPS = 157.3
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def decode_bytes(plan, H, Hq, D, G, esz):
+    """Algorithmic bytes read by one decode-attention call per request-layer:
+    per sorted slot 2 x (uint16 index + coefficient), residual flag words and
+    slot bases, each stored residual's codes and scales, the anchor keys and
+    values, the query and the output."""
+    tot = 0
+    stream = 0
+    for ri in plan.requests:
+        S, k = ri.seq_len, ri.anchors
+        recs = H * S * 2 * (2 + esz)
+        flags = 2 * H * math.ceil(S / 64) * (8 + 4)
+        res = (ri.residuals_k + ri.residuals_v) * (D // 4 + 4 * (D // G))
+        anc = 2 * H * k * D * esz
+        tot += recs + flags + res + anc + Hq * D * esz * 2
+        stream += recs + flags + res + H * k * D * esz  # the streaming kernel reads the value anchors
+    return tot, stream
+
+
+def encode_flops(plan, H, D):
+    """Similarity contraction of both sides on non-anchor rows: 2 sides x 2 FLOP
+    x (S - k) x k x D per head."""
+    return sum(4.0 * H * (ri.seq_len - ri.anchors) * ri.anchors * D for ri in plan.requests)
+
+
+def cpu_baseline(wl, seed):
+    """The CPU oracle on a bounded sample of the same workload: the first
+    S_s = 4096 positions of one layer (all 8 heads), compressed with the same
+    recipe (k = 2 %, 5 % residuals), then one decode step over it."""
+    import numpy as np
+    import synth
+    from oracle import akvref as R
+
+    Ss = 4096
+    sub = synth.Workload("cpu-sample", H=wl.H, Hq=wl.Hq, D=wl.D, seq_lens=[Ss], dtype=wl.dtype,
+                         anchor_frac=wl.anchor_frac, budget=wl.budget, n_centers=wl.n_centers, steps=1, seed=seed)
+    layer = synth.make_layer(sub)
+    K, V, Q = (x[0].float().numpy() for x in (layer.K, layer.V, layer.Qobs))
+    k = sub.k_of(Ss)
+    t0 = time.perf_counter()
+    enc = R.encode(K, V, Q, W=32, k=k, bf16=True, seed=seed, budget=float(np.float32(wl.budget)), G=wl.D)
+    t_enc = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    Kh = R.reconstruct(K, enc, "K", wl.D, seed)
+    Vh = R.reconstruct(V, enc, "V", wl.D, seed)
+    R.attention(Kh, Vh, layer.q[0, 0].float().numpy())
+    t_dec = time.perf_counter() - t0
+    nk, nv = int(enc["nsel"][0]), int(enc["nsel"][1])
+    H, D = wl.H, wl.D
+    byts = (H * Ss * 8 + 2 * H * math.ceil(Ss / 64) * 12 + (nk + nv) * (D // 4 + 4) + 2 * H * k * D * 2
+            + wl.Hq * D * 4)
+    return dict(value=round(byts / t_dec / 1e9, 4), unit="GB/s", cores=R.num_threads(), kind="oracle",
+                sample=f"first {Ss} positions of one layer (H={H}, Hq={wl.Hq}, bf16, k={k}): "
+                       f"oracle encode {t_enc:.2f} s, one oracle decode step {t_dec:.2f} s",
+                encode_mtok_s=round(Ss / t_enc / 1e6, 6), decode_s=round(t_dec, 4), encode_s=round(t_enc, 3))
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--layers", type=int, default=32)
+    ap.add_argument("--decode-steps", type=int, default=64)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU: this build is a single-GPU hot path (no collectives); "
+              "run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2608_02901_amd as akv
+    import synth
+    from paper_2608_02901_amd import _native as N
+
+    torch.cuda.set_device(0)
+    wl = synth.workload(3)
+    NS = args.decode_steps
+    wl.steps = NS
+    S = wl.seq_lens[0]
+    cfg = N.Config.make(num_kv_heads=wl.H, num_q_heads=wl.Hq, head_dim=wl.D, window=wl.window,
+                        anchor_frac=wl.anchor_frac, rho=0.7, kappa=7, budget=wl.budget, dtype=N.BF16,
+                        max_append=NS, seed=wl.seed)
+    plan = N.Plan(cfg, wl.seq_lens)
+    ri = plan.requests[0]
+    log(f"workload {wl.name}: S={S} H={wl.H} Hq={wl.Hq} k={ri.anchors} N_K={ri.residuals_k} "
+        f"N_V={ri.residuals_v} cache={plan.cache_bytes / 1e6:.1f} MB layers={args.layers}")
+
+    L = args.layers
+    layers, caches = [], []
+    for l in range(L):
+        layers.append(synth.make_layer(wl, device="cuda", seed=wl.seed + 1000 * l, steps=NS))
+        caches.append(torch.zeros(plan.cache_bytes, dtype=torch.uint8, device="cuda"))
+        if l % 8 == 0:
+            log(f"generated layer {l}")
+    packed = [(L_.K[0].contiguous(), L_.V[0].contiguous(), L_.Qobs[0].contiguous()) for L_ in layers]
+    ws = torch.empty(plan.encode_ws_bytes, dtype=torch.uint8, device="cuda")
+    dws = torch.empty(plan.decode_ws_bytes, dtype=torch.uint8, device="cuda")
+    out = torch.empty(1, wl.Hq, wl.D, dtype=torch.bfloat16, device="cuda")
+    dense = torch.empty(wl.H, S + NS, wl.D, dtype=torch.float32, device="cuda")
+    torch.cuda.synchronize()
+
+    def step(ev=None):
+        if ev:
+            ev[0].record()
+        for l in range(L):
+            K, V, Q = packed[l]
+            akv.encode(plan, K, V, Q, caches[l], ws)
+        if ev:
+            ev[1].record()
+        for s in range(NS):
+            for l in range(L):
+                lay = layers[l]
+                akv.append(plan, caches[l], s, lay.k_new[s], lay.v_new[s])
+                akv.decode_attn(plan, caches[l], lay.q[s], out, dws, n_appended=s + 1)
+        if ev:
+            ev[2].record()
+        akv.reconstruct(plan, caches[0], 0, 0, n_appended=NS, out=dense)
+        if ev:
+            ev[3].record()
+
+    for i in range(args.warmup):
+        step()
+        torch.cuda.synchronize()
+        log(f"warmup step {i} done")
+
+    kernels = ["k_dec_stream", "k_assign", "k_dec_scores", "k_dec_combine", "k_append"]
+    timer = N.KernelTimer(kernels, max_launches=max(64, args.steps * NS * L + 16))
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(evs[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    log(f"timed {args.steps} steps in {wall:.3f} s")
+    enc_ms = sum(e[0].elapsed_time(e[1]) for e in evs) / args.steps
+    dec_ms = sum(e[1].elapsed_time(e[2]) for e in evs) / args.steps
+    rec_ms = sum(e[2].elapsed_time(e[3]) for e in evs) / args.steps
+    step_ms = sum(e[0].elapsed_time(e[3]) for e in evs) / args.steps
+    ktimes = {}
+    for kname in kernels:
+        ms, n = timer.read(kname)
+        ktimes[kname] = (ms / max(n, 1), n)
+    timer.close()
+
+    dbytes, sbytes = decode_bytes(plan, wl.H, wl.Hq, wl.D, wl.G, 2)
+    dec_calls = NS * L
+    value = dbytes * dec_calls / (dec_ms / 1e3) / 1e9
+    stream_ms = ktimes["k_dec_stream"][0]
+    ach = sbytes / (stream_ms / 1e3) / 1e9
+    fl = encode_flops(plan, wl.H, wl.D)
+    assign_ms = ktimes["k_assign"][0]
+    ach_e = fl / (assign_ms / 1e3) / 1e12
+
+    cache_host = caches[0].cpu().numpy()
+    ex = akv.export(plan, cache_host, 0, NS)
+    fix_k, fix_v = int(ex["stats"][0]), int(ex["stats"][1])
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("cpu baseline (oracle on a bounded sample)")
+        cpu = cpu_baseline(wl, wl.seed)
+
+    res = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(step_ms, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "layers": L, "kv_heads": wl.H, "q_heads": wl.Hq, "head_dim": wl.D,
+                   "seq_len": S, "batch": 1, "decode_steps": NS, "anchors": ri.anchors,
+                   "residuals_per_side": ri.residuals_k, "window": wl.window, "parallelism": "single-gpu"},
+        "decode_us_per_step": round(dec_ms * 1e3 / dec_calls, 3),
+        "decode_attn_bytes_per_call": dbytes,
+        "encode_mtok_s": round(L * S / (enc_ms / 1e3) / 1e6, 3),
+        "encode_ms_per_layer": round(enc_ms / L, 4),
+        "reconstruct_ms": round(rec_ms, 4),
+        "kernel_avg_us": {k: round(v[0] * 1e3, 3) for k, v in ktimes.items()},
+        "fixup_rows_layer0": [fix_k, fix_v],
+        "roofline": {"bound": "hbm", "kernel": "k_dec_stream", "achieved": round(ach, 2), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": None,
+                     "bytes_per_launch": sbytes},
+        "roofline_encode": {"bound": "mfma", "kernel": "k_assign", "achieved": round(ach_e, 2),
+                            "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": round(ach_e / BF16_PEAK_TFLOPS, 4),
+                            "flops_per_launch": fl},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -191,6 +191,18 @@ typedef struct anchorkv_export_arrays {
 anchorkv_status anchorkv_export(const anchorkv_plan* plan, const void* cache_host, int32_t request,
                                 int32_t n_appended, anchorkv_export_arrays* out);
 
+/* Kernel timing for benchmarks and tracing.  While enabled, every launch of
+ * a kernel named in the comma-separated list `kernels` (e.g.
+ * "k_dec_stream,k_assign") is bracketed by a pair of HIP events recorded on
+ * the launch's own stream, up to max_launches pairs per kernel (events are
+ * created here, host side, no device memory).  anchorkv_profile_read waits
+ * for the recorded events of one kernel and returns their summed elapsed
+ * milliseconds and the number of timed launches; disable releases the events.
+ * Process-wide; calls are serialized by a lock. */
+anchorkv_status anchorkv_profile_enable(const char* kernels, int32_t max_launches);
+anchorkv_status anchorkv_profile_read(const char* kernel, float* total_ms, int32_t* launches);
+anchorkv_status anchorkv_profile_disable(void);
+
 const char* anchorkv_status_string(anchorkv_status status);
 const char* anchorkv_last_error(void);
 

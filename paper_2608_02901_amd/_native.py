@@ -23,8 +23,8 @@ BUDGET_FRACTION, BUDGET_THETA, BUDGET_COUNT = 0, 1, 2
 
 EXPORTED = ["anchorkv_plan_create", "anchorkv_plan_destroy", "anchorkv_cache_bytes", "anchorkv_encode_workspace_bytes",
             "anchorkv_decode_workspace_bytes", "anchorkv_plan_request", "anchorkv_encode", "anchorkv_append",
-            "anchorkv_decode_attn", "anchorkv_reconstruct", "anchorkv_export", "anchorkv_status_string",
-            "anchorkv_last_error"]
+            "anchorkv_decode_attn", "anchorkv_reconstruct", "anchorkv_export", "anchorkv_profile_enable",
+            "anchorkv_profile_read", "anchorkv_profile_disable", "anchorkv_status_string", "anchorkv_last_error"]
 
 
 class AnchorKVError(RuntimeError):
@@ -89,6 +89,12 @@ def lib():
         L.anchorkv_reconstruct.argtypes = [vp, vp, i32, i32, i32, vp, vp]
         L.anchorkv_export.restype = i32
         L.anchorkv_export.argtypes = [vp, vp, i32, i32, ctypes.POINTER(ExportArrays)]
+        L.anchorkv_profile_enable.restype = i32
+        L.anchorkv_profile_enable.argtypes = [ctypes.c_char_p, i32]
+        L.anchorkv_profile_read.restype = i32
+        L.anchorkv_profile_read.argtypes = [ctypes.c_char_p, ctypes.POINTER(f32), ctypes.POINTER(i32)]
+        L.anchorkv_profile_disable.restype = i32
+        L.anchorkv_profile_disable.argtypes = []
         L.anchorkv_status_string.restype = ctypes.c_char_p
         L.anchorkv_status_string.argtypes = [i32]
         L.anchorkv_last_error.restype = ctypes.c_char_p
@@ -196,6 +202,25 @@ def reconstruct(plan: Plan, cache, request: int, side: int, n_appended: int = 0,
         out = torch.empty(H, rows, D, dtype=torch.float32, device=cache.device)
     check(lib().anchorkv_reconstruct(plan.handle, _ptr(cache), n_appended, request, side, _ptr(out), _stream(stream)))
     return out
+
+
+class KernelTimer:
+    """Times every launch of the named library kernels with HIP events
+    recorded on each kernel's own stream (anchorkv_profile_*)."""
+
+    def __init__(self, kernels, max_launches: int = 4096):
+        self.kernels = [kernels] if isinstance(kernels, str) else list(kernels)
+        check(lib().anchorkv_profile_enable(",".join(self.kernels).encode(), max_launches))
+
+    def read(self, kernel: str):
+        """(summed milliseconds, number of timed launches) of one kernel."""
+        ms = ctypes.c_float()
+        n = ctypes.c_int32()
+        check(lib().anchorkv_profile_read(kernel.encode(), ctypes.byref(ms), ctypes.byref(n)))
+        return float(ms.value), int(n.value)
+
+    def close(self):
+        check(lib().anchorkv_profile_disable())
 
 
 def export(plan: Plan, cache_host: np.ndarray, request: int, n_appended: int = 0) -> dict:

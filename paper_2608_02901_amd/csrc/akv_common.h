@@ -251,4 +251,15 @@ __device__ inline int locate(const Geo& g, int tile, int mult, int& idx) {
   return -1;
 }
 
+// Kernel timing hook (anchorkv_profile_*): records a HIP event on `st` before
+// (after = false) or after a launch of the named kernel when it is profiled.
+void prof_mark(const char* kernel, hipStream_t st, bool after);
+
 }  // namespace akv
+
+#define AKV_TIMED(name, st, ...)           \
+  do {                                     \
+    ::akv::prof_mark(name, st, false);     \
+    __VA_ARGS__;                           \
+    ::akv::prof_mark(name, st, true);      \
+  } while (0)

@@ -5,6 +5,8 @@
 #include <math.h>
 #include <string.h>
 
+#include <atomic>
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
@@ -522,6 +524,106 @@ extern "C" const char* anchorkv_status_string(anchorkv_status s) {
 
 extern "C" const char* anchorkv_last_error(void) { return g_last_error.c_str(); }
 
+// ------------------------------------------------------------------ kernel timing
+namespace {
+struct KernelEvents {
+  std::string name;
+  std::vector<hipEvent_t> ev;  // 2 per launch
+  int used = 0;
+  bool open = false;
+};
+struct Profiler {
+  std::mutex mu;
+  std::atomic<bool> on{false};
+  std::vector<KernelEvents> k;
+};
+Profiler& profiler() {
+  static Profiler p;
+  return p;
+}
+void release_events(Profiler& p) {
+  for (auto& ke : p.k)
+    for (hipEvent_t e : ke.ev)
+      if (e) (void)hipEventDestroy(e);
+  p.k.clear();
+}
+}  // namespace
+
+void akv::prof_mark(const char* kernel, hipStream_t st, bool after) {
+  Profiler& p = profiler();
+  if (!p.on.load(std::memory_order_acquire)) return;
+  std::lock_guard<std::mutex> lk(p.mu);
+  for (auto& ke : p.k) {
+    if (ke.name != kernel) continue;
+    if (!after) {
+      if (2 * ke.used + 1 < (int)ke.ev.size() && hipEventRecord(ke.ev[2 * ke.used], st) == hipSuccess) ke.open = true;
+    } else if (ke.open) {
+      if (hipEventRecord(ke.ev[2 * ke.used + 1], st) == hipSuccess) ++ke.used;
+      ke.open = false;
+    }
+  }
+}
+
+extern "C" anchorkv_status anchorkv_profile_enable(const char* kernels, int32_t max_launches) {
+  if (!kernels || max_launches < 1) return fail(ANCHORKV_ERR_INVALID_ARG, "bad profile request");
+  Profiler& p = profiler();
+  std::lock_guard<std::mutex> lk(p.mu);
+  p.on.store(false);
+  release_events(p);
+  std::string all(kernels);
+  size_t pos = 0;
+  while (pos <= all.size()) {
+    size_t e = all.find(',', pos);
+    if (e == std::string::npos) e = all.size();
+    if (e > pos) {
+      KernelEvents ke;
+      ke.name = all.substr(pos, e - pos);
+      ke.ev.assign(2 * (size_t)max_launches, nullptr);
+      p.k.push_back(ke);
+      for (auto& ev : p.k.back().ev) {
+        if (hipEventCreate(&ev) != hipSuccess) {
+          ev = nullptr;
+          release_events(p);
+          return fail(ANCHORKV_ERR_HIP, "hipEventCreate failed");
+        }
+      }
+    }
+    pos = e + 1;
+  }
+  if (p.k.empty()) return fail(ANCHORKV_ERR_INVALID_ARG, "no kernel named");
+  p.on.store(true, std::memory_order_release);
+  return ANCHORKV_OK;
+}
+
+extern "C" anchorkv_status anchorkv_profile_read(const char* kernel, float* total_ms, int32_t* launches) {
+  if (!kernel || !total_ms || !launches) return fail(ANCHORKV_ERR_INVALID_ARG, "null argument");
+  Profiler& p = profiler();
+  std::lock_guard<std::mutex> lk(p.mu);
+  for (auto& ke : p.k) {
+    if (ke.name != kernel) continue;
+    float tot = 0.0f;
+    for (int i = 0; i < ke.used; ++i) {
+      if (hipEventSynchronize(ke.ev[2 * i + 1]) != hipSuccess) return fail(ANCHORKV_ERR_HIP, "hipEventSynchronize failed");
+      float ms = 0.0f;
+      if (hipEventElapsedTime(&ms, ke.ev[2 * i], ke.ev[2 * i + 1]) != hipSuccess)
+        return fail(ANCHORKV_ERR_HIP, "hipEventElapsedTime failed");
+      tot += ms;
+    }
+    *total_ms = tot;
+    *launches = ke.used;
+    return ANCHORKV_OK;
+  }
+  return fail(ANCHORKV_ERR_INVALID_ARG, "kernel is not being profiled");
+}
+
+extern "C" anchorkv_status anchorkv_profile_disable(void) {
+  Profiler& p = profiler();
+  std::lock_guard<std::mutex> lk(p.mu);
+  p.on.store(false);
+  release_events(p);
+  return ANCHORKV_OK;
+}
+
 // ------------------------------------------------------------------ init kernel
 namespace akv {
 __global__ void k_init(Geo g, Cache c, Ws w) {
@@ -540,7 +642,7 @@ __global__ void k_init(Geo g, Cache c, Ws w) {
   if (i < 4 * g.B) c.stats[i] = 0;
 }
 hipError_t launch_init(const Geo& g, const Cache& c, const Ws& w, hipStream_t st) {
-  k_init<<<(4 * g.B + 255) / 256 + 1, 256, 0, st>>>(g, c, w);
+  AKV_TIMED("k_init", st, k_init<<<(4 * g.B + 255) / 256 + 1, 256, 0, st>>>(g, c, w));
   return hipGetLastError();
 }
 }  // namespace akv

@@ -525,7 +525,7 @@ template <int DT, int GQ>
 static void launch_stream(const Geo& g, const Cache& c, const DecWs& dw, float scale, int nblk, size_t lds,
                           hipStream_t st) {
   (void)hipFuncSetAttribute((const void*)k_dec_stream<DT, GQ, 8>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-  k_dec_stream<DT, GQ, 8><<<nblk, 256, lds, st>>>(g, c, dw, scale);
+  AKV_TIMED("k_dec_stream", st, k_dec_stream<DT, GQ, 8><<<nblk, 256, lds, st>>>(g, c, dw, scale));
 }
 
 hipError_t launch_decode(const Geo& g, const Cache& c, const DecWs& dw, const void* q, void* out, int out_dtype,
@@ -537,9 +537,9 @@ hipError_t launch_decode(const Geo& g, const Cache& c, const DecWs& dw, const vo
     nst += g.H * ((g.S[b] + L - 1) / L);
   }
   if (g.dtype == 1) {
-    k_dec_scores<1><<<nsc, 256, 0, st>>>(g, c, dw, q);
+    AKV_TIMED("k_dec_scores", st, k_dec_scores<1><<<nsc, 256, 0, st>>>(g, c, dw, q));
   } else {
-    k_dec_scores<0><<<nsc, 256, 0, st>>>(g, c, dw, q);
+    AKV_TIMED("k_dec_scores", st, k_dec_scores<0><<<nsc, 256, 0, st>>>(g, c, dw, q));
   }
   const size_t lds = ((size_t)g.g * g.maxK + (size_t)g.g * (size_t)min(g.maxK, L)) * sizeof(float);
 #define AKV_STREAM(DT)                                                   \
@@ -556,18 +556,18 @@ hipError_t launch_decode(const Geo& g, const Cache& c, const DecWs& dw, const vo
   }
 #undef AKV_STREAM
   if (g.dtype == 1) {
-    k_dec_combine<1><<<g.B * g.Hq, 128, 0, st>>>(g, c, dw, scale, L, n_app, out, out_dtype);
+    AKV_TIMED("k_dec_combine", st, k_dec_combine<1><<<g.B * g.Hq, 128, 0, st>>>(g, c, dw, scale, L, n_app, out, out_dtype));
   } else {
-    k_dec_combine<0><<<g.B * g.Hq, 128, 0, st>>>(g, c, dw, scale, L, n_app, out, out_dtype);
+    AKV_TIMED("k_dec_combine", st, k_dec_combine<0><<<g.B * g.Hq, 128, 0, st>>>(g, c, dw, scale, L, n_app, out, out_dtype));
   }
   return hipGetLastError();
 }
 
 hipError_t launch_append(const Geo& g, const Cache& c, int n_app, const void* kn, const void* vn, hipStream_t st) {
   if (g.dtype == 1) {
-    k_append<1><<<g.B * g.H * 2, 256, 0, st>>>(g, c, n_app, kn, vn);
+    AKV_TIMED("k_append", st, k_append<1><<<g.B * g.H * 2, 256, 0, st>>>(g, c, n_app, kn, vn));
   } else {
-    k_append<0><<<g.B * g.H * 2, 256, 0, st>>>(g, c, n_app, kn, vn);
+    AKV_TIMED("k_append", st, k_append<0><<<g.B * g.H * 2, 256, 0, st>>>(g, c, n_app, kn, vn));
   }
   return hipGetLastError();
 }
@@ -576,9 +576,9 @@ hipError_t launch_reconstruct(const Geo& g, const Cache& c, int b, int side, int
   const int rows = g.S[b] + n_app;
   const int nblk = (g.H * rows + 3) / 4;
   if (g.dtype == 1) {
-    k_reconstruct<1><<<nblk, 256, 0, st>>>(g, c, b, side, n_app, out);
+    AKV_TIMED("k_reconstruct", st, k_reconstruct<1><<<nblk, 256, 0, st>>>(g, c, b, side, n_app, out));
   } else {
-    k_reconstruct<0><<<nblk, 256, 0, st>>>(g, c, b, side, n_app, out);
+    AKV_TIMED("k_reconstruct", st, k_reconstruct<0><<<nblk, 256, 0, st>>>(g, c, b, side, n_app, out));
   }
   return hipGetLastError();
 }

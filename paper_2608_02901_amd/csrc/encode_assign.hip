@@ -224,11 +224,11 @@ hipError_t launch_assign(const Geo& g, const Ws& w, const Cache& c, const void* 
   int nblk = 0;
   for (int b = 0; b < g.B; ++b) nblk += g.H * ((g.S[b] + 127) / 128) * 2;
   if (g.dtype == 1) {
-    k_assign<1><<<nblk, 256, 0, st>>>(g, w, c, K, V);
-    k_fixup<1><<<1024, 256, 0, st>>>(g, w, c, K, V);
+    AKV_TIMED("k_assign", st, k_assign<1><<<nblk, 256, 0, st>>>(g, w, c, K, V));
+    AKV_TIMED("k_fixup", st, k_fixup<1><<<1024, 256, 0, st>>>(g, w, c, K, V));
   } else {
-    k_assign<0><<<nblk, 256, 0, st>>>(g, w, c, K, V);
-    k_fixup<0><<<1024, 256, 0, st>>>(g, w, c, K, V);
+    AKV_TIMED("k_assign", st, k_assign<0><<<nblk, 256, 0, st>>>(g, w, c, K, V));
+    AKV_TIMED("k_fixup", st, k_fixup<0><<<1024, 256, 0, st>>>(g, w, c, K, V));
   }
   return hipGetLastError();
 }

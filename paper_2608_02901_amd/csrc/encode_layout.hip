@@ -309,20 +309,20 @@ hipError_t launch_layout(const Geo& g, const Ws& w, const Cache& c, const void* 
     nrec += g.H * ((g.S[b] + 255) / 256);
   }
   const size_t lds = (size_t)g.maxK * sizeof(int);
-  k_shist<<<nsort, 256, lds, st>>>(g, w);
-  k_sscan<<<g.B * g.H, 1024, 0, st>>>(g, w);
-  k_sscatter<<<nsort, 64, lds, st>>>(g, w, c);
+  AKV_TIMED("k_shist", st, k_shist<<<nsort, 256, lds, st>>>(g, w));
+  AKV_TIMED("k_sscan", st, k_sscan<<<g.B * g.H, 1024, 0, st>>>(g, w));
+  AKV_TIMED("k_sscatter", st, k_sscatter<<<nsort, 64, lds, st>>>(g, w, c));
   if (g.dtype == 1) {
-    k_lrec<1><<<nrec, 256, 0, st>>>(g, w, c);
+    AKV_TIMED("k_lrec", st, k_lrec<1><<<nrec, 256, 0, st>>>(g, w, c));
   } else {
-    k_lrec<0><<<nrec, 256, 0, st>>>(g, w, c);
+    AKV_TIMED("k_lrec", st, k_lrec<0><<<nrec, 256, 0, st>>>(g, w, c));
   }
-  k_lscan<<<g.B * 2, 1024, 0, st>>>(g, w, c);
+  AKV_TIMED("k_lscan", st, k_lscan<<<g.B * 2, 1024, 0, st>>>(g, w, c));
   const int nwords = 2 * g.prefW[g.B] * g.H;
   if (g.dtype == 1) {
-    k_codec<1><<<(nwords + 3) / 4, 256, 0, st>>>(g, w, c, K, V);
+    AKV_TIMED("k_codec", st, k_codec<1><<<(nwords + 3) / 4, 256, 0, st>>>(g, w, c, K, V));
   } else {
-    k_codec<0><<<(nwords + 3) / 4, 256, 0, st>>>(g, w, c, K, V);
+    AKV_TIMED("k_codec", st, k_codec<0><<<(nwords + 3) / 4, 256, 0, st>>>(g, w, c, K, V));
   }
   return hipGetLastError();
 }

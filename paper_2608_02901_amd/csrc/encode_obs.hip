@@ -292,17 +292,17 @@ __global__ __launch_bounds__(128) void k_obs_yreduce(Geo g, Ws w) {
 hipError_t launch_obs(const Geo& g, const Ws& w, const void* K, const void* V, const void* Q, hipStream_t st) {
   int nblk = g.H * g.prefC[g.B];
   if (g.dtype == 1) {
-    k_obs_stats<1><<<nblk, 256, 0, st>>>(g, w, K, Q);
+    AKV_TIMED("k_obs_stats", st, k_obs_stats<1><<<nblk, 256, 0, st>>>(g, w, K, Q));
   } else {
-    k_obs_stats<0><<<nblk, 256, 0, st>>>(g, w, K, Q);
+    AKV_TIMED("k_obs_stats", st, k_obs_stats<0><<<nblk, 256, 0, st>>>(g, w, K, Q));
   }
-  k_obs_reduce<<<g.B * g.H, 256, 0, st>>>(g, w);
+  AKV_TIMED("k_obs_reduce", st, k_obs_reduce<<<g.B * g.H, 256, 0, st>>>(g, w));
   if (g.dtype == 1) {
-    k_obs_pass<1><<<nblk, 256, 0, st>>>(g, w, K, V, Q);
+    AKV_TIMED("k_obs_pass", st, k_obs_pass<1><<<nblk, 256, 0, st>>>(g, w, K, V, Q));
   } else {
-    k_obs_pass<0><<<nblk, 256, 0, st>>>(g, w, K, V, Q);
+    AKV_TIMED("k_obs_pass", st, k_obs_pass<0><<<nblk, 256, 0, st>>>(g, w, K, V, Q));
   }
-  k_obs_yreduce<<<g.B * g.H * g.m, 128, 0, st>>>(g, w);
+  AKV_TIMED("k_obs_yreduce", st, k_obs_yreduce<<<g.B * g.H * g.m, 128, 0, st>>>(g, w));
   return hipGetLastError();
 }
 

@@ -255,13 +255,13 @@ __global__ __launch_bounds__(256) void k_anchor_prep(Geo g, Ws w, Cache c, const
 
 hipError_t launch_select(const Geo& g, const Ws& w, const Cache& c, const void* K, const void* V, const void* Q,
                          const int32_t* ovr, hipStream_t st) {
-  k_select<<<g.B * g.H, 1024, 0, st>>>(g, w, c, ovr);
+  AKV_TIMED("k_select", st, k_select<<<g.B * g.H, 1024, 0, st>>>(g, w, c, ovr));
   int nblk = 0;
   for (int b = 0; b < g.B; ++b) nblk += g.H * ((g.k[b] + 63) / 64);
   if (g.dtype == 1) {
-    k_anchor_prep<1><<<nblk, 256, 0, st>>>(g, w, c, K, V, Q);
+    AKV_TIMED("k_anchor_prep", st, k_anchor_prep<1><<<nblk, 256, 0, st>>>(g, w, c, K, V, Q));
   } else {
-    k_anchor_prep<0><<<nblk, 256, 0, st>>>(g, w, c, K, V, Q);
+    AKV_TIMED("k_anchor_prep", st, k_anchor_prep<0><<<nblk, 256, 0, st>>>(g, w, c, K, V, Q));
   }
   return hipGetLastError();
 }
