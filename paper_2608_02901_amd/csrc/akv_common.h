@@ -38,8 +38,18 @@ struct Geo {
   int prefSp[AKV_MAXB + 1];  // sum of decode splits per head
   int prefNK[AKV_MAXB + 1];  // sum of key residual counts
   int prefNV[AKV_MAXB + 1];  // sum of value residual counts
+  int prefKp[AKV_MAXB + 1];  // sum of k rounded up to 4 (anchor-score table rows)
   int dsplit;                // decode split length (sorted slots per workgroup)
+  int maxRB;                 // decode: most 256-residual blocks any head can need
+  int dsk_lds;               // decode keeps the anchor-score table in LDS
 };
+
+// Per-slot arrays (records, position ids) give every head a stride of
+// ceil(S/64)*64 entries, so a head starts on a 64-slot (mask word) boundary
+// and records can be read with 16-byte vector loads.
+__device__ __host__ inline size_t slot_base(const Geo& g, int b, int h) {
+  return ((size_t)g.prefW[b] * g.H + (size_t)h * ((g.S[b] + 63) / 64)) * 64;
+}
 
 constexpr int OBS_CHUNK = 2048;   // tokens per observation-pass workgroup
 constexpr int SORT_CHUNK = 2048;  // tokens per counting-sort chunk
@@ -105,7 +115,7 @@ struct Ws {
 
 struct DecWs {
   float* SK;            // [b][h][g][k_b] anchor scores q_j . abar^K_a
-  float* qrot;          // [b][Hq][D] FWHT(s * q)
+  float* RK;            // [sum N_K][g] key-residual logit terms q_rot . zhat / D
   float* part;          // [b][Hq][split][2 + 2D] partial (max, sum, y[D], zacc[D])
 };
 
@@ -249,6 +259,28 @@ __device__ inline int locate(const Geo& g, int tile, int mult, int& idx) {
     idx -= n;
   }
   return -1;
+}
+
+// Unnormalized Walsh-Hadamard transform of 128 values held by one wave, two
+// per lane (coordinates 2l and 2l+1), Sylvester stage order h = 1, 2, ..., 64:
+// in stage h the pair (i, i+h) with i & h == 0 becomes (z_i + z_{i+h},
+// z_i - z_{i+h}).
+__device__ inline void fwht_wave(float& z0, float& z1, int lane) {
+  {
+    const float a = z0, bb = z1;
+    z0 = a + bb;
+    z1 = a - bb;
+  }
+  for (int hh = 1; hh < 64; hh <<= 1) {
+    const float o0 = __shfl_xor(z0, hh, 64), o1 = __shfl_xor(z1, hh, 64);
+    if (lane & hh) {
+      z0 = o0 - z0;
+      z1 = o1 - z1;
+    } else {
+      z0 = z0 + o0;
+      z1 = z1 + o1;
+    }
+  }
 }
 
 // Kernel timing hook (anchorkv_profile_*): records a HIP event on `st` before

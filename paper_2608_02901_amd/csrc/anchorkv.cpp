@@ -5,6 +5,7 @@
 #include <math.h>
 #include <string.h>
 
+#include <algorithm>
 #include <atomic>
 #include <mutex>
 #include <new>
@@ -29,6 +30,7 @@ hipError_t launch_decode(const Geo& g, const Cache& c, const DecWs& dw, const vo
 hipError_t launch_append(const Geo& g, const Cache& c, int n_app, const void* kn, const void* vn, hipStream_t st);
 hipError_t launch_reconstruct(const Geo& g, const Cache& c, int b, int side, int n_app, float* out,
                               hipStream_t st);
+size_t decode_stream_lds(const Geo& g, int L, bool sk_in_lds);
 }  // namespace akv
 
 using akv::Geo;
@@ -36,7 +38,6 @@ using akv::Geo;
 static const uint32_t kMagic = 0x314B5641u;  // "AVK1" little endian
 static const uint32_t kVersion = 1;
 static const int kBudgetChunk = 4096;
-static const int kDecodeSplit = 2048;
 
 static thread_local std::string g_last_error;
 
@@ -70,7 +71,7 @@ struct anchorkv_plan {
       w_fix, w_fixcount, w_gpos, w_u, w_sel, w_bhist, w_bstate, w_tiecnt, w_shist, w_wcnt;
   size_t ws_bytes;
   // decode workspace offsets
-  size_t d_SK, d_qrot, d_part;
+  size_t d_SK, d_RK, d_part;
   size_t dws_bytes;
 };
 
@@ -111,6 +112,7 @@ extern "C" anchorkv_status anchorkv_plan_create(const anchorkv_config* cfg, int3
   if (c.dtype != ANCHORKV_F32 && c.dtype != ANCHORKV_BF16) return fail(ANCHORKV_ERR_INVALID_ARG, "bad dtype");
   const int G = c.quant_group ? c.quant_group : c.head_dim;
   if (G < 4 || G % 4 || c.head_dim % G) return fail(ANCHORKV_ERR_INVALID_ARG, "quant_group must divide head_dim and be a multiple of 4");
+  if (G < 32) return fail(ANCHORKV_ERR_UNSUPPORTED, "this build supports quant_group 32, 64 or 128");
   if (c.scale_mode < 0 || c.scale_mode > 2) return fail(ANCHORKV_ERR_INVALID_ARG, "bad scale_mode");
   if (c.budget_mode < 0 || c.budget_mode > 2) return fail(ANCHORKV_ERR_INVALID_ARG, "bad budget_mode");
   if (!(c.budget >= 0.0f) || (c.budget_mode != ANCHORKV_BUDGET_COUNT && c.budget > 1.0f))
@@ -143,7 +145,6 @@ extern "C" anchorkv_status anchorkv_plan_create(const anchorkv_config* cfg, int3
   geo.max_append = c.max_append;
   geo.seed_anchor = mix64(c.seed ^ 1ull);
   geo.seed_sign = mix64(c.seed ^ 2ull);
-  geo.dsplit = kDecodeSplit;
   int64_t totS = 0;
   for (int b = 0; b < batch; ++b) {
     const int S = seq_lens[b];
@@ -213,9 +214,33 @@ extern "C" anchorkv_status anchorkv_plan_create(const anchorkv_config* cfg, int3
     geo.prefC[b + 1] = geo.prefC[b] + (S + akv::OBS_CHUNK - 1) / akv::OBS_CHUNK;
     geo.prefKT[b + 1] = geo.prefKT[b] + H * k * ((S + akv::SORT_CHUNK - 1) / akv::SORT_CHUNK);
     geo.prefBC[b + 1] = geo.prefBC[b] + (H * S + kBudgetChunk - 1) / kBudgetChunk;
-    geo.prefSp[b + 1] = geo.prefSp[b] + (S + kDecodeSplit - 1) / kDecodeSplit;
+    geo.prefKp[b + 1] = geo.prefKp[b] + ((k + 3) & ~3);
     geo.prefNK[b + 1] = geo.prefNK[b] + (int)p->req[b].residuals_k;
     geo.prefNV[b + 1] = geo.prefNV[b] + (int)p->req[b].residuals_v;
+  }
+  // Decode split: 2048 sorted slots per workgroup when that still gives at
+  // least 256 workgroups (one per CU), else 1024.  The anchor-score table
+  // stays in LDS up to 64 KB per workgroup, else it is read from L2.
+  {
+    int Lsel = 1024;
+    for (int Lc : {2048, 1024}) {
+      int64_t n = 0;
+      for (int b = 0; b < batch; ++b) n += (int64_t)H * ((geo.S[b] + Lc - 1) / Lc);
+      if (n >= 256) {
+        Lsel = Lc;
+        break;
+      }
+    }
+    const size_t budget = 64 * 1024;
+    geo.dsplit = Lsel;
+    int64_t mr = 0;
+    for (int b = 0; b < batch; ++b) {
+      const int64_t nh = std::min<int64_t>(p->req[b].residuals_k, (int64_t)geo.S[b] - geo.k[b]);
+      mr = std::max<int64_t>(mr, (nh + 255) / 256);
+    }
+    geo.maxRB = (int)mr;
+    geo.dsk_lds = akv::decode_stream_lds(geo, Lsel, true) <= budget ? 1 : 0;
+    for (int b = 0; b < batch; ++b) geo.prefSp[b + 1] = geo.prefSp[b] + (geo.S[b] + Lsel - 1) / Lsel;
   }
   const size_t TS = (size_t)geo.prefS[batch] * H, TK = (size_t)geo.prefK[batch] * H,
                TW = (size_t)geo.prefW[batch] * H, TC = (size_t)geo.prefC[batch] * H;
@@ -230,11 +255,12 @@ extern "C" anchorkv_status anchorkv_plan_create(const anchorkv_config* cfg, int3
   p->c_nrmV = L.add(8 * TK);
   p->c_invK = L.add(4 * TK);
   p->c_invV = L.add(4 * TK);
-  p->c_idxK = L.add(2 * TS);
-  p->c_idxV = L.add(2 * TS);
-  p->c_gK = L.add(esz * TS);
-  p->c_gV = L.add(esz * TS);
-  p->c_pos = L.add(4 * TS);
+  const size_t TSP = TW * 64;  // per-slot arrays: each head padded to whole mask words
+  p->c_idxK = L.add(2 * TSP);
+  p->c_idxV = L.add(2 * TSP);
+  p->c_gK = L.add(esz * TSP);
+  p->c_gV = L.add(esz * TSP);
+  p->c_pos = L.add(4 * TSP);
   p->c_maskK = L.add(8 * TW);
   p->c_maskV = L.add(8 * TW);
   p->c_pcK = L.add(4 * TW);
@@ -278,8 +304,8 @@ extern "C" anchorkv_status anchorkv_plan_create(const anchorkv_config* cfg, int3
   p->ws_bytes = Wl.total;
 
   Layout Dl;
-  p->d_SK = Dl.add(4 * TK * g);
-  p->d_qrot = Dl.add(4 * (size_t)batch * geo.Hq * D);
+  p->d_SK = Dl.add(4 * (size_t)geo.prefKp[batch] * H * g);
+  p->d_RK = Dl.add(4 * (size_t)geo.prefNK[batch] * g);
   p->d_part = Dl.add(4 * (size_t)geo.prefSp[batch] * geo.Hq * (2 + 2 * D));
   p->dws_bytes = Dl.total;
   *out = p;
@@ -366,7 +392,7 @@ static akv::Ws ws_ptrs(const anchorkv_plan* p, void* base) {
 static akv::DecWs dws_ptrs(const anchorkv_plan* p, void* base) {
   akv::DecWs d;
   d.SK = at<float>(base, p->d_SK);
-  d.qrot = at<float>(base, p->d_qrot);
+  d.RK = at<float>(base, p->d_RK);
   d.part = at<float>(base, p->d_part);
   return d;
 }
@@ -454,7 +480,7 @@ extern "C" anchorkv_status anchorkv_export(const anchorkv_plan* p, const void* c
   if (c.header[2] & 1u) return fail(ANCHORKV_ERR_CORRUPT_CACHE, "invalid anchor override");
   if (c.header[2] & 2u) return fail(ANCHORKV_ERR_CORRUPT_CACHE, "anchor selection count mismatch");
   const int H = g.H, S = g.S[b], k = g.k[b], D = g.D, G = g.G, nw = (S + 63) / 64;
-  const size_t ko = (size_t)g.prefK[b] * H, po = (size_t)g.prefS[b] * H, wo = (size_t)g.prefW[b] * H;
+  const size_t ko = (size_t)g.prefK[b] * H, wo = (size_t)g.prefW[b] * H;
   if (o->anchors) memcpy(o->anchors, c.anc_pos + ko, sizeof(int32_t) * H * k);
   for (int side = 0; side < 2; ++side) {
     int32_t* a_out = side ? o->a_v : o->a_k;
@@ -473,7 +499,7 @@ extern "C" anchorkv_status anchorkv_export(const anchorkv_plan* p, const void* c
     if (sc_out) memset(sc_out, 0, sizeof(float) * (size_t)H * S * (D / G));
     for (int h = 0; h < H; ++h)
       for (int i = 0; i < S; ++i) {
-        const size_t e = po + (size_t)h * S + i;
+        const size_t e = akv::slot_base(g, b, h) + i;
         const int t = c.pos[e];
         if (t < 0 || t >= S) return fail(ANCHORKV_ERR_CORRUPT_CACHE, "position id out of range");
         const size_t te = (size_t)h * S + t;

@@ -11,13 +11,17 @@
 // value residuals is applied once per query instead of once per token, and
 // the key residual term is a dot product in the rotated basis.
 //
-//   k_dec_scores : anchor scores S_K[j][a] = q_j . abar^K_a for every query of
-//                  the group, once per step, and the rotated queries;
-//   k_dec_stream : split-K pass over the value-anchor-grouped records (8 per
-//                  lane, coalesced), S_K gathered from LDS, online softmax
-//                  partials (max, sum, per-anchor value weights turned into
-//                  sum_a w_a abar^V_a over the split's anchor range, rotated
-//                  value residual sum);
+//   k_dec_scores : everything that depends only on the queries, fully parallel:
+//                  the anchor scores S_K[j][a] = q_j . abar^K_a (one thread per
+//                  anchor, the row in registers) and the key-residual terms
+//                  q_rot . zhat^K_t / D (one thread per stored key residual);
+//   k_dec_stream : split-K pass over the value-anchor-grouped records.  Loads
+//                  are issued in two rounds (records, flags, the score table;
+//                  then key-residual terms, value-anchor rows and value
+//                  residual codes); per split it writes the partial (max, sum,
+//                  sum_a w_a abar^V_a, rotated value-residual sum).  Blocks are
+//                  mapped so that all splits of one head share one XCD (and its
+//                  L2) for the score table and the anchor rows;
 //   k_dec_combine: merges the splits, adds appended tokens, applies the
 //                  inverse rotation once and normalizes.
 //   k_append     : encodes one new key/value per head against the existing
@@ -33,335 +37,542 @@ __device__ inline float level(int code) {
   return code < 2 ? -mag : mag;
 }
 
+// sigma * level(code) from the group's four precomputed values.
+__device__ inline float scaled_level(int code, float n1, float n0, float p0, float p1) {
+  const float lo = (code & 1) ? n0 : n1;
+  const float hi = (code & 1) ? p1 : p0;
+  return (code & 2) ? hi : lo;
+}
+
 // ------------------------------------------------------------------ D1
 template <int DT>
 __global__ __launch_bounds__(256) void k_dec_scores(Geo g, Cache c, DecWs dw, const void* qin) {
   using E = typename Elem<DT>::T;
-  __shared__ float qs[8][AKV_D];
-  __shared__ float zb[AKV_D];
+  constexpr int D = AKV_D;
+  constexpr int PER = 16 / sizeof(E);
+  __shared__ float qs[8][D];
+  const int gq = g.g;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   int idx = blockIdx.x;
-  int b = 0;
-  for (; b < g.B; ++b) {
-    const int n = g.H * ((g.k[b] + 63) / 64);
-    if (idx < n) break;
-    idx -= n;
+  int nsc = 0;
+  for (int b = 0; b < g.B; ++b) nsc += g.H * ((g.k[b] + 255) / 256);
+  if (idx < nsc) {
+    // ---- anchor scores
+    int b = 0;
+    for (; b < g.B; ++b) {
+      const int n = g.H * ((g.k[b] + 255) / 256);
+      if (idx < n) break;
+      idx -= n;
+    }
+    const int k = g.k[b], kp = (k + 3) & ~3;
+    const int nch = (k + 255) / 256;
+    const int h = idx / nch, a0 = (idx % nch) * 256;
+    const int a = a0 + threadIdx.x;
+    const size_t ko = (size_t)g.prefK[b] * g.H + (size_t)h * k;
+    const E* row = (const E*)c.ancK + (ko + min(a, k - 1)) * D;
+    uint4 rv[D / PER];
+#pragma unroll
+    for (int i = 0; i < D / PER; ++i) rv[i] = *(const uint4*)(row + i * PER);
+    const E* q = (const E*)qin + ((size_t)b * g.Hq + (size_t)h * gq) * D;
+    for (int i = threadIdx.x; i < gq * D; i += 256) qs[i / D][i % D] = Elem<DT>::get(q, i);
+    __syncthreads();
+    float acc[8];
+#pragma unroll
+    for (int jj = 0; jj < 8; ++jj) acc[jj] = 0.0f;
+#pragma unroll
+    for (int i = 0; i < D / PER; ++i) {
+      const E* e = (const E*)&rv[i];
+#pragma unroll
+      for (int j = 0; j < PER; ++j) {
+        const float x = Elem<DT>::get(e, j);
+#pragma unroll
+        for (int jj = 0; jj < 8; ++jj)
+          if (jj < gq) acc[jj] = fmaf(qs[jj][i * PER + j], x, acc[jj]);
+      }
+    }
+    if (a < k) {
+      float* SK = dw.SK + ((size_t)g.prefKp[b] * g.H + (size_t)h * kp) * gq;
+#pragma unroll
+      for (int jj = 0; jj < 8; ++jj)
+        if (jj < gq) SK[(size_t)jj * kp + a] = acc[jj];
+    }
+    return;
   }
-  const int k = g.k[b], D = AKV_D, gq = g.g;
-  const int nch = (k + 63) / 64;
-  const int h = idx / nch, a0 = (idx % nch) * 64;
-  const E* q = (const E*)qin + ((size_t)b * g.Hq + (size_t)h * gq) * D;
-  for (int i = threadIdx.x; i < gq * D; i += blockDim.x) qs[i / D][i % D] = Elem<DT>::get(q, i);
+  // ---- key-residual terms of one (request, head), 256 residuals per block
+  idx -= nsc;
+  const int rb = idx % g.maxRB, bh = idx / g.maxRB;
+  const int b = bh / g.H, h = bh % g.H;
+  const int S = g.S[b], G = g.G;
+  const int nw = (S + 63) / 64;
+  const size_t wo = (size_t)g.prefW[b] * g.H + (size_t)h * nw;
+  const int e0 = c.pcK[wo];
+  const int e1 = h + 1 < g.H ? c.pcK[wo + nw] : g.prefNK[b + 1];
+  if (e0 + rb * 256 >= e1) return;
+  // Rotated queries q_rot = FWHT(s * q): one wave per query head.
+  for (int jj = wave; jj < gq; jj += 4) {
+    const E* q = (const E*)qin + ((size_t)b * g.Hq + (size_t)h * gq + jj) * D;
+    float z0 = hsign(g.seed_sign, 2 * lane) * Elem<DT>::get(q, 2 * lane);
+    float z1 = hsign(g.seed_sign, 2 * lane + 1) * Elem<DT>::get(q, 2 * lane + 1);
+    fwht_wave(z0, z1, lane);
+    qs[jj][2 * lane] = z0;
+    qs[jj][2 * lane + 1] = z1;
+  }
   __syncthreads();
-  const size_t ko = (size_t)g.prefK[b] * g.H + (size_t)h * k;
-  const E* A = (const E*)c.ancK + ko * D;
-  float* SK = dw.SK + ko * gq;
-  for (int p = threadIdx.x; p < 64 * gq; p += blockDim.x) {
-    const int a = a0 + (p & 63), jj = p >> 6;
-    if (a >= k) continue;
-    const E* row = A + (size_t)a * D;
-    float s = 0.0f;
-    for (int d = 0; d < D; d += 8) {
-      if constexpr (DT == 1) {
-        uint4 v = *(const uint4*)(row + d);
-        const uint16_t* e = (const uint16_t*)&v;
+  const int e = e0 + rb * 256 + threadIdx.x;
+  if (e >= e1) return;
+  const uint4* cp = (const uint4*)(c.codesK + (size_t)e * (D / 4));
+  const uint4 c0 = cp[0], c1 = cp[1];
+  const uint32_t cw[8] = {c0.x, c0.y, c0.z, c0.w, c1.x, c1.y, c1.z, c1.w};
+  float sg[4];
 #pragma unroll
-        for (int i = 0; i < 8; ++i) s = fmaf(qs[jj][d + i], bf2f(e[i]), s);
-      } else {
+  for (int qd = 0; qd < 4; ++qd) sg[qd] = qd < D / G ? c.scalesK[(size_t)e * (D / G) + qd] : 0.0f;
+  float dot[8];
 #pragma unroll
-        for (int i = 0; i < 8; ++i) s = fmaf(qs[jj][d + i], row[d + i], s);
-      }
-    }
-    SK[(size_t)jj * k + a] = s;
-  }
-  // Rotated queries, by the first block of each head.
-  if (a0 == 0) {
-    for (int jj = 0; jj < gq; ++jj) {
-      __syncthreads();
-      if (threadIdx.x < D) zb[threadIdx.x] = hsign(g.seed_sign, threadIdx.x) * qs[jj][threadIdx.x];
-      for (int hh = 1; hh < D; hh <<= 1) {
-        __syncthreads();
-        float v = 0.0f;
-        if (threadIdx.x < D) {
-          const int i = threadIdx.x;
-          const float a = zb[i & ~hh], bb = zb[i | hh];
-          v = (i & hh) ? a - bb : a + bb;
-        }
-        __syncthreads();
-        if (threadIdx.x < D) zb[threadIdx.x] = v;
-      }
-      __syncthreads();
-      if (threadIdx.x < D) dw.qrot[((size_t)b * g.Hq + h * gq + jj) * D + threadIdx.x] = zb[threadIdx.x];
+  for (int jj = 0; jj < 8; ++jj) dot[jj] = 0.0f;
+#pragma unroll
+  for (int qd = 0; qd < 4; ++qd) {  // 32-coordinate quarters lie inside one group (G >= 32)
+    const float s = sg[(qd * 32) / G];
+    const float n1 = -s * AKV_L1, n0 = -s * AKV_L0, p0 = s * AKV_L0, p1 = s * AKV_L1;
+#pragma unroll
+    for (int dd = 0; dd < 32; ++dd) {
+      const int d = qd * 32 + dd;
+      const int code = (cw[d >> 4] >> (2 * (d & 15))) & 3;
+      const float z = scaled_level(code, n1, n0, p0, p1);
+#pragma unroll
+      for (int jj = 0; jj < 8; ++jj)
+        if (jj < gq) dot[jj] = fmaf(qs[jj][d], z, dot[jj]);
     }
   }
+  const float invD = 1.0f / (float)D;
+#pragma unroll
+  for (int jj = 0; jj < 8; ++jj)
+    if (jj < gq) dw.RK[(size_t)e * gq + jj] = dot[jj] * invD;
 }
 
 // ------------------------------------------------------------------ D2
+// R uint16 values starting at p (R * 2 bytes, 8-byte aligned).
+template <int R>
+__device__ inline void load_u16(const uint16_t* p, uint16_t* v) {
+#pragma unroll
+  for (int i = 0; i < R / 4; ++i) {
+    const uint2 x = *(const uint2*)(p + 4 * i);
+    v[4 * i + 0] = (uint16_t)(x.x & 0xffff);
+    v[4 * i + 1] = (uint16_t)(x.x >> 16);
+    v[4 * i + 2] = (uint16_t)(x.y & 0xffff);
+    v[4 * i + 3] = (uint16_t)(x.y >> 16);
+  }
+}
+template <int DT, int R>
+__device__ inline void load_coef(const void* base, size_t i0, float* v) {
+  if constexpr (DT == 1) {
+    uint16_t t[R];
+    load_u16<R>((const uint16_t*)base + i0, t);
+#pragma unroll
+    for (int i = 0; i < R; ++i) v[i] = bf2f(t[i]);
+  } else {
+#pragma unroll
+    for (int i = 0; i < R / 4; ++i) {
+      const float4 x = *(const float4*)((const float*)base + i0 + 4 * i);
+      v[4 * i] = x.x;
+      v[4 * i + 1] = x.y;
+      v[4 * i + 2] = x.z;
+      v[4 * i + 3] = x.w;
+    }
+  }
+}
+__device__ inline unsigned long long low_bits(int n) { return n >= 64 ? ~0ull : ((1ull << n) - 1ull); }
+
+constexpr int DEC_ASTG = 64;   // value-anchor rows staged in LDS per split
+constexpr int DEC_RCW = 512;   // anchor window of the per-anchor value weights
+constexpr int DEC_VCH = 128;   // value residuals staged per chunk
+
 template <int DT, int GQ, int R>
 __global__ __launch_bounds__(256) void k_dec_stream(Geo g, Cache c, DecWs dw, float scale) {
   using E = typename Elem<DT>::T;
-  constexpr int L = 256 * R;
-  constexpr int D = AKV_D;
-  extern __shared__ float lds[];
+  constexpr int D = AKV_D, L = 256 * R, PER = 16 / sizeof(E);
+  constexpr int NAV = DEC_ASTG * D / PER / 256;
+  constexpr int NY = (GQ * D + 255) / 256;  // outputs per thread
+  constexpr int JG = GQ < 4 ? GQ : 4;       // query heads covered by the 4 thread groups
+  extern __shared__ __align__(16) unsigned char smem[];
+  __shared__ float wacc[GQ][DEC_RCW];
+  __shared__ __align__(16) E avs[DEC_ASTG * D];
+  __shared__ __align__(16) uint32_t vcode[DEC_VCH][8];
+  __shared__ float vsc[DEC_VCH][4];
+  __shared__ float vp[DEC_VCH][GQ];
   __shared__ float red[4][GQ];
   __shared__ float mfin[GQ];
-  __shared__ float zred[4][GQ][2 * 64];
-  int idx = blockIdx.x;
-  const int b = locate(g, L, 1, idx);
-  const int S = g.S[b], k = g.k[b], G = g.G;
+
+  // Logical block id: consecutive ids (the splits of one head) share an XCD.
+  int id = blockIdx.x;
+  const int n8 = gridDim.x & ~7;
+  if (id < n8) id = (id & 7) * (n8 >> 3) + (id >> 3);
+  const int b = locate(g, L, 1, id);
+  const int S = g.S[b], k = g.k[b], G = g.G, kp = (k + 3) & ~3;
   const int nsp = (S + L - 1) / L;
-  const int h = idx / nsp, sp = idx % nsp;
+  const int h = id / nsp, sp = id % nsp;
   const int s0 = sp * L, s1 = min(S, s0 + L);
-  const size_t po = (size_t)g.prefS[b] * g.H + (size_t)h * S;
+  const int nw = (S + 63) / 64;
+  const size_t so = slot_base(g, b, h);
+  const size_t wo = (size_t)g.prefW[b] * g.H + (size_t)h * nw;
   const size_t ko = (size_t)g.prefK[b] * g.H + (size_t)h * k;
-  const int range_cap = min(g.maxK, L);
-  float* SKs = lds;                      // [GQ][k]
-  float* wacc = lds + GQ * g.maxK;       // [GQ][range_cap]
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int kpm = (g.maxK + 3) & ~3;
+  float* SKs = (float*)smem;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const float* SKg = dw.SK + ((size_t)g.prefKp[b] * g.H + (size_t)h * kp) * GQ;
+  const E* AVg = (const E*)c.ancV + ko * D;
 
-  // Anchor scores of this head's queries.
-  const float* SK = dw.SK + ko * GQ;
-  for (int i = threadIdx.x; i < GQ * k; i += 256) SKs[(i / k) * g.maxK + (i % k)] = SK[i];
-  const int a_lo = c.idxV[po + s0], a_hi = c.idxV[po + s1 - 1];
-  const int nrange = a_hi - a_lo + 1;
-  for (int i = threadIdx.x; i < GQ * range_cap; i += 256) wacc[i] = 0.0f;
-  // Rotated query coordinates of this lane (2l, 2l+1).
-  float qr0[GQ], qr1[GQ];
-#pragma unroll
-  for (int jj = 0; jj < GQ; ++jj) {
-    const float* qr = dw.qrot + ((size_t)b * g.Hq + h * GQ + jj) * D;
-    qr0[jj] = qr[2 * lane];
-    qr1[jj] = qr[2 * lane + 1];
-  }
-
-  // Records of this lane's R consecutive slots.
-  const int i0 = s0 + (wave * 64 + lane) * R;
+  // ---- round 1: records, flag words, the split's residual ranges, the score table.
+  const int i0 = s0 + tid * R;
+  const bool any = i0 < s1;
   uint16_t ik[R], iv[R];
   float gk[R], gv[R];
-  uint32_t bk = 0, bv = 0;  // residual flag bits of the R slots
-#pragma unroll
-  for (int r = 0; r < R; ++r) {
-    const int i = i0 + r;
-    const bool ok = i < s1;
-    ik[r] = ok ? c.idxK[po + i] : 0;
-    iv[r] = ok ? c.idxV[po + i] : (uint16_t)a_lo;
-    gk[r] = ok ? Elem<DT>::get(c.gK, po + i) : 0.0f;
-    gv[r] = ok ? Elem<DT>::get(c.gV, po + i) : 0.0f;
-  }
-  const size_t wo0 = (size_t)g.prefW[b] * g.H + (size_t)h * ((S + 63) / 64);
   unsigned long long wk = 0, wv = 0;
   int pck = 0, pcv = 0;
-  if (i0 < s1) {
-    const int word = i0 >> 6;
-    wk = c.maskK[wo0 + word];
-    wv = c.maskV[wo0 + word];
-    pck = c.pcK[wo0 + word];
-    pcv = c.pcV[wo0 + word];
-    const int sh = i0 & 63;
-    const unsigned long long lowm = (1ull << sh) - 1ull;
-    pck += __popcll(wk & lowm);
-    pcv += __popcll(wv & lowm);
-    const uint32_t rm = (R >= 32) ? 0xffffffffu : ((1u << R) - 1u);
-    bk = (uint32_t)(wk >> sh) & rm;
-    bv = (uint32_t)(wv >> sh) & rm;
-    const int valid = s1 - i0;
-    if (valid < R) {
-      bk &= (1u << valid) - 1u;
-      bv &= (1u << valid) - 1u;
+  if (any) {
+    load_u16<R>(c.idxK + so + i0, ik);
+    load_u16<R>(c.idxV + so + i0, iv);
+    load_coef<DT, R>(c.gK, so + i0, gk);
+    load_coef<DT, R>(c.gV, so + i0, gv);
+    wk = c.maskK[wo + (i0 >> 6)];
+    wv = c.maskV[wo + (i0 >> 6)];
+    pck = c.pcK[wo + (i0 >> 6)];
+    pcv = c.pcV[wo + (i0 >> 6)];
+  } else {
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      ik[r] = 0;
+      iv[r] = 0;
+      gk[r] = 0.0f;
+      gv[r] = 0.0f;
     }
+  }
+  const int a_lo = c.idxV[so + s0], a_hi = c.idxV[so + s1 - 1];
+  const int pv_lo = c.pcV[wo + (s0 >> 6)];
+  const int w1 = (s1 - 1) >> 6;
+  const int pv_hi = c.pcV[wo + w1] + __popcll(c.maskV[wo + w1] & low_bits(s1 - 64 * w1));
+  if (g.dsk_lds) {
+    const int n4 = GQ * kp / 4;
+    for (int i = tid; i < n4; i += 4 * 256) {
+      float4 t[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        if (i + u * 256 < n4) t[u] = *(const float4*)(SKg + 4 * (size_t)(i + u * 256));
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        if (i + u * 256 < n4) {
+          const int f = 4 * (i + u * 256);
+          *(float4*)(&SKs[(f / kp) * kpm + (f % kp)]) = t[u];
+        }
+    }
+  }
+  const int nrange = a_hi - a_lo + 1;
+  const int nstage = min(nrange, DEC_ASTG);
+  const int nvres = pv_hi - pv_lo;
+
+  // ---- round 2: key-residual terms, value-anchor rows, first value-residual chunk.
+  const int sh = i0 & 63;
+  uint32_t vmask = 0;
+#pragma unroll
+  for (int r = 0; r < R; ++r)
+    if (i0 + r < s1) vmask |= 1u << r;
+  const uint32_t bk = any ? ((uint32_t)(wk >> sh) & vmask) : 0u;
+  const uint32_t bv = any ? ((uint32_t)(wv >> sh) & vmask) : 0u;
+  pck += __popcll(wk & low_bits(sh));
+  pcv += __popcll(wv & low_bits(sh));
+  float rk[R][GQ];
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const int ri = pck + __popc(bk & ((1u << r) - 1u));
+#pragma unroll
+    for (int jj = 0; jj < GQ; ++jj) rk[r][jj] = ((bk >> r) & 1u) ? dw.RK[(size_t)ri * GQ + jj] : 0.0f;
+  }
+  uint4 avr[NAV];
+#pragma unroll
+  for (int i = 0; i < NAV; ++i) {
+    const int ch = tid + 256 * i;
+    const int r = ch / (D / PER), col = (ch % (D / PER)) * PER;
+    avr[i] = r < nstage ? *(const uint4*)(AVg + (size_t)(a_lo + r) * D + col) : make_uint4(0, 0, 0, 0);
+  }
+  const int nv0 = min(nvres, DEC_VCH);
+  uint4 vcr = make_uint4(0, 0, 0, 0);
+  if (tid < 2 * nv0) vcr = ((const uint4*)(c.codesV + (size_t)(pv_lo + (tid >> 1)) * (D / 4)))[tid & 1];
+  float vsr[2];
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    const int f = tid + 256 * u;
+    vsr[u] = f < nv0 * (D / G) ? c.scalesV[(size_t)pv_lo * (D / G) + f] : 0.0f;
   }
   __syncthreads();
 
+  // ---- logits.
   float lg[R][GQ];
 #pragma unroll
-  for (int r = 0; r < R; ++r)
+  for (int r = 0; r < R; ++r) {
+    const int a = min((int)ik[r], k - 1);
 #pragma unroll
-    for (int jj = 0; jj < GQ; ++jj) lg[r][jj] = gk[r] * SKs[jj * g.maxK + min((int)ik[r], k - 1)];
-
-  // Key residuals: the wave takes each flagged slot in turn.
-  const float invD = 1.0f / (float)D;
-  const int grp = (2 * lane) / G;
-  {
-    uint32_t my = bk;
-    int myslot = pck;
-    for (int r = 0; r < R; ++r) {
-      unsigned long long bal = __ballot((my >> r) & 1u);
-      while (bal) {
-        const int src = __ffsll((long long)bal) - 1;
-        bal &= bal - 1;
-        const int slot = __shfl(myslot + __popc(my & ((1u << r) - 1u)), src, 64);
-        const uint8_t byte = c.codesK[(size_t)slot * (D / 4) + lane / 2];
-        const int nib = (lane & 1) ? (byte >> 4) : (byte & 15);
-        const float sg = c.scalesK[(size_t)slot * (D / G) + grp];
-        const float z0 = sg * level(nib & 3), z1 = sg * level(nib >> 2);
-#pragma unroll
-        for (int jj = 0; jj < GQ; ++jj) {
-          const float part = wave_sum(fmaf(qr0[jj], z0, qr1[jj] * z1));
-          if (lane == src) lg[r][jj] += part * invD;
-        }
-      }
+    for (int jj = 0; jj < GQ; ++jj) {
+      const float s = g.dsk_lds ? SKs[jj * kpm + a] : SKg[(size_t)jj * kp + a];
+      lg[r][jj] = (gk[r] * s + rk[r][jj]) * scale;
     }
   }
-  // Softmax statistics of the split.
-  float mx[GQ];
+  // ---- softmax statistics of the split.
 #pragma unroll
   for (int jj = 0; jj < GQ; ++jj) {
     float v = -INFINITY;
 #pragma unroll
-    for (int r = 0; r < R; ++r) {
-      lg[r][jj] *= scale;
-      if (i0 + r < s1) v = fmaxf(v, lg[r][jj]);
-    }
+    for (int r = 0; r < R; ++r)
+      if ((vmask >> r) & 1u) v = fmaxf(v, lg[r][jj]);
     v = wave_max(v);
     if (lane == 0) red[wave][jj] = v;
   }
   __syncthreads();
-  if (threadIdx.x < GQ)
-    mfin[threadIdx.x] = fmaxf(fmaxf(red[0][threadIdx.x], red[1][threadIdx.x]), fmaxf(red[2][threadIdx.x], red[3][threadIdx.x]));
+  if (tid < GQ) mfin[tid] = fmaxf(fmaxf(red[0][tid], red[1][tid]), fmaxf(red[2][tid], red[3][tid]));
   __syncthreads();
-#pragma unroll
-  for (int jj = 0; jj < GQ; ++jj) mx[jj] = mfin[jj];
   float ls[GQ];
 #pragma unroll
-  for (int jj = 0; jj < GQ; ++jj) ls[jj] = 0.0f;
+  for (int jj = 0; jj < GQ; ++jj) {
+    const float m = mfin[jj];
+    ls[jj] = 0.0f;
 #pragma unroll
-  for (int r = 0; r < R; ++r)
-#pragma unroll
-    for (int jj = 0; jj < GQ; ++jj) {
-      const float p = (i0 + r < s1) ? __expf(lg[r][jj] - mx[jj]) : 0.0f;
+    for (int r = 0; r < R; ++r) {
+      const float p = ((vmask >> r) & 1u) ? __expf(lg[r][jj] - m) : 0.0f;
       lg[r][jj] = p;
       ls[jj] += p;
-    }
-  // Per-anchor value weights: runs of equal value anchors accumulate in
-  // registers and are flushed to LDS when the anchor changes.
-  {
-    int cur = iv[0];
-    float run[GQ];
-#pragma unroll
-    for (int jj = 0; jj < GQ; ++jj) run[jj] = 0.0f;
-#pragma unroll
-    for (int r = 0; r < R; ++r) {
-      if (iv[r] != cur) {
-#pragma unroll
-        for (int jj = 0; jj < GQ; ++jj) {
-          if (run[jj] != 0.0f) atomicAdd(&wacc[jj * range_cap + (cur - a_lo)], run[jj]);
-          run[jj] = 0.0f;
-        }
-        cur = iv[r];
-      }
-#pragma unroll
-      for (int jj = 0; jj < GQ; ++jj) run[jj] = fmaf(lg[r][jj], gv[r], run[jj]);
-    }
-#pragma unroll
-    for (int jj = 0; jj < GQ; ++jj)
-      if (run[jj] != 0.0f) atomicAdd(&wacc[jj * range_cap + (cur - a_lo)], run[jj]);
-  }
-  // Value residuals: rotated-domain accumulation, two coordinates per lane.
-  float za0[GQ], za1[GQ];
-#pragma unroll
-  for (int jj = 0; jj < GQ; ++jj) { za0[jj] = 0.0f; za1[jj] = 0.0f; }
-  {
-    uint32_t my = bv;
-    int myslot = pcv;
-    for (int r = 0; r < R; ++r) {
-      unsigned long long bal = __ballot((my >> r) & 1u);
-      while (bal) {
-        const int src = __ffsll((long long)bal) - 1;
-        bal &= bal - 1;
-        const int slot = __shfl(myslot + __popc(my & ((1u << r) - 1u)), src, 64);
-        const uint8_t byte = c.codesV[(size_t)slot * (D / 4) + lane / 2];
-        const int nib = (lane & 1) ? (byte >> 4) : (byte & 15);
-        const float sg = c.scalesV[(size_t)slot * (D / G) + grp];
-        const float z0 = sg * level(nib & 3), z1 = sg * level(nib >> 2);
-#pragma unroll
-        for (int jj = 0; jj < GQ; ++jj) {
-          const float p = __shfl(lg[r][jj], src, 64);
-          za0[jj] = fmaf(p, z0, za0[jj]);
-          za1[jj] = fmaf(p, z1, za1[jj]);
-        }
-      }
     }
   }
 #pragma unroll
   for (int jj = 0; jj < GQ; ++jj) {
     const float v = wave_sum(ls[jj]);
-    zred[wave][jj][2 * lane] = za0[jj];
-    zred[wave][jj][2 * lane + 1] = za1[jj];
     if (lane == 0) red[wave][jj] = v;
   }
-  __syncthreads();
-  // Outputs: thread (jj, d) pairs.
-  float* part = dw.part;
-  const int Hq = g.Hq;
-  for (int p = threadIdx.x; p < GQ * D; p += 256) {
-    const int jj = p / D, d = p % D;
-    const E* AV = (const E*)c.ancV + (ko + a_lo) * D + d;
-    float y = 0.0f;
-    for (int a = 0; a < nrange; ++a) y = fmaf(wacc[jj * range_cap + a], Elem<DT>::get(AV, (size_t)a * D), y);
-    const float z = zred[0][jj][d] + zred[1][jj][d] + zred[2][jj][d] + zred[3][jj][d];
-    const int jq = h * GQ + jj;
-    const size_t pi = ((size_t)(g.prefSp[b] * Hq + jq * nsp + sp)) * (2 + 2 * D);
-    if (d == 0) {
-      part[pi] = mx[jj];
-      part[pi + 1] = red[0][jj] + red[1][jj] + red[2][jj] + red[3][jj];
+  // Stage the value-anchor rows and the first value-residual chunk.
+#pragma unroll
+  for (int i = 0; i < NAV; ++i) {
+    const int ch = tid + 256 * i;
+    const int r = ch / (D / PER), col = (ch % (D / PER)) * PER;
+    *(uint4*)(&avs[r * D + col]) = avr[i];
+  }
+  if (tid < 2 * nv0) *(uint4*)(&vcode[tid >> 1][4 * (tid & 1)]) = vcr;
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    const int f = tid + 256 * u;
+    if (f < nv0 * (D / G)) vsc[f / (D / G)][f % (D / G)] = vsr[u];
+  }
+
+  // ---- value residuals: thread (coordinate pair, query head) accumulates over
+  // the split's stored value residuals, staged DEC_VCH at a time.
+  const int pair = tid & 63, jg = tid >> 6;
+  const int grp = (2 * pair) / G;
+  float za[2][2] = {{0.0f, 0.0f}, {0.0f, 0.0f}};
+  for (int cb = 0; cb < nvres; cb += DEC_VCH) {
+    const int nv = min(DEC_VCH, nvres - cb);
+    if (cb > 0) {
+      __syncthreads();
+      if (tid < 2 * nv) *(uint4*)(&vcode[tid >> 1][4 * (tid & 1)]) =
+          ((const uint4*)(c.codesV + (size_t)(pv_lo + cb + (tid >> 1)) * (D / 4)))[tid & 1];
+      for (int f = tid; f < nv * (D / G); f += 256)
+        vsc[f / (D / G)][f % (D / G)] = c.scalesV[(size_t)(pv_lo + cb) * (D / G) + f];
     }
-    part[pi + 2 + d] = y;
-    part[pi + 2 + D + d] = z;
+    // probabilities of this chunk's residual slots, written by their owners
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+      if ((bv >> r) & 1u) {
+        const int li = pcv + __popc(bv & ((1u << r) - 1u)) - pv_lo - cb;
+        if (li >= 0 && li < nv) {
+#pragma unroll
+          for (int jj = 0; jj < GQ; ++jj) vp[li][jj] = lg[r][jj];
+        }
+      }
+    __syncthreads();
+    if (jg < JG) {
+      for (int e = 0; e < nv; ++e) {
+        const uint32_t word = vcode[e][pair >> 3];
+        const int nib = (word >> (4 * (pair & 7))) & 15;
+        const float sg = vsc[e][grp];
+        const float z0 = sg * level(nib & 3), z1 = sg * level(nib >> 2);
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+          const int jj = jg + 4 * u;
+          if (jj < GQ) {
+            const float p = vp[e][jj];
+            za[u][0] = fmaf(p, z0, za[u][0]);
+            za[u][1] = fmaf(p, z1, za[u][1]);
+          }
+        }
+      }
+    }
+  }
+
+  // ---- per-anchor value weights over anchor windows, and y = sum_a w_a abar^V_a.
+  float y[NY];
+#pragma unroll
+  for (int u = 0; u < NY; ++u) y[u] = 0.0f;
+  for (int wb = 0; wb < nrange; wb += DEC_RCW) {
+    const int wn = min(DEC_RCW, nrange - wb);
+    __syncthreads();
+    for (int i = tid; i < GQ * DEC_RCW; i += 256) (&wacc[0][0])[i] = 0.0f;
+    __syncthreads();
+    {
+      int cur = -1;
+      float run[GQ];
+#pragma unroll
+      for (int jj = 0; jj < GQ; ++jj) run[jj] = 0.0f;
+#pragma unroll
+      for (int r = 0; r < R; ++r) {
+        const int off = (int)iv[r] - a_lo - wb;
+        const bool in = ((vmask >> r) & 1u) && off >= 0 && off < wn;
+        if (in && off != cur) {
+          if (cur >= 0) {
+#pragma unroll
+            for (int jj = 0; jj < GQ; ++jj)
+              if (run[jj] != 0.0f) atomicAdd(&wacc[jj][cur], run[jj]);
+          }
+#pragma unroll
+          for (int jj = 0; jj < GQ; ++jj) run[jj] = 0.0f;
+          cur = off;
+        }
+        if (in) {
+#pragma unroll
+          for (int jj = 0; jj < GQ; ++jj) run[jj] = fmaf(lg[r][jj], gv[r], run[jj]);
+        }
+      }
+      if (cur >= 0) {
+#pragma unroll
+        for (int jj = 0; jj < GQ; ++jj)
+          if (run[jj] != 0.0f) atomicAdd(&wacc[jj][cur], run[jj]);
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < NY; ++u) {
+      const int p = tid + 256 * u;
+      if (p < GQ * D) {
+        const int jj = p / D, d = p % D;
+        float acc = y[u];
+        for (int a = 0; a < wn; ++a) {
+          const int ra = wb + a;
+          const float av = ra < nstage ? Elem<DT>::get(avs, (size_t)ra * D + d)
+                                       : Elem<DT>::get(AVg, (size_t)(a_lo + ra) * D + d);
+          acc = fmaf(wacc[jj][a], av, acc);
+        }
+        y[u] = acc;
+      }
+    }
+  }
+
+  // ---- partial outputs.
+  const int Hq = g.Hq;
+#pragma unroll
+  for (int u = 0; u < NY; ++u) {
+    const int p = tid + 256 * u;
+    if (p < GQ * D) {
+      const int jj = p / D, d = p % D;
+      const size_t pi = ((size_t)(g.prefSp[b] * Hq + (h * GQ + jj) * nsp + sp)) * (2 + 2 * D);
+      if (d == 0) {
+        dw.part[pi] = mfin[jj];
+        dw.part[pi + 1] = red[0][jj] + red[1][jj] + red[2][jj] + red[3][jj];
+      }
+      dw.part[pi + 2 + d] = y[u];
+    }
+  }
+  if (jg < JG) {
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int jj = jg + 4 * u;
+      if (jj < GQ) {
+        const size_t pi = ((size_t)(g.prefSp[b] * Hq + (h * GQ + jj) * nsp + sp)) * (2 + 2 * D);
+        dw.part[pi + 2 + D + 2 * pair] = za[u][0];
+        dw.part[pi + 2 + D + 2 * pair + 1] = za[u][1];
+      }
+    }
   }
 }
 
 // ------------------------------------------------------------------ D3
 template <int DT>
-__global__ __launch_bounds__(128) void k_dec_combine(Geo g, Cache c, DecWs dw, float scale, int L, int n_app,
-                                                     void* out, int out_dtype) {
+__global__ __launch_bounds__(256) void k_dec_combine(Geo g, Cache c, DecWs dw, float scale, int n_app, void* out,
+                                                     int out_dtype) {
   using E = typename Elem<DT>::T;
   constexpr int D = AKV_D;
   __shared__ float zb[D];
+  __shared__ float yb[D];
+  __shared__ float rmax[4], rsum[4];
   const int b = blockIdx.x / g.Hq, jq = blockIdx.x % g.Hq;
   const int h = jq / g.g, jj = jq % g.g;
-  const int S = g.S[b], k = g.k[b];
+  const int S = g.S[b], k = g.k[b], kp = (k + 3) & ~3;
+  const int L = g.dsplit;
   const int nsp = (S + L - 1) / L;
   const size_t ko = (size_t)g.prefK[b] * g.H + (size_t)h * k;
-  const int d = threadIdx.x;
   const size_t pb = (size_t)(g.prefSp[b] * g.Hq + jq * nsp) * (2 + 2 * D);
-  float M = -INFINITY;
-  for (int s = 0; s < nsp; ++s) M = fmaxf(M, dw.part[pb + (size_t)s * (2 + 2 * D)]);
-  // Appended tokens (encoded against the anchors, no residual).
+  const float* part = dw.part + pb;
   const size_t tb = ((size_t)b * g.H + h) * g.max_append;
-  const float* SK = dw.SK + ko * g.g + (size_t)jj * k;
-  for (int n = 0; n < n_app; ++n) {
-    const float l = scale * (Elem<DT>::get(c.tgK, tb + n) * SK[min((int)c.tidxK[tb + n], k - 1)]);
-    M = fmaxf(M, l);
+  const float* SK = dw.SK + ((size_t)g.prefKp[b] * g.H + (size_t)h * kp) * g.g + (size_t)jj * kp;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // Global max over the splits and the appended tokens.
+  float M = -INFINITY;
+  for (int s = tid; s < nsp; s += 256) M = fmaxf(M, part[(size_t)s * (2 + 2 * D)]);
+  for (int n = tid; n < n_app; n += 256)
+    M = fmaxf(M, scale * (Elem<DT>::get(c.tgK, tb + n) * SK[min((int)c.tidxK[tb + n], k - 1)]));
+  M = wave_max(M);
+  if (lane == 0) rmax[wave] = M;
+  __syncthreads();
+  M = fmaxf(fmaxf(rmax[0], rmax[1]), fmaxf(rmax[2], rmax[3]));
+  float l = 0.0f;
+  for (int s = tid; s < nsp; s += 256) {
+    const float* pp = part + (size_t)s * (2 + 2 * D);
+    l += __expf(pp[0] - M) * pp[1];
   }
-  float l = 0.0f, y = 0.0f, z = 0.0f;
-  for (int s = 0; s < nsp; ++s) {
-    const float* pp = dw.part + pb + (size_t)s * (2 + 2 * D);
-    const float f = __expf(pp[0] - M);
-    l += f * pp[1];
-    y += f * pp[2 + d];
-    z += f * pp[2 + D + d];
+  // Each thread owns one output: y[d] (threads 0..127) or zacc[d] (128..255).
+  float acc = 0.0f;
+  int s = 0;
+  for (; s + 8 <= nsp; s += 8) {
+    float mv[8], vv[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const float* pp = part + (size_t)(s + u) * (2 + 2 * D);
+      mv[u] = pp[0];
+      vv[u] = pp[2 + tid];
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) acc = fmaf(__expf(mv[u] - M), vv[u], acc);
   }
+  for (; s < nsp; ++s) {
+    const float* pp = part + (size_t)s * (2 + 2 * D);
+    acc = fmaf(__expf(pp[0] - M), pp[2 + tid], acc);
+  }
+  // Appended tokens: encoded against the anchors, no residual.
   const E* AV = (const E*)c.ancV + ko * D;
   for (int n = 0; n < n_app; ++n) {
-    const float lg = scale * (Elem<DT>::get(c.tgK, tb + n) * SK[min((int)c.tidxK[tb + n], k - 1)]);
-    const float p = __expf(lg - M);
-    l += p;
-    const int av = min((int)c.tidxV[tb + n], k - 1);
-    y = fmaf(p * Elem<DT>::get(c.tgV, tb + n), Elem<DT>::get(AV, (size_t)av * D + d), y);
+    const float lgt = scale * (Elem<DT>::get(c.tgK, tb + n) * SK[min((int)c.tidxK[tb + n], k - 1)]);
+    const float p = __expf(lgt - M);
+    if (tid == 0) l += p;
+    if (tid < D) {
+      const int av = min((int)c.tidxV[tb + n], k - 1);
+      acc = fmaf(p * Elem<DT>::get(c.tgV, tb + n), Elem<DT>::get(AV, (size_t)av * D + tid), acc);
+    }
   }
+  l = wave_sum(l);
+  if (lane == 0) rsum[wave] = l;
+  if (tid < D) yb[tid] = acc; else zb[tid - D] = acc;
   // Inverse rotation of the value-residual sum: s * FWHT(z) / D.
-  zb[d] = z;
   for (int hh = 1; hh < D; hh <<= 1) {
     __syncthreads();
-    const float a = zb[d & ~hh], bb = zb[d | hh];
-    const float v = (d & hh) ? a - bb : a + bb;
+    float v = 0.0f;
+    if (tid < D) {
+      const float x0 = zb[tid & ~hh], x1 = zb[tid | hh];
+      v = (tid & hh) ? x0 - x1 : x0 + x1;
+    }
     __syncthreads();
-    zb[d] = v;
+    if (tid < D) zb[tid] = v;
   }
   __syncthreads();
-  y += hsign(g.seed_sign, d) * zb[d] * (1.0f / (float)D);
-  const float o = y / l;
-  const size_t oi = ((size_t)b * g.Hq + jq) * D + d;
-  if (out_dtype == 1) ((uint16_t*)out)[oi] = f2bf(o); else ((float*)out)[oi] = o;
+  if (tid < D) {
+    const float lt = rsum[0] + rsum[1] + rsum[2] + rsum[3];
+    const float y = yb[tid] + hsign(g.seed_sign, tid) * zb[tid] * (1.0f / (float)D);
+    const float o = y / lt;
+    const size_t oi = ((size_t)b * g.Hq + jq) * D + tid;
+    if (out_dtype == 1) ((uint16_t*)out)[oi] = f2bf(o); else ((float*)out)[oi] = o;
+  }
 }
 
 // ------------------------------------------------------------------ append
@@ -473,10 +684,10 @@ __global__ __launch_bounds__(256) void k_reconstruct(Geo g, Cache c, int b, int 
   bool res = false;
   int slot = 0;
   if (i < S) {
-    const size_t po = (size_t)g.prefS[b] * g.H + (size_t)h * S;
-    t = min(max(c.pos[po + i], 0), S - 1);
-    a = min((int)(side ? c.idxV : c.idxK)[po + i], k - 1);
-    gb = Elem<DT>::get(side ? c.gV : c.gK, po + i);
+    const size_t so = slot_base(g, b, h);
+    t = min(max(c.pos[so + i], 0), S - 1);
+    a = min((int)(side ? c.idxV : c.idxK)[so + i], k - 1);
+    gb = Elem<DT>::get(side ? c.gV : c.gK, so + i);
     const size_t wo = (size_t)g.prefW[b] * g.H + (size_t)h * ((S + 63) / 64) + (i >> 6);
     const unsigned long long wm = (side ? c.maskV : c.maskK)[wo];
     res = (wm >> (i & 63)) & 1ull;
@@ -494,21 +705,7 @@ __global__ __launch_bounds__(256) void k_reconstruct(Geo g, Cache c, int b, int 
     const float sg = (side ? c.scalesV : c.scalesK)[(size_t)slot * (D / G) + (2 * lane) / G];
     const int nib = (cd[lane / 2] >> (4 * (lane & 1))) & 15;
     float z0 = sg * level(nib & 3), z1 = sg * level(nib >> 2);
-    {
-      const float p = z0, q = z1;
-      z0 = p + q;
-      z1 = p - q;
-    }
-    for (int hh = 1; hh < 64; hh <<= 1) {
-      const float o0 = __shfl_xor(z0, hh, 64), o1 = __shfl_xor(z1, hh, 64);
-      if (lane & hh) {
-        z0 = o0 - z0;
-        z1 = o1 - z1;
-      } else {
-        z0 = z0 + o0;
-        z1 = z1 + o1;
-      }
-    }
+    fwht_wave(z0, z1, lane);
     const float invD = 1.0f / (float)D;
     const float r0 = (z0 * invD) * hsign(g.seed_sign, 2 * lane);
     const float r1 = (z1 * invD) * hsign(g.seed_sign, 2 * lane + 1);
@@ -521,44 +718,60 @@ __global__ __launch_bounds__(256) void k_reconstruct(Geo g, Cache c, int b, int 
 }
 
 // ------------------------------------------------------------------ launchers
-template <int DT, int GQ>
+template <int DT, int GQ, int R>
 static void launch_stream(const Geo& g, const Cache& c, const DecWs& dw, float scale, int nblk, size_t lds,
                           hipStream_t st) {
-  (void)hipFuncSetAttribute((const void*)k_dec_stream<DT, GQ, 8>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-  AKV_TIMED("k_dec_stream", st, k_dec_stream<DT, GQ, 8><<<nblk, 256, lds, st>>>(g, c, dw, scale));
+  (void)hipFuncSetAttribute((const void*)k_dec_stream<DT, GQ, R>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                            (int)lds);
+  AKV_TIMED("k_dec_stream", st, k_dec_stream<DT, GQ, R><<<nblk, 256, lds, st>>>(g, c, dw, scale));
+}
+
+template <int DT, int GQ>
+static void launch_stream_r(const Geo& g, const Cache& c, const DecWs& dw, float scale, int nblk, size_t lds,
+                            hipStream_t st) {
+  switch (g.dsplit) {
+    case 2048: launch_stream<DT, GQ, 8>(g, c, dw, scale, nblk, lds, st); break;
+    default: launch_stream<DT, GQ, 4>(g, c, dw, scale, nblk, lds, st); break;
+  }
+}
+
+template <int DT>
+static void launch_stream_g(const Geo& g, const Cache& c, const DecWs& dw, float scale, int nblk, size_t lds,
+                            hipStream_t st) {
+  switch (g.g) {
+    case 1: launch_stream_r<DT, 1>(g, c, dw, scale, nblk, lds, st); break;
+    case 2: launch_stream_r<DT, 2>(g, c, dw, scale, nblk, lds, st); break;
+    case 4: launch_stream_r<DT, 4>(g, c, dw, scale, nblk, lds, st); break;
+    default: launch_stream_r<DT, 8>(g, c, dw, scale, nblk, lds, st); break;
+  }
+}
+
+// Dynamic LDS of the streaming kernel: the anchor-score table when it is kept
+// in LDS (the rest of its LDS is static).
+size_t decode_stream_lds(const Geo& g, int L, bool sk_in_lds) {
+  (void)L;
+  const size_t kpm = (size_t)((g.maxK + 3) & ~3);
+  return sk_in_lds ? g.g * kpm * 4 : 0;
 }
 
 hipError_t launch_decode(const Geo& g, const Cache& c, const DecWs& dw, const void* q, void* out, int out_dtype,
                          float scale, int n_app, hipStream_t st) {
   const int L = g.dsplit;
-  int nsc = 0, nst = 0;
+  int nsc = g.B * g.H * g.maxRB, nst = 0;
   for (int b = 0; b < g.B; ++b) {
-    nsc += g.H * ((g.k[b] + 63) / 64);
+    nsc += g.H * ((g.k[b] + 255) / 256);
     nst += g.H * ((g.S[b] + L - 1) / L);
   }
   if (g.dtype == 1) {
     AKV_TIMED("k_dec_scores", st, k_dec_scores<1><<<nsc, 256, 0, st>>>(g, c, dw, q));
+    launch_stream_g<1>(g, c, dw, scale, nst, decode_stream_lds(g, L, g.dsk_lds != 0), st);
+    AKV_TIMED("k_dec_combine", st,
+              k_dec_combine<1><<<g.B * g.Hq, 256, 0, st>>>(g, c, dw, scale, n_app, out, out_dtype));
   } else {
     AKV_TIMED("k_dec_scores", st, k_dec_scores<0><<<nsc, 256, 0, st>>>(g, c, dw, q));
-  }
-  const size_t lds = ((size_t)g.g * g.maxK + (size_t)g.g * (size_t)min(g.maxK, L)) * sizeof(float);
-#define AKV_STREAM(DT)                                                   \
-  switch (g.g) {                                                         \
-    case 1: launch_stream<DT, 1>(g, c, dw, scale, nst, lds, st); break;  \
-    case 2: launch_stream<DT, 2>(g, c, dw, scale, nst, lds, st); break;  \
-    case 4: launch_stream<DT, 4>(g, c, dw, scale, nst, lds, st); break;  \
-    default: launch_stream<DT, 8>(g, c, dw, scale, nst, lds, st); break; \
-  }
-  if (g.dtype == 1) {
-    AKV_STREAM(1)
-  } else {
-    AKV_STREAM(0)
-  }
-#undef AKV_STREAM
-  if (g.dtype == 1) {
-    AKV_TIMED("k_dec_combine", st, k_dec_combine<1><<<g.B * g.Hq, 128, 0, st>>>(g, c, dw, scale, L, n_app, out, out_dtype));
-  } else {
-    AKV_TIMED("k_dec_combine", st, k_dec_combine<0><<<g.B * g.Hq, 128, 0, st>>>(g, c, dw, scale, L, n_app, out, out_dtype));
+    launch_stream_g<0>(g, c, dw, scale, nst, decode_stream_lds(g, L, g.dsk_lds != 0), st);
+    AKV_TIMED("k_dec_combine", st,
+              k_dec_combine<0><<<g.B * g.Hq, 256, 0, st>>>(g, c, dw, scale, n_app, out, out_dtype));
   }
   return hipGetLastError();
 }

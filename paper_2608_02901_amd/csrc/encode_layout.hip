@@ -109,7 +109,7 @@ __global__ __launch_bounds__(64) void k_sscatter(Geo g, Ws w, Cache c) {
   __syncthreads();
   const int32_t* av = w.apos + (size_t)g.H * g.prefS[g.B] + (size_t)g.prefS[b] * g.H + (size_t)h * S;
   const int32_t* off = shist_base(g, w, b, h);
-  int32_t* pos = c.pos + (size_t)g.prefS[b] * g.H + (size_t)h * S;
+  int32_t* pos = c.pos + slot_base(g, b, h);
   const int t0 = ch * SORT_CHUNK, t1 = min(S, t0 + SORT_CHUNK);
   for (int tb = t0; tb < t1; tb += 64) {
     const int t = tb + lane;
@@ -139,20 +139,28 @@ __global__ __launch_bounds__(256) void k_lrec(Geo g, Ws w, Cache c) {
   const int nt = (S + 255) / 256;
   const int h = idx / nt, i = (idx % nt) * 256 + threadIdx.x;
   const size_t po = (size_t)g.prefS[b] * g.H + (size_t)h * S;
+  const size_t so = slot_base(g, b, h);
   const size_t TS = (size_t)g.prefS[g.B] * g.H;
   bool fk = false, fv = false;
   if (i < S) {
-    int t = c.pos[po + i];
+    int t = c.pos[so + i];
     if (t < 0 || t >= S) {
       atomicOr(&c.header[2], 8u);
       t = 0;
     }
-    c.idxK[po + i] = (uint16_t)w.apos[po + t];
-    c.idxV[po + i] = (uint16_t)w.apos[TS + po + t];
-    Elem<DT>::put(c.gK, po + i, w.gpos[po + t]);
-    Elem<DT>::put(c.gV, po + i, w.gpos[TS + po + t]);
+    c.idxK[so + i] = (uint16_t)w.apos[po + t];
+    c.idxV[so + i] = (uint16_t)w.apos[TS + po + t];
+    Elem<DT>::put(c.gK, so + i, w.gpos[po + t]);
+    Elem<DT>::put(c.gV, so + i, w.gpos[TS + po + t]);
     fk = w.sel[po + t] != 0;
     fv = w.sel[TS + po + t] != 0;
+  } else if (i < ((S + 63) & ~63)) {
+    // Padding slots of the head's last word: anchor 0 with coefficient 0.
+    c.pos[so + i] = 0;
+    c.idxK[so + i] = 0;
+    c.idxV[so + i] = 0;
+    Elem<DT>::put(c.gK, so + i, 0.0f);
+    Elem<DT>::put(c.gV, so + i, 0.0f);
   }
   const unsigned long long mk = __ballot(fk), mv = __ballot(fv);
   if ((threadIdx.x & 63) == 0 && i < S) {
@@ -205,26 +213,6 @@ __global__ __launch_bounds__(1024) void k_lscan(Geo g, Ws w, Cache c) {
   }
 }
 
-// Rotated-residual codec of one token held by a wave, two coordinates per
-// lane (2l, 2l+1).  Butterflies follow the Sylvester stage order h = 1..D/2.
-__device__ inline void fwht_wave(float& z0, float& z1, int lane) {
-  {
-    const float a = z0, bb = z1;
-    z0 = a + bb;
-    z1 = a - bb;
-  }
-  for (int hh = 1; hh < 64; hh <<= 1) {
-    const float o0 = __shfl_xor(z0, hh, 64), o1 = __shfl_xor(z1, hh, 64);
-    if (lane & hh) {
-      z0 = o0 - z0;
-      z1 = o1 - z1;
-    } else {
-      z0 = z0 + o0;
-      z1 = z1 + o1;
-    }
-  }
-}
-
 template <int DT>
 __global__ __launch_bounds__(256) void k_codec(Geo g, Ws w, Cache c, const void* Kin, const void* Vin) {
   using E = typename Elem<DT>::T;
@@ -261,7 +249,7 @@ __global__ __launch_bounds__(256) void k_codec(Geo g, Ws w, Cache c, const void*
     const int bit = __ffsll((long long)mask) - 1;
     mask &= mask - 1;
     const int i = word * 64 + bit;
-    const int t = min(max(c.pos[po + i], 0), S - 1);
+    const int t = min(max(c.pos[slot_base(g, b, h) + i], 0), S - 1);
     const int a = min(max(w.apos[side * TS + po + t], 0), k - 1);
     const float gb = w.gpos[side * TS + po + t];
     const E* x = X + (size_t)t * D;

@@ -52,6 +52,7 @@ def _cfg(**kw):
     (dict(head_dim=64), N.ERR_UNSUPPORTED),
     (dict(kappa=6), N.ERR_INVALID_ARG),
     (dict(quant_group=48), N.ERR_INVALID_ARG),
+    (dict(quant_group=16), N.ERR_UNSUPPORTED),
     (dict(rho=1.5), N.ERR_INVALID_ARG),
     (dict(budget=-0.1), N.ERR_INVALID_ARG),
     (dict(anchor_frac=0.0), N.ERR_INVALID_ARG),
