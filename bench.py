@@ -161,8 +161,7 @@ def main():
         for s in range(NS):
             for l in range(L):
                 lay = layers[l]
-                akv.append(plan, caches[l], s, lay.k_new[s], lay.v_new[s])
-                akv.decode_attn(plan, caches[l], lay.q[s], out, dws, n_appended=s + 1)
+                akv.decode_step(plan, caches[l], s, lay.k_new[s], lay.v_new[s], lay.q[s], out, dws)
         if ev:
             ev[2].record()
         akv.reconstruct(plan, caches[0], 0, 0, n_appended=NS, out=dense)
@@ -174,7 +173,7 @@ def main():
         torch.cuda.synchronize()
         log(f"warmup step {i} done")
 
-    kernels = ["k_dec_stream", "k_assign", "k_dec_scores", "k_dec_combine", "k_append"]
+    kernels = ["k_dec_stream", "k_dec_front", "k_assign"]
     timer = N.KernelTimer(kernels, max_launches=max(64, args.steps * NS * L + 16))
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
     torch.cuda.synchronize()

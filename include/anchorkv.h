@@ -137,24 +137,38 @@ anchorkv_status anchorkv_encode(const anchorkv_plan* plan, const void* K, const 
 
 /* Appends one generated token per request and KV head (config max_append
  * slots).  The token is encoded against the request's existing anchors (its
- * nearest anchor and coefficient, Eqs. nearest-anchor and projection) and
+ * nearest anchor and coefficient, Eqs. nearest-anchor and projection, with the
+ * same certified argmax and canonical coefficient as the compression pass) and
  * stores no residual.  n_appended: tokens already appended to this cache
- * (host-tracked), must be < max_append.  k_new, v_new: device [batch][H][D]. */
+ * (host-tracked), must be < max_append, else ANCHORKV_ERR_CAPACITY.
+ * k_new, v_new: device [batch][H][D], dtype.  workspace: device,
+ * anchorkv_decode_workspace_bytes(plan), contents undefined afterwards. */
 anchorkv_status anchorkv_append(const anchorkv_plan* plan, void* cache, int32_t n_appended, const void* k_new,
-                                const void* v_new, void* stream);
+                                const void* v_new, void* workspace, void* stream);
 
 /* Decode attention over the compressed cache (Eq. exact-attention with the
  * reconstructed keys and values of Eq. reconstruction), never materializing
  * them: q.k^_t = gamma_t (q.k_a(t)) + q.r~_t and the values accumulate as
  * per-anchor weights plus a rotated residual sum (App. E.1).
  *   n_appended : appended tokens included (the first n_appended tail slots).
- *   q          : device [batch][Hq][D], dtype.
+ *   q          : device [batch][Hq][D], dtype; query head j reads KV head j / g.
  *   out        : device [batch][Hq][D], out_dtype (anchorkv_dtype).
  *   softmax_scale : <= 0 selects 1/sqrt(D).
- *   workspace  : device, anchorkv_decode_workspace_bytes(plan). */
+ *   workspace  : device, anchorkv_decode_workspace_bytes(plan); contents
+ *                undefined afterwards.  Two calls that share a workspace must
+ *                not run concurrently. */
 anchorkv_status anchorkv_decode_attn(const anchorkv_plan* plan, const void* cache, int32_t n_appended,
                                      const void* q, void* out, int32_t out_dtype, float softmax_scale,
                                      void* workspace, void* stream);
+
+/* One generation step: anchorkv_append of (k_new, v_new) as tail slot
+ * n_appended, then anchorkv_decode_attn over the cache including it
+ * (n_appended + 1 tail tokens).  The result equals the two calls in sequence;
+ * the append's anchor scan shares the attention's passes over the anchors, so
+ * it adds no pass over HBM.  Arguments as in those two calls. */
+anchorkv_status anchorkv_decode_step(const anchorkv_plan* plan, void* cache, int32_t n_appended, const void* k_new,
+                                     const void* v_new, const void* q, void* out, int32_t out_dtype,
+                                     float softmax_scale, void* workspace, void* stream);
 
 /* Dense reconstruction (Eq. reconstruction) of one side (0 = keys, 1 = values)
  * of one request: out is device fp32 [H][S_b + n_appended][D], position order. */

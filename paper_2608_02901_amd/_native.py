@@ -23,7 +23,7 @@ BUDGET_FRACTION, BUDGET_THETA, BUDGET_COUNT = 0, 1, 2
 
 EXPORTED = ["anchorkv_plan_create", "anchorkv_plan_destroy", "anchorkv_cache_bytes", "anchorkv_encode_workspace_bytes",
             "anchorkv_decode_workspace_bytes", "anchorkv_plan_request", "anchorkv_encode", "anchorkv_append",
-            "anchorkv_decode_attn", "anchorkv_reconstruct", "anchorkv_export", "anchorkv_profile_enable",
+            "anchorkv_decode_attn", "anchorkv_decode_step", "anchorkv_reconstruct", "anchorkv_export", "anchorkv_profile_enable",
             "anchorkv_profile_read", "anchorkv_profile_disable", "anchorkv_status_string", "anchorkv_last_error"]
 
 
@@ -82,9 +82,11 @@ def lib():
         L.anchorkv_encode.restype = i32
         L.anchorkv_encode.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp]
         L.anchorkv_append.restype = i32
-        L.anchorkv_append.argtypes = [vp, vp, i32, vp, vp, vp]
+        L.anchorkv_append.argtypes = [vp, vp, i32, vp, vp, vp, vp]
         L.anchorkv_decode_attn.restype = i32
         L.anchorkv_decode_attn.argtypes = [vp, vp, i32, vp, vp, i32, f32, vp, vp]
+        L.anchorkv_decode_step.restype = i32
+        L.anchorkv_decode_step.argtypes = [vp, vp, i32, vp, vp, vp, vp, i32, f32, vp, vp]
         L.anchorkv_reconstruct.restype = i32
         L.anchorkv_reconstruct.argtypes = [vp, vp, i32, i32, i32, vp, vp]
         L.anchorkv_export.restype = i32
@@ -178,9 +180,22 @@ def encode(plan: Plan, K, V, Qobs, cache, workspace, anchor_override=None, strea
     return K, V, Qobs, ov  # keep packed copies alive until the stream has consumed them
 
 
-def append(plan: Plan, cache, n_appended: int, k_new, v_new, stream=None):
+def append(plan: Plan, cache, n_appended: int, k_new, v_new, workspace, stream=None):
     k_new, v_new = k_new.contiguous(), v_new.contiguous()
-    check(lib().anchorkv_append(plan.handle, _ptr(cache), n_appended, _ptr(k_new), _ptr(v_new), _stream(stream)))
+    check(lib().anchorkv_append(plan.handle, _ptr(cache), n_appended, _ptr(k_new), _ptr(v_new), _ptr(workspace),
+                                _stream(stream)))
+    return k_new, v_new
+
+
+def decode_step(plan: Plan, cache, n_appended: int, k_new, v_new, q, out, workspace, out_dtype: Optional[int] = None,
+                softmax_scale: float = 0.0, stream=None):
+    import torch
+    k_new, v_new, q = k_new.contiguous(), v_new.contiguous(), q.contiguous()
+    if out_dtype is None:
+        out_dtype = F32 if out.dtype == torch.float32 else BF16
+    check(lib().anchorkv_decode_step(plan.handle, _ptr(cache), n_appended, _ptr(k_new), _ptr(v_new), _ptr(q),
+                                     _ptr(out), out_dtype, softmax_scale, _ptr(workspace), _stream(stream)))
+    return out
 
 
 def decode_attn(plan: Plan, cache, q, out, workspace, n_appended: int = 0, out_dtype: Optional[int] = None,

@@ -28,6 +28,7 @@ struct Geo {
   int kappa, scale_mode, max_append;
   int maxS, maxK;
   unsigned long long seed_anchor, seed_sign;
+  unsigned long long sgnbits[2];  // Hadamard sign of coordinate j (bit set = -1), j < 128
   int S[AKV_MAXB], k[AKV_MAXB], ntop[AKV_MAXB], nrand[AKV_MAXB];
   int prefS[AKV_MAXB + 1];   // sum of S over earlier requests
   int prefK[AKV_MAXB + 1];   // sum of k
@@ -39,9 +40,8 @@ struct Geo {
   int prefNK[AKV_MAXB + 1];  // sum of key residual counts
   int prefNV[AKV_MAXB + 1];  // sum of value residual counts
   int prefKp[AKV_MAXB + 1];  // sum of k rounded up to 4 (anchor-score table rows)
+  int prefAB[AKV_MAXB + 1];  // sum of ceil(k/256) (256-anchor blocks per head)
   int dsplit;                // decode split length (sorted slots per workgroup)
-  int maxRB;                 // decode: most 256-residual blocks any head can need
-  int dsk_lds;               // decode keeps the anchor-score table in LDS
 };
 
 // Per-slot arrays (records, position ids) give every head a stride of
@@ -114,9 +114,11 @@ struct Ws {
 };
 
 struct DecWs {
-  float* SK;            // [b][h][g][k_b] anchor scores q_j . abar^K_a
+  float* SK;            // [b][h][kp_b][g] anchor scores q_j . abar^K_a (kp = k rounded up to 4)
   float* RK;            // [sum N_K][g] key-residual logit terms q_rot . zhat / D
-  float* part;          // [b][Hq][split][2 + 2D] partial (max, sum, y[D], zacc[D])
+  float* part;          // [b][Hq][split][4 + D] split record (max, sum, -, -, output[D])
+  float* asc;           // [side][b][h][kp_b] screening score of the appended token per anchor
+  float4* atop;         // [side][b][h][ceil(k_b/256)] top-2 of those scores per 256 anchors
 };
 
 // ------------------------------------------------------------------ vector types
@@ -248,6 +250,86 @@ __device__ inline int wave_sum_i(int v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
   return v;
+}
+
+// Whole-wave reductions through DPP lane moves (quad xor 1, quad xor 2, half-row
+// mirror, row mirror: every lane of a 16-lane row then holds the row's result)
+// and one read of each row; the result is wave-uniform.  Summation order differs
+// from the butterflies above, so these serve only where no integer result
+// depends on the rounding.
+__device__ inline float dpp_f(float v, int ctrl) {
+  switch (ctrl) {  // the control word must be a compile-time constant
+    case 0xB1: return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0xB1, 0xF, 0xF, false));
+    case 0x4E: return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0x4E, 0xF, 0xF, false));
+    case 0x141: return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0x141, 0xF, 0xF, false));
+    default: return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0x140, 0xF, 0xF, false));
+  }
+}
+__device__ inline float rdlane(float v, int l) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), l));
+}
+__device__ inline float wave_max_dpp(float v) {
+  v = fmaxf(v, dpp_f(v, 0xB1));
+  v = fmaxf(v, dpp_f(v, 0x4E));
+  v = fmaxf(v, dpp_f(v, 0x141));
+  v = fmaxf(v, dpp_f(v, 0x140));
+  return fmaxf(fmaxf(rdlane(v, 0), rdlane(v, 16)), fmaxf(rdlane(v, 32), rdlane(v, 48)));
+}
+__device__ inline float wave_sum_dpp(float v) {
+  v = v + dpp_f(v, 0xB1);
+  v = v + dpp_f(v, 0x4E);
+  v = v + dpp_f(v, 0x141);
+  v = v + dpp_f(v, 0x140);
+  return (rdlane(v, 0) + rdlane(v, 16)) + (rdlane(v, 32) + rdlane(v, 48));
+}
+
+// Value of lane (lane ^ M) for M = 1, 2, 4, 8 (DPP moves inside a 16-lane row)
+// and 16, 32 (LDS permute).
+template <int M>
+__device__ inline float lane_xor(float v) {
+  const int x = __builtin_bit_cast(int, v);
+  if constexpr (M == 1) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, x, 0xB1, 0xF, 0xF, false));
+  } else if constexpr (M == 2) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, x, 0x4E, 0xF, 0xF, false));
+  } else if constexpr (M == 4) {  // (i ^ 7) ^ 3
+    const int t = __builtin_amdgcn_update_dpp(0, x, 0x141, 0xF, 0xF, false);
+    return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, t, 0x1B, 0xF, 0xF, false));
+  } else if constexpr (M == 8) {  // (i ^ 15) ^ 7
+    const int t = __builtin_amdgcn_update_dpp(0, x, 0x140, 0xF, 0xF, false);
+    return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, t, 0x141, 0xF, 0xF, false));
+  } else {
+    return __shfl_xor(v, M, 64);
+  }
+}
+
+// Butterfly stage with partner distance M lanes (coordinate distance 2M).
+template <int M>
+__device__ inline void fwht_stage(float& z0, float& z1, int lane) {
+  const float o0 = lane_xor<M>(z0), o1 = lane_xor<M>(z1);
+  const bool hi = lane & M;
+  z0 = hi ? o0 - z0 : z0 + o0;
+  z1 = hi ? o1 - z1 : z1 + o1;
+}
+
+// fwht_wave with DPP lane moves; same stage order and arithmetic.
+__device__ inline void fwht_wave_dpp(float& z0, float& z1, int lane) {
+  {
+    const float a = z0, bb = z1;
+    z0 = a + bb;
+    z1 = a - bb;
+  }
+  fwht_stage<1>(z0, z1, lane);
+  fwht_stage<2>(z0, z1, lane);
+  fwht_stage<4>(z0, z1, lane);
+  fwht_stage<8>(z0, z1, lane);
+  fwht_stage<16>(z0, z1, lane);
+  fwht_stage<32>(z0, z1, lane);
+}
+
+// Sign of coordinate j from the packed sign bits (bit set = -1).
+__device__ inline float sign_bit(const unsigned long long* bits, int j) {
+  return ((bits[j >> 6] >> (j & 63)) & 1ull) ? -1.0f : 1.0f;
 }
 
 // Locates request b for a flat work index over per-request unit counts

@@ -25,12 +25,10 @@ hipError_t launch_epilogue(const Geo& g, const Ws& w, const Cache& c, const void
                            hipStream_t st);
 hipError_t launch_budget(const Geo& g, const Ws& w, hipStream_t st);
 hipError_t launch_layout(const Geo& g, const Ws& w, const Cache& c, const void* K, const void* V, hipStream_t st);
-hipError_t launch_decode(const Geo& g, const Cache& c, const DecWs& dw, const void* q, void* out, int out_dtype,
-                         float scale, int n_app, hipStream_t st);
-hipError_t launch_append(const Geo& g, const Cache& c, int n_app, const void* kn, const void* vn, hipStream_t st);
+hipError_t launch_decode(const Geo& g, const Cache& c, const DecWs& dw, const void* q, const void* kn,
+                         const void* vn, void* out, int out_dtype, float scale, int n_app, hipStream_t st);
 hipError_t launch_reconstruct(const Geo& g, const Cache& c, int b, int side, int n_app, float* out,
                               hipStream_t st);
-size_t decode_stream_lds(const Geo& g, int L, bool sk_in_lds);
 }  // namespace akv
 
 using akv::Geo;
@@ -71,7 +69,7 @@ struct anchorkv_plan {
       w_fix, w_fixcount, w_gpos, w_u, w_sel, w_bhist, w_bstate, w_tiecnt, w_shist, w_wcnt;
   size_t ws_bytes;
   // decode workspace offsets
-  size_t d_SK, d_RK, d_part;
+  size_t d_SK, d_RK, d_part, d_asc, d_atop;
   size_t dws_bytes;
 };
 
@@ -145,6 +143,9 @@ extern "C" anchorkv_status anchorkv_plan_create(const anchorkv_config* cfg, int3
   geo.max_append = c.max_append;
   geo.seed_anchor = mix64(c.seed ^ 1ull);
   geo.seed_sign = mix64(c.seed ^ 2ull);
+  geo.sgnbits[0] = geo.sgnbits[1] = 0;
+  for (int j = 0; j < D; ++j)
+    if (mix64(geo.seed_sign ^ (uint64_t)j) >> 63) geo.sgnbits[j >> 6] |= 1ull << (j & 63);
   int64_t totS = 0;
   for (int b = 0; b < batch; ++b) {
     const int S = seq_lens[b];
@@ -215,31 +216,18 @@ extern "C" anchorkv_status anchorkv_plan_create(const anchorkv_config* cfg, int3
     geo.prefKT[b + 1] = geo.prefKT[b] + H * k * ((S + akv::SORT_CHUNK - 1) / akv::SORT_CHUNK);
     geo.prefBC[b + 1] = geo.prefBC[b] + (H * S + kBudgetChunk - 1) / kBudgetChunk;
     geo.prefKp[b + 1] = geo.prefKp[b] + ((k + 3) & ~3);
+    geo.prefAB[b + 1] = geo.prefAB[b] + (k + 255) / 256;
     geo.prefNK[b + 1] = geo.prefNK[b] + (int)p->req[b].residuals_k;
     geo.prefNV[b + 1] = geo.prefNV[b] + (int)p->req[b].residuals_v;
   }
   // Decode split: 2048 sorted slots per workgroup when that still gives at
-  // least 256 workgroups (one per CU), else 1024.  The anchor-score table
-  // stays in LDS up to 64 KB per workgroup, else it is read from L2.
+  // least 256 workgroups (one per CU), else 1024.
   {
     int Lsel = 1024;
-    for (int Lc : {2048, 1024}) {
-      int64_t n = 0;
-      for (int b = 0; b < batch; ++b) n += (int64_t)H * ((geo.S[b] + Lc - 1) / Lc);
-      if (n >= 256) {
-        Lsel = Lc;
-        break;
-      }
-    }
-    const size_t budget = 64 * 1024;
+    int64_t n = 0;
+    for (int b = 0; b < batch; ++b) n += (int64_t)H * ((geo.S[b] + 2047) / 2048);
+    if (n >= 256) Lsel = 2048;
     geo.dsplit = Lsel;
-    int64_t mr = 0;
-    for (int b = 0; b < batch; ++b) {
-      const int64_t nh = std::min<int64_t>(p->req[b].residuals_k, (int64_t)geo.S[b] - geo.k[b]);
-      mr = std::max<int64_t>(mr, (nh + 255) / 256);
-    }
-    geo.maxRB = (int)mr;
-    geo.dsk_lds = akv::decode_stream_lds(geo, Lsel, true) <= budget ? 1 : 0;
     for (int b = 0; b < batch; ++b) geo.prefSp[b + 1] = geo.prefSp[b] + (geo.S[b] + Lsel - 1) / Lsel;
   }
   const size_t TS = (size_t)geo.prefS[batch] * H, TK = (size_t)geo.prefK[batch] * H,
@@ -306,7 +294,9 @@ extern "C" anchorkv_status anchorkv_plan_create(const anchorkv_config* cfg, int3
   Layout Dl;
   p->d_SK = Dl.add(4 * (size_t)geo.prefKp[batch] * H * g);
   p->d_RK = Dl.add(4 * (size_t)geo.prefNK[batch] * g);
-  p->d_part = Dl.add(4 * (size_t)geo.prefSp[batch] * geo.Hq * (2 + 2 * D));
+  p->d_part = Dl.add(4 * (size_t)geo.prefSp[batch] * geo.Hq * (4 + D));
+  p->d_asc = Dl.add(4 * 2 * (size_t)geo.prefKp[batch] * H);
+  p->d_atop = Dl.add(16 * 2 * (size_t)geo.prefAB[batch] * H);
   p->dws_bytes = Dl.total;
   *out = p;
   return ANCHORKV_OK;
@@ -394,6 +384,8 @@ static akv::DecWs dws_ptrs(const anchorkv_plan* p, void* base) {
   d.SK = at<float>(base, p->d_SK);
   d.RK = at<float>(base, p->d_RK);
   d.part = at<float>(base, p->d_part);
+  d.asc = at<float>(base, p->d_asc);
+  d.atop = at<float4>(base, p->d_atop);
   return d;
 }
 
@@ -425,12 +417,13 @@ extern "C" anchorkv_status anchorkv_encode(const anchorkv_plan* p, const void* K
 }
 
 extern "C" anchorkv_status anchorkv_append(const anchorkv_plan* p, void* cache, int32_t n_appended, const void* k_new,
-                                           const void* v_new, void* stream) {
-  if (!p || !cache || !k_new || !v_new) return fail(ANCHORKV_ERR_INVALID_ARG, "null argument");
+                                           const void* v_new, void* workspace, void* stream) {
+  if (!p || !cache || !k_new || !v_new || !workspace) return fail(ANCHORKV_ERR_INVALID_ARG, "null argument");
   if (n_appended < 0) return fail(ANCHORKV_ERR_INVALID_ARG, "n_appended must be >= 0");
   if (n_appended >= p->cfg.max_append) return fail(ANCHORKV_ERR_CAPACITY, "append capacity exhausted");
   (void)hipGetLastError();
-  return hip_status(akv::launch_append(p->geo, cache_ptrs(p, cache), n_appended, k_new, v_new, (hipStream_t)stream),
+  return hip_status(akv::launch_decode(p->geo, cache_ptrs(p, cache), dws_ptrs(p, workspace), nullptr, k_new, v_new,
+                                       nullptr, 0, 0.0f, n_appended, (hipStream_t)stream),
                     "append");
 }
 
@@ -443,9 +436,25 @@ extern "C" anchorkv_status anchorkv_decode_attn(const anchorkv_plan* p, const vo
   if (out_dtype != ANCHORKV_F32 && out_dtype != ANCHORKV_BF16) return fail(ANCHORKV_ERR_INVALID_ARG, "bad out_dtype");
   const float scale = softmax_scale > 0.0f ? softmax_scale : 1.0f / sqrtf((float)p->geo.D);
   (void)hipGetLastError();
-  return hip_status(akv::launch_decode(p->geo, cache_ptrs(p, (void*)cache), dws_ptrs(p, workspace), q, out, out_dtype,
-                                       scale, n_appended, (hipStream_t)stream),
+  return hip_status(akv::launch_decode(p->geo, cache_ptrs(p, (void*)cache), dws_ptrs(p, workspace), q, nullptr,
+                                       nullptr, out, out_dtype, scale, n_appended, (hipStream_t)stream),
                     "decode");
+}
+
+extern "C" anchorkv_status anchorkv_decode_step(const anchorkv_plan* p, void* cache, int32_t n_appended,
+                                                const void* k_new, const void* v_new, const void* q, void* out,
+                                                int32_t out_dtype, float softmax_scale, void* workspace,
+                                                void* stream) {
+  if (!p || !cache || !k_new || !v_new || !q || !out || !workspace)
+    return fail(ANCHORKV_ERR_INVALID_ARG, "null argument");
+  if (n_appended < 0) return fail(ANCHORKV_ERR_INVALID_ARG, "n_appended must be >= 0");
+  if (n_appended >= p->cfg.max_append) return fail(ANCHORKV_ERR_CAPACITY, "append capacity exhausted");
+  if (out_dtype != ANCHORKV_F32 && out_dtype != ANCHORKV_BF16) return fail(ANCHORKV_ERR_INVALID_ARG, "bad out_dtype");
+  const float scale = softmax_scale > 0.0f ? softmax_scale : 1.0f / sqrtf((float)p->geo.D);
+  (void)hipGetLastError();
+  return hip_status(akv::launch_decode(p->geo, cache_ptrs(p, cache), dws_ptrs(p, workspace), q, k_new, v_new, out,
+                                       out_dtype, scale, n_appended, (hipStream_t)stream),
+                    "decode step");
 }
 
 extern "C" anchorkv_status anchorkv_reconstruct(const anchorkv_plan* p, const void* cache, int32_t n_appended,

@@ -1,35 +1,43 @@
 // Decode attention over the compressed cache (Sec. 3.4 "Storage and
-// Decoding"; App. E.1) and the two cache services around it.
+// Decoding"; App. E.1), the append of generated tokens, and the dense
+// reconstruction of Eq. (reconstruction).
 //
 // Attention of query j (KV head h = j / g) over every stored entry t:
 //   logit_t = scale * (gamma^K_t (q_j . abar^K_a(t)) + [t in R_K] q_rot . zhat^K_t / D)
 //   out     = (sum_a w_a abar^V_a + s * FWHT(sum_t p_t zhat^V_t) / D) / sum_t p_t
 // with p_t = exp(logit_t - max), w_a = sum over tokens of value anchor a of
 // p_t gamma^V_t, zhat the dequantized rotated residual and q_rot = FWHT(s * q).
-// This is the exact algebra of attention over the reconstructed cache (Eq.
-// reconstruction): U is orthogonal and linear, so the inverse rotation of the
-// value residuals is applied once per query instead of once per token, and
-// the key residual term is a dot product in the rotated basis.
+// This is the exact algebra of attention over the reconstructed cache: U is
+// orthogonal and linear, so the inverse rotation of the value residuals is
+// applied once per query and split instead of once per token, and the key
+// residual term is a dot product in the rotated basis.
 //
-//   k_dec_scores : everything that depends only on the queries, fully parallel:
-//                  the anchor scores S_K[j][a] = q_j . abar^K_a (one thread per
-//                  anchor, the row in registers) and the key-residual terms
-//                  q_rot . zhat^K_t / D (one thread per stored key residual);
+// One decode step is two launches:
+//   k_dec_front  : work that depends only on the new query and token, fully
+//                  parallel: anchor scores S_K[a][j] = q_j . abar^K_a (one
+//                  thread per anchor, the row in registers), key-residual terms
+//                  q_rot . zhat^K_e / D (one thread per stored key residual), and,
+//                  when a token is appended, its screening similarity to every
+//                  anchor of both sides with a per-256-anchor top-2;
 //   k_dec_stream : split-K pass over the value-anchor-grouped records.  Loads
-//                  are issued in two rounds (records, flags, the score table;
-//                  then key-residual terms, value-anchor rows and value
-//                  residual codes); per split it writes the partial (max, sum,
-//                  sum_a w_a abar^V_a, rotated value-residual sum).  Blocks are
-//                  mapped so that all splits of one head share one XCD (and its
-//                  L2) for the score table and the anchor rows;
-//   k_dec_combine: merges the splits, adds appended tokens, applies the
-//                  inverse rotation once and normalizes.
-//   k_append     : encodes one new key/value per head against the existing
-//                  anchors (certified argmax, canonical fp64 coefficient).
+//                  come in two rounds (records and flag words; then anchor
+//                  scores, key-residual terms, value-anchor rows and value
+//                  residual codes).  Each split writes (max, sum, output) with
+//                  the rotation of its value residuals already undone.  All
+//                  splits of a head run on one XCD.  Extra workgroups resolve
+//                  the appended token's anchors meanwhile (certified argmax,
+//                  canonical fp64 coefficient);
+//   k_dec_merge  : merges the splits of each query head and the appended tail;
+//   k_app_finish : the argmax resolution alone, for a standalone append.
 //   k_reconstruct: dense x^ of one side of one request (Eq. reconstruction).
 #include "akv_common.h"
 
 namespace akv {
+
+constexpr int PS = 4 + AKV_D;  // split record: max, sum, 2 pad, output[D]
+constexpr int DEC_ASTG = 64;   // value-anchor rows staged in LDS per split
+constexpr int DEC_RCW = 512;   // anchor window of the per-anchor value weights
+constexpr int DEC_VCH = 128;   // value residuals staged per chunk
 
 __device__ inline float level(int code) {
   // 0 -> -L1, 1 -> -L0, 2 -> +L0, 3 -> +L1
@@ -44,112 +52,367 @@ __device__ inline float scaled_level(int code, float n1, float n0, float p0, flo
   return (code & 2) ? hi : lo;
 }
 
-// ------------------------------------------------------------------ D1
-template <int DT>
-__global__ __launch_bounds__(256) void k_dec_scores(Geo g, Cache c, DecWs dw, const void* qin) {
+// Merge of two (best, second best, index of best) summaries of screening
+// scores; ties of the best go to the lower anchor index.
+__device__ inline void top2_merge(float& b1, float& b2, int& i1, float c1, float c2, int j1) {
+  const float t2 = fmaxf(fmaxf(b2, c2), fminf(b1, c1));
+  if (c1 > b1 || (c1 == b1 && j1 < i1)) i1 = j1;
+  b1 = fmaxf(b1, c1);
+  b2 = t2;
+}
+__device__ inline void top2_wave(float& b1, float& b2, int& i1) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const float c1 = __shfl_xor(b1, o, 64), c2 = __shfl_xor(b2, o, 64);
+    const int j1 = __shfl_xor(i1, o, 64);
+    top2_merge(b1, b2, i1, c1, c2, j1);
+  }
+}
+
+// GQ consecutive floats (16-byte aligned when GQ >= 4) as a vector load/store.
+template <int GQ>
+__device__ inline void load_g(const float* p, float* v) {
+  if constexpr (GQ % 4 == 0) {
+#pragma unroll
+    for (int i = 0; i < GQ / 4; ++i) {
+      const float4 t = *(const float4*)(p + 4 * i);
+      v[4 * i] = t.x;
+      v[4 * i + 1] = t.y;
+      v[4 * i + 2] = t.z;
+      v[4 * i + 3] = t.w;
+    }
+  } else if constexpr (GQ == 2) {
+    const float2 t = *(const float2*)p;
+    v[0] = t.x;
+    v[1] = t.y;
+  } else {
+    v[0] = p[0];
+  }
+}
+template <int GQ>
+__device__ inline void store_g(float* p, const float* v) {
+  if constexpr (GQ % 4 == 0) {
+#pragma unroll
+    for (int i = 0; i < GQ / 4; ++i) *(float4*)(p + 4 * i) = make_float4(v[4 * i], v[4 * i + 1], v[4 * i + 2], v[4 * i + 3]);
+  } else if constexpr (GQ == 2) {
+    *(float2*)p = make_float2(v[0], v[1]);
+  } else {
+    p[0] = v[0];
+  }
+}
+
+// ------------------------------------------------------------------ front
+// Dot products of one anchor row (in registers) with the g staged queries
+// ([d][j] layout) and with the appended token.
+template <int DT, int GQ, bool DOQ, bool APP>
+__device__ inline void anchor_dots(const uint4* rv, const float* qs, const float* xs, float* acc, float& s) {
   using E = typename Elem<DT>::T;
-  constexpr int D = AKV_D;
-  constexpr int PER = 16 / sizeof(E);
-  __shared__ float qs[8][D];
-  const int gq = g.g;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  constexpr int PER = 16 / sizeof(E), NV = AKV_D / PER;
+#pragma unroll
+  for (int i = 0; i < NV; ++i) {
+    const E* e = (const E*)&rv[i];
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+      const float x = Elem<DT>::get(e, j);
+      if constexpr (DOQ) {
+        float qv[GQ];
+        load_g<GQ>(&qs[(i * PER + j) * GQ], qv);
+#pragma unroll
+        for (int jj = 0; jj < GQ; ++jj) acc[jj] = fmaf(qv[jj], x, acc[jj]);
+      }
+      if constexpr (APP) s = fmaf(xs[i * PER + j], x, s);
+    }
+  }
+}
+
+template <int M>
+__device__ inline int lane_xor_i(int v) {
+  return __builtin_bit_cast(int, lane_xor<M>(__builtin_bit_cast(float, v)));
+}
+template <int M>
+__device__ inline void top2_step(float& b1, float& b2, int& i1) {
+  const float c1 = lane_xor<M>(b1), c2 = lane_xor<M>(b2);
+  const int j1 = lane_xor_i<M>(i1);
+  top2_merge(b1, b2, i1, c1, c2, j1);
+}
+__device__ inline void top2_wave_dpp(float& b1, float& b2, int& i1) {
+  top2_step<1>(b1, b2, i1);
+  top2_step<2>(b1, b2, i1);
+  top2_step<4>(b1, b2, i1);
+  top2_step<8>(b1, b2, i1);
+  top2_step<16>(b1, b2, i1);
+  top2_step<32>(b1, b2, i1);
+}
+
+// Grid: nAK key-anchor blocks, nAV value-anchor blocks (append only), then
+// ceil(sum N_K / 256) key-residual blocks (attention only).  flags: bit 0 =
+// attention (q given), bit 1 = append (k_new, v_new given).  sl2 = softmax
+// scale * log2(e): the stored anchor scores and key-residual terms are logits
+// in base 2.
+template <int DT, int GQ>
+__global__ __launch_bounds__(256) void k_dec_front(Geo g, Cache c, DecWs dw, const void* q, const void* kin,
+                                                   const void* vin, int flags, int nAK, int nAV, float sl2) {
+  using E = typename Elem<DT>::T;
+  constexpr int D = AKV_D, PER = 16 / sizeof(E), NV = D / PER;
+  __shared__ __align__(16) float qs[D * GQ];          // [d][j] queries, or rotated queries
+  __shared__ __align__(16) float tab[64 * 16 * GQ];   // [pair][nibble][j] residual-term table
+  __shared__ float xs[D];
+  __shared__ float rb1[4], rb2[4];
+  __shared__ int ri1[4];
+  __shared__ int bhr[2];
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const bool attn = flags & 1, app = (flags & 2) != 0;
   int idx = blockIdx.x;
-  int nsc = 0;
-  for (int b = 0; b < g.B; ++b) nsc += g.H * ((g.k[b] + 255) / 256);
-  if (idx < nsc) {
-    // ---- anchor scores
+  if (idx < nAK + nAV) {
+    const int side = idx >= nAK ? 1 : 0;
+    if (side) idx -= nAK;
     int b = 0;
-    for (; b < g.B; ++b) {
+    for (; b < g.B - 1; ++b) {
       const int n = g.H * ((g.k[b] + 255) / 256);
       if (idx < n) break;
       idx -= n;
     }
-    const int k = g.k[b], kp = (k + 3) & ~3;
-    const int nch = (k + 255) / 256;
-    const int h = idx / nch, a0 = (idx % nch) * 256;
-    const int a = a0 + threadIdx.x;
+    const int k = g.k[b], kp = (k + 3) & ~3, nab = (k + 255) / 256;
+    const int h = idx / nab, ch = idx % nab;
+    const int a = ch * 256 + tid;
+    const bool valid = a < k;
     const size_t ko = (size_t)g.prefK[b] * g.H + (size_t)h * k;
-    const E* row = (const E*)c.ancK + (ko + min(a, k - 1)) * D;
-    uint4 rv[D / PER];
+    const E* row = (const E*)(side ? c.ancV : c.ancK) + (ko + min(a, k - 1)) * D;
+    uint4 rv[NV];
 #pragma unroll
-    for (int i = 0; i < D / PER; ++i) rv[i] = *(const uint4*)(row + i * PER);
-    const E* q = (const E*)qin + ((size_t)b * g.Hq + (size_t)h * gq) * D;
-    for (int i = threadIdx.x; i < gq * D; i += 256) qs[i / D][i % D] = Elem<DT>::get(q, i);
-    __syncthreads();
-    float acc[8];
-#pragma unroll
-    for (int jj = 0; jj < 8; ++jj) acc[jj] = 0.0f;
-#pragma unroll
-    for (int i = 0; i < D / PER; ++i) {
-      const E* e = (const E*)&rv[i];
-#pragma unroll
-      for (int j = 0; j < PER; ++j) {
-        const float x = Elem<DT>::get(e, j);
-#pragma unroll
-        for (int jj = 0; jj < 8; ++jj)
-          if (jj < gq) acc[jj] = fmaf(qs[jj][i * PER + j], x, acc[jj]);
-      }
+    for (int i = 0; i < NV; ++i) rv[i] = *(const uint4*)(row + i * PER);
+    const bool doq = attn && side == 0;
+    if (doq) {
+      const E* qp = (const E*)q + ((size_t)b * g.Hq + (size_t)h * GQ) * D;
+      for (int i = tid; i < GQ * D; i += 256) qs[(i % D) * GQ + i / D] = Elem<DT>::get(qp, i);
     }
-    if (a < k) {
-      float* SK = dw.SK + ((size_t)g.prefKp[b] * g.H + (size_t)h * kp) * gq;
+    if (app && tid < D) xs[tid] = Elem<DT>::get((const E*)(side ? vin : kin) + ((size_t)b * g.H + h) * D, tid);
+    __syncthreads();
+    const size_t ab = (size_t)g.prefKp[b] * g.H + (size_t)h * kp;  // anchor-table row of anchor 0
+    float acc[GQ], s = 0.0f;
 #pragma unroll
-      for (int jj = 0; jj < 8; ++jj)
-        if (jj < gq) SK[(size_t)jj * kp + a] = acc[jj];
+    for (int jj = 0; jj < GQ; ++jj) acc[jj] = 0.0f;
+    if (doq && app) anchor_dots<DT, GQ, true, true>(rv, qs, xs, acc, s);
+    else if (doq) anchor_dots<DT, GQ, true, false>(rv, qs, xs, acc, s);
+    else anchor_dots<DT, GQ, false, true>(rv, qs, xs, acc, s);
+    if (doq && valid) {
+#pragma unroll
+      for (int jj = 0; jj < GQ; ++jj) acc[jj] *= sl2;
+      store_g<GQ>(dw.SK + (ab + a) * GQ, acc);
+    }
+    if (app) {
+      const float* inv = (side ? c.invV : c.invK) + ko;
+      const float sc = valid ? fabsf(s) * inv[a] : -1.0f;
+      if (valid) dw.asc[(size_t)side * g.H * g.prefKp[g.B] + ab + a] = sc;
+      float b1 = sc, b2 = -1.0f;
+      int i1 = valid ? a : 0x7fffffff;
+      top2_wave_dpp(b1, b2, i1);
+      if (lane == 0) {
+        rb1[wave] = b1;
+        rb2[wave] = b2;
+        ri1[wave] = i1;
+      }
+      __syncthreads();
+      if (tid == 0) {
+        for (int v = 1; v < 4; ++v) top2_merge(b1, b2, i1, rb1[v], rb2[v], ri1[v]);
+        const size_t ti = (size_t)side * g.H * g.prefAB[g.B] + (size_t)g.prefAB[b] * g.H + (size_t)h * nab + ch;
+        dw.atop[ti] = make_float4(b1, b2, __int_as_float(i1), 0.0f);
+      }
     }
     return;
   }
-  // ---- key-residual terms of one (request, head), 256 residuals per block
-  idx -= nsc;
-  const int rb = idx % g.maxRB, bh = idx / g.maxRB;
-  const int b = bh / g.H, h = bh % g.H;
-  const int S = g.S[b], G = g.G;
-  const int nw = (S + 63) / 64;
-  const size_t wo = (size_t)g.prefW[b] * g.H + (size_t)h * nw;
-  const int e0 = c.pcK[wo];
-  const int e1 = h + 1 < g.H ? c.pcK[wo + nw] : g.prefNK[b + 1];
-  if (e0 + rb * 256 >= e1) return;
-  // Rotated queries q_rot = FWHT(s * q): one wave per query head.
-  for (int jj = wave; jj < gq; jj += 4) {
-    const E* q = (const E*)qin + ((size_t)b * g.Hq + (size_t)h * gq + jj) * D;
-    float z0 = hsign(g.seed_sign, 2 * lane) * Elem<DT>::get(q, 2 * lane);
-    float z1 = hsign(g.seed_sign, 2 * lane + 1) * Elem<DT>::get(q, 2 * lane + 1);
-    fwht_wave(z0, z1, lane);
-    qs[jj][2 * lane] = z0;
-    qs[jj][2 * lane + 1] = z1;
-  }
-  __syncthreads();
-  const int e = e0 + rb * 256 + threadIdx.x;
-  if (e >= e1) return;
-  const uint4* cp = (const uint4*)(c.codesK + (size_t)e * (D / 4));
+
+  // ---- key-residual terms: one thread per stored key residual (global index e).
+  // q_rot . zhat = sum over coordinate pairs of a table entry indexed by the
+  // pair's 4-bit code (its two levels times the two rotated query values),
+  // scaled by the group scale.
+  idx -= nAK + nAV;
+  const int NKt = g.prefNK[g.B];
+  const int e = idx * 256 + tid;
+  const bool valid = e < NKt;
+  const int ec = min(e, NKt - 1);
+  int b = 0;
+  while (b < g.B - 1 && ec >= g.prefNK[b + 1]) ++b;
+  const int S = g.S[b], G = g.G, nw = (S + 63) / 64;
+  const size_t wb = (size_t)g.prefW[b] * g.H;
+  int h = g.H - 1;
+  while (h > 0 && c.pcK[wb + (size_t)h * nw] > ec) --h;  // head whose residual range holds ec
+  const int bh = b * g.H + h;
+  const uint4* cp = (const uint4*)(c.codesK + (size_t)ec * (D / 4));
   const uint4 c0 = cp[0], c1 = cp[1];
-  const uint32_t cw[8] = {c0.x, c0.y, c0.z, c0.w, c1.x, c1.y, c1.z, c1.w};
   float sg[4];
 #pragma unroll
-  for (int qd = 0; qd < 4; ++qd) sg[qd] = qd < D / G ? c.scalesK[(size_t)e * (D / G) + qd] : 0.0f;
-  float dot[8];
-#pragma unroll
-  for (int jj = 0; jj < 8; ++jj) dot[jj] = 0.0f;
-#pragma unroll
-  for (int qd = 0; qd < 4; ++qd) {  // 32-coordinate quarters lie inside one group (G >= 32)
-    const float s = sg[(qd * 32) / G];
-    const float n1 = -s * AKV_L1, n0 = -s * AKV_L0, p0 = s * AKV_L0, p1 = s * AKV_L1;
-#pragma unroll
-    for (int dd = 0; dd < 32; ++dd) {
-      const int d = qd * 32 + dd;
-      const int code = (cw[d >> 4] >> (2 * (d & 15))) & 3;
-      const float z = scaled_level(code, n1, n0, p0, p1);
-#pragma unroll
-      for (int jj = 0; jj < 8; ++jj)
-        if (jj < gq) dot[jj] = fmaf(qs[jj][d], z, dot[jj]);
+  for (int qd = 0; qd < 4; ++qd) sg[qd] = qd < D / G ? c.scalesK[(size_t)ec * (D / G) + qd] : 0.0f;
+  const int lastv = min(255, NKt - 1 - idx * 256);
+  if (tid == 0) bhr[0] = bh;
+  if (tid == lastv) bhr[1] = bh;
+  __syncthreads();
+  const int lo = bhr[0], hi = bhr[1];
+  const uint32_t cw[8] = {c0.x, c0.y, c0.z, c0.w, c1.x, c1.y, c1.z, c1.w};
+  const float qscale = sl2 * (1.0f / (float)D);
+  const float s0v = sign_bit(g.sgnbits, 2 * lane), s1v = sign_bit(g.sgnbits, 2 * lane + 1);
+  for (int p0 = lo; p0 <= hi; ++p0) {
+    const int b2 = p0 / g.H, h2 = p0 % g.H;
+    for (int jj = wave; jj < GQ; jj += 4) {
+      const E* qp = (const E*)q + ((size_t)b2 * g.Hq + (size_t)h2 * GQ + jj) * D;
+      float z0 = s0v * Elem<DT>::get(qp, 2 * lane), z1 = s1v * Elem<DT>::get(qp, 2 * lane + 1);
+      fwht_wave_dpp(z0, z1, lane);
+      qs[(2 * lane) * GQ + jj] = z0 * qscale;
+      qs[(2 * lane + 1) * GQ + jj] = z1 * qscale;
     }
-  }
-  const float invD = 1.0f / (float)D;
+    __syncthreads();
+    {  // table: thread = (pair t/4, nibbles 4 (t%4) .. +3)
+      const int pr = tid >> 2, n0 = 4 * (tid & 3);
+      float qa[GQ], qb[GQ];
+      load_g<GQ>(&qs[(2 * pr) * GQ], qa);
+      load_g<GQ>(&qs[(2 * pr + 1) * GQ], qb);
 #pragma unroll
-  for (int jj = 0; jj < 8; ++jj)
-    if (jj < gq) dw.RK[(size_t)e * gq + jj] = dot[jj] * invD;
+      for (int u = 0; u < 4; ++u) {
+        const int nib = n0 + u;
+        const float la = level(nib & 3), lb = level(nib >> 2);
+        float t[GQ];
+#pragma unroll
+        for (int jj = 0; jj < GQ; ++jj) t[jj] = fmaf(lb, qb[jj], la * qa[jj]);
+        store_g<GQ>(&tab[(pr * 16 + nib) * GQ], t);
+      }
+    }
+    __syncthreads();
+    if (valid && bh == p0) {
+      float dot[GQ];
+#pragma unroll
+      for (int jj = 0; jj < GQ; ++jj) dot[jj] = 0.0f;
+#pragma unroll
+      for (int qd = 0; qd < 4; ++qd) {  // 32-coordinate quarters lie inside one group (G >= 32)
+        float part[GQ];
+#pragma unroll
+        for (int jj = 0; jj < GQ; ++jj) part[jj] = 0.0f;
+#pragma unroll
+        for (int n = 0; n < 16; ++n) {
+          const int pr = qd * 16 + n;
+          const int nib = (cw[pr >> 3] >> (4 * (pr & 7))) & 15;
+          float t[GQ];
+          load_g<GQ>(&tab[(pr * 16 + nib) * GQ], t);
+#pragma unroll
+          for (int jj = 0; jj < GQ; ++jj) part[jj] += t[jj];
+        }
+        const float sq = sg[(qd * 32) / G];
+#pragma unroll
+        for (int jj = 0; jj < GQ; ++jj) dot[jj] = fmaf(sq, part[jj], dot[jj]);
+      }
+      store_g<GQ>(dw.RK + (size_t)e * GQ, dot);
+    }
+    __syncthreads();
+  }
 }
 
-// ------------------------------------------------------------------ D2
+// ------------------------------------------------------------------ append resolution
+// Resolves the appended token of (request b, head h, side) from the screening
+// scores of k_dec_front: the best anchor by |cos| is certified when its margin
+// over the runner-up exceeds the fp32 error bound; otherwise every anchor
+// within the bound is rescored with the canonical fp64 formula (ties to the
+// lowest index).  The coefficient is the canonical fp64 projection rounded to
+// the stored dtype.  Whole-block call; the record goes to tail slot n_app and
+// to *out_idx / *out_gamma (LDS).
+template <int DT>
+__device__ void append_resolve(const Geo& g, const Cache& c, const DecWs& dw, int b, int h, int side, int n_app,
+                               const void* xin, float* fr, double* dr, int* ir, int* out_idx, float* out_gamma) {
+  using E = typename Elem<DT>::T;
+  constexpr int D = AKV_D;
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int k = g.k[b], kp = (k + 3) & ~3, nab = (k + 255) / 256;
+  const size_t ko = (size_t)g.prefK[b] * g.H + (size_t)h * k;
+  const size_t ab = (size_t)g.prefKp[b] * g.H + (size_t)h * kp;
+  const E* x = (const E*)xin + ((size_t)b * g.H + h) * D;
+  const E* A = (const E*)(side ? c.ancV : c.ancK) + ko * D;
+  const double* nrm = (side ? c.nrmV : c.nrmK) + ko;
+  const float* sc = dw.asc + (size_t)side * g.H * g.prefKp[g.B] + ab;
+  if (wave == 0) {
+    const float x0 = Elem<DT>::get(x, 2 * lane), x1 = Elem<DT>::get(x, 2 * lane + 1);
+    const float ss = wave_sum(x0 * x0 + x1 * x1);
+    const float xn = sqrtf(ss) * (1.0f + 1e-5f);
+    float b1 = -1.0f, b2 = -1.0f;
+    int i1 = 0x7fffffff;
+    if (lane < nab) {
+      const float4 t =
+          dw.atop[(size_t)side * g.H * g.prefAB[g.B] + (size_t)g.prefAB[b] * g.H + (size_t)h * nab + lane];
+      b1 = t.x;
+      b2 = t.y;
+      i1 = __float_as_int(t.z);
+    }
+    top2_wave(b1, b2, i1);
+    if (lane == 0) {
+      fr[0] = b1;
+      fr[1] = b2;
+      fr[2] = xn * ((float)D * 1.1920929e-7f + 2.3841858e-7f) * 1.01f + 1e-30f;
+      ir[0] = i1;
+    }
+  }
+  __syncthreads();
+  const float b1 = fr[0], b2 = fr[1], eps = fr[2];
+  int best = ir[0];
+  if (!(b1 - b2 > 2.0f * eps + b1 * 9.094947e-13f)) {
+    const float band = b1 - 2.0f * eps - b1 * 9.094947e-13f;
+    double bc = -INFINITY;
+    int bi = 0x7fffffff;
+    for (int a = tid; a < k; a += 256) {
+      if (sc[a] < band) continue;
+      const double d = dot64_seq<DT>(x, A + (size_t)a * D, D);
+      const double cc = nrm[a] > 0.0 ? (d * d) / nrm[a] : -1.0;
+      if (cc > bc) {
+        bc = cc;
+        bi = a;
+      }
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      const double oc = __shfl_xor(bc, o, 64);
+      const int oi = __shfl_xor(bi, o, 64);
+      if (oc > bc || (oc == bc && oi < bi)) {
+        bc = oc;
+        bi = oi;
+      }
+    }
+    if (lane == 0) {
+      dr[wave] = bc;
+      ir[1 + wave] = bi;
+    }
+    __syncthreads();
+    bc = dr[0];
+    bi = ir[1];
+    for (int v = 1; v < 4; ++v)
+      if (dr[v] > bc || (dr[v] == bc && ir[1 + v] < bi)) {
+        bc = dr[v];
+        bi = ir[1 + v];
+      }
+    best = bi;
+  }
+  if (tid == 0) {
+    const double n = nrm[best];
+    const double d = dot64_seq<DT>(x, A + (size_t)best * D, D);
+    const double g64 = n > 0.0 ? d / n : 0.0;
+    const float gb = Elem<DT>::round_coef((float)g64);
+    const size_t ti = ((size_t)b * g.H + h) * g.max_append + n_app;
+    (side ? c.tidxV : c.tidxK)[ti] = (uint16_t)best;
+    Elem<DT>::put(side ? c.tgV : c.tgK, ti, gb);
+    *out_idx = best;
+    *out_gamma = gb;
+  }
+  __syncthreads();
+}
+
+template <int DT>
+__global__ __launch_bounds__(256) void k_app_finish(Geo g, Cache c, DecWs dw, int n_app, const void* kin,
+                                                    const void* vin) {
+  __shared__ float fr[4];
+  __shared__ double dr[4];
+  __shared__ int ir[5];
+  __shared__ int oi;
+  __shared__ float og;
+  const int side = blockIdx.x & 1, bh = blockIdx.x >> 1;
+  append_resolve<DT>(g, c, dw, bh / g.H, bh % g.H, side, n_app, side ? vin : kin, fr, dr, ir, &oi, &og);
+}
+
+// ------------------------------------------------------------------ stream
 // R uint16 values starting at p (R * 2 bytes, 8-byte aligned).
 template <int R>
 __device__ inline void load_u16(const uint16_t* p, uint16_t* v) {
@@ -182,29 +445,41 @@ __device__ inline void load_coef(const void* base, size_t i0, float* v) {
 }
 __device__ inline unsigned long long low_bits(int n) { return n >= 64 ? ~0ull : ((1ull << n) - 1ull); }
 
-constexpr int DEC_ASTG = 64;   // value-anchor rows staged in LDS per split
-constexpr int DEC_RCW = 512;   // anchor window of the per-anchor value weights
-constexpr int DEC_VCH = 128;   // value residuals staged per chunk
-
+// Grid: nst split workgroups, then, when a token is appended in this step
+// (kin != nullptr), one workgroup per (request, head, side) that resolves it
+// into tail slot n_app while the splits stream.
 template <int DT, int GQ, int R>
-__global__ __launch_bounds__(256) void k_dec_stream(Geo g, Cache c, DecWs dw, float scale) {
+__global__ __launch_bounds__(256) void k_dec_stream(Geo g, Cache c, DecWs dw, int nst, int n_app, const void* kin,
+                                                    const void* vin) {
   using E = typename Elem<DT>::T;
   constexpr int D = AKV_D, L = 256 * R, PER = 16 / sizeof(E);
   constexpr int NAV = DEC_ASTG * D / PER / 256;
-  constexpr int NY = (GQ * D + 255) / 256;  // outputs per thread
-  constexpr int JG = GQ < 4 ? GQ : 4;       // query heads covered by the 4 thread groups
-  extern __shared__ __align__(16) unsigned char smem[];
-  __shared__ float wacc[GQ][DEC_RCW];
-  __shared__ __align__(16) E avs[DEC_ASTG * D];
+  // LDS pool: per-anchor weights and staged value-anchor rows, later reused for
+  // the per-wave output partials.
+  constexpr int WACC_B = DEC_RCW * GQ * 4, AVS_B = DEC_ASTG * D * (int)sizeof(E), ZY_B = 2 * 4 * GQ * D * 4;
+  constexpr int POOL_B = WACC_B + AVS_B > ZY_B ? WACC_B + AVS_B : ZY_B;
+  __shared__ __align__(16) unsigned char pool[POOL_B];
+  float(*wacc)[GQ] = (float(*)[GQ])pool;
+  E* avs = (E*)(pool + WACC_B);
   __shared__ __align__(16) uint32_t vcode[DEC_VCH][8];
   __shared__ float vsc[DEC_VCH][4];
-  __shared__ float vp[DEC_VCH][GQ];
-  __shared__ float red[4][GQ];
-  __shared__ float mfin[GQ];
+  __shared__ __align__(16) float vp[DEC_VCH][GQ];
+  __shared__ float redm[4][GQ], reds[4][GQ];
+  __shared__ float2 lvl2[16];  // levels of a coordinate pair by its 4-bit code
 
+  if ((int)blockIdx.x >= nst) {
+    __shared__ float fr[4];
+    __shared__ double dr[4];
+    __shared__ int ir[5];
+    __shared__ int oi;
+    __shared__ float og;
+    const int r = blockIdx.x - nst, side = r & 1, bh = r >> 1;
+    append_resolve<DT>(g, c, dw, bh / g.H, bh % g.H, side, n_app, side ? vin : kin, fr, dr, ir, &oi, &og);
+    return;
+  }
   // Logical block id: consecutive ids (the splits of one head) share an XCD.
   int id = blockIdx.x;
-  const int n8 = gridDim.x & ~7;
+  const int n8 = nst & ~7;
   if (id < n8) id = (id & 7) * (n8 >> 3) + (id >> 3);
   const int b = locate(g, L, 1, id);
   const int S = g.S[b], k = g.k[b], G = g.G, kp = (k + 3) & ~3;
@@ -215,13 +490,13 @@ __global__ __launch_bounds__(256) void k_dec_stream(Geo g, Cache c, DecWs dw, fl
   const size_t so = slot_base(g, b, h);
   const size_t wo = (size_t)g.prefW[b] * g.H + (size_t)h * nw;
   const size_t ko = (size_t)g.prefK[b] * g.H + (size_t)h * k;
-  const int kpm = (g.maxK + 3) & ~3;
-  float* SKs = (float*)smem;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const float* SKg = dw.SK + ((size_t)g.prefKp[b] * g.H + (size_t)h * kp) * GQ;
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const float* SKh = dw.SK + ((size_t)g.prefKp[b] * g.H + (size_t)h * kp) * GQ;
   const E* AVg = (const E*)c.ancV + ko * D;
+  for (int i = tid; i < GQ * DEC_RCW; i += 256) (&wacc[0][0])[i] = 0.0f;
+  if (tid < 16) lvl2[tid] = make_float2(level(tid & 3), level(tid >> 2));
 
-  // ---- round 1: records, flag words, the split's residual ranges, the score table.
+  // ---- round 1: records, flag words, the split's anchor and residual ranges.
   const int i0 = s0 + tid * R;
   const bool any = i0 < s1;
   uint16_t ik[R], iv[R];
@@ -250,26 +525,11 @@ __global__ __launch_bounds__(256) void k_dec_stream(Geo g, Cache c, DecWs dw, fl
   const int pv_lo = c.pcV[wo + (s0 >> 6)];
   const int w1 = (s1 - 1) >> 6;
   const int pv_hi = c.pcV[wo + w1] + __popcll(c.maskV[wo + w1] & low_bits(s1 - 64 * w1));
-  if (g.dsk_lds) {
-    const int n4 = GQ * kp / 4;
-    for (int i = tid; i < n4; i += 4 * 256) {
-      float4 t[4];
-#pragma unroll
-      for (int u = 0; u < 4; ++u)
-        if (i + u * 256 < n4) t[u] = *(const float4*)(SKg + 4 * (size_t)(i + u * 256));
-#pragma unroll
-      for (int u = 0; u < 4; ++u)
-        if (i + u * 256 < n4) {
-          const int f = 4 * (i + u * 256);
-          *(float4*)(&SKs[(f / kp) * kpm + (f % kp)]) = t[u];
-        }
-    }
-  }
   const int nrange = a_hi - a_lo + 1;
   const int nstage = min(nrange, DEC_ASTG);
   const int nvres = pv_hi - pv_lo;
 
-  // ---- round 2: key-residual terms, value-anchor rows, first value-residual chunk.
+  // ---- round 2: anchor scores, key-residual terms, value-anchor rows, first value-residual chunk.
   const int sh = i0 & 63;
   uint32_t vmask = 0;
 #pragma unroll
@@ -279,12 +539,16 @@ __global__ __launch_bounds__(256) void k_dec_stream(Geo g, Cache c, DecWs dw, fl
   const uint32_t bv = any ? ((uint32_t)(wv >> sh) & vmask) : 0u;
   pck += __popcll(wk & low_bits(sh));
   pcv += __popcll(wv & low_bits(sh));
-  float rk[R][GQ];
+  float lg[R][GQ], rk[R][GQ];
 #pragma unroll
   for (int r = 0; r < R; ++r) {
-    const int ri = pck + __popc(bk & ((1u << r) - 1u));
+    load_g<GQ>(SKh + (size_t)min((int)ik[r], k - 1) * GQ, lg[r]);
+    if ((bk >> r) & 1u) {
+      load_g<GQ>(dw.RK + (size_t)(pck + __popc(bk & ((1u << r) - 1u))) * GQ, rk[r]);
+    } else {
 #pragma unroll
-    for (int jj = 0; jj < GQ; ++jj) rk[r][jj] = ((bk >> r) & 1u) ? dw.RK[(size_t)ri * GQ + jj] : 0.0f;
+      for (int jj = 0; jj < GQ; ++jj) rk[r][jj] = 0.0f;
+    }
   }
   uint4 avr[NAV];
 #pragma unroll
@@ -302,48 +566,40 @@ __global__ __launch_bounds__(256) void k_dec_stream(Geo g, Cache c, DecWs dw, fl
     const int f = tid + 256 * u;
     vsr[u] = f < nv0 * (D / G) ? c.scalesV[(size_t)pv_lo * (D / G) + f] : 0.0f;
   }
-  __syncthreads();
 
-  // ---- logits.
-  float lg[R][GQ];
+  // ---- logits and the split's softmax statistics.
 #pragma unroll
-  for (int r = 0; r < R; ++r) {
-    const int a = min((int)ik[r], k - 1);
+  for (int r = 0; r < R; ++r)
 #pragma unroll
-    for (int jj = 0; jj < GQ; ++jj) {
-      const float s = g.dsk_lds ? SKs[jj * kpm + a] : SKg[(size_t)jj * kp + a];
-      lg[r][jj] = (gk[r] * s + rk[r][jj]) * scale;
-    }
-  }
-  // ---- softmax statistics of the split.
+    for (int jj = 0; jj < GQ; ++jj) lg[r][jj] = fmaf(gk[r], lg[r][jj], rk[r][jj]);
+  float mj[GQ];
 #pragma unroll
   for (int jj = 0; jj < GQ; ++jj) {
     float v = -INFINITY;
 #pragma unroll
     for (int r = 0; r < R; ++r)
       if ((vmask >> r) & 1u) v = fmaxf(v, lg[r][jj]);
-    v = wave_max(v);
-    if (lane == 0) red[wave][jj] = v;
+    v = wave_max_dpp(v);
+    if (lane == 0) redm[wave][jj] = v;
   }
   __syncthreads();
-  if (tid < GQ) mfin[tid] = fmaxf(fmaxf(red[0][tid], red[1][tid]), fmaxf(red[2][tid], red[3][tid]));
-  __syncthreads();
+#pragma unroll
+  for (int jj = 0; jj < GQ; ++jj) mj[jj] = fmaxf(fmaxf(redm[0][jj], redm[1][jj]), fmaxf(redm[2][jj], redm[3][jj]));
   float ls[GQ];
 #pragma unroll
   for (int jj = 0; jj < GQ; ++jj) {
-    const float m = mfin[jj];
     ls[jj] = 0.0f;
 #pragma unroll
     for (int r = 0; r < R; ++r) {
-      const float p = ((vmask >> r) & 1u) ? __expf(lg[r][jj] - m) : 0.0f;
+      const float p = ((vmask >> r) & 1u) ? __builtin_amdgcn_exp2f(lg[r][jj] - mj[jj]) : 0.0f;
       lg[r][jj] = p;
       ls[jj] += p;
     }
   }
 #pragma unroll
   for (int jj = 0; jj < GQ; ++jj) {
-    const float v = wave_sum(ls[jj]);
-    if (lane == 0) red[wave][jj] = v;
+    const float v = wave_sum_dpp(ls[jj]);
+    if (lane == 0) reds[wave][jj] = v;
   }
   // Stage the value-anchor rows and the first value-residual chunk.
 #pragma unroll
@@ -359,17 +615,29 @@ __global__ __launch_bounds__(256) void k_dec_stream(Geo g, Cache c, DecWs dw, fl
     if (f < nv0 * (D / G)) vsc[f / (D / G)][f % (D / G)] = vsr[u];
   }
 
-  // ---- value residuals: thread (coordinate pair, query head) accumulates over
-  // the split's stored value residuals, staged DEC_VCH at a time.
-  const int pair = tid & 63, jg = tid >> 6;
-  const int grp = (2 * pair) / G;
-  float za[2][2] = {{0.0f, 0.0f}, {0.0f, 0.0f}};
+  // ---- value residuals: lane = coordinate pair, wave = every 4th residual,
+  // all query heads at once; staged DEC_VCH residuals at a time.
+  const int grp = (2 * lane) / G;
+  const int nsh = 4 * (lane & 7);
+  float za[GQ][2];
+#pragma unroll
+  for (int jj = 0; jj < GQ; ++jj) za[jj][0] = za[jj][1] = 0.0f;
+  auto vres_acc = [&](uint32_t word, float sgv, const float* pv) {
+    const float2 lv = lvl2[(word >> nsh) & 15];
+    const float z0 = sgv * lv.x, z1 = sgv * lv.y;
+#pragma unroll
+    for (int jj = 0; jj < GQ; ++jj) {
+      za[jj][0] = fmaf(pv[jj], z0, za[jj][0]);
+      za[jj][1] = fmaf(pv[jj], z1, za[jj][1]);
+    }
+  };
   for (int cb = 0; cb < nvres; cb += DEC_VCH) {
     const int nv = min(DEC_VCH, nvres - cb);
     if (cb > 0) {
       __syncthreads();
-      if (tid < 2 * nv) *(uint4*)(&vcode[tid >> 1][4 * (tid & 1)]) =
-          ((const uint4*)(c.codesV + (size_t)(pv_lo + cb + (tid >> 1)) * (D / 4)))[tid & 1];
+      if (tid < 2 * nv)
+        *(uint4*)(&vcode[tid >> 1][4 * (tid & 1)]) =
+            ((const uint4*)(c.codesV + (size_t)(pv_lo + cb + (tid >> 1)) * (D / 4)))[tid & 1];
       for (int f = tid; f < nv * (D / G); f += 256)
         vsc[f / (D / G)][f % (D / G)] = c.scalesV[(size_t)(pv_lo + cb) * (D / G) + f];
     }
@@ -378,291 +646,268 @@ __global__ __launch_bounds__(256) void k_dec_stream(Geo g, Cache c, DecWs dw, fl
     for (int r = 0; r < R; ++r)
       if ((bv >> r) & 1u) {
         const int li = pcv + __popc(bv & ((1u << r) - 1u)) - pv_lo - cb;
-        if (li >= 0 && li < nv) {
-#pragma unroll
-          for (int jj = 0; jj < GQ; ++jj) vp[li][jj] = lg[r][jj];
-        }
+        if (li >= 0 && li < nv) store_g<GQ>(&vp[li][0], lg[r]);
       }
     __syncthreads();
-    if (jg < JG) {
-      for (int e = 0; e < nv; ++e) {
-        const uint32_t word = vcode[e][pair >> 3];
-        const int nib = (word >> (4 * (pair & 7))) & 15;
-        const float sg = vsc[e][grp];
-        const float z0 = sg * level(nib & 3), z1 = sg * level(nib >> 2);
+    int e = wave;
+    for (; e + 12 < nv; e += 16) {
+      uint32_t wd[4];
+      float sg4[4], pv[4][GQ];
 #pragma unroll
-        for (int u = 0; u < 2; ++u) {
-          const int jj = jg + 4 * u;
-          if (jj < GQ) {
-            const float p = vp[e][jj];
-            za[u][0] = fmaf(p, z0, za[u][0]);
-            za[u][1] = fmaf(p, z1, za[u][1]);
-          }
-        }
+      for (int u = 0; u < 4; ++u) {
+        wd[u] = vcode[e + 4 * u][lane >> 3];
+        sg4[u] = vsc[e + 4 * u][grp];
+        load_g<GQ>(&vp[e + 4 * u][0], pv[u]);
       }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) vres_acc(wd[u], sg4[u], pv[u]);
+    }
+    for (; e < nv; e += 4) {
+      float pv[GQ];
+      load_g<GQ>(&vp[e][0], pv);
+      vres_acc(vcode[e][lane >> 3], vsc[e][grp], pv);
     }
   }
 
   // ---- per-anchor value weights over anchor windows, and y = sum_a w_a abar^V_a.
-  float y[NY];
+  float ya[GQ][2];
 #pragma unroll
-  for (int u = 0; u < NY; ++u) y[u] = 0.0f;
+  for (int jj = 0; jj < GQ; ++jj) ya[jj][0] = ya[jj][1] = 0.0f;
+  // Value-anchor row ra of the split, coordinates 2 lane and 2 lane + 1: from
+  // LDS for the first DEC_ASTG rows, else from global memory.
+  auto vpair = [&](const E* p, float& v0, float& v1) {
+    if constexpr (DT == 1) {
+      const uint32_t t = *(const uint32_t*)(p + 2 * lane);
+      v0 = bf2f((uint16_t)(t & 0xffffu));
+      v1 = bf2f((uint16_t)(t >> 16));
+    } else {
+      const float2 t = *(const float2*)(p + 2 * lane);
+      v0 = t.x;
+      v1 = t.y;
+    }
+  };
   for (int wb = 0; wb < nrange; wb += DEC_RCW) {
     const int wn = min(DEC_RCW, nrange - wb);
-    __syncthreads();
-    for (int i = tid; i < GQ * DEC_RCW; i += 256) (&wacc[0][0])[i] = 0.0f;
-    __syncthreads();
+    if (wb > 0) {  // the first window was cleared at the start
+      __syncthreads();
+      for (int i = tid; i < GQ * DEC_RCW; i += 256) (&wacc[0][0])[i] = 0.0f;
+      __syncthreads();
+    }
     {
-      int cur = -1;
-      float run[GQ];
+      // A thread's valid slots are a prefix of its R slots, sorted by value
+      // anchor: a run of the first anchor aF, a run of the last anchor aL, and
+      // only when an anchor holds fewer slots than a thread, anchors between
+      // them (one atomic per such slot).
+      const int nval = __popc(vmask);
+      int aL = iv[0];
 #pragma unroll
-      for (int jj = 0; jj < GQ; ++jj) run[jj] = 0.0f;
+      for (int r = 1; r < R; ++r)
+        if (r < nval) aL = iv[r];
+      const int aF = iv[0];
+      float rf[GQ], rl[GQ];
+#pragma unroll
+      for (int jj = 0; jj < GQ; ++jj) rf[jj] = rl[jj] = 0.0f;
+      bool mid = false;
 #pragma unroll
       for (int r = 0; r < R; ++r) {
-        const int off = (int)iv[r] - a_lo - wb;
-        const bool in = ((vmask >> r) & 1u) && off >= 0 && off < wn;
-        if (in && off != cur) {
-          if (cur >= 0) {
+        const bool v = r < nval;
+        const bool isF = v && (int)iv[r] == aF, isL = v && !isF && (int)iv[r] == aL;
+        mid |= v && !isF && !isL;
+        const float wF = isF ? gv[r] : 0.0f, wL = isL ? gv[r] : 0.0f;
 #pragma unroll
-            for (int jj = 0; jj < GQ; ++jj)
-              if (run[jj] != 0.0f) atomicAdd(&wacc[jj][cur], run[jj]);
-          }
-#pragma unroll
-          for (int jj = 0; jj < GQ; ++jj) run[jj] = 0.0f;
-          cur = off;
-        }
-        if (in) {
-#pragma unroll
-          for (int jj = 0; jj < GQ; ++jj) run[jj] = fmaf(lg[r][jj], gv[r], run[jj]);
+        for (int jj = 0; jj < GQ; ++jj) {
+          rf[jj] = fmaf(lg[r][jj], wF, rf[jj]);
+          rl[jj] = fmaf(lg[r][jj], wL, rl[jj]);
         }
       }
-      if (cur >= 0) {
+      const int oF = aF - a_lo - wb, oL = aL - a_lo - wb;
+      if (nval > 0 && oF >= 0 && oF < wn) {
 #pragma unroll
-        for (int jj = 0; jj < GQ; ++jj)
-          if (run[jj] != 0.0f) atomicAdd(&wacc[jj][cur], run[jj]);
+        for (int jj = 0; jj < GQ; ++jj) atomicAdd(&wacc[oF][jj], rf[jj]);
+      }
+      if (nval > 0 && aL != aF && oL >= 0 && oL < wn) {
+#pragma unroll
+        for (int jj = 0; jj < GQ; ++jj) atomicAdd(&wacc[oL][jj], rl[jj]);
+      }
+      if (mid) {
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+          const int o = (int)iv[r] - a_lo - wb;
+          if (r < nval && (int)iv[r] != aF && (int)iv[r] != aL && o >= 0 && o < wn) {
+#pragma unroll
+            for (int jj = 0; jj < GQ; ++jj) atomicAdd(&wacc[o][jj], lg[r][jj] * gv[r]);
+          }
+        }
       }
     }
     __syncthreads();
+    auto yacc = [&](float v0, float v1, const float* w) {
 #pragma unroll
-    for (int u = 0; u < NY; ++u) {
-      const int p = tid + 256 * u;
-      if (p < GQ * D) {
-        const int jj = p / D, d = p % D;
-        float acc = y[u];
-        for (int a = 0; a < wn; ++a) {
-          const int ra = wb + a;
-          const float av = ra < nstage ? Elem<DT>::get(avs, (size_t)ra * D + d)
-                                       : Elem<DT>::get(AVg, (size_t)(a_lo + ra) * D + d);
-          acc = fmaf(wacc[jj][a], av, acc);
-        }
-        y[u] = acc;
+      for (int jj = 0; jj < GQ; ++jj) {
+        ya[jj][0] = fmaf(w[jj], v0, ya[jj][0]);
+        ya[jj][1] = fmaf(w[jj], v1, ya[jj][1]);
       }
+    };
+    const int wl = max(0, min(wn, nstage - wb));  // rows of this window staged in LDS
+    int a = wave;
+    for (; a + 12 < wl; a += 16) {
+      float v0[4], v1[4], w[4][GQ];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        vpair(avs + (size_t)(wb + a + 4 * u) * D, v0[u], v1[u]);
+        load_g<GQ>(&wacc[a + 4 * u][0], w[u]);
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) yacc(v0[u], v1[u], w[u]);
+    }
+    for (; a < wl; a += 4) {
+      float v0, v1, w[GQ];
+      vpair(avs + (size_t)(wb + a) * D, v0, v1);
+      load_g<GQ>(&wacc[a][0], w);
+      yacc(v0, v1, w);
+    }
+    for (; a < wn; a += 4) {  // rows past the staged ones
+      float v0, v1, w[GQ];
+      vpair(AVg + (size_t)(a_lo + wb + a) * D, v0, v1);
+      load_g<GQ>(&wacc[a][0], w);
+      yacc(v0, v1, w);
     }
   }
 
-  // ---- partial outputs.
-  const int Hq = g.Hq;
+  // ---- split output: o = y + s * FWHT(zacc) / D per query head.
+  __syncthreads();  // the pool now holds the per-wave partials
+  float(*zp)[GQ][D] = (float(*)[GQ][D])pool;
+  float(*yp)[GQ][D] = (float(*)[GQ][D])(pool + 4 * GQ * D * 4);
 #pragma unroll
-  for (int u = 0; u < NY; ++u) {
-    const int p = tid + 256 * u;
-    if (p < GQ * D) {
-      const int jj = p / D, d = p % D;
-      const size_t pi = ((size_t)(g.prefSp[b] * Hq + (h * GQ + jj) * nsp + sp)) * (2 + 2 * D);
-      if (d == 0) {
-        dw.part[pi] = mfin[jj];
-        dw.part[pi + 1] = red[0][jj] + red[1][jj] + red[2][jj] + red[3][jj];
-      }
-      dw.part[pi + 2 + d] = y[u];
-    }
+  for (int jj = 0; jj < GQ; ++jj) {
+    *(float2*)&zp[wave][jj][2 * lane] = make_float2(za[jj][0], za[jj][1]);
+    *(float2*)&yp[wave][jj][2 * lane] = make_float2(ya[jj][0], ya[jj][1]);
   }
-  if (jg < JG) {
+  __syncthreads();
+  const int Hq = g.Hq;
+  const float s0v = sign_bit(g.sgnbits, 2 * lane), s1v = sign_bit(g.sgnbits, 2 * lane + 1);
+  const float invD = 1.0f / (float)D;
+  for (int jj = wave; jj < GQ; jj += 4) {
+    float z0 = 0.0f, z1 = 0.0f, y0 = 0.0f, y1 = 0.0f;
 #pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      const int jj = jg + 4 * u;
-      if (jj < GQ) {
-        const size_t pi = ((size_t)(g.prefSp[b] * Hq + (h * GQ + jj) * nsp + sp)) * (2 + 2 * D);
-        dw.part[pi + 2 + D + 2 * pair] = za[u][0];
-        dw.part[pi + 2 + D + 2 * pair + 1] = za[u][1];
-      }
+    for (int w = 0; w < 4; ++w) {
+      z0 += zp[w][jj][2 * lane];
+      z1 += zp[w][jj][2 * lane + 1];
+      y0 += yp[w][jj][2 * lane];
+      y1 += yp[w][jj][2 * lane + 1];
     }
+    fwht_wave_dpp(z0, z1, lane);
+    const float o0 = y0 + s0v * (z0 * invD), o1 = y1 + s1v * (z1 * invD);
+    float* pr = dw.part + ((size_t)g.prefSp[b] * Hq + (size_t)(h * GQ + jj) * nsp + sp) * PS;
+    if (lane == 0) {
+      pr[0] = fmaxf(fmaxf(redm[0][jj], redm[1][jj]), fmaxf(redm[2][jj], redm[3][jj]));
+      pr[1] = reds[0][jj] + reds[1][jj] + reds[2][jj] + reds[3][jj];
+    }
+    *(float2*)&pr[4 + 2 * lane] = make_float2(o0, o1);
   }
 }
 
-// ------------------------------------------------------------------ D3
-template <int DT>
-__global__ __launch_bounds__(256) void k_dec_combine(Geo g, Cache c, DecWs dw, float scale, int n_app, void* out,
-                                                     int out_dtype) {
+// ------------------------------------------------------------------ merge
+// One workgroup per (request, query head): merges its split records and the
+// appended tail tokens, which carry no residual (logit = scale * gamma^K
+// (q . abar^K_a), value gamma^V abar^V_a).  Thread t owns output coordinates
+// 4 (t % 32) .. +3 of every 8th split / tail token (group t / 32); the groups
+// are summed through LDS at the end.
+template <int DT, int GQ>
+__global__ __launch_bounds__(256) void k_dec_merge(Geo g, Cache c, DecWs dw, int ntail, void* out, int out_dtype) {
   using E = typename Elem<DT>::T;
   constexpr int D = AKV_D;
-  __shared__ float zb[D];
-  __shared__ float yb[D];
-  __shared__ float rmax[4], rsum[4];
-  const int b = blockIdx.x / g.Hq, jq = blockIdx.x % g.Hq;
-  const int h = jq / g.g, jj = jq % g.g;
+  __shared__ float wsp[256];
+  __shared__ int tav[256];
+  __shared__ float red[4];
+  __shared__ __align__(16) float acc[8][D];
+  const int b = blockIdx.x / g.Hq, jq = blockIdx.x % g.Hq, h = jq / GQ, jj = jq % GQ;
   const int S = g.S[b], k = g.k[b], kp = (k + 3) & ~3;
-  const int L = g.dsplit;
-  const int nsp = (S + L - 1) / L;
+  const int nsp = (S + g.dsplit - 1) / g.dsplit;
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int cq = tid & 31, sg = tid >> 5;
   const size_t ko = (size_t)g.prefK[b] * g.H + (size_t)h * k;
-  const size_t pb = (size_t)(g.prefSp[b] * g.Hq + jq * nsp) * (2 + 2 * D);
-  const float* part = dw.part + pb;
+  const float* SKh = dw.SK + ((size_t)g.prefKp[b] * g.H + (size_t)h * kp) * GQ;
+  const E* AVg = (const E*)c.ancV + ko * D;
   const size_t tb = ((size_t)b * g.H + h) * g.max_append;
-  const float* SK = dw.SK + ((size_t)g.prefKp[b] * g.H + (size_t)h * kp) * g.g + (size_t)jj * kp;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  // Global max over the splits and the appended tokens.
+  const float* pb = dw.part + ((size_t)g.prefSp[b] * g.Hq + (size_t)jq * nsp) * PS;
+  auto tail_logit = [&](int n) {
+    const int ak = min((int)c.tidxK[tb + n], k - 1);
+    return Elem<DT>::get(c.tgK, tb + n) * SKh[(size_t)ak * GQ + jj];
+  };
+  // Global max over the splits and the tail.
   float M = -INFINITY;
-  for (int s = tid; s < nsp; s += 256) M = fmaxf(M, part[(size_t)s * (2 + 2 * D)]);
-  for (int n = tid; n < n_app; n += 256)
-    M = fmaxf(M, scale * (Elem<DT>::get(c.tgK, tb + n) * SK[min((int)c.tidxK[tb + n], k - 1)]));
-  M = wave_max(M);
-  if (lane == 0) rmax[wave] = M;
+  for (int s = tid; s < nsp; s += 256) M = fmaxf(M, pb[(size_t)s * PS]);
+  for (int n = tid; n < ntail; n += 256) M = fmaxf(M, tail_logit(n));
+  M = wave_max_dpp(M);
+  if (lane == 0) red[wave] = M;
   __syncthreads();
-  M = fmaxf(fmaxf(rmax[0], rmax[1]), fmaxf(rmax[2], rmax[3]));
+  M = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
   float l = 0.0f;
-  for (int s = tid; s < nsp; s += 256) {
-    const float* pp = part + (size_t)s * (2 + 2 * D);
-    l += __expf(pp[0] - M) * pp[1];
-  }
-  // Each thread owns one output: y[d] (threads 0..127) or zacc[d] (128..255).
-  float acc = 0.0f;
-  int s = 0;
-  for (; s + 8 <= nsp; s += 8) {
-    float mv[8], vv[8];
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const float* pp = part + (size_t)(s + u) * (2 + 2 * D);
-      mv[u] = pp[0];
-      vv[u] = pp[2 + tid];
-    }
-#pragma unroll
-    for (int u = 0; u < 8; ++u) acc = fmaf(__expf(mv[u] - M), vv[u], acc);
-  }
-  for (; s < nsp; ++s) {
-    const float* pp = part + (size_t)s * (2 + 2 * D);
-    acc = fmaf(__expf(pp[0] - M), pp[2 + tid], acc);
-  }
-  // Appended tokens: encoded against the anchors, no residual.
-  const E* AV = (const E*)c.ancV + ko * D;
-  for (int n = 0; n < n_app; ++n) {
-    const float lgt = scale * (Elem<DT>::get(c.tgK, tb + n) * SK[min((int)c.tidxK[tb + n], k - 1)]);
-    const float p = __expf(lgt - M);
-    if (tid == 0) l += p;
-    if (tid < D) {
-      const int av = min((int)c.tidxV[tb + n], k - 1);
-      acc = fmaf(p * Elem<DT>::get(c.tgV, tb + n), Elem<DT>::get(AV, (size_t)av * D + tid), acc);
-    }
-  }
-  l = wave_sum(l);
-  if (lane == 0) rsum[wave] = l;
-  if (tid < D) yb[tid] = acc; else zb[tid - D] = acc;
-  // Inverse rotation of the value-residual sum: s * FWHT(z) / D.
-  for (int hh = 1; hh < D; hh <<= 1) {
-    __syncthreads();
-    float v = 0.0f;
-    if (tid < D) {
-      const float x0 = zb[tid & ~hh], x1 = zb[tid | hh];
-      v = (tid & hh) ? x0 - x1 : x0 + x1;
+  float o[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+  for (int c0 = 0; c0 < nsp; c0 += 256) {
+    const int s = c0 + tid;
+    float w = 0.0f;
+    if (s < nsp) {
+      w = __builtin_amdgcn_exp2f(pb[(size_t)s * PS] - M);
+      l = fmaf(w, pb[(size_t)s * PS + 1], l);
     }
     __syncthreads();
-    if (tid < D) zb[tid] = v;
+    wsp[tid] = w;
+    __syncthreads();
+    const int cn = min(256, nsp - c0);
+    for (int u0 = sg; u0 < cn; u0 += 64) {
+      float4 v[8];
+      float wv[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int u = min(u0 + 8 * j, cn - 1);
+        wv[j] = u0 + 8 * j < cn ? wsp[u] : 0.0f;
+        v[j] = *(const float4*)&pb[(size_t)(c0 + u) * PS + 4 + 4 * cq];
+      }
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        o[0] = fmaf(wv[j], v[j].x, o[0]);
+        o[1] = fmaf(wv[j], v[j].y, o[1]);
+        o[2] = fmaf(wv[j], v[j].z, o[2]);
+        o[3] = fmaf(wv[j], v[j].w, o[3]);
+      }
+    }
   }
+  for (int c0 = 0; c0 < ntail; c0 += 256) {
+    const int n = c0 + tid;
+    float w = 0.0f;
+    int av = 0;
+    if (n < ntail) {
+      const float p = __builtin_amdgcn_exp2f(tail_logit(n) - M);
+      l += p;
+      w = p * Elem<DT>::get(c.tgV, tb + n);
+      av = min((int)c.tidxV[tb + n], k - 1);
+    }
+    __syncthreads();
+    wsp[tid] = w;
+    tav[tid] = av;
+    __syncthreads();
+    const int cn = min(256, ntail - c0);
+    for (int u = sg; u < cn; u += 8) {
+      const E* row = AVg + (size_t)tav[u] * D + 4 * cq;
+      const float wv = wsp[u];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) o[i] = fmaf(wv, Elem<DT>::get(row, i), o[i]);
+    }
+  }
+  l = wave_sum_dpp(l);
+  __syncthreads();
+  if (lane == 0) red[wave] = l;
+  *(float4*)&acc[sg][4 * cq] = make_float4(o[0], o[1], o[2], o[3]);
   __syncthreads();
   if (tid < D) {
-    const float lt = rsum[0] + rsum[1] + rsum[2] + rsum[3];
-    const float y = yb[tid] + hsign(g.seed_sign, tid) * zb[tid] * (1.0f / (float)D);
-    const float o = y / lt;
+    const float lt = (red[0] + red[1]) + (red[2] + red[3]);
+    float y = 0.0f;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) y += acc[q][tid];
     const size_t oi = ((size_t)b * g.Hq + jq) * D + tid;
-    if (out_dtype == 1) ((uint16_t*)out)[oi] = f2bf(o); else ((float*)out)[oi] = o;
-  }
-}
-
-// ------------------------------------------------------------------ append
-template <int DT>
-__global__ __launch_bounds__(256) void k_append(Geo g, Cache c, int n_app, const void* kin, const void* vin) {
-  using E = typename Elem<DT>::T;
-  constexpr int D = AKV_D;
-  __shared__ float xs[D];
-  __shared__ float rb1[4], rb2[4];
-  __shared__ int ri1[4];
-  __shared__ double rc[4];
-  __shared__ int rci[4];
-  const int side = blockIdx.x & 1, bh = blockIdx.x >> 1;
-  const int b = bh / g.H, h = bh % g.H;
-  const int k = g.k[b];
-  const E* x = (const E*)(side ? vin : kin) + (size_t)bh * D;
-  const size_t ko = (size_t)g.prefK[b] * g.H + (size_t)h * k;
-  const E* A = (const E*)(side ? c.ancV : c.ancK) + ko * D;
-  const float* inv = (side ? c.invV : c.invK) + ko;
-  const double* nrm = (side ? c.nrmV : c.nrmK) + ko;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  if (threadIdx.x < D) xs[threadIdx.x] = Elem<DT>::get(x, threadIdx.x);
-  __syncthreads();
-  float ss = 0.0f;
-  for (int d = 0; d < D; ++d) ss = fmaf(xs[d], xs[d], ss);
-  const float xn = sqrtf(ss) * (1.0f + 1e-5f);
-  const float eps = xn * ((float)D * 1.1920929e-7f + 2.3841858e-7f) * 1.01f + 1e-30f;
-  auto score = [&](int a) {
-    const E* row = A + (size_t)a * D;
-    float s = 0.0f;
-    for (int d = 0; d < D; ++d) s = fmaf(xs[d], Elem<DT>::get(row, d), s);
-    return fabsf(s) * inv[a];
-  };
-  float b1 = -1.0f, b2 = -1.0f;
-  int i1 = 0x7fffffff;
-  for (int a = threadIdx.x; a < k; a += 256) {
-    const float v = score(a);
-    b2 = __builtin_amdgcn_fmed3f(b1, b2, v);
-    if (v > b1) { b1 = v; i1 = a; }
-  }
-  for (int o = 32; o > 0; o >>= 1) {
-    const float ob1 = __shfl_xor(b1, o, 64), ob2 = __shfl_xor(b2, o, 64);
-    const int oi = __shfl_xor(i1, o, 64);
-    const float t2 = fmaxf(fmaxf(b2, ob2), fminf(b1, ob1));
-    if (ob1 > b1 || (ob1 == b1 && oi < i1)) i1 = oi;
-    b1 = fmaxf(b1, ob1);
-    b2 = t2;
-  }
-  if (lane == 0) { rb1[wave] = b1; rb2[wave] = b2; ri1[wave] = i1; }
-  __syncthreads();
-  b1 = rb1[0]; b2 = rb2[0]; i1 = ri1[0];
-  for (int v = 1; v < 4; ++v) {
-    const float t2 = fmaxf(fmaxf(b2, rb2[v]), fminf(b1, rb1[v]));
-    if (rb1[v] > b1 || (rb1[v] == b1 && ri1[v] < i1)) i1 = ri1[v];
-    b1 = fmaxf(b1, rb1[v]);
-    b2 = t2;
-  }
-  int best = i1;
-  if (!(b1 - b2 > 2.0f * eps + b1 * 9.094947e-13f)) {
-    const float band = b1 - 2.0f * eps - b1 * 9.094947e-13f;
-    double bc = -INFINITY;
-    int bi = 0x7fffffff;
-    for (int a = threadIdx.x; a < k; a += 256) {
-      if (score(a) < band) continue;
-      const double d = dot64_seq<DT>(x, A + (size_t)a * D, D);
-      const double cc = nrm[a] > 0.0 ? (d * d) / nrm[a] : -1.0;
-      if (cc > bc) { bc = cc; bi = a; }
-    }
-    for (int o = 32; o > 0; o >>= 1) {
-      const double oc = __shfl_xor(bc, o, 64);
-      const int oi = __shfl_xor(bi, o, 64);
-      if (oc > bc || (oc == bc && oi < bi)) { bc = oc; bi = oi; }
-    }
-    __syncthreads();
-    if (lane == 0) { rc[wave] = bc; rci[wave] = bi; }
-    __syncthreads();
-    bc = rc[0];
-    bi = rci[0];
-    for (int v = 1; v < 4; ++v)
-      if (rc[v] > bc || (rc[v] == bc && rci[v] < bi)) { bc = rc[v]; bi = rci[v]; }
-    best = bi;
-  }
-  if (threadIdx.x == 0) {
-    const double n = nrm[best];
-    const double d = dot64_seq<DT>(x, A + (size_t)best * D, D);
-    const double g64 = n > 0.0 ? d / n : 0.0;
-    const float gb = Elem<DT>::round_coef((float)g64);
-    const size_t ti = ((size_t)b * g.H + h) * g.max_append + n_app;
-    (side ? c.tidxV : c.tidxK)[ti] = (uint16_t)best;
-    Elem<DT>::put(side ? c.tgV : c.tgK, ti, gb);
+    if (out_dtype == 1) ((uint16_t*)out)[oi] = f2bf(y / lt); else ((float*)out)[oi] = y / lt;
   }
 }
 
@@ -718,70 +963,57 @@ __global__ __launch_bounds__(256) void k_reconstruct(Geo g, Cache c, int b, int 
 }
 
 // ------------------------------------------------------------------ launchers
-template <int DT, int GQ, int R>
-static void launch_stream(const Geo& g, const Cache& c, const DecWs& dw, float scale, int nblk, size_t lds,
-                          hipStream_t st) {
-  (void)hipFuncSetAttribute((const void*)k_dec_stream<DT, GQ, R>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                            (int)lds);
-  AKV_TIMED("k_dec_stream", st, k_dec_stream<DT, GQ, R><<<nblk, 256, lds, st>>>(g, c, dw, scale));
-}
-
 template <int DT, int GQ>
-static void launch_stream_r(const Geo& g, const Cache& c, const DecWs& dw, float scale, int nblk, size_t lds,
-                            hipStream_t st) {
-  switch (g.dsplit) {
-    case 2048: launch_stream<DT, GQ, 8>(g, c, dw, scale, nblk, lds, st); break;
-    default: launch_stream<DT, GQ, 4>(g, c, dw, scale, nblk, lds, st); break;
+static void launch_steps(const Geo& g, const Cache& c, const DecWs& dw, const void* q, const void* kn,
+                         const void* vn, void* out, int out_dtype, float scale, int n_app, bool attn, bool app,
+                         hipStream_t st) {
+  const int nAK = g.H * g.prefAB[g.B];
+  const int nAV = app ? nAK : 0;
+  const int nR = attn ? (g.prefNK[g.B] + 255) / 256 : 0;
+  const int flags = (attn ? 1 : 0) | (app ? 2 : 0);
+  const float sl2 = scale * 1.4426950408889634f;
+  AKV_TIMED("k_dec_front", st,
+            k_dec_front<DT, GQ><<<nAK + nAV + nR, 256, 0, st>>>(g, c, dw, q, kn, vn, flags, nAK, nAV, sl2));
+  if (!attn) {
+    AKV_TIMED("k_app_finish", st, k_app_finish<DT><<<g.B * g.H * 2, 256, 0, st>>>(g, c, dw, n_app, kn, vn));
+    return;
   }
+  const int L = g.dsplit;
+  int nst = 0;
+  for (int b = 0; b < g.B; ++b) nst += g.H * ((g.S[b] + L - 1) / L);
+  const int nres = app ? g.B * g.H * 2 : 0;
+  if (L == 2048) {
+    AKV_TIMED("k_dec_stream", st, (k_dec_stream<DT, GQ, 8><<<nst + nres, 256, 0, st>>>(g, c, dw, nst, n_app, kn, vn)));
+  } else {
+    AKV_TIMED("k_dec_stream", st, (k_dec_stream<DT, GQ, 4><<<nst + nres, 256, 0, st>>>(g, c, dw, nst, n_app, kn, vn)));
+  }
+  AKV_TIMED("k_dec_merge", st,
+            (k_dec_merge<DT, GQ><<<g.B * g.Hq, 256, 0, st>>>(g, c, dw, n_app + (app ? 1 : 0), out, out_dtype)));
 }
 
 template <int DT>
-static void launch_stream_g(const Geo& g, const Cache& c, const DecWs& dw, float scale, int nblk, size_t lds,
-                            hipStream_t st) {
-  switch (g.g) {
-    case 1: launch_stream_r<DT, 1>(g, c, dw, scale, nblk, lds, st); break;
-    case 2: launch_stream_r<DT, 2>(g, c, dw, scale, nblk, lds, st); break;
-    case 4: launch_stream_r<DT, 4>(g, c, dw, scale, nblk, lds, st); break;
-    default: launch_stream_r<DT, 8>(g, c, dw, scale, nblk, lds, st); break;
+static void launch_steps_g(const Geo& g, const Cache& c, const DecWs& dw, const void* q, const void* kn,
+                           const void* vn, void* out, int out_dtype, float scale, int n_app, bool attn, bool app,
+                           hipStream_t st) {
+  // An append alone needs no query-head grouping: one instantiation serves.
+  const int gq = attn ? g.g : 1;
+  switch (gq) {
+    case 1: launch_steps<DT, 1>(g, c, dw, q, kn, vn, out, out_dtype, scale, n_app, attn, app, st); break;
+    case 2: launch_steps<DT, 2>(g, c, dw, q, kn, vn, out, out_dtype, scale, n_app, attn, app, st); break;
+    case 4: launch_steps<DT, 4>(g, c, dw, q, kn, vn, out, out_dtype, scale, n_app, attn, app, st); break;
+    default: launch_steps<DT, 8>(g, c, dw, q, kn, vn, out, out_dtype, scale, n_app, attn, app, st); break;
   }
 }
 
-// Dynamic LDS of the streaming kernel: the anchor-score table when it is kept
-// in LDS (the rest of its LDS is static).
-size_t decode_stream_lds(const Geo& g, int L, bool sk_in_lds) {
-  (void)L;
-  const size_t kpm = (size_t)((g.maxK + 3) & ~3);
-  return sk_in_lds ? g.g * kpm * 4 : 0;
-}
-
-hipError_t launch_decode(const Geo& g, const Cache& c, const DecWs& dw, const void* q, void* out, int out_dtype,
-                         float scale, int n_app, hipStream_t st) {
-  const int L = g.dsplit;
-  int nsc = g.B * g.H * g.maxRB, nst = 0;
-  for (int b = 0; b < g.B; ++b) {
-    nsc += g.H * ((g.k[b] + 255) / 256);
-    nst += g.H * ((g.S[b] + L - 1) / L);
-  }
-  if (g.dtype == 1) {
-    AKV_TIMED("k_dec_scores", st, k_dec_scores<1><<<nsc, 256, 0, st>>>(g, c, dw, q));
-    launch_stream_g<1>(g, c, dw, scale, nst, decode_stream_lds(g, L, g.dsk_lds != 0), st);
-    AKV_TIMED("k_dec_combine", st,
-              k_dec_combine<1><<<g.B * g.Hq, 256, 0, st>>>(g, c, dw, scale, n_app, out, out_dtype));
-  } else {
-    AKV_TIMED("k_dec_scores", st, k_dec_scores<0><<<nsc, 256, 0, st>>>(g, c, dw, q));
-    launch_stream_g<0>(g, c, dw, scale, nst, decode_stream_lds(g, L, g.dsk_lds != 0), st);
-    AKV_TIMED("k_dec_combine", st,
-              k_dec_combine<0><<<g.B * g.Hq, 256, 0, st>>>(g, c, dw, scale, n_app, out, out_dtype));
-  }
-  return hipGetLastError();
-}
-
-hipError_t launch_append(const Geo& g, const Cache& c, int n_app, const void* kn, const void* vn, hipStream_t st) {
-  if (g.dtype == 1) {
-    AKV_TIMED("k_append", st, k_append<1><<<g.B * g.H * 2, 256, 0, st>>>(g, c, n_app, kn, vn));
-  } else {
-    AKV_TIMED("k_append", st, k_append<0><<<g.B * g.H * 2, 256, 0, st>>>(g, c, n_app, kn, vn));
-  }
+// q == nullptr: append only; kn == nullptr: attention only; both: append the
+// token as tail slot n_app, then attend over it too.
+hipError_t launch_decode(const Geo& g, const Cache& c, const DecWs& dw, const void* q, const void* kn,
+                         const void* vn, void* out, int out_dtype, float scale, int n_app, hipStream_t st) {
+  const bool attn = q != nullptr, app = kn != nullptr;
+  if (g.dtype == 1)
+    launch_steps_g<1>(g, c, dw, q, kn, vn, out, out_dtype, scale, n_app, attn, app, st);
+  else
+    launch_steps_g<0>(g, c, dw, q, kn, vn, out, out_dtype, scale, n_app, attn, app, st);
   return hipGetLastError();
 }
 

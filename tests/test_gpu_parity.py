@@ -147,7 +147,8 @@ def test_decode_matches_oracle_attention(case):
                 assert np.abs(outb[b].float().cpu().numpy() - ref).max() <= 2e-2
 
 
-def test_append_then_decode():
+@pytest.mark.parametrize("fused", [False, True], ids=["append_then_attn", "decode_step"])
+def test_append_then_decode(fused):
     wl = _small("append", seq_lens=[1300], steps=6, append=True, seed=21)
     layer = synth.make_layer(wl)
     cfg = make_cfg(wl)
@@ -160,9 +161,12 @@ def test_append_then_decode():
     Vx = layer.V[0].float().numpy()
     tails_k, tails_v = [], []
     for n in range(wl.steps):
-        akv.append(plan, cache, n, layer.k_new[n].cuda(), layer.v_new[n].cuda())
         out = torch.empty(1, wl.Hq, wl.D, dtype=torch.float32, device="cuda")
-        akv.decode_attn(plan, cache, layer.q[n].cuda(), out, dws, n_appended=n + 1)
+        if fused:
+            akv.decode_step(plan, cache, n, layer.k_new[n].cuda(), layer.v_new[n].cuda(), layer.q[n].cuda(), out, dws)
+        else:
+            akv.append(plan, cache, n, layer.k_new[n].cuda(), layer.v_new[n].cuda(), dws)
+            akv.decode_attn(plan, cache, layer.q[n].cuda(), out, dws, n_appended=n + 1)
         torch.cuda.synchronize()
         tk, tv = [], []
         for h in range(wl.H):

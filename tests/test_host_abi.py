@@ -121,8 +121,12 @@ def test_entry_points_validate_before_touching_the_gpu():
     L = _lib_or_skip()
     p = N.Plan(_cfg(max_append=4), [4096])
     assert L.anchorkv_encode(p.handle, None, None, None, None, None, None, None) == N.ERR_INVALID_ARG
-    assert L.anchorkv_append(p.handle, 1, 4, 1, 1, None) == N.ERR_CAPACITY
-    assert L.anchorkv_append(p.handle, 1, -1, 1, 1, None) == N.ERR_INVALID_ARG
+    assert L.anchorkv_append(p.handle, 1, 4, 1, 1, 1, None) == N.ERR_CAPACITY
+    assert L.anchorkv_append(p.handle, 1, -1, 1, 1, 1, None) == N.ERR_INVALID_ARG
+    assert L.anchorkv_append(p.handle, 1, 0, 1, 1, None, None) == N.ERR_INVALID_ARG
+    assert L.anchorkv_decode_step(p.handle, 1, 4, 1, 1, 1, 1, 0, 0.0, 1, None) == N.ERR_CAPACITY
+    assert L.anchorkv_decode_step(p.handle, 1, 0, 1, 1, 1, 1, 7, 0.0, 1, None) == N.ERR_INVALID_ARG
+    assert L.anchorkv_decode_step(p.handle, 1, 0, 1, 1, None, 1, 0, 0.0, 1, None) == N.ERR_INVALID_ARG
     assert L.anchorkv_decode_attn(p.handle, 1, 5, 1, 1, 0, 0.0, 1, None) == N.ERR_INVALID_ARG
     assert L.anchorkv_decode_attn(p.handle, 1, 0, 1, 1, 9, 0.0, 1, None) == N.ERR_INVALID_ARG
     assert L.anchorkv_reconstruct(p.handle, 1, 0, 3, 0, 1, None) == N.ERR_INVALID_ARG
