@@ -88,9 +88,10 @@ struct Cache {
 // Encode scratch.
 struct Ws {
   float* opmax;         // [b][h][chunk][m] partial row max of the observation logits
-  float* opsum;         // [b][h][chunk][m] partial sum of exp
+  double* opsum;        // [b][h][chunk][m] partial sum of exp (fp64)
   float* oM;            // [b][h][m] row max (scaled logits)
   float* oiZ;           // [b][h][m] 1 / sum exp
+  double* oiZ64;        // [b][h][m] the same in fp64 (selection near-ties)
   float* ypart;         // [b][h][chunk][m][D] partial observation outputs
   float* Y;             // [b][h][m][D]
   uint16_t* Yhi;        // [b][h][m][D] bf16 split of Y: Y ~ hi + lo

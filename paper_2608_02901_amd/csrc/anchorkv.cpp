@@ -65,7 +65,7 @@ struct anchorkv_plan {
       c_stats;
   size_t cache_bytes;
   // encode workspace offsets
-  size_t w_opmax, w_opsum, w_oM, w_oiZ, w_ypart, w_Y, w_Yhi, w_Ylo, w_ynorm, w_sc, w_rank, w_flag, w_QA, w_apos,
+  size_t w_opmax, w_opsum, w_oM, w_oiZ, w_oiZ64, w_ypart, w_Y, w_Yhi, w_Ylo, w_ynorm, w_sc, w_rank, w_flag, w_QA, w_apos,
       w_fix, w_fixcount, w_gpos, w_u, w_sel, w_bhist, w_bstate, w_tiecnt, w_shist, w_wcnt;
   size_t ws_bytes;
   // decode workspace offsets
@@ -266,9 +266,10 @@ extern "C" anchorkv_status anchorkv_plan_create(const anchorkv_config* cfg, int3
 
   Layout Wl;
   p->w_opmax = Wl.add(4 * TC * m);
-  p->w_opsum = Wl.add(4 * TC * m);
+  p->w_opsum = Wl.add(8 * TC * m);
   p->w_oM = Wl.add(4 * batch * H * m);
   p->w_oiZ = Wl.add(4 * batch * H * m);
+  p->w_oiZ64 = Wl.add(8 * batch * H * m);
   p->w_ypart = Wl.add(4 * TC * m * D);
   p->w_Y = Wl.add(4 * batch * H * m * D);
   p->w_Yhi = Wl.add(2 * batch * H * m * D);
@@ -353,9 +354,10 @@ static akv::Cache cache_ptrs(const anchorkv_plan* p, void* base) {
 static akv::Ws ws_ptrs(const anchorkv_plan* p, void* base) {
   akv::Ws w;
   w.opmax = at<float>(base, p->w_opmax);
-  w.opsum = at<float>(base, p->w_opsum);
+  w.opsum = at<double>(base, p->w_opsum);
   w.oM = at<float>(base, p->w_oM);
   w.oiZ = at<float>(base, p->w_oiZ);
+  w.oiZ64 = at<double>(base, p->w_oiZ64);
   w.ypart = at<float>(base, p->w_ypart);
   w.Y = at<float>(base, p->w_Y);
   w.Yhi = at<uint16_t>(base, p->w_Yhi);

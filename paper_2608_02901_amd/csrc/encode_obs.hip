@@ -88,11 +88,15 @@ __global__ __launch_bounds__(256) void k_obs_stats(Geo g, Ws w, const void* Kin,
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int nrb = (m + 31) / 32;
   const float isd = 1.0f / sqrtf((float)D);
-  float mx[2][16], sm[2][16];
+  // Running row max (fp32 logits) and sum of exp in fp64; a change of the
+  // max rescales the sum by an fp64 exp, so the sum keeps ~1e-9 relative
+  // accuracy (the anchor selection re-scores near-ties against it).
+  float mx[2][16];
+  double sm[2][16];
 #pragma unroll
   for (int r = 0; r < 2; ++r)
 #pragma unroll
-    for (int e = 0; e < 16; ++e) { mx[r][e] = NEG; sm[r][e] = 0.0f; }
+    for (int e = 0; e < 16; ++e) { mx[r][e] = NEG; sm[r][e] = 0.0; }
   const int tb = ch * OBS_CHUNK, te = min(S, tb + OBS_CHUNK);
   for (int t0 = tb; t0 < te; t0 += 32) {
     __syncthreads();
@@ -115,10 +119,12 @@ __global__ __launch_bounds__(256) void k_obs_stats(Geo g, Ws w, const void* Kin,
       for (int e = 0; e < 16; ++e) {
         const int wr = rb * 32 + crow(e, lane);
         if (obs_visible(t, S, P, wr, m, g.W)) {
-          float l = acc[e] * isd;
-          float nm = fmaxf(mx[r][e], l);
-          sm[r][e] = sm[r][e] * __expf(mx[r][e] - nm) + __expf(l - nm);
-          mx[r][e] = nm;
+          const float l = acc[e] * isd;
+          if (l > mx[r][e]) {
+            sm[r][e] *= exp((double)mx[r][e] - (double)l);
+            mx[r][e] = l;
+          }
+          sm[r][e] += (double)__expf(l - mx[r][e]);
         }
       }
     }
@@ -130,11 +136,13 @@ __global__ __launch_bounds__(256) void k_obs_stats(Geo g, Ws w, const void* Kin,
     if (rb >= nrb) break;
 #pragma unroll
     for (int e = 0; e < 16; ++e) {
-      float a = mx[r][e], s = sm[r][e];
+      float a = mx[r][e];
+      double s = sm[r][e];
       for (int o = 1; o < 32; o <<= 1) {
-        float oa = __shfl_xor(a, o, 64), os = __shfl_xor(s, o, 64);
-        float nm = fmaxf(a, oa);
-        s = s * __expf(a - nm) + os * __expf(oa - nm);
+        const float oa = __shfl_xor(a, o, 64);
+        const double os = __shfl_xor(s, o, 64);
+        const float nm = fmaxf(a, oa);
+        s = (a == nm ? s : s * exp((double)a - (double)nm)) + (oa == nm ? os : os * exp((double)oa - (double)nm));
         a = nm;
       }
       const int wr = rb * 32 + crow(e, lane);
@@ -154,10 +162,15 @@ __global__ __launch_bounds__(256) void k_obs_reduce(Geo g, Ws w) {
     size_t base = ((size_t)(g.prefC[b] * g.H + h * nch)) * g.m + wr;
     float M = NEG;
     for (int c = 0; c < nch; ++c) M = fmaxf(M, w.opmax[base + (size_t)c * g.m]);
-    float Z = 0.0f;
-    for (int c = 0; c < nch; ++c) Z += w.opsum[base + (size_t)c * g.m] * __expf(w.opmax[base + (size_t)c * g.m] - M);
+    double Z = 0.0;
+    for (int c = 0; c < nch; ++c) {
+      const float mc = w.opmax[base + (size_t)c * g.m];
+      const double sc = w.opsum[base + (size_t)c * g.m];
+      Z += mc == M ? sc : sc * exp((double)mc - (double)M);
+    }
     w.oM[(size_t)(b * g.H + h) * g.m + wr] = M;
-    w.oiZ[(size_t)(b * g.H + h) * g.m + wr] = 1.0f / Z;
+    w.oiZ[(size_t)(b * g.H + h) * g.m + wr] = (float)(1.0 / Z);
+    w.oiZ64[(size_t)(b * g.H + h) * g.m + wr] = 1.0 / Z;
   }
 }
 

@@ -43,10 +43,53 @@ __device__ inline int block_excl_scan(int v, int* tmp /* >= 16 ints */, int& tot
   return r;
 }
 
-__global__ __launch_bounds__(1024) void k_select(Geo g, Ws w, Cache c, const int32_t* ovr) {
+// Positions whose fp32 pooled score lies within SEL_BAND (relative) of the
+// cut are re-scored in fp64 (at most SEL_BAND_MAX of them).  The fp32 score's
+// error is below 1e-4 relative: fp32 accumulation of 128 exact bf16 products
+// (at most 128 * 2^-24 * sum |q_i k_i| / sqrt(D) on a logit), fp32 exp and
+// sums; the band is ten times wider.  The fp64 scores use exact fp64 logits
+// and the row sums Z_w of the observation pass (fp64 sums of fp32-logit
+// exponentials, ~1e-9 relative), so they match the canonical fp64 definition
+// to far better than the gaps between real scores.
+constexpr float SEL_BAND = 1e-3f;
+constexpr int SEL_BAND_MAX = 256;
+
+// fp64 pooled selector score of position t (t < P, so every observation row
+// sees it): (1/kappa) sum_{|d| <= kappa/2, 0 <= t+d < P} (1/m) sum_w
+// exp(dot64(q_w, k_{t+d}) / sqrt(D) - M_w) / Z_w, with the row statistics of
+// the observation pass.  One wave; lane l takes rows l, l + 64, ...; the
+// lane partials are summed in a fixed order.
+template <int DT>
+__device__ double pooled64(const Geo& g, const typename Elem<DT>::T* X, const typename Elem<DT>::T* Q,
+                           const float* oM, const double* oiZ, int t, int P, int m) {
+  const int lane = threadIdx.x & 63, half = g.kappa / 2;
+  double acc = 0.0;
+  for (int wr = lane; wr < m; wr += 64) {
+    const auto* q = Q + (size_t)wr * AKV_D;
+    double rs = 0.0;
+    for (int d = -half; d <= half; ++d) {
+      const int u = t + d;
+      if (u < 0 || u >= P) continue;
+      const double l = dot64_seq<DT>(q, X + (size_t)u * AKV_D, AKV_D) / sqrt((double)AKV_D);
+      rs += exp(l - (double)oM[wr]) * oiZ[wr];
+    }
+    acc += rs;
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) acc += __shfl_xor(acc, o, 64);
+  return acc / (double)m / (double)g.kappa;
+}
+
+template <int DT>
+__global__ __launch_bounds__(1024) void k_select(Geo g, Ws w, Cache c, const int32_t* ovr, const void* Kin,
+                                                 const void* Qin) {
+  using E = typename Elem<DT>::T;
   __shared__ uint32_t hist[256];
   __shared__ int tmp[20];
   __shared__ unsigned long long bcast[2];
+  __shared__ int band[SEL_BAND_MAX];
+  __shared__ double bscore[SEL_BAND_MAX];
+  __shared__ int nband, nabove;
   const int b = blockIdx.x / g.H, h = blockIdx.x % g.H;
   const int S = g.S[b], W = g.W, P = S - W, k = g.k[b];
   const size_t so = (size_t)g.prefS[b] * g.H + (size_t)h * S;
@@ -122,8 +165,49 @@ __global__ __launch_bounds__(1024) void k_select(Geo g, Ws w, Cache c, const int
       pmask |= 255u << shift;
       __syncthreads();
     }
-    // prefix is the bit pattern of the n_top-th largest score; take every
-    // larger score and the first `remaining` equal ones in position order.
+    // prefix is the bit pattern of the n_top-th largest fp32 score.  Scores
+    // clearly above the band are taken; inside the band the decision uses the
+    // fp64 scores (ties to the lower position).
+    const float cut = __uint_as_float(prefix);
+    const float bhi = cut * (1.0f + SEL_BAND), blo = cut * (1.0f - SEL_BAND);
+    if (tid == 0) {
+      nband = 0;
+      nabove = 0;
+    }
+    __syncthreads();
+    for (int t = tid; t < P; t += nt) {
+      const float v = pooled[t];
+      if (v > bhi) {
+        atomicAdd(&nabove, 1);
+      } else if (v >= blo) {
+        const int i = atomicAdd(&nband, 1);
+        if (i < SEL_BAND_MAX) band[i] = t;
+      }
+    }
+    __syncthreads();
+    const int nb = nband;
+    if (nb <= SEL_BAND_MAX) {
+      const E* X = (const E*)Kin + ((size_t)g.prefS[b] * g.H + (size_t)h * S) * AKV_D;
+      const E* Q = (const E*)Qin + ((size_t)b * g.Hq + (size_t)h * g.g) * g.W * AKV_D;
+      const float* oM = w.oM + (size_t)(b * g.H + h) * g.m;
+      const double* oiZ = w.oiZ64 + (size_t)(b * g.H + h) * g.m;
+      for (int i = tid >> 6; i < nb; i += nt >> 6) {
+        const double v = pooled64<DT>(g, X, Q, oM, oiZ, band[i], P, g.m);
+        if ((tid & 63) == 0) bscore[i] = v;
+      }
+      __syncthreads();
+      const int need = ntop - nabove;
+      for (int t = tid; t < P; t += nt) flag[t] = pooled[t] > bhi ? 1 : 0;
+      __syncthreads();
+      for (int i = tid; i < nb; i += nt) {
+        int r = 0;
+        for (int j = 0; j < nb; ++j)
+          r += bscore[j] > bscore[i] || (bscore[j] == bscore[i] && band[j] < band[i]);
+        if (r < need) flag[band[i]] = 1;
+      }
+      __syncthreads();
+    } else {
+    if (tid == 0) atomicOr(&c.header[2], 32u);  // band overflow: the fp32 order decides
     int eq = 0;
     for (int t = lo; t < hi; ++t) eq += (__float_as_uint(pooled[t]) == prefix);
     int tot;
@@ -138,6 +222,7 @@ __global__ __launch_bounds__(1024) void k_select(Geo g, Ws w, Cache c, const int
       }
     }
     __syncthreads();
+    }
   }
 
   // ---- uniform share: the n_rand unflagged positions with the smallest hash.
@@ -255,9 +340,13 @@ __global__ __launch_bounds__(256) void k_anchor_prep(Geo g, Ws w, Cache c, const
 
 hipError_t launch_select(const Geo& g, const Ws& w, const Cache& c, const void* K, const void* V, const void* Q,
                          const int32_t* ovr, hipStream_t st) {
-  AKV_TIMED("k_select", st, k_select<<<g.B * g.H, 1024, 0, st>>>(g, w, c, ovr));
   int nblk = 0;
   for (int b = 0; b < g.B; ++b) nblk += g.H * ((g.k[b] + 63) / 64);
+  if (g.dtype == 1) {
+    AKV_TIMED("k_select", st, k_select<1><<<g.B * g.H, 1024, 0, st>>>(g, w, c, ovr, K, Q));
+  } else {
+    AKV_TIMED("k_select", st, k_select<0><<<g.B * g.H, 1024, 0, st>>>(g, w, c, ovr, K, Q));
+  }
   if (g.dtype == 1) {
     AKV_TIMED("k_anchor_prep", st, k_anchor_prep<1><<<nblk, 256, 0, st>>>(g, w, c, K, V, Q));
   } else {
