@@ -228,7 +228,8 @@ extern "C" anchorkv_status anchorkv_plan_create(const anchorkv_config* cfg, int3
     for (int b = 0; b < batch; ++b) n += (int64_t)H * ((geo.S[b] + 2047) / 2048);
     if (n >= 256) Lsel = 2048;
     geo.dsplit = Lsel;
-    for (int b = 0; b < batch; ++b) geo.prefSp[b + 1] = geo.prefSp[b] + (geo.S[b] + Lsel - 1) / Lsel;
+    // split records per query head: the splits plus one for the appended tail
+    for (int b = 0; b < batch; ++b) geo.prefSp[b + 1] = geo.prefSp[b] + (geo.S[b] + Lsel - 1) / Lsel + 1;
   }
   const size_t TS = (size_t)geo.prefS[batch] * H, TK = (size_t)geo.prefK[batch] * H,
                TW = (size_t)geo.prefW[batch] * H, TC = (size_t)geo.prefC[batch] * H;

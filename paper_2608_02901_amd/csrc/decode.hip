@@ -412,6 +412,146 @@ __global__ __launch_bounds__(256) void k_app_finish(Geo g, Cache c, DecWs dw, in
   append_resolve<DT>(g, c, dw, bh / g.H, bh % g.H, side, n_app, side ? vin : kin, fr, dr, ir, &oi, &og);
 }
 
+// ------------------------------------------------------------------ tail
+// The appended tokens of one (request, KV head) as one more split record
+// (index nsp) for each of its g query heads.  When this step appends a token
+// (kin != nullptr), its anchors are resolved first and it joins the tail as
+// slot n_app.  Tail tokens carry no residual: logit = gamma^K S_K[a^K], value
+// gamma^V abar^V_{a^V}.  Runs beside the split workgroups of the stream pass.
+template <int DT, int GQ>
+__device__ void tail_block(const Geo& g, const Cache& c, const DecWs& dw, int bh, int n_app, const void* kin,
+                           const void* vin, unsigned char* pool) {
+  using E = typename Elem<DT>::T;
+  constexpr int D = AKV_D, TCH = 256;
+  __shared__ float fr[4];
+  __shared__ double dr[4];
+  __shared__ int ir[5];
+  __shared__ int t_idx[2];
+  __shared__ float t_g[2];
+  __shared__ float red[4][GQ];
+  // Carved from the caller's LDS pool (>= 9 KB): weights p * gamma^V per
+  // tail token, their value anchors, and the per-group output partials.
+  float(*tl)[GQ] = (float(*)[GQ])pool;
+  int* tav = (int*)(pool + TCH * GQ * 4);
+  float(*acc)[D] = (float(*)[D])(pool + TCH * GQ * 4 + TCH * 4);
+  const int b = bh / g.H, h = bh % g.H;
+  const int S = g.S[b], k = g.k[b], kp = (k + 3) & ~3;
+  const int nsp = (S + g.dsplit - 1) / g.dsplit;
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const bool app = kin != nullptr;
+  if (app) {
+    append_resolve<DT>(g, c, dw, b, h, 0, n_app, kin, fr, dr, ir, &t_idx[0], &t_g[0]);
+    append_resolve<DT>(g, c, dw, b, h, 1, n_app, vin, fr, dr, ir, &t_idx[1], &t_g[1]);
+  }
+  const int ntail = n_app + (app ? 1 : 0);
+  const size_t ko = (size_t)g.prefK[b] * g.H + (size_t)h * k;
+  const float* SKh = dw.SK + ((size_t)g.prefKp[b] * g.H + (size_t)h * kp) * GQ;
+  const E* AVg = (const E*)c.ancV + ko * D;
+  const size_t tb = ((size_t)b * g.H + h) * g.max_append;
+  auto rec = [&](int n, int& ak, float& gk, int& av, float& gv) {
+    if (app && n == n_app) {
+      ak = t_idx[0];
+      gk = t_g[0];
+      av = t_idx[1];
+      gv = t_g[1];
+    } else {
+      ak = min((int)c.tidxK[tb + n], k - 1);
+      gk = Elem<DT>::get(c.tgK, tb + n);
+      av = min((int)c.tidxV[tb + n], k - 1);
+      gv = Elem<DT>::get(c.tgV, tb + n);
+    }
+  };
+  // Maxima over the whole tail (log2-domain logits).
+  float mloc[GQ];
+#pragma unroll
+  for (int jj = 0; jj < GQ; ++jj) mloc[jj] = -INFINITY;
+  for (int n = tid; n < ntail; n += 256) {
+    int ak, av;
+    float gk, gv;
+    rec(n, ak, gk, av, gv);
+    float sk[GQ];
+    load_g<GQ>(SKh + (size_t)ak * GQ, sk);
+#pragma unroll
+    for (int jj = 0; jj < GQ; ++jj) mloc[jj] = fmaxf(mloc[jj], gk * sk[jj]);
+  }
+#pragma unroll
+  for (int jj = 0; jj < GQ; ++jj) {
+    const float v = wave_max_dpp(mloc[jj]);
+    if (lane == 0) red[wave][jj] = v;
+  }
+  __syncthreads();
+  float M[GQ], lsum[GQ];
+#pragma unroll
+  for (int jj = 0; jj < GQ; ++jj) {
+    M[jj] = fmaxf(fmaxf(red[0][jj], red[1][jj]), fmaxf(red[2][jj], red[3][jj]));
+    lsum[jj] = 0.0f;
+  }
+  // Outputs: thread = (coordinate quad cq, token group sg of 8).
+  const int cq = tid & 31, sg = tid >> 5;
+  float o[GQ][4];
+#pragma unroll
+  for (int jj = 0; jj < GQ; ++jj) o[jj][0] = o[jj][1] = o[jj][2] = o[jj][3] = 0.0f;
+  for (int c0 = 0; c0 < ntail; c0 += TCH) {
+    const int n = c0 + tid;
+    __syncthreads();
+    if (n < ntail) {
+      int ak, av;
+      float gk, gv;
+      rec(n, ak, gk, av, gv);
+      float sk[GQ];
+      load_g<GQ>(SKh + (size_t)ak * GQ, sk);
+#pragma unroll
+      for (int jj = 0; jj < GQ; ++jj) {
+        const float p = __builtin_amdgcn_exp2f(gk * sk[jj] - M[jj]);
+        lsum[jj] += p;
+        tl[tid][jj] = p * gv;
+      }
+      tav[tid] = av;
+    }
+    __syncthreads();
+    const int cn = min(TCH, ntail - c0);
+    for (int u = sg; u < cn; u += 8) {
+      const E* row = AVg + (size_t)tav[u] * D + 4 * cq;
+      float v[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) v[i] = Elem<DT>::get(row, i);
+#pragma unroll
+      for (int jj = 0; jj < GQ; ++jj) {
+        const float w = tl[u][jj];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) o[jj][i] = fmaf(w, v[i], o[jj][i]);
+      }
+    }
+  }
+#pragma unroll
+  for (int jj = 0; jj < GQ; ++jj) {
+    const float v = wave_sum_dpp(lsum[jj]);
+    __syncthreads();
+    if (lane == 0) red[wave][jj] = v;
+    __syncthreads();
+    lsum[jj] = (red[0][jj] + red[1][jj]) + (red[2][jj] + red[3][jj]);
+  }
+  const int Hq = g.Hq;
+#pragma unroll
+  for (int jj = 0; jj < GQ; ++jj) {
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < 4; ++i) acc[sg][4 * cq + i] = o[jj][i];
+    __syncthreads();
+    float* pr = dw.part + ((size_t)g.prefSp[b] * Hq + (size_t)(h * GQ + jj) * (nsp + 1) + nsp) * PS;
+    if (tid < D) {
+      float y = 0.0f;
+#pragma unroll
+      for (int q = 0; q < 8; ++q) y += acc[q][tid];
+      pr[4 + tid] = y;
+    }
+    if (tid == 0) {
+      pr[0] = ntail > 0 ? M[jj] : -INFINITY;
+      pr[1] = lsum[jj];
+    }
+  }
+}
+
 // ------------------------------------------------------------------ stream
 // R uint16 values starting at p (R * 2 bytes, 8-byte aligned).
 template <int R>
@@ -445,36 +585,30 @@ __device__ inline void load_coef(const void* base, size_t i0, float* v) {
 }
 __device__ inline unsigned long long low_bits(int n) { return n >= 64 ? ~0ull : ((1ull << n) - 1ull); }
 
-// Grid: nst split workgroups, then, when a token is appended in this step
-// (kin != nullptr), one workgroup per (request, head, side) that resolves it
-// into tail slot n_app while the splits stream.
+// Grid: nst split workgroups, then one tail workgroup per (request, KV head)
+// (which first resolves this step's appended token when kin != nullptr).
 template <int DT, int GQ, int R>
 __global__ __launch_bounds__(256) void k_dec_stream(Geo g, Cache c, DecWs dw, int nst, int n_app, const void* kin,
                                                     const void* vin) {
   using E = typename Elem<DT>::T;
   constexpr int D = AKV_D, L = 256 * R, PER = 16 / sizeof(E);
   constexpr int NAV = DEC_ASTG * D / PER / 256;
-  // LDS pool: per-anchor weights and staged value-anchor rows, later reused for
-  // the per-wave output partials.
-  constexpr int WACC_B = DEC_RCW * GQ * 4, AVS_B = DEC_ASTG * D * (int)sizeof(E), ZY_B = 2 * 4 * GQ * D * 4;
-  constexpr int POOL_B = WACC_B + AVS_B > ZY_B ? WACC_B + AVS_B : ZY_B;
-  __shared__ __align__(16) unsigned char pool[POOL_B];
-  float(*wacc)[GQ] = (float(*)[GQ])pool;
-  E* avs = (E*)(pool + WACC_B);
   __shared__ __align__(16) uint32_t vcode[DEC_VCH][8];
   __shared__ float vsc[DEC_VCH][4];
   __shared__ __align__(16) float vp[DEC_VCH][GQ];
   __shared__ float redm[4][GQ], reds[4][GQ];
   __shared__ float2 lvl2[16];  // levels of a coordinate pair by its 4-bit code
 
+  // LDS pool: per-anchor weights and staged value-anchor rows, later reused for
+  // the per-wave output partials (tail workgroups use it for their own arrays).
+  constexpr int WACC_B = DEC_RCW * GQ * 4, AVS_B = DEC_ASTG * D * (int)sizeof(E), ZY_B = 2 * 4 * GQ * D * 4;
+  constexpr int POOL_B = WACC_B + AVS_B > ZY_B ? WACC_B + AVS_B : ZY_B;
+  __shared__ __align__(16) unsigned char pool[POOL_B];
+  float(*wacc)[GQ] = (float(*)[GQ])pool;
+  E* avs = (E*)(pool + WACC_B);
+  static_assert(POOL_B >= 256 * GQ * 4 + 256 * 4 + 8 * D * 4, "LDS pool too small for the tail workgroup");
   if ((int)blockIdx.x >= nst) {
-    __shared__ float fr[4];
-    __shared__ double dr[4];
-    __shared__ int ir[5];
-    __shared__ int oi;
-    __shared__ float og;
-    const int r = blockIdx.x - nst, side = r & 1, bh = r >> 1;
-    append_resolve<DT>(g, c, dw, bh / g.H, bh % g.H, side, n_app, side ? vin : kin, fr, dr, ir, &oi, &og);
+    tail_block<DT, GQ>(g, c, dw, (int)blockIdx.x - nst, n_app, kin, vin, pool);
     return;
   }
   // Logical block id: consecutive ids (the splits of one head) share an XCD.
@@ -798,7 +932,7 @@ __global__ __launch_bounds__(256) void k_dec_stream(Geo g, Cache c, DecWs dw, in
     }
     fwht_wave_dpp(z0, z1, lane);
     const float o0 = y0 + s0v * (z0 * invD), o1 = y1 + s1v * (z1 * invD);
-    float* pr = dw.part + ((size_t)g.prefSp[b] * Hq + (size_t)(h * GQ + jj) * nsp + sp) * PS;
+    float* pr = dw.part + ((size_t)g.prefSp[b] * Hq + (size_t)(h * GQ + jj) * (nsp + 1) + sp) * PS;
     if (lane == 0) {
       pr[0] = fmaxf(fmaxf(redm[0][jj], redm[1][jj]), fmaxf(redm[2][jj], redm[3][jj]));
       pr[1] = reds[0][jj] + reds[1][jj] + reds[2][jj] + reds[3][jj];
@@ -808,92 +942,54 @@ __global__ __launch_bounds__(256) void k_dec_stream(Geo g, Cache c, DecWs dw, in
 }
 
 // ------------------------------------------------------------------ merge
-// One workgroup per (request, query head): merges its split records and the
-// appended tail tokens, which carry no residual (logit = scale * gamma^K
-// (q . abar^K_a), value gamma^V abar^V_a).  Thread t owns output coordinates
-// 4 (t % 32) .. +3 of every 8th split / tail token (group t / 32); the groups
-// are summed through LDS at the end.
+// One workgroup per (request, query head): merges its nsp + 1 split records
+// (the last one holds the appended tail) in one pass.  Thread t owns output
+// coordinates 4 (t % 32) .. +3 of every 8th record; the record maxima and
+// values are loaded together, 128 records per round.
 template <int DT, int GQ>
-__global__ __launch_bounds__(256) void k_dec_merge(Geo g, Cache c, DecWs dw, int ntail, void* out, int out_dtype) {
-  using E = typename Elem<DT>::T;
-  constexpr int D = AKV_D;
-  __shared__ float wsp[256];
-  __shared__ int tav[256];
+__global__ __launch_bounds__(256) void k_dec_merge(Geo g, DecWs dw, void* out, int out_dtype) {
+  constexpr int D = AKV_D, RCH = 128;
   __shared__ float red[4];
   __shared__ __align__(16) float acc[8][D];
-  const int b = blockIdx.x / g.Hq, jq = blockIdx.x % g.Hq, h = jq / GQ, jj = jq % GQ;
-  const int S = g.S[b], k = g.k[b], kp = (k + 3) & ~3;
-  const int nsp = (S + g.dsplit - 1) / g.dsplit;
+  const int b = blockIdx.x / g.Hq, jq = blockIdx.x % g.Hq;
+  const int nrec = (g.S[b] + g.dsplit - 1) / g.dsplit + 1;
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int cq = tid & 31, sg = tid >> 5;
-  const size_t ko = (size_t)g.prefK[b] * g.H + (size_t)h * k;
-  const float* SKh = dw.SK + ((size_t)g.prefKp[b] * g.H + (size_t)h * kp) * GQ;
-  const E* AVg = (const E*)c.ancV + ko * D;
-  const size_t tb = ((size_t)b * g.H + h) * g.max_append;
-  const float* pb = dw.part + ((size_t)g.prefSp[b] * g.Hq + (size_t)jq * nsp) * PS;
-  auto tail_logit = [&](int n) {
-    const int ak = min((int)c.tidxK[tb + n], k - 1);
-    return Elem<DT>::get(c.tgK, tb + n) * SKh[(size_t)ak * GQ + jj];
-  };
-  // Global max over the splits and the tail.
+  const float* pb = dw.part + ((size_t)g.prefSp[b] * g.Hq + (size_t)jq * nrec) * PS;
   float M = -INFINITY;
-  for (int s = tid; s < nsp; s += 256) M = fmaxf(M, pb[(size_t)s * PS]);
-  for (int n = tid; n < ntail; n += 256) M = fmaxf(M, tail_logit(n));
+  for (int s = tid; s < nrec; s += 256) M = fmaxf(M, pb[(size_t)s * PS]);
+  // First round of record values, issued before the max is known.
+  float4 v[RCH / 8];
+  float mv[RCH / 8];
+#pragma unroll
+  for (int j = 0; j < RCH / 8; ++j) {
+    const int s = min(sg + 8 * j, nrec - 1);
+    v[j] = *(const float4*)&pb[(size_t)s * PS + 4 + 4 * cq];
+    mv[j] = pb[(size_t)s * PS];
+  }
   M = wave_max_dpp(M);
   if (lane == 0) red[wave] = M;
   __syncthreads();
   M = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
   float l = 0.0f;
+  for (int s = tid; s < nrec; s += 256) l = fmaf(__builtin_amdgcn_exp2f(pb[(size_t)s * PS] - M), pb[(size_t)s * PS + 1], l);
   float o[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-  for (int c0 = 0; c0 < nsp; c0 += 256) {
-    const int s = c0 + tid;
-    float w = 0.0f;
-    if (s < nsp) {
-      w = __builtin_amdgcn_exp2f(pb[(size_t)s * PS] - M);
-      l = fmaf(w, pb[(size_t)s * PS + 1], l);
-    }
-    __syncthreads();
-    wsp[tid] = w;
-    __syncthreads();
-    const int cn = min(256, nsp - c0);
-    for (int u0 = sg; u0 < cn; u0 += 64) {
-      float4 v[8];
-      float wv[8];
+  for (int c0 = 0; c0 < nrec; c0 += RCH) {
+    if (c0 > 0) {
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const int u = min(u0 + 8 * j, cn - 1);
-        wv[j] = u0 + 8 * j < cn ? wsp[u] : 0.0f;
-        v[j] = *(const float4*)&pb[(size_t)(c0 + u) * PS + 4 + 4 * cq];
-      }
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        o[0] = fmaf(wv[j], v[j].x, o[0]);
-        o[1] = fmaf(wv[j], v[j].y, o[1]);
-        o[2] = fmaf(wv[j], v[j].z, o[2]);
-        o[3] = fmaf(wv[j], v[j].w, o[3]);
+      for (int j = 0; j < RCH / 8; ++j) {
+        const int s = min(c0 + sg + 8 * j, nrec - 1);
+        v[j] = *(const float4*)&pb[(size_t)s * PS + 4 + 4 * cq];
+        mv[j] = pb[(size_t)s * PS];
       }
     }
-  }
-  for (int c0 = 0; c0 < ntail; c0 += 256) {
-    const int n = c0 + tid;
-    float w = 0.0f;
-    int av = 0;
-    if (n < ntail) {
-      const float p = __builtin_amdgcn_exp2f(tail_logit(n) - M);
-      l += p;
-      w = p * Elem<DT>::get(c.tgV, tb + n);
-      av = min((int)c.tidxV[tb + n], k - 1);
-    }
-    __syncthreads();
-    wsp[tid] = w;
-    tav[tid] = av;
-    __syncthreads();
-    const int cn = min(256, ntail - c0);
-    for (int u = sg; u < cn; u += 8) {
-      const E* row = AVg + (size_t)tav[u] * D + 4 * cq;
-      const float wv = wsp[u];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) o[i] = fmaf(wv, Elem<DT>::get(row, i), o[i]);
+    for (int j = 0; j < RCH / 8; ++j) {
+      const float w = c0 + sg + 8 * j < nrec ? __builtin_amdgcn_exp2f(mv[j] - M) : 0.0f;
+      o[0] = fmaf(w, v[j].x, o[0]);
+      o[1] = fmaf(w, v[j].y, o[1]);
+      o[2] = fmaf(w, v[j].z, o[2]);
+      o[3] = fmaf(w, v[j].w, o[3]);
     }
   }
   l = wave_sum_dpp(l);
@@ -981,14 +1077,13 @@ static void launch_steps(const Geo& g, const Cache& c, const DecWs& dw, const vo
   const int L = g.dsplit;
   int nst = 0;
   for (int b = 0; b < g.B; ++b) nst += g.H * ((g.S[b] + L - 1) / L);
-  const int nres = app ? g.B * g.H * 2 : 0;
+  const int ntb = g.B * g.H;  // tail workgroups
   if (L == 2048) {
-    AKV_TIMED("k_dec_stream", st, (k_dec_stream<DT, GQ, 8><<<nst + nres, 256, 0, st>>>(g, c, dw, nst, n_app, kn, vn)));
+    AKV_TIMED("k_dec_stream", st, (k_dec_stream<DT, GQ, 8><<<nst + ntb, 256, 0, st>>>(g, c, dw, nst, n_app, kn, vn)));
   } else {
-    AKV_TIMED("k_dec_stream", st, (k_dec_stream<DT, GQ, 4><<<nst + nres, 256, 0, st>>>(g, c, dw, nst, n_app, kn, vn)));
+    AKV_TIMED("k_dec_stream", st, (k_dec_stream<DT, GQ, 4><<<nst + ntb, 256, 0, st>>>(g, c, dw, nst, n_app, kn, vn)));
   }
-  AKV_TIMED("k_dec_merge", st,
-            (k_dec_merge<DT, GQ><<<g.B * g.Hq, 256, 0, st>>>(g, c, dw, n_app + (app ? 1 : 0), out, out_dtype)));
+  AKV_TIMED("k_dec_merge", st, (k_dec_merge<DT, GQ><<<g.B * g.Hq, 256, 0, st>>>(g, dw, out, out_dtype)));
 }
 
 template <int DT>
