@@ -35,9 +35,6 @@
 namespace akv {
 
 constexpr int PS = 4 + AKV_D;  // split record: max, sum, 2 pad, output[D]
-constexpr int DEC_ASTG = 64;   // value-anchor rows staged in LDS per split
-constexpr int DEC_RCW = 512;   // anchor window of the per-anchor value weights
-constexpr int DEC_VCH = 128;   // value residuals staged per chunk
 
 __device__ inline float level(int code) {
   // 0 -> -L1, 1 -> -L0, 2 -> +L0, 3 -> +L1
@@ -306,27 +303,33 @@ __global__ __launch_bounds__(256) void k_dec_front(Geo g, Cache c, DecWs dw, con
 }
 
 // ------------------------------------------------------------------ append resolution
-// Resolves the appended token of (request b, head h, side) from the screening
-// scores of k_dec_front: the best anchor by |cos| is certified when its margin
-// over the runner-up exceeds the fp32 error bound; otherwise every anchor
-// within the bound is rescored with the canonical fp64 formula (ties to the
-// lowest index).  The coefficient is the canonical fp64 projection rounded to
-// the stored dtype.  Whole-block call; the record goes to tail slot n_app and
-// to *out_idx / *out_gamma (LDS).
+// Resolves the appended token of (request b, head h) on both sides at once
+// (waves 0-1: keys, waves 2-3: values) from the screening scores of
+// k_dec_front: the best anchor by |cos| is certified when its margin over the
+// runner-up exceeds the fp32 error bound; otherwise every anchor within the
+// bound is rescored with the canonical fp64 formula (ties to the lowest
+// index).  The coefficient is the canonical fp64 projection rounded to the
+// stored dtype.  Whole-workgroup call; the records go to tail slot n_app and
+// to out_idx[side] / out_gamma[side] (LDS).
 template <int DT>
-__device__ void append_resolve(const Geo& g, const Cache& c, const DecWs& dw, int b, int h, int side, int n_app,
-                               const void* xin, float* fr, double* dr, int* ir, int* out_idx, float* out_gamma) {
+__device__ void append_resolve(const Geo& g, const Cache& c, const DecWs& dw, int b, int h, int n_app,
+                               const void* kin, const void* vin, int* out_idx, float* out_gamma) {
   using E = typename Elem<DT>::T;
   constexpr int D = AKV_D;
+  __shared__ float fr[2][3];
+  __shared__ int ir[2];
+  __shared__ double dr[4];
+  __shared__ int di[4];
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int side = wave >> 1, lt = tid & 127;
   const int k = g.k[b], kp = (k + 3) & ~3, nab = (k + 255) / 256;
   const size_t ko = (size_t)g.prefK[b] * g.H + (size_t)h * k;
   const size_t ab = (size_t)g.prefKp[b] * g.H + (size_t)h * kp;
-  const E* x = (const E*)xin + ((size_t)b * g.H + h) * D;
+  const E* x = (const E*)(side ? vin : kin) + ((size_t)b * g.H + h) * D;
   const E* A = (const E*)(side ? c.ancV : c.ancK) + ko * D;
   const double* nrm = (side ? c.nrmV : c.nrmK) + ko;
   const float* sc = dw.asc + (size_t)side * g.H * g.prefKp[g.B] + ab;
-  if (wave == 0) {
+  if ((wave & 1) == 0) {
     const float x0 = Elem<DT>::get(x, 2 * lane), x1 = Elem<DT>::get(x, 2 * lane + 1);
     const float ss = wave_sum(x0 * x0 + x1 * x1);
     const float xn = sqrtf(ss) * (1.0f + 1e-5f);
@@ -341,20 +344,20 @@ __device__ void append_resolve(const Geo& g, const Cache& c, const DecWs& dw, in
     }
     top2_wave(b1, b2, i1);
     if (lane == 0) {
-      fr[0] = b1;
-      fr[1] = b2;
-      fr[2] = xn * ((float)D * 1.1920929e-7f + 2.3841858e-7f) * 1.01f + 1e-30f;
-      ir[0] = i1;
+      fr[side][0] = b1;
+      fr[side][1] = b2;
+      fr[side][2] = xn * ((float)D * 1.1920929e-7f + 2.3841858e-7f) * 1.01f + 1e-30f;
+      ir[side] = i1;
     }
   }
   __syncthreads();
-  const float b1 = fr[0], b2 = fr[1], eps = fr[2];
-  int best = ir[0];
-  if (!(b1 - b2 > 2.0f * eps + b1 * 9.094947e-13f)) {
+  const float b1 = fr[side][0], b2 = fr[side][1], eps = fr[side][2];
+  const bool certified = b1 - b2 > 2.0f * eps + b1 * 9.094947e-13f;
+  double bc = -INFINITY;
+  int bi = 0x7fffffff;
+  if (!certified) {
     const float band = b1 - 2.0f * eps - b1 * 9.094947e-13f;
-    double bc = -INFINITY;
-    int bi = 0x7fffffff;
-    for (int a = tid; a < k; a += 256) {
+    for (int a = lt; a < k; a += 128) {
       if (sc[a] < band) continue;
       const double d = dot64_seq<DT>(x, A + (size_t)a * D, D);
       const double cc = nrm[a] > 0.0 ? (d * d) / nrm[a] : -1.0;
@@ -374,19 +377,16 @@ __device__ void append_resolve(const Geo& g, const Cache& c, const DecWs& dw, in
     }
     if (lane == 0) {
       dr[wave] = bc;
-      ir[1 + wave] = bi;
+      di[wave] = bi;
     }
-    __syncthreads();
-    bc = dr[0];
-    bi = ir[1];
-    for (int v = 1; v < 4; ++v)
-      if (dr[v] > bc || (dr[v] == bc && ir[1 + v] < bi)) {
-        bc = dr[v];
-        bi = ir[1 + v];
-      }
-    best = bi;
   }
-  if (tid == 0) {
+  __syncthreads();
+  if (lt == 0) {
+    int best = ir[side];
+    if (!certified) {
+      const int w0 = 2 * side;
+      best = (dr[w0 + 1] > dr[w0] || (dr[w0 + 1] == dr[w0] && di[w0 + 1] < di[w0])) ? di[w0 + 1] : di[w0];
+    }
     const double n = nrm[best];
     const double d = dot64_seq<DT>(x, A + (size_t)best * D, D);
     const double g64 = n > 0.0 ? d / n : 0.0;
@@ -394,8 +394,8 @@ __device__ void append_resolve(const Geo& g, const Cache& c, const DecWs& dw, in
     const size_t ti = ((size_t)b * g.H + h) * g.max_append + n_app;
     (side ? c.tidxV : c.tidxK)[ti] = (uint16_t)best;
     Elem<DT>::put(side ? c.tgV : c.tgK, ti, gb);
-    *out_idx = best;
-    *out_gamma = gb;
+    out_idx[side] = best;
+    out_gamma[side] = gb;
   }
   __syncthreads();
 }
@@ -403,13 +403,9 @@ __device__ void append_resolve(const Geo& g, const Cache& c, const DecWs& dw, in
 template <int DT>
 __global__ __launch_bounds__(256) void k_app_finish(Geo g, Cache c, DecWs dw, int n_app, const void* kin,
                                                     const void* vin) {
-  __shared__ float fr[4];
-  __shared__ double dr[4];
-  __shared__ int ir[5];
-  __shared__ int oi;
-  __shared__ float og;
-  const int side = blockIdx.x & 1, bh = blockIdx.x >> 1;
-  append_resolve<DT>(g, c, dw, bh / g.H, bh % g.H, side, n_app, side ? vin : kin, fr, dr, ir, &oi, &og);
+  __shared__ int oi[2];
+  __shared__ float og[2];
+  append_resolve<DT>(g, c, dw, blockIdx.x / g.H, blockIdx.x % g.H, n_app, kin, vin, oi, og);
 }
 
 // ------------------------------------------------------------------ tail
@@ -423,9 +419,6 @@ __device__ void tail_block(const Geo& g, const Cache& c, const DecWs& dw, int bh
                            const void* vin, unsigned char* pool) {
   using E = typename Elem<DT>::T;
   constexpr int D = AKV_D, TCH = 256;
-  __shared__ float fr[4];
-  __shared__ double dr[4];
-  __shared__ int ir[5];
   __shared__ int t_idx[2];
   __shared__ float t_g[2];
   __shared__ float red[4][GQ];
@@ -439,10 +432,7 @@ __device__ void tail_block(const Geo& g, const Cache& c, const DecWs& dw, int bh
   const int nsp = (S + g.dsplit - 1) / g.dsplit;
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const bool app = kin != nullptr;
-  if (app) {
-    append_resolve<DT>(g, c, dw, b, h, 0, n_app, kin, fr, dr, ir, &t_idx[0], &t_g[0]);
-    append_resolve<DT>(g, c, dw, b, h, 1, n_app, vin, fr, dr, ir, &t_idx[1], &t_g[1]);
-  }
+  if (app) append_resolve<DT>(g, c, dw, b, h, n_app, kin, vin, t_idx, t_g);
   const int ntail = n_app + (app ? 1 : 0);
   const size_t ko = (size_t)g.prefK[b] * g.H + (size_t)h * k;
   const float* SKh = dw.SK + ((size_t)g.prefKp[b] * g.H + (size_t)h * kp) * GQ;
@@ -585,28 +575,46 @@ __device__ inline void load_coef(const void* base, size_t i0, float* v) {
 }
 __device__ inline unsigned long long low_bits(int n) { return n >= 64 ? ~0ull : ((1ull << n) - 1ull); }
 
+// Per-wave LDS of the streaming kernel.
+constexpr int SW_VCH = 64;  // value residuals staged per chunk
+constexpr int SW_ACH = 64;  // anchors per weight window
+constexpr int SW_AST = 16;  // value-anchor rows staged per wave
+template <int DT, int GQ>
+struct alignas(16) StreamWaveLds {
+  uint32_t vcode[SW_VCH][8];
+  float vsc[SW_VCH][4];
+  float vp[SW_VCH][GQ];
+  float wacc[SW_ACH][GQ];
+  float2 lvl[16];  // the two levels of a coordinate pair, by its 4-bit code
+  typename Elem<DT>::T avs[SW_AST * AKV_D];
+};
+
+// Orders this wave's LDS writes before its later LDS reads (and vice versa).
+__device__ inline void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
 // Grid: nst split workgroups, then one tail workgroup per (request, KV head)
 // (which first resolves this step's appended token when kin != nullptr).
+// A split of 256 R sorted slots is processed as four independent wave
+// sub-splits of 64 R slots (own softmax statistics, value residuals, anchor
+// weights); one barrier at the end combines them, and the inverse rotation is
+// applied once per query head.
 template <int DT, int GQ, int R>
 __global__ __launch_bounds__(256) void k_dec_stream(Geo g, Cache c, DecWs dw, int nst, int n_app, const void* kin,
                                                     const void* vin) {
   using E = typename Elem<DT>::T;
-  constexpr int D = AKV_D, L = 256 * R, PER = 16 / sizeof(E);
-  constexpr int NAV = DEC_ASTG * D / PER / 256;
-  __shared__ __align__(16) uint32_t vcode[DEC_VCH][8];
-  __shared__ float vsc[DEC_VCH][4];
-  __shared__ __align__(16) float vp[DEC_VCH][GQ];
-  __shared__ float redm[4][GQ], reds[4][GQ];
-  __shared__ float2 lvl2[16];  // levels of a coordinate pair by its 4-bit code
-
-  // LDS pool: per-anchor weights and staged value-anchor rows, later reused for
-  // the per-wave output partials (tail workgroups use it for their own arrays).
-  constexpr int WACC_B = DEC_RCW * GQ * 4, AVS_B = DEC_ASTG * D * (int)sizeof(E), ZY_B = 2 * 4 * GQ * D * 4;
-  constexpr int POOL_B = WACC_B + AVS_B > ZY_B ? WACC_B + AVS_B : ZY_B;
+  using WL = StreamWaveLds<DT, GQ>;
+  constexpr int D = AKV_D, LW = 64 * R, L = 4 * LW, PER = 16 / sizeof(E);
+  constexpr int NAVW = SW_AST * D / PER / 64;  // 16-byte anchor-row chunks per lane
+  constexpr int ZY_B = 2 * 4 * GQ * D * 4;
+  constexpr int WL_B = 4 * (int)sizeof(WL);
+  constexpr int TAIL_B = 256 * GQ * 4 + 256 * 4 + 8 * D * 4;
+  constexpr int POOL_B = (WL_B > ZY_B ? WL_B : ZY_B) > TAIL_B ? (WL_B > ZY_B ? WL_B : ZY_B) : TAIL_B;
   __shared__ __align__(16) unsigned char pool[POOL_B];
-  float(*wacc)[GQ] = (float(*)[GQ])pool;
-  E* avs = (E*)(pool + WACC_B);
-  static_assert(POOL_B >= 256 * GQ * 4 + 256 * 4 + 8 * D * 4, "LDS pool too small for the tail workgroup");
+  __shared__ float wm[4][GQ], wl[4][GQ];
   if ((int)blockIdx.x >= nst) {
     tail_block<DT, GQ>(g, c, dw, (int)blockIdx.x - nst, n_app, kin, vin, pool);
     return;
@@ -627,254 +635,196 @@ __global__ __launch_bounds__(256) void k_dec_stream(Geo g, Cache c, DecWs dw, in
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const float* SKh = dw.SK + ((size_t)g.prefKp[b] * g.H + (size_t)h * kp) * GQ;
   const E* AVg = (const E*)c.ancV + ko * D;
-  for (int i = tid; i < GQ * DEC_RCW; i += 256) (&wacc[0][0])[i] = 0.0f;
-  if (tid < 16) lvl2[tid] = make_float2(level(tid & 3), level(tid >> 2));
+  WL& W = ((WL*)pool)[wave];
 
-  // ---- round 1: records, flag words, the split's anchor and residual ranges.
-  const int i0 = s0 + tid * R;
-  const bool any = i0 < s1;
-  uint16_t ik[R], iv[R];
-  float gk[R], gv[R];
-  unsigned long long wk = 0, wv = 0;
-  int pck = 0, pcv = 0;
-  if (any) {
-    load_u16<R>(c.idxK + so + i0, ik);
-    load_u16<R>(c.idxV + so + i0, iv);
-    load_coef<DT, R>(c.gK, so + i0, gk);
-    load_coef<DT, R>(c.gV, so + i0, gv);
-    wk = c.maskK[wo + (i0 >> 6)];
-    wv = c.maskV[wo + (i0 >> 6)];
-    pck = c.pcK[wo + (i0 >> 6)];
-    pcv = c.pcV[wo + (i0 >> 6)];
-  } else {
+  float za[GQ][2], ya[GQ][2], mw[GQ], lsw[GQ];
 #pragma unroll
-    for (int r = 0; r < R; ++r) {
-      ik[r] = 0;
-      iv[r] = 0;
-      gk[r] = 0.0f;
-      gv[r] = 0.0f;
-    }
+  for (int jj = 0; jj < GQ; ++jj) {
+    za[jj][0] = za[jj][1] = ya[jj][0] = ya[jj][1] = 0.0f;
+    mw[jj] = -INFINITY;
+    lsw[jj] = 0.0f;
   }
-  const int a_lo = c.idxV[so + s0], a_hi = c.idxV[so + s1 - 1];
-  const int pv_lo = c.pcV[wo + (s0 >> 6)];
-  const int w1 = (s1 - 1) >> 6;
-  const int pv_hi = c.pcV[wo + w1] + __popcll(c.maskV[wo + w1] & low_bits(s1 - 64 * w1));
-  const int nrange = a_hi - a_lo + 1;
-  const int nstage = min(nrange, DEC_ASTG);
-  const int nvres = pv_hi - pv_lo;
+  const int ws0 = s0 + wave * LW, ws1 = min(s1, ws0 + LW);
+  if (ws0 < ws1) {
+    for (int i = lane; i < SW_ACH * GQ; i += 64) (&W.wacc[0][0])[i] = 0.0f;
+    if (lane < 16) W.lvl[lane] = make_float2(level(lane & 3), level(lane >> 2));
 
-  // ---- round 2: anchor scores, key-residual terms, value-anchor rows, first value-residual chunk.
-  const int sh = i0 & 63;
-  uint32_t vmask = 0;
-#pragma unroll
-  for (int r = 0; r < R; ++r)
-    if (i0 + r < s1) vmask |= 1u << r;
-  const uint32_t bk = any ? ((uint32_t)(wk >> sh) & vmask) : 0u;
-  const uint32_t bv = any ? ((uint32_t)(wv >> sh) & vmask) : 0u;
-  pck += __popcll(wk & low_bits(sh));
-  pcv += __popcll(wv & low_bits(sh));
-  float lg[R][GQ], rk[R][GQ];
-#pragma unroll
-  for (int r = 0; r < R; ++r) {
-    load_g<GQ>(SKh + (size_t)min((int)ik[r], k - 1) * GQ, lg[r]);
-    if ((bk >> r) & 1u) {
-      load_g<GQ>(dw.RK + (size_t)(pck + __popc(bk & ((1u << r) - 1u))) * GQ, rk[r]);
+    // ---- round 1: records and flag words of this wave's slots.
+    const int i0 = ws0 + lane * R;
+    const bool any = i0 < ws1;
+    uint16_t ik[R], iv[R];
+    float gk[R], gv[R];
+    unsigned long long wk = 0, wv = 0;
+    int pck = 0, pcv = 0;
+    if (any) {
+      load_u16<R>(c.idxK + so + i0, ik);
+      load_u16<R>(c.idxV + so + i0, iv);
+      load_coef<DT, R>(c.gK, so + i0, gk);
+      load_coef<DT, R>(c.gV, so + i0, gv);
+      wk = c.maskK[wo + (i0 >> 6)];
+      wv = c.maskV[wo + (i0 >> 6)];
+      pck = c.pcK[wo + (i0 >> 6)];
+      pcv = c.pcV[wo + (i0 >> 6)];
     } else {
-#pragma unroll
-      for (int jj = 0; jj < GQ; ++jj) rk[r][jj] = 0.0f;
-    }
-  }
-  uint4 avr[NAV];
-#pragma unroll
-  for (int i = 0; i < NAV; ++i) {
-    const int ch = tid + 256 * i;
-    const int r = ch / (D / PER), col = (ch % (D / PER)) * PER;
-    avr[i] = r < nstage ? *(const uint4*)(AVg + (size_t)(a_lo + r) * D + col) : make_uint4(0, 0, 0, 0);
-  }
-  const int nv0 = min(nvres, DEC_VCH);
-  uint4 vcr = make_uint4(0, 0, 0, 0);
-  if (tid < 2 * nv0) vcr = ((const uint4*)(c.codesV + (size_t)(pv_lo + (tid >> 1)) * (D / 4)))[tid & 1];
-  float vsr[2];
-#pragma unroll
-  for (int u = 0; u < 2; ++u) {
-    const int f = tid + 256 * u;
-    vsr[u] = f < nv0 * (D / G) ? c.scalesV[(size_t)pv_lo * (D / G) + f] : 0.0f;
-  }
-
-  // ---- logits and the split's softmax statistics.
-#pragma unroll
-  for (int r = 0; r < R; ++r)
-#pragma unroll
-    for (int jj = 0; jj < GQ; ++jj) lg[r][jj] = fmaf(gk[r], lg[r][jj], rk[r][jj]);
-  float mj[GQ];
-#pragma unroll
-  for (int jj = 0; jj < GQ; ++jj) {
-    float v = -INFINITY;
-#pragma unroll
-    for (int r = 0; r < R; ++r)
-      if ((vmask >> r) & 1u) v = fmaxf(v, lg[r][jj]);
-    v = wave_max_dpp(v);
-    if (lane == 0) redm[wave][jj] = v;
-  }
-  __syncthreads();
-#pragma unroll
-  for (int jj = 0; jj < GQ; ++jj) mj[jj] = fmaxf(fmaxf(redm[0][jj], redm[1][jj]), fmaxf(redm[2][jj], redm[3][jj]));
-  float ls[GQ];
-#pragma unroll
-  for (int jj = 0; jj < GQ; ++jj) {
-    ls[jj] = 0.0f;
-#pragma unroll
-    for (int r = 0; r < R; ++r) {
-      const float p = ((vmask >> r) & 1u) ? __builtin_amdgcn_exp2f(lg[r][jj] - mj[jj]) : 0.0f;
-      lg[r][jj] = p;
-      ls[jj] += p;
-    }
-  }
-#pragma unroll
-  for (int jj = 0; jj < GQ; ++jj) {
-    const float v = wave_sum_dpp(ls[jj]);
-    if (lane == 0) reds[wave][jj] = v;
-  }
-  // Stage the value-anchor rows and the first value-residual chunk.
-#pragma unroll
-  for (int i = 0; i < NAV; ++i) {
-    const int ch = tid + 256 * i;
-    const int r = ch / (D / PER), col = (ch % (D / PER)) * PER;
-    *(uint4*)(&avs[r * D + col]) = avr[i];
-  }
-  if (tid < 2 * nv0) *(uint4*)(&vcode[tid >> 1][4 * (tid & 1)]) = vcr;
-#pragma unroll
-  for (int u = 0; u < 2; ++u) {
-    const int f = tid + 256 * u;
-    if (f < nv0 * (D / G)) vsc[f / (D / G)][f % (D / G)] = vsr[u];
-  }
-
-  // ---- value residuals: lane = coordinate pair, wave = every 4th residual,
-  // all query heads at once; staged DEC_VCH residuals at a time.
-  const int grp = (2 * lane) / G;
-  const int nsh = 4 * (lane & 7);
-  float za[GQ][2];
-#pragma unroll
-  for (int jj = 0; jj < GQ; ++jj) za[jj][0] = za[jj][1] = 0.0f;
-  auto vres_acc = [&](uint32_t word, float sgv, const float* pv) {
-    const float2 lv = lvl2[(word >> nsh) & 15];
-    const float z0 = sgv * lv.x, z1 = sgv * lv.y;
-#pragma unroll
-    for (int jj = 0; jj < GQ; ++jj) {
-      za[jj][0] = fmaf(pv[jj], z0, za[jj][0]);
-      za[jj][1] = fmaf(pv[jj], z1, za[jj][1]);
-    }
-  };
-  for (int cb = 0; cb < nvres; cb += DEC_VCH) {
-    const int nv = min(DEC_VCH, nvres - cb);
-    if (cb > 0) {
-      __syncthreads();
-      if (tid < 2 * nv)
-        *(uint4*)(&vcode[tid >> 1][4 * (tid & 1)]) =
-            ((const uint4*)(c.codesV + (size_t)(pv_lo + cb + (tid >> 1)) * (D / 4)))[tid & 1];
-      for (int f = tid; f < nv * (D / G); f += 256)
-        vsc[f / (D / G)][f % (D / G)] = c.scalesV[(size_t)(pv_lo + cb) * (D / G) + f];
-    }
-    // probabilities of this chunk's residual slots, written by their owners
-#pragma unroll
-    for (int r = 0; r < R; ++r)
-      if ((bv >> r) & 1u) {
-        const int li = pcv + __popc(bv & ((1u << r) - 1u)) - pv_lo - cb;
-        if (li >= 0 && li < nv) store_g<GQ>(&vp[li][0], lg[r]);
-      }
-    __syncthreads();
-    int e = wave;
-    for (; e + 12 < nv; e += 16) {
-      uint32_t wd[4];
-      float sg4[4], pv[4][GQ];
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        wd[u] = vcode[e + 4 * u][lane >> 3];
-        sg4[u] = vsc[e + 4 * u][grp];
-        load_g<GQ>(&vp[e + 4 * u][0], pv[u]);
-      }
-#pragma unroll
-      for (int u = 0; u < 4; ++u) vres_acc(wd[u], sg4[u], pv[u]);
-    }
-    for (; e < nv; e += 4) {
-      float pv[GQ];
-      load_g<GQ>(&vp[e][0], pv);
-      vres_acc(vcode[e][lane >> 3], vsc[e][grp], pv);
-    }
-  }
-
-  // ---- per-anchor value weights over anchor windows, and y = sum_a w_a abar^V_a.
-  float ya[GQ][2];
-#pragma unroll
-  for (int jj = 0; jj < GQ; ++jj) ya[jj][0] = ya[jj][1] = 0.0f;
-  // Value-anchor row ra of the split, coordinates 2 lane and 2 lane + 1: from
-  // LDS for the first DEC_ASTG rows, else from global memory.
-  auto vpair = [&](const E* p, float& v0, float& v1) {
-    if constexpr (DT == 1) {
-      const uint32_t t = *(const uint32_t*)(p + 2 * lane);
-      v0 = bf2f((uint16_t)(t & 0xffffu));
-      v1 = bf2f((uint16_t)(t >> 16));
-    } else {
-      const float2 t = *(const float2*)(p + 2 * lane);
-      v0 = t.x;
-      v1 = t.y;
-    }
-  };
-  for (int wb = 0; wb < nrange; wb += DEC_RCW) {
-    const int wn = min(DEC_RCW, nrange - wb);
-    if (wb > 0) {  // the first window was cleared at the start
-      __syncthreads();
-      for (int i = tid; i < GQ * DEC_RCW; i += 256) (&wacc[0][0])[i] = 0.0f;
-      __syncthreads();
-    }
-    {
-      // A thread's valid slots are a prefix of its R slots, sorted by value
-      // anchor: a run of the first anchor aF, a run of the last anchor aL, and
-      // only when an anchor holds fewer slots than a thread, anchors between
-      // them (one atomic per such slot).
-      const int nval = __popc(vmask);
-      int aL = iv[0];
-#pragma unroll
-      for (int r = 1; r < R; ++r)
-        if (r < nval) aL = iv[r];
-      const int aF = iv[0];
-      float rf[GQ], rl[GQ];
-#pragma unroll
-      for (int jj = 0; jj < GQ; ++jj) rf[jj] = rl[jj] = 0.0f;
-      bool mid = false;
 #pragma unroll
       for (int r = 0; r < R; ++r) {
-        const bool v = r < nval;
-        const bool isF = v && (int)iv[r] == aF, isL = v && !isF && (int)iv[r] == aL;
-        mid |= v && !isF && !isL;
-        const float wF = isF ? gv[r] : 0.0f, wL = isL ? gv[r] : 0.0f;
-#pragma unroll
-        for (int jj = 0; jj < GQ; ++jj) {
-          rf[jj] = fmaf(lg[r][jj], wF, rf[jj]);
-          rl[jj] = fmaf(lg[r][jj], wL, rl[jj]);
-        }
-      }
-      const int oF = aF - a_lo - wb, oL = aL - a_lo - wb;
-      if (nval > 0 && oF >= 0 && oF < wn) {
-#pragma unroll
-        for (int jj = 0; jj < GQ; ++jj) atomicAdd(&wacc[oF][jj], rf[jj]);
-      }
-      if (nval > 0 && aL != aF && oL >= 0 && oL < wn) {
-#pragma unroll
-        for (int jj = 0; jj < GQ; ++jj) atomicAdd(&wacc[oL][jj], rl[jj]);
-      }
-      if (mid) {
-#pragma unroll
-        for (int r = 0; r < R; ++r) {
-          const int o = (int)iv[r] - a_lo - wb;
-          if (r < nval && (int)iv[r] != aF && (int)iv[r] != aL && o >= 0 && o < wn) {
-#pragma unroll
-            for (int jj = 0; jj < GQ; ++jj) atomicAdd(&wacc[o][jj], lg[r][jj] * gv[r]);
-          }
-        }
+        ik[r] = iv[r] = 0;
+        gk[r] = gv[r] = 0.0f;
       }
     }
-    __syncthreads();
+    const int nval = max(0, min(R, ws1 - i0));  // valid slots of this lane (a prefix)
+    const int sh = i0 & 63;
+    const uint32_t vmask = nval >= 32 ? ~0u : ((1u << nval) - 1u);
+    const uint32_t bk = (uint32_t)(wk >> sh) & vmask, bv = (uint32_t)(wv >> sh) & vmask;
+    pck += __popcll(wk & low_bits(sh));
+    pcv += __popcll(wv & low_bits(sh));
+    int aLast = iv[0];
+#pragma unroll
+    for (int r = 1; r < R; ++r)
+      if (r < nval) aLast = iv[r];
+    const int lastl = (ws1 - ws0 - 1) / R;  // last lane with a valid slot (uniform)
+    const int a_lo = __builtin_amdgcn_readfirstlane(iv[0]);
+    const int a_hi = __builtin_amdgcn_readlane(aLast, lastl);
+    const int pv_lo = __builtin_amdgcn_readfirstlane(pcv);
+    const int pv_hi = __builtin_amdgcn_readlane(pcv + __popc(bv), lastl);
+    const int nrange = a_hi - a_lo + 1, nstage = min(nrange, SW_AST), nvres = pv_hi - pv_lo;
+
+    // ---- round 2: anchor scores, key-residual terms, anchor rows, first value residuals.
+    float lg[R][GQ], rk[R][GQ];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      load_g<GQ>(SKh + (size_t)min((int)ik[r], k - 1) * GQ, lg[r]);
+      if ((bk >> r) & 1u) {
+        load_g<GQ>(dw.RK + (size_t)(pck + __popc(bk & ((1u << r) - 1u))) * GQ, rk[r]);
+      } else {
+#pragma unroll
+        for (int jj = 0; jj < GQ; ++jj) rk[r][jj] = 0.0f;
+      }
+    }
+    uint4 avr[NAVW];
+#pragma unroll
+    for (int i = 0; i < NAVW; ++i) {
+      const int ch = lane + 64 * i;
+      const int row = ch / (D / PER), col = (ch % (D / PER)) * PER;
+      avr[i] = row < nstage ? *(const uint4*)(AVg + (size_t)(a_lo + row) * D + col) : make_uint4(0, 0, 0, 0);
+    }
+    auto load_vchunk = [&](int cb, uint4& c0, uint4& c1, float* sv) {
+      const int nv = min(SW_VCH, nvres - cb);
+      if (lane < nv) {
+        const uint4* cp = (const uint4*)(c.codesV + (size_t)(pv_lo + cb + lane) * (D / 4));
+        c0 = cp[0];
+        c1 = cp[1];
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int f = lane + 64 * u;
+        sv[u] = f < nv * (D / G) ? c.scalesV[(size_t)(pv_lo + cb) * (D / G) + f] : 0.0f;
+      }
+    };
+    auto stage_vchunk = [&](int cb, const uint4& c0, const uint4& c1, const float* sv) {
+      const int nv = min(SW_VCH, nvres - cb);
+      if (lane < nv) {
+        *(uint4*)&W.vcode[lane][0] = c0;
+        *(uint4*)&W.vcode[lane][4] = c1;
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int f = lane + 64 * u;
+        if (f < nv * (D / G)) W.vsc[f / (D / G)][f % (D / G)] = sv[u];
+      }
+    };
+    uint4 vc0 = make_uint4(0, 0, 0, 0), vc1 = make_uint4(0, 0, 0, 0);
+    float vsv[4];
+    load_vchunk(0, vc0, vc1, vsv);
+
+    // ---- logits (base 2) and this wave's softmax statistics.
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+#pragma unroll
+      for (int jj = 0; jj < GQ; ++jj) lg[r][jj] = fmaf(gk[r], lg[r][jj], rk[r][jj]);
+#pragma unroll
+    for (int jj = 0; jj < GQ; ++jj) {
+      float v = -INFINITY;
+#pragma unroll
+      for (int r = 0; r < R; ++r)
+        if (r < nval) v = fmaxf(v, lg[r][jj]);
+      mw[jj] = wave_max_dpp(v);
+      float sum = 0.0f;
+#pragma unroll
+      for (int r = 0; r < R; ++r) {
+        const float p = r < nval ? __builtin_amdgcn_exp2f(lg[r][jj] - mw[jj]) : 0.0f;
+        lg[r][jj] = p;
+        sum += p;
+      }
+      lsw[jj] = wave_sum_dpp(sum);
+    }
+    // Stage the anchor rows and the first residual chunk.
+#pragma unroll
+    for (int i = 0; i < NAVW; ++i) {
+      const int ch = lane + 64 * i;
+      const int row = ch / (D / PER), col = (ch % (D / PER)) * PER;
+      *(uint4*)&W.avs[row * D + col] = avr[i];
+    }
+    stage_vchunk(0, vc0, vc1, vsv);
+
+    // ---- value residuals in the rotated basis: lane = coordinate pair.
+    const int grp = (2 * lane) / G, nsh = 4 * (lane & 7);
+    auto vres_acc = [&](uint32_t word, float sgv, const float* pv) {
+      const float2 lv = W.lvl[(word >> nsh) & 15];
+      const float z0 = sgv * lv.x, z1 = sgv * lv.y;
+#pragma unroll
+      for (int jj = 0; jj < GQ; ++jj) {
+        za[jj][0] = fmaf(pv[jj], z0, za[jj][0]);
+        za[jj][1] = fmaf(pv[jj], z1, za[jj][1]);
+      }
+    };
+    for (int cb = 0; cb < nvres; cb += SW_VCH) {
+      const int nv = min(SW_VCH, nvres - cb);
+      if (cb > 0) {
+        wave_lds_sync();
+        load_vchunk(cb, vc0, vc1, vsv);
+        stage_vchunk(cb, vc0, vc1, vsv);
+      }
+#pragma unroll
+      for (int r = 0; r < R; ++r)
+        if ((bv >> r) & 1u) {
+          const int li = pcv + __popc(bv & ((1u << r) - 1u)) - pv_lo - cb;
+          if (li >= 0 && li < nv) store_g<GQ>(&W.vp[li][0], lg[r]);
+        }
+      wave_lds_sync();
+      int e = 0;
+      for (; e + 3 < nv; e += 4) {
+        uint32_t wd[4];
+        float sg4[4], pv[4][GQ];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          wd[u] = W.vcode[e + u][lane >> 3];
+          sg4[u] = W.vsc[e + u][grp];
+          load_g<GQ>(&W.vp[e + u][0], pv[u]);
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) vres_acc(wd[u], sg4[u], pv[u]);
+      }
+      for (; e < nv; ++e) {
+        float pv[GQ];
+        load_g<GQ>(&W.vp[e][0], pv);
+        vres_acc(W.vcode[e][lane >> 3], W.vsc[e][grp], pv);
+      }
+    }
+
+    // ---- per-anchor value weights (first/last run of each lane's slots) and
+    // y = sum_a w_a abar^V_a, in windows of SW_ACH anchors.
+    auto vpair = [&](const E* p, float& v0, float& v1) {
+      if constexpr (DT == 1) {
+        const uint32_t t = *(const uint32_t*)(p + 2 * lane);
+        v0 = bf2f((uint16_t)(t & 0xffffu));
+        v1 = bf2f((uint16_t)(t >> 16));
+      } else {
+        const float2 t = *(const float2*)(p + 2 * lane);
+        v0 = t.x;
+        v1 = t.y;
+      }
+    };
     auto yacc = [&](float v0, float v1, const float* w) {
 #pragma unroll
       for (int jj = 0; jj < GQ; ++jj) {
@@ -882,33 +832,85 @@ __global__ __launch_bounds__(256) void k_dec_stream(Geo g, Cache c, DecWs dw, in
         ya[jj][1] = fmaf(w[jj], v1, ya[jj][1]);
       }
     };
-    const int wl = max(0, min(wn, nstage - wb));  // rows of this window staged in LDS
-    int a = wave;
-    for (; a + 12 < wl; a += 16) {
-      float v0[4], v1[4], w[4][GQ];
+    const int aF = iv[0];
+    float rf[GQ], rl[GQ];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        vpair(avs + (size_t)(wb + a + 4 * u) * D, v0[u], v1[u]);
-        load_g<GQ>(&wacc[a + 4 * u][0], w[u]);
+    for (int jj = 0; jj < GQ; ++jj) rf[jj] = rl[jj] = 0.0f;
+    bool mid = false;
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      const bool v = r < nval;
+      const bool isF = v && (int)iv[r] == aF, isL = v && !isF && (int)iv[r] == aLast;
+      mid |= v && !isF && !isL;
+      const float wF = isF ? gv[r] : 0.0f, wL = isL ? gv[r] : 0.0f;
+#pragma unroll
+      for (int jj = 0; jj < GQ; ++jj) {
+        rf[jj] = fmaf(lg[r][jj], wF, rf[jj]);
+        rl[jj] = fmaf(lg[r][jj], wL, rl[jj]);
       }
+    }
+    for (int wb = 0; wb < nrange; wb += SW_ACH) {
+      const int wn = min(SW_ACH, nrange - wb);
+      if (wb > 0) {
+        wave_lds_sync();
+        for (int i = lane; i < SW_ACH * GQ; i += 64) (&W.wacc[0][0])[i] = 0.0f;
+        wave_lds_sync();
+      }
+      const int oF = aF - a_lo - wb, oL = aLast - a_lo - wb;
+      if (nval > 0 && oF >= 0 && oF < wn) {
 #pragma unroll
-      for (int u = 0; u < 4; ++u) yacc(v0[u], v1[u], w[u]);
-    }
-    for (; a < wl; a += 4) {
-      float v0, v1, w[GQ];
-      vpair(avs + (size_t)(wb + a) * D, v0, v1);
-      load_g<GQ>(&wacc[a][0], w);
-      yacc(v0, v1, w);
-    }
-    for (; a < wn; a += 4) {  // rows past the staged ones
-      float v0, v1, w[GQ];
-      vpair(AVg + (size_t)(a_lo + wb + a) * D, v0, v1);
-      load_g<GQ>(&wacc[a][0], w);
-      yacc(v0, v1, w);
+        for (int jj = 0; jj < GQ; ++jj) atomicAdd(&W.wacc[oF][jj], rf[jj]);
+      }
+      if (nval > 0 && aLast != aF && oL >= 0 && oL < wn) {
+#pragma unroll
+        for (int jj = 0; jj < GQ; ++jj) atomicAdd(&W.wacc[oL][jj], rl[jj]);
+      }
+      if (mid) {
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+          const int o = (int)iv[r] - a_lo - wb;
+          if (r < nval && (int)iv[r] != aF && (int)iv[r] != aLast && o >= 0 && o < wn) {
+#pragma unroll
+            for (int jj = 0; jj < GQ; ++jj) atomicAdd(&W.wacc[o][jj], lg[r][jj] * gv[r]);
+          }
+        }
+      }
+      wave_lds_sync();
+      const int wl_ = max(0, min(wn, nstage - wb));  // rows of this window staged in LDS
+      int a = 0;
+      for (; a + 3 < wl_; a += 4) {
+        float v0[4], v1[4], w[4][GQ];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          vpair(W.avs + (size_t)(wb + a + u) * D, v0[u], v1[u]);
+          load_g<GQ>(&W.wacc[a + u][0], w[u]);
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) yacc(v0[u], v1[u], w[u]);
+      }
+      for (; a < wl_; ++a) {
+        float v0, v1, w[GQ];
+        vpair(W.avs + (size_t)(wb + a) * D, v0, v1);
+        load_g<GQ>(&W.wacc[a][0], w);
+        yacc(v0, v1, w);
+      }
+      for (; a < wn; ++a) {  // rows past the staged ones
+        float v0, v1, w[GQ];
+        vpair(AVg + (size_t)(a_lo + wb + a) * D, v0, v1);
+        load_g<GQ>(&W.wacc[a][0], w);
+        yacc(v0, v1, w);
+      }
     }
   }
 
-  // ---- split output: o = y + s * FWHT(zacc) / D per query head.
+  // ---- combine the four wave sub-splits: o = y + s * FWHT(zacc) / D per query head.
+  if (lane == 0) {
+#pragma unroll
+    for (int jj = 0; jj < GQ; ++jj) {
+      wm[wave][jj] = mw[jj];
+      wl[wave][jj] = lsw[jj];
+    }
+  }
   __syncthreads();  // the pool now holds the per-wave partials
   float(*zp)[GQ][D] = (float(*)[GQ][D])pool;
   float(*yp)[GQ][D] = (float(*)[GQ][D])(pool + 4 * GQ * D * 4);
@@ -922,20 +924,23 @@ __global__ __launch_bounds__(256) void k_dec_stream(Geo g, Cache c, DecWs dw, in
   const float s0v = sign_bit(g.sgnbits, 2 * lane), s1v = sign_bit(g.sgnbits, 2 * lane + 1);
   const float invD = 1.0f / (float)D;
   for (int jj = wave; jj < GQ; jj += 4) {
-    float z0 = 0.0f, z1 = 0.0f, y0 = 0.0f, y1 = 0.0f;
+    const float M = fmaxf(fmaxf(wm[0][jj], wm[1][jj]), fmaxf(wm[2][jj], wm[3][jj]));
+    float z0 = 0.0f, z1 = 0.0f, y0 = 0.0f, y1 = 0.0f, l = 0.0f;
 #pragma unroll
     for (int w = 0; w < 4; ++w) {
-      z0 += zp[w][jj][2 * lane];
-      z1 += zp[w][jj][2 * lane + 1];
-      y0 += yp[w][jj][2 * lane];
-      y1 += yp[w][jj][2 * lane + 1];
+      const float f = wm[w][jj] == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(wm[w][jj] - M);
+      z0 = fmaf(f, zp[w][jj][2 * lane], z0);
+      z1 = fmaf(f, zp[w][jj][2 * lane + 1], z1);
+      y0 = fmaf(f, yp[w][jj][2 * lane], y0);
+      y1 = fmaf(f, yp[w][jj][2 * lane + 1], y1);
+      l = fmaf(f, wl[w][jj], l);
     }
     fwht_wave_dpp(z0, z1, lane);
     const float o0 = y0 + s0v * (z0 * invD), o1 = y1 + s1v * (z1 * invD);
     float* pr = dw.part + ((size_t)g.prefSp[b] * Hq + (size_t)(h * GQ + jj) * (nsp + 1) + sp) * PS;
     if (lane == 0) {
-      pr[0] = fmaxf(fmaxf(redm[0][jj], redm[1][jj]), fmaxf(redm[2][jj], redm[3][jj]));
-      pr[1] = reds[0][jj] + reds[1][jj] + reds[2][jj] + reds[3][jj];
+      pr[0] = M;
+      pr[1] = l;
     }
     *(float2*)&pr[4 + 2 * lane] = make_float2(o0, o1);
   }
@@ -1071,7 +1076,7 @@ static void launch_steps(const Geo& g, const Cache& c, const DecWs& dw, const vo
   AKV_TIMED("k_dec_front", st,
             k_dec_front<DT, GQ><<<nAK + nAV + nR, 256, 0, st>>>(g, c, dw, q, kn, vn, flags, nAK, nAV, sl2));
   if (!attn) {
-    AKV_TIMED("k_app_finish", st, k_app_finish<DT><<<g.B * g.H * 2, 256, 0, st>>>(g, c, dw, n_app, kn, vn));
+    AKV_TIMED("k_app_finish", st, k_app_finish<DT><<<g.B * g.H, 256, 0, st>>>(g, c, dw, n_app, kn, vn));
     return;
   }
   const int L = g.dsplit;
