@@ -102,8 +102,9 @@ struct Ws {
   uint8_t* flag;        // [b][h][S_b] selection marks
   float* QA;            // [b][h][m][k_b] q_w . abar^K_a
   int32_t* apos;        // [side][b][h][S_b] anchor index per position (-1: fixup pending)
-  unsigned long long* fix;  // fixup list entries
-  int32_t* fixcount;    // [2] list length, overflow guard
+  int32_t* fixt;        // [side][b][h][S_b] per-head fixup list: token positions (filled from the front)
+  float* fixb;          // same layout: the best fp32 score the contraction found for the token
+  int32_t* fixcount;    // [side][b][h] fixup list lengths
   float* gpos;          // [side][b][h][S_b] stored coefficient as fp32
   float* u;             // [side][b][h][S_b] utility, -1 for anchors
   uint8_t* sel;         // [side][b][h][S_b] residual flags

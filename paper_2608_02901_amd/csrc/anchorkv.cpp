@@ -282,7 +282,7 @@ extern "C" anchorkv_status anchorkv_plan_create(const anchorkv_config* cfg, int3
   p->w_QA = Wl.add(4 * TK * m);
   p->w_apos = Wl.add(4 * 2 * TS);
   p->w_fix = Wl.add(8 * 2 * TS);
-  p->w_fixcount = Wl.add(16);
+  p->w_fixcount = Wl.add(4 * 2 * (size_t)H * batch);
   p->w_gpos = Wl.add(4 * 2 * TS);
   p->w_u = Wl.add(4 * 2 * TS);
   p->w_sel = Wl.add(2 * TS);
@@ -369,7 +369,8 @@ static akv::Ws ws_ptrs(const anchorkv_plan* p, void* base) {
   w.flag = at<uint8_t>(base, p->w_flag);
   w.QA = at<float>(base, p->w_QA);
   w.apos = at<int32_t>(base, p->w_apos);
-  w.fix = at<unsigned long long>(base, p->w_fix);
+  w.fixt = at<int32_t>(base, p->w_fix);
+  w.fixb = (float*)(w.fixt + 2 * (size_t)p->geo.H * p->geo.prefS[p->geo.B]);
   w.fixcount = at<int32_t>(base, p->w_fixcount);
   w.gpos = at<float>(base, p->w_gpos);
   w.u = at<float>(base, p->w_u);
@@ -674,13 +675,13 @@ __global__ void k_init(Geo g, Cache c, Ws w) {
     c.header[4] = (uint32_t)g.H;
     c.header[5] = (uint32_t)g.D;
     c.header[6] = (uint32_t)g.dtype;
-    w.fixcount[0] = 0;
-    w.fixcount[1] = 0;
   }
   if (i < 4 * g.B) c.stats[i] = 0;
+  if (i < 2 * g.H * g.B) w.fixcount[i] = 0;
 }
 hipError_t launch_init(const Geo& g, const Cache& c, const Ws& w, hipStream_t st) {
-  AKV_TIMED("k_init", st, k_init<<<(4 * g.B + 255) / 256 + 1, 256, 0, st>>>(g, c, w));
+  const int n = 4 * g.B > 2 * g.H * g.B ? 4 * g.B : 2 * g.H * g.B;
+  AKV_TIMED("k_init", st, k_init<<<(n + 255) / 256, 256, 0, st>>>(g, c, w));
   return hipGetLastError();
 }
 }  // namespace akv

@@ -151,9 +151,11 @@ __global__ __launch_bounds__(256) void k_assign(Geo g, Ws w, Cache c, const void
         *apos = i1;
       } else {
         *apos = -1;
-        int slot = atomicAdd(&w.fixcount[0], 1);
-        w.fix[slot] = ((unsigned long long)b << 48) | ((unsigned long long)side << 40) |
-                      ((unsigned long long)h << 32) | (unsigned long long)t;
+        const int grp = (side * g.B + b) * g.H + h;
+        const int slot = atomicAdd(&w.fixcount[grp], 1);  // < S: a token is listed once
+        const size_t lo = (size_t)side * g.H * g.prefS[g.B] + (size_t)g.prefS[b] * g.H + (size_t)h * S;
+        w.fixt[lo + slot] = t;
+        w.fixb[lo + slot] = b1;
         atomicAdd(&c.stats[b * 4 + side], 1);
       }
     }
@@ -161,62 +163,205 @@ __global__ __launch_bounds__(256) void k_assign(Geo g, Ws w, Cache c, const void
 }
 
 // Exact resolution of the tokens whose fp32 margin did not certify the argmax.
-// One wave per listed token; the grid strides over the list (its length is
-// read on the device), so every wave exits once the list is exhausted.
+//
+// The fixup lists are kept per (side, request, head), so a task of 32 listed
+// tokens shares one anchor set.  One workgroup per task recomputes the
+// tokens' scores against every anchor of the head with the same MFMA
+// contraction as k_assign (its four waves take interleaved 32-anchor tiles,
+// read straight from memory with a two-tile prefetch).  With b1 the best fp32
+// score found for the token and eps its error bound, the exact argmax has an
+// fp32 score of at least b1 - 2 eps: its exact score is >= the exact score of
+// b1's anchor, which is >= b1 - eps, and the fp32 score is within eps of the
+// exact one.  Every anchor in that band is re-scored with the canonical fp64
+// formula (sequential fp64 dot d, c = d*d / ||a||^2, -1 for a zero anchor;
+// largest c, then lowest index).  A token with more than FIX_SLOTS band
+// members (a zero vector, many equal anchors) is resolved by a full scan.
+// The number of tasks is read on the device; the grid strides over them and
+// every workgroup exits once they are done.
+constexpr int FIX_SLOTS = 8;
+
+__device__ inline int wave_incl_scan_i(int v, int lane) {
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int u = __shfl_up(v, o, 64);
+    if (lane >= o) v += u;
+  }
+  return v;
+}
+
 template <int DT>
 __global__ __launch_bounds__(256) void k_fixup(Geo g, Ws w, Cache c, const void* Kin, const void* Vin) {
   using E = typename Elem<DT>::T;
-  __shared__ float xs[4][AKV_D];
+  using M = MF<DT>;
+  constexpr int NKS = AKV_D / M::KS;
+  constexpr int PER = 16 / sizeof(E);
+  __shared__ int ccnt[32];
+  __shared__ int cidx[32][FIX_SLOTS];
+  __shared__ double cval[32][FIX_SLOTS];
+  __shared__ int task[3];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int n = w.fixcount[0];
   const int D = AKV_D;
-  for (int e = blockIdx.x * 4 + wave; e < n; e += gridDim.x * 4) {
-    const unsigned long long ent = w.fix[e];
-    const int b = (int)(ent >> 48), side = (int)((ent >> 40) & 0xff), h = (int)((ent >> 32) & 0xff);
-    const int t = (int)(ent & 0xffffffffu);
+  const int ngrp = 2 * g.B * g.H;
+
+  // Total number of 32-token tasks (every wave computes it; the loop bound is uniform).
+  int ntask = 0;
+  for (int g0 = 0; g0 < ngrp; g0 += 64) {
+    const int gi = g0 + lane;
+    ntask += wave_sum_i(gi < ngrp ? (w.fixcount[gi] + 31) >> 5 : 0);
+  }
+
+  for (int q = blockIdx.x; q < ntask; q += gridDim.x) {
+    if (wave == 0) {
+      // The task's group: the first group whose inclusive task prefix exceeds q.
+      int grp = 0, first = 0, base = 0;
+      for (int g0 = 0; g0 < ngrp; g0 += 64) {
+        const int gi = g0 + lane;
+        const int v = gi < ngrp ? (w.fixcount[gi] + 31) >> 5 : 0;
+        const int incl = wave_incl_scan_i(v, lane);
+        const unsigned long long hit = __ballot(base + incl > q);
+        if (hit) {
+          const int L = __ffsll((long long)hit) - 1;
+          grp = g0 + L;
+          first = base + __shfl(incl - v, L, 64);
+          break;
+        }
+        base += __shfl(incl, 63, 64);
+      }
+      if (lane == 0) {
+        task[0] = grp;
+        task[1] = q - first;
+      }
+      if (lane < 32) ccnt[lane] = 0;
+    }
+    __syncthreads();
+    const int grp = task[0], chunk = task[1];
+    const int h = grp % g.H, b = (grp / g.H) % g.B, side = grp / (g.H * g.B);
     const int S = g.S[b], k = g.k[b];
-    const size_t xoff = ((size_t)g.prefS[b] * g.H + (size_t)h * S) * D;
-    const E* x = (const E*)(side ? Vin : Kin) + xoff + (size_t)t * D;
+    const size_t lo = (size_t)side * g.H * g.prefS[g.B] + (size_t)g.prefS[b] * g.H + (size_t)h * S;
+    const int r0 = chunk * 32, nr = min(32, w.fixcount[grp] - r0);
+    const int n = lane & 31, nn = min(n, nr - 1);
+    const int t = w.fixt[lo + r0 + nn];
+    const float b1 = w.fixb[lo + r0 + nn];
+    const E* X = (const E*)(side ? Vin : Kin) + ((size_t)g.prefS[b] * g.H + (size_t)h * S) * D;
     const size_t ko = (size_t)g.prefK[b] * g.H + (size_t)h * k;
     const E* A = (const E*)(side ? c.ancV : c.ancK) + ko * D;
     const float* inv = (side ? c.invV : c.invK) + ko;
     const double* nrm = (side ? c.nrmV : c.nrmK) + ko;
-    float x0 = Elem<DT>::get(x, 2 * lane), x1 = Elem<DT>::get(x, 2 * lane + 1);
-    xs[wave][2 * lane] = x0;
-    xs[wave][2 * lane + 1] = x1;
-    const float ss = wave_sum(fmaf(x0, x0, x1 * x1));
+    int32_t* apos = w.apos + lo;
+
+    typename M::frag xf[NKS];
+    float ss = 0.0f;
+#pragma unroll
+    for (int s = 0; s < NKS; ++s) {
+      xf[s] = M::load(X + (size_t)t * D, kofs(M::KS, s, lane));
+      if constexpr (DT == 1) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          float v = (float)xf[s][i];
+          ss = fmaf(v, v, ss);
+        }
+      } else {
+        ss = fmaf(xf[s], xf[s], ss);
+      }
+    }
+    ss += __shfl_xor(ss, 32, 64);
     const float eps = score_eps(ss, D);
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-    auto score = [&](int a) {
-      const E* row = A + (size_t)a * D;
-      float s = 0.0f;
-      for (int d = 0; d < D; ++d) s = fmaf(xs[wave][d], Elem<DT>::get(row, d), s);
-      return fabsf(s) * inv[a];
+    const float bnd = b1 - 2.0f * eps - b1 * 9.094947e-13f;
+
+    // Band collection: wave w takes anchor tiles w, w+4, ... (rows of the tile
+    // on M, tokens on N), prefetching two tiles ahead.
+    typename M::frag f0[NKS], f1[NKS];
+    auto fetch = [&](typename M::frag (&f)[NKS], int a0) {
+      const E* arow = A + (size_t)min(a0 + (lane & 31), k - 1) * D;
+#pragma unroll
+      for (int s = 0; s < NKS; ++s) f[s] = M::load(arow, kofs(M::KS, s, lane));
     };
-    float smax = -1.0f;
-    for (int a = lane; a < k; a += 64) smax = fmaxf(smax, score(a));
-    smax = wave_max(smax);
-    const float band = smax - 2.0f * eps - smax * 9.094947e-13f;
-    double bc = -INFINITY;
-    int bi = 0x7fffffff;
-    for (int a = lane; a < k; a += 64) {
-      if (score(a) < band) continue;
-      const double d = dot64_seq<DT>(x, A + (size_t)a * D, D);
-      const double cc = nrm[a] > 0.0 ? (d * d) / nrm[a] : -1.0;
-      if (cc > bc) { bc = cc; bi = a; }
+    auto tile = [&](const typename M::frag (&f)[NKS], int a0) {
+      f32x16 acc = {};
+#pragma unroll
+      for (int s = 0; s < NKS; ++s) acc = M::mma(f[s], xf[s], acc);
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int r = a0 + crow(e, lane);
+        if (r < k && n < nr && fabsf(acc[e]) * inv[r] >= bnd) {
+          const int j = atomicAdd(&ccnt[n], 1);
+          if (j < FIX_SLOTS) cidx[n][j] = r;
+        }
+      }
+    };
+    int a0 = wave * 32;
+    if (a0 < k) fetch(f0, a0);
+    if (a0 + 128 < k) fetch(f1, a0 + 128);
+    for (; a0 < k; a0 += 256) {
+      tile(f0, a0);
+      if (a0 + 256 < k) fetch(f0, a0 + 256);
+      if (a0 + 128 >= k) break;
+      tile(f1, a0 + 128);
+      if (a0 + 384 < k) fetch(f1, a0 + 384);
     }
-    // Wave argmax: largest c, then lowest index.
-    for (int o = 32; o > 0; o >>= 1) {
-      double oc = __shfl_xor(bc, o, 64);
-      int oi = __shfl_xor(bi, o, 64);
-      if (oc > bc || (oc == bc && oi < bi)) { bc = oc; bi = oi; }
+    __syncthreads();
+
+    // Canonical fp64 scores of the band members (one thread per member).
+    {
+      const int pn = threadIdx.x / FIX_SLOTS, pj = threadIdx.x % FIX_SLOTS;
+      const int cn = ccnt[pn];
+      if (pn < nr && cn <= FIX_SLOTS && pj < cn) {
+        const int a = cidx[pn][pj];
+        const int tp = w.fixt[lo + r0 + pn];
+        const double d = dot64_seq<DT>(X + (size_t)tp * D, A + (size_t)a * D, D);
+        cval[pn][pj] = nrm[a] > 0.0 ? (d * d) / nrm[a] : -1.0;
+      }
     }
-    if (lane == 0) {
-      w.apos[(size_t)side * g.H * g.prefS[g.B] + (size_t)g.prefS[b] * g.H + (size_t)h * S + t] = bi;
+    __syncthreads();
+    if (wave == 0) {
+      if (lane < nr) {
+        const int cn = ccnt[lane];
+        if (cn <= FIX_SLOTS) {
+          double bc = -INFINITY;
+          int bi = 0x7fffffff;
+          for (int j = 0; j < cn; ++j) {
+            const double cc = cval[lane][j];
+            const int a = cidx[lane][j];
+            if (cc > bc || (cc == bc && a < bi)) { bc = cc; bi = a; }
+          }
+          apos[t] = bi;
+        }
+      }
+      // Tokens with an overflowing band: full scan by the wave.
+      unsigned long long big = __ballot(lane < nr && ccnt[lane] > FIX_SLOTS);
+      while (big) {
+        const int L = __ffsll((long long)big) - 1;
+        big &= big - 1;
+        const int tp = __shfl(t, L, 64);
+        const float bl = __shfl(bnd, L, 64);
+        const E* x = X + (size_t)tp * D;
+        double bc = -INFINITY;
+        int bi = 0x7fffffff;
+        for (int a = lane; a < k; a += 64) {
+          const uint4* row = (const uint4*)(A + (size_t)a * D);
+          const uint4* xr = (const uint4*)x;
+          float s = 0.0f;
+          for (int i = 0; i < AKV_D / PER; ++i) {
+            const uint4 av = row[i], xv = xr[i];
+            const E* ea = (const E*)&av;
+            const E* ex = (const E*)&xv;
+#pragma unroll
+            for (int j = 0; j < PER; ++j) s = fmaf(Elem<DT>::get(ex, j), Elem<DT>::get(ea, j), s);
+          }
+          if (fabsf(s) * inv[a] < bl) continue;
+          const double d = dot64_seq<DT>(x, A + (size_t)a * D, D);
+          const double cc = nrm[a] > 0.0 ? (d * d) / nrm[a] : -1.0;
+          if (cc > bc || (cc == bc && a < bi)) { bc = cc; bi = a; }
+        }
+        for (int o = 32; o > 0; o >>= 1) {
+          const double oc = __shfl_xor(bc, o, 64);
+          const int oi = __shfl_xor(bi, o, 64);
+          if (oc > bc || (oc == bc && oi < bi)) { bc = oc; bi = oi; }
+        }
+        if (lane == 0) apos[tp] = bi;
+      }
     }
-    __builtin_amdgcn_wave_barrier();
+    __syncthreads();
   }
 }
 
@@ -225,10 +370,10 @@ hipError_t launch_assign(const Geo& g, const Ws& w, const Cache& c, const void* 
   for (int b = 0; b < g.B; ++b) nblk += g.H * ((g.S[b] + 127) / 128) * 2;
   if (g.dtype == 1) {
     AKV_TIMED("k_assign", st, k_assign<1><<<nblk, 256, 0, st>>>(g, w, c, K, V));
-    AKV_TIMED("k_fixup", st, k_fixup<1><<<1024, 256, 0, st>>>(g, w, c, K, V));
+    AKV_TIMED("k_fixup", st, k_fixup<1><<<512, 256, 0, st>>>(g, w, c, K, V));
   } else {
     AKV_TIMED("k_assign", st, k_assign<0><<<nblk, 256, 0, st>>>(g, w, c, K, V));
-    AKV_TIMED("k_fixup", st, k_fixup<0><<<1024, 256, 0, st>>>(g, w, c, K, V));
+    AKV_TIMED("k_fixup", st, k_fixup<0><<<512, 256, 0, st>>>(g, w, c, K, V));
   }
   return hipGetLastError();
 }

@@ -72,3 +72,46 @@ def test_edge_case_encode_and_decode(case):
     if case == "budget_all":
         free = wl.H * wl.seq_lens[0] - int(np.count_nonzero(exp["anchors"] >= 0))
         assert int(exp["sel_k"].sum()) == free and int(exp["sel_v"].sum()) == free
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_assignment_exact_ties_and_zero_tokens(dtype):
+    """Exact |cos| ties resolved to the lowest anchor index (Sec. 3.1 nearest
+    anchor, ties to the earliest anchor): 12 copies and 4 negated copies of one
+    token among the anchors, so every other copy has a 16-way tie; zero tokens
+    tie with every non-zero anchor (c = 0) and a zero anchor scores -1.  Both
+    exceed the per-token band slots of the exact resolution and take its
+    full-scan path; the fp32 margins of the rest take the slotted path."""
+    wl = _wl("ties_" + dtype, dtype=dtype, seq_lens=[900], anchor_count=64, anchor_frac=0.0,
+             n_outlier=0 if dtype == "f32" else 4)
+    print(f"[edge] ties {dtype}", flush=True)
+    layer = synth.make_layer(wl)
+    S, W = wl.seq_lens[0], wl.window
+    for X in (layer.K[0], layer.V[0]):
+        for h in range(wl.H):
+            X[h, 20:60] = X[h, 10]
+            X[h, 60:80] = -X[h, 10]
+            X[h, 100:130] = 0
+    base = np.r_[np.arange(20, 32), np.arange(60, 64), [100], np.arange(200, 500, 20)]
+    assert base.size == 64 - W
+    ov = np.stack([np.r_[base, np.arange(S - W, S)] for _ in range(wl.H)]).astype(np.int32)
+    cfg = make_cfg(wl)
+    plan = N.Plan(cfg, wl.seq_lens)
+    cache, ws, dws = gpu_encode(plan, layer, override=ov)
+    enc = oracle_encode(cfg, layer, 0, anchor_override=ov)
+    exp = akv.export(plan, cache.cpu().numpy(), 0, 0)
+    assert_request_parity(exp, enc, cfg)
+    # Copies and negated copies of token 10 go to the first duplicate anchor
+    # (index 0); zero tokens go to anchor 0 as well (the lowest c = 0 anchor).
+    for a in (exp["a_k"], exp["a_v"]):
+        assert (a[:, 10] == 0).all() and (a[:, 32:60] == 0).all() and (a[:, 64:80] == 0).all()
+        assert (a[:, 101:130] == 0).all()
+    assert int(exp["stats"][0]) > 0 and int(exp["stats"][1]) > 0
+    out = torch.empty(1, wl.Hq, wl.D, dtype=torch.float32, device="cuda")
+    akv.decode_attn(plan, cache, layer.q[0].cuda(), out, dws)
+    torch.cuda.synchronize()
+    G = cfg.quant_group or wl.D
+    Kh = R.reconstruct(layer.K[0].float().numpy(), enc, "K", G, cfg.seed)
+    Vh = R.reconstruct(layer.V[0].float().numpy(), enc, "V", G, cfg.seed)
+    ref = R.attention(Kh, Vh, layer.q[0, 0].float().numpy())
+    assert np.abs(out[0].cpu().numpy() - ref).max() <= (1e-4 if dtype == "f32" else 2e-3)
