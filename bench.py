@@ -65,6 +65,51 @@ def decode_bytes(plan, H, Hq, D, G, esz):
     return tot, stream
 
 
+def hbm_copy_gbs(torch, nbytes=1 << 30, reps=5):
+    """Device-to-device copy of nbytes (one plain copy kernel per call): bytes
+    read + written per second.  A reference for what a streaming kernel can
+    reach on this GPU, and the calibration kernel of the HBM traffic counters."""
+    src = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    e1.record()
+    torch.cuda.synchronize()
+    gbs = 2.0 * nbytes * reps / (e0.elapsed_time(e1) / 1e3) / 1e9
+    del src, dst
+    return gbs
+
+
+def traffic_from_profile(kernel, sources):
+    """HBM bytes per launch of `kernel` from the committed counter summary
+    (FETCH_SIZE + WRITE_SIZE, calibrated by a plain copy kernel), or None when
+    the kernel's sources changed since the counters were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", f"{kernel}_hbm_traffic_128k.md")
+    if not os.path.exists(path):
+        return None
+    h = hashlib.sha256()
+    for src in sources:
+        with open(os.path.join(ROOT, src), "rb") as f:
+            h.update(f.read())
+    fields = {}
+    with open(path) as f:
+        for line in f:
+            if line.startswith("- ") and ": " in line:
+                key, val = line[2:].split(": ", 1)
+                fields[key.strip()] = val.strip().strip("`")
+    if fields.get("source sha256") != h.hexdigest():
+        return None
+    try:
+        return float(fields["traffic bytes per launch"])
+    except (KeyError, ValueError):
+        return None
+
+
 def encode_flops(plan, H, D):
     """Similarity contraction of both sides on non-anchor rows: 2 sides x 2 FLOP
     x (S - k) x k x D per head."""
@@ -211,6 +256,11 @@ def main():
     assign_ms = ktimes["k_assign"][0]
     ach_e = fl / (assign_ms / 1e3) / 1e12
 
+    copy_gbs = hbm_copy_gbs(torch)
+    log(f"device copy {copy_gbs:.0f} GB/s (read + write)")
+    dec_sources = ["paper_2608_02901_amd/csrc/decode.hip", "paper_2608_02901_amd/csrc/akv_common.h"]
+    traffic = traffic_from_profile("k_dec_stream", dec_sources)
+
     cache_host = caches[0].cpu().numpy()
     ex = akv.export(plan, cache_host, 0, NS)
     fix_k, fix_v = int(ex["stats"][0]), int(ex["stats"][1])
@@ -244,8 +294,9 @@ def main():
         "kernel_avg_us": {k: round(v[0] * 1e3, 3) for k, v in ktimes.items()},
         "fixup_rows_layer0": [fix_k, fix_v],
         "roofline": {"bound": "hbm", "kernel": "k_dec_stream", "achieved": round(ach, 2), "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": None,
+                     "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": traffic,
                      "bytes_per_launch": sbytes},
+        "hbm_copy_gbs": round(copy_gbs, 1),
         "roofline_encode": {"bound": "mfma", "kernel": "k_assign", "achieved": round(ach_e, 2),
                             "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": round(ach_e / BF16_PEAK_TFLOPS, 4),
                             "flops_per_launch": fl},
