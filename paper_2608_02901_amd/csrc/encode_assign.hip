@@ -21,6 +21,13 @@
 
 namespace akv {
 
+// A score with its low 5 mantissa bits replaced by a tag is within 2^-18 of
+// its value (inflated by 1 %).
+__device__ inline float tag_score(float v, uint32_t tag) {
+  return __uint_as_float((__float_as_uint(v) & ~31u) | tag);
+}
+__device__ inline float tag_eps(float b1) { return b1 * 3.8528442e-6f; }
+
 __device__ inline float score_eps(float xnorm2, int D) {
   float xn = sqrtf(xnorm2) * (1.0f + 1e-5f);
   return xn * ((float)D * 1.1920929e-7f + 2.3841858e-7f) * 1.01f + 1e-30f;
@@ -98,8 +105,15 @@ __global__ __launch_bounds__(256) void k_assign(Geo g, Ws w, Cache c, const void
     if (threadIdx.x < STAGE) WS[buf][threadIdx.x] = prew;
   };
 
+  // Scores carry their row inside the 32-anchor tile in the low 5 mantissa
+  // bits (31 - row, so that equal scores favour the lower row); the tile of
+  // the best score is tracked per tile.  The tag moves a score by less than
+  // 2^-18 of its value, which the certification bound includes.
+  uint32_t tag[16];
+#pragma unroll
+  for (int e = 0; e < 16; ++e) tag[e] = 31u - (uint32_t)crow(e, lane);
   float b1 = -1.0f, b2 = -1.0f;
-  int i1 = 0;
+  int tb1 = 0;
   fetch(0);
   commit(0);
   __syncthreads();
@@ -116,20 +130,19 @@ __global__ __launch_bounds__(256) void k_assign(Geo g, Ws w, Cache c, const void
         auto af = M::load_lds(&AS[cur][(blk * 32 + (lane & 31)) * LDA], kofs(M::KS, s, lane));
         acc = M::mma(af, xf[s], acc);
       }
+      const float b1o = b1;
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
-        const int r = blk * 32 + crow(e, lane);
-        const float v = fabsf(acc[e]) * WS[cur][r];
-        const float nb2 = __builtin_amdgcn_fmed3f(b1, b2, v);
-        const bool gt = v > b1;
-        i1 = gt ? st * STAGE + r : i1;
+        const float v = tag_score(fabsf(acc[e]) * WS[cur][blk * 32 + crow(e, lane)], tag[e]);
+        b2 = __builtin_amdgcn_fmed3f(b1, b2, v);
         b1 = fmaxf(b1, v);
-        b2 = nb2;
       }
+      tb1 = b1 != b1o ? abase >> 5 : tb1;
     }
     if (st + 1 < nstage) commit(cur ^ 1);
     __syncthreads();
   }
+  int i1 = tb1 * 32 + (31 - (int)(__float_as_uint(b1) & 31u));
   // Merge the two lanes holding the same token (rows 0-3 / 4-7 of each 8).
   {
     const float ob1 = __shfl_xor(b1, 32, 64), ob2 = __shfl_xor(b2, 32, 64);
@@ -146,8 +159,8 @@ __global__ __launch_bounds__(256) void k_assign(Geo g, Ws w, Cache c, const void
     if (rk >= 0) {
       *apos = rk;
     } else {
-      const float eps = score_eps(ss, D);
-      if (b1 - b2 > 2.0f * eps + b1 * 9.094947e-13f) {
+      const float eps = score_eps(ss, D) + tag_eps(b1);
+      if (b1 - b2 > 2.0f * eps + b1 * 9.094947e-13f && i1 < k) {
         *apos = i1;
       } else {
         *apos = -1;
@@ -265,7 +278,7 @@ __global__ __launch_bounds__(256) void k_fixup(Geo g, Ws w, Cache c, const void*
       }
     }
     ss += __shfl_xor(ss, 32, 64);
-    const float eps = score_eps(ss, D);
+    const float eps = score_eps(ss, D) + tag_eps(b1);
     const float bnd = b1 - 2.0f * eps - b1 * 9.094947e-13f;
 
     // Band collection: wave w takes anchor tiles w, w+4, ... (rows of the tile
