@@ -21,12 +21,16 @@
 
 namespace akv {
 
-// A score with its low 5 mantissa bits replaced by a tag is within 2^-18 of
-// its value (inflated by 1 %).
+// A score with its low 4 mantissa bits replaced by a tag is within 2^-19 of
+// its value; the bound used is 2^-18 (inflated by 1 %).
 __device__ inline float tag_score(float v, uint32_t tag) {
-  return __uint_as_float((__float_as_uint(v) & ~31u) | tag);
+  return __uint_as_float((__float_as_uint(v) & ~15u) | tag);
 }
 __device__ inline float tag_eps(float b1) { return b1 * 3.8528442e-6f; }
+
+// Token groups of 32 per wave and tokens per workgroup of k_assign.
+constexpr int ASSIGN_NT = 2;
+constexpr int ASSIGN_TOK = 4 * 32 * ASSIGN_NT;
 
 __device__ inline float score_eps(float xnorm2, int D) {
   float xn = sqrtf(xnorm2) * (1.0f + 1e-5f);
@@ -46,11 +50,11 @@ __global__ __launch_bounds__(256) void k_assign(Geo g, Ws w, Cache c, const void
   __shared__ float WS[2][STAGE];
 
   int idx = blockIdx.x;
-  const int b = locate(g, 128, 2, idx);
+  const int b = locate(g, ASSIGN_TOK, 2, idx);
   const int side = idx & 1;
   idx >>= 1;
   const int S = g.S[b], k = g.k[b], D = AKV_D;
-  const int ntile = (S + 127) / 128;
+  const int ntile = (S + ASSIGN_TOK - 1) / ASSIGN_TOK;
   const int h = idx / ntile, tile = idx % ntile;
   const size_t xoff = ((size_t)g.prefS[b] * g.H + (size_t)h * S) * D;
   const E* X = (const E*)(side ? Vin : Kin) + xoff;
@@ -58,26 +62,31 @@ __global__ __launch_bounds__(256) void k_assign(Geo g, Ws w, Cache c, const void
   const E* A = (const E*)(side ? c.ancV : c.ancK) + ko * D;
   const float* inv = (side ? c.invV : c.invK) + ko;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int t = tile * 128 + wave * 32 + (lane & 31);
-  const int tc = min(t, S - 1);
 
-  // Token fragments (B operand) and the token's squared norm.
-  typename M::frag xf[NKS];
-  float ss = 0.0f;
+  // Token fragments (B operand) of the wave's ASSIGN_NT groups of 32 tokens,
+  // and the tokens' squared norms.
+  typename M::frag xf[ASSIGN_NT][NKS];
+  float ss[ASSIGN_NT];
 #pragma unroll
-  for (int s = 0; s < NKS; ++s) {
-    xf[s] = M::load(X + (size_t)tc * D, kofs(M::KS, s, lane));
-    if constexpr (DT == 1) {
+  for (int n = 0; n < ASSIGN_NT; ++n) {
+    const int t = tile * ASSIGN_TOK + (wave * ASSIGN_NT + n) * 32 + (lane & 31);
+    const int tc = min(t, S - 1);
+    ss[n] = 0.0f;
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        float v = (float)xf[s][i];
-        ss = fmaf(v, v, ss);
+    for (int s = 0; s < NKS; ++s) {
+      xf[n][s] = M::load(X + (size_t)tc * D, kofs(M::KS, s, lane));
+      if constexpr (DT == 1) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          float v = (float)xf[n][s][i];
+          ss[n] = fmaf(v, v, ss[n]);
+        }
+      } else {
+        ss[n] = fmaf(xf[n][s], xf[n][s], ss[n]);
       }
-    } else {
-      ss = fmaf(xf[s], xf[s], ss);
     }
+    ss[n] += __shfl_xor(ss[n], 32, 64);
   }
-  ss += __shfl_xor(ss, 32, 64);
 
   const int nstage = (k + STAGE - 1) / STAGE;
   uint4 pre[NLD];
@@ -105,71 +114,116 @@ __global__ __launch_bounds__(256) void k_assign(Geo g, Ws w, Cache c, const void
     if (threadIdx.x < STAGE) WS[buf][threadIdx.x] = prew;
   };
 
-  // Scores carry their row inside the 32-anchor tile in the low 5 mantissa
-  // bits (31 - row, so that equal scores favour the lower row); the tile of
-  // the best score is tracked per tile.  The tag moves a score by less than
-  // 2^-18 of its value, which the certification bound includes.
-  uint32_t tag[16];
+  // Scores carry their accumulator slot e (15 - e: within a lane the row
+  // grows with e, so equal scores favour the lower row) in the low 4
+  // mantissa bits; the tile of the best score is tracked per tile.  The tag
+  // moves a score by less than 2^-18 of its value, which the certification
+  // bound includes.  Every anchor fragment read from LDS feeds the MFMAs of
+  // all ASSIGN_NT token groups, and the scores of a tile are processed while
+  // the MFMAs of the next tile run (two accumulator sets, P and Q).
+  float b1[ASSIGN_NT], b2[ASSIGN_NT];
+  int tb1[ASSIGN_NT];
 #pragma unroll
-  for (int e = 0; e < 16; ++e) tag[e] = 31u - (uint32_t)crow(e, lane);
-  float b1 = -1.0f, b2 = -1.0f;
-  int tb1 = 0;
+  for (int n = 0; n < ASSIGN_NT; ++n) {
+    b1[n] = b2[n] = -1.0f;
+    tb1[n] = 0;
+  }
+  auto mma_tile = [&](f32x16 (&acc)[ASSIGN_NT], int buf, int blk) {
+#pragma unroll
+    for (int n = 0; n < ASSIGN_NT; ++n) acc[n] = f32x16{};
+#pragma unroll
+    for (int s = 0; s < NKS; ++s) {
+      auto af = M::load_lds(&AS[buf][(blk * 32 + (lane & 31)) * LDA], kofs(M::KS, s, lane));
+#pragma unroll
+      for (int n = 0; n < ASSIGN_NT; ++n) acc[n] = M::mma(af, xf[n][s], acc[n]);
+    }
+  };
+  auto load_ws = [&](float (&wsr)[16], int buf, int blk) {
+#pragma unroll
+    for (int e = 0; e < 16; ++e) wsr[e] = WS[buf][blk * 32 + crow(e, lane)];
+  };
+  auto scores = [&](const f32x16 (&acc)[ASSIGN_NT], const float (&wsr)[16], int abase) {
+#pragma unroll
+    for (int n = 0; n < ASSIGN_NT; ++n) {
+      const float b1o = b1[n];
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const float v = tag_score(fabsf(acc[n][e]) * wsr[e], 15u - (uint32_t)e);
+        b2[n] = __builtin_amdgcn_fmed3f(b1[n], b2[n], v);
+        b1[n] = fmaxf(b1[n], v);
+      }
+      tb1[n] = b1[n] != b1o ? abase >> 5 : tb1[n];
+    }
+  };
+  // Before the first tile, P holds a tile of zero scores, so that every
+  // stage has the same branch-free schedule; it only matters for a token
+  // whose every score is 0, which the certification sends to the fixup.
+  f32x16 accP[ASSIGN_NT], accQ[ASSIGN_NT];
+  float wsP[16], wsQ[16];
+#pragma unroll
+  for (int n = 0; n < ASSIGN_NT; ++n) accP[n] = f32x16{};
+#pragma unroll
+  for (int e = 0; e < 16; ++e) wsP[e] = 0.0f;
+  int pend = 0;         // anchor base of the tile whose scores are pending
+  bool pendQ = false;   // pending tile sits in Q (a last stage with one tile)
   fetch(0);
   commit(0);
   __syncthreads();
   for (int st = 0; st < nstage; ++st) {
     const int cur = st & 1;
     if (st + 1 < nstage) fetch(st + 1);
-#pragma unroll
-    for (int blk = 0; blk < STAGE / 32; ++blk) {
-      const int abase = st * STAGE + blk * 32;
-      if (abase >= k) break;
-      f32x16 acc = {};
-#pragma unroll
-      for (int s = 0; s < NKS; ++s) {
-        auto af = M::load_lds(&AS[cur][(blk * 32 + (lane & 31)) * LDA], kofs(M::KS, s, lane));
-        acc = M::mma(af, xf[s], acc);
-      }
-      const float b1o = b1;
-#pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const float v = tag_score(fabsf(acc[e]) * WS[cur][blk * 32 + crow(e, lane)], tag[e]);
-        b2 = __builtin_amdgcn_fmed3f(b1, b2, v);
-        b1 = fmaxf(b1, v);
-      }
-      tb1 = b1 != b1o ? abase >> 5 : tb1;
+    const int a0 = st * STAGE, a1 = a0 + 32;
+    // tile 0 of the stage into Q; the pending tile (P) is scored meanwhile
+    mma_tile(accQ, cur, 0);
+    scores(accP, wsP, pend);
+    load_ws(wsQ, cur, 0);
+    pend = a0;
+    pendQ = true;
+    if (a1 < k) {
+      mma_tile(accP, cur, 1);
+      scores(accQ, wsQ, a0);
+      load_ws(wsP, cur, 1);
+      pend = a1;
+      pendQ = false;
     }
     if (st + 1 < nstage) commit(cur ^ 1);
     __syncthreads();
   }
-  int i1 = tb1 * 32 + (31 - (int)(__float_as_uint(b1) & 31u));
-  // Merge the two lanes holding the same token (rows 0-3 / 4-7 of each 8).
-  {
-    const float ob1 = __shfl_xor(b1, 32, 64), ob2 = __shfl_xor(b2, 32, 64);
-    const int oi1 = __shfl_xor(i1, 32, 64);
-    const float top2 = fmaxf(fmaxf(b2, ob2), fminf(b1, ob1));
-    if (ob1 > b1 || (ob1 == b1 && oi1 < i1)) i1 = oi1;
-    b1 = fmaxf(b1, ob1);
-    b2 = top2;
-  }
-  if (lane < 32 && t < S) {
-    const size_t po = (size_t)g.prefS[b] * g.H + (size_t)h * S + t;
-    int32_t* apos = w.apos + (size_t)side * g.H * g.prefS[g.B] + po;
-    const int rk = w.rank[po];
-    if (rk >= 0) {
-      *apos = rk;
-    } else {
-      const float eps = score_eps(ss, D) + tag_eps(b1);
-      if (b1 - b2 > 2.0f * eps + b1 * 9.094947e-13f && i1 < k) {
-        *apos = i1;
+  if (pendQ) scores(accQ, wsQ, pend);
+  else scores(accP, wsP, pend);
+#pragma unroll
+  for (int n = 0; n < ASSIGN_NT; ++n) {
+    const int t = tile * ASSIGN_TOK + (wave * ASSIGN_NT + n) * 32 + (lane & 31);
+    int i1 = tb1[n] * 32 + crow(15 - (int)(__float_as_uint(b1[n]) & 15u), lane);
+    float B1 = b1[n], B2 = b2[n];
+    // Merge the two lanes holding the same token (rows 0-3 / 4-7 of each 8).
+    {
+      const float ob1 = __shfl_xor(B1, 32, 64), ob2 = __shfl_xor(B2, 32, 64);
+      const int oi1 = __shfl_xor(i1, 32, 64);
+      const float top2 = fmaxf(fmaxf(B2, ob2), fminf(B1, ob1));
+      if (ob1 > B1 || (ob1 == B1 && oi1 < i1)) i1 = oi1;
+      B1 = fmaxf(B1, ob1);
+      B2 = top2;
+    }
+    if (lane < 32 && t < S) {
+      const size_t po = (size_t)g.prefS[b] * g.H + (size_t)h * S + t;
+      int32_t* apos = w.apos + (size_t)side * g.H * g.prefS[g.B] + po;
+      const int rk = w.rank[po];
+      if (rk >= 0) {
+        *apos = rk;
       } else {
-        *apos = -1;
-        const int grp = (side * g.B + b) * g.H + h;
-        const int slot = atomicAdd(&w.fixcount[grp], 1);  // < S: a token is listed once
-        const size_t lo = (size_t)side * g.H * g.prefS[g.B] + (size_t)g.prefS[b] * g.H + (size_t)h * S;
-        w.fixt[lo + slot] = t;
-        w.fixb[lo + slot] = b1;
-        atomicAdd(&c.stats[b * 4 + side], 1);
+        const float eps = score_eps(ss[n], D) + tag_eps(B1);
+        if (B1 - B2 > 2.0f * eps + B1 * 9.094947e-13f && i1 < k) {
+          *apos = i1;
+        } else {
+          *apos = -1;
+          const int grp = (side * g.B + b) * g.H + h;
+          const int slot = atomicAdd(&w.fixcount[grp], 1);  // < S: a token is listed once
+          const size_t lo = (size_t)side * g.H * g.prefS[g.B] + (size_t)g.prefS[b] * g.H + (size_t)h * S;
+          w.fixt[lo + slot] = t;
+          w.fixb[lo + slot] = B1;
+          atomicAdd(&c.stats[b * 4 + side], 1);
+        }
       }
     }
   }
@@ -380,7 +434,7 @@ __global__ __launch_bounds__(256) void k_fixup(Geo g, Ws w, Cache c, const void*
 
 hipError_t launch_assign(const Geo& g, const Ws& w, const Cache& c, const void* K, const void* V, hipStream_t st) {
   int nblk = 0;
-  for (int b = 0; b < g.B; ++b) nblk += g.H * ((g.S[b] + 127) / 128) * 2;
+  for (int b = 0; b < g.B; ++b) nblk += g.H * ((g.S[b] + ASSIGN_TOK - 1) / ASSIGN_TOK) * 2;
   if (g.dtype == 1) {
     AKV_TIMED("k_assign", st, k_assign<1><<<nblk, 256, 0, st>>>(g, w, c, K, V));
     AKV_TIMED("k_fixup", st, k_fixup<1><<<512, 256, 0, st>>>(g, w, c, K, V));
