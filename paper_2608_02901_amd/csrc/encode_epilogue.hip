@@ -85,10 +85,17 @@ __global__ __launch_bounds__(256) void k_epilogue(Geo g, Ws w, Cache c, const vo
         if (side == 0) { gK_s[tl] = gb; aK_s[tl] = a; cand_s[tl] = 1; }
         if (side == 1) {
           float s = 0.0f;
-          for (int j = 0; j < D; ++j) {
-            float p = gb * Elem<DT>::get(arow, j);
-            float r = Elem<DT>::get(xrow, j) - p;
-            s = fmaf(r, r, s);
+          for (int j0 = 0; j0 < D; j0 += PER) {
+            const uint4 av = *(const uint4*)(arow + j0);
+            const uint4 xv = *(const uint4*)(xrow + j0);
+            const E* ea = (const E*)&av;
+            const E* ex = (const E*)&xv;
+#pragma unroll
+            for (int j = 0; j < PER; ++j) {
+              float p = gb * Elem<DT>::get(ea, j);
+              float r = Elem<DT>::get(ex, j) - p;
+              s = fmaf(r, r, s);
+            }
           }
           rv2_s[tl] = s;
         }
@@ -121,41 +128,60 @@ __global__ __launch_bounds__(256) void k_epilogue(Geo g, Ws w, Cache c, const vo
   const float gk = gK_s[tl];
   const int ak = aK_s[tl];
   const float vn = vn_s[tl];
+  const bool vec = (m & 3) == 0;  // the row tables can be read as float4
   for (int rb = wave; rb < nrb; rb += 4) {
-    const int arow = rb * 32 + (lane & 31);
-    const bool rowok = arow < m;
+    // Rows past m (a partial last block) load row m - 1 and contribute 0.
+    const int arow = min(rb * 32 + (lane & 31), m - 1);
+    const E* qrow = Q + (size_t)arow * D;
+    const size_t yo = ((size_t)(b * g.H + h) * m + arow) * D;
     f32x16 accL = {}, accY = {};
+#pragma unroll
     for (int s = 0; s < D / M::KS; ++s) {
       const int k0 = kofs(M::KS, s, lane);
-      typename M::frag zero;
-      if constexpr (DT == 1) zero = __builtin_bit_cast(bf16x8, make_uint4(0, 0, 0, 0)); else zero = 0.0f;
-      auto qa = rowok ? M::load(Q + (size_t)arow * D, k0) : zero;
+      auto qa = M::load(qrow, k0);
       auto kb = M::load_lds(&KT[tl * LD], k0);
       auto vb = M::load_lds(&VT[tl * LD], k0);
       accL = M::mma(qa, kb, accL);
       if constexpr (DT == 1) {
-        const size_t yo = ((size_t)(b * g.H + h) * m + min(arow, m - 1)) * D;
-        auto yh = rowok ? M::load(w.Yhi + yo, k0) : zero;
-        auto yl = rowok ? M::load(w.Ylo + yo, k0) : zero;
-        accY = M::mma(yh, vb, accY);
-        accY = M::mma(yl, vb, accY);
+        accY = M::mma(M::load(w.Yhi + yo, k0), vb, accY);
+        accY = M::mma(M::load(w.Ylo + yo, k0), vb, accY);
       } else {
-        const size_t yo = ((size_t)(b * g.H + h) * m + min(arow, m - 1)) * D;
-        float yf = rowok ? w.Y[yo + k0] : 0.0f;
-        accY = M::mma(yf, vb, accY);
+        accY = M::mma(w.Y[yo + k0], vb, accY);
       }
     }
     float tk = 0.0f, tv = 0.0f;
     if (cand) {
+      // Rows of accumulator entries 4j .. 4j+3 are consecutive.
+      const float* qa = QA + (size_t)ak * m;
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int wr = rb * 32 + crow(e, lane);
-        if (wr < m) {
+      for (int j = 0; j < 4; ++j) {
+        const int w0 = rb * 32 + j * 8 + (lane >> 5) * 4;
+        float qv[4], mv[4], zv[4], yv[4];
+        if (vec && w0 < m) {
+          const float4 q4 = *(const float4*)(qa + w0), m4 = *(const float4*)(oM + w0);
+          const float4 z4 = *(const float4*)(oiZ + w0), y4 = *(const float4*)(yn + w0);
+          qv[0] = q4.x; qv[1] = q4.y; qv[2] = q4.z; qv[3] = q4.w;
+          mv[0] = m4.x; mv[1] = m4.y; mv[2] = m4.z; mv[3] = m4.w;
+          zv[0] = z4.x; zv[1] = z4.y; zv[2] = z4.z; zv[3] = z4.w;
+          yv[0] = y4.x; yv[1] = y4.y; yv[2] = y4.z; yv[3] = y4.w;
+        } else {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int wr = min(w0 + i, m - 1);
+            qv[i] = qa[wr];
+            mv[i] = oM[wr];
+            zv[i] = oiZ[wr];
+            yv[i] = yn[wr];
+          }
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int e = 4 * j + i;
           const float l = accL[e];
-          const float al = __expf(l * isd - oM[wr]) * oiZ[wr];
-          const float a2 = al * al;
-          const float qr = l - gk * QA[(size_t)wr * k + ak];
-          const float vv = vn - 2.0f * accY[e] + yn[wr];
+          const float al = __expf(l * isd - mv[i]) * zv[i];
+          const float a2 = w0 + i < m ? al * al : 0.0f;
+          const float qr = l - gk * qv[i];
+          const float vv = vn - 2.0f * accY[e] + yv[i];
           tk += a2 * (qr * qr) * vv;
           tv += a2;
         }

@@ -11,7 +11,7 @@
 //                   position -> anchor-index map.
 //   k_anchor_prep : copies anchor keys/values into the cache, their canonical
 //                   fp64 squared norms and fp32 inverse norms, and the table
-//                   QA[w][a] = q_w . abar^K_a used by the key utilities.
+//                   QA[a][w] = q_w . abar^K_a used by the key utilities.
 #include "akv_common.h"
 
 namespace akv {
@@ -326,15 +326,16 @@ __global__ __launch_bounds__(256) void k_anchor_prep(Geo g, Ws w, Cache c, const
     (side ? c.nrmV : c.nrmK)[ko + a0 + a] = n;
     (side ? c.invV : c.invK)[ko + a0 + a] = n > 0.0 ? (float)(1.0 / sqrt(n)) : 0.0f;
   }
-  // QA[w][a] = q_w . abar^K_a (raw dot, fp32).
+  // QA[a][w] = q_w . abar^K_a (raw dot, fp32), anchor-major so that a token
+  // reads the m values of its anchor contiguously.
   const E* Q = (const E*)Qin + ((size_t)b * g.Hq + (size_t)h * g.g) * g.W * D;
   float* QA = w.QA + ko * m;
   for (int i = threadIdx.x; i < m * na; i += blockDim.x) {
-    int wr = i / na, a = i % na;
+    int a = i / m, wr = i % m;
     const E* q = Q + (size_t)wr * D;
     float s = 0.0f;
     for (int d = 0; d < D; ++d) s = fmaf(Elem<DT>::get(q, d), AK[a][d], s);
-    QA[(size_t)wr * k + a0 + a] = s;
+    QA[(size_t)(a0 + a) * m + wr] = s;
   }
 }
 
