@@ -80,7 +80,7 @@ typedef struct anchorkv_config {
   int32_t anchor_count;   /* k per head when > 0 (window included) ... */
   float anchor_frac;      /* ... else k = max(W, floor(anchor_frac * S)), capped at S */
   float rho;              /* share of the k - W free anchors taken by score (paper: 0.7) */
-  int32_t kappa;          /* odd average-pooling width of the selector score (paper: 7) */
+  int32_t kappa;          /* odd average-pooling width of the selector score, <= 255 (paper: 7) */
   int32_t budget_mode;    /* anchorkv_budget_mode */
   float budget;           /* FRACTION: residual fraction; THETA: retained fraction theta */
   int64_t budget_count;   /* COUNT: residuals per side */

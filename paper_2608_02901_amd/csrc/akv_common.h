@@ -52,6 +52,7 @@ __device__ __host__ inline size_t slot_base(const Geo& g, int b, int h) {
 }
 
 constexpr int OBS_CHUNK = 2048;   // tokens per observation-pass workgroup
+constexpr int SEL_BAND_MAX = 256; // largest band re-scored in fp64 at the selection cut
 constexpr int SORT_CHUNK = 2048;  // tokens per counting-sort chunk
 
 // Device pointers into the cache blob (layouts in position p = request-major,
@@ -100,6 +101,9 @@ struct Ws {
   float* sc;            // [b][h][S_b] selector score, then pooled score
   int32_t* rank;        // [b][h][S_b] anchor index of an anchor position, -1 otherwise
   uint8_t* flag;        // [b][h][S_b] selection marks
+  int32_t* sband;       // [b][h][SEL_BAND_MAX] positions in the fp64 band around the top-n cut
+  double* sbscore;      // [b][h][SEL_BAND_MAX] their fp64 pooled scores
+  int32_t* sstate;      // [b][h][4] cut bits, remaining, taken above the band, band size (-1: none)
   float* QA;            // [b][h][m][k_b] q_w . abar^K_a
   int32_t* apos;        // [side][b][h][S_b] anchor index per position (-1: fixup pending)
   int32_t* fixt;        // [side][b][h][S_b] per-head fixup list: token positions (filled from the front)

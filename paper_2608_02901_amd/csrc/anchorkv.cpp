@@ -65,7 +65,7 @@ struct anchorkv_plan {
       c_stats;
   size_t cache_bytes;
   // encode workspace offsets
-  size_t w_opmax, w_opsum, w_oM, w_oiZ, w_oiZ64, w_ypart, w_Y, w_Yhi, w_Ylo, w_ynorm, w_sc, w_rank, w_flag, w_QA, w_apos,
+  size_t w_opmax, w_opsum, w_oM, w_oiZ, w_oiZ64, w_ypart, w_Y, w_Yhi, w_Ylo, w_ynorm, w_sc, w_rank, w_flag, w_sband, w_sbscore, w_sstate, w_QA, w_apos,
       w_fix, w_fixcount, w_gpos, w_u, w_sel, w_bhist, w_bstate, w_tiecnt, w_shist, w_wcnt;
   size_t ws_bytes;
   // decode workspace offsets
@@ -105,7 +105,8 @@ extern "C" anchorkv_status anchorkv_plan_create(const anchorkv_config* cfg, int3
   if (c.head_dim != AKV_D) return fail(ANCHORKV_ERR_UNSUPPORTED, "this build supports head_dim = 128");
   if (c.window < 1) return fail(ANCHORKV_ERR_INVALID_ARG, "window must be >= 1");
   if (c.window * g > 256) return fail(ANCHORKV_ERR_UNSUPPORTED, "window * (Hq/H) must be <= 256");
-  if (c.kappa < 1 || (c.kappa & 1) == 0) return fail(ANCHORKV_ERR_INVALID_ARG, "kappa must be odd and >= 1");
+  if (c.kappa < 1 || (c.kappa & 1) == 0 || c.kappa > 255)
+    return fail(ANCHORKV_ERR_INVALID_ARG, "kappa must be odd, in [1, 255]");
   if (!(c.rho >= 0.0f && c.rho <= 1.0f)) return fail(ANCHORKV_ERR_INVALID_ARG, "rho must be in [0, 1]");
   if (c.dtype != ANCHORKV_F32 && c.dtype != ANCHORKV_BF16) return fail(ANCHORKV_ERR_INVALID_ARG, "bad dtype");
   const int G = c.quant_group ? c.quant_group : c.head_dim;
@@ -279,6 +280,9 @@ extern "C" anchorkv_status anchorkv_plan_create(const anchorkv_config* cfg, int3
   p->w_sc = Wl.add(4 * TS);
   p->w_rank = Wl.add(4 * TS);
   p->w_flag = Wl.add(TS);
+  p->w_sband = Wl.add(4 * (size_t)batch * H * akv::SEL_BAND_MAX);
+  p->w_sbscore = Wl.add(8 * (size_t)batch * H * akv::SEL_BAND_MAX);
+  p->w_sstate = Wl.add(4 * 4 * (size_t)batch * H);
   p->w_QA = Wl.add(4 * TK * m);
   p->w_apos = Wl.add(4 * 2 * TS);
   p->w_fix = Wl.add(8 * 2 * TS);
@@ -367,6 +371,9 @@ static akv::Ws ws_ptrs(const anchorkv_plan* p, void* base) {
   w.sc = at<float>(base, p->w_sc);
   w.rank = at<int32_t>(base, p->w_rank);
   w.flag = at<uint8_t>(base, p->w_flag);
+  w.sband = at<int32_t>(base, p->w_sband);
+  w.sbscore = at<double>(base, p->w_sbscore);
+  w.sstate = at<int32_t>(base, p->w_sstate);
   w.QA = at<float>(base, p->w_QA);
   w.apos = at<int32_t>(base, p->w_apos);
   w.fixt = at<int32_t>(base, p->w_fix);

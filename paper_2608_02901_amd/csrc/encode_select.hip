@@ -52,45 +52,134 @@ __device__ inline int block_excl_scan(int v, int* tmp /* >= 16 ints */, int& tot
 // exponentials, ~1e-9 relative), so they match the canonical fp64 definition
 // to far better than the gaps between real scores.
 constexpr float SEL_BAND = 1e-3f;
-constexpr int SEL_BAND_MAX = 256;
 
-// fp64 pooled selector score of position t (t < P, so every observation row
-// sees it): (1/kappa) sum_{|d| <= kappa/2, 0 <= t+d < P} (1/m) sum_w
-// exp(dot64(q_w, k_{t+d}) / sqrt(D) - M_w) / Z_w, with the row statistics of
-// the observation pass.  One wave; lane l takes rows l, l + 64, ...; the
-// lane partials are summed in a fixed order.
+// fp64 pooled selector score of band member i of (request b, head h), one
+// workgroup per member (k_sel_band): (1/kappa) sum_{|d| <= kappa/2,
+// 0 <= t+d < P} (1/m) sum_w exp(dot64(q_w, k_{t+d}) / sqrt(D) - M_w) / Z_w,
+// with the row statistics of the observation pass.  The m query rows and the
+// kappa key rows are staged in LDS when they fit; thread = (row, offset)
+// pair.  The dot products are exact fp64 products (fused multiply-add of an
+// exact product rounds once, like an add) in four interleaved partial sums
+// (the order differs from a sequential sum by ~1e-16 relative, far below the
+// band's resolution); the terms are combined in a fixed order.
+constexpr int SEL_QLDS = 32768;  // bytes of staged query rows
+constexpr int SEL_KLDS = 8192;   // bytes of staged key rows
+
 template <int DT>
-__device__ double pooled64(const Geo& g, const typename Elem<DT>::T* X, const typename Elem<DT>::T* Q,
-                           const float* oM, const double* oiZ, int t, int P, int m) {
-  const int lane = threadIdx.x & 63, half = g.kappa / 2;
+__global__ __launch_bounds__(256) void k_sel_band(Geo g, Ws w, const void* Kin, const void* Qin) {
+  using E = typename Elem<DT>::T;
+  constexpr int PER = 16 / sizeof(E), NCH = AKV_D / PER;
+  __shared__ __align__(16) unsigned char qlds[SEL_QLDS];
+  __shared__ __align__(16) unsigned char klds[SEL_KLDS];
+  __shared__ double part[256 * 2];
+  const int bh = blockIdx.x / SEL_BAND_MAX, i = blockIdx.x % SEL_BAND_MAX;
+  const int b = bh / g.H, h = bh % g.H;
+  const int nb = w.sstate[bh * 4 + 3];
+  if (i >= nb) return;  // also an overflowed band (nb < 0)
+  const int S = g.S[b], P = S - g.W, m = g.m;
+  const int tid = threadIdx.x, nt = blockDim.x, half = g.kappa / 2, nk = 2 * half + 1;
+  const int t = w.sband[(size_t)bh * SEL_BAND_MAX + i];
+  const E* X = (const E*)Kin + ((size_t)g.prefS[b] * g.H + (size_t)h * S) * AKV_D;
+  const E* Q = (const E*)Qin + ((size_t)b * g.Hq + (size_t)h * g.g) * g.W * AKV_D;
+  const float* oM = w.oM + (size_t)bh * m;
+  const double* oiZ = w.oiZ64 + (size_t)bh * m;
+  const double isd = 1.0 / sqrt((double)AKV_D);
+  const bool qst = (size_t)m * AKV_D * sizeof(E) <= SEL_QLDS;
+  const bool kst = (size_t)nk * AKV_D * sizeof(E) <= SEL_KLDS;
+  E* qs = (E*)qlds;
+  E* ks = (E*)klds;
+  if (qst)
+    for (int c = tid; c < m * NCH; c += nt) ((uint4*)qs)[c] = ((const uint4*)Q)[c];
+  if (kst)
+    for (int c = tid; c < nk * NCH; c += nt) {
+      const int u = min(max(t + c / NCH - half, 0), P - 1);
+      ((uint4*)ks)[c] = ((const uint4*)(X + (size_t)u * AKV_D))[c % NCH];
+    }
+  __syncthreads();
   double acc = 0.0;
-  for (int wr = lane; wr < m; wr += 64) {
-    const auto* q = Q + (size_t)wr * AKV_D;
+  for (int wr = tid; wr < m; wr += nt) {
+    const E* q = qst ? qs + (size_t)wr * AKV_D : Q + (size_t)wr * AKV_D;
     double rs = 0.0;
-    for (int d = -half; d <= half; ++d) {
-      const int u = t + d;
+    for (int r = 0; r < nk; ++r) {
+      const int u = t + r - half;
       if (u < 0 || u >= P) continue;
-      const double l = dot64_seq<DT>(q, X + (size_t)u * AKV_D, AKV_D) / sqrt((double)AKV_D);
+      const E* x = kst ? ks + (size_t)r * AKV_D : X + (size_t)u * AKV_D;
+      double p4[4] = {0.0, 0.0, 0.0, 0.0};
+#pragma unroll 4
+      for (int ch = 0; ch < NCH; ++ch) {
+        const uint4 qv = ((const uint4*)q)[ch], xv = ((const uint4*)x)[ch];
+        const E* qe = (const E*)&qv;
+        const E* xe = (const E*)&xv;
+#pragma unroll
+        for (int e = 0; e < PER; ++e)
+          p4[e & 3] = fma((double)Elem<DT>::get(qe, e), (double)Elem<DT>::get(xe, e), p4[e & 3]);
+      }
+      const double l = ((p4[0] + p4[1]) + (p4[2] + p4[3])) * isd;
       rs += exp(l - (double)oM[wr]) * oiZ[wr];
     }
     acc += rs;
   }
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) acc += __shfl_xor(acc, o, 64);
-  return acc / (double)m / (double)g.kappa;
+  // rows summed per thread (rows tid, tid + nt, ...), then over threads in order
+  part[tid] = acc;
+  __syncthreads();
+  if (tid == 0) {
+    double tot = 0.0;
+    for (int r = 0; r < nt; ++r) tot += part[r];
+    w.sbscore[(size_t)bh * SEL_BAND_MAX + i] = tot / (double)m / (double)g.kappa;
+  }
 }
 
+// Radix digit search over a 4096-bin histogram: the bin where the running
+// count (from the top when `desc`, else from the bottom) reaches `need`.
+// Writes (bin, count before it) to out[0..1].  Whole workgroup.
+__device__ inline void digit_pick(const uint32_t* hist, int nbin, int need, bool desc, int* tmp, int* out) {
+  const int tid = threadIdx.x, nt = blockDim.x;
+  const int per = (nbin + nt - 1) / nt;
+  int loc = 0;
+  for (int i = 0; i < per; ++i) {
+    const int bin = tid * per + i;
+    if (bin < nbin) loc += (int)hist[desc ? nbin - 1 - bin : bin];
+  }
+  int tot;
+  const int before = block_excl_scan(loc, tmp, tot);
+  int run = before;
+  for (int i = 0; i < per; ++i) {
+    const int bin = tid * per + i;
+    if (bin >= nbin) break;
+    const int c = (int)hist[desc ? nbin - 1 - bin : bin];
+    if (run < need && run + c >= need) {
+      out[0] = desc ? nbin - 1 - bin : bin;
+      out[1] = run;
+    }
+    run += c;
+  }
+  __syncthreads();
+}
+
+constexpr int SEL_NBIN = 4096;  // 12-bit radix digits
+constexpr int SEL_TILE = 3840;  // pooled positions per LDS tile (tile + halo fit the histogram)
+constexpr int SEL_HALO = 254;   // 2 * (kappa / 2) for kappa <= 255
+constexpr int SEL_CAND = 1024;  // hash candidates kept in the last digit's bin
+constexpr int SEL_U = 8;        // elements per thread per batch (independent loads)
+
+// Passes over [0, n) visit t = t0 + u * nt (u < SEL_U) per batch: coalesced
+// across lanes, SEL_U independent loads in flight per thread.
+template <typename F>
+__device__ inline void sel_batches(int n, F&& body) {
+  for (int t0 = threadIdx.x; t0 < n; t0 += SEL_U * blockDim.x) body(t0);
+}
+
+// Selection, first half (one workgroup per request and head): marks reset,
+// pooled scores, the exact n_top-th largest pooled fp32 value, the positions
+// clearly above it (taken) and the band around it, whose members k_sel_band
+// re-scores in fp64.  An anchor override replaces the selection.
 template <int DT>
-__global__ __launch_bounds__(1024) void k_select(Geo g, Ws w, Cache c, const int32_t* ovr, const void* Kin,
-                                                 const void* Qin) {
-  using E = typename Elem<DT>::T;
-  __shared__ uint32_t hist[256];
+__global__ __launch_bounds__(1024) void k_sel_top(Geo g, Ws w, Cache c, const int32_t* ovr) {
+  __shared__ uint32_t hist[SEL_NBIN];
   __shared__ int tmp[20];
-  __shared__ unsigned long long bcast[2];
-  __shared__ int band[SEL_BAND_MAX];
-  __shared__ double bscore[SEL_BAND_MAX];
+  __shared__ int pick[2];
   __shared__ int nband, nabove;
-  const int b = blockIdx.x / g.H, h = blockIdx.x % g.H;
+  const int bh = blockIdx.x, b = bh / g.H, h = bh % g.H;
   const int S = g.S[b], W = g.W, P = S - W, k = g.k[b];
   const size_t so = (size_t)g.prefS[b] * g.H + (size_t)h * S;
   int32_t* rank = w.rank + so;
@@ -98,12 +187,20 @@ __global__ __launch_bounds__(1024) void k_select(Geo g, Ws w, Cache c, const int
   const float* sc = w.sc + so;
   float* pooled = w.u + so;  // the utility buffer is free until the epilogue
   int32_t* anc = c.anc_pos + (size_t)g.prefK[b] * g.H + (size_t)h * k;
+  int32_t* st = w.sstate + bh * 4;  // prefix, remaining, nabove, nband (-1: none / overflow)
   const int tid = threadIdx.x, nt = blockDim.x;
 
-  for (int t = tid; t < S; t += nt) {
-    rank[t] = -1;
-    flag[t] = 0;
-  }
+  sel_batches(S, [&](int t0) {
+#pragma unroll
+    for (int u = 0; u < SEL_U; ++u) {
+      const int t = t0 + u * nt;
+      if (t < S) {
+        rank[t] = -1;
+        flag[t] = 0;
+      }
+    }
+  });
+  if (tid == 0) st[3] = -1;
   __syncthreads();
   if (ovr) {
     const int32_t* o = ovr + (size_t)g.prefK[b] * g.H + (size_t)h * k;
@@ -119,95 +216,105 @@ __global__ __launch_bounds__(1024) void k_select(Geo g, Ws w, Cache c, const int
     return;
   }
 
-  // Average pooling of width kappa over [0, P), zero padded, divided by kappa.
+  // Average pooling of width kappa over [0, P), zero padded, divided by kappa
+  // (terms added in offset order, from -kappa/2), in tiles of SEL_TILE
+  // positions staged through LDS with their halo; the next tile's values are
+  // loaded while the current one is pooled.
   const int half = g.kappa / 2;
-  for (int t = tid; t < P; t += nt) {
-    float s = 0.0f;
-    for (int d = -half; d <= half; ++d) {
-      int u = t + d;
-      if (u >= 0 && u < P) s += sc[u];
+  {
+    float* stile = (float*)hist;  // the histogram is not in use yet
+    constexpr int TV = (SEL_TILE + SEL_HALO + 1023) / 1024;  // staged values per thread
+    float nxt[TV];
+    auto load_tile = [&](int c0) {
+#pragma unroll
+      for (int i = 0; i < TV; ++i) {
+        const int j = tid + i * nt, u = c0 - half + j;
+        nxt[i] = (j < SEL_TILE + 2 * half && u >= 0 && u < P) ? sc[u] : 0.0f;
+      }
+    };
+    load_tile(0);
+    for (int c0 = 0; c0 < P; c0 += SEL_TILE) {
+      __syncthreads();
+#pragma unroll
+      for (int i = 0; i < TV; ++i) {
+        const int j = tid + i * nt;
+        if (j < SEL_TILE + 2 * half) stile[j] = nxt[i];
+      }
+      __syncthreads();
+      if (c0 + SEL_TILE < P) load_tile(c0 + SEL_TILE);
+      for (int t = tid; t < SEL_TILE && c0 + t < P; t += nt) {
+        float s = 0.0f;
+        for (int d = 0; d <= 2 * half; ++d) s += stile[t + d];
+        pooled[c0 + t] = s / (float)g.kappa;
+      }
     }
-    pooled[t] = s / (float)g.kappa;
   }
   __syncthreads();
 
-  // Contiguous range of [0, P) owned by this thread (for ordered ranks).
-  const int per = (P + nt - 1) / nt;
-  const int lo = min(P, tid * per), hi = min(P, lo + per);
-
-  // ---- top n_top by pooled score, ties to the lower position.
+  // ---- top n_top by pooled score, ties to the lower position: radix select
+  // on the fp32 bits (non-negative scores order as their bits), digits
+  // [31:20], [19:8], [7:0].
   const int ntop = g.ntop[b];
-  if (ntop > 0) {
-    uint32_t prefix = 0, pmask = 0;
-    int remaining = ntop;
-    for (int pass = 0; pass < 4; ++pass) {
-      const int shift = 24 - 8 * pass;
-      for (int i = tid; i < 256; i += nt) hist[i] = 0;
-      __syncthreads();
-      for (int t = tid; t < P; t += nt) {
-        uint32_t u = __float_as_uint(pooled[t]);
-        if ((u & pmask) == prefix) atomicAdd(&hist[(u >> shift) & 255u], 1u);
-      }
-      __syncthreads();
-      if (tid == 0) {
-        int cum = 0, dg = 255;
-        for (; dg > 0; --dg) {
-          if (cum + (int)hist[dg] >= remaining) break;
-          cum += hist[dg];
-        }
-        remaining -= cum;
-        bcast[0] = ((unsigned long long)dg << 32) | (unsigned)remaining;
-      }
-      __syncthreads();
-      const uint32_t dg = (uint32_t)(bcast[0] >> 32);
-      remaining = (int)(bcast[0] & 0xffffffffu);
-      prefix |= dg << shift;
-      pmask |= 255u << shift;
-      __syncthreads();
-    }
-    // prefix is the bit pattern of the n_top-th largest fp32 score.  Scores
-    // clearly above the band are taken; inside the band the decision uses the
-    // fp64 scores (ties to the lower position).
-    const float cut = __uint_as_float(prefix);
-    const float bhi = cut * (1.0f + SEL_BAND), blo = cut * (1.0f - SEL_BAND);
-    if (tid == 0) {
-      nband = 0;
-      nabove = 0;
-    }
+  if (ntop <= 0) return;
+  uint32_t prefix = 0, pmask = 0;
+  int remaining = ntop;
+  for (int pass = 0; pass < 3; ++pass) {
+    const int shift = pass == 0 ? 20 : (pass == 1 ? 8 : 0);
+    const int nbin = pass == 2 ? 256 : SEL_NBIN;
+    for (int i = tid; i < nbin; i += nt) hist[i] = 0;
     __syncthreads();
-    for (int t = tid; t < P; t += nt) {
-      const float v = pooled[t];
-      if (v > bhi) {
+    sel_batches(P, [&](int t0) {
+      uint32_t v[SEL_U];
+#pragma unroll
+      for (int u = 0; u < SEL_U; ++u) v[u] = t0 + u * nt < P ? __float_as_uint(pooled[t0 + u * nt]) : 0u;
+#pragma unroll
+      for (int u = 0; u < SEL_U; ++u)
+        if (t0 + u * nt < P && (v[u] & pmask) == prefix) atomicAdd(&hist[(v[u] >> shift) & (nbin - 1)], 1u);
+    });
+    __syncthreads();
+    digit_pick(hist, nbin, remaining, true, tmp, pick);
+    remaining -= pick[1];
+    prefix |= (uint32_t)pick[0] << shift;
+    pmask |= (uint32_t)(nbin - 1) << shift;
+    __syncthreads();
+  }
+  // prefix is the bit pattern of the n_top-th largest fp32 score.  Scores
+  // clearly above the band are taken; inside the band the decision uses the
+  // fp64 scores (ties to the lower position).
+  const float cut = __uint_as_float(prefix);
+  const float bhi = cut * (1.0f + SEL_BAND), blo = cut * (1.0f - SEL_BAND);
+  if (tid == 0) {
+    nband = 0;
+    nabove = 0;
+  }
+  __syncthreads();
+  int32_t* band = w.sband + (size_t)bh * SEL_BAND_MAX;
+  sel_batches(P, [&](int t0) {
+    float v[SEL_U];
+#pragma unroll
+    for (int u = 0; u < SEL_U; ++u) v[u] = t0 + u * nt < P ? pooled[t0 + u * nt] : -1.0f;
+#pragma unroll
+    for (int u = 0; u < SEL_U; ++u) {
+      const int t = t0 + u * nt;
+      if (t >= P) continue;
+      if (v[u] > bhi) {
         atomicAdd(&nabove, 1);
-      } else if (v >= blo) {
+        flag[t] = 1;
+      } else if (v[u] >= blo) {
         const int i = atomicAdd(&nband, 1);
         if (i < SEL_BAND_MAX) band[i] = t;
       }
     }
+  });
+  __syncthreads();
+  const int nb = nband;
+  if (nb > SEL_BAND_MAX) {
+    // Band overflow: the fp32 order decides (ties to the lower position).
+    if (tid == 0) atomicOr(&c.header[2], 32u);
+    const int per = (P + nt - 1) / nt;
+    const int lo = min(P, tid * per), hi = min(P, lo + per);
+    for (int t = lo; t < hi; ++t) flag[t] = 0;
     __syncthreads();
-    const int nb = nband;
-    if (nb <= SEL_BAND_MAX) {
-      const E* X = (const E*)Kin + ((size_t)g.prefS[b] * g.H + (size_t)h * S) * AKV_D;
-      const E* Q = (const E*)Qin + ((size_t)b * g.Hq + (size_t)h * g.g) * g.W * AKV_D;
-      const float* oM = w.oM + (size_t)(b * g.H + h) * g.m;
-      const double* oiZ = w.oiZ64 + (size_t)(b * g.H + h) * g.m;
-      for (int i = tid >> 6; i < nb; i += nt >> 6) {
-        const double v = pooled64<DT>(g, X, Q, oM, oiZ, band[i], P, g.m);
-        if ((tid & 63) == 0) bscore[i] = v;
-      }
-      __syncthreads();
-      const int need = ntop - nabove;
-      for (int t = tid; t < P; t += nt) flag[t] = pooled[t] > bhi ? 1 : 0;
-      __syncthreads();
-      for (int i = tid; i < nb; i += nt) {
-        int r = 0;
-        for (int j = 0; j < nb; ++j)
-          r += bscore[j] > bscore[i] || (bscore[j] == bscore[i] && band[j] < band[i]);
-        if (r < need) flag[band[i]] = 1;
-      }
-      __syncthreads();
-    } else {
-    if (tid == 0) atomicOr(&c.header[2], 32u);  // band overflow: the fp32 order decides
     int eq = 0;
     for (int t = lo; t < hi; ++t) eq += (__float_as_uint(pooled[t]) == prefix);
     int tot;
@@ -221,65 +328,157 @@ __global__ __launch_bounds__(1024) void k_select(Geo g, Ws w, Cache c, const int
         ++before;
       }
     }
-    __syncthreads();
+  } else if (tid == 0) {
+    st[0] = (int)prefix;
+    st[1] = remaining;
+    st[2] = nabove;
+    st[3] = nb;
+  }
+}
+
+// Selection, second half: the band members ranked by their fp64 scores, the
+// uniform share (the n_rand unflagged positions with the smallest SplitMix64
+// key: the top 12 bits locate the bin holding the n_rand-th smallest key, keys
+// below it are taken, the keys inside it are ranked exactly; keys are
+// distinct since SplitMix64 is a bijection), and the ascending anchor list
+// with the position -> anchor-index map.
+template <int DT>
+__global__ __launch_bounds__(1024) void k_sel_rest(Geo g, Ws w, Cache c, const int32_t* ovr) {
+  __shared__ uint32_t hist[SEL_NBIN];
+  __shared__ int tmp[20];
+  __shared__ int pick[2];
+  __shared__ unsigned long long ckey[SEL_CAND];
+  __shared__ int cpos[SEL_CAND];
+  __shared__ int ncand;
+  if (ovr) return;
+  const int bh = blockIdx.x, b = bh / g.H, h = bh % g.H;
+  const int S = g.S[b], W = g.W, P = S - W, k = g.k[b];
+  const size_t so = (size_t)g.prefS[b] * g.H + (size_t)h * S;
+  int32_t* rank = w.rank + so;
+  uint8_t* flag = w.flag + so;
+  int32_t* anc = c.anc_pos + (size_t)g.prefK[b] * g.H + (size_t)h * k;
+  const int tid = threadIdx.x, nt = blockDim.x;
+
+  const int nb = w.sstate[bh * 4 + 3];
+  if (nb > 0) {
+    const int need = g.ntop[b] - w.sstate[bh * 4 + 2];
+    const int32_t* band = w.sband + (size_t)bh * SEL_BAND_MAX;
+    const double* bscore = w.sbscore + (size_t)bh * SEL_BAND_MAX;
+    for (int i = tid; i < nb; i += nt) {
+      int r = 0;
+      for (int j = 0; j < nb; ++j)
+        r += bscore[j] > bscore[i] || (bscore[j] == bscore[i] && band[j] < band[i]);
+      if (r < need) flag[band[i]] = 1;
     }
+    __syncthreads();
   }
 
-  // ---- uniform share: the n_rand unflagged positions with the smallest hash.
   const int nrand = g.nrand[b];
   const unsigned long long hs = g.seed_anchor ^ ((unsigned long long)h << 40);
   if (nrand > 0) {
-    unsigned long long prefix = 0, pmask = 0;
-    int remaining = nrand;
-    for (int pass = 0; pass < 8; ++pass) {
-      const int shift = 56 - 8 * pass;
-      for (int i = tid; i < 256; i += nt) hist[i] = 0;
-      __syncthreads();
+    for (int i = tid; i < SEL_NBIN; i += nt) hist[i] = 0;
+    if (tid == 0) ncand = 0;
+    __syncthreads();
+    sel_batches(P, [&](int t0) {
+      uint8_t f[SEL_U];
+#pragma unroll
+      for (int u = 0; u < SEL_U; ++u) f[u] = t0 + u * nt < P ? flag[t0 + u * nt] : 1;
+#pragma unroll
+      for (int u = 0; u < SEL_U; ++u)
+        if (!f[u]) atomicAdd(&hist[splitmix64(hs ^ (unsigned long long)(t0 + u * nt)) >> 52], 1u);
+    });
+    __syncthreads();
+    digit_pick(hist, SEL_NBIN, nrand, false, tmp, pick);
+    const unsigned long long bin = (unsigned long long)pick[0];
+    const int need = nrand - pick[1];
+    sel_batches(P, [&](int t0) {
+      uint8_t f[SEL_U];
+#pragma unroll
+      for (int u = 0; u < SEL_U; ++u) f[u] = t0 + u * nt < P ? flag[t0 + u * nt] : 1;
+#pragma unroll
+      for (int u = 0; u < SEL_U; ++u) {
+        if (f[u]) continue;
+        const int t = t0 + u * nt;
+        const unsigned long long key = splitmix64(hs ^ (unsigned long long)t);
+        if ((key >> 52) < bin) {
+          flag[t] = 2;
+        } else if ((key >> 52) == bin) {
+          const int i = atomicAdd(&ncand, 1);
+          if (i < SEL_CAND) {
+            ckey[i] = key;
+            cpos[i] = t;
+          }
+        }
+      }
+    });
+    __syncthreads();
+    const int nc = ncand;
+    if (nc <= SEL_CAND) {
+      for (int i = tid; i < nc; i += nt) {
+        int r = 0;
+        for (int j = 0; j < nc; ++j) r += ckey[j] < ckey[i];
+        if (r < need) flag[cpos[i]] = 2;
+      }
+    } else {
+      // More candidates than the buffer holds (far from the expected P/4096):
+      // finish the radix select on the remaining 52 bits (digits of 12, 12,
+      // 12, 12 and 4 bits).
+      if (tid == 0) atomicOr(&c.header[2], 64u);
+      unsigned long long prefix = bin << 52, pmask = 0xfffull << 52;
+      int remaining = need;
+      for (int dgt = 0; dgt < 5; ++dgt) {
+        const int shift = dgt < 4 ? 40 - 12 * dgt : 0;
+        const int nbin = dgt < 4 ? SEL_NBIN : 16;
+        for (int i = tid; i < nbin; i += nt) hist[i] = 0;
+        __syncthreads();
+        for (int t = tid; t < P; t += nt) {
+          if (flag[t]) continue;
+          const unsigned long long key = splitmix64(hs ^ (unsigned long long)t);
+          if ((key & pmask) == prefix) atomicAdd(&hist[(key >> shift) & (unsigned long long)(nbin - 1)], 1u);
+        }
+        __syncthreads();
+        digit_pick(hist, nbin, remaining, false, tmp, pick);
+        remaining -= pick[1];
+        prefix |= (unsigned long long)pick[0] << shift;
+        pmask |= (unsigned long long)(nbin - 1) << shift;
+        __syncthreads();
+      }
       for (int t = tid; t < P; t += nt) {
         if (flag[t]) continue;
-        unsigned long long key = splitmix64(hs ^ (unsigned long long)t);
-        if ((key & pmask) == prefix) atomicAdd(&hist[(key >> shift) & 255ull], 1u);
+        const unsigned long long key = splitmix64(hs ^ (unsigned long long)t);
+        if ((key & (0xfffull << 52)) == (bin << 52) && key <= prefix) flag[t] = 2;
       }
-      __syncthreads();
-      if (tid == 0) {
-        int cum = 0, dg = 0;
-        for (; dg < 255; ++dg) {
-          if (cum + (int)hist[dg] >= remaining) break;
-          cum += hist[dg];
-        }
-        remaining -= cum;
-        bcast[1] = ((unsigned long long)dg << 32) | (unsigned)remaining;
-      }
-      __syncthreads();
-      const unsigned long long dg = bcast[1] >> 32;
-      remaining = (int)(bcast[1] & 0xffffffffu);
-      prefix |= dg << shift;
-      pmask |= 255ull << shift;
-      __syncthreads();
-    }
-    // Keys are distinct (SplitMix64 is a bijection), so exactly the keys
-    // <= prefix are taken.
-    for (int t = tid; t < P; t += nt) {
-      if (flag[t]) continue;
-      unsigned long long key = splitmix64(hs ^ (unsigned long long)t);
-      if (key <= prefix) flag[t] = 2;
     }
     __syncthreads();
   }
 
   // ---- ascending anchor list: flagged positions of [0, P), then the window.
+  const int per = (P + nt - 1) / nt;
+  const int lo = min(P, tid * per), hi = min(P, lo + per);
   int cnt = 0;
-  for (int t = lo; t < hi; ++t) cnt += flag[t] != 0;
+  for (int t0 = lo; t0 < hi; t0 += 16) {
+    uint8_t f[16];
+#pragma unroll
+    for (int u = 0; u < 16; ++u) f[u] = t0 + u < hi ? flag[t0 + u] : 0;
+#pragma unroll
+    for (int u = 0; u < 16; ++u) cnt += f[u] != 0;
+  }
   int tot;
   int at = block_excl_scan(cnt, tmp, tot);
-  for (int t = lo; t < hi; ++t)
-    if (flag[t]) {
-      if (at < k - W) {
-        anc[at] = t;
-        rank[t] = at;
+  for (int t0 = lo; t0 < hi; t0 += 16) {
+    uint8_t f[16];
+#pragma unroll
+    for (int u = 0; u < 16; ++u) f[u] = t0 + u < hi ? flag[t0 + u] : 0;
+#pragma unroll
+    for (int u = 0; u < 16; ++u)
+      if (f[u]) {
+        if (at < k - W) {
+          anc[at] = t0 + u;
+          rank[t0 + u] = at;
+        }
+        ++at;
       }
-      ++at;
-    }
+  }
   for (int i = tid; i < W; i += nt) {
     anc[k - W + i] = P + i;
     rank[P + i] = k - W + i;
@@ -343,10 +542,15 @@ hipError_t launch_select(const Geo& g, const Ws& w, const Cache& c, const void* 
                          const int32_t* ovr, hipStream_t st) {
   int nblk = 0;
   for (int b = 0; b < g.B; ++b) nblk += g.H * ((g.k[b] + 63) / 64);
+  const int nbh = g.B * g.H;
   if (g.dtype == 1) {
-    AKV_TIMED("k_select", st, k_select<1><<<g.B * g.H, 1024, 0, st>>>(g, w, c, ovr, K, Q));
+    AKV_TIMED("k_select", st, k_sel_top<1><<<nbh, 1024, 0, st>>>(g, w, c, ovr));
+    if (!ovr) AKV_TIMED("k_sel_band", st, k_sel_band<1><<<nbh * SEL_BAND_MAX, 256, 0, st>>>(g, w, K, Q));
+    AKV_TIMED("k_sel_rest", st, k_sel_rest<1><<<nbh, 1024, 0, st>>>(g, w, c, ovr));
   } else {
-    AKV_TIMED("k_select", st, k_select<0><<<g.B * g.H, 1024, 0, st>>>(g, w, c, ovr, K, Q));
+    AKV_TIMED("k_select", st, k_sel_top<0><<<nbh, 1024, 0, st>>>(g, w, c, ovr));
+    if (!ovr) AKV_TIMED("k_sel_band", st, k_sel_band<0><<<nbh * SEL_BAND_MAX, 256, 0, st>>>(g, w, K, Q));
+    AKV_TIMED("k_sel_rest", st, k_sel_rest<0><<<nbh, 1024, 0, st>>>(g, w, c, ovr));
   }
   if (g.dtype == 1) {
     AKV_TIMED("k_anchor_prep", st, k_anchor_prep<1><<<nblk, 256, 0, st>>>(g, w, c, K, V, Q));

@@ -51,6 +51,7 @@ def _cfg(**kw):
     (dict(head_dim=96), N.ERR_INVALID_ARG),
     (dict(head_dim=64), N.ERR_UNSUPPORTED),
     (dict(kappa=6), N.ERR_INVALID_ARG),
+    (dict(kappa=257), N.ERR_INVALID_ARG),
     (dict(quant_group=48), N.ERR_INVALID_ARG),
     (dict(quant_group=16), N.ERR_UNSUPPORTED),
     (dict(rho=1.5), N.ERR_INVALID_ARG),
