@@ -350,6 +350,8 @@ __global__ __launch_bounds__(1024) void k_sel_rest(Geo g, Ws w, Cache c, const i
   __shared__ unsigned long long ckey[SEL_CAND];
   __shared__ int cpos[SEL_CAND];
   __shared__ int ncand;
+  __shared__ int cnts[SEL_U * 16];     // flags per (u, wave) of a batch (16 waves of 1024 threads)
+  __shared__ int cpre[SEL_U * 16 + 1];  // their exclusive prefix, then the batch total
   if (ovr) return;
   const int bh = blockIdx.x, b = bh / g.H, h = bh % g.H;
   const int S = g.S[b], W = g.W, P = S - W, k = g.k[b];
@@ -453,37 +455,56 @@ __global__ __launch_bounds__(1024) void k_sel_rest(Geo g, Ws w, Cache c, const i
   }
 
   // ---- ascending anchor list: flagged positions of [0, P), then the window.
-  const int per = (P + nt - 1) / nt;
-  const int lo = min(P, tid * per), hi = min(P, lo + per);
-  int cnt = 0;
-  for (int t0 = lo; t0 < hi; t0 += 16) {
-    uint8_t f[16];
+  // Batches of SEL_U x nt positions in (u, thread) order; a flag's rank is the
+  // count before its batch plus the flags before it inside the batch (wave
+  // ballots, then per-(u, wave) counts in LDS).
+  {
+    static_assert(SEL_U * 16 == 128, "two scan entries per lane of one wave");
+    const int lane = tid & 63, wv = tid >> 6;
+    int base = 0;
+    for (int t0 = tid; t0 - tid < P; t0 += SEL_U * nt) {
+      uint8_t f[SEL_U];
 #pragma unroll
-    for (int u = 0; u < 16; ++u) f[u] = t0 + u < hi ? flag[t0 + u] : 0;
+      for (int u = 0; u < SEL_U; ++u) f[u] = t0 + u * nt < P ? flag[t0 + u * nt] : 0;
+      unsigned long long bal[SEL_U];
 #pragma unroll
-    for (int u = 0; u < 16; ++u) cnt += f[u] != 0;
-  }
-  int tot;
-  int at = block_excl_scan(cnt, tmp, tot);
-  for (int t0 = lo; t0 < hi; t0 += 16) {
-    uint8_t f[16];
-#pragma unroll
-    for (int u = 0; u < 16; ++u) f[u] = t0 + u < hi ? flag[t0 + u] : 0;
-#pragma unroll
-    for (int u = 0; u < 16; ++u)
-      if (f[u]) {
-        if (at < k - W) {
-          anc[at] = t0 + u;
-          rank[t0 + u] = at;
-        }
-        ++at;
+      for (int u = 0; u < SEL_U; ++u) {
+        bal[u] = __ballot(f[u] != 0);
+        if (lane == 0) cnts[u * 16 + wv] = __popcll(bal[u]);
       }
+      __syncthreads();
+      if (wv == 0) {  // exclusive scan of the (u, wave) counts, u-major
+        const int c0 = cnts[2 * lane], c1 = cnts[2 * lane + 1];
+        int x = c0 + c1;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+          const int y = __shfl_up(x, o, 64);
+          if (lane >= o) x += y;
+        }
+        const int ex = x - c0 - c1;
+        cpre[2 * lane] = ex;
+        cpre[2 * lane + 1] = ex + c0;
+        if (lane == 63) cpre[SEL_U * 16] = x;
+      }
+      __syncthreads();
+#pragma unroll
+      for (int u = 0; u < SEL_U; ++u) {
+        const int r = base + cpre[u * 16 + wv] + __popcll(bal[u] & ((1ull << lane) - 1ull));
+        if (f[u] && r < k - W) {
+          const int t = t0 + u * nt;
+          anc[r] = t;
+          rank[t] = r;
+        }
+      }
+      base += cpre[SEL_U * 16];
+      __syncthreads();
+    }
+    if (tid == 0 && base + W != k) atomicOr(&c.header[2], 2u);
   }
   for (int i = tid; i < W; i += nt) {
     anc[k - W + i] = P + i;
     rank[P + i] = k - W + i;
   }
-  if (tid == 0 && tot + W != k) atomicOr(&c.header[2], 2u);
 }
 
 template <int DT>
