@@ -58,38 +58,63 @@ __global__ __launch_bounds__(256) void k_shist(Geo g, Ws w) {
   for (int a = threadIdx.x; a < k; a += blockDim.x) out[(size_t)a * nT + ch] = hist[a];
 }
 
+// Per head, the (anchor, chunk) histogram becomes its exclusive prefix sums,
+// in place.  Batches of 8 x 1024 entries in (u, thread) order: coalesced
+// loads (the next batch's issued before the current one is scanned), wave
+// scans, and one scan of the per-(u, wave) totals per batch.
 __global__ __launch_bounds__(1024) void k_sscan(Geo g, Ws w) {
-  __shared__ int tmp[20];
+  constexpr int U = 8;
+  __shared__ int cnts[U * 16];
+  __shared__ int cpre[U * 16 + 1];
   const int b = blockIdx.x / g.H, h = blockIdx.x % g.H;
   const int nT = (g.S[b] + SORT_CHUNK - 1) / SORT_CHUNK;
   const int n = g.k[b] * nT;
   int32_t* a = shist_base(g, w, b, h);
-  const int per = (n + blockDim.x - 1) / blockDim.x;
-  const int lo = min(n, (int)threadIdx.x * per), hi = min(n, lo + per);
-  int s = 0;
-  for (int i = lo; i < hi; ++i) s += a[i];
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  int x = s;
-  for (int o = 1; o < 64; o <<= 1) {
-    int y = __shfl_up(x, o, 64);
-    if (lane >= o) x += y;
-  }
-  if (lane == 63) tmp[wave] = x;
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    int acc = 0;
-    for (int i = 0; i < (int)(blockDim.x >> 6); ++i) {
-      int v = tmp[i];
-      tmp[i] = acc;
-      acc += v;
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, nt = blockDim.x;  // nt = 1024
+  int cur[U], nxt[U];
+#pragma unroll
+  for (int u = 0; u < U; ++u) nxt[u] = u * nt + tid < n ? a[u * nt + tid] : 0;
+  int base = 0;
+  for (int c0 = 0; c0 < n; c0 += U * nt) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) cur[u] = nxt[u];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int i = c0 + U * nt + u * nt + tid;
+      nxt[u] = i < n ? a[i] : 0;
     }
-  }
-  __syncthreads();
-  int run = x - s + tmp[wave];
-  for (int i = lo; i < hi; ++i) {
-    int v = a[i];
-    a[i] = run;
-    run += v;
+    int x[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      x[u] = cur[u];
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        const int y = __shfl_up(x[u], o, 64);
+        if (lane >= o) x[u] += y;
+      }
+      if (lane == 63) cnts[u * 16 + wv] = x[u];
+    }
+    __syncthreads();
+    if (wv == 0) {
+      const int v0 = cnts[2 * lane], v1 = cnts[2 * lane + 1];
+      int y = v0 + v1;
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        const int z = __shfl_up(y, o, 64);
+        if (lane >= o) y += z;
+      }
+      cpre[2 * lane] = y - v0 - v1;
+      cpre[2 * lane + 1] = y - v1;
+      if (lane == 63) cpre[U * 16] = y;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int i = c0 + u * nt + tid;
+      if (i < n) a[i] = base + cpre[u * 16 + wv] + x[u] - cur[u];
+    }
+    base += cpre[U * 16];
+    __syncthreads();
   }
 }
 
