@@ -51,6 +51,40 @@ __device__ inline void load_rows_t(typename Elem<DT>::T* lds, const typename Ele
   }
 }
 
+// A tile of 32 token rows held in registers between its load and its LDS
+// store (RPT 16-byte chunks per thread), so the next tile's loads are in
+// flight while the current tile is processed.
+template <int DT>
+struct RowTile {
+  using E = typename Elem<DT>::T;
+  static constexpr int PER = 16 / sizeof(E), CPR = AKV_D / PER, RPT = 32 * CPR / 256;
+  uint4 v[RPT];
+  __device__ void load(const E* X, int t0, int S) {
+#pragma unroll
+    for (int i = 0; i < RPT; ++i) {
+      const int c = threadIdx.x + 256 * i, r = c / CPR, col = (c % CPR) * PER;
+      v[i] = t0 + r < S ? *(const uint4*)(X + (size_t)(t0 + r) * AKV_D + col) : make_uint4(0, 0, 0, 0);
+    }
+  }
+  __device__ void store(E* lds, int LD) const {
+#pragma unroll
+    for (int i = 0; i < RPT; ++i) {
+      const int c = threadIdx.x + 256 * i, r = c / CPR, col = (c % CPR) * PER;
+      *(uint4*)(lds + r * LD + col) = v[i];
+    }
+  }
+  // Transposed: lds[d * LDT + r] = X[t0 + r][d].
+  __device__ void store_t(E* lds, int LDT) const {
+#pragma unroll
+    for (int i = 0; i < RPT; ++i) {
+      const int c = threadIdx.x + 256 * i, r = c / CPR, col = (c % CPR) * PER;
+      const E* e = (const E*)&v[i];
+#pragma unroll
+      for (int j = 0; j < PER; ++j) lds[(col + j) * LDT + r] = e[j];
+    }
+  }
+};
+
 template <int DT>
 __device__ inline typename MF<DT>::frag zero_frag() {
   if constexpr (DT == 1) {
@@ -72,7 +106,8 @@ __device__ inline bool obs_visible(int t, int S, int P, int wr, int m, int W) {
 
 constexpr float NEG = -1e30f;
 
-template <int DT>
+// R = row blocks of 32 observation rows per wave (4 waves cover 128 R rows).
+template <int DT, int R>
 __global__ __launch_bounds__(256) void k_obs_stats(Geo g, Ws w, const void* Kin, const void* Qin) {
   using E = typename Elem<DT>::T;
   using M = MF<DT>;
@@ -91,28 +126,38 @@ __global__ __launch_bounds__(256) void k_obs_stats(Geo g, Ws w, const void* Kin,
   // Running row max (fp32 logits) and sum of exp in fp64; a change of the
   // max rescales the sum by an fp64 exp, so the sum keeps ~1e-9 relative
   // accuracy (the anchor selection re-scores near-ties against it).
-  float mx[2][16];
-  double sm[2][16];
+  float mx[R][16];
+  double sm[R][16];
 #pragma unroll
-  for (int r = 0; r < 2; ++r)
+  for (int r = 0; r < R; ++r)
 #pragma unroll
     for (int e = 0; e < 16; ++e) { mx[r][e] = NEG; sm[r][e] = 0.0; }
+  // Query fragments of the wave's row blocks stay in registers.
+  constexpr int NKS = AKV_D / M::KS;
+  typename M::frag qf[R][NKS];
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const int arow = min((wave + 4 * r) * 32 + (lane & 31), m - 1);
+#pragma unroll
+    for (int s = 0; s < NKS; ++s) qf[r][s] = M::load(Q + (size_t)arow * D, kofs(M::KS, s, lane));
+  }
   const int tb = ch * OBS_CHUNK, te = min(S, tb + OBS_CHUNK);
+  RowTile<DT> kt;
+  kt.load(X, tb, S);
   for (int t0 = tb; t0 < te; t0 += 32) {
     __syncthreads();
-    load_rows<DT>(KT, X, t0, S, D, LD);
+    kt.store(KT, LD);
     __syncthreads();
+    if (t0 + 32 < te) kt.load(X, t0 + 32, S);
 #pragma unroll
-    for (int r = 0; r < 2; ++r) {
+    for (int r = 0; r < R; ++r) {
       const int rb = wave + 4 * r;
       if (rb >= nrb) break;
-      const int arow = rb * 32 + (lane & 31);
       f32x16 acc = {};
-      for (int s = 0; s < D / M::KS; ++s) {
-        const int k0 = kofs(M::KS, s, lane);
-        auto a = arow < m ? M::load(Q + (size_t)arow * D, k0) : zero_frag<DT>();
-        auto bb = M::load_lds(&KT[(lane & 31) * LD], k0);
-        acc = M::mma(a, bb, acc);
+#pragma unroll
+      for (int s = 0; s < NKS; ++s) {
+        auto bb = M::load_lds(&KT[(lane & 31) * LD], kofs(M::KS, s, lane));
+        acc = M::mma(qf[r][s], bb, acc);
       }
       const int t = t0 + (lane & 31);
 #pragma unroll
@@ -131,7 +176,7 @@ __global__ __launch_bounds__(256) void k_obs_stats(Geo g, Ws w, const void* Kin,
   }
   // Merge the 32 lanes that share each row.
 #pragma unroll
-  for (int r = 0; r < 2; ++r) {
+  for (int r = 0; r < R; ++r) {
     const int rb = wave + 4 * r;
     if (rb >= nrb) break;
 #pragma unroll
@@ -174,7 +219,7 @@ __global__ __launch_bounds__(256) void k_obs_reduce(Geo g, Ws w) {
   }
 }
 
-template <int DT>
+template <int DT, int R>
 __global__ __launch_bounds__(256) void k_obs_pass(Geo g, Ws w, const void* Kin, const void* Vin, const void* Qin) {
   using E = typename Elem<DT>::T;
   using M = MF<DT>;
@@ -182,8 +227,8 @@ __global__ __launch_bounds__(256) void k_obs_pass(Geo g, Ws w, const void* Kin, 
   constexpr int LDT = 32 + (DT ? 8 : 4);  // transposed value tile / alpha tile row stride
   __shared__ __align__(16) E KT[32 * LD];
   __shared__ __align__(16) E VT[AKV_D * LDT];
-  __shared__ __align__(16) E AH[4][2][32 * LDT];  // alpha (hi part for bf16)
-  __shared__ __align__(16) E AL[DT ? 4 : 1][2][DT ? 32 * LDT : 1];  // alpha lo part (bf16 only)
+  __shared__ __align__(16) E AH[4][R][32 * LDT];  // alpha (hi part for bf16)
+  __shared__ __align__(16) E AL[DT ? 4 : 1][R][DT ? 32 * LDT : 1];  // alpha lo part (bf16 only)
   __shared__ float scb[32];
   int idx = blockIdx.x;
   const int b = locate(g, OBS_CHUNK, 1, idx);
@@ -199,30 +244,45 @@ __global__ __launch_bounds__(256) void k_obs_pass(Geo g, Ws w, const void* Kin, 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int nrb = (m + 31) / 32;
   const float isd = 1.0f / sqrtf((float)D);
-  f32x16 yacc[2][4];
+  f32x16 yacc[R][4];
 #pragma unroll
-  for (int r = 0; r < 2; ++r)
+  for (int r = 0; r < R; ++r)
 #pragma unroll
     for (int db = 0; db < 4; ++db) yacc[r][db] = f32x16{};
+  // Query fragments of the wave's row blocks stay in registers; the next
+  // token tile's keys and values are loaded while the current one is used.
+  constexpr int NKS = AKV_D / M::KS;
+  typename M::frag qf[R][NKS];
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const int arow = min((wave + 4 * r) * 32 + (lane & 31), m - 1);
+#pragma unroll
+    for (int s = 0; s < NKS; ++s) qf[r][s] = M::load(Q + (size_t)arow * D, kofs(M::KS, s, lane));
+  }
   const int tb = ch * OBS_CHUNK, te = min(S, tb + OBS_CHUNK);
   float* sc = w.sc + (size_t)g.prefS[b] * g.H + (size_t)h * S;
+  RowTile<DT> kt, vt;
+  kt.load(X, tb, S);
+  vt.load(Vx, tb, S);
   for (int t0 = tb; t0 < te; t0 += 32) {
     __syncthreads();
-    load_rows<DT>(KT, X, t0, S, D, LD);
-    load_rows_t<DT>(VT, Vx, t0, S, D, LDT);
+    kt.store(KT, LD);
+    vt.store_t(VT, LDT);
     if (threadIdx.x < 32) scb[threadIdx.x] = 0.0f;
     __syncthreads();
+    if (t0 + 32 < te) {
+      kt.load(X, t0 + 32, S);
+      vt.load(Vx, t0 + 32, S);
+    }
 #pragma unroll
-    for (int r = 0; r < 2; ++r) {
+    for (int r = 0; r < R; ++r) {
       const int rb = wave + 4 * r;
       if (rb >= nrb) break;
-      const int arow = rb * 32 + (lane & 31);
       f32x16 acc = {};
-      for (int s = 0; s < D / M::KS; ++s) {
-        const int k0 = kofs(M::KS, s, lane);
-        auto a = arow < m ? M::load(Q + (size_t)arow * D, k0) : zero_frag<DT>();
-        auto bb = M::load_lds(&KT[(lane & 31) * LD], k0);
-        acc = M::mma(a, bb, acc);
+#pragma unroll
+      for (int s = 0; s < NKS; ++s) {
+        auto bb = M::load_lds(&KT[(lane & 31) * LD], kofs(M::KS, s, lane));
+        acc = M::mma(qf[r][s], bb, acc);
       }
       const int tl = lane & 31, t = t0 + tl;
       float col = 0.0f;
@@ -266,7 +326,7 @@ __global__ __launch_bounds__(256) void k_obs_pass(Geo g, Ws w, const void* Kin, 
   // Partial outputs of this chunk.
   float* yp = w.ypart + ((size_t)(g.prefC[b] * g.H + h * nch + ch)) * m * D;
 #pragma unroll
-  for (int r = 0; r < 2; ++r) {
+  for (int r = 0; r < R; ++r) {
     const int rb = wave + 4 * r;
     if (rb >= nrb) break;
 #pragma unroll
@@ -304,16 +364,21 @@ __global__ __launch_bounds__(128) void k_obs_yreduce(Geo g, Ws w) {
 // ------------------------------------------------------------------ launchers
 hipError_t launch_obs(const Geo& g, const Ws& w, const void* K, const void* V, const void* Q, hipStream_t st) {
   int nblk = g.H * g.prefC[g.B];
+  const bool r2 = g.m > 128;  // 4 waves x 2 row blocks of 32 for up to 256 rows
   if (g.dtype == 1) {
-    AKV_TIMED("k_obs_stats", st, k_obs_stats<1><<<nblk, 256, 0, st>>>(g, w, K, Q));
+    if (r2) AKV_TIMED("k_obs_stats", st, (k_obs_stats<1, 2><<<nblk, 256, 0, st>>>(g, w, K, Q)));
+    else AKV_TIMED("k_obs_stats", st, (k_obs_stats<1, 1><<<nblk, 256, 0, st>>>(g, w, K, Q)));
   } else {
-    AKV_TIMED("k_obs_stats", st, k_obs_stats<0><<<nblk, 256, 0, st>>>(g, w, K, Q));
+    if (r2) AKV_TIMED("k_obs_stats", st, (k_obs_stats<0, 2><<<nblk, 256, 0, st>>>(g, w, K, Q)));
+    else AKV_TIMED("k_obs_stats", st, (k_obs_stats<0, 1><<<nblk, 256, 0, st>>>(g, w, K, Q)));
   }
   AKV_TIMED("k_obs_reduce", st, k_obs_reduce<<<g.B * g.H, 256, 0, st>>>(g, w));
   if (g.dtype == 1) {
-    AKV_TIMED("k_obs_pass", st, k_obs_pass<1><<<nblk, 256, 0, st>>>(g, w, K, V, Q));
+    if (r2) AKV_TIMED("k_obs_pass", st, (k_obs_pass<1, 2><<<nblk, 256, 0, st>>>(g, w, K, V, Q)));
+    else AKV_TIMED("k_obs_pass", st, (k_obs_pass<1, 1><<<nblk, 256, 0, st>>>(g, w, K, V, Q)));
   } else {
-    AKV_TIMED("k_obs_pass", st, k_obs_pass<0><<<nblk, 256, 0, st>>>(g, w, K, V, Q));
+    if (r2) AKV_TIMED("k_obs_pass", st, (k_obs_pass<0, 2><<<nblk, 256, 0, st>>>(g, w, K, V, Q)));
+    else AKV_TIMED("k_obs_pass", st, (k_obs_pass<0, 1><<<nblk, 256, 0, st>>>(g, w, K, V, Q)));
   }
   AKV_TIMED("k_obs_yreduce", st, k_obs_yreduce<<<g.B * g.H * g.m, 128, 0, st>>>(g, w));
   return hipGetLastError();
