@@ -85,6 +85,47 @@ struct RowTile {
   }
 };
 
+// Position of token r in row d of the transposed value tile: groups of 8
+// tokens stay contiguous (one MFMA operand load) and are permuted by d, which
+// spreads the stores of one wave over the LDS banks.
+__device__ inline int vt_pos(int d, int r) { return (((r >> 3) ^ (d >> 3)) & 3) * 8 + (r & 7); }
+
+// Value tile for the transposed LDS layout lds[d * LDT + vt_pos(d, r)] = X[t0 + r][d]:
+// thread c takes rows 2p, 2p+1 (p = c / CPR) of one 16-byte column chunk, so
+// for bf16 the two tokens of a column are stored as one 32-bit word.
+template <int DT>
+struct PairTile {
+  using E = typename Elem<DT>::T;
+  static constexpr int PER = 16 / sizeof(E), CPR = AKV_D / PER, NP = 16 * CPR / 256;
+  uint4 v0[NP], v1[NP];
+  __device__ void load(const E* X, int t0, int S) {
+#pragma unroll
+    for (int i = 0; i < NP; ++i) {
+      const int c = threadIdx.x + 256 * i, p = c / CPR, col = (c % CPR) * PER;
+      const int r0 = t0 + 2 * p;
+      v0[i] = r0 < S ? *(const uint4*)(X + (size_t)r0 * AKV_D + col) : make_uint4(0, 0, 0, 0);
+      v1[i] = r0 + 1 < S ? *(const uint4*)(X + (size_t)(r0 + 1) * AKV_D + col) : make_uint4(0, 0, 0, 0);
+    }
+  }
+  __device__ void store_t(E* lds, int LDT) const {
+#pragma unroll
+    for (int i = 0; i < NP; ++i) {
+      const int c = threadIdx.x + 256 * i, p = c / CPR, col = (c % CPR) * PER;
+      const E* e0 = (const E*)&v0[i];
+      const E* e1 = (const E*)&v1[i];
+      if constexpr (sizeof(E) == 2) {
+#pragma unroll
+        for (int j = 0; j < PER; ++j)
+          *(uint32_t*)(lds + (col + j) * LDT + vt_pos(col + j, 2 * p)) = (uint32_t)e0[j] | ((uint32_t)e1[j] << 16);
+      } else {
+#pragma unroll
+        for (int j = 0; j < PER; ++j)
+          *(float2*)(lds + (col + j) * LDT + vt_pos(col + j, 2 * p)) = make_float2(e0[j], e1[j]);
+      }
+    }
+  }
+};
+
 template <int DT>
 __device__ inline typename MF<DT>::frag zero_frag() {
   if constexpr (DT == 1) {
@@ -224,7 +265,7 @@ __global__ __launch_bounds__(256) void k_obs_pass(Geo g, Ws w, const void* Kin, 
   using E = typename Elem<DT>::T;
   using M = MF<DT>;
   constexpr int LD = TileLD<DT>::v;
-  constexpr int LDT = 32 + (DT ? 8 : 4);  // transposed value tile / alpha tile row stride
+  constexpr int LDT = 32 + (DT ? 8 : 4);  // transposed value tile / alpha tile row stride (16-byte aligned rows)
   __shared__ __align__(16) E KT[32 * LD];
   __shared__ __align__(16) E VT[AKV_D * LDT];
   __shared__ __align__(16) E AH[4][R][32 * LDT];  // alpha (hi part for bf16)
@@ -261,7 +302,8 @@ __global__ __launch_bounds__(256) void k_obs_pass(Geo g, Ws w, const void* Kin, 
   }
   const int tb = ch * OBS_CHUNK, te = min(S, tb + OBS_CHUNK);
   float* sc = w.sc + (size_t)g.prefS[b] * g.H + (size_t)h * S;
-  RowTile<DT> kt, vt;
+  RowTile<DT> kt;
+  PairTile<DT> vt;
   kt.load(X, tb, S);
   vt.load(Vx, tb, S);
   for (int t0 = tb; t0 < te; t0 += 32) {
@@ -311,7 +353,8 @@ __global__ __launch_bounds__(256) void k_obs_pass(Geo g, Ws w, const void* Kin, 
         auto ah = M::load_lds(&AH[wave][r][(lane & 31) * LDT], k0);
 #pragma unroll
         for (int db = 0; db < 4; ++db) {
-          auto vb = M::load_lds(&VT[(db * 32 + (lane & 31)) * LDT], k0);
+          const int d = db * 32 + (lane & 31);
+          auto vb = M::load_lds(&VT[d * LDT + vt_pos(d, k0)], 0);
           yacc[r][db] = M::mma(ah, vb, yacc[r][db]);
           if constexpr (DT == 1) {
             auto alo = M::load_lds(&AL[wave][r][(lane & 31) * LDT], k0);
