@@ -207,9 +207,10 @@ anchorkv_status anchorkv_export(const anchorkv_plan* plan, const void* cache_hos
 
 /* Kernel timing for benchmarks and tracing.  While enabled, every launch of
  * a kernel named in the comma-separated list `kernels` (e.g.
- * "k_dec_stream,k_assign") is bracketed by a pair of HIP events recorded on
- * the launch's own stream, up to max_launches pairs per kernel (events are
- * created here, host side, no device memory).  anchorkv_profile_read waits
+ * "k_dec_stream,k_assign") carries a pair of HIP events that the launch on
+ * its own stream stamps with the kernel's begin and end (hipExtLaunchKernel),
+ * up to max_launches pairs per kernel (events are created here, host side,
+ * no device memory).  anchorkv_profile_read waits
  * for the recorded events of one kernel and returns their summed elapsed
  * milliseconds and the number of timed launches; disable releases the events.
  * Process-wide; calls are serialized by a lock. */

@@ -8,6 +8,7 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+#include <hip/hip_ext.h>
 #include <stdint.h>
 
 // Every floating-point expression of the library is evaluated as written:
@@ -371,15 +372,22 @@ __device__ inline void fwht_wave(float& z0, float& z1, int lane) {
   }
 }
 
-// Kernel timing hook (anchorkv_profile_*): records a HIP event on `st` before
-// (after = false) or after a launch of the named kernel when it is profiled.
-void prof_mark(const char* kernel, hipStream_t st, bool after);
+// Kernel timing hook (anchorkv_profile_*): when launches of the named kernel
+// are being timed, returns the start/stop event pair of this launch (else
+// false).  The pair is handed to hipExtLaunchKernel, which stamps them with
+// the kernel's own begin and end, so the measured time excludes the gaps
+// between launches.
+bool prof_events(const char* kernel, hipEvent_t* start, hipEvent_t* stop);
+
+// Launches kernel<<<grid, block, lds, st>>>(args...), timed when profiled.
+template <typename... KArgs, typename... Args>
+inline void launch(const char* name, void (*kernel)(KArgs...), dim3 grid, dim3 block, uint32_t lds, hipStream_t st,
+                   Args... args) {
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  if (prof_events(name, &e0, &e1))
+    hipExtLaunchKernelGGL(kernel, grid, block, lds, st, e0, e1, 0, static_cast<KArgs>(args)...);
+  else
+    hipLaunchKernelGGL(kernel, grid, block, lds, st, static_cast<KArgs>(args)...);
+}
 
 }  // namespace akv
-
-#define AKV_TIMED(name, st, ...)           \
-  do {                                     \
-    ::akv::prof_mark(name, st, false);     \
-    __VA_ARGS__;                           \
-    ::akv::prof_mark(name, st, true);      \
-  } while (0)

@@ -576,7 +576,6 @@ struct KernelEvents {
   std::string name;
   std::vector<hipEvent_t> ev;  // 2 per launch
   int used = 0;
-  bool open = false;
 };
 struct Profiler {
   std::mutex mu;
@@ -595,19 +594,18 @@ void release_events(Profiler& p) {
 }
 }  // namespace
 
-void akv::prof_mark(const char* kernel, hipStream_t st, bool after) {
+bool akv::prof_events(const char* kernel, hipEvent_t* start, hipEvent_t* stop) {
   Profiler& p = profiler();
-  if (!p.on.load(std::memory_order_acquire)) return;
+  if (!p.on.load(std::memory_order_acquire)) return false;
   std::lock_guard<std::mutex> lk(p.mu);
   for (auto& ke : p.k) {
-    if (ke.name != kernel) continue;
-    if (!after) {
-      if (2 * ke.used + 1 < (int)ke.ev.size() && hipEventRecord(ke.ev[2 * ke.used], st) == hipSuccess) ke.open = true;
-    } else if (ke.open) {
-      if (hipEventRecord(ke.ev[2 * ke.used + 1], st) == hipSuccess) ++ke.used;
-      ke.open = false;
-    }
+    if (ke.name != kernel || 2 * ke.used + 1 >= (int)ke.ev.size()) continue;
+    *start = ke.ev[2 * ke.used];
+    *stop = ke.ev[2 * ke.used + 1];
+    ++ke.used;
+    return true;
   }
+  return false;
 }
 
 extern "C" anchorkv_status anchorkv_profile_enable(const char* kernels, int32_t max_launches) {
@@ -688,7 +686,7 @@ __global__ void k_init(Geo g, Cache c, Ws w) {
 }
 hipError_t launch_init(const Geo& g, const Cache& c, const Ws& w, hipStream_t st) {
   const int n = 4 * g.B > 2 * g.H * g.B ? 4 * g.B : 2 * g.H * g.B;
-  AKV_TIMED("k_init", st, k_init<<<(n + 255) / 256, 256, 0, st>>>(g, c, w));
+  launch("k_init", k_init, dim3((n + 255) / 256), dim3(256), 0, st, g, c, w);
   return hipGetLastError();
 }
 }  // namespace akv

@@ -1073,10 +1073,9 @@ static void launch_steps(const Geo& g, const Cache& c, const DecWs& dw, const vo
   const int nR = attn ? (g.prefNK[g.B] + 255) / 256 : 0;
   const int flags = (attn ? 1 : 0) | (app ? 2 : 0);
   const float sl2 = scale * 1.4426950408889634f;
-  AKV_TIMED("k_dec_front", st,
-            k_dec_front<DT, GQ><<<nAK + nAV + nR, 256, 0, st>>>(g, c, dw, q, kn, vn, flags, nAK, nAV, sl2));
+  launch("k_dec_front", k_dec_front<DT, GQ>, dim3(nAK + nAV + nR), dim3(256), 0, st, g, c, dw, q, kn, vn, flags, nAK, nAV, sl2);
   if (!attn) {
-    AKV_TIMED("k_app_finish", st, k_app_finish<DT><<<g.B * g.H, 256, 0, st>>>(g, c, dw, n_app, kn, vn));
+    launch("k_app_finish", k_app_finish<DT>, dim3(g.B * g.H), dim3(256), 0, st, g, c, dw, n_app, kn, vn);
     return;
   }
   const int L = g.dsplit;
@@ -1084,11 +1083,11 @@ static void launch_steps(const Geo& g, const Cache& c, const DecWs& dw, const vo
   for (int b = 0; b < g.B; ++b) nst += g.H * ((g.S[b] + L - 1) / L);
   const int ntb = g.B * g.H;  // tail workgroups
   if (L == 2048) {
-    AKV_TIMED("k_dec_stream", st, (k_dec_stream<DT, GQ, 8><<<nst + ntb, 256, 0, st>>>(g, c, dw, nst, n_app, kn, vn)));
+    launch("k_dec_stream", k_dec_stream<DT, GQ, 8>, dim3(nst + ntb), dim3(256), 0, st, g, c, dw, nst, n_app, kn, vn);
   } else {
-    AKV_TIMED("k_dec_stream", st, (k_dec_stream<DT, GQ, 4><<<nst + ntb, 256, 0, st>>>(g, c, dw, nst, n_app, kn, vn)));
+    launch("k_dec_stream", k_dec_stream<DT, GQ, 4>, dim3(nst + ntb), dim3(256), 0, st, g, c, dw, nst, n_app, kn, vn);
   }
-  AKV_TIMED("k_dec_merge", st, (k_dec_merge<DT, GQ><<<g.B * g.Hq, 256, 0, st>>>(g, dw, out, out_dtype)));
+  launch("k_dec_merge", k_dec_merge<DT, GQ>, dim3(g.B * g.Hq), dim3(256), 0, st, g, dw, out, out_dtype);
 }
 
 template <int DT>
@@ -1121,9 +1120,9 @@ hipError_t launch_reconstruct(const Geo& g, const Cache& c, int b, int side, int
   const int rows = g.S[b] + n_app;
   const int nblk = (g.H * rows + 3) / 4;
   if (g.dtype == 1) {
-    AKV_TIMED("k_reconstruct", st, k_reconstruct<1><<<nblk, 256, 0, st>>>(g, c, b, side, n_app, out));
+    launch("k_reconstruct", k_reconstruct<1>, dim3(nblk), dim3(256), 0, st, g, c, b, side, n_app, out);
   } else {
-    AKV_TIMED("k_reconstruct", st, k_reconstruct<0><<<nblk, 256, 0, st>>>(g, c, b, side, n_app, out));
+    launch("k_reconstruct", k_reconstruct<0>, dim3(nblk), dim3(256), 0, st, g, c, b, side, n_app, out);
   }
   return hipGetLastError();
 }

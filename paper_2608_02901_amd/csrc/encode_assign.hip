@@ -436,11 +436,11 @@ hipError_t launch_assign(const Geo& g, const Ws& w, const Cache& c, const void* 
   int nblk = 0;
   for (int b = 0; b < g.B; ++b) nblk += g.H * ((g.S[b] + ASSIGN_TOK - 1) / ASSIGN_TOK) * 2;
   if (g.dtype == 1) {
-    AKV_TIMED("k_assign", st, k_assign<1><<<nblk, 256, 0, st>>>(g, w, c, K, V));
-    AKV_TIMED("k_fixup", st, k_fixup<1><<<512, 256, 0, st>>>(g, w, c, K, V));
+    launch("k_assign", k_assign<1>, dim3(nblk), dim3(256), 0, st, g, w, c, K, V);
+    launch("k_fixup", k_fixup<1>, dim3(512), dim3(256), 0, st, g, w, c, K, V);
   } else {
-    AKV_TIMED("k_assign", st, k_assign<0><<<nblk, 256, 0, st>>>(g, w, c, K, V));
-    AKV_TIMED("k_fixup", st, k_fixup<0><<<512, 256, 0, st>>>(g, w, c, K, V));
+    launch("k_assign", k_assign<0>, dim3(nblk), dim3(256), 0, st, g, w, c, K, V);
+    launch("k_fixup", k_fixup<0>, dim3(512), dim3(256), 0, st, g, w, c, K, V);
   }
   return hipGetLastError();
 }

@@ -190,15 +190,15 @@ __global__ __launch_bounds__(256) void k_bmark(Geo g, Ws w) {
 hipError_t launch_budget(const Geo& g, const Ws& w, hipStream_t st) {
   int nblk = 0;
   for (int b = 0; b < g.B; ++b) nblk += 2 * ((g.H * g.S[b] + BCHUNK - 1) / BCHUNK);
-  AKV_TIMED("k_binit", st, k_binit<<<g.B * 2, 256, 0, st>>>(g, w));
+  launch("k_binit", k_binit, dim3(g.B * 2), dim3(256), 0, st, g, w);
   for (int pass = 0; pass < 4; ++pass) {
     const int shift = 24 - 8 * pass;
-    AKV_TIMED("k_bhist", st, k_bhist<<<nblk, 256, 0, st>>>(g, w, shift));
-    AKV_TIMED("k_bpick", st, k_bpick<<<g.B * 2, 256, 0, st>>>(g, w, shift));
+    launch("k_bhist", k_bhist, dim3(nblk), dim3(256), 0, st, g, w, shift);
+    launch("k_bpick", k_bpick, dim3(g.B * 2), dim3(256), 0, st, g, w, shift);
   }
-  AKV_TIMED("k_btie", st, k_btie<<<nblk, 256, 0, st>>>(g, w));
-  AKV_TIMED("k_btscan", st, k_btscan<<<g.B * 2, 64, 0, st>>>(g, w));
-  AKV_TIMED("k_bmark", st, k_bmark<<<nblk, 256, 0, st>>>(g, w));
+  launch("k_btie", k_btie, dim3(nblk), dim3(256), 0, st, g, w);
+  launch("k_btscan", k_btscan, dim3(g.B * 2), dim3(64), 0, st, g, w);
+  launch("k_bmark", k_bmark, dim3(nblk), dim3(256), 0, st, g, w);
   return hipGetLastError();
 }
 

@@ -214,9 +214,9 @@ hipError_t launch_epilogue(const Geo& g, const Ws& w, const Cache& c, const void
   int nblk = 0;
   for (int b = 0; b < g.B; ++b) nblk += g.H * ((g.S[b] + 31) / 32);
   if (g.dtype == 1) {
-    AKV_TIMED("k_epilogue", st, k_epilogue<1><<<nblk, 256, 0, st>>>(g, w, c, K, V, Q));
+    launch("k_epilogue", k_epilogue<1>, dim3(nblk), dim3(256), 0, st, g, w, c, K, V, Q);
   } else {
-    AKV_TIMED("k_epilogue", st, k_epilogue<0><<<nblk, 256, 0, st>>>(g, w, c, K, V, Q));
+    launch("k_epilogue", k_epilogue<0>, dim3(nblk), dim3(256), 0, st, g, w, c, K, V, Q);
   }
   return hipGetLastError();
 }

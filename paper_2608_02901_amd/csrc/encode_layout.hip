@@ -322,20 +322,20 @@ hipError_t launch_layout(const Geo& g, const Ws& w, const Cache& c, const void* 
     nrec += g.H * ((g.S[b] + 255) / 256);
   }
   const size_t lds = (size_t)g.maxK * sizeof(int);
-  AKV_TIMED("k_shist", st, k_shist<<<nsort, 256, lds, st>>>(g, w));
-  AKV_TIMED("k_sscan", st, k_sscan<<<g.B * g.H, 1024, 0, st>>>(g, w));
-  AKV_TIMED("k_sscatter", st, k_sscatter<<<nsort, 64, lds, st>>>(g, w, c));
+  launch("k_shist", k_shist, dim3(nsort), dim3(256), lds, st, g, w);
+  launch("k_sscan", k_sscan, dim3(g.B * g.H), dim3(1024), 0, st, g, w);
+  launch("k_sscatter", k_sscatter, dim3(nsort), dim3(64), lds, st, g, w, c);
   if (g.dtype == 1) {
-    AKV_TIMED("k_lrec", st, k_lrec<1><<<nrec, 256, 0, st>>>(g, w, c));
+    launch("k_lrec", k_lrec<1>, dim3(nrec), dim3(256), 0, st, g, w, c);
   } else {
-    AKV_TIMED("k_lrec", st, k_lrec<0><<<nrec, 256, 0, st>>>(g, w, c));
+    launch("k_lrec", k_lrec<0>, dim3(nrec), dim3(256), 0, st, g, w, c);
   }
-  AKV_TIMED("k_lscan", st, k_lscan<<<g.B * 2, 1024, 0, st>>>(g, w, c));
+  launch("k_lscan", k_lscan, dim3(g.B * 2), dim3(1024), 0, st, g, w, c);
   const int nwords = 2 * g.prefW[g.B] * g.H;
   if (g.dtype == 1) {
-    AKV_TIMED("k_codec", st, k_codec<1><<<(nwords + 3) / 4, 256, 0, st>>>(g, w, c, K, V));
+    launch("k_codec", k_codec<1>, dim3((nwords + 3) / 4), dim3(256), 0, st, g, w, c, K, V);
   } else {
-    AKV_TIMED("k_codec", st, k_codec<0><<<(nwords + 3) / 4, 256, 0, st>>>(g, w, c, K, V));
+    launch("k_codec", k_codec<0>, dim3((nwords + 3) / 4), dim3(256), 0, st, g, w, c, K, V);
   }
   return hipGetLastError();
 }

@@ -409,21 +409,21 @@ hipError_t launch_obs(const Geo& g, const Ws& w, const void* K, const void* V, c
   int nblk = g.H * g.prefC[g.B];
   const bool r2 = g.m > 128;  // 4 waves x 2 row blocks of 32 for up to 256 rows
   if (g.dtype == 1) {
-    if (r2) AKV_TIMED("k_obs_stats", st, (k_obs_stats<1, 2><<<nblk, 256, 0, st>>>(g, w, K, Q)));
-    else AKV_TIMED("k_obs_stats", st, (k_obs_stats<1, 1><<<nblk, 256, 0, st>>>(g, w, K, Q)));
+    if (r2) launch("k_obs_stats", k_obs_stats<1, 2>, dim3(nblk), dim3(256), 0, st, g, w, K, Q);
+    else launch("k_obs_stats", k_obs_stats<1, 1>, dim3(nblk), dim3(256), 0, st, g, w, K, Q);
   } else {
-    if (r2) AKV_TIMED("k_obs_stats", st, (k_obs_stats<0, 2><<<nblk, 256, 0, st>>>(g, w, K, Q)));
-    else AKV_TIMED("k_obs_stats", st, (k_obs_stats<0, 1><<<nblk, 256, 0, st>>>(g, w, K, Q)));
+    if (r2) launch("k_obs_stats", k_obs_stats<0, 2>, dim3(nblk), dim3(256), 0, st, g, w, K, Q);
+    else launch("k_obs_stats", k_obs_stats<0, 1>, dim3(nblk), dim3(256), 0, st, g, w, K, Q);
   }
-  AKV_TIMED("k_obs_reduce", st, k_obs_reduce<<<g.B * g.H, 256, 0, st>>>(g, w));
+  launch("k_obs_reduce", k_obs_reduce, dim3(g.B * g.H), dim3(256), 0, st, g, w);
   if (g.dtype == 1) {
-    if (r2) AKV_TIMED("k_obs_pass", st, (k_obs_pass<1, 2><<<nblk, 256, 0, st>>>(g, w, K, V, Q)));
-    else AKV_TIMED("k_obs_pass", st, (k_obs_pass<1, 1><<<nblk, 256, 0, st>>>(g, w, K, V, Q)));
+    if (r2) launch("k_obs_pass", k_obs_pass<1, 2>, dim3(nblk), dim3(256), 0, st, g, w, K, V, Q);
+    else launch("k_obs_pass", k_obs_pass<1, 1>, dim3(nblk), dim3(256), 0, st, g, w, K, V, Q);
   } else {
-    if (r2) AKV_TIMED("k_obs_pass", st, (k_obs_pass<0, 2><<<nblk, 256, 0, st>>>(g, w, K, V, Q)));
-    else AKV_TIMED("k_obs_pass", st, (k_obs_pass<0, 1><<<nblk, 256, 0, st>>>(g, w, K, V, Q)));
+    if (r2) launch("k_obs_pass", k_obs_pass<0, 2>, dim3(nblk), dim3(256), 0, st, g, w, K, V, Q);
+    else launch("k_obs_pass", k_obs_pass<0, 1>, dim3(nblk), dim3(256), 0, st, g, w, K, V, Q);
   }
-  AKV_TIMED("k_obs_yreduce", st, k_obs_yreduce<<<g.B * g.H * g.m, 128, 0, st>>>(g, w));
+  launch("k_obs_yreduce", k_obs_yreduce, dim3(g.B * g.H * g.m), dim3(128), 0, st, g, w);
   return hipGetLastError();
 }
 

@@ -565,18 +565,18 @@ hipError_t launch_select(const Geo& g, const Ws& w, const Cache& c, const void* 
   for (int b = 0; b < g.B; ++b) nblk += g.H * ((g.k[b] + 63) / 64);
   const int nbh = g.B * g.H;
   if (g.dtype == 1) {
-    AKV_TIMED("k_select", st, k_sel_top<1><<<nbh, 1024, 0, st>>>(g, w, c, ovr));
-    if (!ovr) AKV_TIMED("k_sel_band", st, k_sel_band<1><<<nbh * SEL_BAND_MAX, 256, 0, st>>>(g, w, K, Q));
-    AKV_TIMED("k_sel_rest", st, k_sel_rest<1><<<nbh, 1024, 0, st>>>(g, w, c, ovr));
+    launch("k_select", k_sel_top<1>, dim3(nbh), dim3(1024), 0, st, g, w, c, ovr);
+    if (!ovr) launch("k_sel_band", k_sel_band<1>, dim3(nbh * SEL_BAND_MAX), dim3(256), 0, st, g, w, K, Q);
+    launch("k_sel_rest", k_sel_rest<1>, dim3(nbh), dim3(1024), 0, st, g, w, c, ovr);
   } else {
-    AKV_TIMED("k_select", st, k_sel_top<0><<<nbh, 1024, 0, st>>>(g, w, c, ovr));
-    if (!ovr) AKV_TIMED("k_sel_band", st, k_sel_band<0><<<nbh * SEL_BAND_MAX, 256, 0, st>>>(g, w, K, Q));
-    AKV_TIMED("k_sel_rest", st, k_sel_rest<0><<<nbh, 1024, 0, st>>>(g, w, c, ovr));
+    launch("k_select", k_sel_top<0>, dim3(nbh), dim3(1024), 0, st, g, w, c, ovr);
+    if (!ovr) launch("k_sel_band", k_sel_band<0>, dim3(nbh * SEL_BAND_MAX), dim3(256), 0, st, g, w, K, Q);
+    launch("k_sel_rest", k_sel_rest<0>, dim3(nbh), dim3(1024), 0, st, g, w, c, ovr);
   }
   if (g.dtype == 1) {
-    AKV_TIMED("k_anchor_prep", st, k_anchor_prep<1><<<nblk, 256, 0, st>>>(g, w, c, K, V, Q));
+    launch("k_anchor_prep", k_anchor_prep<1>, dim3(nblk), dim3(256), 0, st, g, w, c, K, V, Q);
   } else {
-    AKV_TIMED("k_anchor_prep", st, k_anchor_prep<0><<<nblk, 256, 0, st>>>(g, w, c, K, V, Q));
+    launch("k_anchor_prep", k_anchor_prep<0>, dim3(nblk), dim3(256), 0, st, g, w, c, K, V, Q);
   }
   return hipGetLastError();
 }
