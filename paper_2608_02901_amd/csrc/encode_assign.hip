@@ -97,7 +97,9 @@ __global__ __launch_bounds__(256) void k_assign(Geo g, Ws w, Cache c, const void
       int ch = threadIdx.x + 256 * i;
       int r = ch / (AKV_D / PER), col = (ch % (AKV_D / PER)) * PER;
       int a = st * STAGE + r;
-      pre[i] = a < k ? *(const uint4*)(A + (size_t)a * D + col) : make_uint4(0, 0, 0, 0);
+      // rows past k repeat row k - 1; their inverse norm is 0, so they score 0
+      const uint4* src = (const uint4*)(A + (size_t)min(a, k - 1) * D + col);
+      pre[i] = make_uint4(src->x, src->y, src->z, src->w);
     }
     if (threadIdx.x < STAGE) {
       int a = st * STAGE + threadIdx.x;
@@ -142,15 +144,19 @@ __global__ __launch_bounds__(256) void k_assign(Geo g, Ws w, Cache c, const void
 #pragma unroll
     for (int e = 0; e < 16; ++e) wsr[e] = WS[buf][blk * 32 + crow(e, lane)];
   };
+  // Two scores at a time: the runner-up of {b1, b2, v0, v1} (b1 >= b2) is
+  // max(b2, med3(b1, v0, v1)) and the best is max3(b1, v0, v1), three VALU
+  // operations per pair instead of four.
   auto scores = [&](const f32x16 (&acc)[ASSIGN_NT], const float (&wsr)[16], int abase) {
 #pragma unroll
     for (int n = 0; n < ASSIGN_NT; ++n) {
       const float b1o = b1[n];
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const float v = tag_score(fabsf(acc[n][e]) * wsr[e], 15u - (uint32_t)e);
-        b2[n] = __builtin_amdgcn_fmed3f(b1[n], b2[n], v);
-        b1[n] = fmaxf(b1[n], v);
+      for (int e = 0; e < 16; e += 2) {
+        const float v0 = tag_score(fabsf(acc[n][e]) * wsr[e], 15u - (uint32_t)e);
+        const float v1 = tag_score(fabsf(acc[n][e + 1]) * wsr[e + 1], 14u - (uint32_t)e);
+        b2[n] = fmaxf(b2[n], __builtin_amdgcn_fmed3f(b1[n], v0, v1));
+        b1[n] = fmaxf(fmaxf(b1[n], v0), v1);
       }
       tb1[n] = b1[n] != b1o ? abase >> 5 : tb1[n];
     }
