@@ -125,7 +125,7 @@ struct DecWs {
   float* RK;            // [sum N_K][g] key-residual logit terms q_rot . zhat / D
   float* part;          // [b][Hq][split][4 + D] split record (max, sum, -, -, output[D])
   float* asc;           // [side][b][h][kp_b] screening score of the appended token per anchor
-  float4* atop;         // [side][b][h][ceil(k_b/256)] top-2 of those scores per 256 anchors
+  float4* atop;         // [side][b][h][4 ceil(k_b/256)] top-2 of those scores per 64 anchors
 };
 
 // ------------------------------------------------------------------ vector types

@@ -302,7 +302,7 @@ extern "C" anchorkv_status anchorkv_plan_create(const anchorkv_config* cfg, int3
   p->d_RK = Dl.add(4 * (size_t)geo.prefNK[batch] * g);
   p->d_part = Dl.add(4 * (size_t)geo.prefSp[batch] * geo.Hq * (4 + D));
   p->d_asc = Dl.add(4 * 2 * (size_t)geo.prefKp[batch] * H);
-  p->d_atop = Dl.add(16 * 2 * (size_t)geo.prefAB[batch] * H);
+  p->d_atop = Dl.add(16 * 2 * 4 * (size_t)geo.prefAB[batch] * H);
   p->dws_bytes = Dl.total;
   *out = p;
   return ANCHORKV_OK;

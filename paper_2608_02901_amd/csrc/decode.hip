@@ -14,11 +14,13 @@
 //
 // One decode step is two launches:
 //   k_dec_front  : work that depends only on the new query and token, fully
-//                  parallel: anchor scores S_K[a][j] = q_j . abar^K_a (one
-//                  thread per anchor, the row in registers), key-residual terms
-//                  q_rot . zhat^K_e / D (one thread per stored key residual), and,
-//                  when a token is appended, its screening similarity to every
-//                  anchor of both sides with a per-256-anchor top-2;
+//                  parallel: anchor scores S_K[a][j] = q_j . abar^K_a (bf16:
+//                  one MFMA contraction of 16-anchor tiles with the queries and
+//                  the appended token as columns; fp32: one thread per anchor,
+//                  the row in registers), key-residual terms q_rot . zhat^K_e / D
+//                  (one thread per stored key residual), and, when a token is
+//                  appended, its screening similarity to every anchor of both
+//                  sides with a per-64-anchor top-2;
 //   k_dec_stream : split-K pass over the value-anchor-grouped records.  Loads
 //                  come in two rounds (records and flag words; then anchor
 //                  scores, key-residual terms, value-anchor rows and value
@@ -141,6 +143,111 @@ __device__ inline void top2_wave_dpp(float& b1, float& b2, int& i1) {
   top2_step<32>(b1, b2, i1);
 }
 
+// Screening top-2 records of the appended token: one per 64 anchors (a wave's
+// share of a 256-anchor block), [side][b][h][4 ceil(k_b / 256)].
+__device__ inline size_t atop_index(const Geo& g, int side, int b, int h, int chunk) {
+  const int nab = (g.k[b] + 255) / 256;
+  return 4 * ((size_t)side * g.H * g.prefAB[g.B] + (size_t)g.prefAB[b] * g.H + (size_t)h * nab) + chunk;
+}
+
+// One block of 256 bf16 anchors of (request b, head h, side) on MFMA
+// (v_mfma_f32_16x16x32_bf16).  Wave w takes anchors ch * 256 + 64 w .. +63 as
+// four 16-row tiles, loaded straight into A fragments; B holds the g queries
+// in columns 0 .. g-1 (key side, attention) and the appended token in column
+// g (append), zeros elsewhere.  One contraction gives the anchor scores
+// S_K[a][j] (stored scaled by sl2) and the screening products x . abar_a; the
+// screening score |x . abar_a| / ||abar_a|| and the block's top-2 follow.  fp32
+// accumulation of exact bf16 products in any order stays within the error
+// bound the appended token's certification assumes.
+template <int GQ>
+__device__ void anchor_block_mfma(const Geo& g, const Cache& c, const DecWs& dw, const void* q, const void* kin,
+                                  const void* vin, bool attn, bool app, int side, int b, int h, int ch, float sl2) {
+  static_assert(GQ < 16, "queries and the appended token share one 16-column tile");
+  constexpr int D = AKV_D;
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int k = g.k[b], kp = (k + 3) & ~3;
+  const size_t ko = (size_t)g.prefK[b] * g.H + (size_t)h * k;
+  const size_t ab = (size_t)g.prefKp[b] * g.H + (size_t)h * kp;
+  const uint16_t* A = (const uint16_t*)(side ? c.ancV : c.ancK) + ko * D;
+  const bool doq = attn && side == 0;
+  const int col = lane & 15, kq = lane >> 4;
+  const uint16_t* bsrc = nullptr;
+  if (doq && col < GQ) bsrc = (const uint16_t*)q + ((size_t)b * g.Hq + (size_t)h * GQ + col) * D;
+  if (app && col == GQ) bsrc = (const uint16_t*)(side ? vin : kin) + ((size_t)b * g.H + h) * D;
+  bf16x8 bf[4];
+#pragma unroll
+  for (int ks = 0; ks < 4; ++ks) {
+    const uint4 v = bsrc ? *(const uint4*)(bsrc + 32 * ks + 8 * kq) : make_uint4(0, 0, 0, 0);
+    bf[ks] = __builtin_bit_cast(bf16x8, v);
+  }
+  const int a0 = ch * 256 + wave * 64;
+  // inverse norms of the lane's 16 anchors, issued with the rows; loaded and
+  // used by every lane (only column g keeps them), so the loads stay here
+  const float* inv = (side ? c.invV : c.invK) + ko;
+  float ivs[4][4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) ivs[t][i] = inv[min(a0 + 16 * t + 4 * kq + i, k - 1)];
+  bf16x8 af[4][4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    const uint16_t* row = A + (size_t)min(a0 + 16 * t + col, k - 1) * D + 8 * kq;
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) af[t][ks] = __builtin_bit_cast(bf16x8, *(const uint4*)(row + 32 * ks));
+  }
+  float* ascp = dw.asc + (size_t)side * g.H * g.prefKp[g.B] + ab + a0 + 4 * kq;
+  float4* atopp = dw.atop + atop_index(g, side, b, h, 4 * ch + wave);
+  f32x4 acc[4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    acc[t] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[t][ks], bf[ks], acc[t], 0, 0, 0);
+  }
+  // lane holds column col of anchors a0 + 16 t + 4 kq + i, i = 0..3; a
+  // wave whose 64 anchors all exist (every wave but a head's last) stores
+  // without per-element guards.
+  const bool full = a0 + 63 < k;
+  if (doq && col < GQ) {
+    float* skp = dw.SK + (ab + a0 + 4 * kq) * GQ + col;
+    if (full) {
+#pragma unroll
+      for (int t = 0; t < 4; ++t)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) skp[(16 * t + i) * GQ] = acc[t][i] * sl2;
+    } else {
+#pragma unroll
+      for (int t = 0; t < 4; ++t)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          if (a0 + 16 * t + 4 * kq + i < k) skp[(16 * t + i) * GQ] = acc[t][i] * sl2;
+    }
+  }
+  if (!app) return;
+  float b1 = -1.0f, b2 = -1.0f;
+  int i1 = 0x7fffffff;
+  float sc[4][4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int a = a0 + 16 * t + 4 * kq + i;
+      const bool ok = col == GQ && (full || a < k);
+      sc[t][i] = ok ? fabsf(acc[t][i]) * ivs[t][i] : -1.0f;
+      top2_merge(b1, b2, i1, sc[t][i], -1.0f, ok ? a : 0x7fffffff);
+    }
+  if (col == GQ) {
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        if (full || a0 + 16 * t + 4 * kq + i < k) ascp[16 * t + i] = sc[t][i];
+  }
+  top2_wave_dpp(b1, b2, i1);
+  if (lane == 0) *atopp = make_float4(b1, b2, __int_as_float(i1), 0.0f);
+}
+
 // Grid: nAK key-anchor blocks, nAV value-anchor blocks (append only), then
 // ceil(sum N_K / 256) key-residual blocks (attention only).  flags: bit 0 =
 // attention (q given), bit 1 = append (k_new, v_new given).  sl2 = softmax
@@ -154,8 +261,7 @@ __global__ __launch_bounds__(256) void k_dec_front(Geo g, Cache c, DecWs dw, con
   __shared__ __align__(16) float qs[D * GQ];          // [d][j] queries, or rotated queries
   __shared__ __align__(16) float tab[64 * 16 * GQ];   // [pair][nibble][j] residual-term table
   __shared__ float xs[D];
-  __shared__ float rb1[4], rb2[4];
-  __shared__ int ri1[4];
+  __shared__ __align__(16) E qraw[64 * D];            // queries of one request (key-residual blocks)
   __shared__ int bhr[2];
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const bool attn = flags & 1, app = (flags & 2) != 0;
@@ -171,6 +277,10 @@ __global__ __launch_bounds__(256) void k_dec_front(Geo g, Cache c, DecWs dw, con
     }
     const int k = g.k[b], kp = (k + 3) & ~3, nab = (k + 255) / 256;
     const int h = idx / nab, ch = idx % nab;
+    if constexpr (DT == 1) {
+      anchor_block_mfma<GQ>(g, c, dw, q, kin, vin, attn, app, side, b, h, ch, sl2);
+      return;
+    }
     const int a = ch * 256 + tid;
     const bool valid = a < k;
     const size_t ko = (size_t)g.prefK[b] * g.H + (size_t)h * k;
@@ -204,17 +314,7 @@ __global__ __launch_bounds__(256) void k_dec_front(Geo g, Cache c, DecWs dw, con
       float b1 = sc, b2 = -1.0f;
       int i1 = valid ? a : 0x7fffffff;
       top2_wave_dpp(b1, b2, i1);
-      if (lane == 0) {
-        rb1[wave] = b1;
-        rb2[wave] = b2;
-        ri1[wave] = i1;
-      }
-      __syncthreads();
-      if (tid == 0) {
-        for (int v = 1; v < 4; ++v) top2_merge(b1, b2, i1, rb1[v], rb2[v], ri1[v]);
-        const size_t ti = (size_t)side * g.H * g.prefAB[g.B] + (size_t)g.prefAB[b] * g.H + (size_t)h * nab + ch;
-        dw.atop[ti] = make_float4(b1, b2, __int_as_float(i1), 0.0f);
-      }
+      if (lane == 0) dw.atop[atop_index(g, side, b, h, 4 * ch + wave)] = make_float4(b1, b2, __int_as_float(i1), 0.0f);
     }
     return;
   }
@@ -228,21 +328,61 @@ __global__ __launch_bounds__(256) void k_dec_front(Geo g, Cache c, DecWs dw, con
   const int e = idx * 256 + tid;
   const bool valid = e < NKt;
   const int ec = min(e, NKt - 1);
-  int b = 0;
-  while (b < g.B - 1 && ec >= g.prefNK[b + 1]) ++b;
-  const int S = g.S[b], G = g.G, nw = (S + 63) / 64;
-  const size_t wb = (size_t)g.prefW[b] * g.H;
-  int h = g.H - 1;
-  while (h > 0 && c.pcK[wb + (size_t)h * nw] > ec) --h;  // head whose residual range holds ec
-  const int bh = b * g.H + h;
+  const int G = g.G;
+  // The queries of the block's first request, loaded beside the codes so that
+  // the rotation below does not wait for them (at most 64 query heads).
+  int bq = 0;
+  while (bq < g.B - 1 && idx * 256 >= g.prefNK[bq + 1]) ++bq;
+  const bool qpre = g.Hq <= 64;
+  constexpr int QPT = 64 * D / PER / 256;  // 16-byte chunks per thread at 64 query heads
+  const int nq4 = g.Hq * D / PER;
+  uint4 qv[QPT];
+  if (qpre) {
+    const uint4* qsrc = (const uint4*)((const E*)q + (size_t)bq * g.Hq * D);
+#pragma unroll
+    for (int u = 0; u < QPT; ++u) {  // past the end: reload the last chunk, not stored
+      const uint4 t = qsrc[min(tid + 256 * u, nq4 - 1)];
+      qv[u] = make_uint4(t.x, t.y, t.z, t.w);
+    }
+  }
+  __builtin_amdgcn_sched_barrier(0);  // issue the query loads first
   const uint4* cp = (const uint4*)(c.codesK + (size_t)ec * (D / 4));
   const uint4 c0 = cp[0], c1 = cp[1];
   float sg[4];
 #pragma unroll
   for (int qd = 0; qd < 4; ++qd) sg[qd] = qd < D / G ? c.scalesK[(size_t)ec * (D / G) + qd] : 0.0f;
+  // (request, head) of a residual index: the last head whose first residual
+  // index (the flag-word prefix of its first word) is at most the index.
+  // Each wave reads the head starts of its first residual's request one per
+  // lane (one round trip) and counts with a ballot; residuals of a later
+  // request (a wave straddling requests) scan that request's starts.
+  int bw = 0;
+  const int ew = min(idx * 256 + wave * 64, NKt - 1);
+  while (bw < g.B - 1 && ew >= g.prefNK[bw + 1]) ++bw;
+  const size_t wbw = (size_t)g.prefW[bw] * g.H;
+  const int nww = (g.S[bw] + 63) / 64;
+  int hst = 0x7fffffff;  // start of head `lane` (lanes 1 .. H-1; H <= 64 heads per ballot)
+  for (int hh = lane; hh < g.H; hh += 64)
+    if (hh == lane && hh >= 1) hst = c.pcK[wbw + (size_t)hh * nww];
+  int b = bw;
+  while (b < g.B - 1 && ec >= g.prefNK[b + 1]) ++b;
+  int hcnt = 0;
+  if (b == bw && g.H <= 64) {
+    for (int l = 1; l < g.H; ++l) hcnt += __builtin_amdgcn_readlane(hst, l) <= ec ? 1 : 0;
+  } else {
+    const int nw = (g.S[b] + 63) / 64;
+    const size_t wb = (size_t)g.prefW[b] * g.H;
+    for (int hh = 1; hh < g.H; ++hh) hcnt += c.pcK[wb + (size_t)hh * nw] <= ec ? 1 : 0;
+  }
+  const int bh = b * g.H + hcnt;
   const int lastv = min(255, NKt - 1 - idx * 256);
   if (tid == 0) bhr[0] = bh;
   if (tid == lastv) bhr[1] = bh;
+  if (qpre) {
+#pragma unroll
+    for (int u = 0; u < QPT; ++u)
+      if (tid + 256 * u < nq4) ((uint4*)qraw)[tid + 256 * u] = qv[u];
+  }
   __syncthreads();
   const int lo = bhr[0], hi = bhr[1];
   const uint32_t cw[8] = {c0.x, c0.y, c0.z, c0.w, c1.x, c1.y, c1.z, c1.w};
@@ -251,8 +391,16 @@ __global__ __launch_bounds__(256) void k_dec_front(Geo g, Cache c, DecWs dw, con
   for (int p0 = lo; p0 <= hi; ++p0) {
     const int b2 = p0 / g.H, h2 = p0 % g.H;
     for (int jj = wave; jj < GQ; jj += 4) {
-      const E* qp = (const E*)q + ((size_t)b2 * g.Hq + (size_t)h2 * GQ + jj) * D;
-      float z0 = s0v * Elem<DT>::get(qp, 2 * lane), z1 = s1v * Elem<DT>::get(qp, 2 * lane + 1);
+      float z0, z1;
+      if (qpre && b2 == bq) {
+        const E* qp = qraw + ((size_t)h2 * GQ + jj) * D;
+        z0 = s0v * Elem<DT>::get(qp, 2 * lane);
+        z1 = s1v * Elem<DT>::get(qp, 2 * lane + 1);
+      } else {
+        const E* qp = (const E*)q + ((size_t)b2 * g.Hq + (size_t)h2 * GQ + jj) * D;
+        z0 = s0v * Elem<DT>::get(qp, 2 * lane);
+        z1 = s1v * Elem<DT>::get(qp, 2 * lane + 1);
+      }
       fwht_wave_dpp(z0, z1, lane);
       qs[(2 * lane) * GQ + jj] = z0 * qscale;
       qs[(2 * lane + 1) * GQ + jj] = z1 * qscale;
@@ -335,12 +483,9 @@ __device__ void append_resolve(const Geo& g, const Cache& c, const DecWs& dw, in
     const float xn = sqrtf(ss) * (1.0f + 1e-5f);
     float b1 = -1.0f, b2 = -1.0f;
     int i1 = 0x7fffffff;
-    if (lane < nab) {
-      const float4 t =
-          dw.atop[(size_t)side * g.H * g.prefAB[g.B] + (size_t)g.prefAB[b] * g.H + (size_t)h * nab + lane];
-      b1 = t.x;
-      b2 = t.y;
-      i1 = __float_as_int(t.z);
+    for (int ci = lane; ci < 4 * nab; ci += 64) {
+      const float4 t = dw.atop[atop_index(g, side, b, h, ci)];
+      top2_merge(b1, b2, i1, t.x, t.y, __float_as_int(t.z));
     }
     top2_wave(b1, b2, i1);
     if (lane == 0) {
