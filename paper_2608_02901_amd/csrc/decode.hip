@@ -198,6 +198,13 @@ __device__ void anchor_block_mfma(const Geo& g, const Cache& c, const DecWs& dw,
   }
   float* ascp = dw.asc + (size_t)side * g.H * g.prefKp[g.B] + ab + a0 + 4 * kq;
   float4* atopp = dw.atop + atop_index(g, side, b, h, 4 * ch + wave);
+  // Anchor the inverse-norm loads here (issued before the rows, so waiting
+  // for them costs nothing the contraction would not wait for anyway);
+  // otherwise they are sunk to the screening and pay a full round trip there.
+#pragma unroll
+  for (int t = 0; t < 4; ++t)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) asm volatile("" ::"v"(ivs[t][i]));
   f32x4 acc[4];
 #pragma unroll
   for (int t = 0; t < 4; ++t) {
@@ -207,8 +214,25 @@ __device__ void anchor_block_mfma(const Geo& g, const Cache& c, const DecWs& dw,
   }
   // lane holds column col of anchors a0 + 16 t + 4 kq + i, i = 0..3; a
   // wave whose 64 anchors all exist (every wave but a head's last) stores
-  // without per-element guards.
+  // without per-element guards.  The screening math (which waits for the
+  // inverse norms) comes before every store: loads and stores share one
+  // completion counter, so a wait issued after the stores would wait for them.
   const bool full = a0 + 63 < k;
+  float b1 = -1.0f, b2 = -1.0f;
+  int i1 = 0x7fffffff;
+  float sc[4][4];
+  if (app) {
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int a = a0 + 16 * t + 4 * kq + i;
+        const bool ok = col == GQ && (full || a < k);
+        sc[t][i] = ok ? fabsf(acc[t][i]) * ivs[t][i] : -1.0f;
+        top2_merge(b1, b2, i1, sc[t][i], -1.0f, ok ? a : 0x7fffffff);
+      }
+    top2_wave_dpp(b1, b2, i1);
+  }
   if (doq && col < GQ) {
     float* skp = dw.SK + (ab + a0 + 4 * kq) * GQ + col;
     if (full) {
@@ -225,18 +249,6 @@ __device__ void anchor_block_mfma(const Geo& g, const Cache& c, const DecWs& dw,
     }
   }
   if (!app) return;
-  float b1 = -1.0f, b2 = -1.0f;
-  int i1 = 0x7fffffff;
-  float sc[4][4];
-#pragma unroll
-  for (int t = 0; t < 4; ++t)
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int a = a0 + 16 * t + 4 * kq + i;
-      const bool ok = col == GQ && (full || a < k);
-      sc[t][i] = ok ? fabsf(acc[t][i]) * ivs[t][i] : -1.0f;
-      top2_merge(b1, b2, i1, sc[t][i], -1.0f, ok ? a : 0x7fffffff);
-    }
   if (col == GQ) {
 #pragma unroll
     for (int t = 0; t < 4; ++t)
@@ -244,12 +256,13 @@ __device__ void anchor_block_mfma(const Geo& g, const Cache& c, const DecWs& dw,
       for (int i = 0; i < 4; ++i)
         if (full || a0 + 16 * t + 4 * kq + i < k) ascp[16 * t + i] = sc[t][i];
   }
-  top2_wave_dpp(b1, b2, i1);
   if (lane == 0) *atopp = make_float4(b1, b2, __int_as_float(i1), 0.0f);
 }
 
+constexpr int RK_PER_BLOCK = 128;  // stored key residuals per key-residual block
+
 // Grid: nAK key-anchor blocks, nAV value-anchor blocks (append only), then
-// ceil(sum N_K / 256) key-residual blocks (attention only).  flags: bit 0 =
+// ceil(sum N_K / 128) key-residual blocks (attention only).  flags: bit 0 =
 // attention (q given), bit 1 = append (k_new, v_new given).  sl2 = softmax
 // scale * log2(e): the stored anchor scores and key-residual terms are logits
 // in base 2.
@@ -258,8 +271,9 @@ __global__ __launch_bounds__(256) void k_dec_front(Geo g, Cache c, DecWs dw, con
                                                    const void* vin, int flags, int nAK, int nAV, float sl2) {
   using E = typename Elem<DT>::T;
   constexpr int D = AKV_D, PER = 16 / sizeof(E), NV = D / PER;
-  __shared__ __align__(16) float qs[D * GQ];          // [d][j] queries, or rotated queries
-  __shared__ __align__(16) float tab[64 * 16 * GQ];   // [pair][nibble][j] residual-term table
+  constexpr int RK_TABS = GQ <= 4 ? 2 : 1;            // key-residual tables built per pass
+  __shared__ __align__(16) float qs[RK_TABS * D * GQ];          // [head][d][j] queries, or rotated queries
+  __shared__ __align__(16) float tab[RK_TABS * 64 * 16 * GQ];   // [head][pair][nibble][j] residual-term table
   __shared__ float xs[D];
   __shared__ __align__(16) E qraw[64 * D];            // queries of one request (key-residual blocks)
   __shared__ int bhr[2];
@@ -319,20 +333,22 @@ __global__ __launch_bounds__(256) void k_dec_front(Geo g, Cache c, DecWs dw, con
     return;
   }
 
-  // ---- key-residual terms: one thread per stored key residual (global index e).
-  // q_rot . zhat = sum over coordinate pairs of a table entry indexed by the
-  // pair's 4-bit code (its two levels times the two rotated query values),
-  // scaled by the group scale.
+  // ---- key-residual terms: two threads per stored key residual (global index
+  // e), 128 residuals per block.  q_rot . zhat = sum over coordinate pairs of
+  // a table entry indexed by the pair's 4-bit code (its two levels times the
+  // two rotated query values), scaled by the group scale; each thread sums 32
+  // pairs and the partner's sum is added with a lane swap.
   idx -= nAK + nAV;
   const int NKt = g.prefNK[g.B];
-  const int e = idx * 256 + tid;
+  const int e0 = idx * RK_PER_BLOCK;
+  const int e = e0 + (tid >> 1), half = tid & 1;
   const bool valid = e < NKt;
   const int ec = min(e, NKt - 1);
   const int G = g.G;
   // The queries of the block's first request, loaded beside the codes so that
   // the rotation below does not wait for them (at most 64 query heads).
   int bq = 0;
-  while (bq < g.B - 1 && idx * 256 >= g.prefNK[bq + 1]) ++bq;
+  while (bq < g.B - 1 && e0 >= g.prefNK[bq + 1]) ++bq;
   const bool qpre = g.Hq <= 64;
   constexpr int QPT = 64 * D / PER / 256;  // 16-byte chunks per thread at 64 query heads
   const int nq4 = g.Hq * D / PER;
@@ -346,18 +362,18 @@ __global__ __launch_bounds__(256) void k_dec_front(Geo g, Cache c, DecWs dw, con
     }
   }
   __builtin_amdgcn_sched_barrier(0);  // issue the query loads first
-  const uint4* cp = (const uint4*)(c.codesK + (size_t)ec * (D / 4));
-  const uint4 c0 = cp[0], c1 = cp[1];
-  float sg[4];
+  // this thread's half of the codes (pairs 32 half .. +31) and its two scales
+  const uint4 ch4 = *(const uint4*)(c.codesK + (size_t)ec * (D / 4) + 16 * half);
+  float sg[2];
 #pragma unroll
-  for (int qd = 0; qd < 4; ++qd) sg[qd] = qd < D / G ? c.scalesK[(size_t)ec * (D / G) + qd] : 0.0f;
+  for (int u = 0; u < 2; ++u) sg[u] = c.scalesK[(size_t)ec * (D / G) + ((2 * half + u) * 32) / G];
   // (request, head) of a residual index: the last head whose first residual
   // index (the flag-word prefix of its first word) is at most the index.
   // Each wave reads the head starts of its first residual's request one per
-  // lane (one round trip) and counts with a ballot; residuals of a later
-  // request (a wave straddling requests) scan that request's starts.
+  // lane (one round trip) and counts them; residuals of a later request (a
+  // wave straddling requests) scan that request's starts.
   int bw = 0;
-  const int ew = min(idx * 256 + wave * 64, NKt - 1);
+  const int ew = min(e0 + wave * 32, NKt - 1);
   while (bw < g.B - 1 && ew >= g.prefNK[bw + 1]) ++bw;
   const size_t wbw = (size_t)g.prefW[bw] * g.H;
   const int nww = (g.S[bw] + 63) / 64;
@@ -375,7 +391,7 @@ __global__ __launch_bounds__(256) void k_dec_front(Geo g, Cache c, DecWs dw, con
     for (int hh = 1; hh < g.H; ++hh) hcnt += c.pcK[wb + (size_t)hh * nw] <= ec ? 1 : 0;
   }
   const int bh = b * g.H + hcnt;
-  const int lastv = min(255, NKt - 1 - idx * 256);
+  const int lastv = 2 * min(RK_PER_BLOCK - 1, NKt - 1 - e0);
   if (tid == 0) bhr[0] = bh;
   if (tid == lastv) bhr[1] = bh;
   if (qpre) {
@@ -385,12 +401,17 @@ __global__ __launch_bounds__(256) void k_dec_front(Geo g, Cache c, DecWs dw, con
   }
   __syncthreads();
   const int lo = bhr[0], hi = bhr[1];
-  const uint32_t cw[8] = {c0.x, c0.y, c0.z, c0.w, c1.x, c1.y, c1.z, c1.w};
+  const uint32_t cw[4] = {ch4.x, ch4.y, ch4.z, ch4.w};
   const float qscale = sl2 * (1.0f / (float)D);
   const float s0v = sign_bit(g.sgnbits, 2 * lane), s1v = sign_bit(g.sgnbits, 2 * lane + 1);
-  for (int p0 = lo; p0 <= hi; ++p0) {
-    const int b2 = p0 / g.H, h2 = p0 % g.H;
-    for (int jj = wave; jj < GQ; jj += 4) {
+  float dot[GQ];
+#pragma unroll
+  for (int jj = 0; jj < GQ; ++jj) dot[jj] = 0.0f;
+  for (int p0 = lo; p0 <= hi; p0 += RK_TABS) {  // RK_TABS heads per pass
+    for (int f = wave; f < RK_TABS * GQ; f += 4) {
+      const int p = p0 + f / GQ, jj = f % GQ;
+      if (p > hi) continue;
+      const int b2 = p / g.H, h2 = p % g.H;
       float z0, z1;
       if (qpre && b2 == bq) {
         const E* qp = qraw + ((size_t)h2 * GQ + jj) * D;
@@ -402,52 +423,55 @@ __global__ __launch_bounds__(256) void k_dec_front(Geo g, Cache c, DecWs dw, con
         z1 = s1v * Elem<DT>::get(qp, 2 * lane + 1);
       }
       fwht_wave_dpp(z0, z1, lane);
-      qs[(2 * lane) * GQ + jj] = z0 * qscale;
-      qs[(2 * lane + 1) * GQ + jj] = z1 * qscale;
+      float* qt = qs + (f / GQ) * D * GQ;
+      qt[(2 * lane) * GQ + jj] = z0 * qscale;
+      qt[(2 * lane + 1) * GQ + jj] = z1 * qscale;
     }
     __syncthreads();
-    {  // table: thread = (pair t/4, nibbles 4 (t%4) .. +3)
+    for (int t = 0; t < RK_TABS && p0 + t <= hi; ++t) {  // table: thread = (pair t/4, nibbles 4 (t%4) .. +3)
+      const float* qt = qs + t * D * GQ;
+      float* tb = tab + t * 64 * 16 * GQ;
       const int pr = tid >> 2, n0 = 4 * (tid & 3);
       float qa[GQ], qb[GQ];
-      load_g<GQ>(&qs[(2 * pr) * GQ], qa);
-      load_g<GQ>(&qs[(2 * pr + 1) * GQ], qb);
+      load_g<GQ>(&qt[(2 * pr) * GQ], qa);
+      load_g<GQ>(&qt[(2 * pr + 1) * GQ], qb);
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
         const int nib = n0 + u;
         const float la = level(nib & 3), lb = level(nib >> 2);
-        float t[GQ];
+        float tv[GQ];
 #pragma unroll
-        for (int jj = 0; jj < GQ; ++jj) t[jj] = fmaf(lb, qb[jj], la * qa[jj]);
-        store_g<GQ>(&tab[(pr * 16 + nib) * GQ], t);
+        for (int jj = 0; jj < GQ; ++jj) tv[jj] = fmaf(lb, qb[jj], la * qa[jj]);
+        store_g<GQ>(&tb[(pr * 16 + nib) * GQ], tv);
       }
     }
     __syncthreads();
-    if (valid && bh == p0) {
-      float dot[GQ];
+    if (bh >= p0 && bh < p0 + RK_TABS) {
+      const float* tb = tab + (bh - p0) * 64 * 16 * GQ;
 #pragma unroll
-      for (int jj = 0; jj < GQ; ++jj) dot[jj] = 0.0f;
-#pragma unroll
-      for (int qd = 0; qd < 4; ++qd) {  // 32-coordinate quarters lie inside one group (G >= 32)
+      for (int qh = 0; qh < 2; ++qh) {  // 32-coordinate quarters lie inside one group (G >= 32)
+        const int qd = 2 * half + qh;
         float part[GQ];
 #pragma unroll
         for (int jj = 0; jj < GQ; ++jj) part[jj] = 0.0f;
 #pragma unroll
         for (int n = 0; n < 16; ++n) {
-          const int pr = qd * 16 + n;
-          const int nib = (cw[pr >> 3] >> (4 * (pr & 7))) & 15;
-          float t[GQ];
-          load_g<GQ>(&tab[(pr * 16 + nib) * GQ], t);
+          const int pr = qd * 16 + n, lp = qh * 16 + n;  // lp: pair within this thread's half
+          const int nib = (cw[lp >> 3] >> (4 * (lp & 7))) & 15;
+          float tv[GQ];
+          load_g<GQ>(&tb[(pr * 16 + nib) * GQ], tv);
 #pragma unroll
-          for (int jj = 0; jj < GQ; ++jj) part[jj] += t[jj];
+          for (int jj = 0; jj < GQ; ++jj) part[jj] += tv[jj];
         }
-        const float sq = sg[(qd * 32) / G];
 #pragma unroll
-        for (int jj = 0; jj < GQ; ++jj) dot[jj] = fmaf(sq, part[jj], dot[jj]);
+        for (int jj = 0; jj < GQ; ++jj) dot[jj] = fmaf(sg[qh], part[jj], dot[jj]);
       }
-      store_g<GQ>(dw.RK + (size_t)e * GQ, dot);
     }
     __syncthreads();
   }
+#pragma unroll
+  for (int jj = 0; jj < GQ; ++jj) dot[jj] += lane_xor<1>(dot[jj]);
+  if (valid && half == 0) store_g<GQ>(dw.RK + (size_t)e * GQ, dot);
 }
 
 // ------------------------------------------------------------------ append resolution
@@ -1215,7 +1239,7 @@ static void launch_steps(const Geo& g, const Cache& c, const DecWs& dw, const vo
                          hipStream_t st) {
   const int nAK = g.H * g.prefAB[g.B];
   const int nAV = app ? nAK : 0;
-  const int nR = attn ? (g.prefNK[g.B] + 255) / 256 : 0;
+  const int nR = attn ? (g.prefNK[g.B] + RK_PER_BLOCK - 1) / RK_PER_BLOCK : 0;
   const int flags = (attn ? 1 : 0) | (app ? 2 : 0);
   const float sl2 = scale * 1.4426950408889634f;
   launch("k_dec_front", k_dec_front<DT, GQ>, dim3(nAK + nAV + nR), dim3(256), 0, st, g, c, dw, q, kn, vn, flags, nAK, nAV, sl2);
