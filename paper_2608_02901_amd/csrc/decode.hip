@@ -818,27 +818,73 @@ __global__ __launch_bounds__(256) void k_dec_stream(Geo g, Cache c, DecWs dw, in
     for (int i = lane; i < SW_ACH * GQ; i += 64) (&W.wacc[0][0])[i] = 0.0f;
     if (lane < 16) W.lvl[lane] = make_float2(level(lane & 3), level(lane >> 2));
 
-    // ---- round 1: records and flag words of this wave's slots.
+    // ---- round 1: records and flag words of this wave's slots.  Every
+    // lane reads raw words (a lane past the split end re-reads the wave's
+    // first group and discards it), all loads are issued before any is
+    // unpacked.
     const int i0 = ws0 + lane * R;
     const bool any = i0 < ws1;
+    const int i0c = any ? i0 : ws0;
     uint16_t ik[R], iv[R];
     float gk[R], gv[R];
-    unsigned long long wk = 0, wv = 0;
-    int pck = 0, pcv = 0;
-    if (any) {
-      load_u16<R>(c.idxK + so + i0, ik);
-      load_u16<R>(c.idxV + so + i0, iv);
-      load_coef<DT, R>(c.gK, so + i0, gk);
-      load_coef<DT, R>(c.gV, so + i0, gv);
-      wk = c.maskK[wo + (i0 >> 6)];
-      wv = c.maskV[wo + (i0 >> 6)];
-      pck = c.pcK[wo + (i0 >> 6)];
-      pcv = c.pcV[wo + (i0 >> 6)];
-    } else {
+    unsigned long long wk, wv;
+    int pck, pcv;
+    {
+      constexpr int NU = R / 4;                       // uint2 words per index array
+      constexpr int NG = DT == 1 ? R / 4 : R / 2;     // uint2 words per coefficient array
+      uint2 rik[NU], riv[NU], rgk[NG], rgv[NG];
 #pragma unroll
-      for (int r = 0; r < R; ++r) {
-        ik[r] = iv[r] = 0;
-        gk[r] = gv[r] = 0.0f;
+      for (int u = 0; u < NU; ++u) {
+        rik[u] = ((const uint2*)(c.idxK + so + i0c))[u];
+        riv[u] = ((const uint2*)(c.idxV + so + i0c))[u];
+      }
+#pragma unroll
+      for (int u = 0; u < NG; ++u) {
+        rgk[u] = ((const uint2*)((const E*)c.gK + so + i0c))[u];
+        rgv[u] = ((const uint2*)((const E*)c.gV + so + i0c))[u];
+      }
+      wk = c.maskK[wo + (i0c >> 6)];
+      wv = c.maskV[wo + (i0c >> 6)];
+      pck = c.pcK[wo + (i0c >> 6)];
+      pcv = c.pcV[wo + (i0c >> 6)];
+      __builtin_amdgcn_sched_barrier(0);  // all loads above are issued before the unpacking
+#pragma unroll
+      for (int u = 0; u < NU; ++u) {
+        ik[4 * u] = (uint16_t)(rik[u].x & 0xffff);
+        ik[4 * u + 1] = (uint16_t)(rik[u].x >> 16);
+        ik[4 * u + 2] = (uint16_t)(rik[u].y & 0xffff);
+        ik[4 * u + 3] = (uint16_t)(rik[u].y >> 16);
+        iv[4 * u] = (uint16_t)(riv[u].x & 0xffff);
+        iv[4 * u + 1] = (uint16_t)(riv[u].x >> 16);
+        iv[4 * u + 2] = (uint16_t)(riv[u].y & 0xffff);
+        iv[4 * u + 3] = (uint16_t)(riv[u].y >> 16);
+      }
+#pragma unroll
+      for (int u = 0; u < NG; ++u) {
+        if constexpr (DT == 1) {
+          gk[4 * u] = bf2f((uint16_t)(rgk[u].x & 0xffff));
+          gk[4 * u + 1] = bf2f((uint16_t)(rgk[u].x >> 16));
+          gk[4 * u + 2] = bf2f((uint16_t)(rgk[u].y & 0xffff));
+          gk[4 * u + 3] = bf2f((uint16_t)(rgk[u].y >> 16));
+          gv[4 * u] = bf2f((uint16_t)(rgv[u].x & 0xffff));
+          gv[4 * u + 1] = bf2f((uint16_t)(rgv[u].x >> 16));
+          gv[4 * u + 2] = bf2f((uint16_t)(rgv[u].y & 0xffff));
+          gv[4 * u + 3] = bf2f((uint16_t)(rgv[u].y >> 16));
+        } else {
+          gk[2 * u] = __uint_as_float(rgk[u].x);
+          gk[2 * u + 1] = __uint_as_float(rgk[u].y);
+          gv[2 * u] = __uint_as_float(rgv[u].x);
+          gv[2 * u + 1] = __uint_as_float(rgv[u].y);
+        }
+      }
+      if (!any) {
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+          ik[r] = iv[r] = 0;
+          gk[r] = gv[r] = 0.0f;
+        }
+        wk = wv = 0;
+        pck = pcv = 0;
       }
     }
     const int nval = max(0, min(R, ws1 - i0));  // valid slots of this lane (a prefix)
