@@ -199,10 +199,15 @@ __device__ inline int crow(int r, int lane) { return (r >> 2) * 8 + (lane >> 5) 
 // ------------------------------------------------------------------ canonical fp64 dot
 // Products of fp32 / bf16 values are exact in fp64; the sum runs j = 0..D-1
 // with one rounding per addition and no fused multiply-add.
+// The length is the head dimension AKV_D (the argument must equal it); the
+// unrolled loop lets the row loads be issued ahead of the addition chain
+// instead of one round trip per 16-byte chunk.
 template <int DT>
-__device__ inline double dot64_seq(const typename Elem<DT>::T* x, const typename Elem<DT>::T* y, int D) {
+__device__ inline double dot64_seq(const typename Elem<DT>::T* x, const typename Elem<DT>::T* y, int) {
+  constexpr int D = AKV_D;
   double s = 0.0;
   if constexpr (DT == 1) {
+#pragma unroll
     for (int j = 0; j < D; j += 8) {
       uint4 xv = *(const uint4*)(x + j);
       uint4 yv = *(const uint4*)(y + j);
@@ -212,6 +217,7 @@ __device__ inline double dot64_seq(const typename Elem<DT>::T* x, const typename
       for (int i = 0; i < 8; ++i) s = s + (double)bf2f(xs[i]) * (double)bf2f(ys[i]);
     }
   } else {
+#pragma unroll
     for (int j = 0; j < D; j += 4) {
       float4 xv = *(const float4*)(x + j);
       float4 yv = *(const float4*)(y + j);

@@ -43,7 +43,8 @@ __global__ __launch_bounds__(256) void k_epilogue(Geo g, Ws w, Cache c, const vo
   const size_t ko = (size_t)g.prefK[b] * g.H + (size_t)h * k;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
 
-  for (int ch = threadIdx.x; ch < 32 * (D / PER); ch += 256) {
+#pragma unroll
+  for (int ch = threadIdx.x; ch < 32 * (AKV_D / PER); ch += 256) {
     int r = ch / (D / PER), col = (ch % (D / PER)) * PER;
     uint4 kv = make_uint4(0, 0, 0, 0), vv = make_uint4(0, 0, 0, 0);
     if (t0 + r < S) {
@@ -85,7 +86,8 @@ __global__ __launch_bounds__(256) void k_epilogue(Geo g, Ws w, Cache c, const vo
         if (side == 0) { gK_s[tl] = gb; aK_s[tl] = a; cand_s[tl] = 1; }
         if (side == 1) {
           float s = 0.0f;
-          for (int j0 = 0; j0 < D; j0 += PER) {
+#pragma unroll
+          for (int j0 = 0; j0 < AKV_D; j0 += PER) {
             const uint4 av = *(const uint4*)(arow + j0);
             const uint4 xv = *(const uint4*)(xrow + j0);
             const E* ea = (const E*)&av;
