@@ -43,6 +43,26 @@ __global__ __launch_bounds__(256) void k_epilogue(Geo g, Ws w, Cache c, const vo
   const size_t ko = (size_t)g.prefK[b] * g.H + (size_t)h * k;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
 
+  // Threads 0..63 = (token, side): the anchor rank and the assigned anchor
+  // are read first, and the anchor row right after them, so that the
+  // coefficient below waits for no memory (the rows of K and V load meanwhile).
+  int rk0 = -1, ap0 = 0;
+  uint4 arv[AKV_D / PER];
+  double nrm0 = 0.0;
+  if (threadIdx.x < 64) {
+    const int side = threadIdx.x >> 5, t = min(t0 + (threadIdx.x & 31), S - 1);
+    rk0 = w.rank[po + t];
+    ap0 = w.apos[side * TS + po + t];
+    const int a = (ap0 < 0 || ap0 >= k) ? 0 : ap0;
+    const E* arow = (const E*)(side ? c.ancV : c.ancK) + (ko + a) * D;
+#pragma unroll
+    for (int i = 0; i < AKV_D / PER; ++i) {
+      const uint4 v = *(const uint4*)(arow + i * PER);
+      arv[i] = make_uint4(v.x, v.y, v.z, v.w);
+    }
+    nrm0 = (side ? c.nrmV : c.nrmK)[ko + a];
+  }
+
 #pragma unroll
   for (int ch = threadIdx.x; ch < 32 * (AKV_D / PER); ch += 256) {
     int r = ch / (D / PER), col = (ch % (D / PER)) * PER;
@@ -64,7 +84,7 @@ __global__ __launch_bounds__(256) void k_epilogue(Geo g, Ws w, Cache c, const vo
   if (threadIdx.x < 64) {
     const int tl = threadIdx.x & 31, side = threadIdx.x >> 5, t = t0 + tl;
     if (t < S) {
-      const int rk = w.rank[po + t];
+      const int rk = rk0;
       const size_t o = side * TS + po + t;
       const E* xrow = &(side ? VT : KT)[tl * LD];
       if (rk >= 0) {
@@ -72,13 +92,13 @@ __global__ __launch_bounds__(256) void k_epilogue(Geo g, Ws w, Cache c, const vo
         if (side == 0) { gK_s[tl] = 1.0f; aK_s[tl] = rk; cand_s[tl] = 0; }
         if (side == 1) rv2_s[tl] = 0.0f;
       } else {
-        int a = w.apos[o];
+        int a = ap0;
         if (a < 0 || a >= k) {
           atomicOr(&c.header[2], 4u);
           a = 0;
         }
-        const E* arow = (const E*)(side ? c.ancV : c.ancK) + (ko + a) * D;
-        const double n = (side ? c.nrmV : c.nrmK)[ko + a];
+        const E* arow = (const E*)arv;  // the prefetched row of anchor a
+        const double n = nrm0;
         const double d = dot64_seq<DT>(xrow, arow, D);
         const double g64 = n > 0.0 ? d / n : 0.0;
         const float gb = Elem<DT>::round_coef((float)g64);
