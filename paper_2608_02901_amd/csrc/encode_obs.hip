@@ -18,36 +18,21 @@ namespace akv {
 
 template <int DT> struct TileLD { static constexpr int v = AKV_D + (DT ? 8 : 4); };
 
-// Loads 32 token rows [t0, t0+32) of X ([S][D], row-major) into LDS with row
-// stride LD; rows at or past S are zero.
+// Orientation of the observation logits: the MFMA takes the key tile as its
+// row operand and the query fragments as its column operand, so lane l holds
+// the logits of observation row w = l % 32 (of its row block) against the 16
+// tokens crow(e, l), e = 0..15, of the 32-token tile.  A lane's row max, 1/Z
+// and causal limit are then single registers, and its 16 probabilities serve
+// directly as the row operand of the value contraction, whose k index kappa
+// runs over the tokens in the order the accumulator entries are taken:
+// kappa = KS s + KL (l / 32) + j holds entry e = KL s + j, i.e. token
+// kap_tok(kappa); the value tile is stored in that order.
 template <int DT>
-__device__ inline void load_rows(typename Elem<DT>::T* lds, const typename Elem<DT>::T* X, int t0, int S, int D,
-                                 int LD) {
-  using E = typename Elem<DT>::T;
-  constexpr int PER = 16 / sizeof(E);  // elements per 16-byte chunk
-  const int cpr = D / PER;             // chunks per row
-  for (int c = threadIdx.x; c < 32 * cpr; c += blockDim.x) {
-    int r = c / cpr, col = (c % cpr) * PER;
-    uint4 v = make_uint4(0, 0, 0, 0);
-    if (t0 + r < S) v = *(const uint4*)(X + (size_t)(t0 + r) * D + col);
-    *(uint4*)(lds + r * LD + col) = v;
-  }
-}
-
-// Loads 32 token rows transposed: lds[d * LDT + r] = X[t0 + r][d].
-template <int DT>
-__device__ inline void load_rows_t(typename Elem<DT>::T* lds, const typename Elem<DT>::T* X, int t0, int S, int D,
-                                   int LDT) {
-  using E = typename Elem<DT>::T;
-  constexpr int PER = 16 / sizeof(E);
-  const int cpr = D / PER;
-  for (int c = threadIdx.x; c < 32 * cpr; c += blockDim.x) {
-    int r = c / cpr, col = (c % cpr) * PER;
-    uint4 v = make_uint4(0, 0, 0, 0);
-    if (t0 + r < S) v = *(const uint4*)(X + (size_t)(t0 + r) * D + col);
-    const E* e = (const E*)&v;
-#pragma unroll
-    for (int i = 0; i < PER; ++i) lds[(col + i) * LDT + r] = e[i];
+__device__ inline int tok_kap(int t) {  // token -> kappa (inverse of the entry order)
+  if constexpr (DT == 1) {
+    return (t & ~12) | ((t >> 2) & 1) << 3 | ((t >> 3) & 1) << 2;  // bits 2 and 3 swapped
+  } else {
+    return (t & ~7) | (t & 3) << 1 | ((t >> 2) & 1);
   }
 }
 
@@ -73,26 +58,16 @@ struct RowTile {
       *(uint4*)(lds + r * LD + col) = v[i];
     }
   }
-  // Transposed: lds[d * LDT + r] = X[t0 + r][d].
-  __device__ void store_t(E* lds, int LDT) const {
-#pragma unroll
-    for (int i = 0; i < RPT; ++i) {
-      const int c = threadIdx.x + 256 * i, r = c / CPR, col = (c % CPR) * PER;
-      const E* e = (const E*)&v[i];
-#pragma unroll
-      for (int j = 0; j < PER; ++j) lds[(col + j) * LDT + r] = e[j];
-    }
-  }
 };
 
-// Position of token r in row d of the transposed value tile: groups of 8
-// tokens stay contiguous (one MFMA operand load) and are permuted by d, which
-// spreads the stores of one wave over the LDS banks.
-__device__ inline int vt_pos(int d, int r) { return (((r >> 3) ^ (d >> 3)) & 3) * 8 + (r & 7); }
+// Position of contraction index kappa in row d of the transposed value tile:
+// groups of 8 stay contiguous (one MFMA operand load) and are permuted by d,
+// which spreads the stores of one wave over the LDS banks.
+__device__ inline int vt_pos(int d, int kap) { return (((kap >> 3) ^ (d >> 3)) & 3) * 8 + (kap & 7); }
 
-// Value tile for the transposed LDS layout lds[d * LDT + vt_pos(d, r)] = X[t0 + r][d]:
-// thread c takes rows 2p, 2p+1 (p = c / CPR) of one 16-byte column chunk, so
-// for bf16 the two tokens of a column are stored as one 32-bit word.
+// Value tile, transposed: lds[d * LDT + vt_pos(d, tok_kap(r))] = X[t0 + r][d].
+// Thread c takes rows 2p, 2p+1 (p = c / CPR) of one 16-byte column chunk; for
+// bf16 the two tokens have adjacent kappa and are stored as one 32-bit word.
 template <int DT>
 struct PairTile {
   using E = typename Elem<DT>::T;
@@ -113,27 +88,21 @@ struct PairTile {
       const int c = threadIdx.x + 256 * i, p = c / CPR, col = (c % CPR) * PER;
       const E* e0 = (const E*)&v0[i];
       const E* e1 = (const E*)&v1[i];
+      const int k0 = tok_kap<DT>(2 * p), k1 = tok_kap<DT>(2 * p + 1);
       if constexpr (sizeof(E) == 2) {
 #pragma unroll
         for (int j = 0; j < PER; ++j)
-          *(uint32_t*)(lds + (col + j) * LDT + vt_pos(col + j, 2 * p)) = (uint32_t)e0[j] | ((uint32_t)e1[j] << 16);
+          *(uint32_t*)(lds + (col + j) * LDT + vt_pos(col + j, k0)) = (uint32_t)e0[j] | ((uint32_t)e1[j] << 16);
       } else {
 #pragma unroll
-        for (int j = 0; j < PER; ++j)
-          *(float2*)(lds + (col + j) * LDT + vt_pos(col + j, 2 * p)) = make_float2(e0[j], e1[j]);
+        for (int j = 0; j < PER; ++j) {
+          lds[(col + j) * LDT + vt_pos(col + j, k0)] = e0[j];
+          lds[(col + j) * LDT + vt_pos(col + j, k1)] = e1[j];
+        }
       }
     }
   }
 };
-
-template <int DT>
-__device__ inline typename MF<DT>::frag zero_frag() {
-  if constexpr (DT == 1) {
-    return __builtin_bit_cast(bf16x8, make_uint4(0, 0, 0, 0));
-  } else {
-    return 0.0f;
-  }
-}
 
 // Query row w of KV head h (rows w = jj*W + i are contiguous in [Hq][W][D]).
 template <int DT>
@@ -141,11 +110,40 @@ __device__ inline const typename Elem<DT>::T* qrows(const Geo& g, const void* Qi
   return (const typename Elem<DT>::T*)Qin + ((size_t)b * g.Hq + (size_t)h * g.g) * g.W * g.D;
 }
 
-__device__ inline bool obs_visible(int t, int S, int P, int wr, int m, int W) {
-  return t < S && wr < m && (t < P || t <= P + (wr % W));
-}
+// Last position observation row wr attends to (the rows are the queries of
+// positions P .. P+W-1, causal inside the window); -1 for padding rows.
+__device__ inline int obs_limit(int wr, int m, int P, int W) { return wr < m ? P + wr % W : -1; }
 
 constexpr float NEG = -1e30f;
+
+template <int CTRL>
+__device__ inline float dpp_mov(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, 0xF, 0xF, false));
+}
+
+// Sum of v[e] over the 16 lanes of each DPP row: four exchanges (row mirror,
+// half-row mirror, quad reversal, quad swap) in which a lane keeps half of its
+// entries and adds the partner's copy of them; lane l ends with the row sum of
+// entry l & 15.
+__device__ inline float row_reduce_scatter16(const float (&v)[16], int lane) {
+  float a[8], b[4], c[2];
+  const bool s3 = lane & 8, s2 = lane & 4, s1 = lane & 2, s0 = lane & 1;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) a[i] = (s3 ? v[8 + i] : v[i]) + dpp_mov<0x140>(s3 ? v[i] : v[8 + i]);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) b[i] = (s2 ? a[4 + i] : a[i]) + dpp_mov<0x141>(s2 ? a[i] : a[4 + i]);
+#pragma unroll
+  for (int i = 0; i < 2; ++i) c[i] = (s1 ? b[2 + i] : b[i]) + dpp_mov<0x1B>(s1 ? b[i] : b[2 + i]);
+  return (s0 ? c[1] : c[0]) + dpp_mov<0xB1>(s0 ? c[0] : c[1]);
+}
+
+// Two fp32 values rounded to nearest-even bf16, packed low | high << 16.
+__device__ inline uint32_t pk_bf16(float x0, float x1) {
+  typedef __attribute__((ext_vector_type(2))) float f32x2;
+  typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2;
+  const f32x2 v = {x0, x1};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
+}
 
 // R = row blocks of 32 observation rows per wave (4 waves cover 128 R rows).
 template <int DT, int R>
@@ -164,21 +162,22 @@ __global__ __launch_bounds__(256) void k_obs_stats(Geo g, Ws w, const void* Kin,
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int nrb = (m + 31) / 32;
   const float isd = 1.0f / sqrtf((float)D);
-  // Running row max (fp32 logits) and sum of exp in fp64; a change of the
-  // max rescales the sum by an fp64 exp, so the sum keeps ~1e-9 relative
-  // accuracy (the anchor selection re-scores near-ties against it).
-  float mx[R][16];
-  double sm[R][16];
-#pragma unroll
-  for (int r = 0; r < R; ++r)
-#pragma unroll
-    for (int e = 0; e < 16; ++e) { mx[r][e] = NEG; sm[r][e] = 0.0; }
-  // Query fragments of the wave's row blocks stay in registers.
+  // Running max (fp32 logits) and sum of exp in fp64 of the lane's row over
+  // its tokens; the max moves at most once per tile and then rescales the sum
+  // by an fp64 exp, so the sum keeps ~1e-9 relative accuracy (the anchor
+  // selection re-scores near-ties against it).
+  float mx[R];
+  double sm[R];
+  int lim[R];
   constexpr int NKS = AKV_D / M::KS;
   typename M::frag qf[R][NKS];
 #pragma unroll
   for (int r = 0; r < R; ++r) {
-    const int arow = min((wave + 4 * r) * 32 + (lane & 31), m - 1);
+    mx[r] = NEG;
+    sm[r] = 0.0;
+    const int wr = (wave + 4 * r) * 32 + (lane & 31);
+    lim[r] = obs_limit(wr, m, P, g.W);
+    const int arow = min(wr, m - 1);
 #pragma unroll
     for (int s = 0; s < NKS; ++s) qf[r][s] = M::load(Q + (size_t)arow * D, kofs(M::KS, s, lane));
   }
@@ -186,7 +185,6 @@ __global__ __launch_bounds__(256) void k_obs_stats(Geo g, Ws w, const void* Kin,
   RowTile<DT> kt;
   kt.load(X, tb, S);
   for (int t0 = tb; t0 < te; t0 += 32) {
-    __syncthreads();
     kt.store(KT, LD);
     __syncthreads();
     if (t0 + 32 < te) kt.load(X, t0 + 32, S);
@@ -197,46 +195,45 @@ __global__ __launch_bounds__(256) void k_obs_stats(Geo g, Ws w, const void* Kin,
       f32x16 acc = {};
 #pragma unroll
       for (int s = 0; s < NKS; ++s) {
-        auto bb = M::load_lds(&KT[(lane & 31) * LD], kofs(M::KS, s, lane));
-        acc = M::mma(qf[r][s], bb, acc);
+        auto kb = M::load_lds(&KT[(lane & 31) * LD], kofs(M::KS, s, lane));
+        acc = M::mma(kb, qf[r][s], acc);
       }
-      const int t = t0 + (lane & 31);
+      float l[16];
+      float tm = NEG;
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
-        const int wr = rb * 32 + crow(e, lane);
-        if (obs_visible(t, S, P, wr, m, g.W)) {
-          const float l = acc[e] * isd;
-          if (l > mx[r][e]) {
-            sm[r][e] *= exp((double)mx[r][e] - (double)l);
-            mx[r][e] = l;
-          }
-          sm[r][e] += (double)__expf(l - mx[r][e]);
-        }
+        l[e] = t0 + crow(e, lane) <= lim[r] ? acc[e] * isd : NEG;
+        tm = fmaxf(tm, l[e]);
       }
+      if (tm > mx[r]) {
+        sm[r] *= exp((double)mx[r] - (double)tm);
+        mx[r] = tm;
+      }
+      double p[16];
+#pragma unroll
+      for (int e = 0; e < 16; ++e) p[e] = l[e] > NEG ? (double)__expf(l[e] - mx[r]) : 0.0;
+#pragma unroll
+      for (int o = 8; o > 0; o >>= 1)
+#pragma unroll
+        for (int e = 0; e < o; ++e) p[e] += p[e + o];
+      sm[r] += p[0];
     }
+    __syncthreads();
   }
-  // Merge the 32 lanes that share each row.
+  // Merge the two lanes (l, l + 32) that share each row.
 #pragma unroll
   for (int r = 0; r < R; ++r) {
     const int rb = wave + 4 * r;
     if (rb >= nrb) break;
-#pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      float a = mx[r][e];
-      double s = sm[r][e];
-      for (int o = 1; o < 32; o <<= 1) {
-        const float oa = __shfl_xor(a, o, 64);
-        const double os = __shfl_xor(s, o, 64);
-        const float nm = fmaxf(a, oa);
-        s = (a == nm ? s : s * exp((double)a - (double)nm)) + (oa == nm ? os : os * exp((double)oa - (double)nm));
-        a = nm;
-      }
-      const int wr = rb * 32 + crow(e, lane);
-      if ((lane & 31) == 0 && wr < m) {
-        size_t o = ((size_t)(g.prefC[b] * g.H + h * nch + ch)) * m + wr;
-        w.opmax[o] = a;
-        w.opsum[o] = s;
-      }
+    const float a = mx[r], oa = __shfl_xor(a, 32, 64);
+    const double s = sm[r], os = __shfl_xor(s, 32, 64);
+    const float nm = fmaxf(a, oa);
+    const double z = (a == nm ? s : s * exp((double)a - (double)nm)) + (oa == nm ? os : os * exp((double)oa - (double)nm));
+    const int wr = rb * 32 + lane;
+    if (lane < 32 && wr < m) {
+      size_t o = ((size_t)(g.prefC[b] * g.H + h * nch + ch)) * m + wr;
+      w.opmax[o] = nm;
+      w.opsum[o] = z;
     }
   }
 }
@@ -265,12 +262,10 @@ __global__ __launch_bounds__(256) void k_obs_pass(Geo g, Ws w, const void* Kin, 
   using E = typename Elem<DT>::T;
   using M = MF<DT>;
   constexpr int LD = TileLD<DT>::v;
-  constexpr int LDT = 32 + (DT ? 8 : 4);  // transposed value tile / alpha tile row stride (16-byte aligned rows)
+  constexpr int LDT = 32 + (DT ? 8 : 4);  // transposed value tile row stride (16-byte aligned rows)
   __shared__ __align__(16) E KT[32 * LD];
   __shared__ __align__(16) E VT[AKV_D * LDT];
-  __shared__ __align__(16) E AH[4][R][32 * LDT];  // alpha (hi part for bf16)
-  __shared__ __align__(16) E AL[DT ? 4 : 1][R][DT ? 32 * LDT : 1];  // alpha lo part (bf16 only)
-  __shared__ float scb[32];
+  __shared__ float scw[4][32];
   int idx = blockIdx.x;
   const int b = locate(g, OBS_CHUNK, 1, idx);
   const int S = g.S[b], P = S - g.W, D = g.D, m = g.m;
@@ -290,13 +285,20 @@ __global__ __launch_bounds__(256) void k_obs_pass(Geo g, Ws w, const void* Kin, 
   for (int r = 0; r < R; ++r)
 #pragma unroll
     for (int db = 0; db < 4; ++db) yacc[r][db] = f32x16{};
-  // Query fragments of the wave's row blocks stay in registers; the next
-  // token tile's keys and values are loaded while the current one is used.
+  // The lane's row of each row block: query fragments, row max, 1/Z and
+  // causal limit stay in registers; the next token tile's keys and values are
+  // loaded while the current one is used.
   constexpr int NKS = AKV_D / M::KS;
   typename M::frag qf[R][NKS];
+  float rmax[R], riz[R];
+  int lim[R];
 #pragma unroll
   for (int r = 0; r < R; ++r) {
-    const int arow = min((wave + 4 * r) * 32 + (lane & 31), m - 1);
+    const int wr = (wave + 4 * r) * 32 + (lane & 31);
+    const int arow = min(wr, m - 1);
+    lim[r] = obs_limit(wr, m, P, g.W);
+    rmax[r] = oM[arow];
+    riz[r] = oiZ[arow];
 #pragma unroll
     for (int s = 0; s < NKS; ++s) qf[r][s] = M::load(Q + (size_t)arow * D, kofs(M::KS, s, lane));
   }
@@ -307,15 +309,16 @@ __global__ __launch_bounds__(256) void k_obs_pass(Geo g, Ws w, const void* Kin, 
   kt.load(X, tb, S);
   vt.load(Vx, tb, S);
   for (int t0 = tb; t0 < te; t0 += 32) {
-    __syncthreads();
     kt.store(KT, LD);
     vt.store_t(VT, LDT);
-    if (threadIdx.x < 32) scb[threadIdx.x] = 0.0f;
     __syncthreads();
     if (t0 + 32 < te) {
       kt.load(X, t0 + 32, S);
       vt.load(Vx, t0 + 32, S);
     }
+    float cs[16];
+#pragma unroll
+    for (int e = 0; e < 16; ++e) cs[e] = 0.0f;
 #pragma unroll
     for (int r = 0; r < R; ++r) {
       const int rb = wave + 4 * r;
@@ -323,48 +326,54 @@ __global__ __launch_bounds__(256) void k_obs_pass(Geo g, Ws w, const void* Kin, 
       f32x16 acc = {};
 #pragma unroll
       for (int s = 0; s < NKS; ++s) {
-        auto bb = M::load_lds(&KT[(lane & 31) * LD], kofs(M::KS, s, lane));
-        acc = M::mma(qf[r][s], bb, acc);
+        auto kb = M::load_lds(&KT[(lane & 31) * LD], kofs(M::KS, s, lane));
+        acc = M::mma(kb, qf[r][s], acc);
       }
-      const int tl = lane & 31, t = t0 + tl;
-      float col = 0.0f;
+      // alpha of the lane's row and tokens t0 + crow(e, lane).
+      float al[16];
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
-        const int wl = crow(e, lane), wr = rb * 32 + wl;
-        float al = 0.0f;
-        if (obs_visible(t, S, P, wr, m, g.W)) al = __expf(acc[e] * isd - oM[wr]) * oiZ[wr];
-        col += al;
-        if constexpr (DT == 1) {
-          uint16_t hi = f2bf(al);
-          AH[wave][r][wl * LDT + tl] = hi;
-          AL[wave][r][wl * LDT + tl] = f2bf(al - bf2f(hi));
-        } else {
-          AH[wave][r][wl * LDT + tl] = al;
-        }
+        const float a = __expf(acc[e] * isd - rmax[r]) * riz[r];
+        al[e] = t0 + crow(e, lane) <= lim[r] ? a : 0.0f;
+        cs[e] += al[e];
       }
-      col += __shfl_xor(col, 32, 64);
-      if (lane < 32) atomicAdd(&scb[lane], col);
-      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-      __builtin_amdgcn_wave_barrier();
-      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-      // y_w += alpha[w][t] V[t][d]: A = alpha (rows w, k = tokens), B = V^T tile.
+      // y_w += sum_t alpha[w][t] V[t][d]: row operand = alpha (entries KL s ..
+      // KL s + KL - 1 for step s), column operand = the value tile in kappa order.
+#pragma unroll
       for (int s = 0; s < 32 / M::KS; ++s) {
+        typename M::frag ah, alo;
+        if constexpr (DT == 1) {
+          uint32_t hw[4], lw[4];
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const float x0 = al[8 * s + 2 * j], x1 = al[8 * s + 2 * j + 1];
+            hw[j] = pk_bf16(x0, x1);
+            lw[j] = pk_bf16(x0 - __builtin_bit_cast(float, hw[j] << 16),
+                            x1 - __builtin_bit_cast(float, hw[j] & 0xFFFF0000u));
+          }
+          ah = __builtin_bit_cast(bf16x8, make_uint4(hw[0], hw[1], hw[2], hw[3]));
+          alo = __builtin_bit_cast(bf16x8, make_uint4(lw[0], lw[1], lw[2], lw[3]));
+        } else {
+          ah = al[s];
+        }
         const int k0 = kofs(M::KS, s, lane);
-        auto ah = M::load_lds(&AH[wave][r][(lane & 31) * LDT], k0);
 #pragma unroll
         for (int db = 0; db < 4; ++db) {
           const int d = db * 32 + (lane & 31);
           auto vb = M::load_lds(&VT[d * LDT + vt_pos(d, k0)], 0);
           yacc[r][db] = M::mma(ah, vb, yacc[r][db]);
-          if constexpr (DT == 1) {
-            auto alo = M::load_lds(&AL[wave][r][(lane & 31) * LDT], k0);
-            yacc[r][db] = M::mma(alo, vb, yacc[r][db]);
-          }
+          if constexpr (DT == 1) yacc[r][db] = M::mma(alo, vb, yacc[r][db]);
         }
       }
     }
+    // Column sums over the wave's rows: the 16 lanes of a DPP row, then the
+    // two rows of each half; lanes 0-15 and 32-47 hold tokens crow(l & 15, l).
+    float csum = row_reduce_scatter16(cs, lane);
+    csum += lane_xor<16>(csum);
+    if ((lane & 16) == 0) scw[wave][crow(lane & 15, lane)] = csum;
     __syncthreads();
-    if (threadIdx.x < 32 && t0 + threadIdx.x < S) sc[t0 + threadIdx.x] = scb[threadIdx.x] / (float)m;
+    if (threadIdx.x < 32 && t0 + threadIdx.x < S)
+      sc[t0 + threadIdx.x] = (scw[0][threadIdx.x] + scw[1][threadIdx.x] + scw[2][threadIdx.x] + scw[3][threadIdx.x]) / (float)m;
   }
   // Partial outputs of this chunk.
   float* yp = w.ypart + ((size_t)(g.prefC[b] * g.H + h * nch + ch)) * m * D;
