@@ -35,7 +35,7 @@ struct Geo {
   int prefK[AKV_MAXB + 1];   // sum of k
   int prefW[AKV_MAXB + 1];   // sum of ceil(S/64) (mask words per head)
   int prefC[AKV_MAXB + 1];   // sum of observation chunks per head
-  int prefKT[AKV_MAXB + 1];  // sum of H * k * (sort chunks): counting-sort table offsets
+  int prefKT[AKV_MAXB + 1];  // sum of H * k * (sort chunks + 1): counting-sort table offsets
   int prefBC[AKV_MAXB + 1];  // sum of budget chunks (H * S / 4096, rounded up)
   int prefSp[AKV_MAXB + 1];  // sum of decode splits per head
   int prefNK[AKV_MAXB + 1];  // sum of key residual counts
@@ -113,10 +113,12 @@ struct Ws {
   float* gpos;          // [side][b][h][S_b] stored coefficient as fp32
   float* u;             // [side][b][h][S_b] utility, -1 for anchors
   uint8_t* sel;         // [side][b][h][S_b] residual flags
+  uint8_t* sflag;       // [side][slots] residual flags in sorted slot order
   uint32_t* bhist;      // [b][side][256]
   int32_t* bstate;      // [b][side][4]: prefix bits, remaining, threshold bits, need
   int32_t* tiecnt;      // [b][side][nchunk]
-  int32_t* shist;       // [b][h][k_b][sort chunks] counting-sort histograms, then offsets
+  int32_t* shist;       // [b][h][sort chunks + 1][k_b] per-chunk anchor histograms, then column prefixes; last row: anchor totals, then their exclusive prefix
+  int32_t* scnt;        // [b][h] counting-sort scan blocks done (zeroed at the start of an encode)
   int32_t* wcnt;        // [side][b][h][ceil(S_b/64)] popcounts for the slot scan
 };
 

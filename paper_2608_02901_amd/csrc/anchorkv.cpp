@@ -66,7 +66,7 @@ struct anchorkv_plan {
   size_t cache_bytes;
   // encode workspace offsets
   size_t w_opmax, w_opsum, w_oM, w_oiZ, w_oiZ64, w_ypart, w_Y, w_Yhi, w_Ylo, w_ynorm, w_sc, w_rank, w_flag, w_sband, w_sbscore, w_sstate, w_QA, w_apos,
-      w_fix, w_fixcount, w_gpos, w_u, w_sel, w_bhist, w_bstate, w_tiecnt, w_shist, w_wcnt;
+      w_fix, w_fixcount, w_gpos, w_u, w_sel, w_sflag, w_bhist, w_bstate, w_tiecnt, w_shist, w_scnt, w_wcnt;
   size_t ws_bytes;
   // decode workspace offsets
   size_t d_SK, d_RK, d_part, d_asc, d_atop;
@@ -214,7 +214,7 @@ extern "C" anchorkv_status anchorkv_plan_create(const anchorkv_config* cfg, int3
     geo.prefK[b + 1] = geo.prefK[b] + k;
     geo.prefW[b + 1] = geo.prefW[b] + (S + 63) / 64;
     geo.prefC[b + 1] = geo.prefC[b] + (S + akv::OBS_CHUNK - 1) / akv::OBS_CHUNK;
-    geo.prefKT[b + 1] = geo.prefKT[b] + H * k * ((S + akv::SORT_CHUNK - 1) / akv::SORT_CHUNK);
+    geo.prefKT[b + 1] = geo.prefKT[b] + H * k * ((S + akv::SORT_CHUNK - 1) / akv::SORT_CHUNK + 1);
     geo.prefBC[b + 1] = geo.prefBC[b] + (H * S + kBudgetChunk - 1) / kBudgetChunk;
     geo.prefKp[b + 1] = geo.prefKp[b] + ((k + 3) & ~3);
     geo.prefAB[b + 1] = geo.prefAB[b] + (k + 255) / 256;
@@ -290,10 +290,12 @@ extern "C" anchorkv_status anchorkv_plan_create(const anchorkv_config* cfg, int3
   p->w_gpos = Wl.add(4 * 2 * TS);
   p->w_u = Wl.add(4 * 2 * TS);
   p->w_sel = Wl.add(2 * TS);
+  p->w_sflag = Wl.add(2 * TW * 64);
   p->w_bhist = Wl.add(4 * 2 * 256 * batch);
   p->w_bstate = Wl.add(4 * 2 * 4 * batch);
   p->w_tiecnt = Wl.add(4 * 2 * (size_t)geo.prefBC[batch]);
   p->w_shist = Wl.add(4 * (size_t)geo.prefKT[batch]);
+  p->w_scnt = Wl.add(4 * (size_t)batch * H);
   p->w_wcnt = Wl.add(4 * 2 * TW);
   p->ws_bytes = Wl.total;
 
@@ -382,10 +384,12 @@ static akv::Ws ws_ptrs(const anchorkv_plan* p, void* base) {
   w.gpos = at<float>(base, p->w_gpos);
   w.u = at<float>(base, p->w_u);
   w.sel = at<uint8_t>(base, p->w_sel);
+  w.sflag = at<uint8_t>(base, p->w_sflag);
   w.bhist = at<uint32_t>(base, p->w_bhist);
   w.bstate = at<int32_t>(base, p->w_bstate);
   w.tiecnt = at<int32_t>(base, p->w_tiecnt);
   w.shist = at<int32_t>(base, p->w_shist);
+  w.scnt = at<int32_t>(base, p->w_scnt);
   w.wcnt = at<int32_t>(base, p->w_wcnt);
   return w;
 }
@@ -683,6 +687,7 @@ __global__ void k_init(Geo g, Cache c, Ws w) {
   }
   if (i < 4 * g.B) c.stats[i] = 0;
   if (i < 2 * g.H * g.B) w.fixcount[i] = 0;
+  if (i < g.H * g.B) w.scnt[i] = 0;
 }
 hipError_t launch_init(const Geo& g, const Cache& c, const Ws& w, hipStream_t st) {
   const int n = 4 * g.B > 2 * g.H * g.B ? 4 * g.B : 2 * g.H * g.B;

@@ -1,6 +1,6 @@
 // Per-token epilogue of the compression: projection coefficient and
 // residual (Sec. 3.1 Eq. projection) and the attention-output-aware
-// utilities (Sec. 3.3 Eq. utilities, App. A.3), for 32 tokens of one
+// utilities (Sec. 3.3 Eq. utilities, App. A.3), for EPI_TOK tokens of one
 // (request, head) per workgroup.
 //
 // Coefficient (bit-exact with the CPU oracle): d = sequential fp64 dot of the
@@ -14,27 +14,43 @@
 // with q_w . rK_t = q_w . k_t - gamma_t (q_w . abar_a(t)) (the second term from
 // the QA table), ||v_t - y_w||^2 = ||v_t||^2 - 2 v_t . y_w + ||y_w||^2 and the
 // logits and v_t . y_w on MFMA; anchors get u = -1 and never compete.
+//
+// Schedule: first the 2 x EPI_TOK coefficient chains of the workgroup's
+// tokens (two per thread, spread over all waves), then the utilities tile by
+// tile (32 tokens), with the observation rows staged in LDS once, each wave's
+// y fragments and its rows' softmax constants held in registers for all
+// tiles, and the next tile's keys and values loaded while the current tile is
+// processed.
 #include "akv_common.h"
 
 namespace akv {
 
-template <int DT>
+constexpr int EPI_TOK = 256;  // tokens per workgroup: 8 tiles of 32
+
+template <int DT, int R>
 __global__ __launch_bounds__(256) void k_epilogue(Geo g, Ws w, Cache c, const void* Kin, const void* Vin,
                                                   const void* Qin) {
   using E = typename Elem<DT>::T;
   using M = MF<DT>;
   constexpr int LD = AKV_D + (DT ? 8 : 4);
   constexpr int PER = 16 / sizeof(E);
+  constexpr int CPR = AKV_D / PER;          // 16-byte chunks per row
+  constexpr int RPT = 32 * CPR / 256;       // chunks per thread of one 32-row tile
+  constexpr int NKS = AKV_D / M::KS;
+  constexpr int NT = EPI_TOK / 32;
   __shared__ __align__(16) E KT[32 * LD];
   __shared__ __align__(16) E VT[32 * LD];
-  __shared__ float gK_s[32], rv2_s[32], vn_s[32], sumK[32], sumV[32];
-  __shared__ int aK_s[32], cand_s[32];
+  __shared__ float gK_s[EPI_TOK], rv2_s[EPI_TOK], vn_s[EPI_TOK];
+  __shared__ int aK_s[EPI_TOK];
+  __shared__ float sumK[4][EPI_TOK], sumV[4][EPI_TOK];
+  extern __shared__ __align__(16) char qlds_raw[];  // the m observation rows, row stride LD
+  E* QS = (E*)qlds_raw;
 
   int idx = blockIdx.x;
-  const int b = locate(g, 32, 1, idx);
+  const int b = locate(g, EPI_TOK, 1, idx);
   const int S = g.S[b], k = g.k[b], D = AKV_D, m = g.m;
-  const int ntile = (S + 31) / 32;
-  const int h = idx / ntile, t0 = (idx % ntile) * 32;
+  const int nchunk = (S + EPI_TOK - 1) / EPI_TOK;
+  const int h = idx / nchunk, tb = (idx % nchunk) * EPI_TOK;
   const size_t xoff = ((size_t)g.prefS[b] * g.H + (size_t)h * S) * D;
   const E* Kx = (const E*)Kin + xoff;
   const E* Vx = (const E*)Vin + xoff;
@@ -43,187 +59,190 @@ __global__ __launch_bounds__(256) void k_epilogue(Geo g, Ws w, Cache c, const vo
   const size_t ko = (size_t)g.prefK[b] * g.H + (size_t)h * k;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
 
-  // Threads 0..63 = (token, side): the anchor rank and the assigned anchor
-  // are read first, and the anchor row right after them, so that the
-  // coefficient below waits for no memory (the rows of K and V load meanwhile).
-  int rk0 = -1, ap0 = 0;
-  uint4 arv[AKV_D / PER];
-  double nrm0 = 0.0;
-  if (threadIdx.x < 64) {
-    const int side = threadIdx.x >> 5, t = min(t0 + (threadIdx.x & 31), S - 1);
-    rk0 = w.rank[po + t];
-    ap0 = w.apos[side * TS + po + t];
-    const int a = (ap0 < 0 || ap0 >= k) ? 0 : ap0;
-    const E* arow = (const E*)(side ? c.ancV : c.ancK) + (ko + a) * D;
-#pragma unroll
-    for (int i = 0; i < AKV_D / PER; ++i) {
-      const uint4 v = *(const uint4*)(arow + i * PER);
-      arv[i] = make_uint4(v.x, v.y, v.z, v.w);
-    }
-    nrm0 = (side ? c.nrmV : c.nrmK)[ko + a];
+  const E* Q = (const E*)Qin + ((size_t)b * g.Hq + (size_t)h * g.g) * g.W * D;
+  for (int ch = threadIdx.x; ch < m * CPR; ch += 256) {
+    const int r = ch / CPR, col = (ch % CPR) * PER;
+    *(uint4*)(&QS[r * LD + col]) = *(const uint4*)(Q + (size_t)r * D + col);
   }
 
+  // ---- coefficients: thread = token tb + tid, both sides.  A token with
+  // an invalid assignment raises the error bit and uses anchor 0; the
+  // K side marks utility candidates (non-anchors), the V side also leaves
+  // ||rV||^2 and ||v||^2.
+  {
+    const int tl = threadIdx.x, t = tb + tl;
+    const bool in = t < S;
+    const int tc = in ? t : S - 1;
+    const int rk = w.rank[po + tc];
+#pragma unroll 1
+    for (int side = 0; side < 2; ++side) {
+      const int ap = w.apos[side * TS + po + tc];
+      const bool bad = ap < 0 || ap >= k;
+      const int a = bad ? 0 : ap;
+      const E* xrow = (side ? Vx : Kx) + (size_t)tc * D;
+      const E* arow = (const E*)(side ? c.ancV : c.ancK) + (ko + a) * D;
+      const double n = (side ? c.nrmV : c.nrmK)[ko + a];
+      uint4 xv[CPR], av[CPR];
 #pragma unroll
-  for (int ch = threadIdx.x; ch < 32 * (AKV_D / PER); ch += 256) {
-    int r = ch / (D / PER), col = (ch % (D / PER)) * PER;
-    uint4 kv = make_uint4(0, 0, 0, 0), vv = make_uint4(0, 0, 0, 0);
-    if (t0 + r < S) {
-      kv = *(const uint4*)(Kx + (size_t)(t0 + r) * D + col);
-      vv = *(const uint4*)(Vx + (size_t)(t0 + r) * D + col);
-    }
-    *(uint4*)(&KT[r * LD + col]) = kv;
-    *(uint4*)(&VT[r * LD + col]) = vv;
-  }
-  if (threadIdx.x < 32) {
-    sumK[threadIdx.x] = 0.0f;
-    sumV[threadIdx.x] = 0.0f;
-  }
-  __syncthreads();
-
-  // Coefficients: threads 0..63 = (token, side).
-  if (threadIdx.x < 64) {
-    const int tl = threadIdx.x & 31, side = threadIdx.x >> 5, t = t0 + tl;
-    if (t < S) {
-      const int rk = rk0;
-      const size_t o = side * TS + po + t;
-      const E* xrow = &(side ? VT : KT)[tl * LD];
-      if (rk >= 0) {
-        w.gpos[o] = 1.0f;
-        if (side == 0) { gK_s[tl] = 1.0f; aK_s[tl] = rk; cand_s[tl] = 0; }
-        if (side == 1) rv2_s[tl] = 0.0f;
-      } else {
-        int a = ap0;
-        if (a < 0 || a >= k) {
-          atomicOr(&c.header[2], 4u);
-          a = 0;
-        }
-        const E* arow = (const E*)arv;  // the prefetched row of anchor a
-        const double n = nrm0;
-        const double d = dot64_seq<DT>(xrow, arow, D);
-        const double g64 = n > 0.0 ? d / n : 0.0;
-        const float gb = Elem<DT>::round_coef((float)g64);
-        w.gpos[o] = gb;
-        if (side == 0) { gK_s[tl] = gb; aK_s[tl] = a; cand_s[tl] = 1; }
-        if (side == 1) {
-          float s = 0.0f;
-#pragma unroll
-          for (int j0 = 0; j0 < AKV_D; j0 += PER) {
-            const uint4 av = *(const uint4*)(arow + j0);
-            const uint4 xv = *(const uint4*)(xrow + j0);
-            const E* ea = (const E*)&av;
-            const E* ex = (const E*)&xv;
-#pragma unroll
-            for (int j = 0; j < PER; ++j) {
-              float p = gb * Elem<DT>::get(ea, j);
-              float r = Elem<DT>::get(ex, j) - p;
-              s = fmaf(r, r, s);
-            }
-          }
-          rv2_s[tl] = s;
-        }
+      for (int i = 0; i < CPR; ++i) {
+        const uint4 x4 = *(const uint4*)(xrow + i * PER);
+        const uint4 a4 = *(const uint4*)(arow + i * PER);
+        xv[i] = make_uint4(x4.x, x4.y, x4.z, x4.w);
+        av[i] = make_uint4(a4.x, a4.y, a4.z, a4.w);
       }
-    } else if (side == 0) {
-      cand_s[tl] = 0;
-      gK_s[tl] = 0.0f;
-      aK_s[tl] = 0;
+      const E* xe = (const E*)xv;
+      const E* ae = (const E*)av;
+      float gb = 1.0f;
+      if (in && rk < 0) {
+        if (bad) atomicOr(&c.header[2], 4u);
+        const double d = dot64_seq<DT>(xe, ae, D);
+        const double g64 = n > 0.0 ? d / n : 0.0;
+        gb = Elem<DT>::round_coef((float)g64);
+      }
+      if (in) w.gpos[side * TS + po + t] = gb;
+      if (side == 0) {
+        gK_s[tl] = in ? gb : 0.0f;
+        aK_s[tl] = (in && rk < 0) ? a : -1;  // -1: no utility (anchor or past S)
+      } else {
+        float rs = 0.0f, vs = 0.0f;
+#pragma unroll
+        for (int j = 0; j < AKV_D; ++j) {
+          const float x = Elem<DT>::get(xe, j);
+          const float r = x - gb * Elem<DT>::get(ae, j);
+          rs = fmaf(r, r, rs);
+          vs = fmaf(x, x, vs);
+        }
+        rv2_s[tl] = (in && rk < 0) ? rs : 0.0f;
+        vn_s[tl] = vs;
+      }
     }
-  } else if (threadIdx.x < 96) {
-    const int tl = threadIdx.x - 64;
-    float s = 0.0f;
-    for (int j = 0; j < D; ++j) {
-      float v = Elem<DT>::get(&VT[tl * LD], j);
-      s = fmaf(v, v, s);
-    }
-    vn_s[tl] = s;
   }
-  __syncthreads();
 
+  // ---- utilities.  Wave rows: row block rb = wave + 4 r; lane l supplies
+  // row rb*32 + l%32 of the fragments and owns the accumulator rows
+  // rb*32 + crow(e, l) of token column l%32.
   const int nrb = (m + 31) / 32;
   const float isd = 1.0f / sqrtf((float)D);
-  const E* Q = (const E*)Qin + ((size_t)b * g.Hq + (size_t)h * g.g) * g.W * D;
   const float* oM = w.oM + (size_t)(b * g.H + h) * m;
   const float* oiZ = w.oiZ + (size_t)(b * g.H + h) * m;
   const float* yn = w.ynorm + (size_t)(b * g.H + h) * m;
   const float* QA = w.QA + ko * m;
-  const int tl = lane & 31;
-  const bool cand = cand_s[tl] != 0;
-  const float gk = gK_s[tl];
-  const int ak = aK_s[tl];
-  const float vn = vn_s[tl];
-  const bool vec = (m & 3) == 0;  // the row tables can be read as float4
-  for (int rb = wave; rb < nrb; rb += 4) {
-    // Rows past m (a partial last block) load row m - 1 and contribute 0.
-    const int arow = min(rb * 32 + (lane & 31), m - 1);
-    const E* qrow = Q + (size_t)arow * D;
-    const size_t yo = ((size_t)(b * g.H + h) * m + arow) * D;
-    f32x16 accL = {}, accY = {};
+  typename M::frag yh[R][NKS], yl[R][DT ? NKS : 1];
+  // alpha = exp(l / sqrt(D) - M_w) / Z_w is taken as exp(l / sqrt(D) - c_w)
+  // with c_w = M_w + ln Z_w (one register per row).
+  float cv[R][16], yv[R][16];
 #pragma unroll
-    for (int s = 0; s < D / M::KS; ++s) {
+  for (int r = 0; r < R; ++r) {
+    const int rb = wave + 4 * r;
+    const int arow = min(rb * 32 + (lane & 31), m - 1);
+    const size_t yo = ((size_t)(b * g.H + h) * m + arow) * D;
+#pragma unroll
+    for (int s = 0; s < NKS; ++s) {
       const int k0 = kofs(M::KS, s, lane);
-      auto qa = M::load(qrow, k0);
-      auto kb = M::load_lds(&KT[tl * LD], k0);
-      auto vb = M::load_lds(&VT[tl * LD], k0);
-      accL = M::mma(qa, kb, accL);
       if constexpr (DT == 1) {
-        accY = M::mma(M::load(w.Yhi + yo, k0), vb, accY);
-        accY = M::mma(M::load(w.Ylo + yo, k0), vb, accY);
+        yh[r][s] = M::load(w.Yhi + yo, k0);
+        yl[r][s] = M::load(w.Ylo + yo, k0);
       } else {
-        accY = M::mma(w.Y[yo + k0], vb, accY);
+        yh[r][s] = w.Y[yo + k0];
       }
     }
-    float tk = 0.0f, tv = 0.0f;
-    if (cand) {
-      // Rows of accumulator entries 4j .. 4j+3 are consecutive.
-      const float* qa = QA + (size_t)ak * m;
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int w0 = rb * 32 + j * 8 + (lane >> 5) * 4;
-        float qv[4], mv[4], zv[4], yv[4];
-        if (vec && w0 < m) {
-          const float4 q4 = *(const float4*)(qa + w0), m4 = *(const float4*)(oM + w0);
-          const float4 z4 = *(const float4*)(oiZ + w0), y4 = *(const float4*)(yn + w0);
-          qv[0] = q4.x; qv[1] = q4.y; qv[2] = q4.z; qv[3] = q4.w;
-          mv[0] = m4.x; mv[1] = m4.y; mv[2] = m4.z; mv[3] = m4.w;
-          zv[0] = z4.x; zv[1] = z4.y; zv[2] = z4.z; zv[3] = z4.w;
-          yv[0] = y4.x; yv[1] = y4.y; yv[2] = y4.z; yv[3] = y4.w;
-        } else {
+    for (int e = 0; e < 16; ++e) {
+      const int wr = min(rb * 32 + crow(e, lane), m - 1);
+      cv[r][e] = oM[wr] - __logf(oiZ[wr]);
+      yv[r][e] = yn[wr];
+    }
+  }
+  // Next tile's keys and values, 16-byte chunks (rows past S are zero).
+  uint4 kpre[RPT], vpre[RPT];
+  auto fetch = [&](int t0) {
+#pragma unroll
+    for (int i = 0; i < RPT; ++i) {
+      const int ch = threadIdx.x + 256 * i, r = ch / CPR, col = (ch % CPR) * PER;
+      kpre[i] = make_uint4(0, 0, 0, 0);
+      vpre[i] = make_uint4(0, 0, 0, 0);
+      if (t0 + r < S) {
+        kpre[i] = *(const uint4*)(Kx + (size_t)(t0 + r) * D + col);
+        vpre[i] = *(const uint4*)(Vx + (size_t)(t0 + r) * D + col);
+      }
+    }
+  };
+  const int ntl = min(NT, (S - tb + 31) / 32);
+  fetch(tb);
+  for (int it = 0; it < ntl; ++it) {
+    const int t0 = tb + 32 * it;
+    __syncthreads();  // previous tile's LDS reads are done (and, at it = 0, the coefficients are in LDS)
+#pragma unroll
+    for (int i = 0; i < RPT; ++i) {
+      const int ch = threadIdx.x + 256 * i, r = ch / CPR, col = (ch % CPR) * PER;
+      *(uint4*)(&KT[r * LD + col]) = kpre[i];
+      *(uint4*)(&VT[r * LD + col]) = vpre[i];
+    }
+    __syncthreads();
+    if (it + 1 < ntl) fetch(t0 + 32);
+    const int tl = 32 * it + (lane & 31);
+    const int ak = aK_s[tl];
+    const float gk = gK_s[tl], vn = vn_s[tl];
+    float tk = 0.0f, tv = 0.0f;
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      const int rb = wave + 4 * r;
+      if (rb >= nrb) break;
+      f32x16 accL = {}, accY = {};
+#pragma unroll
+      for (int s = 0; s < NKS; ++s) {
+        const int k0 = kofs(M::KS, s, lane);
+        const auto kb = M::load_lds(&KT[(lane & 31) * LD], k0);
+        const auto vb = M::load_lds(&VT[(lane & 31) * LD], k0);
+        accL = M::mma(M::load_lds(&QS[(min(rb * 32 + (lane & 31), m - 1)) * LD], k0), kb, accL);
+        accY = M::mma(yh[r][s], vb, accY);
+        if constexpr (DT == 1) accY = M::mma(yl[r][s], vb, accY);
+      }
+      if (ak >= 0) {
+        // Rows of accumulator entries 4j .. 4j+3 are consecutive.
+        const float* qa = QA + (size_t)ak * m;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int w0 = rb * 32 + j * 8 + (lane >> 5) * 4;
+          float qv[4];
+          if ((m & 3) == 0 && w0 < m) {
+            const float4 q4 = *(const float4*)(qa + w0);
+            qv[0] = q4.x; qv[1] = q4.y; qv[2] = q4.z; qv[3] = q4.w;
+          } else {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) qv[i] = qa[min(w0 + i, m - 1)];
+          }
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
-            const int wr = min(w0 + i, m - 1);
-            qv[i] = qa[wr];
-            mv[i] = oM[wr];
-            zv[i] = oiZ[wr];
-            yv[i] = yn[wr];
+            const int e = 4 * j + i;
+            const float l = accL[e];
+            const float al = __expf(l * isd - cv[r][e]);
+            const float a2 = w0 + i < m ? al * al : 0.0f;
+            const float qr = l - gk * qv[i];
+            const float vv = vn - 2.0f * accY[e] + yv[r][e];
+            tk += a2 * (qr * qr) * vv;
+            tv += a2;
           }
-        }
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int e = 4 * j + i;
-          const float l = accL[e];
-          const float al = __expf(l * isd - mv[i]) * zv[i];
-          const float a2 = w0 + i < m ? al * al : 0.0f;
-          const float qr = l - gk * qv[i];
-          const float vv = vn - 2.0f * accY[e] + yv[i];
-          tk += a2 * (qr * qr) * vv;
-          tv += a2;
         }
       }
     }
     tk += __shfl_xor(tk, 32, 64);
     tv += __shfl_xor(tv, 32, 64);
     if (lane < 32) {
-      atomicAdd(&sumK[tl], tk);
-      atomicAdd(&sumV[tl], tv);
+      sumK[wave][tl] = tk;
+      sumV[wave][tl] = tv;
     }
   }
   __syncthreads();
-  if (threadIdx.x < 32) {
-    const int t = t0 + threadIdx.x;
+  {
+    const int tl = threadIdx.x, t = tb + tl;
     if (t < S) {
       float uk = -1.0f, uv = -1.0f;
-      if (cand_s[threadIdx.x]) {
-        uk = sumK[threadIdx.x] / ((float)m * (float)D);
-        uv = rv2_s[threadIdx.x] * sumV[threadIdx.x] / (float)m;
+      if (aK_s[tl] >= 0) {
+        const float sk = (sumK[0][tl] + sumK[1][tl]) + (sumK[2][tl] + sumK[3][tl]);
+        const float sv = (sumV[0][tl] + sumV[1][tl]) + (sumV[2][tl] + sumV[3][tl]);
+        uk = sk / ((float)m * (float)D);
+        uv = rv2_s[tl] * sv / (float)m;
       }
       w.u[po + t] = uk;
       w.u[TS + po + t] = uv;
@@ -234,11 +253,24 @@ __global__ __launch_bounds__(256) void k_epilogue(Geo g, Ws w, Cache c, const vo
 hipError_t launch_epilogue(const Geo& g, const Ws& w, const Cache& c, const void* K, const void* V, const void* Q,
                            hipStream_t st) {
   int nblk = 0;
-  for (int b = 0; b < g.B; ++b) nblk += g.H * ((g.S[b] + 31) / 32);
+  for (int b = 0; b < g.B; ++b) nblk += g.H * ((g.S[b] + EPI_TOK - 1) / EPI_TOK);
+  const bool r2 = g.m > 128;  // 4 waves x 2 row blocks of 32 for up to 256 rows
+  const uint32_t qlds = (uint32_t)g.m * (AKV_D + (g.dtype == 1 ? 8 : 4)) * (g.dtype == 1 ? 2 : 4);
+  // With 256 observation rows the staged rows and the kernel's static arrays
+  // pass 64 KiB; the kernel then asks for the larger LDS allocation gfx950
+  // offers.
+  if (qlds > 32768) {
+    const void* f = g.dtype == 1 ? (r2 ? (const void*)k_epilogue<1, 2> : (const void*)k_epilogue<1, 1>)
+                                 : (r2 ? (const void*)k_epilogue<0, 2> : (const void*)k_epilogue<0, 1>);
+    const hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, (int)qlds);
+    if (e != hipSuccess) return e;
+  }
   if (g.dtype == 1) {
-    launch("k_epilogue", k_epilogue<1>, dim3(nblk), dim3(256), 0, st, g, w, c, K, V, Q);
+    if (r2) launch("k_epilogue", k_epilogue<1, 2>, dim3(nblk), dim3(256), qlds, st, g, w, c, K, V, Q);
+    else launch("k_epilogue", k_epilogue<1, 1>, dim3(nblk), dim3(256), qlds, st, g, w, c, K, V, Q);
   } else {
-    launch("k_epilogue", k_epilogue<0>, dim3(nblk), dim3(256), 0, st, g, w, c, K, V, Q);
+    if (r2) launch("k_epilogue", k_epilogue<0, 2>, dim3(nblk), dim3(256), qlds, st, g, w, c, K, V, Q);
+    else launch("k_epilogue", k_epilogue<0, 1>, dim3(nblk), dim3(256), qlds, st, g, w, c, K, V, Q);
   }
   return hipGetLastError();
 }

@@ -13,9 +13,13 @@
 // offsets folded in), which makes slot lookup O(1).
 //
 //   k_shist    : per 2048-token chunk, histogram of a_V over the k anchors;
-//   k_sscan    : per head, exclusive scan in (anchor, chunk) order;
-//   k_sscatter : stable scatter of the positions, 64 tokens at a time;
-//   k_lrec     : records, flag words and popcounts per sorted slot;
+//   k_sscan    : per block of 256 anchors, each anchor's column of chunk
+//                counts becomes its exclusive prefix, its total goes to the
+//                table's last row;
+//   k_sscatter : per chunk, the anchors' start slots (scan of the totals plus
+//                the column prefix), then a stable scatter of the chunk's
+//                tokens 64 at a time, writing each token's record at its slot;
+//   k_lrec     : flag words and popcounts per sorted slot;
 //   k_lscan    : per request and side, slot bases of every word;
 //   k_codec    : one wave per flagged token: r = x - gamma * abar (fp32),
 //                z = FWHT(s * r), per-group scale, 2-bit codes packed four per
@@ -35,9 +39,10 @@ __device__ inline int locate_sort(const Geo& g, int& idx) {
 
 __device__ inline int32_t* shist_base(const Geo& g, const Ws& w, int b, int h) {
   const int nT = (g.S[b] + SORT_CHUNK - 1) / SORT_CHUNK;
-  return w.shist + (size_t)g.prefKT[b] + (size_t)h * g.k[b] * nT;
+  return w.shist + (size_t)g.prefKT[b] + (size_t)h * g.k[b] * (nT + 1);
 }
 
+// Table of a head: rows = sort chunks, columns = anchors (row nT: totals).
 __global__ __launch_bounds__(256) void k_shist(Geo g, Ws w) {
   extern __shared__ int hist[];
   int idx = blockIdx.x;
@@ -54,108 +59,205 @@ __global__ __launch_bounds__(256) void k_shist(Geo g, Ws w) {
     if (a >= 0 && a < k) atomicAdd(&hist[a], 1);
   }
   __syncthreads();
-  int32_t* out = shist_base(g, w, b, h);
-  for (int a = threadIdx.x; a < k; a += blockDim.x) out[(size_t)a * nT + ch] = hist[a];
+  int32_t* out = shist_base(g, w, b, h) + (size_t)ch * k;
+  for (int a = threadIdx.x; a < k; a += blockDim.x) out[a] = hist[a];
 }
 
-// Per head, the (anchor, chunk) histogram becomes its exclusive prefix sums,
-// in place.  Batches of 8 x 1024 entries in (u, thread) order: coalesced
-// loads (the next batch's issued before the current one is scanned), wave
-// scans, and one scan of the per-(u, wave) totals per batch.
-__global__ __launch_bounds__(1024) void k_sscan(Geo g, Ws w) {
-  constexpr int U = 8;
-  __shared__ int cnts[U * 16];
-  __shared__ int cpre[U * 16 + 1];
-  const int b = blockIdx.x / g.H, h = blockIdx.x % g.H;
+// One thread per (request, head, anchor): the anchor's column of chunk counts
+// becomes its exclusive prefix sum in place (the counts of its tokens in the
+// earlier chunks), and its total goes to row nT; loads are issued 32 rows at
+// a time.  The last workgroup of a head to finish (a per-head counter) turns
+// row nT into the exclusive prefix of the totals, the anchors' first slots:
+// up to 16 tiles of 256 totals per round, all loaded before the wave scans
+// and one scan of the (tile, wave) sums.
+__global__ __launch_bounds__(256) void k_sscan(Geo g, Ws w) {
+  constexpr int TU = 16;
+  __shared__ int wsum[TU * 4];
+  __shared__ int wpre[TU * 4 + 1];
+  __shared__ int last;
+  int idx = blockIdx.x;
+  int b = 0;
+  for (; b < g.B; ++b) {
+    const int n = g.H * ((g.k[b] + 255) / 256);
+    if (idx < n) break;
+    idx -= n;
+  }
+  const int k = g.k[b];
   const int nT = (g.S[b] + SORT_CHUNK - 1) / SORT_CHUNK;
-  const int n = g.k[b] * nT;
-  int32_t* a = shist_base(g, w, b, h);
-  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, nt = blockDim.x;  // nt = 1024
-  int cur[U], nxt[U];
+  const int nab = (k + 255) / 256;
+  const int h = idx / nab, a = (idx % nab) * 256 + threadIdx.x;
+  int32_t* tab = shist_base(g, w, b, h);
+  if (a < k) {
+    int32_t* col = tab + a;
+    constexpr int U = 32;
+    int s = 0;
+    for (int c0 = 0; c0 < nT; c0 += U) {
+      int v[U];
 #pragma unroll
-  for (int u = 0; u < U; ++u) nxt[u] = u * nt + tid < n ? a[u * nt + tid] : 0;
-  int base = 0;
-  for (int c0 = 0; c0 < n; c0 += U * nt) {
+      for (int u = 0; u < U; ++u) v[u] = c0 + u < nT ? col[(size_t)(c0 + u) * k] : 0;
 #pragma unroll
-    for (int u = 0; u < U; ++u) cur[u] = nxt[u];
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int i = c0 + U * nt + u * nt + tid;
-      nxt[u] = i < n ? a[i] : 0;
+      for (int u = 0; u < U; ++u) {
+        if (c0 + u < nT) col[(size_t)(c0 + u) * k] = s;
+        s += v[u];
+      }
     }
-    int x[U];
+    col[(size_t)nT * k] = s;
+  }
+  __threadfence();
+  __syncthreads();
+  if (threadIdx.x == 0) last = atomicAdd(&w.scnt[b * g.H + h], 1) == nab - 1;
+  __syncthreads();
+  if (!last) return;
+  __threadfence();
+  int32_t* tot = tab + (size_t)nT * k;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  int carry = 0;
+  for (int a0 = 0; a0 < k; a0 += TU * 256) {
+    int v[TU], x[TU];
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      x[u] = cur[u];
+    for (int u = 0; u < TU; ++u) {
+      const int i = a0 + u * 256 + threadIdx.x;
+      v[u] = i < k ? tot[i] : 0;
+    }
+#pragma unroll
+    for (int u = 0; u < TU; ++u) {
+      x[u] = v[u];
 #pragma unroll
       for (int o = 1; o < 64; o <<= 1) {
         const int y = __shfl_up(x[u], o, 64);
         if (lane >= o) x[u] += y;
       }
-      if (lane == 63) cnts[u * 16 + wv] = x[u];
+      if (lane == 63) wsum[u * 4 + wave] = x[u];
     }
     __syncthreads();
-    if (wv == 0) {
-      const int v0 = cnts[2 * lane], v1 = cnts[2 * lane + 1];
-      int y = v0 + v1;
+    if (wave == 0) {
+      const int c = wsum[lane];
+      int y = c;
 #pragma unroll
       for (int o = 1; o < 64; o <<= 1) {
         const int z = __shfl_up(y, o, 64);
         if (lane >= o) y += z;
       }
-      cpre[2 * lane] = y - v0 - v1;
-      cpre[2 * lane + 1] = y - v1;
-      if (lane == 63) cpre[U * 16] = y;
+      wpre[lane] = y - c;
+      if (lane == 63) wpre[TU * 4] = y;
     }
     __syncthreads();
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int i = c0 + u * nt + tid;
-      if (i < n) a[i] = base + cpre[u * 16 + wv] + x[u] - cur[u];
+    for (int u = 0; u < TU; ++u) {
+      const int i = a0 + u * 256 + threadIdx.x;
+      if (i < k) tot[i] = carry + wpre[u * 4 + wave] + x[u] - v[u];
     }
-    base += cpre[U * 16];
+    carry += wpre[TU * 4];
     __syncthreads();
   }
 }
 
-// One wave per chunk: tokens in groups of 64 in position order; the rank of a
-// token among equal anchors of its group comes from a lane scan, a running
-// per-anchor count in LDS carries it across groups.
-__global__ __launch_bounds__(64) void k_sscatter(Geo g, Ws w, Cache c) {
-  extern __shared__ int run[];
+// One workgroup per chunk.  The anchors' start slots for this chunk (first
+// slot of the anchor plus its column prefix) and the chunk's token records
+// (anchor indices, stored coefficients, residual flags) are staged in LDS by
+// all four waves; then one wave takes the tokens in groups of 64 in position
+// order.  Lanes holding the same anchor find each other with one ballot per
+// bit of the anchor index; a token's slot is its anchor's start plus the
+// equal tokens before it in the group, and the group's last such lane
+// advances the start.  The token's record is written at its slot, so the
+// records are read in position order and only the writes scatter.
+template <int DT>
+__global__ __launch_bounds__(256) void k_sscatter(Geo g, Ws w, Cache c) {
+  extern __shared__ __align__(16) int lds[];
+  int* sa = lds;                       // [SORT_CHUNK] value-side anchor
+  int* ska = sa + SORT_CHUNK;          // [SORT_CHUNK] key-side anchor
+  float* sgk = (float*)(ska + SORT_CHUNK);
+  float* sgv = sgk + SORT_CHUNK;
+  uint8_t* sfk = (uint8_t*)(sgv + SORT_CHUNK);
+  uint8_t* sfv = sfk + SORT_CHUNK;
+  int* run = (int*)(sfv + SORT_CHUNK);  // [k] running start slot per anchor
   int idx = blockIdx.x;
   const int b = locate_sort(g, idx);
   const int S = g.S[b], k = g.k[b];
   const int nT = (S + SORT_CHUNK - 1) / SORT_CHUNK;
   const int h = idx / nT, ch = idx % nT;
-  const int lane = threadIdx.x;
-  for (int a = lane; a < k; a += 64) run[a] = 0;
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int32_t* tab = shist_base(g, w, b, h);
+  const int32_t* first = tab + (size_t)nT * k;
+  const int32_t* colp = tab + (size_t)ch * k;
+  const size_t TS = (size_t)g.prefS[g.B] * g.H;
+  const size_t TSP = (size_t)g.prefW[g.B] * g.H * 64;
+  const size_t po = (size_t)g.prefS[b] * g.H + (size_t)h * S;
+  const size_t so = slot_base(g, b, h);
+  const int t0 = ch * SORT_CHUNK, t1 = min(S, t0 + SORT_CHUNK), nt = t1 - t0;
+  constexpr int RU = SORT_CHUNK / 256;
+  {
+    int f[RU];
+    float gk[RU], gv[RU];
+    int ak[RU], av[RU];
+    uint8_t fk[RU], fv[RU];
+#pragma unroll
+    for (int u = 0; u < RU; ++u) {
+      const int i = min(u * 256 + tid, nt - 1);
+      av[u] = w.apos[TS + po + t0 + i];
+      ak[u] = w.apos[po + t0 + i];
+      gk[u] = w.gpos[po + t0 + i];
+      gv[u] = w.gpos[TS + po + t0 + i];
+      fk[u] = w.sel[po + t0 + i];
+      fv[u] = w.sel[TS + po + t0 + i];
+    }
+    for (int a0 = 0; a0 < k; a0 += 256 * RU) {
+#pragma unroll
+      for (int u = 0; u < RU; ++u) {
+        const int a = min(a0 + u * 256 + tid, k - 1);
+        f[u] = first[a] + colp[a];
+      }
+#pragma unroll
+      for (int u = 0; u < RU; ++u)
+        if (a0 + u * 256 + tid < k) run[a0 + u * 256 + tid] = f[u];
+    }
+#pragma unroll
+    for (int u = 0; u < RU; ++u) {
+      const int i = u * 256 + tid;
+      sa[i] = av[u];
+      ska[i] = ak[u];
+      sgk[i] = gk[u];
+      sgv[i] = gv[u];
+      sfk[i] = fk[u];
+      sfv[i] = fv[u];
+    }
+  }
   __syncthreads();
-  const int32_t* av = w.apos + (size_t)g.H * g.prefS[g.B] + (size_t)g.prefS[b] * g.H + (size_t)h * S;
-  const int32_t* off = shist_base(g, w, b, h);
-  int32_t* pos = c.pos + slot_base(g, b, h);
-  const int t0 = ch * SORT_CHUNK, t1 = min(S, t0 + SORT_CHUNK);
-  for (int tb = t0; tb < t1; tb += 64) {
-    const int t = tb + lane;
-    int a = t < t1 ? av[t] : -1;
-    if (a >= k) a = -1;
-    int before = 0, after = 0;
-    for (int o = 0; o < 64; ++o) {
-      const int ao = __shfl(a, o, 64);
-      before += (o < lane && ao == a);
-      after += (o > lane && ao == a);
+  if (tid >= 64) return;
+  const int nbits = 32 - __clz(k);  // key a + 1 lies in [0, k]
+  for (int i0 = 0; i0 < nt; i0 += 64) {
+    const int i = i0 + lane;
+    const int a = (i >= nt || sa[i] >= k) ? -1 : sa[i];
+    const unsigned key = (unsigned)(a + 1);
+    unsigned long long peers = ~0ull;
+    for (int bit = 0; bit < nbits; ++bit) {
+      const bool on = (key >> bit) & 1u;
+      const unsigned long long bb = __ballot(on);
+      peers &= on ? bb : ~bb;
     }
+    const int before = __popcll(peers & ((1ull << lane) - 1ull));
+    const bool lastp = (peers >> lane) == 1ull;
     if (a >= 0) {
-      const int dest = off[(size_t)a * nT + ch] + run[a] + before;
-      if (dest >= 0 && dest < S) pos[dest] = t;
+      const int dest = run[a] + before;
+      if (dest >= 0 && dest < S) {
+        const size_t o = so + dest;
+        c.pos[o] = t0 + i;
+        c.idxK[o] = (uint16_t)ska[i];
+        c.idxV[o] = (uint16_t)a;
+        Elem<DT>::put(c.gK, o, sgk[i]);
+        Elem<DT>::put(c.gV, o, sgv[i]);
+        w.sflag[o] = sfk[i];
+        w.sflag[TSP + o] = sfv[i];
+      }
+      if (lastp) run[a] = dest + 1;
     }
-    __syncthreads();
-    if (a >= 0 && after == 0) run[a] += before + 1;
-    __syncthreads();
   }
 }
 
+// Per 256 sorted slots: residual flag words and their popcounts from the
+// slot-order flags; a slot holding an out-of-range position raises the layout
+// error bit.  Padding slots of the head's last word get anchor 0 with
+// coefficient 0.
 template <int DT>
 __global__ __launch_bounds__(256) void k_lrec(Geo g, Ws w, Cache c) {
   int idx = blockIdx.x;
@@ -163,24 +265,15 @@ __global__ __launch_bounds__(256) void k_lrec(Geo g, Ws w, Cache c) {
   const int S = g.S[b];
   const int nt = (S + 255) / 256;
   const int h = idx / nt, i = (idx % nt) * 256 + threadIdx.x;
-  const size_t po = (size_t)g.prefS[b] * g.H + (size_t)h * S;
   const size_t so = slot_base(g, b, h);
-  const size_t TS = (size_t)g.prefS[g.B] * g.H;
+  const size_t TSP = (size_t)g.prefW[g.B] * g.H * 64;
   bool fk = false, fv = false;
   if (i < S) {
-    int t = c.pos[so + i];
-    if (t < 0 || t >= S) {
-      atomicOr(&c.header[2], 8u);
-      t = 0;
-    }
-    c.idxK[so + i] = (uint16_t)w.apos[po + t];
-    c.idxV[so + i] = (uint16_t)w.apos[TS + po + t];
-    Elem<DT>::put(c.gK, so + i, w.gpos[po + t]);
-    Elem<DT>::put(c.gV, so + i, w.gpos[TS + po + t]);
-    fk = w.sel[po + t] != 0;
-    fv = w.sel[TS + po + t] != 0;
+    const int t = c.pos[so + i];
+    if (t < 0 || t >= S) atomicOr(&c.header[2], 8u);
+    fk = w.sflag[so + i] != 0;
+    fv = w.sflag[TSP + so + i] != 0;
   } else if (i < ((S + 63) & ~63)) {
-    // Padding slots of the head's last word: anchor 0 with coefficient 0.
     c.pos[so + i] = 0;
     c.idxK[so + i] = 0;
     c.idxV[so + i] = 0;
@@ -258,9 +351,12 @@ __global__ __launch_bounds__(256) void k_codec(Geo g, Ws w, Cache c, const void*
   const int nw = (S + 63) / 64;
   const int h = wid / nw, word = wid % nw;
   const size_t wo = (size_t)g.prefW[b] * g.H + (size_t)h * nw + word;
+  // The word's mask, first residual slot and the positions of its 64 slots
+  // are read together (the positions without waiting for the mask).
   unsigned long long mask = (side ? c.maskV : c.maskK)[wo];
-  if (!mask) return;
   int slot = (side ? c.pcV : c.pcK)[wo];
+  const int tj = min(max(c.pos[slot_base(g, b, h) + (size_t)word * 64 + lane], 0), S - 1);
+  if (!mask) return;
   const size_t po = (size_t)g.prefS[b] * g.H + (size_t)h * S;
   const size_t TS = (size_t)g.prefS[g.B] * g.H;
   const size_t ko = (size_t)g.prefK[b] * g.H + (size_t)h * k;
@@ -270,48 +366,73 @@ __global__ __launch_bounds__(256) void k_codec(Geo g, Ws w, Cache c, const void*
   uint8_t* codes = side ? c.codesV : c.codesK;
   float* scales = side ? c.scalesV : c.scalesK;
   const float s0 = hsign(g.seed_sign, 2 * lane), s1 = hsign(g.seed_sign, 2 * lane + 1);
+  // Anchor and coefficient of every flagged slot of the word, one lane each.
+  int aj = 0;
+  float gj = 0.0f;
+  if ((mask >> lane) & 1ull) {
+    aj = min(max(w.apos[side * TS + po + tj], 0), k - 1);
+    gj = w.gpos[side * TS + po + tj];
+  }
+  // Up to CB flagged slots per round; their token and anchor coordinates
+  // (2 per lane) are loaded together before any is encoded.
+  constexpr int CB = 4;
   while (mask) {
-    const int bit = __ffsll((long long)mask) - 1;
-    mask &= mask - 1;
-    const int i = word * 64 + bit;
-    const int t = min(max(c.pos[slot_base(g, b, h) + i], 0), S - 1);
-    const int a = min(max(w.apos[side * TS + po + t], 0), k - 1);
-    const float gb = w.gpos[side * TS + po + t];
-    const E* x = X + (size_t)t * D;
-    const E* ar = A + (size_t)a * D;
-    float p0 = gb * Elem<DT>::get(ar, 2 * lane), p1 = gb * Elem<DT>::get(ar, 2 * lane + 1);
-    float r0 = Elem<DT>::get(x, 2 * lane) - p0, r1 = Elem<DT>::get(x, 2 * lane + 1) - p1;
-    float z0 = s0 * r0, z1 = s1 * r1;
-    fwht_wave(z0, z1, lane);
-    // Group scale (G coordinates = G/2 lanes).
-    const int gl = G / 2;
-    float sigma;
-    if (g.scale_mode == 2) {
-      // Sequential fp32 sum of squares over the group, in coordinate order.
-      const int gbase = (lane / gl) * gl;
-      float acc = 0.0f;
-      for (int j = 0; j < gl; ++j) {
-        const float a0 = __shfl(z0, gbase + j, 64), a1 = __shfl(z1, gbase + j, 64);
-        const float q0 = a0 * a0;
-        acc = acc + q0;
-        const float q1 = a1 * a1;
-        acc = acc + q1;
+    int bit[CB];
+    float x0[CB], x1[CB], a0[CB], a1[CB], gq[CB];
+#pragma unroll
+    for (int q = 0; q < CB; ++q) {
+      bit[q] = mask ? __ffsll((long long)mask) - 1 : -1;
+      mask &= mask - 1;
+      x0[q] = x1[q] = a0[q] = a1[q] = gq[q] = 0.0f;
+      if (bit[q] >= 0) {
+        const int t = __builtin_amdgcn_readlane(tj, bit[q]);
+        const int a = __builtin_amdgcn_readlane(aj, bit[q]);
+        gq[q] = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, gj), bit[q]));
+        const E* x = X + (size_t)t * D;
+        const E* ar = A + (size_t)a * D;
+        x0[q] = Elem<DT>::get(x, 2 * lane);
+        x1[q] = Elem<DT>::get(x, 2 * lane + 1);
+        a0[q] = Elem<DT>::get(ar, 2 * lane);
+        a1[q] = Elem<DT>::get(ar, 2 * lane + 1);
       }
-      const float ms = acc / (float)G;
-      sigma = sqrtf(ms);
-    } else {
-      float am = fmaxf(fabsf(z0), fabsf(z1));
-      for (int o = 1; o < gl; o <<= 1) am = fmaxf(am, __shfl_xor(am, o, 64));
-      sigma = g.scale_mode == 1 ? am : am / AKV_L1;
     }
-    const float T = sigma * AKV_T;
-    const int c0 = z0 < 0.0f ? (fabsf(z0) > T ? 0 : 1) : (fabsf(z0) > T ? 3 : 2);
-    const int c1 = z1 < 0.0f ? (fabsf(z1) > T ? 0 : 1) : (fabsf(z1) > T ? 3 : 2);
-    const int nib = c0 | (c1 << 2);
-    const int onib = __shfl_xor(nib, 1, 64);
-    if ((lane & 1) == 0) codes[(size_t)slot * (D / 4) + lane / 2] = (uint8_t)(nib | (onib << 4));
-    if (lane % gl == 0) scales[(size_t)slot * (D / G) + lane / gl] = sigma;
-    ++slot;
+#pragma unroll
+    for (int q = 0; q < CB; ++q) {
+      if (bit[q] < 0) break;
+      const float p0 = gq[q] * a0[q], p1 = gq[q] * a1[q];
+      const float r0 = x0[q] - p0, r1 = x1[q] - p1;
+      float z0 = s0 * r0, z1 = s1 * r1;
+      fwht_wave_dpp(z0, z1, lane);
+      // Group scale (G coordinates = G/2 lanes).
+      const int gl = G / 2;
+      float sigma;
+      if (g.scale_mode == 2) {
+        // Sequential fp32 sum of squares over the group, in coordinate order.
+        const int gbase = (lane / gl) * gl;
+        float acc = 0.0f;
+        for (int j = 0; j < gl; ++j) {
+          const float b0 = __shfl(z0, gbase + j, 64), b1 = __shfl(z1, gbase + j, 64);
+          const float q0 = b0 * b0;
+          acc = acc + q0;
+          const float q1 = b1 * b1;
+          acc = acc + q1;
+        }
+        const float ms = acc / (float)G;
+        sigma = sqrtf(ms);
+      } else {
+        float am = fmaxf(fabsf(z0), fabsf(z1));
+        for (int o = 1; o < gl; o <<= 1) am = fmaxf(am, __shfl_xor(am, o, 64));
+        sigma = g.scale_mode == 1 ? am : am / AKV_L1;
+      }
+      const float T = sigma * AKV_T;
+      const int c0 = z0 < 0.0f ? (fabsf(z0) > T ? 0 : 1) : (fabsf(z0) > T ? 3 : 2);
+      const int c1 = z1 < 0.0f ? (fabsf(z1) > T ? 0 : 1) : (fabsf(z1) > T ? 3 : 2);
+      const int nib = c0 | (c1 << 2);
+      const int onib = __shfl_xor(nib, 1, 64);
+      if ((lane & 1) == 0) codes[(size_t)slot * (D / 4) + lane / 2] = (uint8_t)(nib | (onib << 4));
+      if (lane % gl == 0) scales[(size_t)slot * (D / G) + lane / gl] = sigma;
+      ++slot;
+    }
   }
 }
 
@@ -322,12 +443,24 @@ hipError_t launch_layout(const Geo& g, const Ws& w, const Cache& c, const void* 
     nrec += g.H * ((g.S[b] + 255) / 256);
   }
   const size_t lds = (size_t)g.maxK * sizeof(int);
+  int nscan = 0;
+  for (int b = 0; b < g.B; ++b) nscan += g.H * ((g.k[b] + 255) / 256);
+  const size_t lds_scatter = (size_t)SORT_CHUNK * 18 + (size_t)g.maxK * sizeof(int);
   launch("k_shist", k_shist, dim3(nsort), dim3(256), lds, st, g, w);
-  launch("k_sscan", k_sscan, dim3(g.B * g.H), dim3(1024), 0, st, g, w);
-  launch("k_sscatter", k_sscatter, dim3(nsort), dim3(64), lds, st, g, w, c);
+  launch("k_sscan", k_sscan, dim3(nscan), dim3(256), 0, st, g, w);
+  // Above 64 KiB (more than about 7000 anchors per head) the kernel asks
+  // for the larger LDS allocation gfx950 offers.
+  if (lds_scatter > 65536) {
+    const hipError_t e = g.dtype == 1
+        ? hipFuncSetAttribute((const void*)k_sscatter<1>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_scatter)
+        : hipFuncSetAttribute((const void*)k_sscatter<0>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_scatter);
+    if (e != hipSuccess) return e;
+  }
   if (g.dtype == 1) {
+    launch("k_sscatter", k_sscatter<1>, dim3(nsort), dim3(256), lds_scatter, st, g, w, c);
     launch("k_lrec", k_lrec<1>, dim3(nrec), dim3(256), 0, st, g, w, c);
   } else {
+    launch("k_sscatter", k_sscatter<0>, dim3(nsort), dim3(256), lds_scatter, st, g, w, c);
     launch("k_lrec", k_lrec<0>, dim3(nrec), dim3(256), 0, st, g, w, c);
   }
   launch("k_lscan", k_lscan, dim3(g.B * 2), dim3(1024), 0, st, g, w, c);

@@ -238,22 +238,42 @@ __global__ __launch_bounds__(256) void k_obs_stats(Geo g, Ws w, const void* Kin,
   }
 }
 
+// Row statistics from the chunk statistics: per workgroup 64 rows of one
+// (request, head); the four waves take every fourth chunk, and their partial
+// (max, sum) pairs are merged in LDS.
 __global__ __launch_bounds__(256) void k_obs_reduce(Geo g, Ws w) {
-  const int b = blockIdx.x / g.H, h = blockIdx.x % g.H;
+  __shared__ float pm[4][64];
+  __shared__ double ps[4][64];
+  const int nrg = (g.m + 63) / 64;
+  const int bh = blockIdx.x / nrg, b = bh / g.H, h = bh % g.H;
+  const int lane = threadIdx.x & 63, part = threadIdx.x >> 6;
+  const int wr = (blockIdx.x % nrg) * 64 + lane;
   const int nch = (g.S[b] + OBS_CHUNK - 1) / OBS_CHUNK;
-  for (int wr = threadIdx.x; wr < g.m; wr += blockDim.x) {
-    size_t base = ((size_t)(g.prefC[b] * g.H + h * nch)) * g.m + wr;
-    float M = NEG;
-    for (int c = 0; c < nch; ++c) M = fmaxf(M, w.opmax[base + (size_t)c * g.m]);
-    double Z = 0.0;
-    for (int c = 0; c < nch; ++c) {
-      const float mc = w.opmax[base + (size_t)c * g.m];
-      const double sc = w.opsum[base + (size_t)c * g.m];
-      Z += mc == M ? sc : sc * exp((double)mc - (double)M);
+  const int wc = min(wr, g.m - 1);
+  const size_t base = ((size_t)(g.prefC[b] * g.H + h * nch)) * g.m + wc;
+  float M = NEG;
+  for (int c = part; c < nch; c += 4) M = fmaxf(M, w.opmax[base + (size_t)c * g.m]);
+  double Z = 0.0;
+  for (int c = part; c < nch; c += 4) {
+    const float mc = w.opmax[base + (size_t)c * g.m];
+    const double sc = w.opsum[base + (size_t)c * g.m];
+    Z += mc == M ? sc : sc * exp((double)mc - (double)M);
+  }
+  pm[part][lane] = M;
+  ps[part][lane] = Z;
+  __syncthreads();
+  if (part == 0 && wr < g.m) {
+    float Mt = pm[0][lane];
+    for (int p = 1; p < 4; ++p) Mt = fmaxf(Mt, pm[p][lane]);
+    double Zt = 0.0;
+    for (int p = 0; p < 4; ++p) {
+      const float mp = pm[p][lane];
+      if (mp == NEG) continue;  // a part without chunks
+      Zt += mp == Mt ? ps[p][lane] : ps[p][lane] * exp((double)mp - (double)Mt);
     }
-    w.oM[(size_t)(b * g.H + h) * g.m + wr] = M;
-    w.oiZ[(size_t)(b * g.H + h) * g.m + wr] = (float)(1.0 / Z);
-    w.oiZ64[(size_t)(b * g.H + h) * g.m + wr] = 1.0 / Z;
+    w.oM[(size_t)(b * g.H + h) * g.m + wr] = Mt;
+    w.oiZ[(size_t)(b * g.H + h) * g.m + wr] = (float)(1.0 / Zt);
+    w.oiZ64[(size_t)(b * g.H + h) * g.m + wr] = 1.0 / Zt;
   }
 }
 
@@ -424,7 +444,7 @@ hipError_t launch_obs(const Geo& g, const Ws& w, const void* K, const void* V, c
     if (r2) launch("k_obs_stats", k_obs_stats<0, 2>, dim3(nblk), dim3(256), 0, st, g, w, K, Q);
     else launch("k_obs_stats", k_obs_stats<0, 1>, dim3(nblk), dim3(256), 0, st, g, w, K, Q);
   }
-  launch("k_obs_reduce", k_obs_reduce, dim3(g.B * g.H), dim3(256), 0, st, g, w);
+  launch("k_obs_reduce", k_obs_reduce, dim3(g.B * g.H * ((g.m + 63) / 64)), dim3(256), 0, st, g, w);
   if (g.dtype == 1) {
     if (r2) launch("k_obs_pass", k_obs_pass<1, 2>, dim3(nblk), dim3(256), 0, st, g, w, K, V, Q);
     else launch("k_obs_pass", k_obs_pass<1, 1>, dim3(nblk), dim3(256), 0, st, g, w, K, V, Q);

@@ -511,7 +511,11 @@ template <int DT>
 __global__ __launch_bounds__(256) void k_anchor_prep(Geo g, Ws w, Cache c, const void* Kin, const void* Vin,
                                                      const void* Qin) {
   using E = typename Elem<DT>::T;
-  __shared__ float AK[64][AKV_D + 1];
+  using M = MF<DT>;
+  constexpr int PER = 16 / sizeof(E), CPR = AKV_D / PER;
+  constexpr int LD = AKV_D + (DT ? 8 : 4);  // LDS row stride (16-byte aligned rows)
+  __shared__ __align__(16) E AK[64 * LD];
+  __shared__ __align__(16) E AV[64 * LD];
   int idx = blockIdx.x;
   int b = 0;
   for (; b < g.B; ++b) {
@@ -519,43 +523,62 @@ __global__ __launch_bounds__(256) void k_anchor_prep(Geo g, Ws w, Cache c, const
     if (idx < n) break;
     idx -= n;
   }
-  const int k = g.k[b], S = g.S[b], D = g.D, m = g.m;
+  const int k = g.k[b], S = g.S[b], D = AKV_D, m = g.m;
   const int nch = (k + 63) / 64;
   const int h = idx / nch, a0 = (idx % nch) * 64;
   const size_t xoff = ((size_t)g.prefS[b] * g.H + (size_t)h * S) * D;
   const size_t ko = (size_t)g.prefK[b] * g.H + (size_t)h * k;
   const int32_t* anc = c.anc_pos + ko;
   const int na = min(64, k - a0);
-  // Copy rows and stage the keys in LDS as fp32.
-  for (int i = threadIdx.x; i < na * D; i += blockDim.x) {
-    int a = i / D, d = i % D;
-    int p = anc[a0 + a];
-    p = min(max(p, 0), S - 1);
-    E kv = ((const E*)Kin)[xoff + (size_t)p * D + d];
-    E vv = ((const E*)Vin)[xoff + (size_t)p * D + d];
-    ((E*)c.ancK)[(ko + a0 + a) * D + d] = kv;
-    ((E*)c.ancV)[(ko + a0 + a) * D + d] = vv;
-    AK[a][d] = Elem<DT>::get(&kv, 0);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  // Copy the 64 anchor rows in 16-byte chunks and stage them in LDS (rows
+  // past na are zero).
+#pragma unroll
+  for (int i = threadIdx.x; i < 64 * CPR; i += 256) {
+    const int a = i / CPR, col = (i % CPR) * PER;
+    uint4 kv = make_uint4(0, 0, 0, 0), vv = make_uint4(0, 0, 0, 0);
+    if (a < na) {
+      const int p = min(max(anc[a0 + a], 0), S - 1);
+      kv = *(const uint4*)((const E*)Kin + xoff + (size_t)p * D + col);
+      vv = *(const uint4*)((const E*)Vin + xoff + (size_t)p * D + col);
+      *(uint4*)((E*)c.ancK + (ko + a0 + a) * D + col) = kv;
+      *(uint4*)((E*)c.ancV + (ko + a0 + a) * D + col) = vv;
+    }
+    *(uint4*)&AK[a * LD + col] = kv;
+    *(uint4*)&AV[a * LD + col] = vv;
   }
   __syncthreads();
   // Canonical squared norms (fp64, sequential) and fp32 inverse norms.
   if (threadIdx.x < 2 * na) {
     const int a = threadIdx.x % na, side = threadIdx.x / na;
-    const E* row = (const E*)(side ? c.ancV : c.ancK) + (ko + a0 + a) * D;
+    const E* row = &(side ? AV : AK)[a * LD];
     double n = dot64_seq<DT>(row, row, D);
     (side ? c.nrmV : c.nrmK)[ko + a0 + a] = n;
     (side ? c.invV : c.invK)[ko + a0 + a] = n > 0.0 ? (float)(1.0 / sqrt(n)) : 0.0f;
   }
-  // QA[a][w] = q_w . abar^K_a (raw dot, fp32), anchor-major so that a token
-  // reads the m values of its anchor contiguously.
+  // QA[a][w] = q_w . abar^K_a (fp32 accumulation of exact products), anchor-
+  // major so that a token reads the m values of its anchor contiguously: one
+  // 32x32 MFMA tile (anchors x observation rows) per wave and step.
   const E* Q = (const E*)Qin + ((size_t)b * g.Hq + (size_t)h * g.g) * g.W * D;
   float* QA = w.QA + ko * m;
-  for (int i = threadIdx.x; i < m * na; i += blockDim.x) {
-    int a = i / m, wr = i % m;
-    const E* q = Q + (size_t)wr * D;
-    float s = 0.0f;
-    for (int d = 0; d < D; ++d) s = fmaf(Elem<DT>::get(q, d), AK[a][d], s);
-    QA[(size_t)(a0 + a) * m + wr] = s;
+  const int nrb = (m + 31) / 32, nat = (na + 31) / 32;
+  for (int ti = wave; ti < nat * nrb; ti += 4) {
+    const int at = ti % nat, wt = ti / nat;
+    const int wr = wt * 32 + (lane & 31);
+    const E* qrow = Q + (size_t)min(wr, m - 1) * D;
+    f32x16 acc = {};
+#pragma unroll
+    for (int s = 0; s < AKV_D / M::KS; ++s) {
+      const int k0 = kofs(M::KS, s, lane);
+      acc = M::mma(M::load_lds(&AK[(at * 32 + (lane & 31)) * LD], k0), M::load(qrow, k0), acc);
+    }
+    if (wr < m) {
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int a = at * 32 + crow(e, lane);
+        if (a < na) QA[(size_t)(a0 + a) * m + wr] = acc[e];
+      }
+    }
   }
 }
 
