@@ -55,6 +55,23 @@ __device__ __host__ inline size_t slot_base(const Geo& g, int b, int h) {
 constexpr int OBS_CHUNK = 2048;   // tokens per observation-pass workgroup
 constexpr int SEL_BAND_MAX = 256; // largest band re-scored in fp64 at the selection cut
 constexpr int SORT_CHUNK = 2048;  // tokens per counting-sort chunk
+constexpr int SEL_SLICE = 4096;   // positions per workgroup of the selection passes
+constexpr int SEL_CMAX = 32768;   // first-digit candidates kept for the exact top-n cut
+constexpr int SEL_CAND = 1024;    // hash candidates kept in the uniform share's bin
+// Selection state fields per (request, head), zeroed at the start of an encode.
+enum : int {
+  SS_PREFIX = 0,  // bits of the n_top-th largest pooled fp32 score
+  SS_REMAIN = 1,  // positions equal to it still to take
+  SS_NABOVE = 2,  // positions clearly above the band (taken)
+  SS_NBAND = 3,   // band members listed (more than SEL_BAND_MAX: overflow)
+  SS_BIN1 = 5,    // first digit of the cut
+  SS_ABOVE1 = 6,  // positions whose first digit is larger
+  SS_NCAND = 7,   // first-digit candidates appended
+  SS_RBIN = 8,    // hash bin of the uniform share's last key
+  SS_RNEED = 9,   // keys still to take inside it
+  SS_NRC = 10,    // hash candidates appended
+  SS_N = 16
+};
 
 // Device pointers into the cache blob (layouts in position p = request-major,
 // head-major order; "sorted" arrays are in decode order, see the layout build).
@@ -104,7 +121,12 @@ struct Ws {
   uint8_t* flag;        // [b][h][S_b] selection marks
   int32_t* sband;       // [b][h][SEL_BAND_MAX] positions in the fp64 band around the top-n cut
   double* sbscore;      // [b][h][SEL_BAND_MAX] their fp64 pooled scores
-  int32_t* sstate;      // [b][h][4] cut bits, remaining, taken above the band, band size (-1: none)
+  int32_t* sstate;      // [b][h][SS_N] selection state (fields SS_*)
+  uint32_t* sghist;     // [b][h][4096] selection histogram summed over workgroups (zero between passes)
+  float* scand;         // [b][h][SEL_CMAX] pooled scores in the first digit's bin of the cut
+  unsigned long long* rkey;  // [b][h][SEL_CAND] hash keys in the uniform share's bin
+  int32_t* rpos;        // [b][h][SEL_CAND] their positions
+  int32_t* slcnt;       // [b][h][ceil(maxS / SEL_SLICE)] anchors flagged per selection slice
   float* QA;            // [b][h][m][k_b] q_w . abar^K_a
   int32_t* apos;        // [side][b][h][S_b] anchor index per position (-1: fixup pending)
   int32_t* fixt;        // [side][b][h][S_b] per-head fixup list: token positions (filled from the front)
@@ -113,12 +135,11 @@ struct Ws {
   float* gpos;          // [side][b][h][S_b] stored coefficient as fp32
   float* u;             // [side][b][h][S_b] utility, -1 for anchors
   uint8_t* sel;         // [side][b][h][S_b] residual flags
-  uint8_t* sflag;       // [side][slots] residual flags in sorted slot order
+  uint4* srec;          // [slots] record of the token placed at a sorted slot (position and flags, anchors, coefficients)
   uint32_t* bhist;      // [b][side][256]
   int32_t* bstate;      // [b][side][4]: prefix bits, remaining, threshold bits, need
   int32_t* tiecnt;      // [b][side][nchunk]
-  int32_t* shist;       // [b][h][sort chunks + 1][k_b] per-chunk anchor histograms, then column prefixes; last row: anchor totals, then their exclusive prefix
-  int32_t* scnt;        // [b][h] counting-sort scan blocks done (zeroed at the start of an encode)
+  int32_t* shist;       // [b][h][sort chunks + 1][k_b] per-chunk anchor histograms, then column prefixes; last row: anchor totals
   int32_t* wcnt;        // [side][b][h][ceil(S_b/64)] popcounts for the slot scan
 };
 
@@ -200,10 +221,12 @@ __device__ inline int crow(int r, int lane) { return (r >> 2) * 8 + (lane >> 5) 
 
 // ------------------------------------------------------------------ canonical fp64 dot
 // Products of fp32 / bf16 values are exact in fp64; the sum runs j = 0..D-1
-// with one rounding per addition and no fused multiply-add.
-// The length is the head dimension AKV_D (the argument must equal it); the
-// unrolled loop lets the row loads be issued ahead of the addition chain
-// instead of one round trip per 16-byte chunk.
+// with one rounding per addition.  Each step is an fp64 fused multiply-add,
+// which rounds once, on the exact product: the same value as the addition of
+// the separately formed product.  The length is the head dimension AKV_D
+// (the argument must equal it); the unrolled loop lets the row loads be
+// issued ahead of the addition chain instead of one round trip per 16-byte
+// chunk.
 template <int DT>
 __device__ inline double dot64_seq(const typename Elem<DT>::T* x, const typename Elem<DT>::T* y, int) {
   constexpr int D = AKV_D;
@@ -216,17 +239,17 @@ __device__ inline double dot64_seq(const typename Elem<DT>::T* x, const typename
       const uint16_t* xs = (const uint16_t*)&xv;
       const uint16_t* ys = (const uint16_t*)&yv;
 #pragma unroll
-      for (int i = 0; i < 8; ++i) s = s + (double)bf2f(xs[i]) * (double)bf2f(ys[i]);
+      for (int i = 0; i < 8; ++i) s = fma((double)bf2f(xs[i]), (double)bf2f(ys[i]), s);
     }
   } else {
 #pragma unroll
     for (int j = 0; j < D; j += 4) {
       float4 xv = *(const float4*)(x + j);
       float4 yv = *(const float4*)(y + j);
-      s = s + (double)xv.x * (double)yv.x;
-      s = s + (double)xv.y * (double)yv.y;
-      s = s + (double)xv.z * (double)yv.z;
-      s = s + (double)xv.w * (double)yv.w;
+      s = fma((double)xv.x, (double)yv.x, s);
+      s = fma((double)xv.y, (double)yv.y, s);
+      s = fma((double)xv.z, (double)yv.z, s);
+      s = fma((double)xv.w, (double)yv.w, s);
     }
   }
   return s;

@@ -65,8 +65,8 @@ struct anchorkv_plan {
       c_stats;
   size_t cache_bytes;
   // encode workspace offsets
-  size_t w_opmax, w_opsum, w_oM, w_oiZ, w_oiZ64, w_ypart, w_Y, w_Yhi, w_Ylo, w_ynorm, w_sc, w_rank, w_flag, w_sband, w_sbscore, w_sstate, w_QA, w_apos,
-      w_fix, w_fixcount, w_gpos, w_u, w_sel, w_sflag, w_bhist, w_bstate, w_tiecnt, w_shist, w_scnt, w_wcnt;
+  size_t w_opmax, w_opsum, w_oM, w_oiZ, w_oiZ64, w_ypart, w_Y, w_Yhi, w_Ylo, w_ynorm, w_sc, w_rank, w_flag, w_sband, w_sbscore, w_sstate, w_sghist, w_scand, w_rkey, w_rpos, w_slcnt, w_QA, w_apos,
+      w_fix, w_fixcount, w_gpos, w_u, w_sel, w_srec, w_bhist, w_bstate, w_tiecnt, w_shist, w_wcnt;
   size_t ws_bytes;
   // decode workspace offsets
   size_t d_SK, d_RK, d_part, d_asc, d_atop;
@@ -282,7 +282,12 @@ extern "C" anchorkv_status anchorkv_plan_create(const anchorkv_config* cfg, int3
   p->w_flag = Wl.add(TS);
   p->w_sband = Wl.add(4 * (size_t)batch * H * akv::SEL_BAND_MAX);
   p->w_sbscore = Wl.add(8 * (size_t)batch * H * akv::SEL_BAND_MAX);
-  p->w_sstate = Wl.add(4 * 4 * (size_t)batch * H);
+  p->w_sstate = Wl.add(4 * akv::SS_N * (size_t)batch * H);
+  p->w_sghist = Wl.add(4 * 4096 * (size_t)batch * H);
+  p->w_scand = Wl.add(4 * (size_t)akv::SEL_CMAX * batch * H);
+  p->w_rkey = Wl.add(8 * (size_t)akv::SEL_CAND * batch * H);
+  p->w_rpos = Wl.add(4 * (size_t)akv::SEL_CAND * batch * H);
+  p->w_slcnt = Wl.add(4 * (size_t)((geo.maxS + akv::SEL_SLICE - 1) / akv::SEL_SLICE) * batch * H);
   p->w_QA = Wl.add(4 * TK * m);
   p->w_apos = Wl.add(4 * 2 * TS);
   p->w_fix = Wl.add(8 * 2 * TS);
@@ -290,12 +295,11 @@ extern "C" anchorkv_status anchorkv_plan_create(const anchorkv_config* cfg, int3
   p->w_gpos = Wl.add(4 * 2 * TS);
   p->w_u = Wl.add(4 * 2 * TS);
   p->w_sel = Wl.add(2 * TS);
-  p->w_sflag = Wl.add(2 * TW * 64);
+  p->w_srec = Wl.add(16 * TW * 64);
   p->w_bhist = Wl.add(4 * 2 * 256 * batch);
   p->w_bstate = Wl.add(4 * 2 * 4 * batch);
   p->w_tiecnt = Wl.add(4 * 2 * (size_t)geo.prefBC[batch]);
   p->w_shist = Wl.add(4 * (size_t)geo.prefKT[batch]);
-  p->w_scnt = Wl.add(4 * (size_t)batch * H);
   p->w_wcnt = Wl.add(4 * 2 * TW);
   p->ws_bytes = Wl.total;
 
@@ -376,6 +380,11 @@ static akv::Ws ws_ptrs(const anchorkv_plan* p, void* base) {
   w.sband = at<int32_t>(base, p->w_sband);
   w.sbscore = at<double>(base, p->w_sbscore);
   w.sstate = at<int32_t>(base, p->w_sstate);
+  w.sghist = at<uint32_t>(base, p->w_sghist);
+  w.scand = at<float>(base, p->w_scand);
+  w.rkey = at<unsigned long long>(base, p->w_rkey);
+  w.rpos = at<int32_t>(base, p->w_rpos);
+  w.slcnt = at<int32_t>(base, p->w_slcnt);
   w.QA = at<float>(base, p->w_QA);
   w.apos = at<int32_t>(base, p->w_apos);
   w.fixt = at<int32_t>(base, p->w_fix);
@@ -384,12 +393,11 @@ static akv::Ws ws_ptrs(const anchorkv_plan* p, void* base) {
   w.gpos = at<float>(base, p->w_gpos);
   w.u = at<float>(base, p->w_u);
   w.sel = at<uint8_t>(base, p->w_sel);
-  w.sflag = at<uint8_t>(base, p->w_sflag);
+  w.srec = at<uint4>(base, p->w_srec);
   w.bhist = at<uint32_t>(base, p->w_bhist);
   w.bstate = at<int32_t>(base, p->w_bstate);
   w.tiecnt = at<int32_t>(base, p->w_tiecnt);
   w.shist = at<int32_t>(base, p->w_shist);
-  w.scnt = at<int32_t>(base, p->w_scnt);
   w.wcnt = at<int32_t>(base, p->w_wcnt);
   return w;
 }
@@ -687,10 +695,12 @@ __global__ void k_init(Geo g, Cache c, Ws w) {
   }
   if (i < 4 * g.B) c.stats[i] = 0;
   if (i < 2 * g.H * g.B) w.fixcount[i] = 0;
-  if (i < g.H * g.B) w.scnt[i] = 0;
+  if (i < akv::SS_N * g.H * g.B) w.sstate[i] = 0;
+  if (i < 4096 * g.H * g.B) w.sghist[i] = 0u;
 }
 hipError_t launch_init(const Geo& g, const Cache& c, const Ws& w, hipStream_t st) {
-  const int n = 4 * g.B > 2 * g.H * g.B ? 4 * g.B : 2 * g.H * g.B;
+  int n = 4 * g.B > 2 * g.H * g.B ? 4 * g.B : 2 * g.H * g.B;
+  if (4096 * g.H * g.B > n) n = 4096 * g.H * g.B;
   launch("k_init", k_init, dim3((n + 255) / 256), dim3(256), 0, st, g, c, w);
   return hipGetLastError();
 }

@@ -43,6 +43,7 @@ __global__ __launch_bounds__(256) void k_epilogue(Geo g, Ws w, Cache c, const vo
   __shared__ float gK_s[EPI_TOK], rv2_s[EPI_TOK], vn_s[EPI_TOK];
   __shared__ int aK_s[EPI_TOK];
   __shared__ float sumK[4][EPI_TOK], sumV[4][EPI_TOK];
+  __shared__ __align__(16) float CVS[256], YVS[256];  // per observation row: softmax constant, ||y_w||^2
   extern __shared__ __align__(16) char qlds_raw[];  // the m observation rows, row stride LD
   E* QS = (E*)qlds_raw;
 
@@ -108,7 +109,7 @@ __global__ __launch_bounds__(256) void k_epilogue(Geo g, Ws w, Cache c, const vo
 #pragma unroll
         for (int j = 0; j < AKV_D; ++j) {
           const float x = Elem<DT>::get(xe, j);
-          const float r = x - gb * Elem<DT>::get(ae, j);
+          const float r = fmaf(-gb, Elem<DT>::get(ae, j), x);
           rs = fmaf(r, r, rs);
           vs = fmaf(x, x, vs);
         }
@@ -122,15 +123,21 @@ __global__ __launch_bounds__(256) void k_epilogue(Geo g, Ws w, Cache c, const vo
   // row rb*32 + l%32 of the fragments and owns the accumulator rows
   // rb*32 + crow(e, l) of token column l%32.
   const int nrb = (m + 31) / 32;
-  const float isd = 1.0f / sqrtf((float)D);
+  constexpr float LOG2E = 1.4426950408889634f;
+  const float isl = LOG2E / sqrtf((float)D);  // logit scale in base 2
   const float* oM = w.oM + (size_t)(b * g.H + h) * m;
   const float* oiZ = w.oiZ + (size_t)(b * g.H + h) * m;
   const float* yn = w.ynorm + (size_t)(b * g.H + h) * m;
   const float* QA = w.QA + ko * m;
+  // alpha = exp(l / sqrt(D) - M_w) / Z_w is taken as exp2(l log2(e) / sqrt(D)
+  // - c_w) with c_w = (M_w + ln Z_w) log2(e); rows past m get c_w = 1e30,
+  // hence alpha = 0.  c_w and ||y_w||^2 sit in LDS, the y fragments in
+  // registers.
+  for (int wr = threadIdx.x; wr < nrb * 32; wr += 256) {
+    CVS[wr] = wr < m ? (oM[wr] - __logf(oiZ[wr])) * LOG2E : 1e30f;
+    YVS[wr] = wr < m ? yn[wr] : 0.0f;
+  }
   typename M::frag yh[R][NKS], yl[R][DT ? NKS : 1];
-  // alpha = exp(l / sqrt(D) - M_w) / Z_w is taken as exp(l / sqrt(D) - c_w)
-  // with c_w = M_w + ln Z_w (one register per row).
-  float cv[R][16], yv[R][16];
 #pragma unroll
   for (int r = 0; r < R; ++r) {
     const int rb = wave + 4 * r;
@@ -145,12 +152,6 @@ __global__ __launch_bounds__(256) void k_epilogue(Geo g, Ws w, Cache c, const vo
       } else {
         yh[r][s] = w.Y[yo + k0];
       }
-    }
-#pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      const int wr = min(rb * 32 + crow(e, lane), m - 1);
-      cv[r][e] = oM[wr] - __logf(oiZ[wr]);
-      yv[r][e] = yn[wr];
     }
   }
   // Next tile's keys and values, 16-byte chunks (rows past S are zero).
@@ -183,11 +184,27 @@ __global__ __launch_bounds__(256) void k_epilogue(Geo g, Ws w, Cache c, const vo
     const int tl = 32 * it + (lane & 31);
     const int ak = aK_s[tl];
     const float gk = gK_s[tl], vn = vn_s[tl];
+    // The token's QA row (rows of accumulator entries 4j .. 4j+3 are
+    // consecutive) is read before the contraction, for every token (anchor 0
+    // stands in for an anchor position), so its latency overlaps the MFMAs.
+    const float* qa = QA + (size_t)max(ak, 0) * m;
     float tk = 0.0f, tv = 0.0f;
 #pragma unroll
     for (int r = 0; r < R; ++r) {
       const int rb = wave + 4 * r;
       if (rb >= nrb) break;
+      float qv[16];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int w0 = rb * 32 + j * 8 + (lane >> 5) * 4;
+        if ((m & 3) == 0) {
+          const float4 q4 = *(const float4*)(qa + min(w0, m - 4));
+          qv[4 * j] = q4.x; qv[4 * j + 1] = q4.y; qv[4 * j + 2] = q4.z; qv[4 * j + 3] = q4.w;
+        } else {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) qv[4 * j + i] = qa[min(w0 + i, m - 1)];
+        }
+      }
       f32x16 accL = {}, accY = {};
 #pragma unroll
       for (int s = 0; s < NKS; ++s) {
@@ -199,28 +216,21 @@ __global__ __launch_bounds__(256) void k_epilogue(Geo g, Ws w, Cache c, const vo
         if constexpr (DT == 1) accY = M::mma(yl[r][s], vb, accY);
       }
       if (ak >= 0) {
-        // Rows of accumulator entries 4j .. 4j+3 are consecutive.
-        const float* qa = QA + (size_t)ak * m;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           const int w0 = rb * 32 + j * 8 + (lane >> 5) * 4;
-          float qv[4];
-          if ((m & 3) == 0 && w0 < m) {
-            const float4 q4 = *(const float4*)(qa + w0);
-            qv[0] = q4.x; qv[1] = q4.y; qv[2] = q4.z; qv[3] = q4.w;
-          } else {
-#pragma unroll
-            for (int i = 0; i < 4; ++i) qv[i] = qa[min(w0 + i, m - 1)];
-          }
+          const float4 c4 = *(const float4*)&CVS[w0];
+          const float4 y4 = *(const float4*)&YVS[w0];
+          const float cq[4] = {c4.x, c4.y, c4.z, c4.w}, yq[4] = {y4.x, y4.y, y4.z, y4.w};
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
             const int e = 4 * j + i;
             const float l = accL[e];
-            const float al = __expf(l * isd - cv[r][e]);
-            const float a2 = w0 + i < m ? al * al : 0.0f;
-            const float qr = l - gk * qv[i];
-            const float vv = vn - 2.0f * accY[e] + yv[r][e];
-            tk += a2 * (qr * qr) * vv;
+            const float al = __builtin_amdgcn_exp2f(fmaf(l, isl, -cq[i]));
+            const float a2 = al * al;
+            const float qr = fmaf(-gk, qv[e], l);
+            const float vv = fmaf(-2.0f, accY[e], vn + yq[i]);
+            tk = fmaf(a2 * vv, qr * qr, tk);
             tv += a2;
           }
         }

@@ -18,8 +18,9 @@
 //                table's last row;
 //   k_sscatter : per chunk, the anchors' start slots (scan of the totals plus
 //                the column prefix), then a stable scatter of the chunk's
-//                tokens 64 at a time, writing each token's record at its slot;
-//   k_lrec     : flag words and popcounts per sorted slot;
+//                tokens 64 at a time, one 16-byte record per token;
+//   k_lrec     : per sorted slot, the record spread over the layout's arrays,
+//                flag words and popcounts;
 //   k_lscan    : per request and side, slot bases of every word;
 //   k_codec    : one wave per flagged token: r = x - gamma * abar (fp32),
 //                z = FWHT(s * r), per-group scale, 2-bit codes packed four per
@@ -66,15 +67,8 @@ __global__ __launch_bounds__(256) void k_shist(Geo g, Ws w) {
 // One thread per (request, head, anchor): the anchor's column of chunk counts
 // becomes its exclusive prefix sum in place (the counts of its tokens in the
 // earlier chunks), and its total goes to row nT; loads are issued 32 rows at
-// a time.  The last workgroup of a head to finish (a per-head counter) turns
-// row nT into the exclusive prefix of the totals, the anchors' first slots:
-// up to 16 tiles of 256 totals per round, all loaded before the wave scans
-// and one scan of the (tile, wave) sums.
+// a time.
 __global__ __launch_bounds__(256) void k_sscan(Geo g, Ws w) {
-  constexpr int TU = 16;
-  __shared__ int wsum[TU * 4];
-  __shared__ int wpre[TU * 4 + 1];
-  __shared__ int last;
   int idx = blockIdx.x;
   int b = 0;
   for (; b < g.B; ++b) {
@@ -86,70 +80,21 @@ __global__ __launch_bounds__(256) void k_sscan(Geo g, Ws w) {
   const int nT = (g.S[b] + SORT_CHUNK - 1) / SORT_CHUNK;
   const int nab = (k + 255) / 256;
   const int h = idx / nab, a = (idx % nab) * 256 + threadIdx.x;
-  int32_t* tab = shist_base(g, w, b, h);
-  if (a < k) {
-    int32_t* col = tab + a;
-    constexpr int U = 32;
-    int s = 0;
-    for (int c0 = 0; c0 < nT; c0 += U) {
-      int v[U];
+  if (a >= k) return;
+  int32_t* col = shist_base(g, w, b, h) + a;
+  constexpr int U = 32;
+  int s = 0;
+  for (int c0 = 0; c0 < nT; c0 += U) {
+    int v[U];
 #pragma unroll
-      for (int u = 0; u < U; ++u) v[u] = c0 + u < nT ? col[(size_t)(c0 + u) * k] : 0;
+    for (int u = 0; u < U; ++u) v[u] = c0 + u < nT ? col[(size_t)(c0 + u) * k] : 0;
 #pragma unroll
-      for (int u = 0; u < U; ++u) {
-        if (c0 + u < nT) col[(size_t)(c0 + u) * k] = s;
-        s += v[u];
-      }
+    for (int u = 0; u < U; ++u) {
+      if (c0 + u < nT) col[(size_t)(c0 + u) * k] = s;
+      s += v[u];
     }
-    col[(size_t)nT * k] = s;
   }
-  __threadfence();
-  __syncthreads();
-  if (threadIdx.x == 0) last = atomicAdd(&w.scnt[b * g.H + h], 1) == nab - 1;
-  __syncthreads();
-  if (!last) return;
-  __threadfence();
-  int32_t* tot = tab + (size_t)nT * k;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  int carry = 0;
-  for (int a0 = 0; a0 < k; a0 += TU * 256) {
-    int v[TU], x[TU];
-#pragma unroll
-    for (int u = 0; u < TU; ++u) {
-      const int i = a0 + u * 256 + threadIdx.x;
-      v[u] = i < k ? tot[i] : 0;
-    }
-#pragma unroll
-    for (int u = 0; u < TU; ++u) {
-      x[u] = v[u];
-#pragma unroll
-      for (int o = 1; o < 64; o <<= 1) {
-        const int y = __shfl_up(x[u], o, 64);
-        if (lane >= o) x[u] += y;
-      }
-      if (lane == 63) wsum[u * 4 + wave] = x[u];
-    }
-    __syncthreads();
-    if (wave == 0) {
-      const int c = wsum[lane];
-      int y = c;
-#pragma unroll
-      for (int o = 1; o < 64; o <<= 1) {
-        const int z = __shfl_up(y, o, 64);
-        if (lane >= o) y += z;
-      }
-      wpre[lane] = y - c;
-      if (lane == 63) wpre[TU * 4] = y;
-    }
-    __syncthreads();
-#pragma unroll
-    for (int u = 0; u < TU; ++u) {
-      const int i = a0 + u * 256 + threadIdx.x;
-      if (i < k) tot[i] = carry + wpre[u * 4 + wave] + x[u] - v[u];
-    }
-    carry += wpre[TU * 4];
-    __syncthreads();
-  }
+  col[(size_t)nT * k] = s;
 }
 
 // One workgroup per chunk.  The anchors' start slots for this chunk (first
@@ -159,11 +104,13 @@ __global__ __launch_bounds__(256) void k_sscan(Geo g, Ws w) {
 // order.  Lanes holding the same anchor find each other with one ballot per
 // bit of the anchor index; a token's slot is its anchor's start plus the
 // equal tokens before it in the group, and the group's last such lane
-// advances the start.  The token's record is written at its slot, so the
-// records are read in position order and only the writes scatter.
+// advances the start.  The token's record goes to its slot as one 16-byte
+// write, so the records are read in position order and each token costs one
+// scattered write; k_lrec then spreads them over the layout's arrays.
 template <int DT>
 __global__ __launch_bounds__(256) void k_sscatter(Geo g, Ws w, Cache c) {
   extern __shared__ __align__(16) int lds[];
+  __shared__ int wsum[64], wpre[65];
   int* sa = lds;                       // [SORT_CHUNK] value-side anchor
   int* ska = sa + SORT_CHUNK;          // [SORT_CHUNK] key-side anchor
   float* sgk = (float*)(ska + SORT_CHUNK);
@@ -181,13 +128,11 @@ __global__ __launch_bounds__(256) void k_sscatter(Geo g, Ws w, Cache c) {
   const int32_t* first = tab + (size_t)nT * k;
   const int32_t* colp = tab + (size_t)ch * k;
   const size_t TS = (size_t)g.prefS[g.B] * g.H;
-  const size_t TSP = (size_t)g.prefW[g.B] * g.H * 64;
   const size_t po = (size_t)g.prefS[b] * g.H + (size_t)h * S;
   const size_t so = slot_base(g, b, h);
   const int t0 = ch * SORT_CHUNK, t1 = min(S, t0 + SORT_CHUNK), nt = t1 - t0;
   constexpr int RU = SORT_CHUNK / 256;
   {
-    int f[RU];
     float gk[RU], gv[RU];
     int ak[RU], av[RU];
     uint8_t fk[RU], fv[RU];
@@ -201,15 +146,49 @@ __global__ __launch_bounds__(256) void k_sscatter(Geo g, Ws w, Cache c) {
       fk[u] = w.sel[po + t0 + i];
       fv[u] = w.sel[TS + po + t0 + i];
     }
-    for (int a0 = 0; a0 < k; a0 += 256 * RU) {
+    // First slot of each anchor: exclusive scan of the anchor totals, up to
+    // TU tiles of 256 per round (all loaded before the wave scans, then one
+    // scan of the (tile, wave) sums); plus the column prefix of this chunk.
+    constexpr int TU = 16;
+    int carry = 0;
+    for (int a0 = 0; a0 < k; a0 += TU * 256) {
+      int v[TU], x[TU], cp[TU];
 #pragma unroll
-      for (int u = 0; u < RU; ++u) {
-        const int a = min(a0 + u * 256 + tid, k - 1);
-        f[u] = first[a] + colp[a];
+      for (int u = 0; u < TU; ++u) {
+        const int a = a0 + u * 256 + tid;
+        v[u] = a < k ? first[a] : 0;
+        cp[u] = a < k ? colp[a] : 0;
       }
 #pragma unroll
-      for (int u = 0; u < RU; ++u)
-        if (a0 + u * 256 + tid < k) run[a0 + u * 256 + tid] = f[u];
+      for (int u = 0; u < TU; ++u) {
+        x[u] = v[u];
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+          const int y = __shfl_up(x[u], o, 64);
+          if (lane >= o) x[u] += y;
+        }
+        if (lane == 63) wsum[u * 4 + (tid >> 6)] = x[u];
+      }
+      __syncthreads();
+      if (tid < 64) {
+        const int c0 = wsum[lane];
+        int y = c0;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+          const int z = __shfl_up(y, o, 64);
+          if (lane >= o) y += z;
+        }
+        wpre[lane] = y - c0;
+        if (lane == 63) wpre[TU * 4] = y;
+      }
+      __syncthreads();
+#pragma unroll
+      for (int u = 0; u < TU; ++u) {
+        const int a = a0 + u * 256 + tid;
+        if (a < k) run[a] = carry + wpre[u * 4 + (tid >> 6)] + x[u] - v[u] + cp[u];
+      }
+      carry += wpre[TU * 4];
+      __syncthreads();
     }
 #pragma unroll
     for (int u = 0; u < RU; ++u) {
@@ -240,24 +219,21 @@ __global__ __launch_bounds__(256) void k_sscatter(Geo g, Ws w, Cache c) {
     if (a >= 0) {
       const int dest = run[a] + before;
       if (dest >= 0 && dest < S) {
-        const size_t o = so + dest;
-        c.pos[o] = t0 + i;
-        c.idxK[o] = (uint16_t)ska[i];
-        c.idxV[o] = (uint16_t)a;
-        Elem<DT>::put(c.gK, o, sgk[i]);
-        Elem<DT>::put(c.gV, o, sgv[i]);
-        w.sflag[o] = sfk[i];
-        w.sflag[TSP + o] = sfv[i];
+        // One 16-byte record per token: position with the residual flags in
+        // bits 30 and 31, the two anchor indices, the two coefficients.
+        const uint32_t w0 = (uint32_t)(t0 + i) | (sfk[i] ? 1u << 30 : 0u) | (sfv[i] ? 1u << 31 : 0u);
+        const uint32_t w1 = (uint32_t)(uint16_t)ska[i] | ((uint32_t)a << 16);
+        w.srec[so + dest] = make_uint4(w0, w1, __float_as_uint(sgk[i]), __float_as_uint(sgv[i]));
       }
       if (lastp) run[a] = dest + 1;
     }
   }
 }
 
-// Per 256 sorted slots: residual flag words and their popcounts from the
-// slot-order flags; a slot holding an out-of-range position raises the layout
-// error bit.  Padding slots of the head's last word get anchor 0 with
-// coefficient 0.
+// Per 256 sorted slots: the records become the layout's per-slot arrays,
+// and the residual flag words and their popcounts; a slot holding an
+// out-of-range position raises the layout error bit.  Padding slots of the
+// head's last word get anchor 0 with coefficient 0.
 template <int DT>
 __global__ __launch_bounds__(256) void k_lrec(Geo g, Ws w, Cache c) {
   int idx = blockIdx.x;
@@ -266,13 +242,18 @@ __global__ __launch_bounds__(256) void k_lrec(Geo g, Ws w, Cache c) {
   const int nt = (S + 255) / 256;
   const int h = idx / nt, i = (idx % nt) * 256 + threadIdx.x;
   const size_t so = slot_base(g, b, h);
-  const size_t TSP = (size_t)g.prefW[g.B] * g.H * 64;
   bool fk = false, fv = false;
   if (i < S) {
-    const int t = c.pos[so + i];
-    if (t < 0 || t >= S) atomicOr(&c.header[2], 8u);
-    fk = w.sflag[so + i] != 0;
-    fv = w.sflag[TSP + so + i] != 0;
+    const uint4 r = w.srec[so + i];
+    const int t = (int)(r.x & 0x3FFFFFFFu);
+    if (t >= S) atomicOr(&c.header[2], 8u);
+    fk = (r.x >> 30) & 1u;
+    fv = r.x >> 31;
+    c.pos[so + i] = t;
+    c.idxK[so + i] = (uint16_t)(r.y & 0xFFFFu);
+    c.idxV[so + i] = (uint16_t)(r.y >> 16);
+    Elem<DT>::put(c.gK, so + i, __uint_as_float(r.z));
+    Elem<DT>::put(c.gV, so + i, __uint_as_float(r.w));
   } else if (i < ((S + 63) & ~63)) {
     c.pos[so + i] = 0;
     c.idxK[so + i] = 0;

@@ -1,14 +1,31 @@
 // Anchor selection (Sec. 3.2 "Anchor selection"; App. A.2 Eq. selector-score;
 // Algorithm 1, first step) and anchor preparation.
-//   k_select      : one workgroup per (request, head).  Average-pools the
-//                   observation score over kappa positions (zero padding,
-//                   divided by kappa), takes the floor(rho (k - W)) best pooled
-//                   positions of [0, S - W) (ties to the lower position) by an
-//                   exact radix select on the fp32 bits, samples the rest of the
-//                   non-window budget uniformly without replacement (the
-//                   positions with the smallest SplitMix64 hash), adds the
-//                   window and writes the ascending anchor list and the
-//                   position -> anchor-index map.
+//
+// Selection: average-pool the observation score over kappa positions (zero
+// padding, divided by kappa), take the floor(rho (k - W)) best pooled
+// positions of [0, S - W) (ties to the lower position) by an exact radix
+// select on the fp32 bits, sample the rest of the non-window budget uniformly
+// without replacement (the positions with the smallest SplitMix64 hash), add
+// the window, and write the ascending anchor list and the position ->
+// anchor-index map.  Every pass runs on SEL_SLICE-position slices of all
+// (request, head) pairs at once.  A decision that needs a whole head (a digit
+// of the radix select, the exact cut among candidates, the ranking of hash
+// candidates) is taken by every workgroup of the next pass from the totals
+// and lists the previous pass left in memory (the kernel boundary publishes
+// them), so no workgroup waits for another:
+//   k_sel_pool  : marks reset, pooled scores, histogram of their first 12-bit
+//                 digit;
+//   k_sel_cand  : the digit of the n_top-th largest; scores inside its bin
+//                 appended as candidates;
+//   k_sel_class : the exact cut (remaining two digits) among the candidates;
+//                 positions clearly above it taken, the band around it listed
+//                 for the fp64 re-scoring (k_sel_band);
+//   k_sel_rhist : band decisions (fp32 order on a band overflow), histogram of
+//                 the hash's top 12 bits over the untaken positions;
+//   k_sel_rcand : the bin of the n_rand-th smallest key; keys below it taken,
+//                 keys inside it appended; per-slice anchor counts;
+//   k_sel_list  : the bin's keys ranked and the smallest taken; the anchor
+//                 list and the map, slices placed by the counts.
 //   k_anchor_prep : copies anchor keys/values into the cache, their canonical
 //                   fp64 squared norms and fp32 inverse norms, and the table
 //                   QA[a][w] = q_w . abar^K_a used by the key utilities.
@@ -74,8 +91,8 @@ __global__ __launch_bounds__(256) void k_sel_band(Geo g, Ws w, const void* Kin, 
   __shared__ double part[256 * 2];
   const int bh = blockIdx.x / SEL_BAND_MAX, i = blockIdx.x % SEL_BAND_MAX;
   const int b = bh / g.H, h = bh % g.H;
-  const int nb = w.sstate[bh * 4 + 3];
-  if (i >= nb) return;  // also an overflowed band (nb < 0)
+  const int nb = w.sstate[bh * SS_N + SS_NBAND];
+  if (i >= nb || nb > SEL_BAND_MAX) return;  // past the band, or an overflowed band
   const int S = g.S[b], P = S - g.W, m = g.m;
   const int tid = threadIdx.x, nt = blockDim.x, half = g.kappa / 2, nk = 2 * half + 1;
   const int t = w.sband[(size_t)bh * SEL_BAND_MAX + i];
@@ -157,9 +174,7 @@ __device__ inline void digit_pick(const uint32_t* hist, int nbin, int need, bool
 }
 
 constexpr int SEL_NBIN = 4096;  // 12-bit radix digits
-constexpr int SEL_TILE = 3840;  // pooled positions per LDS tile (tile + halo fit the histogram)
 constexpr int SEL_HALO = 254;   // 2 * (kappa / 2) for kappa <= 255
-constexpr int SEL_CAND = 1024;  // hash candidates kept in the last digit's bin
 constexpr int SEL_U = 8;        // elements per thread per batch (independent loads)
 
 // Passes over [0, n) visit t = t0 + u * nt (u < SEL_U) per batch: coalesced
@@ -169,272 +184,375 @@ __device__ inline void sel_batches(int n, F&& body) {
   for (int t0 = threadIdx.x; t0 < n; t0 += SEL_U * blockDim.x) body(t0);
 }
 
-// Selection, first half (one workgroup per request and head): marks reset,
-// pooled scores, the exact n_top-th largest pooled fp32 value, the positions
-// clearly above it (taken) and the band around it, whose members k_sel_band
-// re-scores in fp64.  An anchor override replaces the selection.
-template <int DT>
-__global__ __launch_bounds__(1024) void k_sel_top(Geo g, Ws w, Cache c, const int32_t* ovr) {
-  __shared__ uint32_t hist[SEL_NBIN];
-  __shared__ int tmp[20];
-  __shared__ int pick[2];
-  __shared__ int nband, nabove;
-  const int bh = blockIdx.x, b = bh / g.H, h = bh % g.H;
-  const int S = g.S[b], W = g.W, P = S - W, k = g.k[b];
-  const size_t so = (size_t)g.prefS[b] * g.H + (size_t)h * S;
-  int32_t* rank = w.rank + so;
-  uint8_t* flag = w.flag + so;
-  const float* sc = w.sc + so;
-  float* pooled = w.u + so;  // the utility buffer is free until the epilogue
-  int32_t* anc = c.anc_pos + (size_t)g.prefK[b] * g.H + (size_t)h * k;
-  int32_t* st = w.sstate + bh * 4;  // prefix, remaining, nabove, nband (-1: none / overflow)
-  const int tid = threadIdx.x, nt = blockDim.x;
+// ------------------------------------------------------------------ slice passes
+// Slice sl of (request b, head h): positions [sl * SEL_SLICE, ...) of [0, S).
+struct SelSlice {
+  int b, h, bh, sl, nsl, S, P, k, t0, t1;  // [t0, t1) = the slice's part of [0, P)
+  size_t so;                                // offset of the head's position arrays
+};
+__device__ inline SelSlice sel_slice(const Geo& g) {
+  SelSlice q;
+  int idx = blockIdx.x;
+  q.b = locate(g, SEL_SLICE, 1, idx);
+  q.S = g.S[q.b];
+  q.P = q.S - g.W;
+  q.k = g.k[q.b];
+  q.nsl = (q.S + SEL_SLICE - 1) / SEL_SLICE;
+  q.h = idx / q.nsl;
+  q.sl = idx % q.nsl;
+  q.bh = q.b * g.H + q.h;
+  q.t0 = q.sl * SEL_SLICE;
+  q.t1 = min(q.P, q.t0 + SEL_SLICE);
+  q.so = (size_t)g.prefS[q.b] * g.H + (size_t)q.h * q.S;
+  return q;
+}
 
-  sel_batches(S, [&](int t0) {
+// Appends the lanes' `take` values to a per-head list: one atomic per wave.
+// Returns the slot (or -1 for lanes that append nothing).
+__device__ inline int wave_append(bool take, int32_t* count) {
+  const unsigned long long bal = __ballot(take);
+  if (!bal) return -1;
+  const int lane = threadIdx.x & 63;
+  const int leader = __ffsll((long long)bal) - 1;
+  int base = 0;
+  if (lane == leader) base = atomicAdd(count, __popcll(bal));
+  base = __shfl(base, leader, 64);
+  return take ? base + __popcll(bal & ((1ull << lane) - 1ull)) : -1;
+}
+
+// Radix digit histogram of `nbin` bins over the values v with (v & pmask) ==
+// prefix, into LDS hist (zeroed here); whole workgroup.
+template <typename F>
+__device__ inline void digit_hist(uint32_t* hist, int nbin, int n, F&& value, uint32_t pmask, uint32_t prefix,
+                                  int shift) {
+  for (int i = threadIdx.x; i < nbin; i += blockDim.x) hist[i] = 0;
+  __syncthreads();
+  sel_batches(n, [&](int t0) {
+    uint32_t v[SEL_U];
 #pragma unroll
-    for (int u = 0; u < SEL_U; ++u) {
-      const int t = t0 + u * nt;
-      if (t < S) {
-        rank[t] = -1;
-        flag[t] = 0;
-      }
-    }
+    for (int u = 0; u < SEL_U; ++u) v[u] = t0 + u * (int)blockDim.x < n ? value(t0 + u * blockDim.x) : 0u;
+#pragma unroll
+    for (int u = 0; u < SEL_U; ++u)
+      if (t0 + u * (int)blockDim.x < n && (v[u] & pmask) == prefix) atomicAdd(&hist[(v[u] >> shift) & (nbin - 1)], 1u);
   });
-  if (tid == 0) st[3] = -1;
   __syncthreads();
-  if (ovr) {
-    const int32_t* o = ovr + (size_t)g.prefK[b] * g.H + (size_t)h * k;
-    bool bad = false;
-    for (int a = tid; a < k; a += nt) {
-      int p = o[a];
-      bool ok = p >= 0 && p < S && (a == 0 || o[a - 1] < p) && (a < k - W || p == P + (a - (k - W)));
-      if (!ok) bad = true;
-      anc[a] = p;
-      if (p >= 0 && p < S) rank[p] = a;
-    }
-    if (bad) atomicOr(&c.header[2], 1u);
-    return;
-  }
+}
 
-  // Average pooling of width kappa over [0, P), zero padded, divided by kappa
-  // (terms added in offset order, from -kappa/2), in tiles of SEL_TILE
-  // positions staged through LDS with their halo; the next tile's values are
-  // loaded while the current one is pooled.
+// The bin of a head's summed histogram where the running count (from the
+// top when `desc`) reaches `need`, and the count before it; whole workgroup.
+__device__ inline void pick_global(const uint32_t* gh, uint32_t* hist, int need, bool desc, int* tmp, int* pick) {
+  for (int i = threadIdx.x; i < SEL_NBIN; i += blockDim.x) hist[i] = gh[i];
+  __syncthreads();
+  digit_pick(hist, SEL_NBIN, need, desc, tmp, pick);
+}
+
+// Marks reset over the slice's positions of [0, S), pooled scores over its
+// part of [0, P) (the scores with their halo staged in LDS; terms added in
+// offset order from -kappa/2), and the histogram of their first digit
+// [31:20] (non-negative scores order as their bits) added to the head's.
+__global__ __launch_bounds__(256) void k_sel_pool(Geo g, Ws w, int override_anchors) {
+  __shared__ uint32_t hist[SEL_NBIN];
+  __shared__ float stile[SEL_SLICE + SEL_HALO];
+  const SelSlice q = sel_slice(g);
+  const int tid = threadIdx.x, nt = blockDim.x;
+  int32_t* rank = w.rank + q.so;
+  uint8_t* flag = w.flag + q.so;
+  for (int t = q.t0 + tid; t < min(q.S, q.t0 + SEL_SLICE); t += nt) {
+    rank[t] = -1;
+    flag[t] = 0;
+  }
+  if (override_anchors) return;
   const int half = g.kappa / 2;
-  {
-    float* stile = (float*)hist;  // the histogram is not in use yet
-    constexpr int TV = (SEL_TILE + SEL_HALO + 1023) / 1024;  // staged values per thread
-    float nxt[TV];
-    auto load_tile = [&](int c0) {
-#pragma unroll
-      for (int i = 0; i < TV; ++i) {
-        const int j = tid + i * nt, u = c0 - half + j;
-        nxt[i] = (j < SEL_TILE + 2 * half && u >= 0 && u < P) ? sc[u] : 0.0f;
-      }
-    };
-    load_tile(0);
-    for (int c0 = 0; c0 < P; c0 += SEL_TILE) {
-      __syncthreads();
-#pragma unroll
-      for (int i = 0; i < TV; ++i) {
-        const int j = tid + i * nt;
-        if (j < SEL_TILE + 2 * half) stile[j] = nxt[i];
-      }
-      __syncthreads();
-      if (c0 + SEL_TILE < P) load_tile(c0 + SEL_TILE);
-      for (int t = tid; t < SEL_TILE && c0 + t < P; t += nt) {
-        float s = 0.0f;
-        for (int d = 0; d <= 2 * half; ++d) s += stile[t + d];
-        pooled[c0 + t] = s / (float)g.kappa;
-      }
-    }
+  const float* sc = w.sc + q.so;
+  float* pooled = w.u + q.so;  // the utility buffer is free until the epilogue
+  const int ntile = q.t1 - q.t0 + 2 * half;
+  for (int j = tid; j < ntile; j += nt) {
+    const int u = q.t0 - half + j;
+    stile[j] = (u >= 0 && u < q.P) ? sc[u] : 0.0f;
+  }
+  for (int i = tid; i < SEL_NBIN; i += nt) hist[i] = 0;
+  __syncthreads();
+  const int ntop = g.ntop[q.b];
+  for (int t = q.t0 + tid; t < q.t1; t += nt) {
+    float s = 0.0f;
+    for (int d = 0; d <= 2 * half; ++d) s += stile[t - q.t0 + d];
+    const float v = s / (float)g.kappa;
+    pooled[t] = v;
+    if (ntop > 0) atomicAdd(&hist[__float_as_uint(v) >> 20], 1u);
   }
   __syncthreads();
+  uint32_t* gh = w.sghist + (size_t)q.bh * SEL_NBIN;
+  if (ntop > 0)
+    for (int i = tid; i < SEL_NBIN; i += nt)
+      if (hist[i]) atomicAdd(&gh[i], hist[i]);
+}
 
-  // ---- top n_top by pooled score, ties to the lower position: radix select
-  // on the fp32 bits (non-negative scores order as their bits), digits
-  // [31:20], [19:8], [7:0].
-  const int ntop = g.ntop[b];
+// The first digit of the n_top-th largest score and the count above its bin
+// (every workgroup, from the head's histogram); the slice's scores inside
+// the bin are appended as candidates.
+__global__ __launch_bounds__(256) void k_sel_cand(Geo g, Ws w) {
+  __shared__ uint32_t hist[SEL_NBIN];
+  __shared__ int tmp[8], pick[2];
+  const SelSlice q = sel_slice(g);
+  const int ntop = g.ntop[q.b];
   if (ntop <= 0) return;
-  uint32_t prefix = 0, pmask = 0;
-  int remaining = ntop;
-  for (int pass = 0; pass < 3; ++pass) {
-    const int shift = pass == 0 ? 20 : (pass == 1 ? 8 : 0);
-    const int nbin = pass == 2 ? 256 : SEL_NBIN;
-    for (int i = tid; i < nbin; i += nt) hist[i] = 0;
-    __syncthreads();
-    sel_batches(P, [&](int t0) {
-      uint32_t v[SEL_U];
-#pragma unroll
-      for (int u = 0; u < SEL_U; ++u) v[u] = t0 + u * nt < P ? __float_as_uint(pooled[t0 + u * nt]) : 0u;
-#pragma unroll
-      for (int u = 0; u < SEL_U; ++u)
-        if (t0 + u * nt < P && (v[u] & pmask) == prefix) atomicAdd(&hist[(v[u] >> shift) & (nbin - 1)], 1u);
-    });
-    __syncthreads();
+  const int tid = threadIdx.x;
+  int32_t* st = w.sstate + q.bh * SS_N;
+  pick_global(w.sghist + (size_t)q.bh * SEL_NBIN, hist, ntop, true, tmp, pick);
+  const uint32_t bin1 = (uint32_t)pick[0];
+  if (q.sl == 0 && tid == 0) {
+    st[SS_BIN1] = pick[0];
+    st[SS_ABOVE1] = pick[1];
+  }
+  const float* pooled = w.u + q.so;
+  float* cand = w.scand + (size_t)q.bh * SEL_CMAX;
+  for (int t0 = q.t0; t0 < q.t1; t0 += blockDim.x) {
+    const int t = t0 + tid;
+    const float v = t < q.t1 ? pooled[t] : 0.0f;
+    const bool take = t < q.t1 && (__float_as_uint(v) >> 20) == bin1;
+    const int slot = wave_append(take, &st[SS_NCAND]);
+    if (slot >= 0 && slot < SEL_CMAX) cand[slot] = v;
+  }
+}
+
+// The exact cut (every workgroup): digits [19:8] and [7:0] of the n_top-th
+// largest score and the count still to take among scores equal to it, from
+// the candidate list or, when it overflowed, from all of [0, P) (same
+// digits, same result).  Then the slice's scores clearly above the band
+// around the cut are taken and the band's members listed.
+__global__ __launch_bounds__(256) void k_sel_class(Geo g, Ws w) {
+  __shared__ uint32_t hist[SEL_NBIN];
+  __shared__ int tmp[8], pick[2];
+  const SelSlice q = sel_slice(g);
+  const int ntop = g.ntop[q.b];
+  if (ntop <= 0) return;
+  const int tid = threadIdx.x, nt = blockDim.x;
+  int32_t* st = w.sstate + q.bh * SS_N;
+  const float* pooled = w.u + q.so;
+  const float* cand = w.scand + (size_t)q.bh * SEL_CMAX;
+  const int nc = st[SS_NCAND];
+  int remaining = ntop - st[SS_ABOVE1];
+  uint32_t prefix = (uint32_t)st[SS_BIN1] << 20, pmask = 0xFFF00000u;
+  for (int pass = 0; pass < 2; ++pass) {
+    const int shift = pass == 0 ? 8 : 0, nbin = pass == 0 ? SEL_NBIN : 256;
+    if (nc <= SEL_CMAX)
+      digit_hist(hist, nbin, nc, [&](int i) { return __float_as_uint(cand[i]); }, pmask, prefix, shift);
+    else
+      digit_hist(hist, nbin, q.P, [&](int t) { return __float_as_uint(pooled[t]); }, pmask, prefix, shift);
     digit_pick(hist, nbin, remaining, true, tmp, pick);
     remaining -= pick[1];
     prefix |= (uint32_t)pick[0] << shift;
     pmask |= (uint32_t)(nbin - 1) << shift;
     __syncthreads();
   }
-  // prefix is the bit pattern of the n_top-th largest fp32 score.  Scores
-  // clearly above the band are taken; inside the band the decision uses the
-  // fp64 scores (ties to the lower position).
+  if (q.sl == 0 && tid == 0) {
+    st[SS_PREFIX] = (int)prefix;
+    st[SS_REMAIN] = remaining;
+  }
+  // The head's histogram is read by no later workgroup of this pass; clear it
+  // for the hash histogram.
+  if (q.sl == 0)
+    for (int i = tid; i < SEL_NBIN; i += nt) w.sghist[(size_t)q.bh * SEL_NBIN + i] = 0u;
   const float cut = __uint_as_float(prefix);
   const float bhi = cut * (1.0f + SEL_BAND), blo = cut * (1.0f - SEL_BAND);
-  if (tid == 0) {
-    nband = 0;
-    nabove = 0;
-  }
-  __syncthreads();
-  int32_t* band = w.sband + (size_t)bh * SEL_BAND_MAX;
-  sel_batches(P, [&](int t0) {
-    float v[SEL_U];
-#pragma unroll
-    for (int u = 0; u < SEL_U; ++u) v[u] = t0 + u * nt < P ? pooled[t0 + u * nt] : -1.0f;
-#pragma unroll
-    for (int u = 0; u < SEL_U; ++u) {
-      const int t = t0 + u * nt;
-      if (t >= P) continue;
-      if (v[u] > bhi) {
-        atomicAdd(&nabove, 1);
-        flag[t] = 1;
-      } else if (v[u] >= blo) {
-        const int i = atomicAdd(&nband, 1);
-        if (i < SEL_BAND_MAX) band[i] = t;
-      }
+  uint8_t* flag = w.flag + q.so;
+  int32_t* band = w.sband + (size_t)q.bh * SEL_BAND_MAX;
+  int above = 0;
+  for (int t0 = q.t0; t0 < q.t1; t0 += nt) {
+    const int t = t0 + tid;
+    const float v = t < q.t1 ? pooled[t] : -1.0f;
+    if (v > bhi) {
+      flag[t] = 1;
+      ++above;
     }
-  });
-  __syncthreads();
-  const int nb = nband;
-  if (nb > SEL_BAND_MAX) {
-    // Band overflow: the fp32 order decides (ties to the lower position).
-    if (tid == 0) atomicOr(&c.header[2], 32u);
-    const int per = (P + nt - 1) / nt;
-    const int lo = min(P, tid * per), hi = min(P, lo + per);
-    for (int t = lo; t < hi; ++t) flag[t] = 0;
-    __syncthreads();
-    int eq = 0;
-    for (int t = lo; t < hi; ++t) eq += (__float_as_uint(pooled[t]) == prefix);
-    int tot;
-    int before = block_excl_scan(eq, tmp, tot);
-    for (int t = lo; t < hi; ++t) {
-      uint32_t u = __float_as_uint(pooled[t]);
-      if (u > prefix) {
-        flag[t] = 1;
-      } else if (u == prefix) {
-        if (before < remaining) flag[t] = 1;
-        ++before;
-      }
-    }
-  } else if (tid == 0) {
-    st[0] = (int)prefix;
-    st[1] = remaining;
-    st[2] = nabove;
-    st[3] = nb;
+    const int slot = wave_append(v <= bhi && v >= blo, &st[SS_NBAND]);
+    if (slot >= 0 && slot < SEL_BAND_MAX) band[slot] = t;
   }
+  above = wave_sum_i(above);
+  if ((tid & 63) == 0 && above) atomicAdd(&st[SS_NABOVE], above);
 }
 
-// Selection, second half: the band members ranked by their fp64 scores, the
-// uniform share (the n_rand unflagged positions with the smallest SplitMix64
-// key: the top 12 bits locate the bin holding the n_rand-th smallest key, keys
-// below it are taken, the keys inside it are ranked exactly; keys are
-// distinct since SplitMix64 is a bijection), and the ascending anchor list
-// with the position -> anchor-index map.
-template <int DT>
-__global__ __launch_bounds__(1024) void k_sel_rest(Geo g, Ws w, Cache c, const int32_t* ovr) {
+// Band decisions for the slice's members: rank by fp64 score (ties to the
+// lower position) against all members.  On a band overflow the fp32 order
+// decides instead: scores above the cut are taken, and of those equal to it
+// the first `remaining` in position order (equal scores in earlier slices
+// counted here).  Then the histogram of the hash's top 12 bits over the
+// slice's untaken positions is added to the head's.
+__global__ __launch_bounds__(256) void k_sel_rhist(Geo g, Ws w, Cache c) {
   __shared__ uint32_t hist[SEL_NBIN];
-  __shared__ int tmp[20];
-  __shared__ int pick[2];
-  __shared__ unsigned long long ckey[SEL_CAND];
-  __shared__ int cpos[SEL_CAND];
-  __shared__ int ncand;
-  __shared__ int cnts[SEL_U * 16];     // flags per (u, wave) of a batch (16 waves of 1024 threads)
-  __shared__ int cpre[SEL_U * 16 + 1];  // their exclusive prefix, then the batch total
-  if (ovr) return;
-  const int bh = blockIdx.x, b = bh / g.H, h = bh % g.H;
-  const int S = g.S[b], W = g.W, P = S - W, k = g.k[b];
-  const size_t so = (size_t)g.prefS[b] * g.H + (size_t)h * S;
-  int32_t* rank = w.rank + so;
-  uint8_t* flag = w.flag + so;
-  int32_t* anc = c.anc_pos + (size_t)g.prefK[b] * g.H + (size_t)h * k;
+  __shared__ uint8_t sflag[SEL_SLICE];
+  __shared__ int tmp[8];
+  const SelSlice q = sel_slice(g);
   const int tid = threadIdx.x, nt = blockDim.x;
-
-  const int nb = w.sstate[bh * 4 + 3];
-  if (nb > 0) {
-    const int need = g.ntop[b] - w.sstate[bh * 4 + 2];
-    const int32_t* band = w.sband + (size_t)bh * SEL_BAND_MAX;
-    const double* bscore = w.sbscore + (size_t)bh * SEL_BAND_MAX;
-    for (int i = tid; i < nb; i += nt) {
-      int r = 0;
-      for (int j = 0; j < nb; ++j)
-        r += bscore[j] > bscore[i] || (bscore[j] == bscore[i] && band[j] < band[i]);
-      if (r < need) flag[band[i]] = 1;
+  int32_t* st = w.sstate + q.bh * SS_N;
+  uint8_t* flag = w.flag + q.so;
+  const int ntop = g.ntop[q.b];
+  const int nb = ntop > 0 ? st[SS_NBAND] : 0;
+  if (nb > SEL_BAND_MAX) {
+    if (q.sl == 0 && tid == 0) atomicOr(&c.header[2], 32u);
+    const uint32_t prefix = (uint32_t)st[SS_PREFIX];
+    const float* pooled = w.u + q.so;
+    int eq = 0;
+    for (int t = tid; t < q.t0 && t < q.P; t += nt) eq += __float_as_uint(pooled[t]) == prefix;
+    int before_slice;
+    block_excl_scan(eq, tmp, before_slice);
+    const int per = SEL_SLICE / 256;
+    const int lo = min(q.t1, q.t0 + tid * per), hi = min(q.t1, lo + per);
+    int e2 = 0;
+    for (int t = lo; t < hi; ++t) e2 += __float_as_uint(pooled[t]) == prefix;
+    int tot;
+    int before = before_slice + block_excl_scan(e2, tmp, tot);
+    const int remaining = st[SS_REMAIN];
+    for (int t = lo; t < hi; ++t) {
+      const uint32_t u = __float_as_uint(pooled[t]);
+      uint8_t f = 0;
+      if (u > prefix) {
+        f = 1;
+      } else if (u == prefix) {
+        if (before < remaining) f = 1;
+        ++before;
+      }
+      flag[t] = f;
+      sflag[t - q.t0] = f;
     }
-    __syncthreads();
-  }
-
-  const int nrand = g.nrand[b];
-  const unsigned long long hs = g.seed_anchor ^ ((unsigned long long)h << 40);
-  if (nrand > 0) {
-    for (int i = tid; i < SEL_NBIN; i += nt) hist[i] = 0;
-    if (tid == 0) ncand = 0;
-    __syncthreads();
-    sel_batches(P, [&](int t0) {
-      uint8_t f[SEL_U];
-#pragma unroll
-      for (int u = 0; u < SEL_U; ++u) f[u] = t0 + u * nt < P ? flag[t0 + u * nt] : 1;
-#pragma unroll
-      for (int u = 0; u < SEL_U; ++u)
-        if (!f[u]) atomicAdd(&hist[splitmix64(hs ^ (unsigned long long)(t0 + u * nt)) >> 52], 1u);
-    });
-    __syncthreads();
-    digit_pick(hist, SEL_NBIN, nrand, false, tmp, pick);
-    const unsigned long long bin = (unsigned long long)pick[0];
-    const int need = nrand - pick[1];
-    sel_batches(P, [&](int t0) {
-      uint8_t f[SEL_U];
-#pragma unroll
-      for (int u = 0; u < SEL_U; ++u) f[u] = t0 + u * nt < P ? flag[t0 + u * nt] : 1;
-#pragma unroll
-      for (int u = 0; u < SEL_U; ++u) {
-        if (f[u]) continue;
-        const int t = t0 + u * nt;
-        const unsigned long long key = splitmix64(hs ^ (unsigned long long)t);
-        if ((key >> 52) < bin) {
-          flag[t] = 2;
-        } else if ((key >> 52) == bin) {
-          const int i = atomicAdd(&ncand, 1);
-          if (i < SEL_CAND) {
-            ckey[i] = key;
-            cpos[i] = t;
-          }
+  } else {
+    for (int t = q.t0 + tid; t < q.t1; t += nt) sflag[t - q.t0] = flag[t];
+    if (nb > 0) {
+      const int need = ntop - st[SS_NABOVE];
+      const int32_t* band = w.sband + (size_t)q.bh * SEL_BAND_MAX;
+      const double* bscore = w.sbscore + (size_t)q.bh * SEL_BAND_MAX;
+      __syncthreads();
+      for (int i = tid; i < nb; i += nt) {
+        const int t = band[i];
+        if (t < q.t0 || t >= q.t1) continue;
+        const double si = bscore[i];
+        int r = 0;
+        for (int j = 0; j < nb; ++j) r += bscore[j] > si || (bscore[j] == si && band[j] < t);
+        if (r < need) {
+          flag[t] = 1;
+          sflag[t - q.t0] = 1;
         }
       }
-    });
-    __syncthreads();
-    const int nc = ncand;
+    }
+  }
+  const int nrand = g.nrand[q.b];
+  if (nrand <= 0) return;
+  for (int i = tid; i < SEL_NBIN; i += nt) hist[i] = 0;
+  __syncthreads();
+  const unsigned long long hs = g.seed_anchor ^ ((unsigned long long)q.h << 40);
+  for (int t = q.t0 + tid; t < q.t1; t += nt)
+    if (!sflag[t - q.t0]) atomicAdd(&hist[splitmix64(hs ^ (unsigned long long)t) >> 52], 1u);
+  __syncthreads();
+  uint32_t* gh = w.sghist + (size_t)q.bh * SEL_NBIN;
+  for (int i = tid; i < SEL_NBIN; i += nt)
+    if (hist[i]) atomicAdd(&gh[i], hist[i]);
+}
+
+// The bin of the n_rand-th smallest key (every workgroup, from the head's
+// histogram); the slice's untaken positions with a key below it are taken,
+// those inside it appended (keys are distinct: SplitMix64 is a bijection).
+// Each workgroup leaves its slice's anchor count (bin members excluded).
+__global__ __launch_bounds__(256) void k_sel_rcand(Geo g, Ws w) {
+  __shared__ uint32_t hist[SEL_NBIN];
+  __shared__ int tmp[8], pick[2], wcnt[4];
+  const SelSlice q = sel_slice(g);
+  const int tid = threadIdx.x, nt = blockDim.x;
+  int32_t* st = w.sstate + q.bh * SS_N;
+  uint8_t* flag = w.flag + q.so;
+  const int nrand = g.nrand[q.b];
+  unsigned long long bin = ~0ull;
+  if (nrand > 0) {
+    pick_global(w.sghist + (size_t)q.bh * SEL_NBIN, hist, nrand, false, tmp, pick);
+    bin = (unsigned long long)pick[0];
+    if (q.sl == 0 && tid == 0) {
+      st[SS_RBIN] = pick[0];
+      st[SS_RNEED] = nrand - pick[1];
+    }
+  }
+  const unsigned long long hs = g.seed_anchor ^ ((unsigned long long)q.h << 40);
+  unsigned long long* ckey = w.rkey + (size_t)q.bh * SEL_CAND;
+  int32_t* cpos = w.rpos + (size_t)q.bh * SEL_CAND;
+  int cnt = 0;
+  for (int t0 = q.t0; t0 < q.t1; t0 += nt) {
+    const int t = t0 + tid;
+    uint8_t f = t < q.t1 ? flag[t] : 1;
+    bool app = false;
+    if (!f && nrand > 0) {
+      const unsigned long long key = splitmix64(hs ^ (unsigned long long)t);
+      if ((key >> 52) < bin) {
+        flag[t] = 2;
+        f = 2;
+      } else if ((key >> 52) == bin) {
+        app = true;
+      }
+    }
+    const int slot = wave_append(app, &st[SS_NRC]);
+    if (slot >= 0 && slot < SEL_CAND) {
+      ckey[slot] = splitmix64(hs ^ (unsigned long long)t);
+      cpos[slot] = t;
+    }
+    cnt += (t < q.t1 && f != 0);
+  }
+  cnt = wave_sum_i(cnt);
+  if ((tid & 63) == 0) wcnt[tid >> 6] = cnt;
+  __syncthreads();
+  const int nslmax = (g.maxS + SEL_SLICE - 1) / SEL_SLICE;
+  if (tid == 0) w.slcnt[(size_t)q.bh * nslmax + q.sl] = (wcnt[0] + wcnt[1]) + (wcnt[2] + wcnt[3]);
+}
+
+// The hash bin's keys are ranked (every workgroup; on a candidate overflow
+// the radix select finishes on the remaining 52 bits over all of [0, P), in
+// digits of 12, 12, 12, 12 and 4 bits) and the smallest taken.  The slice's
+// flagged positions then go after those of the earlier slices (their counts
+// plus the bin members taken there), in position order (wave ballots and a
+// scan of the per-wave counts); then the window.  The slice holding
+// position P - 1 (or the first slice when P = 0) checks the total.
+__global__ __launch_bounds__(256) void k_sel_list(Geo g, Ws w, Cache c) {
+  __shared__ uint32_t hist[SEL_NBIN];
+  __shared__ int tmp[8], pick[2], wc[4], wpre[5], basev, extra;
+  const SelSlice q = sel_slice(g);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int W = g.W, k = g.k[q.b];
+  const int nslmax = (g.maxS + SEL_SLICE - 1) / SEL_SLICE;
+  const int32_t* slc = w.slcnt + (size_t)q.bh * nslmax;
+  const int32_t* st = w.sstate + q.bh * SS_N;
+  int32_t* rank = w.rank + q.so;
+  uint8_t* flag = w.flag + q.so;
+  int32_t* anc = c.anc_pos + (size_t)g.prefK[q.b] * g.H + (size_t)q.h * k;
+  if (tid == 0) extra = 0;
+  __syncthreads();
+  const int nrand = g.nrand[q.b];
+  if (nrand > 0) {
+    const int need = st[SS_RNEED];
+    const int nc = st[SS_NRC];
+    const unsigned long long bin = (unsigned long long)st[SS_RBIN];
+    const unsigned long long* ckey = w.rkey + (size_t)q.bh * SEL_CAND;
+    const int32_t* cpos = w.rpos + (size_t)q.bh * SEL_CAND;
     if (nc <= SEL_CAND) {
-      for (int i = tid; i < nc; i += nt) {
+      int ex = 0;
+      for (int i = tid; i < nc; i += blockDim.x) {
         int r = 0;
         for (int j = 0; j < nc; ++j) r += ckey[j] < ckey[i];
-        if (r < need) flag[cpos[i]] = 2;
+        if (r < need) {
+          const int t = cpos[i];
+          if (t < q.t0) ++ex;
+          else if (t < q.t1) flag[t] = 2;
+        }
       }
+      ex = wave_sum_i(ex);
+      if (lane == 0 && ex) atomicAdd(&extra, ex);
     } else {
-      // More candidates than the buffer holds (far from the expected P/4096):
-      // finish the radix select on the remaining 52 bits (digits of 12, 12,
-      // 12, 12 and 4 bits).
-      if (tid == 0) atomicOr(&c.header[2], 64u);
+      if (q.sl == 0 && tid == 0) atomicOr(&c.header[2], 64u);
+      const unsigned long long hs = g.seed_anchor ^ ((unsigned long long)q.h << 40);
       unsigned long long prefix = bin << 52, pmask = 0xfffull << 52;
       int remaining = need;
       for (int dgt = 0; dgt < 5; ++dgt) {
         const int shift = dgt < 4 ? 40 - 12 * dgt : 0;
         const int nbin = dgt < 4 ? SEL_NBIN : 16;
-        for (int i = tid; i < nbin; i += nt) hist[i] = 0;
+        for (int i = tid; i < nbin; i += blockDim.x) hist[i] = 0;
         __syncthreads();
-        for (int t = tid; t < P; t += nt) {
-          if (flag[t]) continue;
+        for (int t = tid; t < q.P; t += blockDim.x) {
+          if (flag[t] == 1) continue;  // bin members may be taken meanwhile (2)
           const unsigned long long key = splitmix64(hs ^ (unsigned long long)t);
           if ((key & pmask) == prefix) atomicAdd(&hist[(key >> shift) & (unsigned long long)(nbin - 1)], 1u);
         }
@@ -445,66 +563,83 @@ __global__ __launch_bounds__(1024) void k_sel_rest(Geo g, Ws w, Cache c, const i
         pmask |= (unsigned long long)(nbin - 1) << shift;
         __syncthreads();
       }
-      for (int t = tid; t < P; t += nt) {
-        if (flag[t]) continue;
+      // Positions in the bin with a key up to the threshold are taken:
+      // counted in the earlier slices, flagged in this one.  Keys in the bin
+      // mark exactly the positions left untaken by the earlier passes, so
+      // the 2s other workgroups write meanwhile change nothing here.
+      int ex = 0;
+      for (int t = tid; t < q.t1; t += blockDim.x) {
+        if (flag[t] == 1) continue;
         const unsigned long long key = splitmix64(hs ^ (unsigned long long)t);
-        if ((key & (0xfffull << 52)) == (bin << 52) && key <= prefix) flag[t] = 2;
+        if ((key & (0xfffull << 52)) == (bin << 52) && key <= prefix) {
+          if (t < q.t0) ++ex;
+          else flag[t] = 2;
+        }
       }
+      ex = wave_sum_i(ex);
+      if (lane == 0 && ex) atomicAdd(&extra, ex);
+    }
+  }
+  if (tid < 64) {
+    int s = 0;
+    const int nbefore = min(q.sl, (q.P + SEL_SLICE - 1) / SEL_SLICE);
+    for (int i = lane; i < nbefore; i += 64) s += slc[i];
+    s = wave_sum_i(s);
+    if (lane == 0) basev = s;
+  }
+  __syncthreads();
+  int base = basev + extra;
+  for (int t0 = q.t0; t0 < q.t1; t0 += blockDim.x) {
+    const int t = t0 + tid;
+    const bool f = t < q.t1 && flag[t] != 0;
+    const unsigned long long bal = __ballot(f);
+    if (lane == 0) wc[wave] = __popcll(bal);
+    __syncthreads();
+    if (tid == 0) {
+      int s = 0;
+      for (int i = 0; i < 4; ++i) {
+        wpre[i] = s;
+        s += wc[i];
+      }
+      wpre[4] = s;
     }
     __syncthreads();
-  }
-
-  // ---- ascending anchor list: flagged positions of [0, P), then the window.
-  // Batches of SEL_U x nt positions in (u, thread) order; a flag's rank is the
-  // count before its batch plus the flags before it inside the batch (wave
-  // ballots, then per-(u, wave) counts in LDS).
-  {
-    static_assert(SEL_U * 16 == 128, "two scan entries per lane of one wave");
-    const int lane = tid & 63, wv = tid >> 6;
-    int base = 0;
-    for (int t0 = tid; t0 - tid < P; t0 += SEL_U * nt) {
-      uint8_t f[SEL_U];
-#pragma unroll
-      for (int u = 0; u < SEL_U; ++u) f[u] = t0 + u * nt < P ? flag[t0 + u * nt] : 0;
-      unsigned long long bal[SEL_U];
-#pragma unroll
-      for (int u = 0; u < SEL_U; ++u) {
-        bal[u] = __ballot(f[u] != 0);
-        if (lane == 0) cnts[u * 16 + wv] = __popcll(bal[u]);
-      }
-      __syncthreads();
-      if (wv == 0) {  // exclusive scan of the (u, wave) counts, u-major
-        const int c0 = cnts[2 * lane], c1 = cnts[2 * lane + 1];
-        int x = c0 + c1;
-#pragma unroll
-        for (int o = 1; o < 64; o <<= 1) {
-          const int y = __shfl_up(x, o, 64);
-          if (lane >= o) x += y;
-        }
-        const int ex = x - c0 - c1;
-        cpre[2 * lane] = ex;
-        cpre[2 * lane + 1] = ex + c0;
-        if (lane == 63) cpre[SEL_U * 16] = x;
-      }
-      __syncthreads();
-#pragma unroll
-      for (int u = 0; u < SEL_U; ++u) {
-        const int r = base + cpre[u * 16 + wv] + __popcll(bal[u] & ((1ull << lane) - 1ull));
-        if (f[u] && r < k - W) {
-          const int t = t0 + u * nt;
-          anc[r] = t;
-          rank[t] = r;
-        }
-      }
-      base += cpre[SEL_U * 16];
-      __syncthreads();
+    const int r = base + wpre[wave] + __popcll(bal & ((1ull << lane) - 1ull));
+    if (f && r < k - W) {
+      anc[r] = t;
+      rank[t] = r;
     }
+    base += wpre[4];
+    __syncthreads();
+  }
+  const bool tail = q.P > 0 ? (q.t0 <= q.P - 1 && q.P - 1 < q.t0 + SEL_SLICE) : q.sl == 0;
+  if (tail) {
     if (tid == 0 && base + W != k) atomicOr(&c.header[2], 2u);
+    for (int i = tid; i < W; i += blockDim.x) {
+      anc[k - W + i] = q.P + i;
+      rank[q.P + i] = k - W + i;
+    }
   }
-  for (int i = tid; i < W; i += nt) {
-    anc[k - W + i] = P + i;
-    rank[P + i] = k - W + i;
+}
+
+// An anchor override replaces the selection: validated (ascending, inside
+// [0, S), the window last) and copied; the marks were reset by k_sel_pool.
+__global__ __launch_bounds__(256) void k_sel_override(Geo g, Ws w, Cache c, const int32_t* ovr) {
+  const int bh = blockIdx.x, b = bh / g.H, h = bh % g.H;
+  const int S = g.S[b], W = g.W, P = S - W, k = g.k[b];
+  const size_t so = (size_t)g.prefS[b] * g.H + (size_t)h * S;
+  int32_t* rank = w.rank + so;
+  int32_t* anc = c.anc_pos + (size_t)g.prefK[b] * g.H + (size_t)h * k;
+  const int32_t* o = ovr + (size_t)g.prefK[b] * g.H + (size_t)h * k;
+  bool bad = false;
+  for (int a = threadIdx.x; a < k; a += blockDim.x) {
+    const int p = o[a];
+    const bool ok = p >= 0 && p < S && (a == 0 || o[a - 1] < p) && (a < k - W || p == P + (a - (k - W)));
+    if (!ok) bad = true;
+    anc[a] = p;
+    if (p >= 0 && p < S) rank[p] = a;
   }
+  if (bad) atomicOr(&c.header[2], 1u);
 }
 
 template <int DT>
@@ -584,17 +719,23 @@ __global__ __launch_bounds__(256) void k_anchor_prep(Geo g, Ws w, Cache c, const
 
 hipError_t launch_select(const Geo& g, const Ws& w, const Cache& c, const void* K, const void* V, const void* Q,
                          const int32_t* ovr, hipStream_t st) {
-  int nblk = 0;
-  for (int b = 0; b < g.B; ++b) nblk += g.H * ((g.k[b] + 63) / 64);
+  int nblk = 0, nsel = 0;
+  for (int b = 0; b < g.B; ++b) {
+    nblk += g.H * ((g.k[b] + 63) / 64);
+    nsel += g.H * ((g.S[b] + SEL_SLICE - 1) / SEL_SLICE);
+  }
   const int nbh = g.B * g.H;
-  if (g.dtype == 1) {
-    launch("k_select", k_sel_top<1>, dim3(nbh), dim3(1024), 0, st, g, w, c, ovr);
-    if (!ovr) launch("k_sel_band", k_sel_band<1>, dim3(nbh * SEL_BAND_MAX), dim3(256), 0, st, g, w, K, Q);
-    launch("k_sel_rest", k_sel_rest<1>, dim3(nbh), dim3(1024), 0, st, g, w, c, ovr);
+  launch("k_sel_pool", k_sel_pool, dim3(nsel), dim3(256), 0, st, g, w, ovr ? 1 : 0);
+  if (ovr) {
+    launch("k_sel_override", k_sel_override, dim3(nbh), dim3(256), 0, st, g, w, c, ovr);
   } else {
-    launch("k_select", k_sel_top<0>, dim3(nbh), dim3(1024), 0, st, g, w, c, ovr);
-    if (!ovr) launch("k_sel_band", k_sel_band<0>, dim3(nbh * SEL_BAND_MAX), dim3(256), 0, st, g, w, K, Q);
-    launch("k_sel_rest", k_sel_rest<0>, dim3(nbh), dim3(1024), 0, st, g, w, c, ovr);
+    launch("k_sel_cand", k_sel_cand, dim3(nsel), dim3(256), 0, st, g, w);
+    launch("k_sel_class", k_sel_class, dim3(nsel), dim3(256), 0, st, g, w);
+    if (g.dtype == 1) launch("k_sel_band", k_sel_band<1>, dim3(nbh * SEL_BAND_MAX), dim3(256), 0, st, g, w, K, Q);
+    else launch("k_sel_band", k_sel_band<0>, dim3(nbh * SEL_BAND_MAX), dim3(256), 0, st, g, w, K, Q);
+    launch("k_sel_rhist", k_sel_rhist, dim3(nsel), dim3(256), 0, st, g, w, c);
+    launch("k_sel_rcand", k_sel_rcand, dim3(nsel), dim3(256), 0, st, g, w);
+    launch("k_sel_list", k_sel_list, dim3(nsel), dim3(256), 0, st, g, w, c);
   }
   if (g.dtype == 1) {
     launch("k_anchor_prep", k_anchor_prep<1>, dim3(nblk), dim3(256), 0, st, g, w, c, K, V, Q);
