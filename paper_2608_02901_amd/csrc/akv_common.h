@@ -136,9 +136,11 @@ struct Ws {
   float* u;             // [side][b][h][S_b] utility, -1 for anchors
   uint8_t* sel;         // [side][b][h][S_b] residual flags
   uint4* srec;          // [slots] record of the token placed at a sorted slot (position and flags, anchors, coefficients)
-  uint32_t* bhist;      // [b][side][256]
-  int32_t* bstate;      // [b][side][4]: prefix bits, remaining, threshold bits, need
-  int32_t* tiecnt;      // [b][side][nchunk]
+  uint32_t* bhist;      // [b][side][4096] first-digit histogram of the utilities (zeroed at the start of an encode)
+  int32_t* bstate;      // [b][side][4]: candidates appended, threshold bits, count to take at the threshold, -
+  float* bcval;         // [b][side][BCMAX] utilities in the threshold's first-digit bin
+  int32_t* bcpos;       // [b][side][BCMAX] their flattened (h, t) index
+  int32_t* tiecnt;      // [b][side][nchunk] threshold ties in the earlier chunks
   int32_t* shist;       // [b][h][sort chunks + 1][k_b] per-chunk anchor histograms, then column prefixes; last row: anchor totals
   int32_t* wcnt;        // [side][b][h][ceil(S_b/64)] popcounts for the slot scan
 };
@@ -401,6 +403,120 @@ __device__ inline void fwht_wave(float& z0, float& z1, int lane) {
       z1 = z1 + o1;
     }
   }
+}
+
+// ------------------------------------------------------------------ radix select helpers
+constexpr int SEL_NBIN = 4096;  // 12-bit radix digits
+constexpr int SEL_U = 8;        // elements per thread per batch (independent loads)
+
+// Exclusive scan of one int per thread over the workgroup.
+__device__ inline int block_excl_scan(int v, int* tmp /* >= 16 ints */, int& total) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  int x = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    int y = __shfl_up(x, o, 64);
+    if (lane >= o) x += y;
+  }
+  if (lane == 63) tmp[wave] = x;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int s = 0;
+    for (int i = 0; i < nw; ++i) {
+      int t = tmp[i];
+      tmp[i] = s;
+      s += t;
+    }
+    tmp[nw] = s;
+  }
+  __syncthreads();
+  int r = x - v + tmp[wave];
+  total = tmp[nw];
+  __syncthreads();
+  return r;
+}
+
+// Radix digit search over a 4096-bin histogram: the bin where the running
+// count (from the top when `desc`, else from the bottom) reaches `need`.
+// Writes (bin, count before it) to out[0..1].  Whole workgroup.
+__device__ inline void digit_pick(const uint32_t* hist, int nbin, int need, bool desc, int* tmp, int* out) {
+  const int tid = threadIdx.x, nt = blockDim.x;
+  const int per = (nbin + nt - 1) / nt;
+  int loc = 0;
+  for (int i = 0; i < per; ++i) {
+    const int bin = tid * per + i;
+    if (bin < nbin) loc += (int)hist[desc ? nbin - 1 - bin : bin];
+  }
+  int tot;
+  const int before = block_excl_scan(loc, tmp, tot);
+  int run = before;
+  for (int i = 0; i < per; ++i) {
+    const int bin = tid * per + i;
+    if (bin >= nbin) break;
+    const int c = (int)hist[desc ? nbin - 1 - bin : bin];
+    if (run < need && run + c >= need) {
+      out[0] = desc ? nbin - 1 - bin : bin;
+      out[1] = run;
+    }
+    run += c;
+  }
+  __syncthreads();
+}
+
+constexpr int SEL_HALO = 254;   // 2 * (kappa / 2) for kappa <= 255
+
+// Passes over [0, n) visit t = t0 + u * nt (u < SEL_U) per batch: coalesced
+// across lanes, SEL_U independent loads in flight per thread.
+template <typename F>
+__device__ inline void sel_batches(int n, F&& body) {
+  for (int t0 = threadIdx.x; t0 < n; t0 += SEL_U * blockDim.x) body(t0);
+}
+
+// Radix digit histogram of `nbin` bins over the values v with (v & pmask) ==
+// prefix, into LDS hist (zeroed here); whole workgroup.
+template <typename F>
+__device__ inline void digit_hist(uint32_t* hist, int nbin, int n, F&& value, uint32_t pmask, uint32_t prefix,
+                                  int shift) {
+  for (int i = threadIdx.x; i < nbin; i += blockDim.x) hist[i] = 0;
+  __syncthreads();
+  sel_batches(n, [&](int t0) {
+    uint32_t v[SEL_U];
+#pragma unroll
+    for (int u = 0; u < SEL_U; ++u) v[u] = t0 + u * (int)blockDim.x < n ? value(t0 + u * blockDim.x) : 0u;
+#pragma unroll
+    for (int u = 0; u < SEL_U; ++u)
+      if (t0 + u * (int)blockDim.x < n && (v[u] & pmask) == prefix) atomicAdd(&hist[(v[u] >> shift) & (nbin - 1)], 1u);
+  });
+  __syncthreads();
+}
+
+// Reserves `cnt` consecutive slots per thread in a list whose length is the
+// global counter `count`: a workgroup scan of the counts and one atomic per
+// workgroup.  Returns the thread's first slot.  All threads call it; `tmp`
+// holds at least blockDim.x / 64 + 1 ints of LDS.
+__device__ inline int wg_reserve(int cnt, int32_t* count, int* tmp) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  int x = cnt;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(x, o, 64);
+    if (lane >= o) x += y;
+  }
+  if (lane == 63) tmp[wave] = x;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int s = 0;
+    for (int i = 0; i < nw; ++i) {
+      const int t = tmp[i];
+      tmp[i] = s;
+      s += t;
+    }
+    tmp[nw] = s ? atomicAdd(count, s) : 0;
+  }
+  __syncthreads();
+  const int r = tmp[nw] + tmp[wave] + x - cnt;
+  __syncthreads();
+  return r;
 }
 
 // Kernel timing hook (anchorkv_profile_*): when launches of the named kernel

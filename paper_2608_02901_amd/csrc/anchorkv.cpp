@@ -66,7 +66,7 @@ struct anchorkv_plan {
   size_t cache_bytes;
   // encode workspace offsets
   size_t w_opmax, w_opsum, w_oM, w_oiZ, w_oiZ64, w_ypart, w_Y, w_Yhi, w_Ylo, w_ynorm, w_sc, w_rank, w_flag, w_sband, w_sbscore, w_sstate, w_sghist, w_scand, w_rkey, w_rpos, w_slcnt, w_QA, w_apos,
-      w_fix, w_fixcount, w_gpos, w_u, w_sel, w_srec, w_bhist, w_bstate, w_tiecnt, w_shist, w_wcnt;
+      w_fix, w_fixcount, w_gpos, w_u, w_sel, w_srec, w_bhist, w_bstate, w_bcval, w_bcpos, w_tiecnt, w_shist, w_wcnt;
   size_t ws_bytes;
   // decode workspace offsets
   size_t d_SK, d_RK, d_part, d_asc, d_atop;
@@ -296,8 +296,10 @@ extern "C" anchorkv_status anchorkv_plan_create(const anchorkv_config* cfg, int3
   p->w_u = Wl.add(4 * 2 * TS);
   p->w_sel = Wl.add(2 * TS);
   p->w_srec = Wl.add(16 * TW * 64);
-  p->w_bhist = Wl.add(4 * 2 * 256 * batch);
+  p->w_bhist = Wl.add(4 * 2 * 4096 * batch);
   p->w_bstate = Wl.add(4 * 2 * 4 * batch);
+  p->w_bcval = Wl.add(4 * 2 * (size_t)32768 * batch);
+  p->w_bcpos = Wl.add(4 * 2 * (size_t)32768 * batch);
   p->w_tiecnt = Wl.add(4 * 2 * (size_t)geo.prefBC[batch]);
   p->w_shist = Wl.add(4 * (size_t)geo.prefKT[batch]);
   p->w_wcnt = Wl.add(4 * 2 * TW);
@@ -396,6 +398,8 @@ static akv::Ws ws_ptrs(const anchorkv_plan* p, void* base) {
   w.srec = at<uint4>(base, p->w_srec);
   w.bhist = at<uint32_t>(base, p->w_bhist);
   w.bstate = at<int32_t>(base, p->w_bstate);
+  w.bcval = at<float>(base, p->w_bcval);
+  w.bcpos = at<int32_t>(base, p->w_bcpos);
   w.tiecnt = at<int32_t>(base, p->w_tiecnt);
   w.shist = at<int32_t>(base, p->w_shist);
   w.wcnt = at<int32_t>(base, p->w_wcnt);
@@ -697,10 +701,13 @@ __global__ void k_init(Geo g, Cache c, Ws w) {
   if (i < 2 * g.H * g.B) w.fixcount[i] = 0;
   if (i < akv::SS_N * g.H * g.B) w.sstate[i] = 0;
   if (i < 4096 * g.H * g.B) w.sghist[i] = 0u;
+  if (i < 2 * 4096 * g.B) w.bhist[i] = 0u;
+  if (i < 2 * 4 * g.B) w.bstate[i] = 0;
 }
 hipError_t launch_init(const Geo& g, const Cache& c, const Ws& w, hipStream_t st) {
   int n = 4 * g.B > 2 * g.H * g.B ? 4 * g.B : 2 * g.H * g.B;
   if (4096 * g.H * g.B > n) n = 4096 * g.H * g.B;
+  if (2 * 4096 * g.B > n) n = 2 * 4096 * g.B;
   launch("k_init", k_init, dim3((n + 255) / 256), dim3(256), 0, st, g, c, w);
   return hipGetLastError();
 }

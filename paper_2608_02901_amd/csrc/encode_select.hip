@@ -33,33 +33,6 @@
 
 namespace akv {
 
-// Exclusive scan of one int per thread over a 1024-thread block.
-__device__ inline int block_excl_scan(int v, int* tmp /* >= 16 ints */, int& total) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
-  int x = v;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    int y = __shfl_up(x, o, 64);
-    if (lane >= o) x += y;
-  }
-  if (lane == 63) tmp[wave] = x;
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    int s = 0;
-    for (int i = 0; i < nw; ++i) {
-      int t = tmp[i];
-      tmp[i] = s;
-      s += t;
-    }
-    tmp[nw] = s;
-  }
-  __syncthreads();
-  int r = x - v + tmp[wave];
-  total = tmp[nw];
-  __syncthreads();
-  return r;
-}
-
 // Positions whose fp32 pooled score lies within SEL_BAND (relative) of the
 // cut are re-scored in fp64 (at most SEL_BAND_MAX of them).  The fp32 score's
 // error is below 1e-4 relative: fp32 accumulation of 128 exact bf16 products
@@ -146,44 +119,6 @@ __global__ __launch_bounds__(256) void k_sel_band(Geo g, Ws w, const void* Kin, 
   }
 }
 
-// Radix digit search over a 4096-bin histogram: the bin where the running
-// count (from the top when `desc`, else from the bottom) reaches `need`.
-// Writes (bin, count before it) to out[0..1].  Whole workgroup.
-__device__ inline void digit_pick(const uint32_t* hist, int nbin, int need, bool desc, int* tmp, int* out) {
-  const int tid = threadIdx.x, nt = blockDim.x;
-  const int per = (nbin + nt - 1) / nt;
-  int loc = 0;
-  for (int i = 0; i < per; ++i) {
-    const int bin = tid * per + i;
-    if (bin < nbin) loc += (int)hist[desc ? nbin - 1 - bin : bin];
-  }
-  int tot;
-  const int before = block_excl_scan(loc, tmp, tot);
-  int run = before;
-  for (int i = 0; i < per; ++i) {
-    const int bin = tid * per + i;
-    if (bin >= nbin) break;
-    const int c = (int)hist[desc ? nbin - 1 - bin : bin];
-    if (run < need && run + c >= need) {
-      out[0] = desc ? nbin - 1 - bin : bin;
-      out[1] = run;
-    }
-    run += c;
-  }
-  __syncthreads();
-}
-
-constexpr int SEL_NBIN = 4096;  // 12-bit radix digits
-constexpr int SEL_HALO = 254;   // 2 * (kappa / 2) for kappa <= 255
-constexpr int SEL_U = 8;        // elements per thread per batch (independent loads)
-
-// Passes over [0, n) visit t = t0 + u * nt (u < SEL_U) per batch: coalesced
-// across lanes, SEL_U independent loads in flight per thread.
-template <typename F>
-__device__ inline void sel_batches(int n, F&& body) {
-  for (int t0 = threadIdx.x; t0 < n; t0 += SEL_U * blockDim.x) body(t0);
-}
-
 // ------------------------------------------------------------------ slice passes
 // Slice sl of (request b, head h): positions [sl * SEL_SLICE, ...) of [0, S).
 struct SelSlice {
@@ -218,24 +153,6 @@ __device__ inline int wave_append(bool take, int32_t* count) {
   if (lane == leader) base = atomicAdd(count, __popcll(bal));
   base = __shfl(base, leader, 64);
   return take ? base + __popcll(bal & ((1ull << lane) - 1ull)) : -1;
-}
-
-// Radix digit histogram of `nbin` bins over the values v with (v & pmask) ==
-// prefix, into LDS hist (zeroed here); whole workgroup.
-template <typename F>
-__device__ inline void digit_hist(uint32_t* hist, int nbin, int n, F&& value, uint32_t pmask, uint32_t prefix,
-                                  int shift) {
-  for (int i = threadIdx.x; i < nbin; i += blockDim.x) hist[i] = 0;
-  __syncthreads();
-  sel_batches(n, [&](int t0) {
-    uint32_t v[SEL_U];
-#pragma unroll
-    for (int u = 0; u < SEL_U; ++u) v[u] = t0 + u * (int)blockDim.x < n ? value(t0 + u * blockDim.x) : 0u;
-#pragma unroll
-    for (int u = 0; u < SEL_U; ++u)
-      if (t0 + u * (int)blockDim.x < n && (v[u] & pmask) == prefix) atomicAdd(&hist[(v[u] >> shift) & (nbin - 1)], 1u);
-  });
-  __syncthreads();
 }
 
 // The bin of a head's summed histogram where the running count (from the
@@ -306,13 +223,22 @@ __global__ __launch_bounds__(256) void k_sel_cand(Geo g, Ws w) {
   }
   const float* pooled = w.u + q.so;
   float* cand = w.scand + (size_t)q.bh * SEL_CMAX;
-  for (int t0 = q.t0; t0 < q.t1; t0 += blockDim.x) {
-    const int t = t0 + tid;
-    const float v = t < q.t1 ? pooled[t] : 0.0f;
-    const bool take = t < q.t1 && (__float_as_uint(v) >> 20) == bin1;
-    const int slot = wave_append(take, &st[SS_NCAND]);
-    if (slot >= 0 && slot < SEL_CMAX) cand[slot] = v;
+  constexpr int per = SEL_SLICE / 256;
+  float v[per];
+  int cnt = 0;
+#pragma unroll
+  for (int j = 0; j < per; ++j) {
+    const int t = q.t0 + j * 256 + tid;
+    v[j] = t < q.t1 ? pooled[t] : -1.0f;
+    cnt += v[j] >= 0.0f && (__float_as_uint(v[j]) >> 20) == bin1;
   }
+  int slot = wg_reserve(cnt, &st[SS_NCAND], tmp);
+#pragma unroll
+  for (int j = 0; j < per; ++j)
+    if (v[j] >= 0.0f && (__float_as_uint(v[j]) >> 20) == bin1) {
+      if (slot < SEL_CMAX) cand[slot] = v[j];
+      ++slot;
+    }
 }
 
 // The exact cut (every workgroup): digits [19:8] and [7:0] of the n_top-th
