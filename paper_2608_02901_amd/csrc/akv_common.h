@@ -223,16 +223,18 @@ __device__ inline int crow(int r, int lane) { return (r >> 2) * 8 + (lane >> 5) 
 
 // ------------------------------------------------------------------ canonical fp64 dot
 // Products of fp32 / bf16 values are exact in fp64; the sum runs j = 0..D-1
-// with one rounding per addition.  Each step is an fp64 fused multiply-add,
-// which rounds once, on the exact product: the same value as the addition of
-// the separately formed product.  The length is the head dimension AKV_D
-// (the argument must equal it); the unrolled loop lets the row loads be
-// issued ahead of the addition chain instead of one round trip per 16-byte
-// chunk.
-template <int DT>
+// with one rounding per addition.  With FMA the step is an fp64 fused
+// multiply-add, which rounds once, on the exact product: the same value as
+// the addition of the separately formed product (fewer instructions; the
+// separate form leaves the register allocation of the decode kernels that
+// inline it unchanged).  The length is the head dimension AKV_D (the argument
+// must equal it); the unrolled loop lets the row loads be issued ahead of the
+// addition chain instead of one round trip per 16-byte chunk.
+template <int DT, bool FMA = false>
 __device__ inline double dot64_seq(const typename Elem<DT>::T* x, const typename Elem<DT>::T* y, int) {
   constexpr int D = AKV_D;
   double s = 0.0;
+  auto step = [&](double a, double b) { s = FMA ? fma(a, b, s) : s + a * b; };
   if constexpr (DT == 1) {
 #pragma unroll
     for (int j = 0; j < D; j += 8) {
@@ -241,17 +243,17 @@ __device__ inline double dot64_seq(const typename Elem<DT>::T* x, const typename
       const uint16_t* xs = (const uint16_t*)&xv;
       const uint16_t* ys = (const uint16_t*)&yv;
 #pragma unroll
-      for (int i = 0; i < 8; ++i) s = fma((double)bf2f(xs[i]), (double)bf2f(ys[i]), s);
+      for (int i = 0; i < 8; ++i) step((double)bf2f(xs[i]), (double)bf2f(ys[i]));
     }
   } else {
 #pragma unroll
     for (int j = 0; j < D; j += 4) {
       float4 xv = *(const float4*)(x + j);
       float4 yv = *(const float4*)(y + j);
-      s = fma((double)xv.x, (double)yv.x, s);
-      s = fma((double)xv.y, (double)yv.y, s);
-      s = fma((double)xv.z, (double)yv.z, s);
-      s = fma((double)xv.w, (double)yv.w, s);
+      step((double)xv.x, (double)yv.x);
+      step((double)xv.y, (double)yv.y);
+      step((double)xv.z, (double)yv.z);
+      step((double)xv.w, (double)yv.w);
     }
   }
   return s;

@@ -96,7 +96,7 @@ __global__ __launch_bounds__(256) void k_epilogue(Geo g, Ws w, Cache c, const vo
       float gb = 1.0f;
       if (in && rk < 0) {
         if (bad) atomicOr(&c.header[2], 4u);
-        const double d = dot64_seq<DT>(xe, ae, D);
+        const double d = dot64_seq<DT, true>(xe, ae, D);
         const double g64 = n > 0.0 ? d / n : 0.0;
         gb = Elem<DT>::round_coef((float)g64);
       }

@@ -285,8 +285,16 @@ __global__ __launch_bounds__(1024) void k_lscan(Geo g, Ws w, Cache c) {
   int32_t* pc = (side ? c.pcV : c.pcK) + wo;
   const int per = (nw + blockDim.x - 1) / blockDim.x;
   const int lo = min(nw, (int)threadIdx.x * per), hi = min(nw, lo + per);
+  // The thread's words are read 16 at a time (independent loads in flight).
+  constexpr int U = 16;
   int s = 0;
-  for (int i = lo; i < hi; ++i) s += cnt[i];
+  for (int c0 = lo; c0 < hi; c0 += U) {
+    int v[U];
+#pragma unroll
+    for (int j = 0; j < U; ++j) v[j] = c0 + j < hi ? cnt[c0 + j] : 0;
+#pragma unroll
+    for (int j = 0; j < U; ++j) s += v[j];
+  }
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   int x = s;
   for (int o = 1; o < 64; o <<= 1) {
@@ -305,10 +313,16 @@ __global__ __launch_bounds__(1024) void k_lscan(Geo g, Ws w, Cache c) {
   }
   __syncthreads();
   int run = x - s + tmp[wave] + (side ? g.prefNV[b] : g.prefNK[b]);
-  for (int i = lo; i < hi; ++i) {
-    int v = cnt[i];
-    pc[i] = run;
-    run += v;
+  for (int c0 = lo; c0 < hi; c0 += U) {
+    int v[U];
+#pragma unroll
+    for (int j = 0; j < U; ++j) v[j] = c0 + j < hi ? cnt[c0 + j] : 0;
+#pragma unroll
+    for (int j = 0; j < U; ++j)
+      if (c0 + j < hi) {
+        pc[c0 + j] = run;
+        run += v[j];
+      }
   }
 }
 
