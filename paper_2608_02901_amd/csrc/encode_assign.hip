@@ -342,35 +342,42 @@ __global__ __launch_bounds__(256) void k_fixup(Geo g, Ws w, Cache c, const void*
     const float bnd = b1 - 2.0f * eps - b1 * 9.094947e-13f;
 
     // Band collection: wave w takes anchor tiles w, w+4, ... (rows of the tile
-    // on M, tokens on N), prefetching two tiles ahead.
+    // on M, tokens on N), prefetching two tiles ahead together with the
+    // inverse norms of the lane's 16 rows (rows past k read 0: score 0).
     typename M::frag f0[NKS], f1[NKS];
-    auto fetch = [&](typename M::frag (&f)[NKS], int a0) {
+    float i0[16], i1[16];
+    auto fetch = [&](typename M::frag (&f)[NKS], float (&iv)[16], int a0) {
       const E* arow = A + (size_t)min(a0 + (lane & 31), k - 1) * D;
 #pragma unroll
       for (int s = 0; s < NKS; ++s) f[s] = M::load(arow, kofs(M::KS, s, lane));
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int r = a0 + crow(e, lane);
+        iv[e] = inv[min(r, k - 1)] * (r < k ? 1.0f : 0.0f);
+      }
     };
-    auto tile = [&](const typename M::frag (&f)[NKS], int a0) {
+    auto tile = [&](const typename M::frag (&f)[NKS], const float (&iv)[16], int a0) {
       f32x16 acc = {};
 #pragma unroll
       for (int s = 0; s < NKS; ++s) acc = M::mma(f[s], xf[s], acc);
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
         const int r = a0 + crow(e, lane);
-        if (r < k && n < nr && fabsf(acc[e]) * inv[r] >= bnd) {
+        if (r < k && n < nr && fabsf(acc[e]) * iv[e] >= bnd) {
           const int j = atomicAdd(&ccnt[n], 1);
           if (j < FIX_SLOTS) cidx[n][j] = r;
         }
       }
     };
     int a0 = wave * 32;
-    if (a0 < k) fetch(f0, a0);
-    if (a0 + 128 < k) fetch(f1, a0 + 128);
+    if (a0 < k) fetch(f0, i0, a0);
+    if (a0 + 128 < k) fetch(f1, i1, a0 + 128);
     for (; a0 < k; a0 += 256) {
-      tile(f0, a0);
-      if (a0 + 256 < k) fetch(f0, a0 + 256);
+      tile(f0, i0, a0);
+      if (a0 + 256 < k) fetch(f0, i0, a0 + 256);
       if (a0 + 128 >= k) break;
-      tile(f1, a0 + 128);
-      if (a0 + 384 < k) fetch(f1, a0 + 384);
+      tile(f1, i1, a0 + 128);
+      if (a0 + 384 < k) fetch(f1, i1, a0 + 384);
     }
     __syncthreads();
 

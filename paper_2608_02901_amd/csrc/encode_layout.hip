@@ -274,55 +274,67 @@ __global__ __launch_bounds__(256) void k_lrec(Geo g, Ws w, Cache c) {
 }
 
 // Slot base of every word: the request's first slot plus an exclusive scan
-// over its (head, word) sequence.
+// over its (head, word) sequence.  Words are read coalesced, up to 16 tiles
+// of 1024 per round (all loads issued before the wave scans), then one scan
+// of the (tile, wave) sums.
 __global__ __launch_bounds__(1024) void k_lscan(Geo g, Ws w, Cache c) {
-  __shared__ int tmp[20];
+  constexpr int TU = 16;
+  __shared__ int wsum[TU * 16], wpre[TU * 16 + 1];
   const int b = blockIdx.x >> 1, side = blockIdx.x & 1;
   const int nw = g.H * ((g.S[b] + 63) / 64);
   const size_t WT = (size_t)g.prefW[g.B] * g.H;
   const size_t wo = (size_t)g.prefW[b] * g.H;
   const int32_t* cnt = w.wcnt + side * WT + wo;
   int32_t* pc = (side ? c.pcV : c.pcK) + wo;
-  const int per = (nw + blockDim.x - 1) / blockDim.x;
-  const int lo = min(nw, (int)threadIdx.x * per), hi = min(nw, lo + per);
-  // The thread's words are read 16 at a time (independent loads in flight).
-  constexpr int U = 16;
-  int s = 0;
-  for (int c0 = lo; c0 < hi; c0 += U) {
-    int v[U];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  int carry = side ? g.prefNV[b] : g.prefNK[b];
+  for (int a0 = 0; a0 < nw; a0 += TU * 1024) {
+    int v[TU], x[TU];
 #pragma unroll
-    for (int j = 0; j < U; ++j) v[j] = c0 + j < hi ? cnt[c0 + j] : 0;
-#pragma unroll
-    for (int j = 0; j < U; ++j) s += v[j];
-  }
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  int x = s;
-  for (int o = 1; o < 64; o <<= 1) {
-    int y = __shfl_up(x, o, 64);
-    if (lane >= o) x += y;
-  }
-  if (lane == 63) tmp[wave] = x;
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    int acc = 0;
-    for (int i = 0; i < (int)(blockDim.x >> 6); ++i) {
-      int v = tmp[i];
-      tmp[i] = acc;
-      acc += v;
+    for (int u = 0; u < TU; ++u) {
+      const int i = a0 + u * 1024 + tid;
+      v[u] = i < nw ? cnt[i] : 0;
     }
-  }
-  __syncthreads();
-  int run = x - s + tmp[wave] + (side ? g.prefNV[b] : g.prefNK[b]);
-  for (int c0 = lo; c0 < hi; c0 += U) {
-    int v[U];
 #pragma unroll
-    for (int j = 0; j < U; ++j) v[j] = c0 + j < hi ? cnt[c0 + j] : 0;
+    for (int u = 0; u < TU; ++u) {
+      x[u] = v[u];
 #pragma unroll
-    for (int j = 0; j < U; ++j)
-      if (c0 + j < hi) {
-        pc[c0 + j] = run;
-        run += v[j];
+      for (int o = 1; o < 64; o <<= 1) {
+        const int y = __shfl_up(x[u], o, 64);
+        if (lane >= o) x[u] += y;
       }
+      if (lane == 63) wsum[u * 16 + wave] = x[u];
+    }
+    __syncthreads();
+    if (tid < 64) {  // 256 sums, four per lane in order
+      int c4[4], t4 = 0;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        c4[j] = wsum[4 * lane + j];
+        t4 += c4[j];
+      }
+      int y = t4;
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        const int z = __shfl_up(y, o, 64);
+        if (lane >= o) y += z;
+      }
+      int run = y - t4;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        wpre[4 * lane + j] = run;
+        run += c4[j];
+      }
+      if (lane == 63) wpre[TU * 16] = y;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < TU; ++u) {
+      const int i = a0 + u * 1024 + tid;
+      if (i < nw) pc[i] = carry + wpre[u * 16 + wave] + x[u] - v[u];
+    }
+    carry += wpre[TU * 16];
+    __syncthreads();
   }
 }
 
