@@ -106,8 +106,8 @@ struct Cache {
 
 // Encode scratch.
 struct Ws {
-  float* opmax;         // [b][h][chunk][m] partial row max of the observation logits
-  double* opsum;        // [b][h][chunk][m] partial sum of exp (fp64)
+  float* opmax;         // [b][h][chunk][2][m] partial row max of the observation logits (per half chunk)
+  double* opsum;        // [b][h][chunk][2][m] partial sum of exp (fp64)
   float* oM;            // [b][h][m] row max (scaled logits)
   float* oiZ;           // [b][h][m] 1 / sum exp
   double* oiZ64;        // [b][h][m] the same in fp64 (selection near-ties)

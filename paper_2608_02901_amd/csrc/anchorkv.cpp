@@ -267,8 +267,8 @@ extern "C" anchorkv_status anchorkv_plan_create(const anchorkv_config* cfg, int3
   p->cache_bytes = L.total;
 
   Layout Wl;
-  p->w_opmax = Wl.add(4 * TC * m);
-  p->w_opsum = Wl.add(8 * TC * m);
+  p->w_opmax = Wl.add(4 * 2 * TC * m);  // two halves per observation chunk
+  p->w_opsum = Wl.add(8 * 2 * TC * m);
   p->w_oM = Wl.add(4 * batch * H * m);
   p->w_oiZ = Wl.add(4 * batch * H * m);
   p->w_oiZ64 = Wl.add(8 * batch * H * m);

@@ -3,8 +3,8 @@
 // utilities).  For every KV head the m = W * (Hq/H) observation rows (the
 // queries of the last W positions, causal inside the window) attend to all
 // positions:
-//   k_obs_stats   : per chunk of 2048 tokens, MFMA logits q_w.k_t / sqrt(D) and
-//                   the per-row running max and sum of exp;
+//   k_obs_stats   : per half chunk (1024 tokens), MFMA logits q_w.k_t / sqrt(D)
+//                   and the per-row running max and sum of exp;
 //   k_obs_reduce  : merges the chunk statistics into M_w and 1/Z_w;
 //   k_obs_pass    : recomputes the logits, alpha = exp(l - M)/Z, the SnapKV
 //                   column score sc(t) = (1/m) sum_w alpha_wt, and the partial
@@ -151,8 +151,9 @@ __global__ __launch_bounds__(256) void k_obs_stats(Geo g, Ws w, const void* Kin,
   using E = typename Elem<DT>::T;
   using M = MF<DT>;
   constexpr int LD = TileLD<DT>::v;
-  __shared__ __align__(16) E KT[32 * LD];
-  int idx = blockIdx.x;
+  __shared__ __align__(16) E KT[2][32 * LD];  // double-buffered key tile
+  int idx = blockIdx.x >> 1;
+  const int hs = blockIdx.x & 1;  // half of the chunk (OBS_CHUNK / 2 tokens)
   const int b = locate(g, OBS_CHUNK, 1, idx);
   const int S = g.S[b], P = S - g.W, D = g.D, m = g.m;
   const int nch = (S + OBS_CHUNK - 1) / OBS_CHUNK;
@@ -181,13 +182,20 @@ __global__ __launch_bounds__(256) void k_obs_stats(Geo g, Ws w, const void* Kin,
 #pragma unroll
     for (int s = 0; s < NKS; ++s) qf[r][s] = M::load(Q + (size_t)arow * D, kofs(M::KS, s, lane));
   }
-  const int tb = ch * OBS_CHUNK, te = min(S, tb + OBS_CHUNK);
+  const int tb = ch * OBS_CHUNK + hs * (OBS_CHUNK / 2), te = min(S, tb + OBS_CHUNK / 2);
+  // Tile it sits in KT[it & 1]; the tile after it is stored into the other
+  // buffer right after the barrier that ends the reads of tile it - 1, so
+  // one barrier per tile suffices.
   RowTile<DT> kt;
   kt.load(X, tb, S);
-  for (int t0 = tb; t0 < te; t0 += 32) {
-    kt.store(KT, LD);
+  kt.store(KT[0], LD);
+  if (tb + 32 < te) kt.load(X, tb + 32, S);
+  int it = 0;
+  for (int t0 = tb; t0 < te; t0 += 32, ++it) {
+    const int cb = it & 1;
     __syncthreads();
-    if (t0 + 32 < te) kt.load(X, t0 + 32, S);
+    if (t0 + 32 < te) kt.store(KT[cb ^ 1], LD);
+    if (t0 + 64 < te) kt.load(X, t0 + 64, S);
 #pragma unroll
     for (int r = 0; r < R; ++r) {
       const int rb = wave + 4 * r;
@@ -195,7 +203,7 @@ __global__ __launch_bounds__(256) void k_obs_stats(Geo g, Ws w, const void* Kin,
       f32x16 acc = {};
 #pragma unroll
       for (int s = 0; s < NKS; ++s) {
-        auto kb = M::load_lds(&KT[(lane & 31) * LD], kofs(M::KS, s, lane));
+        auto kb = M::load_lds(&KT[cb][(lane & 31) * LD], kofs(M::KS, s, lane));
         acc = M::mma(kb, qf[r][s], acc);
       }
       float l[16];
@@ -218,7 +226,6 @@ __global__ __launch_bounds__(256) void k_obs_stats(Geo g, Ws w, const void* Kin,
         for (int e = 0; e < o; ++e) p[e] += p[e + o];
       sm[r] += p[0];
     }
-    __syncthreads();
   }
   // Merge the two lanes (l, l + 32) that share each row.
 #pragma unroll
@@ -231,7 +238,7 @@ __global__ __launch_bounds__(256) void k_obs_stats(Geo g, Ws w, const void* Kin,
     const double z = (a == nm ? s : s * exp((double)a - (double)nm)) + (oa == nm ? os : os * exp((double)oa - (double)nm));
     const int wr = rb * 32 + lane;
     if (lane < 32 && wr < m) {
-      size_t o = ((size_t)(g.prefC[b] * g.H + h * nch + ch)) * m + wr;
+      size_t o = ((size_t)(g.prefC[b] * g.H + h * nch + ch) * 2 + hs) * m + wr;
       w.opmax[o] = nm;
       w.opsum[o] = z;
     }
@@ -239,22 +246,23 @@ __global__ __launch_bounds__(256) void k_obs_stats(Geo g, Ws w, const void* Kin,
 }
 
 // Row statistics from the chunk statistics: per workgroup 64 rows of one
-// (request, head); the four waves take every fourth chunk, and their partial
-// (max, sum) pairs are merged in LDS.
-__global__ __launch_bounds__(256) void k_obs_reduce(Geo g, Ws w) {
-  __shared__ float pm[4][64];
-  __shared__ double ps[4][64];
+// (request, head); the 16 waves take every 16th half-chunk entry, and their
+// partial (max, sum) pairs are merged in LDS.
+__global__ __launch_bounds__(1024) void k_obs_reduce(Geo g, Ws w) {
+  constexpr int NP = 16;
+  __shared__ float pm[NP][64];
+  __shared__ double ps[NP][64];
   const int nrg = (g.m + 63) / 64;
   const int bh = blockIdx.x / nrg, b = bh / g.H, h = bh % g.H;
   const int lane = threadIdx.x & 63, part = threadIdx.x >> 6;
   const int wr = (blockIdx.x % nrg) * 64 + lane;
   const int nch = (g.S[b] + OBS_CHUNK - 1) / OBS_CHUNK;
   const int wc = min(wr, g.m - 1);
-  const size_t base = ((size_t)(g.prefC[b] * g.H + h * nch)) * g.m + wc;
+  const size_t base = ((size_t)(g.prefC[b] * g.H + h * nch)) * 2 * g.m + wc;
   float M = NEG;
-  for (int c = part; c < nch; c += 4) M = fmaxf(M, w.opmax[base + (size_t)c * g.m]);
+  for (int c = part; c < 2 * nch; c += NP) M = fmaxf(M, w.opmax[base + (size_t)c * g.m]);
   double Z = 0.0;
-  for (int c = part; c < nch; c += 4) {
+  for (int c = part; c < 2 * nch; c += NP) {
     const float mc = w.opmax[base + (size_t)c * g.m];
     const double sc = w.opsum[base + (size_t)c * g.m];
     Z += mc == M ? sc : sc * exp((double)mc - (double)M);
@@ -264,11 +272,11 @@ __global__ __launch_bounds__(256) void k_obs_reduce(Geo g, Ws w) {
   __syncthreads();
   if (part == 0 && wr < g.m) {
     float Mt = pm[0][lane];
-    for (int p = 1; p < 4; ++p) Mt = fmaxf(Mt, pm[p][lane]);
+    for (int p = 1; p < NP; ++p) Mt = fmaxf(Mt, pm[p][lane]);
     double Zt = 0.0;
-    for (int p = 0; p < 4; ++p) {
+    for (int p = 0; p < NP; ++p) {
       const float mp = pm[p][lane];
-      if (mp == NEG) continue;  // a part without chunks
+      if (mp == NEG) continue;  // a part without entries
       Zt += mp == Mt ? ps[p][lane] : ps[p][lane] * exp((double)mp - (double)Mt);
     }
     w.oM[(size_t)(b * g.H + h) * g.m + wr] = Mt;
@@ -283,9 +291,9 @@ __global__ __launch_bounds__(256) void k_obs_pass(Geo g, Ws w, const void* Kin, 
   using M = MF<DT>;
   constexpr int LD = TileLD<DT>::v;
   constexpr int LDT = 32 + (DT ? 8 : 4);  // transposed value tile row stride (16-byte aligned rows)
-  __shared__ __align__(16) E KT[32 * LD];
-  __shared__ __align__(16) E VT[AKV_D * LDT];
-  __shared__ float scw[4][32];
+  __shared__ __align__(16) E KT[2][32 * LD];      // double-buffered tiles
+  __shared__ __align__(16) E VT[2][AKV_D * LDT];
+  __shared__ float scw[2][4][32];
   int idx = blockIdx.x;
   const int b = locate(g, OBS_CHUNK, 1, idx);
   const int S = g.S[b], P = S - g.W, D = g.D, m = g.m;
@@ -324,17 +332,34 @@ __global__ __launch_bounds__(256) void k_obs_pass(Geo g, Ws w, const void* Kin, 
   }
   const int tb = ch * OBS_CHUNK, te = min(S, tb + OBS_CHUNK);
   float* sc = w.sc + (size_t)g.prefS[b] * g.H + (size_t)h * S;
+  // Tile it sits in KT/VT[it & 1] and leaves its column sums in scw[it & 1];
+  // after the barrier that starts tile it, the next tile is stored into the
+  // other buffer and the column sums of tile it - 1 are final.  One barrier
+  // per tile.
   RowTile<DT> kt;
   PairTile<DT> vt;
   kt.load(X, tb, S);
   vt.load(Vx, tb, S);
-  for (int t0 = tb; t0 < te; t0 += 32) {
-    kt.store(KT, LD);
-    vt.store_t(VT, LDT);
+  kt.store(KT[0], LD);
+  vt.store_t(VT[0], LDT);
+  if (tb + 32 < te) {
+    kt.load(X, tb + 32, S);
+    vt.load(Vx, tb + 32, S);
+  }
+  int it = 0;
+  for (int t0 = tb; t0 < te; t0 += 32, ++it) {
+    const int cb = it & 1;
     __syncthreads();
+    if (it > 0 && threadIdx.x < 32 && t0 - 32 + threadIdx.x < S)
+      sc[t0 - 32 + threadIdx.x] = (scw[cb ^ 1][0][threadIdx.x] + scw[cb ^ 1][1][threadIdx.x] +
+                                   scw[cb ^ 1][2][threadIdx.x] + scw[cb ^ 1][3][threadIdx.x]) / (float)m;
     if (t0 + 32 < te) {
-      kt.load(X, t0 + 32, S);
-      vt.load(Vx, t0 + 32, S);
+      kt.store(KT[cb ^ 1], LD);
+      vt.store_t(VT[cb ^ 1], LDT);
+    }
+    if (t0 + 64 < te) {
+      kt.load(X, t0 + 64, S);
+      vt.load(Vx, t0 + 64, S);
     }
     float cs[16];
 #pragma unroll
@@ -346,7 +371,7 @@ __global__ __launch_bounds__(256) void k_obs_pass(Geo g, Ws w, const void* Kin, 
       f32x16 acc = {};
 #pragma unroll
       for (int s = 0; s < NKS; ++s) {
-        auto kb = M::load_lds(&KT[(lane & 31) * LD], kofs(M::KS, s, lane));
+        auto kb = M::load_lds(&KT[cb][(lane & 31) * LD], kofs(M::KS, s, lane));
         acc = M::mma(kb, qf[r][s], acc);
       }
       // alpha of the lane's row and tokens t0 + crow(e, lane).
@@ -380,7 +405,7 @@ __global__ __launch_bounds__(256) void k_obs_pass(Geo g, Ws w, const void* Kin, 
 #pragma unroll
         for (int db = 0; db < 4; ++db) {
           const int d = db * 32 + (lane & 31);
-          auto vb = M::load_lds(&VT[d * LDT + vt_pos(d, k0)], 0);
+          auto vb = M::load_lds(&VT[cb][d * LDT + vt_pos(d, k0)], 0);
           yacc[r][db] = M::mma(ah, vb, yacc[r][db]);
           if constexpr (DT == 1) yacc[r][db] = M::mma(alo, vb, yacc[r][db]);
         }
@@ -390,10 +415,15 @@ __global__ __launch_bounds__(256) void k_obs_pass(Geo g, Ws w, const void* Kin, 
     // two rows of each half; lanes 0-15 and 32-47 hold tokens crow(l & 15, l).
     float csum = row_reduce_scatter16(cs, lane);
     csum += lane_xor<16>(csum);
-    if ((lane & 16) == 0) scw[wave][crow(lane & 15, lane)] = csum;
-    __syncthreads();
-    if (threadIdx.x < 32 && t0 + threadIdx.x < S)
-      sc[t0 + threadIdx.x] = (scw[0][threadIdx.x] + scw[1][threadIdx.x] + scw[2][threadIdx.x] + scw[3][threadIdx.x]) / (float)m;
+    if ((lane & 16) == 0) scw[cb][wave][crow(lane & 15, lane)] = csum;
+  }
+  __syncthreads();
+  {
+    const int tl = tb + 32 * (it - 1);  // first token of the last tile
+    const int cl = (it - 1) & 1;
+    if (threadIdx.x < 32 && tl + threadIdx.x < S)
+      sc[tl + threadIdx.x] = (scw[cl][0][threadIdx.x] + scw[cl][1][threadIdx.x] + scw[cl][2][threadIdx.x] +
+                              scw[cl][3][threadIdx.x]) / (float)m;
   }
   // Partial outputs of this chunk.
   float* yp = w.ypart + ((size_t)(g.prefC[b] * g.H + h * nch + ch)) * m * D;
@@ -418,9 +448,18 @@ __global__ __launch_bounds__(128) void k_obs_yreduce(Geo g, Ws w) {
   const int D = g.D;
   __shared__ float red[2];
   for (int d = threadIdx.x; d < D; d += blockDim.x) {
+    // Chunks added in order, their partial outputs loaded 16 at a time.
+    const float* yp = w.ypart + (((size_t)(g.prefC[b] * g.H + h * nch)) * g.m + wr) * D + d;
+    const size_t cs = (size_t)g.m * D;
     float y = 0.0f;
-    for (int c = 0; c < nch; ++c)
-      y += w.ypart[(((size_t)(g.prefC[b] * g.H + h * nch + c)) * g.m + wr) * D + d];
+    for (int c0 = 0; c0 < nch; c0 += 16) {
+      float v[16];
+#pragma unroll
+      for (int u = 0; u < 16; ++u) v[u] = c0 + u < nch ? yp[(size_t)(c0 + u) * cs] : 0.0f;
+#pragma unroll
+      for (int u = 0; u < 16; ++u)
+        if (c0 + u < nch) y += v[u];
+    }
     size_t o = ((size_t)bh * g.m + wr) * D + d;
     w.Y[o] = y;
     uint16_t hi = f2bf(y);
@@ -438,13 +477,13 @@ hipError_t launch_obs(const Geo& g, const Ws& w, const void* K, const void* V, c
   int nblk = g.H * g.prefC[g.B];
   const bool r2 = g.m > 128;  // 4 waves x 2 row blocks of 32 for up to 256 rows
   if (g.dtype == 1) {
-    if (r2) launch("k_obs_stats", k_obs_stats<1, 2>, dim3(nblk), dim3(256), 0, st, g, w, K, Q);
-    else launch("k_obs_stats", k_obs_stats<1, 1>, dim3(nblk), dim3(256), 0, st, g, w, K, Q);
+    if (r2) launch("k_obs_stats", k_obs_stats<1, 2>, dim3(2 * nblk), dim3(256), 0, st, g, w, K, Q);
+    else launch("k_obs_stats", k_obs_stats<1, 1>, dim3(2 * nblk), dim3(256), 0, st, g, w, K, Q);
   } else {
-    if (r2) launch("k_obs_stats", k_obs_stats<0, 2>, dim3(nblk), dim3(256), 0, st, g, w, K, Q);
-    else launch("k_obs_stats", k_obs_stats<0, 1>, dim3(nblk), dim3(256), 0, st, g, w, K, Q);
+    if (r2) launch("k_obs_stats", k_obs_stats<0, 2>, dim3(2 * nblk), dim3(256), 0, st, g, w, K, Q);
+    else launch("k_obs_stats", k_obs_stats<0, 1>, dim3(2 * nblk), dim3(256), 0, st, g, w, K, Q);
   }
-  launch("k_obs_reduce", k_obs_reduce, dim3(g.B * g.H * ((g.m + 63) / 64)), dim3(256), 0, st, g, w);
+  launch("k_obs_reduce", k_obs_reduce, dim3(g.B * g.H * ((g.m + 63) / 64)), dim3(1024), 0, st, g, w);
   if (g.dtype == 1) {
     if (r2) launch("k_obs_pass", k_obs_pass<1, 2>, dim3(nblk), dim3(256), 0, st, g, w, K, V, Q);
     else launch("k_obs_pass", k_obs_pass<1, 1>, dim3(nblk), dim3(256), 0, st, g, w, K, V, Q);
