@@ -133,6 +133,7 @@ struct Ws {
   float* fixb;          // same layout: the best fp32 score the contraction found for the token
   int32_t* fixcount;    // [side][b][h] fixup list lengths
   float* gpos;          // [side][b][h][S_b] stored coefficient as fp32
+  float* xn2;           // [side][b][h][S_b] squared norm of the token (fp32 sum of squares)
   float* u;             // [side][b][h][S_b] utility, -1 for anchors
   uint8_t* sel;         // [side][b][h][S_b] residual flags
   uint4* srec;          // [slots] record of the token placed at a sorted slot (position and flags, anchors, coefficients)

@@ -66,7 +66,7 @@ struct anchorkv_plan {
   size_t cache_bytes;
   // encode workspace offsets
   size_t w_opmax, w_opsum, w_oM, w_oiZ, w_oiZ64, w_ypart, w_Y, w_Yhi, w_Ylo, w_ynorm, w_sc, w_rank, w_flag, w_sband, w_sbscore, w_sstate, w_sghist, w_scand, w_rkey, w_rpos, w_slcnt, w_QA, w_apos,
-      w_fix, w_fixcount, w_gpos, w_u, w_sel, w_srec, w_bhist, w_bstate, w_bcval, w_bcpos, w_tiecnt, w_shist, w_wcnt;
+      w_fix, w_fixcount, w_gpos, w_xn2, w_u, w_sel, w_srec, w_bhist, w_bstate, w_bcval, w_bcpos, w_tiecnt, w_shist, w_wcnt;
   size_t ws_bytes;
   // decode workspace offsets
   size_t d_SK, d_RK, d_part, d_asc, d_atop;
@@ -293,6 +293,7 @@ extern "C" anchorkv_status anchorkv_plan_create(const anchorkv_config* cfg, int3
   p->w_fix = Wl.add(8 * 2 * TS);
   p->w_fixcount = Wl.add(4 * 2 * (size_t)H * batch);
   p->w_gpos = Wl.add(4 * 2 * TS);
+  p->w_xn2 = Wl.add(4 * 2 * TS);
   p->w_u = Wl.add(4 * 2 * TS);
   p->w_sel = Wl.add(2 * TS);
   p->w_srec = Wl.add(16 * TW * 64);
@@ -393,6 +394,7 @@ static akv::Ws ws_ptrs(const anchorkv_plan* p, void* base) {
   w.fixb = (float*)(w.fixt + 2 * (size_t)p->geo.H * p->geo.prefS[p->geo.B]);
   w.fixcount = at<int32_t>(base, p->w_fixcount);
   w.gpos = at<float>(base, p->w_gpos);
+  w.xn2 = at<float>(base, p->w_xn2);
   w.u = at<float>(base, p->w_u);
   w.sel = at<uint8_t>(base, p->w_sel);
   w.srec = at<uint4>(base, p->w_srec);

@@ -214,6 +214,7 @@ __global__ __launch_bounds__(256) void k_assign(Geo g, Ws w, Cache c, const void
     if (lane < 32 && t < S) {
       const size_t po = (size_t)g.prefS[b] * g.H + (size_t)h * S + t;
       int32_t* apos = w.apos + (size_t)side * g.H * g.prefS[g.B] + po;
+      w.xn2[(size_t)side * g.H * g.prefS[g.B] + po] = ss[n];  // the token's squared norm (fp32 sum)
       const int rk = w.rank[po];
       if (rk >= 0) {
         *apos = rk;

@@ -6,7 +6,9 @@
 // Coefficient (bit-exact with the CPU oracle): d = sequential fp64 dot of the
 // token and its anchor, gamma = d / ||a||^2 in fp64, rounded to fp32 and, for
 // a bf16 cache, to bf16 (round to nearest even).  Anchor positions keep
-// gamma = 1.
+// gamma = 1.  For a bf16 cache an fp32 estimate of d with a proven error
+// bound decides the rounded value when its whole error interval rounds alike
+// (nearly always); otherwise the sequential fp64 sum is formed.
 //
 // Utilities (fp32, no positional rotation on this path, R_t = I):
 //   uK_t = (1/m) sum_w alpha_wt^2 (q_w . rK_t)^2 / D * ||v_t - y_w||^2
@@ -27,8 +29,16 @@ namespace akv {
 
 constexpr int EPI_TOK = 256;  // tokens per workgroup: 8 tiles of 32
 
+// The canonical sequential fp64 dot of a token row and an anchor row, read
+// from memory: the rare fallback of the certified coefficient, kept out of
+// line so that it holds no registers in the caller.
+template <int DT>
+__device__ __attribute__((noinline)) double dot64_rows(const typename Elem<DT>::T* x, const typename Elem<DT>::T* a) {
+  return dot64_seq<DT, true>(x, a, AKV_D);
+}
+
 template <int DT, int R>
-__global__ __launch_bounds__(256) void k_epilogue(Geo g, Ws w, Cache c, const void* Kin, const void* Vin,
+__global__ __launch_bounds__(256, R == 1 ? 2 : 1) void k_epilogue(Geo g, Ws w, Cache c, const void* Kin, const void* Vin,
                                                   const void* Qin) {
   using E = typename Elem<DT>::T;
   using M = MF<DT>;
@@ -69,7 +79,7 @@ __global__ __launch_bounds__(256) void k_epilogue(Geo g, Ws w, Cache c, const vo
   // ---- coefficients: thread = token tb + tid, both sides.  A token with
   // an invalid assignment raises the error bit and uses anchor 0; the
   // K side marks utility candidates (non-anchors), the V side also leaves
-  // ||rV||^2 and ||v||^2.
+  // ||rV||^2 and ||v||^2 (the latter from the assignment pass).
   {
     const int tl = threadIdx.x, t = tb + tl;
     const bool in = t < S;
@@ -96,25 +106,61 @@ __global__ __launch_bounds__(256) void k_epilogue(Geo g, Ws w, Cache c, const vo
       float gb = 1.0f;
       if (in && rk < 0) {
         if (bad) atomicOr(&c.header[2], 4u);
-        const double d = dot64_seq<DT, true>(xe, ae, D);
-        const double g64 = n > 0.0 ? d / n : 0.0;
-        gb = Elem<DT>::round_coef((float)g64);
+        bool done = false;
+        if constexpr (DT == 1) {
+          // Certified shortcut for a bf16 cache.  Four interleaved fp32 FMA
+          // chains over the exact bf16 products give d32 with |d32 - d| <=
+          // 35 u (1 + 35 u) sum|x_j a_j| <= 36 u sqrt(xx n) (u = 2^-24; 32
+          // steps per chain and three combining adds; xx is the token's fp32
+          // sum of squares, within 130 u of the exact one), and the
+          // sequential fp64 sum lies within 2^-44 sqrt(xx n) of d.  The
+          // stored value bf16(fp32(fl64(d / n))) is monotone in d, so when
+          // both ends of the interval round to the same bits, those are the
+          // canonical bits; otherwise the sequential fp64 chain decides.
+          float e0 = 0.0f, e1 = 0.0f, e2 = 0.0f, e3 = 0.0f;
+#pragma unroll
+          for (int j = 0; j < AKV_D; j += 4) {
+            e0 = fmaf(Elem<DT>::get(xe, j), Elem<DT>::get(ae, j), e0);
+            e1 = fmaf(Elem<DT>::get(xe, j + 1), Elem<DT>::get(ae, j + 1), e1);
+            e2 = fmaf(Elem<DT>::get(xe, j + 2), Elem<DT>::get(ae, j + 2), e2);
+            e3 = fmaf(Elem<DT>::get(xe, j + 3), Elem<DT>::get(ae, j + 3), e3);
+          }
+          const float f32 = (e0 + e1) + (e2 + e3);
+          const double d32 = (double)f32;
+          if (n > 0.0 && __builtin_isfinite(f32)) {
+            // + 128 * 2^-126 for products flushed to zero below the fp32
+            // normal range
+            const double E = 2.1482e-6 * sqrt((double)w.xn2[side * TS + po + tc] * n) + 3e-36;
+            const float lo = Elem<DT>::round_coef((float)((d32 - E) / n));
+            const float hi = Elem<DT>::round_coef((float)((d32 + E) / n));
+            if (__float_as_uint(lo) == __float_as_uint(hi)) {
+              gb = lo;
+              done = true;
+            }
+          } else if (!(n > 0.0)) {
+            gb = 0.0f;  // canonical gamma of a zero anchor
+            done = true;
+          }
+        }
+        if (!done) {
+          const double d = DT == 1 ? dot64_rows<DT>(xrow, arow) : dot64_seq<DT, true>(xe, ae, D);
+          const double g64 = n > 0.0 ? d / n : 0.0;
+          gb = Elem<DT>::round_coef((float)g64);
+        }
       }
       if (in) w.gpos[side * TS + po + t] = gb;
       if (side == 0) {
         gK_s[tl] = in ? gb : 0.0f;
         aK_s[tl] = (in && rk < 0) ? a : -1;  // -1: no utility (anchor or past S)
       } else {
-        float rs = 0.0f, vs = 0.0f;
+        float rs = 0.0f;
 #pragma unroll
         for (int j = 0; j < AKV_D; ++j) {
-          const float x = Elem<DT>::get(xe, j);
-          const float r = fmaf(-gb, Elem<DT>::get(ae, j), x);
+          const float r = fmaf(-gb, Elem<DT>::get(ae, j), Elem<DT>::get(xe, j));
           rs = fmaf(r, r, rs);
-          vs = fmaf(x, x, vs);
         }
+        vn_s[tl] = w.xn2[TS + po + tc];
         rv2_s[tl] = (in && rk < 0) ? rs : 0.0f;
-        vn_s[tl] = vs;
       }
     }
   }
