@@ -115,3 +115,47 @@ def test_assignment_exact_ties_and_zero_tokens(dtype):
     Vh = R.reconstruct(layer.V[0].float().numpy(), enc, "V", G, cfg.seed)
     ref = R.attention(Kh, Vh, layer.q[0, 0].float().numpy())
     assert np.abs(out[0].cpu().numpy() - ref).max() <= (1e-4 if dtype == "f32" else 2e-3)
+
+
+def test_coefficient_rounding_boundaries():
+    """Stored coefficients at and next to bf16 rounding boundaries (Sec. 3.1
+    Eq. projection; the coefficient is rounded to the cache dtype): with the
+    anchor a = (1, ..., 1), tokens 1 + e_0/2 and 1 + 3 e_0/2 give gamma =
+    1 + 2^-8 and 1 + 3 * 2^-8, exact ties between bf16 neighbours (to even:
+    1 and 1 + 2^-6), which the kernel's certified fp32 estimate cannot decide,
+    so the sequential fp64 sum does; tokens with one more coordinate at
+    1 +- 2^-7 sit 2^-14 from a tie and are decided by the estimate."""
+    wl = _wl("gamma_ties", seq_lens=[600], anchor_count=64, anchor_frac=0.0, n_outlier=0)
+    print("[edge] coefficient rounding boundaries", flush=True)
+    layer = synth.make_layer(wl)
+    S, W = wl.seq_lens[0], wl.window
+    one = torch.ones(wl.D, dtype=torch.bfloat16)
+    rows = []
+    for c0 in (1.5, 2.5):
+        for c1 in (1.0, 1.0078125, 0.9921875):
+            r = one.clone()
+            r[0] = c0
+            r[1] = c1
+            rows.append(r)
+    for X in (layer.K[0], layer.V[0]):
+        for h in range(wl.H):
+            X[h, 5] = one
+            for i, r in enumerate(rows):
+                X[h, 100 + 4 * i:104 + 4 * i] = r
+    base = np.r_[[5], np.arange(200, 200 + 5 * (64 - W - 1), 5)]
+    assert base.size == 64 - W
+    ov = np.stack([np.r_[base, np.arange(S - W, S)] for _ in range(wl.H)]).astype(np.int32)
+    cfg = make_cfg(wl)
+    plan = N.Plan(cfg, wl.seq_lens)
+    cache, ws, dws = gpu_encode(plan, layer, override=ov)
+    enc = oracle_encode(cfg, layer, 0, anchor_override=ov)
+    exp = akv.export(plan, cache.cpu().numpy(), 0, 0)
+    assert_request_parity(exp, enc, cfg)
+    for side in ("k", "v"):
+        a, gm = exp["a_" + side], exp["gamma_" + side]
+        assert (a[:, 100:124] == 0).all()
+        # (c0, c1) = (1.5, 1), (1.5, 1 + 2^-7), (1.5, 1 - 2^-7), then c0 = 2.5:
+        # exact ties to even, then 2^-14 above and below the tie
+        want = [1.0, 1.0078125, 1.0, 1.015625, 1.015625, 1.0078125]
+        got = [float(gm[0, 100 + 4 * i]) for i in range(6)]
+        assert got == want, (side, got)
