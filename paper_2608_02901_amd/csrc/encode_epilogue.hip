@@ -18,16 +18,16 @@
 // logits and v_t . y_w on MFMA; anchors get u = -1 and never compete.
 //
 // Schedule: first the 2 x EPI_TOK coefficient chains of the workgroup's
-// tokens (two per thread, spread over all waves), then the utilities tile by
+// tokens (four per thread, spread over all waves), then the utilities tile by
 // tile (32 tokens), with the observation rows staged in LDS once, each wave's
-// y fragments and its rows' softmax constants held in registers for all
+// y fragments in registers and its rows' softmax constants in LDS for all
 // tiles, and the next tile's keys and values loaded while the current tile is
 // processed.
 #include "akv_common.h"
 
 namespace akv {
 
-constexpr int EPI_TOK = 256;  // tokens per workgroup: 8 tiles of 32
+constexpr int EPI_TOK = 512;  // tokens per workgroup: 16 tiles of 32
 
 // The canonical sequential fp64 dot of a token row and an anchor row, read
 // from memory: the rare fallback of the certified coefficient, kept out of
@@ -76,12 +76,15 @@ __global__ __launch_bounds__(256, R == 1 ? 2 : 1) void k_epilogue(Geo g, Ws w, C
     *(uint4*)(&QS[r * LD + col]) = *(const uint4*)(Q + (size_t)r * D + col);
   }
 
-  // ---- coefficients: thread = token tb + tid, both sides.  A token with
+  // ---- coefficients: thread = token tb + tid + 256 p (p < EPI_TOK / 256),
+  // both sides.  A token with
   // an invalid assignment raises the error bit and uses anchor 0; the
   // K side marks utility candidates (non-anchors), the V side also leaves
   // ||rV||^2 and ||v||^2 (the latter from the assignment pass).
   {
-    const int tl = threadIdx.x, t = tb + tl;
+#pragma unroll 1
+  for (int pp = 0; pp < EPI_TOK / 256; ++pp) {
+    const int tl = threadIdx.x + 256 * pp, t = tb + tl;
     const bool in = t < S;
     const int tc = in ? t : S - 1;
     const int rk = w.rank[po + tc];
@@ -163,6 +166,7 @@ __global__ __launch_bounds__(256, R == 1 ? 2 : 1) void k_epilogue(Geo g, Ws w, C
         rv2_s[tl] = (in && rk < 0) ? rs : 0.0f;
       }
     }
+  }
   }
 
   // ---- utilities.  Wave rows: row block rb = wave + 4 r; lane l supplies
@@ -291,7 +295,8 @@ __global__ __launch_bounds__(256, R == 1 ? 2 : 1) void k_epilogue(Geo g, Ws w, C
   }
   __syncthreads();
   {
-    const int tl = threadIdx.x, t = tb + tl;
+   for (int tl = threadIdx.x; tl < EPI_TOK; tl += 256) {
+    const int t = tb + tl;
     if (t < S) {
       float uk = -1.0f, uv = -1.0f;
       if (aK_s[tl] >= 0) {
@@ -303,6 +308,7 @@ __global__ __launch_bounds__(256, R == 1 ? 2 : 1) void k_epilogue(Geo g, Ws w, C
       w.u[po + t] = uk;
       w.u[TS + po + t] = uv;
     }
+   }
   }
 }
 
