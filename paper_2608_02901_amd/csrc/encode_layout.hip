@@ -358,14 +358,13 @@ __global__ __launch_bounds__(256) void k_codec(Geo g, Ws w, Cache c, const void*
   const int nw = (S + 63) / 64;
   const int h = wid / nw, word = wid % nw;
   const size_t wo = (size_t)g.prefW[b] * g.H + (size_t)h * nw + word;
-  // The word's mask, first residual slot and the positions of its 64 slots
-  // are read together (the positions without waiting for the mask).
+  // The word's mask, first residual slot and the records of its 64 slots
+  // (position, anchors, coefficients, as the scatter left them) are read
+  // together, the records without waiting for the mask.
   unsigned long long mask = (side ? c.maskV : c.maskK)[wo];
   int slot = (side ? c.pcV : c.pcK)[wo];
-  const int tj = min(max(c.pos[slot_base(g, b, h) + (size_t)word * 64 + lane], 0), S - 1);
+  const uint4 rec = w.srec[slot_base(g, b, h) + (size_t)word * 64 + lane];
   if (!mask) return;
-  const size_t po = (size_t)g.prefS[b] * g.H + (size_t)h * S;
-  const size_t TS = (size_t)g.prefS[g.B] * g.H;
   const size_t ko = (size_t)g.prefK[b] * g.H + (size_t)h * k;
   const size_t xoff = ((size_t)g.prefS[b] * g.H + (size_t)h * S) * D;
   const E* X = (const E*)(side ? Vin : Kin) + xoff;
@@ -373,13 +372,11 @@ __global__ __launch_bounds__(256) void k_codec(Geo g, Ws w, Cache c, const void*
   uint8_t* codes = side ? c.codesV : c.codesK;
   float* scales = side ? c.scalesV : c.scalesK;
   const float s0 = hsign(g.seed_sign, 2 * lane), s1 = hsign(g.seed_sign, 2 * lane + 1);
-  // Anchor and coefficient of every flagged slot of the word, one lane each.
-  int aj = 0;
-  float gj = 0.0f;
-  if ((mask >> lane) & 1ull) {
-    aj = min(max(w.apos[side * TS + po + tj], 0), k - 1);
-    gj = w.gpos[side * TS + po + tj];
-  }
+  // Position, anchor and coefficient of every slot of the word, one lane each
+  // (clamped: padding slots of the last word hold no record and no flag).
+  const int tj = min((int)(rec.x & 0x3FFFFFFFu), S - 1);
+  const int aj = min((int)(side ? rec.y >> 16 : rec.y & 0xFFFFu), k - 1);
+  const float gj = __uint_as_float(side ? rec.w : rec.z);
   // Up to CB flagged slots per round; their token and anchor coordinates
   // (2 per lane) are loaded together before any is encoded.
   constexpr int CB = 4;
