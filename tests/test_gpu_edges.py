@@ -159,3 +159,33 @@ def test_coefficient_rounding_boundaries():
         want = [1.0, 1.0078125, 1.0, 1.015625, 1.015625, 1.0078125]
         got = [float(gm[0, 100 + 4 * i]) for i in range(6)]
         assert got == want, (side, got)
+
+
+def test_selection_and_budget_overflow_paths():
+    """Uniform observation scores (Q_obs = 0: every logit is 0, so every
+    position before the window gets the same pooled score up to fp32
+    rounding).  The first-digit bin of the top-n cut then holds all P >
+    SEL_CMAX positions (the exact cut is taken over all positions), the band
+    around the cut overflows (the fp32 order decides, ties to the lower
+    position; the header records bit 32), and every key utility is 0, so the
+    budget's candidate list overflows too (its cut and tie counts are taken
+    over all utilities).  The anchor list must be valid, and with those anchors
+    the rest of the encode must match the oracle."""
+    wl = _wl("sel_overflow", H=2, Hq=4, seq_lens=[40000], anchor_frac=0.02)
+    print("[edge] selection and budget overflow paths", flush=True)
+    layer = synth.make_layer(wl)
+    layer.Qobs[0].zero_()
+    cfg = make_cfg(wl)
+    plan = N.Plan(cfg, wl.seq_lens)
+    cache, ws, dws = gpu_encode(plan, layer)
+    flags = int(cache[8:12].view(torch.int32).item())
+    assert flags & 32 and not flags & ~(32 | 64), flags
+    exp = akv.export(plan, cache.cpu().numpy(), 0, 0)
+    S, W, k = wl.seq_lens[0], wl.window, plan.requests[0].anchors
+    anc = exp["anchors"]
+    assert anc.shape == (wl.H, k)
+    for h in range(wl.H):
+        assert (np.diff(anc[h]) > 0).all() and anc[h, 0] >= 0
+        assert (anc[h, -W:] == np.arange(S - W, S)).all()
+    enc = oracle_encode(cfg, layer, 0, anchor_override=anc)
+    assert_request_parity(exp, enc, cfg)
