@@ -1176,9 +1176,12 @@ __global__ __launch_bounds__(256) void k_dec_merge(Geo g, DecWs dw, void* out, i
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int cq = tid & 31, sg = tid >> 5;
   const float* pb = dw.part + ((size_t)g.prefSp[b] * g.Hq + (size_t)jq * nrec) * PS;
-  float M = -INFINITY;
-  for (int s = tid; s < nrec; s += 256) M = fmaxf(M, pb[(size_t)s * PS]);
-  // First round of record values, issued before the max is known.
+  // Maxima and sums of the first 256 records are loaded once, beside the
+  // first round of record values (issued before the max is known).
+  const float m0 = tid < nrec ? pb[(size_t)tid * PS] : -INFINITY;
+  const float l0 = tid < nrec ? pb[(size_t)tid * PS + 1] : 0.0f;
+  float M = m0;
+  for (int s = tid + 256; s < nrec; s += 256) M = fmaxf(M, pb[(size_t)s * PS]);
   float4 v[RCH / 8];
   float mv[RCH / 8];
 #pragma unroll
@@ -1191,8 +1194,8 @@ __global__ __launch_bounds__(256) void k_dec_merge(Geo g, DecWs dw, void* out, i
   if (lane == 0) red[wave] = M;
   __syncthreads();
   M = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
-  float l = 0.0f;
-  for (int s = tid; s < nrec; s += 256) l = fmaf(__builtin_amdgcn_exp2f(pb[(size_t)s * PS] - M), pb[(size_t)s * PS + 1], l);
+  float l = tid < nrec ? __builtin_amdgcn_exp2f(m0 - M) * l0 : 0.0f;
+  for (int s = tid + 256; s < nrec; s += 256) l = fmaf(__builtin_amdgcn_exp2f(pb[(size_t)s * PS] - M), pb[(size_t)s * PS + 1], l);
   float o[4] = {0.0f, 0.0f, 0.0f, 0.0f};
   for (int c0 = 0; c0 < nrec; c0 += RCH) {
     if (c0 > 0) {
