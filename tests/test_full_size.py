@@ -237,3 +237,25 @@ def test_workload5_ragged16():
     err = _decode_property(plan, cache, dws, lay, picks + [int(order[-1])], steps=1, append=False)
     print(f"[full] workload 5: decode vs dense fp64 attention max|err| {err:.3g}", flush=True)
     assert err <= 2e-3
+
+
+def test_long_sequence_more_than_256_splits():
+    """One request of 540000 tokens: 264 splits of 2048 slots plus the tail
+    record, so the merge takes its second round of records (more than one per
+    thread).  decode_step over two appended tokens equals fp64 attention over
+    the dense reconstruction."""
+    wl = synth.Workload("long-540K", H=1, Hq=4, D=128, seq_lens=[540000], dtype="bf16", anchor_frac=0.02,
+                        budget=0.05, n_centers=256, steps=2, append=True, seed=12)
+    print(f"[full] {wl.name}", flush=True)
+    lay = _layer_on_gpu(wl, steps=2)
+    cfg = make_cfg(wl, max_append=2)
+    plan = N.Plan(cfg, wl.seq_lens)
+    assert math.ceil(wl.seq_lens[0] / 2048) + 1 > 256
+    cache, ws, dws = plan.alloc("cuda")
+    keep = akv.encode(plan, lay.K[0], lay.V[0], lay.Qobs[0], cache, ws)
+    torch.cuda.synchronize()
+    del keep
+    assert _header_flags(cache) == 0
+    err = _decode_property(plan, cache, dws, lay, [0], steps=2, append=True)
+    print(f"[full] {wl.name}: decode_step vs dense fp64 attention max|err| {err:.3g}", flush=True)
+    assert err <= 2e-3
