@@ -25,12 +25,16 @@
  *              assignment (exhaustive search, closed-form special cases,
  *              projection orthogonality), decode attention (all-anchor case
  *              equals dense attention; output-error theorem of App. A.4),
- *              selector (brute force on tiny inputs).
+ *              selector (brute force on tiny inputs; the raw score against
+ *              column means of scipy's causal softmax and the pool against a
+ *              centred zero-padded numpy convolution at kappa = 1..9),
+ *              utilities (numpy brute force over m = 6 observation rows, each
+ *              with its own causal softmax and y_w; finite-difference test of
+ *              the two-channel expansion, Eq. channels).  Planted mistakes in
+ *              a copy of this file (off-centre or renormalised pool, one-row
+ *              sums, offset-major rows, alpha for alpha^2) fail these pins.
  *   parity unpinned beyond self-consistency: the absmax scale readings of the
- *              codec (Sec. 3.1 / App. A.1 leave the scale rule ambiguous) and
- *              the utility values (Eq. utilities; the paper prints none) --
- *              the utilities are additionally checked by a finite-difference
- *              test of the two-channel expansion (Eq. channels).
+ *              codec (Sec. 3.1 / App. A.1 leave the scale rule ambiguous).
  */
 #include <math.h>
 #include <stdint.h>
