@@ -42,6 +42,9 @@ struct Geo {
   int prefNV[AKV_MAXB + 1];  // sum of value residual counts
   int prefKp[AKV_MAXB + 1];  // sum of k rounded up to 4 (anchor-score table rows)
   int prefAB[AKV_MAXB + 1];  // sum of ceil(k/256) (256-anchor blocks per head)
+  int prefC64[AKV_MAXB + 1]; // sum of fp64 observation chunks per head
+  int oc64;                  // tokens per fp64 observation chunk
+  int mpad;                  // m rounded up to 16 (rows of the fp64 partial outputs)
   int dsplit;                // decode split length (sorted slots per workgroup)
 };
 
@@ -58,6 +61,25 @@ constexpr int SORT_CHUNK = 2048;  // tokens per counting-sort chunk
 constexpr int SEL_SLICE = 4096;   // positions per workgroup of the selection passes
 constexpr int SEL_CMAX = 32768;   // first-digit candidates kept for the exact top-n cut
 constexpr int SEL_CAND = 1024;    // hash candidates kept in the uniform share's bin
+constexpr int BAND_CAP = 65536;   // residual-budget candidates re-scored in fp64 per request and side
+constexpr int BST_N = 8;          // budget state fields per request and side (BST_*)
+enum : int {
+  BST_NCAND = 0,  // first-digit candidates appended
+  BST_T = 1,      // bits of the N-th largest fp32 utility
+  BST_REMAIN = 2, // count still to take at that value (fp32 order)
+  BST_NBAND = 3,  // band members listed (more than BAND_CAP: overflow)
+  BST_A = 4,      // bits of min{lower bound : u >= T}  (no exact utility below it is selected)
+  BST_B = 5,      // bits of max{upper bound : u <= T}  (every exact utility above it is selected)
+  BST_NEED = 6    // band members the fp32 order selected (= selections the band must supply)
+};
+// Cache header flag bits (header[2]).
+enum : uint32_t {
+  HDR_BAD_OVERRIDE = 1u,  // anchor override broke its rules
+  HDR_SEL_COUNT = 2u,     // anchor selection count mismatch
+  HDR_BAD_ASSIGN = 4u,    // a token without a valid anchor index
+  HDR_BAND_OVERFLOW = 8u, // a budget band above BAND_CAP: that cut fell back to fp32 order
+  HDR_BUDGET_CUT = 16u    // the budget's radix select found no cut (fewer candidates than N)
+};
 // Selection state fields per (request, head), zeroed at the start of an encode.
 enum : int {
   SS_PREFIX = 0,  // bits of the n_top-th largest pooled fp32 score
@@ -110,12 +132,18 @@ struct Ws {
   double* opsum;        // [b][h][chunk][2][m] partial sum of exp (fp64)
   float* oM;            // [b][h][m] row max (scaled logits)
   float* oiZ;           // [b][h][m] 1 / sum exp
-  double* oiZ64;        // [b][h][m] the same in fp64 (selection near-ties)
-  float* ypart;         // [b][h][chunk][m][D] partial observation outputs
-  float* Y;             // [b][h][m][D]
+  double* o64M;         // [b][h][chunk64][mpad] fp64 pass: chunk row max of the logits
+  double* o64Z;         // [b][h][chunk64][mpad] chunk sum of exp(l - chunk max)
+  double* o64O;         // [b][h][chunk64][mpad/16][8][4][64] chunk outputs (unnormalized, lane order)
+  double* M64;          // [b][h][m] row max of the fp64 logits
+  double* Z64;          // [b][h][m] sum_t exp(l_wt - M_w)
+  double* Y64;          // [b][h][m][D] y_w in fp64
+  float* Y;             // [b][h][m][D] fp32 rounding of y_w
   uint16_t* Yhi;        // [b][h][m][D] bf16 split of Y: Y ~ hi + lo
   uint16_t* Ylo;
-  float* ynorm;         // [b][h][m] ||y_w||^2
+  float* ynorm;         // [b][h][m] ||y_w||^2 (fp32 rounding of the fp64 sum)
+  float* cw;            // [b][h][m] (M_w + ln Z_w) log2(e), fp32
+  float* qn;            // [b][h][m] ||q_w||, rounded up
   float* sc;            // [b][h][S_b] selector score, then pooled score
   int32_t* rank;        // [b][h][S_b] anchor index of an anchor position, -1 otherwise
   uint8_t* flag;        // [b][h][S_b] selection marks
@@ -135,10 +163,14 @@ struct Ws {
   float* gpos;          // [side][b][h][S_b] stored coefficient as fp32
   float* xn2;           // [side][b][h][S_b] squared norm of the token (fp32 sum of squares)
   float* u;             // [side][b][h][S_b] utility, -1 for anchors
+  float* uL;            // [side][b][h][S_b] proven lower bound of the fp64 utility
+  float* uU;            // [side][b][h][S_b] proven upper bound
   uint8_t* sel;         // [side][b][h][S_b] residual flags
   uint4* srec;          // [slots] record of the token placed at a sorted slot (position and flags, anchors, coefficients)
   uint32_t* bhist;      // [b][side][4096] first-digit histogram of the utilities (zeroed at the start of an encode)
-  int32_t* bstate;      // [b][side][4]: candidates appended, threshold bits, count to take at the threshold, -
+  int32_t* bstate;      // [b][side][BST_N] budget state (fields BST_*)
+  int32_t* bandpos;     // [b][side][BAND_CAP] flattened (h, t) of the band members
+  double* bandu;        // [b][side][BAND_CAP] their fp64 utilities
   float* bcval;         // [b][side][BCMAX] utilities in the threshold's first-digit bin
   int32_t* bcpos;       // [b][side][BCMAX] their flattened (h, t) index
   int32_t* tiecnt;      // [b][side][nchunk] threshold ties in the earlier chunks
@@ -441,10 +473,15 @@ __device__ inline int block_excl_scan(int v, int* tmp /* >= 16 ints */, int& tot
 
 // Radix digit search over a 4096-bin histogram: the bin where the running
 // count (from the top when `desc`, else from the bottom) reaches `need`.
-// Writes (bin, count before it) to out[0..1].  Whole workgroup.
+// Writes (bin, count before it) to out[0..1], or (-1, 0) when the total is
+// below `need`.  Whole workgroup.
 __device__ inline void digit_pick(const uint32_t* hist, int nbin, int need, bool desc, int* tmp, int* out) {
   const int tid = threadIdx.x, nt = blockDim.x;
   const int per = (nbin + nt - 1) / nt;
+  if (tid == 0) {  // stays (-1, 0) when the counts never reach `need`
+    out[0] = -1;
+    out[1] = 0;
+  }
   int loc = 0;
   for (int i = 0; i < per; ++i) {
     const int bin = tid * per + i;

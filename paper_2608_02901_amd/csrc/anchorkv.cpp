@@ -18,12 +18,14 @@
 namespace akv {
 hipError_t launch_init(const Geo& g, const Cache& c, const Ws& w, hipStream_t st);
 hipError_t launch_obs(const Geo& g, const Ws& w, const void* K, const void* V, const void* Q, hipStream_t st);
+hipError_t launch_obs64(const Geo& g, const Ws& w, const void* K, const void* V, const void* Q, hipStream_t st);
 hipError_t launch_select(const Geo& g, const Ws& w, const Cache& c, const void* K, const void* V, const void* Q,
                          const int32_t* ovr, hipStream_t st);
 hipError_t launch_assign(const Geo& g, const Ws& w, const Cache& c, const void* K, const void* V, hipStream_t st);
 hipError_t launch_epilogue(const Geo& g, const Ws& w, const Cache& c, const void* K, const void* V, const void* Q,
                            hipStream_t st);
-hipError_t launch_budget(const Geo& g, const Ws& w, hipStream_t st);
+hipError_t launch_budget(const Geo& g, const Ws& w, const Cache& c, const void* K, const void* V, const void* Q,
+                         hipStream_t st);
 hipError_t launch_layout(const Geo& g, const Ws& w, const Cache& c, const void* K, const void* V, hipStream_t st);
 hipError_t launch_decode(const Geo& g, const Cache& c, const DecWs& dw, const void* q, const void* kn,
                          const void* vn, void* out, int out_dtype, float scale, int n_app, hipStream_t st);
@@ -65,7 +67,8 @@ struct anchorkv_plan {
       c_stats;
   size_t cache_bytes;
   // encode workspace offsets
-  size_t w_opmax, w_opsum, w_oM, w_oiZ, w_oiZ64, w_ypart, w_Y, w_Yhi, w_Ylo, w_ynorm, w_sc, w_rank, w_flag, w_sband, w_sbscore, w_sstate, w_sghist, w_scand, w_rkey, w_rpos, w_slcnt, w_QA, w_apos,
+  size_t w_opmax, w_opsum, w_oM, w_oiZ, w_o64M, w_o64Z, w_o64O, w_M64, w_Z64, w_Y64, w_Y, w_Yhi, w_Ylo, w_ynorm,
+      w_cw, w_qn, w_uL, w_uU, w_bandpos, w_bandu, w_sc, w_rank, w_flag, w_sband, w_sbscore, w_sstate, w_sghist, w_scand, w_rkey, w_rpos, w_slcnt, w_QA, w_apos,
       w_fix, w_fixcount, w_gpos, w_xn2, w_u, w_sel, w_srec, w_bhist, w_bstate, w_bcval, w_bcpos, w_tiecnt, w_shist, w_wcnt;
   size_t ws_bytes;
   // decode workspace offsets
@@ -221,6 +224,22 @@ extern "C" anchorkv_status anchorkv_plan_create(const anchorkv_config* cfg, int3
     geo.prefNK[b + 1] = geo.prefNK[b] + (int)p->req[b].residuals_k;
     geo.prefNV[b + 1] = geo.prefNV[b] + (int)p->req[b].residuals_v;
   }
+  // fp64 observation chunks: the smallest power of two (>= 256 tokens) that
+  // keeps the launch at about 1024 workgroups of 64 rows and a head at <= 256
+  // chunks (the partial outputs are 1 KB per chunk and row).
+  {
+    geo.mpad = (geo.m + 15) / 16 * 16;
+    const int nrg = (geo.m + 63) / 64;
+    int oc = 256;
+    for (;;) {
+      int64_t n = 0;
+      for (int b = 0; b < batch; ++b) n += (int64_t)H * nrg * ((geo.S[b] + oc - 1) / oc);
+      if ((n <= 1024 && (geo.maxS + oc - 1) / oc <= 256) || oc >= (1 << 16)) break;
+      oc *= 2;
+    }
+    geo.oc64 = oc;
+    for (int b = 0; b < batch; ++b) geo.prefC64[b + 1] = geo.prefC64[b] + (geo.S[b] + oc - 1) / oc;
+  }
   // Decode split: 2048 sorted slots per workgroup when that still gives at
   // least 256 workgroups (one per CU), else 1024.
   {
@@ -271,8 +290,17 @@ extern "C" anchorkv_status anchorkv_plan_create(const anchorkv_config* cfg, int3
   p->w_opsum = Wl.add(8 * 2 * TC * m);
   p->w_oM = Wl.add(4 * batch * H * m);
   p->w_oiZ = Wl.add(4 * batch * H * m);
-  p->w_oiZ64 = Wl.add(8 * batch * H * m);
-  p->w_ypart = Wl.add(4 * TC * m * D);
+  {
+    const size_t TC64 = (size_t)geo.prefC64[batch] * H, mp = geo.mpad;
+    p->w_o64M = Wl.add(8 * TC64 * mp);
+    p->w_o64Z = Wl.add(8 * TC64 * mp);
+    p->w_o64O = Wl.add(8 * TC64 * mp * D);
+  }
+  p->w_M64 = Wl.add(8 * batch * H * m);
+  p->w_Z64 = Wl.add(8 * batch * H * m);
+  p->w_Y64 = Wl.add(8 * batch * H * m * D);
+  p->w_cw = Wl.add(4 * batch * H * m);
+  p->w_qn = Wl.add(4 * batch * H * m);
   p->w_Y = Wl.add(4 * batch * H * m * D);
   p->w_Yhi = Wl.add(2 * batch * H * m * D);
   p->w_Ylo = Wl.add(2 * batch * H * m * D);
@@ -295,10 +323,14 @@ extern "C" anchorkv_status anchorkv_plan_create(const anchorkv_config* cfg, int3
   p->w_gpos = Wl.add(4 * 2 * TS);
   p->w_xn2 = Wl.add(4 * 2 * TS);
   p->w_u = Wl.add(4 * 2 * TS);
+  p->w_uL = Wl.add(4 * 2 * TS);
+  p->w_uU = Wl.add(4 * 2 * TS);
   p->w_sel = Wl.add(2 * TS);
   p->w_srec = Wl.add(16 * TW * 64);
   p->w_bhist = Wl.add(4 * 2 * 4096 * batch);
-  p->w_bstate = Wl.add(4 * 2 * 4 * batch);
+  p->w_bstate = Wl.add(4 * 2 * akv::BST_N * batch);
+  p->w_bandpos = Wl.add(4 * 2 * (size_t)akv::BAND_CAP * batch);
+  p->w_bandu = Wl.add(8 * 2 * (size_t)akv::BAND_CAP * batch);
   p->w_bcval = Wl.add(4 * 2 * (size_t)32768 * batch);
   p->w_bcpos = Wl.add(4 * 2 * (size_t)32768 * batch);
   p->w_tiecnt = Wl.add(4 * 2 * (size_t)geo.prefBC[batch]);
@@ -371,8 +403,14 @@ static akv::Ws ws_ptrs(const anchorkv_plan* p, void* base) {
   w.opsum = at<double>(base, p->w_opsum);
   w.oM = at<float>(base, p->w_oM);
   w.oiZ = at<float>(base, p->w_oiZ);
-  w.oiZ64 = at<double>(base, p->w_oiZ64);
-  w.ypart = at<float>(base, p->w_ypart);
+  w.o64M = at<double>(base, p->w_o64M);
+  w.o64Z = at<double>(base, p->w_o64Z);
+  w.o64O = at<double>(base, p->w_o64O);
+  w.M64 = at<double>(base, p->w_M64);
+  w.Z64 = at<double>(base, p->w_Z64);
+  w.Y64 = at<double>(base, p->w_Y64);
+  w.cw = at<float>(base, p->w_cw);
+  w.qn = at<float>(base, p->w_qn);
   w.Y = at<float>(base, p->w_Y);
   w.Yhi = at<uint16_t>(base, p->w_Yhi);
   w.Ylo = at<uint16_t>(base, p->w_Ylo);
@@ -396,10 +434,14 @@ static akv::Ws ws_ptrs(const anchorkv_plan* p, void* base) {
   w.gpos = at<float>(base, p->w_gpos);
   w.xn2 = at<float>(base, p->w_xn2);
   w.u = at<float>(base, p->w_u);
+  w.uL = at<float>(base, p->w_uL);
+  w.uU = at<float>(base, p->w_uU);
   w.sel = at<uint8_t>(base, p->w_sel);
   w.srec = at<uint4>(base, p->w_srec);
   w.bhist = at<uint32_t>(base, p->w_bhist);
   w.bstate = at<int32_t>(base, p->w_bstate);
+  w.bandpos = at<int32_t>(base, p->w_bandpos);
+  w.bandu = at<double>(base, p->w_bandu);
   w.bcval = at<float>(base, p->w_bcval);
   w.bcpos = at<int32_t>(base, p->w_bcpos);
   w.tiecnt = at<int32_t>(base, p->w_tiecnt);
@@ -435,12 +477,13 @@ extern "C" anchorkv_status anchorkv_encode(const anchorkv_plan* p, const void* K
   anchorkv_status s;
   if ((s = hip_status(akv::launch_init(g, c, w, st), "init")) != ANCHORKV_OK) return s;
   if ((s = hip_status(akv::launch_obs(g, w, K, V, Q_obs, st), "observation pass")) != ANCHORKV_OK) return s;
+  if ((s = hip_status(akv::launch_obs64(g, w, K, V, Q_obs, st), "fp64 observation pass")) != ANCHORKV_OK) return s;
   if ((s = hip_status(akv::launch_select(g, w, c, K, V, Q_obs, anchor_pos_override, st), "anchor selection")) !=
       ANCHORKV_OK)
     return s;
   if ((s = hip_status(akv::launch_assign(g, w, c, K, V, st), "assignment")) != ANCHORKV_OK) return s;
   if ((s = hip_status(akv::launch_epilogue(g, w, c, K, V, Q_obs, st), "utilities")) != ANCHORKV_OK) return s;
-  if ((s = hip_status(akv::launch_budget(g, w, st), "budget")) != ANCHORKV_OK) return s;
+  if ((s = hip_status(akv::launch_budget(g, w, c, K, V, Q_obs, st), "budget")) != ANCHORKV_OK) return s;
   if ((s = hip_status(akv::launch_layout(g, w, c, K, V, st), "layout")) != ANCHORKV_OK) return s;
   return ANCHORKV_OK;
 }
@@ -704,12 +747,13 @@ __global__ void k_init(Geo g, Cache c, Ws w) {
   if (i < akv::SS_N * g.H * g.B) w.sstate[i] = 0;
   if (i < 4096 * g.H * g.B) w.sghist[i] = 0u;
   if (i < 2 * 4096 * g.B) w.bhist[i] = 0u;
-  if (i < 2 * 4 * g.B) w.bstate[i] = 0;
+  if (i < 2 * akv::BST_N * g.B) w.bstate[i] = (i % akv::BST_N) == akv::BST_A ? 0x7F800000 : 0;
 }
 hipError_t launch_init(const Geo& g, const Cache& c, const Ws& w, hipStream_t st) {
   int n = 4 * g.B > 2 * g.H * g.B ? 4 * g.B : 2 * g.H * g.B;
   if (4096 * g.H * g.B > n) n = 4096 * g.H * g.B;
   if (2 * 4096 * g.B > n) n = 2 * 4096 * g.B;
+  if (2 * akv::BST_N * g.B > n) n = 2 * akv::BST_N * g.B;
   launch("k_init", k_init, dim3((n + 255) / 256), dim3(256), 0, st, g, c, w);
   return hipGetLastError();
 }

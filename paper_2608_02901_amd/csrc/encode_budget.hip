@@ -2,10 +2,12 @@
 // pooled over heads").  Per request and side, the N_side candidates of highest
 // utility among the non-anchor positions of all H heads get a residual; ties
 // go to the lower head, then the lower position (the flattened (h, t) order).
+// The utility ranked is the canonical fp64 one (Sec. 3.3 Eq. utilities in fp64
+// from exact fp64 logits and the fp64 observation statistics).
 //
-// The cut is an exact radix select on the fp32 bit patterns (utilities are
-// >= 0, so their bits order like the values; anchors carry -1 and are
-// skipped):
+// First the fp32 estimates u are cut by an exact radix select on their bit
+// patterns (utilities are >= 0, so their bits order like the values; anchors
+// carry -1 and are skipped):
 //   k_bhist : per chunk of the flattened (h, t) range, histogram of the first
 //             12-bit digit [31:20], added to the request's;
 //   k_bcand : every workgroup finds the digit of the N-th largest from that
@@ -19,6 +21,23 @@
 //   k_bmark : marks: above the threshold taken, ties taken in flattened order
 //             while the count lasts.
 // N <= 0 takes nothing; N at least the number of candidates takes them all.
+//
+// Then the fp32 order is corrected to the fp64 one.  The epilogue gives every
+// candidate proven bounds uL <= u64 <= uU.  With T the N-th largest fp32
+// estimate, A = min{uL : u >= T} is at most the N-th largest fp64 utility X
+// (the N candidates with u >= T all have u64 >= A) and B = max{uU : u <= T} is
+// at least X (only the fewer than N candidates with u > T can exceed B).  So
+// uL > B is surely selected, uU < A surely not (both agree with the fp32
+// marks), and the band of the rest holds X and every candidate whose order
+// matters:
+//   k_bbound   : A and B per request and side;
+//   k_bmark    : also lists the band and counts the band members the fp32
+//                order selected (the selections the band must supply);
+//   k_brescore : the fp64 utility of every band member, computed as the
+//                oracle does (sequential fp64 dots, one wave per member);
+//   k_bselect  : re-marks the band: the `need` largest fp64 utilities, ties to
+//                the lower flattened index.
+// A band above BAND_CAP keeps the fp32 marks and raises HDR_BAND_OVERFLOW.
 #include "akv_common.h"
 
 namespace akv {
@@ -98,7 +117,7 @@ __global__ __launch_bounds__(256) void k_bcand(Geo g, Ws w) {
     v[j] = e < e1 ? u[e] : -1.0f;
     cnt += v[j] >= 0.0f && (__float_as_uint(v[j]) >> 20) == bin1;
   }
-  int slot = wg_reserve(cnt, &w.bstate[bs * 4], tmp);
+  int slot = wg_reserve(cnt, &w.bstate[bs * BST_N + BST_NCAND], tmp);
 #pragma unroll
   for (int j = 0; j < per; ++j) {
     if (v[j] >= 0.0f && (__float_as_uint(v[j]) >> 20) == bin1) {
@@ -111,20 +130,28 @@ __global__ __launch_bounds__(256) void k_bcand(Geo g, Ws w) {
   }
 }
 
-__global__ __launch_bounds__(1024) void k_bcut(Geo g, Ws w) {
+__global__ __launch_bounds__(1024) void k_bcut(Geo g, Ws w, Cache c) {
   __shared__ uint32_t hist[SEL_NBIN];
   __shared__ int tmp[20], pick[2];
   const int bs = blockIdx.x, b = bs >> 1, side = bs & 1;
   const int n = g.H * g.S[b];
   const int nch = (n + BCHUNK - 1) / BCHUNK;
   int32_t* tc = w.tiecnt + 2 * g.prefBC[b] + side * nch;
-  int32_t* st = w.bstate + bs * 4;
+  int32_t* st = w.bstate + bs * BST_N;
   if (bmode(g, b, side) != 0) return;
   const int N = nside(g, b, side);
   const uint32_t* gh = w.bhist + (size_t)bs * SEL_NBIN;
   for (int i = threadIdx.x; i < SEL_NBIN; i += blockDim.x) hist[i] = gh[i];
   __syncthreads();
   digit_pick(hist, SEL_NBIN, N, true, tmp, pick);
+  if (pick[0] < 0) {  // fewer candidates than N: cannot happen with N < candidates
+    if (threadIdx.x == 0) {
+      atomicOr(&c.header[2], HDR_BUDGET_CUT);
+      st[BST_T] = 0x7F800000;
+      st[BST_REMAIN] = 0;
+    }
+    return;
+  }
   int remaining = N - pick[1];
   uint32_t prefix = (uint32_t)pick[0] << 20, pmask = 0xFFF00000u;
   const int nc = st[0];
@@ -140,6 +167,14 @@ __global__ __launch_bounds__(1024) void k_bcut(Geo g, Ws w) {
     else
       digit_hist(hist, nbin, n, [&](int e) { return __float_as_uint(u[e]); }, pmask, prefix, shift);
     digit_pick(hist, nbin, remaining, true, tmp, pick);
+    if (pick[0] < 0) {
+      if (threadIdx.x == 0) {
+        atomicOr(&c.header[2], HDR_BUDGET_CUT);
+        st[BST_T] = 0x7F800000;
+        st[BST_REMAIN] = 0;
+      }
+      return;
+    }
     remaining -= pick[1];
     prefix |= (uint32_t)pick[0] << shift;
     pmask |= (uint32_t)(nbin - 1) << shift;
@@ -172,21 +207,65 @@ __global__ __launch_bounds__(1024) void k_bcut(Geo g, Ws w) {
     __syncthreads();
   }
   if (threadIdx.x == 0) {
-    st[1] = (int)prefix;
-    st[2] = remaining;
+    st[BST_T] = (int)prefix;
+    st[BST_REMAIN] = remaining;
+  }
+}
+
+// Band limits A = min{uL : u >= T}, B = max{uU : u <= T} (float bits of
+// non-negative values order like the values).
+__global__ __launch_bounds__(256) void k_bbound(Geo g, Ws w) {
+  __shared__ unsigned red[2][4];
+  int idx = blockIdx.x;
+  const int b = locate_b(g, idx);
+  const int side = idx & 1, ch = idx >> 1;
+  if (bmode(g, b, side) != 0) return;
+  const int bs = b * 2 + side;
+  const uint32_t T = (uint32_t)w.bstate[bs * BST_N + BST_T];
+  const int n = g.H * g.S[b];
+  const size_t base = (size_t)side * g.H * g.prefS[g.B] + (size_t)g.prefS[b] * g.H;
+  const int e0 = ch * BCHUNK, e1 = min(n, e0 + BCHUNK);
+  unsigned amin = 0x7F800000u, bmax = 0u;
+  for (int e = e0 + threadIdx.x; e < e1; e += blockDim.x) {
+    const float v = w.u[base + e];
+    if (!(v >= 0.0f)) continue;
+    const uint32_t vb = __float_as_uint(v);
+    if (vb >= T) amin = min(amin, __float_as_uint(w.uL[base + e]));
+    if (vb <= T) bmax = max(bmax, __float_as_uint(w.uU[base + e]));
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    amin = min(amin, (unsigned)__shfl_xor((int)amin, o, 64));
+    bmax = max(bmax, (unsigned)__shfl_xor((int)bmax, o, 64));
+  }
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  if (lane == 0) {
+    red[0][wave] = amin;
+    red[1][wave] = bmax;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int i = 1; i < 4; ++i) {
+      amin = min(amin, red[0][i]);
+      bmax = max(bmax, red[1][i]);
+    }
+    atomicMin((unsigned*)&w.bstate[bs * BST_N + BST_A], amin);
+    atomicMax((unsigned*)&w.bstate[bs * BST_N + BST_B], bmax);
   }
 }
 
 __global__ __launch_bounds__(256) void k_bmark(Geo g, Ws w) {
   __shared__ int wtot[4];
+  __shared__ int tmp[8];
   int idx = blockIdx.x;
   const int b = locate_b(g, idx);
   const int side = idx & 1, ch = idx >> 1;
   const int bs = b * 2 + side;
-  const int32_t* st = w.bstate + bs * 4;
+  int32_t* st = w.bstate + bs * BST_N;
   const int mode = bmode(g, b, side);
-  const uint32_t T = (uint32_t)st[1];
-  const int need = st[2];
+  const uint32_t T = (uint32_t)st[BST_T];
+  const int need = st[BST_REMAIN];
+  const uint32_t A = (uint32_t)st[BST_A], Bb = (uint32_t)st[BST_B];
   const int n = g.H * g.S[b];
   const int nch = (n + BCHUNK - 1) / BCHUNK;
   const int32_t* tc = w.tiecnt + 2 * g.prefBC[b] + side * nch;
@@ -214,6 +293,8 @@ __global__ __launch_bounds__(256) void k_bmark(Geo g, Ws w) {
   __syncthreads();
   int before = x - eq + (mode == 0 ? tc[ch] : 0);
   for (int i = 0; i < wave; ++i) before += wtot[i];
+  unsigned bandbits = 0;  // element j of the thread is a band member
+  int nb = 0, nsel = 0;
 #pragma unroll
   for (int j = 0; j < per; ++j) {
     if (lo + j >= e1) break;
@@ -229,19 +310,174 @@ __global__ __launch_bounds__(256) void k_bmark(Geo g, Ws w) {
           s = before < need;
           ++before;
         }
+        const uint32_t lb = __float_as_uint(w.uL[base + lo + j]), ub = __float_as_uint(w.uU[base + lo + j]);
+        if (!(lb > Bb) && !(ub < A)) {
+          bandbits |= 1u << j;
+          ++nb;
+          nsel += s;
+        }
       }
     }
     sel[lo + j] = s;
   }
+  if (mode != 0) return;  // uniform per workgroup
+  // List the band members (one slot reservation per workgroup).
+  int slot = wg_reserve(nb, &st[BST_NBAND], tmp);
+  int32_t* bp = w.bandpos + (size_t)bs * BAND_CAP;
+#pragma unroll
+  for (int j = 0; j < per; ++j)
+    if ((bandbits >> j) & 1u) {
+      if (slot < BAND_CAP) bp[slot] = lo + j;
+      ++slot;
+    }
+  const int ns = wave_sum_i(nsel);
+  if (lane == 0 && ns) atomicAdd(&st[BST_NEED], ns);
 }
 
-hipError_t launch_budget(const Geo& g, const Ws& w, hipStream_t st) {
+// fp64 utility of every listed band member, one wave per member, computed as
+// the oracle computes it (Sec. 3.3 Eq. utilities): the stored coefficient's
+// residual r = x - fp32(gamma a) in fp32; per observation row w (lane w, w + 64,
+// ...) the sequential fp64 dots l = q_w.k_t / sqrt(D), alpha = exp(l - M_w) /
+// Z_w, and for keys q_w.r and ||v_t - y_w||^2, for values ||r||^2; the row
+// terms alpha^2 (q.r)^2 / D ||v - y||^2 (or alpha^2 ||r||^2) summed in row
+// order and divided by m.
+template <int DT>
+__global__ __launch_bounds__(256) void k_brescore(Geo g, Ws w, Cache c, const void* Kin, const void* Vin,
+                                                  const void* Qin) {
+  using E = typename Elem<DT>::T;
+  __shared__ float xs[4][AKV_D], vs[4][AKV_D], rs[4][AKV_D];
+  __shared__ double terms[4][256];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int nw = gridDim.x * 4;
+  const int gw = blockIdx.x * 4 + wave;
+  const int m = g.m, D = AKV_D;
+  const size_t TS = (size_t)g.prefS[g.B] * g.H;
+  const double sqd = sqrt((double)D);
+  int base = 0;  // members of the earlier lists
+  for (int bs = 0; bs < 2 * g.B; ++bs) {
+    const int b = bs >> 1, side = bs & 1;
+    const int nl = w.bstate[bs * BST_N + BST_NBAND];
+    const int n = (bmode(g, b, side) == 0 && nl <= BAND_CAP) ? nl : 0;
+    int i0 = gw - base;
+    if (i0 < 0) i0 += ((-i0 + nw - 1) / nw) * nw;
+    for (int i = i0; i < n; i += nw) {
+      const int S = g.S[b], k = g.k[b];
+      const int f = w.bandpos[(size_t)bs * BAND_CAP + i];
+      const int h = f / S, t = f % S;
+      const size_t po = (size_t)g.prefS[b] * g.H + (size_t)h * S;
+      const size_t ko = (size_t)g.prefK[b] * g.H + (size_t)h * k;
+      const size_t xo = (po + t) * D;
+      const int a = min(max(w.apos[side * TS + po + t], 0), k - 1);
+      const float gm = w.gpos[side * TS + po + t];
+      const E* xr = (const E*)(side ? Vin : Kin) + xo;
+      const E* ar = (const E*)(side ? c.ancV : c.ancK) + (ko + a) * D;
+      const E* kr = (const E*)Kin + xo;
+      const E* vr = (const E*)Vin + xo;
+      for (int j = lane; j < D; j += 64) {
+        const float p = gm * Elem<DT>::get(ar, j);
+        rs[wave][j] = Elem<DT>::get(xr, j) - p;
+        xs[wave][j] = Elem<DT>::get(kr, j);
+        vs[wave][j] = Elem<DT>::get(vr, j);
+      }
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+      double rvn = 0.0;
+      if (side == 1)
+        for (int j = 0; j < D; ++j) rvn += (double)rs[wave][j] * (double)rs[wave][j];
+      const size_t bh = (size_t)b * g.H + h;
+      const E* Q = (const E*)Qin + ((size_t)b * g.Hq + (size_t)h * g.g) * g.W * D;
+      for (int wr = lane; wr < m; wr += 64) {
+        const E* q = Q + (size_t)wr * D;
+        double l = 0.0;
+        for (int j = 0; j < D; ++j) l += (double)Elem<DT>::get(q, j) * (double)xs[wave][j];
+        l = l / sqd;
+        const double al = exp(l - w.M64[bh * m + wr]) / w.Z64[bh * m + wr];
+        const double a2 = al * al;
+        double term;
+        if (side == 0) {
+          double qr = 0.0;
+          for (int j = 0; j < D; ++j) qr += (double)Elem<DT>::get(q, j) * (double)rs[wave][j];
+          const double* y = w.Y64 + (bh * m + wr) * D;
+          double vy = 0.0;
+          for (int j = 0; j < D; ++j) {
+            const double dv = (double)vs[wave][j] - y[j];
+            vy += dv * dv;
+          }
+          term = a2 * (qr * qr / D) * vy;
+        } else {
+          term = a2 * rvn;
+        }
+        terms[wave][wr] = term;
+      }
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+      if (lane == 0) {
+        double su = 0.0;
+        for (int wr = 0; wr < m; ++wr) su += terms[wave][wr];
+        w.bandu[(size_t)bs * BAND_CAP + i] = su / m;
+      }
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+    }
+    base += n;
+  }
+}
+
+// Exact ranks inside the band: member i is selected when fewer than `need`
+// members precede it in (fp64 utility descending, flattened index ascending)
+// order.  Grid: (request, side) x BAND_CAP / 1024 member blocks.
+__global__ __launch_bounds__(1024) void k_bselect(Geo g, Ws w, Cache c) {
+  __shared__ double su[1024];
+  __shared__ int sp[1024];
+  constexpr int NBLK = BAND_CAP / 1024;
+  const int bs = blockIdx.x / NBLK, blk = blockIdx.x % NBLK;
+  const int b = bs >> 1, side = bs & 1;
+  if (bmode(g, b, side) != 0) return;
+  const int n = w.bstate[bs * BST_N + BST_NBAND];
+  if (n > BAND_CAP) {
+    if (blk == 0 && threadIdx.x == 0) atomicOr(&c.header[2], HDR_BAND_OVERFLOW);
+    return;
+  }
+  if (blk * 1024 >= n) return;
+  const int need = w.bstate[bs * BST_N + BST_NEED];
+  const int32_t* bp = w.bandpos + (size_t)bs * BAND_CAP;
+  const double* bu = w.bandu + (size_t)bs * BAND_CAP;
+  const int i = blk * 1024 + threadIdx.x;
+  const bool mine = i < n;
+  const double ui = mine ? bu[i] : 0.0;
+  const int pi = mine ? bp[i] : 0;
+  int rank = 0;
+  for (int j0 = 0; j0 < n; j0 += 1024) {
+    __syncthreads();
+    if (j0 + (int)threadIdx.x < n) {
+      su[threadIdx.x] = bu[j0 + threadIdx.x];
+      sp[threadIdx.x] = bp[j0 + threadIdx.x];
+    }
+    __syncthreads();
+    const int nj = min(1024, n - j0);
+    if (mine)
+      for (int j = 0; j < nj; ++j) rank += (su[j] > ui || (su[j] == ui && sp[j] < pi)) ? 1 : 0;
+  }
+  if (mine) {
+    uint8_t* sel = w.sel + (size_t)side * g.H * g.prefS[g.B] + (size_t)g.prefS[b] * g.H;
+    sel[pi] = rank < need ? 1 : 0;
+  }
+}
+
+hipError_t launch_budget(const Geo& g, const Ws& w, const Cache& c, const void* K, const void* V, const void* Q,
+                         hipStream_t st) {
   int nblk = 0;
   for (int b = 0; b < g.B; ++b) nblk += 2 * ((g.H * g.S[b] + BCHUNK - 1) / BCHUNK);
   launch("k_bhist", k_bhist, dim3(nblk), dim3(256), 0, st, g, w);
   launch("k_bcand", k_bcand, dim3(nblk), dim3(256), 0, st, g, w);
-  launch("k_bcut", k_bcut, dim3(g.B * 2), dim3(1024), 0, st, g, w);
+  launch("k_bcut", k_bcut, dim3(g.B * 2), dim3(1024), 0, st, g, w, c);
+  launch("k_bbound", k_bbound, dim3(nblk), dim3(256), 0, st, g, w);
   launch("k_bmark", k_bmark, dim3(nblk), dim3(256), 0, st, g, w);
+  if (g.dtype == 1)
+    launch("k_brescore", k_brescore<1>, dim3(1024), dim3(256), 0, st, g, w, c, K, V, Q);
+  else
+    launch("k_brescore", k_brescore<0>, dim3(1024), dim3(256), 0, st, g, w, c, K, V, Q);
+  launch("k_bselect", k_bselect, dim3(g.B * 2 * (BAND_CAP / 1024)), dim3(1024), 0, st, g, w, c);
   return hipGetLastError();
 }
 

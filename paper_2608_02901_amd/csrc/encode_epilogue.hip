@@ -50,10 +50,11 @@ __global__ __launch_bounds__(256, R == 1 ? 2 : 1) void k_epilogue(Geo g, Ws w, C
   constexpr int NT = EPI_TOK / 32;
   __shared__ __align__(16) E KT[32 * LD];
   __shared__ __align__(16) E VT[32 * LD];
-  __shared__ float gK_s[EPI_TOK], rv2_s[EPI_TOK], vn_s[EPI_TOK];
+  __shared__ float gK_s[EPI_TOK], rv2_s[EPI_TOK], vn_s[EPI_TOK], rk2_s[EPI_TOK];
   __shared__ int aK_s[EPI_TOK];
   __shared__ float sumK[4][EPI_TOK], sumV[4][EPI_TOK];
   __shared__ __align__(16) float CVS[256], YVS[256];  // per observation row: softmax constant, ||y_w||^2
+  __shared__ unsigned hmax[3];  // head maxima (float bits): ||q_w||, ||y_w||^2, |c_w|
   extern __shared__ __align__(16) char qlds_raw[];  // the m observation rows, row stride LD
   E* QS = (E*)qlds_raw;
 
@@ -152,18 +153,22 @@ __global__ __launch_bounds__(256, R == 1 ? 2 : 1) void k_epilogue(Geo g, Ws w, C
         }
       }
       if (in) w.gpos[side * TS + po + t] = gb;
+      // ||r||^2 of the side's fp32 residual (the key side bounds q.r_K, the
+      // value side is the value utility's factor)
+      float rs = 0.0f;
+#pragma unroll
+      for (int j = 0; j < AKV_D; ++j) {
+        const float r = fmaf(-gb, Elem<DT>::get(ae, j), Elem<DT>::get(xe, j));
+        rs = fmaf(r, r, rs);
+      }
+      rs = (in && rk < 0) ? rs : 0.0f;
       if (side == 0) {
         gK_s[tl] = in ? gb : 0.0f;
         aK_s[tl] = (in && rk < 0) ? a : -1;  // -1: no utility (anchor or past S)
+        rk2_s[tl] = rs;
       } else {
-        float rs = 0.0f;
-#pragma unroll
-        for (int j = 0; j < AKV_D; ++j) {
-          const float r = fmaf(-gb, Elem<DT>::get(ae, j), Elem<DT>::get(xe, j));
-          rs = fmaf(r, r, rs);
-        }
         vn_s[tl] = w.xn2[TS + po + tc];
-        rv2_s[tl] = (in && rk < 0) ? rs : 0.0f;
+        rv2_s[tl] = rs;
       }
     }
   }
@@ -175,17 +180,25 @@ __global__ __launch_bounds__(256, R == 1 ? 2 : 1) void k_epilogue(Geo g, Ws w, C
   const int nrb = (m + 31) / 32;
   constexpr float LOG2E = 1.4426950408889634f;
   const float isl = LOG2E / sqrtf((float)D);  // logit scale in base 2
-  const float* oM = w.oM + (size_t)(b * g.H + h) * m;
-  const float* oiZ = w.oiZ + (size_t)(b * g.H + h) * m;
+  const float* cw = w.cw + (size_t)(b * g.H + h) * m;
+  const float* qn = w.qn + (size_t)(b * g.H + h) * m;
   const float* yn = w.ynorm + (size_t)(b * g.H + h) * m;
   const float* QA = w.QA + ko * m;
   // alpha = exp(l / sqrt(D) - M_w) / Z_w is taken as exp2(l log2(e) / sqrt(D)
-  // - c_w) with c_w = (M_w + ln Z_w) log2(e); rows past m get c_w = 1e30,
-  // hence alpha = 0.  c_w and ||y_w||^2 sit in LDS, the y fragments in
-  // registers.
+  // - c_w) with c_w = (M_w + ln Z_w) log2(e) from the fp64 row statistics;
+  // rows past m get c_w = 1e30, hence alpha = 0.  c_w and ||y_w||^2 sit in
+  // LDS, the y fragments in registers; the head maxima of ||q_w||, ||y_w||^2
+  // and |c_w| feed the error bounds.
+  if (threadIdx.x < 3) hmax[threadIdx.x] = 0u;
+  __syncthreads();
   for (int wr = threadIdx.x; wr < nrb * 32; wr += 256) {
-    CVS[wr] = wr < m ? (oM[wr] - __logf(oiZ[wr])) * LOG2E : 1e30f;
+    CVS[wr] = wr < m ? cw[wr] : 1e30f;
     YVS[wr] = wr < m ? yn[wr] : 0.0f;
+    if (wr < m) {
+      atomicMax(&hmax[0], __float_as_uint(qn[wr]));
+      atomicMax(&hmax[1], __float_as_uint(yn[wr]));
+      atomicMax(&hmax[2], __float_as_uint(fabsf(cw[wr])));
+    }
   }
   typename M::frag yh[R][NKS], yl[R][DT ? NKS : 1];
 #pragma unroll
@@ -279,7 +292,9 @@ __global__ __launch_bounds__(256, R == 1 ? 2 : 1) void k_epilogue(Geo g, Ws w, C
             const float al = __builtin_amdgcn_exp2f(fmaf(l, isl, -cq[i]));
             const float a2 = al * al;
             const float qr = fmaf(-gk, qv[e], l);
-            const float vv = fmaf(-2.0f, accY[e], vn + yq[i]);
+            // ||v - y||^2 >= 0: the cancellation form can dip below zero
+            // when y nearly equals v; the bounds below cover the clamp.
+            const float vv = fmaxf(fmaf(-2.0f, accY[e], vn + yq[i]), 0.0f);
             tk = fmaf(a2 * vv, qr * qr, tk);
             tv += a2;
           }
@@ -294,21 +309,89 @@ __global__ __launch_bounds__(256, R == 1 ? 2 : 1) void k_epilogue(Geo g, Ws w, C
     }
   }
   __syncthreads();
+  // ---- per token: the fp32 estimates and proven bounds [uL, uU] of the
+  // canonical fp64 utilities (Sec. 3.3 Eq. utilities computed in fp64 from
+  // the exact fp64 logits, y_w, M_w and Z_w).  With u = 2^-24:
+  //   alpha: |ln(alpha32 / alpha)| <= eta = ln2 [c1 qmax |k| isl
+  //          + u (3 qmax |k| isl + 2 cmax)] + 4u  (logit MFMA error c1 |q||k|,
+  //          c1 = 512u; the roundings of isl, the fma and c_w; exp2);
+  //   q.r_K: |qr32 - qr| <= e = qmax (|k| + |gamma| |a|) (c1 + 4u) (logit and
+  //          QA-table MFMA errors, the residual's rounding);
+  //   vv   : |vv32 - ||v - y||^2| <= dvv = 258u |v|^2 + 4u ymax^2
+  //          + 9.3e-5 |v| ymax (|v|^2 and ||y||^2 roundings, the bf16 hi/lo
+  //          split of y and the MFMA error of v.y, the fp32 combination);
+  // and with tk = sum a2 vv qr^2 (a2 = alpha32^2), tv = sum a2 (fp32 sums of
+  // non-negative terms, relative error <= 301u), S0 = sum a2 vv <= V2 tv,
+  // S2 = sum a2 qr^2 <= Qr2 tv, S3 = sum a2 |qr| <= sqrt(Qr2) tv and
+  // sum a2 vv |qr| <= sqrt(tk S0):
+  //   m D uK <= (1+ea)^2 [tk + 2e sqrt(tk S0) + e^2 S0 + dvv (S2 + 2e S3 + e^2 tv)]
+  //   m D uK >= (1-ea)^2 [tk - 2e sqrt(tk S0) - dvv S2]
+  // (ea = eta (1 + eta)); the value side scales ||r_V||^2 tv / m likewise.
   {
-   for (int tl = threadIdx.x; tl < EPI_TOK; tl += 256) {
-    const int t = tb + tl;
-    if (t < S) {
-      float uk = -1.0f, uv = -1.0f;
-      if (aK_s[tl] >= 0) {
+    constexpr float U = 5.9604645e-8f;  // 2^-24
+    constexpr float C1 = 512.0f * U;
+    const float qmax = __uint_as_float(hmax[0]);
+    const float ymax2 = __uint_as_float(hmax[1]) * (1.0f + 8.0f * U);
+    const float ymax = sqrtf(ymax2) * (1.0f + 2.0f * U);
+    const float cmax = __uint_as_float(hmax[2]);
+    const float isl1 = LOG2E / sqrtf((float)D) * (1.0f + 4.0f * U);
+    for (int tl = threadIdx.x; tl < EPI_TOK; tl += 256) {
+      const int t = tb + tl;
+      if (t >= S) continue;
+      float uk = -1.0f, uv = -1.0f, ukl = -1.0f, uku = -1.0f, uvl = -1.0f, uvu = -1.0f;
+      const int ak = aK_s[tl];
+      if (ak >= 0) {
         const float sk = (sumK[0][tl] + sumK[1][tl]) + (sumK[2][tl] + sumK[3][tl]);
         const float sv = (sumV[0][tl] + sumV[1][tl]) + (sumV[2][tl] + sumV[3][tl]);
         uk = sk / ((float)m * (float)D);
         uv = rv2_s[tl] * sv / (float)m;
+        // token quantities (upper bounds of the norms)
+        const float kn = sqrtf(w.xn2[po + t] * (1.0f + 300.0f * U)) * (1.0f + 2.0f * U);
+        const float vn2 = vn_s[tl] * (1.0f + 300.0f * U);
+        const float vnm = sqrtf(vn2) * (1.0f + 2.0f * U);
+        const float gk = fabsf(gK_s[tl]);
+        const float an = (float)sqrt((c.nrmK)[ko + ak]) * (1.0f + 2.0f * U);
+        const float rkn = sqrtf(rk2_s[tl] * (1.0f + 300.0f * U)) * (1.0f + 2.0f * U);
+        const float qk = qmax * kn * isl1;
+        const float eta = 0.6931472f * (C1 * qk + U * (3.0f * qk + 2.0f * cmax)) + 4.0f * U;
+        const float ea = eta * (1.0f + eta) * 1.0001f;
+        const float e = qmax * (kn + gk * an) * (C1 + 4.0f * U) * 1.0001f;
+        const float dvv = (258.0f * U * vn2 + 4.0f * U * ymax2 + 9.3e-5f * vnm * ymax) * 1.0001f;
+        const float V2 = (vnm + ymax) * (vnm + ymax) * 1.0001f + dvv;
+        const float qr1 = qmax * rkn + e;
+        const float Qr2 = qr1 * qr1 * 1.0001f;
+        const float r1 = 301.0f * U * 1.01f;
+        const float tkh = sk * (1.0f + r1), tkl = sk * (1.0f - r1);
+        const float tvh = sv * (1.0f + r1), tvl = sv * (1.0f - r1);
+        const float S0 = V2 * tvh;
+        const float cs = sqrtf(tkh * S0) * (1.0f + 2.0f * U);
+        const float hiK = tkh + 2.0f * e * cs + e * e * S0 + dvv * (Qr2 * tvh + 2.0f * e * qr1 * tvh + e * e * tvh);
+        const float loK = tkl - 2.0f * e * cs - dvv * Qr2 * tvh;
+        const float md = (float)m * (float)D;
+        // fp32 underflow (flushed or subnormal intermediates) leaves at most
+        // 2^-126 (Qr2 V2 + Qr2 + 1) per row term, m terms, / (m D)
+        const float ufK = fmaxf(2.4e-38f, 2.4e-38f * (Qr2 * V2 + Qr2 + 1.0f) / (float)D);
+        uku = (1.0f + ea) * (1.0f + ea) * hiK / md * (1.0f + 8.0f * U) + ufK;
+        ukl = fmaxf(0.0f, (1.0f - ea) * (1.0f - ea) * loK / md * (1.0f - 8.0f * U) - ufK);
+        // value side: ||r_V||^2 (fp32 sum of squares of the fp32 residual; for
+        // an fp32 cache the residual's product rounding differs from the
+        // canonical form by <= 2u |gamma| |a| per coordinate)
+        const int av = w.apos[TS + po + t];
+        const float gv = fabsf(w.gpos[TS + po + t]);
+        const float anv = (av >= 0 && av < k) ? (float)sqrt((c.nrmV)[ko + av]) * (1.0f + 2.0f * U) : 0.0f;
+        const float rv2 = rv2_s[tl];
+        const float drv = 300.0f * U * rv2 + (DT == 1 ? 0.0f : 4.1f * U * sqrtf(rv2) * gv * anv * 1.01f);
+        const float ufV = fmaxf(2.4e-38f, 2.4e-38f * (rv2 + drv + 1.0f));
+        uvu = (1.0f + ea) * (1.0f + ea) * (rv2 + drv) * tvh / (float)m * (1.0f + 8.0f * U) + ufV;
+        uvl = fmaxf(0.0f, (1.0f - ea) * (1.0f - ea) * (rv2 - drv) * tvl / (float)m * (1.0f - 8.0f * U) - ufV);
       }
       w.u[po + t] = uk;
       w.u[TS + po + t] = uv;
+      w.uL[po + t] = ukl;
+      w.uU[po + t] = uku;
+      w.uL[TS + po + t] = uvl;
+      w.uU[TS + po + t] = uvu;
     }
-   }
   }
 }
 

@@ -6,35 +6,15 @@
 //   k_obs_stats   : per half chunk (1024 tokens), MFMA logits q_w.k_t / sqrt(D)
 //                   and the per-row running max and sum of exp;
 //   k_obs_reduce  : merges the chunk statistics into M_w and 1/Z_w;
-//   k_obs_pass    : recomputes the logits, alpha = exp(l - M)/Z, the SnapKV
-//                   column score sc(t) = (1/m) sum_w alpha_wt, and the partial
-//                   outputs y_w = sum_t alpha_wt v_t on MFMA (alpha split into two
-//                   bf16 terms so y keeps about 16 bits);
-//   k_obs_yreduce : sums the partial outputs, ||y_w||^2 and the bf16 hi/lo split
-//                   of y used by the utility epilogue.
+//   k_obs_pass    : recomputes the logits, alpha = exp(l - M)/Z and the SnapKV
+//                   column score sc(t) = (1/m) sum_w alpha_wt.
+// The outputs y_w and the fp64 row statistics come from the fp64 pass
+// (encode_obs64.hip).
 #include "akv_common.h"
 
 namespace akv {
 
 template <int DT> struct TileLD { static constexpr int v = AKV_D + (DT ? 8 : 4); };
-
-// Orientation of the observation logits: the MFMA takes the key tile as its
-// row operand and the query fragments as its column operand, so lane l holds
-// the logits of observation row w = l % 32 (of its row block) against the 16
-// tokens crow(e, l), e = 0..15, of the 32-token tile.  A lane's row max, 1/Z
-// and causal limit are then single registers, and its 16 probabilities serve
-// directly as the row operand of the value contraction, whose k index kappa
-// runs over the tokens in the order the accumulator entries are taken:
-// kappa = KS s + KL (l / 32) + j holds entry e = KL s + j, i.e. token
-// kap_tok(kappa); the value tile is stored in that order.
-template <int DT>
-__device__ inline int tok_kap(int t) {  // token -> kappa (inverse of the entry order)
-  if constexpr (DT == 1) {
-    return (t & ~12) | ((t >> 2) & 1) << 3 | ((t >> 3) & 1) << 2;  // bits 2 and 3 swapped
-  } else {
-    return (t & ~7) | (t & 3) << 1 | ((t >> 2) & 1);
-  }
-}
 
 // A tile of 32 token rows held in registers between its load and its LDS
 // store (RPT 16-byte chunks per thread), so the next tile's loads are in
@@ -56,50 +36,6 @@ struct RowTile {
     for (int i = 0; i < RPT; ++i) {
       const int c = threadIdx.x + 256 * i, r = c / CPR, col = (c % CPR) * PER;
       *(uint4*)(lds + r * LD + col) = v[i];
-    }
-  }
-};
-
-// Position of contraction index kappa in row d of the transposed value tile:
-// groups of 8 stay contiguous (one MFMA operand load) and are permuted by d,
-// which spreads the stores of one wave over the LDS banks.
-__device__ inline int vt_pos(int d, int kap) { return (((kap >> 3) ^ (d >> 3)) & 3) * 8 + (kap & 7); }
-
-// Value tile, transposed: lds[d * LDT + vt_pos(d, tok_kap(r))] = X[t0 + r][d].
-// Thread c takes rows 2p, 2p+1 (p = c / CPR) of one 16-byte column chunk; for
-// bf16 the two tokens have adjacent kappa and are stored as one 32-bit word.
-template <int DT>
-struct PairTile {
-  using E = typename Elem<DT>::T;
-  static constexpr int PER = 16 / sizeof(E), CPR = AKV_D / PER, NP = 16 * CPR / 256;
-  uint4 v0[NP], v1[NP];
-  __device__ void load(const E* X, int t0, int S) {
-#pragma unroll
-    for (int i = 0; i < NP; ++i) {
-      const int c = threadIdx.x + 256 * i, p = c / CPR, col = (c % CPR) * PER;
-      const int r0 = t0 + 2 * p;
-      v0[i] = r0 < S ? *(const uint4*)(X + (size_t)r0 * AKV_D + col) : make_uint4(0, 0, 0, 0);
-      v1[i] = r0 + 1 < S ? *(const uint4*)(X + (size_t)(r0 + 1) * AKV_D + col) : make_uint4(0, 0, 0, 0);
-    }
-  }
-  __device__ void store_t(E* lds, int LDT) const {
-#pragma unroll
-    for (int i = 0; i < NP; ++i) {
-      const int c = threadIdx.x + 256 * i, p = c / CPR, col = (c % CPR) * PER;
-      const E* e0 = (const E*)&v0[i];
-      const E* e1 = (const E*)&v1[i];
-      const int k0 = tok_kap<DT>(2 * p), k1 = tok_kap<DT>(2 * p + 1);
-      if constexpr (sizeof(E) == 2) {
-#pragma unroll
-        for (int j = 0; j < PER; ++j)
-          *(uint32_t*)(lds + (col + j) * LDT + vt_pos(col + j, k0)) = (uint32_t)e0[j] | ((uint32_t)e1[j] << 16);
-      } else {
-#pragma unroll
-        for (int j = 0; j < PER; ++j) {
-          lds[(col + j) * LDT + vt_pos(col + j, k0)] = e0[j];
-          lds[(col + j) * LDT + vt_pos(col + j, k1)] = e1[j];
-        }
-      }
     }
   }
 };
@@ -135,14 +71,6 @@ __device__ inline float row_reduce_scatter16(const float (&v)[16], int lane) {
 #pragma unroll
   for (int i = 0; i < 2; ++i) c[i] = (s1 ? b[2 + i] : b[i]) + dpp_mov<0x1B>(s1 ? b[i] : b[2 + i]);
   return (s0 ? c[1] : c[0]) + dpp_mov<0xB1>(s0 ? c[0] : c[1]);
-}
-
-// Two fp32 values rounded to nearest-even bf16, packed low | high << 16.
-__device__ inline uint32_t pk_bf16(float x0, float x1) {
-  typedef __attribute__((ext_vector_type(2))) float f32x2;
-  typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2;
-  const f32x2 v = {x0, x1};
-  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
 }
 
 // R = row blocks of 32 observation rows per wave (4 waves cover 128 R rows).
@@ -281,18 +209,15 @@ __global__ __launch_bounds__(1024) void k_obs_reduce(Geo g, Ws w) {
     }
     w.oM[(size_t)(b * g.H + h) * g.m + wr] = Mt;
     w.oiZ[(size_t)(b * g.H + h) * g.m + wr] = (float)(1.0 / Zt);
-    w.oiZ64[(size_t)(b * g.H + h) * g.m + wr] = 1.0 / Zt;
   }
 }
 
 template <int DT, int R>
-__global__ __launch_bounds__(256) void k_obs_pass(Geo g, Ws w, const void* Kin, const void* Vin, const void* Qin) {
+__global__ __launch_bounds__(256) void k_obs_pass(Geo g, Ws w, const void* Kin, const void* Qin) {
   using E = typename Elem<DT>::T;
   using M = MF<DT>;
   constexpr int LD = TileLD<DT>::v;
-  constexpr int LDT = 32 + (DT ? 8 : 4);  // transposed value tile row stride (16-byte aligned rows)
-  __shared__ __align__(16) E KT[2][32 * LD];      // double-buffered tiles
-  __shared__ __align__(16) E VT[2][AKV_D * LDT];
+  __shared__ __align__(16) E KT[2][32 * LD];  // double-buffered key tiles
   __shared__ float scw[2][4][32];
   int idx = blockIdx.x;
   const int b = locate(g, OBS_CHUNK, 1, idx);
@@ -301,21 +226,15 @@ __global__ __launch_bounds__(256) void k_obs_pass(Geo g, Ws w, const void* Kin, 
   const int h = idx / nch, ch = idx % nch;
   const size_t xoff = ((size_t)g.prefS[b] * g.H + (size_t)h * S) * D;
   const E* X = (const E*)Kin + xoff;
-  const E* Vx = (const E*)Vin + xoff;
   const E* Q = qrows<DT>(g, Qin, b, h);
   const float* oM = w.oM + (size_t)(b * g.H + h) * m;
   const float* oiZ = w.oiZ + (size_t)(b * g.H + h) * m;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int nrb = (m + 31) / 32;
   const float isd = 1.0f / sqrtf((float)D);
-  f32x16 yacc[R][4];
-#pragma unroll
-  for (int r = 0; r < R; ++r)
-#pragma unroll
-    for (int db = 0; db < 4; ++db) yacc[r][db] = f32x16{};
   // The lane's row of each row block: query fragments, row max, 1/Z and
-  // causal limit stay in registers; the next token tile's keys and values are
-  // loaded while the current one is used.
+  // causal limit stay in registers; the next key tile is loaded while the
+  // current one is used.
   constexpr int NKS = AKV_D / M::KS;
   typename M::frag qf[R][NKS];
   float rmax[R], riz[R];
@@ -332,20 +251,14 @@ __global__ __launch_bounds__(256) void k_obs_pass(Geo g, Ws w, const void* Kin, 
   }
   const int tb = ch * OBS_CHUNK, te = min(S, tb + OBS_CHUNK);
   float* sc = w.sc + (size_t)g.prefS[b] * g.H + (size_t)h * S;
-  // Tile it sits in KT/VT[it & 1] and leaves its column sums in scw[it & 1];
+  // Tile it sits in KT[it & 1] and leaves its column sums in scw[it & 1];
   // after the barrier that starts tile it, the next tile is stored into the
   // other buffer and the column sums of tile it - 1 are final.  One barrier
   // per tile.
   RowTile<DT> kt;
-  PairTile<DT> vt;
   kt.load(X, tb, S);
-  vt.load(Vx, tb, S);
   kt.store(KT[0], LD);
-  vt.store_t(VT[0], LDT);
-  if (tb + 32 < te) {
-    kt.load(X, tb + 32, S);
-    vt.load(Vx, tb + 32, S);
-  }
+  if (tb + 32 < te) kt.load(X, tb + 32, S);
   int it = 0;
   for (int t0 = tb; t0 < te; t0 += 32, ++it) {
     const int cb = it & 1;
@@ -353,14 +266,8 @@ __global__ __launch_bounds__(256) void k_obs_pass(Geo g, Ws w, const void* Kin, 
     if (it > 0 && threadIdx.x < 32 && t0 - 32 + threadIdx.x < S)
       sc[t0 - 32 + threadIdx.x] = (scw[cb ^ 1][0][threadIdx.x] + scw[cb ^ 1][1][threadIdx.x] +
                                    scw[cb ^ 1][2][threadIdx.x] + scw[cb ^ 1][3][threadIdx.x]) / (float)m;
-    if (t0 + 32 < te) {
-      kt.store(KT[cb ^ 1], LD);
-      vt.store_t(VT[cb ^ 1], LDT);
-    }
-    if (t0 + 64 < te) {
-      kt.load(X, t0 + 64, S);
-      vt.load(Vx, t0 + 64, S);
-    }
+    if (t0 + 32 < te) kt.store(KT[cb ^ 1], LD);
+    if (t0 + 64 < te) kt.load(X, t0 + 64, S);
     float cs[16];
 #pragma unroll
     for (int e = 0; e < 16; ++e) cs[e] = 0.0f;
@@ -375,40 +282,10 @@ __global__ __launch_bounds__(256) void k_obs_pass(Geo g, Ws w, const void* Kin, 
         acc = M::mma(kb, qf[r][s], acc);
       }
       // alpha of the lane's row and tokens t0 + crow(e, lane).
-      float al[16];
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
         const float a = __expf(acc[e] * isd - rmax[r]) * riz[r];
-        al[e] = t0 + crow(e, lane) <= lim[r] ? a : 0.0f;
-        cs[e] += al[e];
-      }
-      // y_w += sum_t alpha[w][t] V[t][d]: row operand = alpha (entries KL s ..
-      // KL s + KL - 1 for step s), column operand = the value tile in kappa order.
-#pragma unroll
-      for (int s = 0; s < 32 / M::KS; ++s) {
-        typename M::frag ah, alo;
-        if constexpr (DT == 1) {
-          uint32_t hw[4], lw[4];
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            const float x0 = al[8 * s + 2 * j], x1 = al[8 * s + 2 * j + 1];
-            hw[j] = pk_bf16(x0, x1);
-            lw[j] = pk_bf16(x0 - __builtin_bit_cast(float, hw[j] << 16),
-                            x1 - __builtin_bit_cast(float, hw[j] & 0xFFFF0000u));
-          }
-          ah = __builtin_bit_cast(bf16x8, make_uint4(hw[0], hw[1], hw[2], hw[3]));
-          alo = __builtin_bit_cast(bf16x8, make_uint4(lw[0], lw[1], lw[2], lw[3]));
-        } else {
-          ah = al[s];
-        }
-        const int k0 = kofs(M::KS, s, lane);
-#pragma unroll
-        for (int db = 0; db < 4; ++db) {
-          const int d = db * 32 + (lane & 31);
-          auto vb = M::load_lds(&VT[cb][d * LDT + vt_pos(d, k0)], 0);
-          yacc[r][db] = M::mma(ah, vb, yacc[r][db]);
-          if constexpr (DT == 1) yacc[r][db] = M::mma(alo, vb, yacc[r][db]);
-        }
+        cs[e] += t0 + crow(e, lane) <= lim[r] ? a : 0.0f;
       }
     }
     // Column sums over the wave's rows: the 16 lanes of a DPP row, then the
@@ -425,51 +302,6 @@ __global__ __launch_bounds__(256) void k_obs_pass(Geo g, Ws w, const void* Kin, 
       sc[tl + threadIdx.x] = (scw[cl][0][threadIdx.x] + scw[cl][1][threadIdx.x] + scw[cl][2][threadIdx.x] +
                               scw[cl][3][threadIdx.x]) / (float)m;
   }
-  // Partial outputs of this chunk.
-  float* yp = w.ypart + ((size_t)(g.prefC[b] * g.H + h * nch + ch)) * m * D;
-#pragma unroll
-  for (int r = 0; r < R; ++r) {
-    const int rb = wave + 4 * r;
-    if (rb >= nrb) break;
-#pragma unroll
-    for (int db = 0; db < 4; ++db)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int wr = rb * 32 + crow(e, lane);
-        if (wr < m) yp[(size_t)wr * D + db * 32 + (lane & 31)] = yacc[r][db][e];
-      }
-  }
-}
-
-__global__ __launch_bounds__(128) void k_obs_yreduce(Geo g, Ws w) {
-  const int bh = blockIdx.x / g.m, wr = blockIdx.x % g.m;
-  const int b = bh / g.H, h = bh % g.H;
-  const int nch = (g.S[b] + OBS_CHUNK - 1) / OBS_CHUNK;
-  const int D = g.D;
-  __shared__ float red[2];
-  for (int d = threadIdx.x; d < D; d += blockDim.x) {
-    // Chunks added in order, their partial outputs loaded 16 at a time.
-    const float* yp = w.ypart + (((size_t)(g.prefC[b] * g.H + h * nch)) * g.m + wr) * D + d;
-    const size_t cs = (size_t)g.m * D;
-    float y = 0.0f;
-    for (int c0 = 0; c0 < nch; c0 += 16) {
-      float v[16];
-#pragma unroll
-      for (int u = 0; u < 16; ++u) v[u] = c0 + u < nch ? yp[(size_t)(c0 + u) * cs] : 0.0f;
-#pragma unroll
-      for (int u = 0; u < 16; ++u)
-        if (c0 + u < nch) y += v[u];
-    }
-    size_t o = ((size_t)bh * g.m + wr) * D + d;
-    w.Y[o] = y;
-    uint16_t hi = f2bf(y);
-    w.Yhi[o] = hi;
-    w.Ylo[o] = f2bf(y - bf2f(hi));
-    float sq = wave_sum(y * y);
-    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = sq;
-  }
-  __syncthreads();
-  if (threadIdx.x == 0) w.ynorm[(size_t)bh * g.m + wr] = red[0] + (D > 64 ? red[1] : 0.0f);
 }
 
 // ------------------------------------------------------------------ launchers
@@ -485,13 +317,12 @@ hipError_t launch_obs(const Geo& g, const Ws& w, const void* K, const void* V, c
   }
   launch("k_obs_reduce", k_obs_reduce, dim3(g.B * g.H * ((g.m + 63) / 64)), dim3(1024), 0, st, g, w);
   if (g.dtype == 1) {
-    if (r2) launch("k_obs_pass", k_obs_pass<1, 2>, dim3(nblk), dim3(256), 0, st, g, w, K, V, Q);
-    else launch("k_obs_pass", k_obs_pass<1, 1>, dim3(nblk), dim3(256), 0, st, g, w, K, V, Q);
+    if (r2) launch("k_obs_pass", k_obs_pass<1, 2>, dim3(nblk), dim3(256), 0, st, g, w, K, Q);
+    else launch("k_obs_pass", k_obs_pass<1, 1>, dim3(nblk), dim3(256), 0, st, g, w, K, Q);
   } else {
-    if (r2) launch("k_obs_pass", k_obs_pass<0, 2>, dim3(nblk), dim3(256), 0, st, g, w, K, V, Q);
-    else launch("k_obs_pass", k_obs_pass<0, 1>, dim3(nblk), dim3(256), 0, st, g, w, K, V, Q);
+    if (r2) launch("k_obs_pass", k_obs_pass<0, 2>, dim3(nblk), dim3(256), 0, st, g, w, K, Q);
+    else launch("k_obs_pass", k_obs_pass<0, 1>, dim3(nblk), dim3(256), 0, st, g, w, K, Q);
   }
-  launch("k_obs_yreduce", k_obs_yreduce, dim3(g.B * g.H * g.m), dim3(128), 0, st, g, w);
   return hipGetLastError();
 }
 

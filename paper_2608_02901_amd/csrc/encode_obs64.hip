@@ -1,0 +1,292 @@
+// fp64 observation attention of the compression pass: for every KV head the
+// m = W * (Hq/H) observation rows (the queries of the last W positions,
+// causal inside the window; Sec. 3.2, App. A.2) attend to all positions, and
+// this pass returns per row the logit max M_w, Z_w = sum_t exp(l_wt - M_w) and
+// y_w = sum_t alpha_wt v_t in fp64 (Sec. 3.3 Eq. utilities uses alpha_wt and
+// y_w).  The utility epilogue reads them to bound its fp32 utilities, the
+// residual budget re-scores the candidates at its cut with them, and the
+// anchor selection re-scores its near-ties with M_w and Z_w.
+//
+//   k_obs64        : one workgroup per (request, head, 64 rows, chunk of
+//                    oc64 tokens); each wave owns 16 rows and runs an online
+//                    softmax over the chunk on v_mfma_f64_16x16x4_f64:
+//                    S^T = K Q^T per 16-key tile (A = keys, B = queries), then
+//                    O^T += V^T P^T (A = values, B = the probabilities, which
+//                    the S^T accumulators already hold in the B layout);
+//   k_obs64_reduce : merges the chunk statistics and outputs of 16 rows and
+//                    derives the fp32 forms the epilogue uses.
+//
+// f64 16x16x4 MFMA operand layout: lane l supplies A[l%16][l/16] and
+// B[l/16][l%16]; accumulator register r of lane l holds D[l/16 + 4r][l%16].
+#include "akv_common.h"
+
+namespace akv {
+
+typedef __attribute__((ext_vector_type(4))) double f64x4;
+
+constexpr int O64_KT = 32;          // keys per LDS tile (two MFMA key tiles)
+constexpr int O64_MAXCH = 256;      // most chunks per head (the reduce keeps their scales in LDS)
+constexpr double O64_NEG = -1e300;  // running-max sentinel (finite: exp of differences stays defined)
+
+template <int DT>
+__device__ inline double e2d(const void* p, int i) {
+  if constexpr (DT == 1) return (double)bf2f(((const uint16_t*)p)[i]);
+  else return (double)((const float*)p)[i];
+}
+
+__device__ inline f64x4 mfma64(double a, double b, f64x4 c) {
+  return __builtin_amdgcn_mfma_f64_16x16x4f64(a, b, c, 0, 0, 0);
+}
+
+template <int DT>
+__global__ __launch_bounds__(256) void k_obs64(Geo g, Ws w, const void* Kin, const void* Vin, const void* Qin) {
+  using E = typename Elem<DT>::T;
+  constexpr int PER = 16 / sizeof(E);      // elements per 16-byte chunk
+  constexpr int LDK = AKV_D + PER;         // LDS row stride in elements (one chunk of padding)
+  constexpr int CPR = AKV_D / PER;         // chunks per row
+  constexpr int NLD = O64_KT * CPR / 256;  // chunks per thread per tile and side
+  __shared__ __align__(16) E KT[2][O64_KT * LDK];
+  __shared__ __align__(16) E VT[2][O64_KT * LDK];
+  const int nrg = (g.m + 63) / 64;
+  int idx = blockIdx.x;
+  int b = 0;
+  for (; b < g.B; ++b) {
+    const int n = g.H * nrg * ((g.S[b] + g.oc64 - 1) / g.oc64);
+    if (idx < n) break;
+    idx -= n;
+  }
+  const int S = g.S[b], P = S - g.W, m = g.m, D = AKV_D;
+  const int nch = (S + g.oc64 - 1) / g.oc64;
+  const int rg = idx % nrg, hc = idx / nrg, h = hc / nch, ch = hc % nch;
+  const size_t xoff = ((size_t)g.prefS[b] * g.H + (size_t)h * S) * D;
+  const E* X = (const E*)Kin + xoff;
+  const E* Vx = (const E*)Vin + xoff;
+  const E* Q = (const E*)Qin + ((size_t)b * g.Hq + (size_t)h * g.g) * g.W * D;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int rbase = rg * 64 + wave * 16;
+  const bool active = rbase < m;  // wave-uniform: the wave owns at least one row
+  const int row = rbase + (lane & 15);
+  const int lim = row < m ? P + row % g.W : -1;  // last position the row attends to
+  const int kq = lane >> 4;                      // contraction group of the lane
+  const double isd = 1.0 / sqrt((double)D);
+
+  // Query fragment of the lane: Q[row][32 kq + s], s = 0..31 (the contraction
+  // index d = 32 (l/16) + s, the same bijection on both operands).
+  uint4 qraw[32 / PER];
+  {
+    const E* qr = Q + (size_t)min(row, m - 1) * D + 32 * kq;
+#pragma unroll
+    for (int c = 0; c < 32 / PER; ++c) qraw[c] = *(const uint4*)(qr + c * PER);
+  }
+
+  const int tb = ch * g.oc64, te = min(S, tb + g.oc64);
+  uint4 kpre[NLD], vpre[NLD];
+  auto fetch = [&](int t0) {
+#pragma unroll
+    for (int i = 0; i < NLD; ++i) {
+      const int c = threadIdx.x + 256 * i, r = c / CPR, col = (c % CPR) * PER;
+      const bool in = t0 + r < S;
+      kpre[i] = in ? *(const uint4*)(X + (size_t)(t0 + r) * D + col) : make_uint4(0, 0, 0, 0);
+      vpre[i] = in ? *(const uint4*)(Vx + (size_t)(t0 + r) * D + col) : make_uint4(0, 0, 0, 0);
+    }
+  };
+  auto stash = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < NLD; ++i) {
+      const int c = threadIdx.x + 256 * i, r = c / CPR, col = (c % CPR) * PER;
+      *(uint4*)&KT[buf][r * LDK + col] = kpre[i];
+      *(uint4*)&VT[buf][r * LDK + col] = vpre[i];
+    }
+  };
+
+  double mrow = O64_NEG, zl = 0.0;  // running max of the row (same on its 4 lanes), lane-partial sum
+  f64x4 O[8];
+#pragma unroll
+  for (int blk = 0; blk < 8; ++blk) O[blk] = f64x4{0.0, 0.0, 0.0, 0.0};
+
+  fetch(tb);
+  stash(0);
+  if (tb + O64_KT < te) fetch(tb + O64_KT);
+  int it = 0;
+  for (int t0 = tb; t0 < te; t0 += O64_KT, ++it) {
+    const int cb = it & 1;
+    __syncthreads();  // tile it - 1 is no longer read: its buffer takes tile it + 1
+    if (t0 + O64_KT < te) stash(cb ^ 1);
+    if (t0 + 2 * O64_KT < te) fetch(t0 + 2 * O64_KT);
+    if (!active) continue;
+    // ---- logits of 32 keys: two 16-key tiles.  Register r of sacc[u] is
+    // key t0 + 16u + kq + 4r against row l%16.
+    f64x4 sacc[2];
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      uint4 kraw[32 / PER];
+      const E* kr = &KT[cb][(16 * u + (lane & 15)) * LDK + 32 * kq];
+#pragma unroll
+      for (int c = 0; c < 32 / PER; ++c) kraw[c] = *(const uint4*)(kr + c * PER);
+      f64x4 acc = {0.0, 0.0, 0.0, 0.0};
+#pragma unroll
+      for (int s = 0; s < 32; ++s) acc = mfma64(e2d<DT>(kraw, s), e2d<DT>(qraw, s), acc);
+      sacc[u] = acc;
+    }
+    double lg[8];
+    bool ok[8];
+    double tmax = O64_NEG;
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int e = 4 * u + r;
+        ok[e] = t0 + 16 * u + kq + 4 * r <= lim;
+        lg[e] = sacc[u][r] * isd;
+        if (ok[e]) tmax = fmax(tmax, lg[e]);
+      }
+    tmax = fmax(tmax, __shfl_xor(tmax, 16, 64));
+    tmax = fmax(tmax, __shfl_xor(tmax, 32, 64));
+    const double nm = fmax(mrow, tmax);
+    const double scl = exp(mrow - nm);  // 1 when the max stays, 0 on the first valid tile
+    zl *= scl;
+#pragma unroll
+    for (int blk = 0; blk < 8; ++blk) O[blk] *= scl;
+    mrow = nm;
+    double p[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      p[e] = ok[e] ? exp(lg[e] - nm) : 0.0;
+      zl += p[e];
+    }
+    // ---- values: MFMA (u, r) contracts the keys 16u + kq + 4r, k = kq; lane
+    // l supplies V[key][8 (l%16) + blk] as A and its own p as B, so output
+    // register r' of O[blk] is O^T[dim 8 (l/16 + 4 r') + blk][row l%16].
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const E* vr = &VT[cb][(16 * u + kq + 4 * r) * LDK + 8 * (lane & 15)];
+        uint4 vraw[8 / PER];
+#pragma unroll
+        for (int c = 0; c < 8 / PER; ++c) vraw[c] = *(const uint4*)(vr + c * PER);
+#pragma unroll
+        for (int blk = 0; blk < 8; ++blk) O[blk] = mfma64(e2d<DT>(vraw, blk), p[4 * u + r], O[blk]);
+      }
+  }
+  if (!active) return;
+  zl += __shfl_xor(zl, 16, 64);
+  zl += __shfl_xor(zl, 32, 64);
+  const size_t gc = ((size_t)g.prefC64[b] * g.H + (size_t)h * nch + ch);
+  if (lane < 16 && row < m) {
+    w.o64M[gc * g.mpad + row] = mrow;
+    w.o64Z[gc * g.mpad + row] = zl;
+  }
+  double* op = w.o64O + (gc * (g.mpad / 16) + rbase / 16) * 2048;
+#pragma unroll
+  for (int blk = 0; blk < 8; ++blk)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) op[(blk * 4 + r) * 64 + lane] = O[blk][r];
+}
+
+// One workgroup per (request, head, 16 rows): M_w = max of the chunk maxima,
+// Z_w = sum_c Z_c exp(M_c - M_w), y_w = sum_c O_c exp(M_c - M_w) / Z_w (chunks
+// in order), then the fp32 forms: y rounded and its bf16 hi/lo split, ||y||^2,
+// (M + ln Z) log2(e) and ||q_w||.
+template <int DT>
+__global__ __launch_bounds__(256) void k_obs64_reduce(Geo g, Ws w, const void* Qin) {
+  using E = typename Elem<DT>::T;
+  __shared__ double scl[O64_MAXCH][16];
+  __shared__ double red[16][16];
+  __shared__ double Msh[16], Zsh[16];
+  const int nrb = g.mpad / 16;
+  const int bh = blockIdx.x / nrb, rb16 = blockIdx.x % nrb, b = bh / g.H, h = bh % g.H;
+  const int m = g.m, D = AKV_D;
+  const int nch = (g.S[b] + g.oc64 - 1) / g.oc64;
+  const size_t gc0 = (size_t)g.prefC64[b] * g.H + (size_t)h * nch;
+  const int tid = threadIdx.x, r16 = tid & 15, part = tid >> 4;
+  const int row = rb16 * 16 + r16;
+  const bool rok = row < m;
+  double mx = O64_NEG;
+  if (rok)
+    for (int c = part; c < nch; c += 16) mx = fmax(mx, w.o64M[(gc0 + c) * g.mpad + row]);
+  red[part][r16] = mx;
+  __syncthreads();
+  if (tid < 16) {
+    double M = red[0][tid];
+    for (int p = 1; p < 16; ++p) M = fmax(M, red[p][tid]);
+    Msh[tid] = M;
+  }
+  __syncthreads();
+  double za = 0.0;
+  for (int c = part; c < nch; c += 16) {
+    const double s = rok ? exp(w.o64M[(gc0 + c) * g.mpad + row] - Msh[r16]) : 0.0;
+    scl[c][r16] = s;
+    za += rok ? w.o64Z[(gc0 + c) * g.mpad + row] * s : 0.0;
+  }
+  red[part][r16] = za;
+  __syncthreads();
+  if (tid < 16) {
+    double Z = 0.0;
+    for (int p = 0; p < 16; ++p) Z += red[p][tid];
+    Zsh[tid] = Z;
+  }
+  __syncthreads();
+  // Outputs: the thread's lane slot in the chunk layout, 8 elements of row r16.
+  const int lane = tid & 63;
+  const size_t bhm = (size_t)bh * m;
+  double sq = 0.0;
+#pragma unroll
+  for (int e = 0; e < 2; ++e) {
+    const int blk = 2 * (tid >> 6) + e;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const double* op = w.o64O + (gc0 * nrb + rb16) * 2048 + (blk * 4 + r) * 64 + lane;
+      double acc = 0.0;
+      for (int c = 0; c < nch; ++c) acc += op[(size_t)c * nrb * 2048] * scl[c][r16];
+      const double y = acc / Zsh[r16];
+      const int dim = 8 * ((lane >> 4) + 4 * r) + blk;
+      if (rok) {
+        const size_t o = (bhm + row) * D + dim;
+        w.Y64[o] = y;
+        const float y32 = (float)y;
+        w.Y[o] = y32;
+        const uint16_t hi = f2bf(y32);
+        w.Yhi[o] = hi;
+        w.Ylo[o] = f2bf(y32 - bf2f(hi));
+      }
+      sq += y * y;
+    }
+  }
+  __syncthreads();
+  red[part][r16] = sq;
+  __syncthreads();
+  if (tid < 16 && rok) {
+    double t = 0.0;
+    for (int p = 0; p < 16; ++p) t += red[p][tid];
+    const int rw = rb16 * 16 + tid;
+    w.ynorm[bhm + rw] = (float)t;
+    w.M64[bhm + rw] = Msh[tid];
+    w.Z64[bhm + rw] = Zsh[tid];
+    w.cw[bhm + rw] = (float)((Msh[tid] + log(Zsh[tid])) * 1.4426950408889634);
+    const E* q = (const E*)Qin + ((size_t)b * g.Hq + (size_t)h * g.g) * g.W * D + (size_t)rw * D;
+    double qq = 0.0;
+    for (int j = 0; j < D; ++j) {
+      const double x = e2d<DT>(q, j);
+      qq += x * x;
+    }
+    w.qn[bhm + rw] = (float)(sqrt(qq) * (1.0 + 1e-6));
+  }
+}
+
+hipError_t launch_obs64(const Geo& g, const Ws& w, const void* K, const void* V, const void* Q, hipStream_t st) {
+  const int nrg = (g.m + 63) / 64;
+  int nblk = 0;
+  for (int b = 0; b < g.B; ++b) nblk += g.H * nrg * ((g.S[b] + g.oc64 - 1) / g.oc64);
+  const int nred = g.B * g.H * (g.mpad / 16);
+  if (g.dtype == 1) {
+    launch("k_obs64", k_obs64<1>, dim3(nblk), dim3(256), 0, st, g, w, K, V, Q);
+    launch("k_obs64_reduce", k_obs64_reduce<1>, dim3(nred), dim3(256), 0, st, g, w, Q);
+  } else {
+    launch("k_obs64", k_obs64<0>, dim3(nblk), dim3(256), 0, st, g, w, K, V, Q);
+    launch("k_obs64_reduce", k_obs64_reduce<0>, dim3(nred), dim3(256), 0, st, g, w, Q);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace akv

@@ -38,15 +38,15 @@ namespace akv {
 // error is below 1e-4 relative: fp32 accumulation of 128 exact bf16 products
 // (at most 128 * 2^-24 * sum |q_i k_i| / sqrt(D) on a logit), fp32 exp and
 // sums; the band is ten times wider.  The fp64 scores use exact fp64 logits
-// and the row sums Z_w of the observation pass (fp64 sums of fp32-logit
-// exponentials, ~1e-9 relative), so they match the canonical fp64 definition
-// to far better than the gaps between real scores.
+// and the row maxima M_w and sums Z_w of the fp64 observation pass (fp64
+// logits and exponentials throughout), so they match the canonical fp64
+// definition to rounding order, far below the gaps between real scores.
 constexpr float SEL_BAND = 1e-3f;
 
 // fp64 pooled selector score of band member i of (request b, head h), one
 // workgroup per member (k_sel_band): (1/kappa) sum_{|d| <= kappa/2,
 // 0 <= t+d < P} (1/m) sum_w exp(dot64(q_w, k_{t+d}) / sqrt(D) - M_w) / Z_w,
-// with the row statistics of the observation pass.  The m query rows and the
+// with the row statistics of the fp64 observation pass.  The m query rows and the
 // kappa key rows are staged in LDS when they fit; thread = (row, offset)
 // pair.  The dot products are exact fp64 products (fused multiply-add of an
 // exact product rounds once, like an add) in four interleaved partial sums
@@ -71,8 +71,8 @@ __global__ __launch_bounds__(256) void k_sel_band(Geo g, Ws w, const void* Kin, 
   const int t = w.sband[(size_t)bh * SEL_BAND_MAX + i];
   const E* X = (const E*)Kin + ((size_t)g.prefS[b] * g.H + (size_t)h * S) * AKV_D;
   const E* Q = (const E*)Qin + ((size_t)b * g.Hq + (size_t)h * g.g) * g.W * AKV_D;
-  const float* oM = w.oM + (size_t)bh * m;
-  const double* oiZ = w.oiZ64 + (size_t)bh * m;
+  const double* M64 = w.M64 + (size_t)bh * m;
+  const double* Z64 = w.Z64 + (size_t)bh * m;
   const double isd = 1.0 / sqrt((double)AKV_D);
   const bool qst = (size_t)m * AKV_D * sizeof(E) <= SEL_QLDS;
   const bool kst = (size_t)nk * AKV_D * sizeof(E) <= SEL_KLDS;
@@ -105,7 +105,7 @@ __global__ __launch_bounds__(256) void k_sel_band(Geo g, Ws w, const void* Kin, 
           p4[e & 3] = fma((double)Elem<DT>::get(qe, e), (double)Elem<DT>::get(xe, e), p4[e & 3]);
       }
       const double l = ((p4[0] + p4[1]) + (p4[2] + p4[3])) * isd;
-      rs += exp(l - (double)oM[wr]) * oiZ[wr];
+      rs += exp(l - M64[wr]) / Z64[wr];
     }
     acc += rs;
   }

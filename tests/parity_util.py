@@ -11,7 +11,6 @@ import paper_2608_02901_amd as akv
 from paper_2608_02901_amd import _native as N
 from oracle import akvref as R
 
-UTIL_RTOL = 2e-3  # fp32 utilities on the GPU vs fp64 in the oracle
 
 
 def make_cfg(wl, **kw):
@@ -65,20 +64,19 @@ def selection_gap_ok(pooled, n_top, rel=1e-4):
     return a - b > rel * max(a, 1e-30)
 
 
-def compare_sets(gsel, osel, u, nsel, rtol=UTIL_RTOL):
-    """Residual sets: equal except for candidates whose oracle utility lies
-    within rtol of the cut (several results are then valid); counts equal."""
+def compare_sets(gsel, osel, u, nsel):
+    """Residual sets: identical (the pooled top-N of the oracle's fp64
+    utilities, ties to the lower head, then the lower position); on a
+    mismatch the message gives the mismatched utilities relative to the cut."""
     assert int(gsel.sum()) == int(osel.sum()) == int(nsel)
     diff = gsel != osel
-    if not diff.any():
-        return 0
-    cand = u[u >= 0]
-    if nsel == 0 or nsel >= cand.size:
-        raise AssertionError("set mismatch with a trivial budget")
-    cut = np.sort(cand)[::-1][nsel - 1]
-    near = np.abs(u - cut) <= rtol * cut
-    assert np.all(near[diff]), f"{int(diff.sum())} mismatches, {int((diff & ~near).sum())} outside the tie band"
-    return int(diff.sum())
+    if diff.any():
+        cand = u[u >= 0]
+        cut = np.sort(cand)[::-1][nsel - 1] if 0 < nsel <= cand.size else float("nan")
+        rel = np.abs(u[diff] - cut) / cut
+        raise AssertionError(f"{int(diff.sum())} residual-set mismatches; oracle utilities at relative distance "
+                             f"{np.sort(rel)[:6]} from the cut {cut:.6g}")
+    return 0
 
 
 def assert_request_parity(exp, enc, cfg, check_sets=True):

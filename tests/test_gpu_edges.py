@@ -169,8 +169,11 @@ def test_selection_and_budget_overflow_paths():
     around the cut overflows (the fp32 order decides, ties to the lower
     position; the header records bit 32), and every key utility is 0, so the
     budget's candidate list overflows too (its cut and tie counts are taken
-    over all utilities).  The anchor list must be valid, and with those anchors
-    the rest of the encode must match the oracle."""
+    over all utilities), and so does the key side's fp64 band (every
+    candidate's bounds touch the cut; the header records bit 8 and the fp32
+    order stands, which is exact here: every key utility is 0 in both
+    precisions).  The anchor list must be valid, and with those anchors the
+    rest of the encode must match the oracle."""
     wl = _wl("sel_overflow", H=2, Hq=4, seq_lens=[40000], anchor_frac=0.02)
     print("[edge] selection and budget overflow paths", flush=True)
     layer = synth.make_layer(wl)
@@ -179,7 +182,7 @@ def test_selection_and_budget_overflow_paths():
     plan = N.Plan(cfg, wl.seq_lens)
     cache, ws, dws = gpu_encode(plan, layer)
     flags = int(cache[8:12].view(torch.int32).item())
-    assert flags & 32 and not flags & ~(32 | 64), flags
+    assert flags & 32 and not flags & ~(8 | 32 | 64), flags
     exp = akv.export(plan, cache.cpu().numpy(), 0, 0)
     S, W, k = wl.seq_lens[0], wl.window, plan.requests[0].anchors
     anc = exp["anchors"]
@@ -188,4 +191,38 @@ def test_selection_and_budget_overflow_paths():
         assert (np.diff(anc[h]) > 0).all() and anc[h, 0] >= 0
         assert (anc[h, -W:] == np.arange(S - W, S)).all()
     enc = oracle_encode(cfg, layer, 0, anchor_override=anc)
+    assert_request_parity(exp, enc, cfg)
+
+
+def test_budget_cut_inside_exact_utility_ties():
+    """The pooled residual budget (Sec. 3.4, Algorithm 1) with its cut inside a
+    block of exactly equal utilities: 61 identical tokens of head 0 (positions
+    299..359, none of them an anchor) share one utility, and the key budget is
+    set so that 30 of them are taken.  The oracle takes the 30 lowest positions
+    (ties to the lower head, then the lower position); the GPU's fp64
+    re-scoring of the band must reproduce that exactly."""
+    wl = _wl("util_ties", seq_lens=[900], anchor_count=64, anchor_frac=0.0)
+    print("[edge] budget cut inside exact utility ties", flush=True)
+    layer = synth.make_layer(wl)
+    S, W = wl.seq_lens[0], wl.window
+    for X in (layer.K[0], layer.V[0]):
+        for h in range(wl.H):
+            X[h, 300:360] = X[h, 299]
+    base = np.r_[np.arange(0, 250, 8)][: 64 - W]
+    assert base.size == 64 - W and base.max() < 299
+    ov = np.stack([np.r_[base, np.arange(S - W, S)] for _ in range(wl.H)]).astype(np.int32)
+    probe = oracle_encode(make_cfg(wl), layer, 0, anchor_override=ov)
+    uK = probe["uK"]
+    group = uK[0, 299]
+    assert np.all(uK[0, 299:360] == group) and group > 0
+    n_above = int(np.sum(uK > group))
+    assert int(np.sum(uK == group)) == 61
+    cfg = make_cfg(wl, budget_mode=N.BUDGET_COUNT, budget_count=n_above + 30)
+    plan = N.Plan(cfg, wl.seq_lens)
+    cache, ws, dws = gpu_encode(plan, layer, override=ov)
+    assert int(cache[8:12].view(torch.int32).item()) == 0
+    enc = oracle_encode(cfg, layer, 0, anchor_override=ov)
+    sel = enc["selK"][0]
+    assert sel[299:329].all() and not sel[329:360].any()
+    exp = akv.export(plan, cache.cpu().numpy(), 0, 0)
     assert_request_parity(exp, enc, cfg)
