@@ -253,7 +253,7 @@ def export(plan: Plan, cache_host: np.ndarray, request: int, n_appended: int = 0
         codes_v=np.zeros((H, S, D // 4), np.uint8), scales_v=np.zeros((H, S, D // G), np.float32),
         tail_a_k=np.zeros((H, max(n_appended, 1)), np.int32), tail_gamma_k=np.zeros((H, max(n_appended, 1)), np.float32),
         tail_a_v=np.zeros((H, max(n_appended, 1)), np.int32), tail_gamma_v=np.zeros((H, max(n_appended, 1)), np.float32),
-        stats=np.zeros(4, np.int64))
+        stats=np.zeros(6, np.int64))
     ea = ExportArrays(*[out[n].ctypes.data for n, _ in ExportArrays._fields_])
     host = np.ascontiguousarray(cache_host, dtype=np.uint8)
     check(lib().anchorkv_export(plan.handle, host.ctypes.data, request, n_appended, ctypes.byref(ea)))

@@ -128,10 +128,6 @@ struct Cache {
 
 // Encode scratch.
 struct Ws {
-  float* opmax;         // [b][h][chunk][2][m] partial row max of the observation logits (per half chunk)
-  double* opsum;        // [b][h][chunk][2][m] partial sum of exp (fp64)
-  float* oM;            // [b][h][m] row max (scaled logits)
-  float* oiZ;           // [b][h][m] 1 / sum exp
   double* o64M;         // [b][h][chunk64][mpad] fp64 pass: chunk row max of the logits
   double* o64Z;         // [b][h][chunk64][mpad] chunk sum of exp(l - chunk max)
   double* o64O;         // [b][h][chunk64][mpad/16][8][4][64] chunk outputs (unnormalized, lane order)
@@ -171,6 +167,7 @@ struct Ws {
   int32_t* bstate;      // [b][side][BST_N] budget state (fields BST_*)
   int32_t* bandpos;     // [b][side][BAND_CAP] flattened (h, t) of the band members
   double* bandu;        // [b][side][BAND_CAP] their fp64 utilities
+  int32_t* brank;       // [b][side][BAND_CAP] their ranks inside the band
   float* bcval;         // [b][side][BCMAX] utilities in the threshold's first-digit bin
   int32_t* bcpos;       // [b][side][BCMAX] their flattened (h, t) index
   int32_t* tiecnt;      // [b][side][nchunk] threshold ties in the earlier chunks

@@ -17,7 +17,7 @@
 
 namespace akv {
 hipError_t launch_init(const Geo& g, const Cache& c, const Ws& w, hipStream_t st);
-hipError_t launch_obs(const Geo& g, const Ws& w, const void* K, const void* V, const void* Q, hipStream_t st);
+hipError_t launch_obs(const Geo& g, const Ws& w, const void* K, const void* Q, hipStream_t st);
 hipError_t launch_obs64(const Geo& g, const Ws& w, const void* K, const void* V, const void* Q, hipStream_t st);
 hipError_t launch_select(const Geo& g, const Ws& w, const Cache& c, const void* K, const void* V, const void* Q,
                          const int32_t* ovr, hipStream_t st);
@@ -67,8 +67,8 @@ struct anchorkv_plan {
       c_stats;
   size_t cache_bytes;
   // encode workspace offsets
-  size_t w_opmax, w_opsum, w_oM, w_oiZ, w_o64M, w_o64Z, w_o64O, w_M64, w_Z64, w_Y64, w_Y, w_Yhi, w_Ylo, w_ynorm,
-      w_cw, w_qn, w_uL, w_uU, w_bandpos, w_bandu, w_sc, w_rank, w_flag, w_sband, w_sbscore, w_sstate, w_sghist, w_scand, w_rkey, w_rpos, w_slcnt, w_QA, w_apos,
+  size_t w_o64M, w_o64Z, w_o64O, w_M64, w_Z64, w_Y64, w_Y, w_Yhi, w_Ylo, w_ynorm,
+      w_cw, w_qn, w_uL, w_uU, w_bandpos, w_bandu, w_brank, w_sc, w_rank, w_flag, w_sband, w_sbscore, w_sstate, w_sghist, w_scand, w_rkey, w_rpos, w_slcnt, w_QA, w_apos,
       w_fix, w_fixcount, w_gpos, w_xn2, w_u, w_sel, w_srec, w_bhist, w_bstate, w_bcval, w_bcpos, w_tiecnt, w_shist, w_wcnt;
   size_t ws_bytes;
   // decode workspace offsets
@@ -252,7 +252,7 @@ extern "C" anchorkv_status anchorkv_plan_create(const anchorkv_config* cfg, int3
     for (int b = 0; b < batch; ++b) geo.prefSp[b + 1] = geo.prefSp[b] + (geo.S[b] + Lsel - 1) / Lsel + 1;
   }
   const size_t TS = (size_t)geo.prefS[batch] * H, TK = (size_t)geo.prefK[batch] * H,
-               TW = (size_t)geo.prefW[batch] * H, TC = (size_t)geo.prefC[batch] * H;
+               TW = (size_t)geo.prefW[batch] * H;
   const size_t NKt = geo.prefNK[batch], NVt = geo.prefNV[batch];
   const size_t esz = geo.esz, m = geo.m, cap = c.max_append;
   Layout L;
@@ -286,10 +286,6 @@ extern "C" anchorkv_status anchorkv_plan_create(const anchorkv_config* cfg, int3
   p->cache_bytes = L.total;
 
   Layout Wl;
-  p->w_opmax = Wl.add(4 * 2 * TC * m);  // two halves per observation chunk
-  p->w_opsum = Wl.add(8 * 2 * TC * m);
-  p->w_oM = Wl.add(4 * batch * H * m);
-  p->w_oiZ = Wl.add(4 * batch * H * m);
   {
     const size_t TC64 = (size_t)geo.prefC64[batch] * H, mp = geo.mpad;
     p->w_o64M = Wl.add(8 * TC64 * mp);
@@ -331,6 +327,7 @@ extern "C" anchorkv_status anchorkv_plan_create(const anchorkv_config* cfg, int3
   p->w_bstate = Wl.add(4 * 2 * akv::BST_N * batch);
   p->w_bandpos = Wl.add(4 * 2 * (size_t)akv::BAND_CAP * batch);
   p->w_bandu = Wl.add(8 * 2 * (size_t)akv::BAND_CAP * batch);
+  p->w_brank = Wl.add(4 * 2 * (size_t)akv::BAND_CAP * batch);
   p->w_bcval = Wl.add(4 * 2 * (size_t)32768 * batch);
   p->w_bcpos = Wl.add(4 * 2 * (size_t)32768 * batch);
   p->w_tiecnt = Wl.add(4 * 2 * (size_t)geo.prefBC[batch]);
@@ -399,10 +396,6 @@ static akv::Cache cache_ptrs(const anchorkv_plan* p, void* base) {
 
 static akv::Ws ws_ptrs(const anchorkv_plan* p, void* base) {
   akv::Ws w;
-  w.opmax = at<float>(base, p->w_opmax);
-  w.opsum = at<double>(base, p->w_opsum);
-  w.oM = at<float>(base, p->w_oM);
-  w.oiZ = at<float>(base, p->w_oiZ);
   w.o64M = at<double>(base, p->w_o64M);
   w.o64Z = at<double>(base, p->w_o64Z);
   w.o64O = at<double>(base, p->w_o64O);
@@ -442,6 +435,7 @@ static akv::Ws ws_ptrs(const anchorkv_plan* p, void* base) {
   w.bstate = at<int32_t>(base, p->w_bstate);
   w.bandpos = at<int32_t>(base, p->w_bandpos);
   w.bandu = at<double>(base, p->w_bandu);
+  w.brank = at<int32_t>(base, p->w_brank);
   w.bcval = at<float>(base, p->w_bcval);
   w.bcpos = at<int32_t>(base, p->w_bcpos);
   w.tiecnt = at<int32_t>(base, p->w_tiecnt);
@@ -476,8 +470,8 @@ extern "C" anchorkv_status anchorkv_encode(const anchorkv_plan* p, const void* K
   (void)hipGetLastError();
   anchorkv_status s;
   if ((s = hip_status(akv::launch_init(g, c, w, st), "init")) != ANCHORKV_OK) return s;
-  if ((s = hip_status(akv::launch_obs(g, w, K, V, Q_obs, st), "observation pass")) != ANCHORKV_OK) return s;
   if ((s = hip_status(akv::launch_obs64(g, w, K, V, Q_obs, st), "fp64 observation pass")) != ANCHORKV_OK) return s;
+  if ((s = hip_status(akv::launch_obs(g, w, K, Q_obs, st), "observation pass")) != ANCHORKV_OK) return s;
   if ((s = hip_status(akv::launch_select(g, w, c, K, V, Q_obs, anchor_pos_override, st), "anchor selection")) !=
       ANCHORKV_OK)
     return s;
@@ -613,6 +607,8 @@ extern "C" anchorkv_status anchorkv_export(const anchorkv_plan* p, const void* c
     o->stats[1] = c.stats[b * 4 + 1];
     o->stats[2] = p->req[b].residuals_k;
     o->stats[3] = p->req[b].residuals_v;
+    o->stats[4] = c.stats[b * 4 + 2];
+    o->stats[5] = c.stats[b * 4 + 3];
   }
   return ANCHORKV_OK;
 }

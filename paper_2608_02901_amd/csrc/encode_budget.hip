@@ -35,8 +35,9 @@
 //                order selected (the selections the band must supply);
 //   k_brescore : the fp64 utility of every band member, computed as the
 //                oracle does (sequential fp64 dots, one wave per member);
-//   k_bselect  : re-marks the band: the `need` largest fp64 utilities, ties to
-//                the lower flattened index.
+//   k_brank    : each band member's rank in (fp64 utility descending,
+//                flattened index ascending) order;
+//   k_bsel     : re-marks the band: ranks below `need` are selected.
 // A band above BAND_CAP keeps the fp32 marks and raises HDR_BAND_OVERFLOW.
 #include "akv_common.h"
 
@@ -327,7 +328,10 @@ __global__ __launch_bounds__(256) void k_bmark(Geo g, Ws w) {
 #pragma unroll
   for (int j = 0; j < per; ++j)
     if ((bandbits >> j) & 1u) {
-      if (slot < BAND_CAP) bp[slot] = lo + j;
+      if (slot < BAND_CAP) {
+        bp[slot] = lo + j;
+        w.brank[(size_t)bs * BAND_CAP + slot] = 0;
+      }
       ++slot;
     }
   const int ns = wave_sum_i(nsel);
@@ -386,22 +390,41 @@ __global__ __launch_bounds__(256) void k_brescore(Geo g, Ws w, Cache c, const vo
         for (int j = 0; j < D; ++j) rvn += (double)rs[wave][j] * (double)rs[wave][j];
       const size_t bh = (size_t)b * g.H + h;
       const E* Q = (const E*)Qin + ((size_t)b * g.Hq + (size_t)h * g.g) * g.W * D;
+      constexpr int PER = 16 / sizeof(E);
+      constexpr int NC = AKV_D / PER;
       for (int wr = lane; wr < m; wr += 64) {
-        const E* q = Q + (size_t)wr * D;
-        double l = 0.0;
-        for (int j = 0; j < D; ++j) l += (double)Elem<DT>::get(q, j) * (double)xs[wave][j];
+        // q.k and q.r_K in one pass over the lane's query row, 16 bytes at a
+        // time with the next chunk's load in flight (sequential sums)
+        const uint4* q4 = (const uint4*)(Q + (size_t)wr * D);
+        double l = 0.0, qr = 0.0;
+        uint4 cur = q4[0];
+        for (int c4 = 0; c4 < NC; ++c4) {
+          const uint4 nxt = q4[min(c4 + 1, NC - 1)];
+#pragma unroll
+          for (int e = 0; e < PER; ++e) {
+            const double qe = (double)Elem<DT>::get(&cur, e);
+            l += qe * (double)xs[wave][c4 * PER + e];
+            qr += qe * (double)rs[wave][c4 * PER + e];
+          }
+          cur = nxt;
+        }
         l = l / sqd;
         const double al = exp(l - w.M64[bh * m + wr]) / w.Z64[bh * m + wr];
         const double a2 = al * al;
         double term;
         if (side == 0) {
-          double qr = 0.0;
-          for (int j = 0; j < D; ++j) qr += (double)Elem<DT>::get(q, j) * (double)rs[wave][j];
-          const double* y = w.Y64 + (bh * m + wr) * D;
+          const double4* y4 = (const double4*)(w.Y64 + (bh * m + wr) * D);
           double vy = 0.0;
-          for (int j = 0; j < D; ++j) {
-            const double dv = (double)vs[wave][j] - y[j];
-            vy += dv * dv;
+          double4 yc = y4[0];
+          for (int c4 = 0; c4 < AKV_D / 4; ++c4) {
+            const double4 yn = y4[min(c4 + 1, AKV_D / 4 - 1)];
+            const double ye[4] = {yc.x, yc.y, yc.z, yc.w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              const double dv = (double)vs[wave][4 * c4 + e] - ye[e];
+              vy += dv * dv;
+            }
+            yc = yn;
           }
           term = a2 * (qr * qr / D) * vy;
         } else {
@@ -425,43 +448,59 @@ __global__ __launch_bounds__(256) void k_brescore(Geo g, Ws w, Cache c, const vo
 
 // Exact ranks inside the band: member i is selected when fewer than `need`
 // members precede it in (fp64 utility descending, flattened index ascending)
-// order.  Grid: (request, side) x BAND_CAP / 1024 member blocks.
-__global__ __launch_bounds__(1024) void k_bselect(Geo g, Ws w, Cache c) {
-  __shared__ double su[1024];
-  __shared__ int sp[1024];
-  constexpr int NBLK = BAND_CAP / 1024;
-  const int bs = blockIdx.x / NBLK, blk = blockIdx.x % NBLK;
-  const int b = bs >> 1, side = bs & 1;
+// order.  k_brank counts, per 256 x 256 tile of (member i, member j) pairs,
+// the j that precede each i and adds the counts to brank[i] (zeroed when the
+// member was listed); the tiles of all lists are spread over a fixed grid.
+// k_bsel then marks the band members from their ranks.
+constexpr int RANK_T = 256;
+__global__ __launch_bounds__(RANK_T) void k_brank(Geo g, Ws w) {
+  __shared__ double su[RANK_T];
+  __shared__ int sp[RANK_T];
+  int tile0 = 0;
+  for (int bs = 0; bs < 2 * g.B; ++bs) {
+    const int b = bs >> 1, side = bs & 1;
+    const int nl = w.bstate[bs * BST_N + BST_NBAND];
+    const int n = (bmode(g, b, side) == 0 && nl <= BAND_CAP) ? nl : 0;
+    const int nt = (n + RANK_T - 1) / RANK_T;
+    const int32_t* bp = w.bandpos + (size_t)bs * BAND_CAP;
+    const double* bu = w.bandu + (size_t)bs * BAND_CAP;
+    int32_t* br = w.brank + (size_t)bs * BAND_CAP;
+    int t = (int)blockIdx.x - tile0;
+    if (t < 0) t += ((-t + (int)gridDim.x - 1) / (int)gridDim.x) * (int)gridDim.x;
+    for (; t < nt * nt; t += gridDim.x) {  // uniform per workgroup
+      const int ti = t / nt, tj = t % nt;
+      const int j = tj * RANK_T + threadIdx.x;
+      __syncthreads();
+      su[threadIdx.x] = j < n ? bu[j] : 0.0;
+      sp[threadIdx.x] = j < n ? bp[j] : 0x7FFFFFFF;
+      __syncthreads();
+      const int i = ti * RANK_T + threadIdx.x;
+      if (i < n) {
+        const double ui = bu[i];
+        const int pi = bp[i];
+        const int nj = min(RANK_T, n - tj * RANK_T);
+        int r = 0;
+        for (int jj = 0; jj < nj; ++jj) r += (su[jj] > ui || (su[jj] == ui && sp[jj] < pi)) ? 1 : 0;
+        if (r) atomicAdd(&br[i], r);
+      }
+    }
+    tile0 += nt * nt;
+  }
+}
+
+__global__ __launch_bounds__(256) void k_bsel(Geo g, Ws w, Cache c) {
+  const int bs = blockIdx.y, b = bs >> 1, side = bs & 1;
   if (bmode(g, b, side) != 0) return;
   const int n = w.bstate[bs * BST_N + BST_NBAND];
-  if (n > BAND_CAP) {
-    if (blk == 0 && threadIdx.x == 0) atomicOr(&c.header[2], HDR_BAND_OVERFLOW);
-    return;
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    c.stats[b * 4 + 2 + side] = n;  // band size, reported by the export
+    if (n > BAND_CAP) atomicOr(&c.header[2], HDR_BAND_OVERFLOW);
   }
-  if (blk * 1024 >= n) return;
+  if (n > BAND_CAP) return;
   const int need = w.bstate[bs * BST_N + BST_NEED];
-  const int32_t* bp = w.bandpos + (size_t)bs * BAND_CAP;
-  const double* bu = w.bandu + (size_t)bs * BAND_CAP;
-  const int i = blk * 1024 + threadIdx.x;
-  const bool mine = i < n;
-  const double ui = mine ? bu[i] : 0.0;
-  const int pi = mine ? bp[i] : 0;
-  int rank = 0;
-  for (int j0 = 0; j0 < n; j0 += 1024) {
-    __syncthreads();
-    if (j0 + (int)threadIdx.x < n) {
-      su[threadIdx.x] = bu[j0 + threadIdx.x];
-      sp[threadIdx.x] = bp[j0 + threadIdx.x];
-    }
-    __syncthreads();
-    const int nj = min(1024, n - j0);
-    if (mine)
-      for (int j = 0; j < nj; ++j) rank += (su[j] > ui || (su[j] == ui && sp[j] < pi)) ? 1 : 0;
-  }
-  if (mine) {
-    uint8_t* sel = w.sel + (size_t)side * g.H * g.prefS[g.B] + (size_t)g.prefS[b] * g.H;
-    sel[pi] = rank < need ? 1 : 0;
-  }
+  uint8_t* sel = w.sel + (size_t)side * g.H * g.prefS[g.B] + (size_t)g.prefS[b] * g.H;
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x)
+    sel[w.bandpos[(size_t)bs * BAND_CAP + i]] = w.brank[(size_t)bs * BAND_CAP + i] < need ? 1 : 0;
 }
 
 hipError_t launch_budget(const Geo& g, const Ws& w, const Cache& c, const void* K, const void* V, const void* Q,
@@ -477,7 +516,8 @@ hipError_t launch_budget(const Geo& g, const Ws& w, const Cache& c, const void* 
     launch("k_brescore", k_brescore<1>, dim3(1024), dim3(256), 0, st, g, w, c, K, V, Q);
   else
     launch("k_brescore", k_brescore<0>, dim3(1024), dim3(256), 0, st, g, w, c, K, V, Q);
-  launch("k_bselect", k_bselect, dim3(g.B * 2 * (BAND_CAP / 1024)), dim3(1024), 0, st, g, w, c);
+  launch("k_brank", k_brank, dim3(2048), dim3(RANK_T), 0, st, g, w);
+  launch("k_bsel", k_bsel, dim3(64, g.B * 2), dim3(256), 0, st, g, w, c);
   return hipGetLastError();
 }
 

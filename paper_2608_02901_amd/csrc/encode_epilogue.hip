@@ -52,7 +52,12 @@ __global__ __launch_bounds__(256, R == 1 ? 2 : 1) void k_epilogue(Geo g, Ws w, C
   __shared__ __align__(16) E VT[32 * LD];
   __shared__ float gK_s[EPI_TOK], rv2_s[EPI_TOK], vn_s[EPI_TOK], rk2_s[EPI_TOK];
   __shared__ int aK_s[EPI_TOK];
-  __shared__ float sumK[4][EPI_TOK], sumV[4][EPI_TOK];
+  // Row sums per token: each wave leaves its partials of a tile in tpart
+  // (double-buffered by tile parity); 32 threads add the four waves' partials
+  // in a fixed order into sumK (sum a2 vv qr^2), sumV (sum a2) and sumQ
+  // (sum a2 qr^2) after the next tile's first barrier.
+  __shared__ float tpart[2][3][4][32];
+  __shared__ float sumK[EPI_TOK], sumV[EPI_TOK], sumQ[EPI_TOK];
   __shared__ __align__(16) float CVS[256], YVS[256];  // per observation row: softmax constant, ||y_w||^2
   __shared__ unsigned hmax[3];  // head maxima (float bits): ||q_w||, ||y_w||^2, |c_w|
   extern __shared__ __align__(16) char qlds_raw[];  // the m observation rows, row stride LD
@@ -233,9 +238,17 @@ __global__ __launch_bounds__(256, R == 1 ? 2 : 1) void k_epilogue(Geo g, Ws w, C
   };
   const int ntl = min(NT, (S - tb + 31) / 32);
   fetch(tb);
+  auto fold = [&](int tt) {  // tile tt's partials into the per-token sums
+    const int tl = 32 * tt + threadIdx.x;
+    const float(*pp)[4][32] = tpart[tt & 1];
+    sumK[tl] = (pp[0][0][threadIdx.x] + pp[0][1][threadIdx.x]) + (pp[0][2][threadIdx.x] + pp[0][3][threadIdx.x]);
+    sumV[tl] = (pp[1][0][threadIdx.x] + pp[1][1][threadIdx.x]) + (pp[1][2][threadIdx.x] + pp[1][3][threadIdx.x]);
+    sumQ[tl] = (pp[2][0][threadIdx.x] + pp[2][1][threadIdx.x]) + (pp[2][2][threadIdx.x] + pp[2][3][threadIdx.x]);
+  };
   for (int it = 0; it < ntl; ++it) {
     const int t0 = tb + 32 * it;
     __syncthreads();  // previous tile's LDS reads are done (and, at it = 0, the coefficients are in LDS)
+    if (it > 0 && threadIdx.x < 32) fold(it - 1);
 #pragma unroll
     for (int i = 0; i < RPT; ++i) {
       const int ch = threadIdx.x + 256 * i, r = ch / CPR, col = (ch % CPR) * PER;
@@ -251,7 +264,7 @@ __global__ __launch_bounds__(256, R == 1 ? 2 : 1) void k_epilogue(Geo g, Ws w, C
     // consecutive) is read before the contraction, for every token (anchor 0
     // stands in for an anchor position), so its latency overlaps the MFMAs.
     const float* qa = QA + (size_t)max(ak, 0) * m;
-    float tk = 0.0f, tv = 0.0f;
+    float tk = 0.0f, tv = 0.0f, tq = 0.0f;
 #pragma unroll
     for (int r = 0; r < R; ++r) {
       const int rb = wave + 4 * r;
@@ -295,7 +308,9 @@ __global__ __launch_bounds__(256, R == 1 ? 2 : 1) void k_epilogue(Geo g, Ws w, C
             // ||v - y||^2 >= 0: the cancellation form can dip below zero
             // when y nearly equals v; the bounds below cover the clamp.
             const float vv = fmaxf(fmaf(-2.0f, accY[e], vn + yq[i]), 0.0f);
-            tk = fmaf(a2 * vv, qr * qr, tk);
+            const float q2 = qr * qr;
+            tk = fmaf(a2 * vv, q2, tk);
+            tq = fmaf(a2, q2, tq);
             tv += a2;
           }
         }
@@ -303,33 +318,39 @@ __global__ __launch_bounds__(256, R == 1 ? 2 : 1) void k_epilogue(Geo g, Ws w, C
     }
     tk += __shfl_xor(tk, 32, 64);
     tv += __shfl_xor(tv, 32, 64);
+    tq += __shfl_xor(tq, 32, 64);
     if (lane < 32) {
-      sumK[wave][tl] = tk;
-      sumV[wave][tl] = tv;
+      tpart[it & 1][0][wave][lane] = tk;
+      tpart[it & 1][1][wave][lane] = tv;
+      tpart[it & 1][2][wave][lane] = tq;
     }
   }
+  __syncthreads();
+  if (threadIdx.x < 32) fold(ntl - 1);
   __syncthreads();
   // ---- per token: the fp32 estimates and proven bounds [uL, uU] of the
   // canonical fp64 utilities (Sec. 3.3 Eq. utilities computed in fp64 from
   // the exact fp64 logits, y_w, M_w and Z_w).  With u = 2^-24:
   //   alpha: |ln(alpha32 / alpha)| <= eta = ln2 [c1 qmax |k| isl
-  //          + u (3 qmax |k| isl + 2 cmax)] + 4u  (logit MFMA error c1 |q||k|,
-  //          c1 = 512u; the roundings of isl, the fma and c_w; exp2);
+  //          + u (3 qmax |k| isl + 2 cmax)] + 4u  (logit MFMA error c1 |q||k|:
+  //          twice the error bound of a sequential fp32 sum of the 128
+  //          products, which are exact for bf16 (c1 = 256u) and rounded for
+  //          fp32 (c1 = 512u); the roundings of isl, the fma and c_w; exp2);
   //   q.r_K: |qr32 - qr| <= e = qmax (|k| + |gamma| |a|) (c1 + 4u) (logit and
   //          QA-table MFMA errors, the residual's rounding);
   //   vv   : |vv32 - ||v - y||^2| <= dvv = 258u |v|^2 + 4u ymax^2
   //          + 9.3e-5 |v| ymax (|v|^2 and ||y||^2 roundings, the bf16 hi/lo
   //          split of y and the MFMA error of v.y, the fp32 combination);
-  // and with tk = sum a2 vv qr^2 (a2 = alpha32^2), tv = sum a2 (fp32 sums of
-  // non-negative terms, relative error <= 301u), S0 = sum a2 vv <= V2 tv,
-  // S2 = sum a2 qr^2 <= Qr2 tv, S3 = sum a2 |qr| <= sqrt(Qr2) tv and
-  // sum a2 vv |qr| <= sqrt(tk S0):
+  // and with tk = sum a2 vv qr^2 (a2 = alpha32^2), tv = sum a2, S2 = sum a2
+  // qr^2 (fp32 sums of non-negative terms, relative error <= 301u), S0 = sum
+  // a2 vv <= V2 tv, S3 = sum a2 |qr| <= sqrt(S2 tv) and sum a2 vv |qr| <=
+  // sqrt(tk S0) (Cauchy-Schwarz):
   //   m D uK <= (1+ea)^2 [tk + 2e sqrt(tk S0) + e^2 S0 + dvv (S2 + 2e S3 + e^2 tv)]
   //   m D uK >= (1-ea)^2 [tk - 2e sqrt(tk S0) - dvv S2]
   // (ea = eta (1 + eta)); the value side scales ||r_V||^2 tv / m likewise.
   {
     constexpr float U = 5.9604645e-8f;  // 2^-24
-    constexpr float C1 = 512.0f * U;
+    constexpr float C1 = (DT == 1 ? 256.0f : 512.0f) * U;
     const float qmax = __uint_as_float(hmax[0]);
     const float ymax2 = __uint_as_float(hmax[1]) * (1.0f + 8.0f * U);
     const float ymax = sqrtf(ymax2) * (1.0f + 2.0f * U);
@@ -341,8 +362,7 @@ __global__ __launch_bounds__(256, R == 1 ? 2 : 1) void k_epilogue(Geo g, Ws w, C
       float uk = -1.0f, uv = -1.0f, ukl = -1.0f, uku = -1.0f, uvl = -1.0f, uvu = -1.0f;
       const int ak = aK_s[tl];
       if (ak >= 0) {
-        const float sk = (sumK[0][tl] + sumK[1][tl]) + (sumK[2][tl] + sumK[3][tl]);
-        const float sv = (sumV[0][tl] + sumV[1][tl]) + (sumV[2][tl] + sumV[3][tl]);
+        const float sk = sumK[tl], sv = sumV[tl], sq = sumQ[tl];
         uk = sk / ((float)m * (float)D);
         uv = rv2_s[tl] * sv / (float)m;
         // token quantities (upper bounds of the norms)
@@ -365,8 +385,10 @@ __global__ __launch_bounds__(256, R == 1 ? 2 : 1) void k_epilogue(Geo g, Ws w, C
         const float tvh = sv * (1.0f + r1), tvl = sv * (1.0f - r1);
         const float S0 = V2 * tvh;
         const float cs = sqrtf(tkh * S0) * (1.0f + 2.0f * U);
-        const float hiK = tkh + 2.0f * e * cs + e * e * S0 + dvv * (Qr2 * tvh + 2.0f * e * qr1 * tvh + e * e * tvh);
-        const float loK = tkl - 2.0f * e * cs - dvv * Qr2 * tvh;
+        const float S2 = sq * (1.0f + r1);
+        const float S3 = sqrtf(S2 * tvh) * (1.0f + 2.0f * U);
+        const float hiK = tkh + 2.0f * e * cs + e * e * S0 + dvv * (S2 + 2.0f * e * S3 + e * e * tvh);
+        const float loK = tkl - 2.0f * e * cs - dvv * S2;
         const float md = (float)m * (float)D;
         // fp32 underflow (flushed or subnormal intermediates) leaves at most
         // 2^-126 (Qr2 V2 + Qr2 + 1) per row term, m terms, / (m D)

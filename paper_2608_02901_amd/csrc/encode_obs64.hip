@@ -114,51 +114,56 @@ __global__ __launch_bounds__(256) void k_obs64(Geo g, Ws w, const void* Kin, con
     if (t0 + O64_KT < te) stash(cb ^ 1);
     if (t0 + 2 * O64_KT < te) fetch(t0 + 2 * O64_KT);
     if (!active) continue;
-    // ---- logits of 32 keys: two 16-key tiles.  Register r of sacc[u] is
-    // key t0 + 16u + kq + 4r against row l%16.
-    f64x4 sacc[2];
+    // Two 16-key steps per LDS tile, unrolled so that the scheduler can
+    // overlap one step's softmax with the other's contractions.
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
+      // ---- logits: register r of acc is key t0 + 16u + kq + 4r against row l%16
       uint4 kraw[32 / PER];
       const E* kr = &KT[cb][(16 * u + (lane & 15)) * LDK + 32 * kq];
 #pragma unroll
       for (int c = 0; c < 32 / PER; ++c) kraw[c] = *(const uint4*)(kr + c * PER);
-      f64x4 acc = {0.0, 0.0, 0.0, 0.0};
+      // The query fragment stays packed: converting it once outside the loop
+      // would hold 64 more registers for the whole chunk.
 #pragma unroll
-      for (int s = 0; s < 32; ++s) acc = mfma64(e2d<DT>(kraw, s), e2d<DT>(qraw, s), acc);
-      sacc[u] = acc;
-    }
-    double lg[8];
-    bool ok[8];
-    double tmax = O64_NEG;
+      for (int c = 0; c < 32 / PER; ++c)
+        asm volatile("" : "+v"(qraw[c].x), "+v"(qraw[c].y), "+v"(qraw[c].z), "+v"(qraw[c].w));
+      // two independent accumulation chains (even and odd s)
+      f64x4 acc = {0.0, 0.0, 0.0, 0.0}, acc1 = {0.0, 0.0, 0.0, 0.0};
 #pragma unroll
-    for (int u = 0; u < 2; ++u)
+      for (int s = 0; s < 32; s += 2) {
+        acc = mfma64(e2d<DT>(kraw, s), e2d<DT>(qraw, s), acc);
+        acc1 = mfma64(e2d<DT>(kraw, s + 1), e2d<DT>(qraw, s + 1), acc1);
+      }
+      acc += acc1;
+      double lg[4];
+      bool ok[4];
+      double tmax = O64_NEG;
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int e = 4 * u + r;
-        ok[e] = t0 + 16 * u + kq + 4 * r <= lim;
-        lg[e] = sacc[u][r] * isd;
-        if (ok[e]) tmax = fmax(tmax, lg[e]);
+        ok[r] = t0 + 16 * u + kq + 4 * r <= lim;
+        lg[r] = acc[r] * isd;
+        if (ok[r]) tmax = fmax(tmax, lg[r]);
       }
-    tmax = fmax(tmax, __shfl_xor(tmax, 16, 64));
-    tmax = fmax(tmax, __shfl_xor(tmax, 32, 64));
-    const double nm = fmax(mrow, tmax);
-    const double scl = exp(mrow - nm);  // 1 when the max stays, 0 on the first valid tile
-    zl *= scl;
+      tmax = fmax(tmax, __shfl_xor(tmax, 16, 64));
+      tmax = fmax(tmax, __shfl_xor(tmax, 32, 64));
+      const double nm = fmax(mrow, tmax);
+      if (__ballot(nm > mrow)) {  // some row's max moved: rescale (factor 1 on the others)
+        const double scl = exp(mrow - nm);
+        zl *= scl;
 #pragma unroll
-    for (int blk = 0; blk < 8; ++blk) O[blk] *= scl;
-    mrow = nm;
-    double p[8];
+        for (int blk = 0; blk < 8; ++blk) O[blk] *= scl;
+      }
+      mrow = nm;
+      double p[4];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      p[e] = ok[e] ? exp(lg[e] - nm) : 0.0;
-      zl += p[e];
-    }
-    // ---- values: MFMA (u, r) contracts the keys 16u + kq + 4r, k = kq; lane
-    // l supplies V[key][8 (l%16) + blk] as A and its own p as B, so output
-    // register r' of O[blk] is O^T[dim 8 (l/16 + 4 r') + blk][row l%16].
-#pragma unroll
-    for (int u = 0; u < 2; ++u)
+      for (int r = 0; r < 4; ++r) {
+        p[r] = ok[r] ? exp(lg[r] - nm) : 0.0;
+        zl += p[r];
+      }
+      // ---- values: MFMA r contracts the keys 16u + kq + 4r (k = kq); lane l
+      // supplies V[key][8 (l%16) + blk] as A and its own p as B, so output
+      // register r' of O[blk] is O^T[dim 8 (l/16 + 4 r') + blk][row l%16].
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const E* vr = &VT[cb][(16 * u + kq + 4 * r) * LDK + 8 * (lane & 15)];
@@ -166,8 +171,9 @@ __global__ __launch_bounds__(256) void k_obs64(Geo g, Ws w, const void* Kin, con
 #pragma unroll
         for (int c = 0; c < 8 / PER; ++c) vraw[c] = *(const uint4*)(vr + c * PER);
 #pragma unroll
-        for (int blk = 0; blk < 8; ++blk) O[blk] = mfma64(e2d<DT>(vraw, blk), p[4 * u + r], O[blk]);
+        for (int blk = 0; blk < 8; ++blk) O[blk] = mfma64(e2d<DT>(vraw, blk), p[r], O[blk]);
       }
+    }
   }
   if (!active) return;
   zl += __shfl_xor(zl, 16, 64);
@@ -237,8 +243,16 @@ __global__ __launch_bounds__(256) void k_obs64_reduce(Geo g, Ws w, const void* Q
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const double* op = w.o64O + (gc0 * nrb + rb16) * 2048 + (blk * 4 + r) * 64 + lane;
+      // chunks added in order, their partial outputs loaded 8 at a time
       double acc = 0.0;
-      for (int c = 0; c < nch; ++c) acc += op[(size_t)c * nrb * 2048] * scl[c][r16];
+      for (int c0 = 0; c0 < nch; c0 += 8) {
+        double v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) v[u] = c0 + u < nch ? op[(size_t)(c0 + u) * nrb * 2048] : 0.0;
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          if (c0 + u < nch) acc += v[u] * scl[c0 + u][r16];
+      }
       const double y = acc / Zsh[r16];
       const int dim = 8 * ((lane >> 4) + 4 * r) + blk;
       if (rok) {

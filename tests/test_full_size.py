@@ -82,7 +82,7 @@ def test_small_workloads_whole_against_oracle(wi):
     for h in range(wl.H):
         assert selection_gap_ok(enc["pooled"][h], ri.n_top, SEL_GAP), "near-tie at the selection cut"
     mism = assert_request_parity(exp, enc, cfg)
-    print(f"[full] workload {wi}: set ties {mism}, fixup rows {exp['stats'][:2]}", flush=True)
+    print(f"[full] workload {wi}: fixup rows {exp['stats'][:2]}, budget bands {exp['stats'][4:6]}", flush=True)
     out = torch.empty(1, wl.Hq, wl.D, dtype=torch.float32, device="cuda")
     akv.decode_attn(plan, cache, lay.q[0].cuda(), out, dws)
     torch.cuda.synchronize()
@@ -177,6 +177,7 @@ def test_workload3_128k_sampled_and_decode_steps():
     del keep
     assert _header_flags(cache) == 0
     exp = _export(plan, cache, 0)
+    print(f"[full] workload 3: fixup rows {exp['stats'][:2]}, budget bands {exp['stats'][4:6]}", flush=True)
     n = _sampled_request_check(cfg, lay, 0, exp, 256, np.random.default_rng(30))
     print(f"[full] workload 3: sampled codes checked {n}", flush=True)
     err = _decode_property(plan, cache, dws, lay, [0], steps=4, append=True)
