@@ -17,11 +17,18 @@
  *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).  All
  *     work is enqueued on it in order; results are valid once it completes.
  *   - Host pointers are read (or written) only during the call.
+ *   - Every buffer comes with its size in bytes.  A size below what the plan
+ *     needs returns ANCHORKV_ERR_BUFFER_TOO_SMALL (larger buffers are fine);
+ *     the library never reads or writes past the size the plan needs.
  *   - Every argument is validated before anything is enqueued.  On an error
  *     nothing is enqueued, the status says why and anchorkv_last_error()
  *     returns a detail string for the calling thread.  A HIP launch failure
  *     returns ANCHORKV_ERR_HIP; the stream state is then undefined for the
  *     work of that call.  No entry point throws or aborts.
+ *   - Fault injection (tests of the error path): when the environment
+ *     variable ANCHORKV_FAULT_INJECT names a kernel (e.g. "k_assign"), a call
+ *     that reaches that kernel enqueues nothing from it on, and returns
+ *     ANCHORKV_ERR_HIP with a message naming the kernel.
  *   - Query head j reads KV head j / (num_q_heads / num_kv_heads) (GQA).
  */
 #ifndef ANCHORKV_H
@@ -40,7 +47,8 @@ typedef enum {
   ANCHORKV_ERR_UNSUPPORTED = 2,   /* valid for the method, outside this build's limits */
   ANCHORKV_ERR_CAPACITY = 3,      /* append beyond the capacity reserved at plan time */
   ANCHORKV_ERR_CORRUPT_CACHE = 4, /* export of a blob whose header does not match the plan */
-  ANCHORKV_ERR_HIP = 5            /* a HIP runtime call failed */
+  ANCHORKV_ERR_HIP = 5,           /* a HIP runtime call failed (or a fault was injected) */
+  ANCHORKV_ERR_BUFFER_TOO_SMALL = 6 /* a buffer's size is below what the plan needs */
 } anchorkv_status;
 
 typedef enum { ANCHORKV_F32 = 0, ANCHORKV_BF16 = 1 } anchorkv_dtype;
@@ -120,20 +128,26 @@ anchorkv_status anchorkv_plan_request(const anchorkv_plan* plan, int32_t request
 
 /* The compression pass (Algorithm 1) for all requests of the plan.
  *   K, V    : device, dtype; request b is a contiguous [H][S_b][D] block, the
- *             blocks packed back to back in request order.
+ *             blocks packed back to back in request order.  kv_bytes: the size
+ *             of each (>= sum_b H S_b D element bytes).
  *   Q_obs   : device, dtype; request b is [Hq][W][D] (the queries of the last W
- *             positions, the observation window of Sec. 3.2), packed likewise.
+ *             positions, the observation window of Sec. 3.2), packed likewise;
+ *             q_obs_bytes >= batch Hq W D element bytes.
  *   anchor_pos_override : NULL, or device int32 [sum_b H*k_b]: per request and
  *             head the k_b anchor positions, strictly increasing, containing the
  *             last W positions; replaces the selection step.  An override that
  *             breaks these rules marks the cache invalid (anchorkv_export then
- *             returns ANCHORKV_ERR_CORRUPT_CACHE).
- *   cache   : device, anchorkv_cache_bytes(plan); receives the compressed layer.
- *   workspace : device, anchorkv_encode_workspace_bytes(plan); scratch, contents
- *             undefined afterwards.  cache and workspace must not overlap the inputs. */
-anchorkv_status anchorkv_encode(const anchorkv_plan* plan, const void* K, const void* V, const void* Q_obs,
-                                const int32_t* anchor_pos_override, void* cache, void* workspace,
-                                void* stream);
+ *             returns ANCHORKV_ERR_CORRUPT_CACHE).  override_bytes >= 4 sum_b H k_b
+ *             when it is given.
+ *   cache   : device, cache_bytes >= anchorkv_cache_bytes(plan); receives the
+ *             compressed layer.
+ *   workspace : device, workspace_bytes >= anchorkv_encode_workspace_bytes(plan);
+ *             scratch, contents undefined afterwards.  cache and workspace must
+ *             not overlap the inputs. */
+anchorkv_status anchorkv_encode(const anchorkv_plan* plan, const void* K, const void* V, size_t kv_bytes,
+                                const void* Q_obs, size_t q_obs_bytes, const int32_t* anchor_pos_override,
+                                size_t override_bytes, void* cache, size_t cache_bytes, void* workspace,
+                                size_t workspace_bytes, void* stream);
 
 /* Appends one generated token per request and KV head (config max_append
  * slots).  The token is encoded against the request's existing anchors (its
@@ -141,39 +155,47 @@ anchorkv_status anchorkv_encode(const anchorkv_plan* plan, const void* K, const 
  * same certified argmax and canonical coefficient as the compression pass) and
  * stores no residual.  n_appended: tokens already appended to this cache
  * (host-tracked), must be < max_append, else ANCHORKV_ERR_CAPACITY.
- * k_new, v_new: device [batch][H][D], dtype.  workspace: device,
- * anchorkv_decode_workspace_bytes(plan), contents undefined afterwards. */
-anchorkv_status anchorkv_append(const anchorkv_plan* plan, void* cache, int32_t n_appended, const void* k_new,
-                                const void* v_new, void* workspace, void* stream);
+ * k_new, v_new: device [batch][H][D], dtype, new_bytes the size of each.
+ * workspace: device, workspace_bytes >= anchorkv_decode_workspace_bytes(plan),
+ * contents undefined afterwards. */
+anchorkv_status anchorkv_append(const anchorkv_plan* plan, void* cache, size_t cache_bytes, int32_t n_appended,
+                                const void* k_new, const void* v_new, size_t new_bytes, void* workspace,
+                                size_t workspace_bytes, void* stream);
 
 /* Decode attention over the compressed cache (Eq. exact-attention with the
  * reconstructed keys and values of Eq. reconstruction), never materializing
  * them: q.k^_t = gamma_t (q.k_a(t)) + q.r~_t and the values accumulate as
  * per-anchor weights plus a rotated residual sum (App. E.1).
  *   n_appended : appended tokens included (the first n_appended tail slots).
- *   q          : device [batch][Hq][D], dtype; query head j reads KV head j / g.
- *   out        : device [batch][Hq][D], out_dtype (anchorkv_dtype).
+ *   q          : device [batch][Hq][D], dtype (q_bytes its size); query head j
+ *                reads KV head j / g.
+ *   out        : device [batch][Hq][D], out_dtype (anchorkv_dtype), out_bytes
+ *                its size.
  *   softmax_scale : <= 0 selects 1/sqrt(D).
- *   workspace  : device, anchorkv_decode_workspace_bytes(plan); contents
- *                undefined afterwards.  Two calls that share a workspace must
- *                not run concurrently. */
-anchorkv_status anchorkv_decode_attn(const anchorkv_plan* plan, const void* cache, int32_t n_appended,
-                                     const void* q, void* out, int32_t out_dtype, float softmax_scale,
-                                     void* workspace, void* stream);
+ *   workspace  : device, workspace_bytes >= anchorkv_decode_workspace_bytes(plan);
+ *                contents undefined afterwards.  Two calls that share a
+ *                workspace must not run concurrently. */
+anchorkv_status anchorkv_decode_attn(const anchorkv_plan* plan, const void* cache, size_t cache_bytes,
+                                     int32_t n_appended, const void* q, size_t q_bytes, void* out, size_t out_bytes,
+                                     int32_t out_dtype, float softmax_scale, void* workspace, size_t workspace_bytes,
+                                     void* stream);
 
 /* One generation step: anchorkv_append of (k_new, v_new) as tail slot
  * n_appended, then anchorkv_decode_attn over the cache including it
  * (n_appended + 1 tail tokens).  The result equals the two calls in sequence;
  * the append's anchor scan shares the attention's passes over the anchors, so
  * it adds no pass over HBM.  Arguments as in those two calls. */
-anchorkv_status anchorkv_decode_step(const anchorkv_plan* plan, void* cache, int32_t n_appended, const void* k_new,
-                                     const void* v_new, const void* q, void* out, int32_t out_dtype,
-                                     float softmax_scale, void* workspace, void* stream);
+anchorkv_status anchorkv_decode_step(const anchorkv_plan* plan, void* cache, size_t cache_bytes, int32_t n_appended,
+                                     const void* k_new, const void* v_new, size_t new_bytes, const void* q,
+                                     size_t q_bytes, void* out, size_t out_bytes, int32_t out_dtype,
+                                     float softmax_scale, void* workspace, size_t workspace_bytes, void* stream);
 
 /* Dense reconstruction (Eq. reconstruction) of one side (0 = keys, 1 = values)
- * of one request: out is device fp32 [H][S_b + n_appended][D], position order. */
-anchorkv_status anchorkv_reconstruct(const anchorkv_plan* plan, const void* cache, int32_t n_appended,
-                                     int32_t request, int32_t side, float* out, void* stream);
+ * of one request: out is device fp32 [H][S_b + n_appended][D], position order,
+ * out_bytes its size. */
+anchorkv_status anchorkv_reconstruct(const anchorkv_plan* plan, const void* cache, size_t cache_bytes,
+                                     int32_t n_appended, int32_t request, int32_t side, float* out, size_t out_bytes,
+                                     void* stream);
 
 /* Logical content of one request, in position order, from a HOST copy of the
  * cache blob (pure host code).  Every pointer is caller-allocated host memory,
@@ -181,8 +203,10 @@ anchorkv_status anchorkv_reconstruct(const anchorkv_plan* plan, const void* cach
  *   anchors [H][k] int32; a_X [H][S] int32 anchor index; gamma_X [H][S] fp32
  *   stored coefficient; sel_X [H][S] uint8 residual flag; codes_X [H][S][D/4];
  *   scales_X [H][S][D/G] (zero where no residual); tail_a_X, tail_gamma_X
- *   [H][n_appended]; stats[4]: tokens resolved by the exact fp64 path of the
- *   certified argmax, keys then values, then N_K, N_V. */
+ *   [H][n_appended]; stats[6]: tokens resolved by the exact fp64 path of the
+ *   certified argmax, keys then values, then N_K, N_V, then the candidates
+ *   whose utility bounds straddled the residual budget's cut and were re-scored
+ *   in fp64, keys then values. */
 typedef struct anchorkv_export_arrays {
   int32_t* anchors;
   int32_t* a_k;
@@ -202,7 +226,10 @@ typedef struct anchorkv_export_arrays {
   int64_t* stats;
 } anchorkv_export_arrays;
 
-anchorkv_status anchorkv_export(const anchorkv_plan* plan, const void* cache_host, int32_t request,
+/* Decodes request `request` of a host copy of cache_bytes bytes (>= the
+ * plan's cache size) with n_appended tail tokens.  The export is a host-side
+ * reading of the layout the compression pass writes (App. A.1 "Layout"). */
+anchorkv_status anchorkv_export(const anchorkv_plan* plan, const void* cache_host, size_t cache_bytes, int32_t request,
                                 int32_t n_appended, anchorkv_export_arrays* out);
 
 /* Kernel timing for benchmarks and tracing.  While enabled, every launch of

@@ -16,7 +16,7 @@ import numpy as np
 _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "lib", "libanchorkv.so")
 
-OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_CAPACITY, ERR_CORRUPT_CACHE, ERR_HIP = range(6)
+OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_CAPACITY, ERR_CORRUPT_CACHE, ERR_HIP, ERR_BUFFER_TOO_SMALL = range(7)
 F32, BF16 = 0, 1
 SCALE_ABSMAX_OUTER, SCALE_ABSMAX_LITERAL, SCALE_RMS = 0, 1, 2
 BUDGET_FRACTION, BUDGET_THETA, BUDGET_COUNT = 0, 1, 2
@@ -79,18 +79,19 @@ def lib():
             getattr(L, n).argtypes = [vp]
         L.anchorkv_plan_request.restype = i32
         L.anchorkv_plan_request.argtypes = [vp, i32, ctypes.POINTER(RequestInfo)]
+        sz = ctypes.c_size_t
         L.anchorkv_encode.restype = i32
-        L.anchorkv_encode.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp]
+        L.anchorkv_encode.argtypes = [vp, vp, vp, sz, vp, sz, vp, sz, vp, sz, vp, sz, vp]
         L.anchorkv_append.restype = i32
-        L.anchorkv_append.argtypes = [vp, vp, i32, vp, vp, vp, vp]
+        L.anchorkv_append.argtypes = [vp, vp, sz, i32, vp, vp, sz, vp, sz, vp]
         L.anchorkv_decode_attn.restype = i32
-        L.anchorkv_decode_attn.argtypes = [vp, vp, i32, vp, vp, i32, f32, vp, vp]
+        L.anchorkv_decode_attn.argtypes = [vp, vp, sz, i32, vp, sz, vp, sz, i32, f32, vp, sz, vp]
         L.anchorkv_decode_step.restype = i32
-        L.anchorkv_decode_step.argtypes = [vp, vp, i32, vp, vp, vp, vp, i32, f32, vp, vp]
+        L.anchorkv_decode_step.argtypes = [vp, vp, sz, i32, vp, vp, sz, vp, sz, vp, sz, i32, f32, vp, sz, vp]
         L.anchorkv_reconstruct.restype = i32
-        L.anchorkv_reconstruct.argtypes = [vp, vp, i32, i32, i32, vp, vp]
+        L.anchorkv_reconstruct.argtypes = [vp, vp, sz, i32, i32, i32, vp, sz, vp]
         L.anchorkv_export.restype = i32
-        L.anchorkv_export.argtypes = [vp, vp, i32, i32, ctypes.POINTER(ExportArrays)]
+        L.anchorkv_export.argtypes = [vp, vp, sz, i32, i32, ctypes.POINTER(ExportArrays)]
         L.anchorkv_profile_enable.restype = i32
         L.anchorkv_profile_enable.argtypes = [ctypes.c_char_p, i32]
         L.anchorkv_profile_read.restype = i32
@@ -118,6 +119,32 @@ def _ptr(t) -> Optional[int]:
     if t is None:
         return None
     return t.data_ptr()
+
+
+def _nbytes(t) -> int:
+    return 0 if t is None else t.numel() * t.element_size()
+
+
+def _dev(t, what, dtype=None, shape=None):
+    """Checks that a tensor handed to a device entry point lives on the GPU,
+    is contiguous and, when given, has the dtype and shape the plan implies
+    (the library also checks the byte sizes)."""
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError(f"{what} must be a GPU tensor (got {t.device})")
+    if not t.is_contiguous():
+        raise ValueError(f"{what} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{what} must be {dtype} (got {t.dtype})")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{what} must have shape {tuple(shape)} (got {tuple(t.shape)})")
+    return t
+
+
+def _tdtype(code):
+    import torch
+    return torch.float32 if code == F32 else torch.bfloat16
 
 
 def _stream(stream) -> Optional[int]:
@@ -173,17 +200,41 @@ def _packed(x):
 
 
 def encode(plan: Plan, K, V, Qobs, cache, workspace, anchor_override=None, stream=None):
+    import torch
     K, V, Qobs = _packed(K), _packed(V), _packed(Qobs)
     ov = None if anchor_override is None else _packed(anchor_override)
-    check(lib().anchorkv_encode(plan.handle, _ptr(K), _ptr(V), _ptr(Qobs), _ptr(ov), _ptr(cache), _ptr(workspace),
+    dt = _tdtype(plan.cfg.dtype)
+    for t, n in ((K, "K"), (V, "V"), (Qobs, "Q_obs")):
+        _dev(t, n, dt)
+    _dev(ov, "anchor_override", torch.int32)
+    _dev(cache, "cache", torch.uint8)
+    _dev(workspace, "workspace", torch.uint8)
+    if _nbytes(K) != _nbytes(V):
+        raise ValueError("K and V must have the same size")
+    check(lib().anchorkv_encode(plan.handle, _ptr(K), _ptr(V), _nbytes(K), _ptr(Qobs), _nbytes(Qobs), _ptr(ov),
+                                _nbytes(ov), _ptr(cache), _nbytes(cache), _ptr(workspace), _nbytes(workspace),
                                 _stream(stream)))
     return K, V, Qobs, ov  # keep packed copies alive until the stream has consumed them
 
 
+def _new_shape(plan):
+    return (len(plan.seq_lens), plan.cfg.num_kv_heads, plan.cfg.head_dim)
+
+
+def _q_shape(plan):
+    return (len(plan.seq_lens), plan.cfg.num_q_heads, plan.cfg.head_dim)
+
+
 def append(plan: Plan, cache, n_appended: int, k_new, v_new, workspace, stream=None):
+    import torch
     k_new, v_new = k_new.contiguous(), v_new.contiguous()
-    check(lib().anchorkv_append(plan.handle, _ptr(cache), n_appended, _ptr(k_new), _ptr(v_new), _ptr(workspace),
-                                _stream(stream)))
+    dt = _tdtype(plan.cfg.dtype)
+    _dev(k_new, "k_new", dt, _new_shape(plan))
+    _dev(v_new, "v_new", dt, _new_shape(plan))
+    _dev(cache, "cache", torch.uint8)
+    _dev(workspace, "workspace", torch.uint8)
+    check(lib().anchorkv_append(plan.handle, _ptr(cache), _nbytes(cache), n_appended, _ptr(k_new), _ptr(v_new),
+                                _nbytes(k_new), _ptr(workspace), _nbytes(workspace), _stream(stream)))
     return k_new, v_new
 
 
@@ -193,8 +244,16 @@ def decode_step(plan: Plan, cache, n_appended: int, k_new, v_new, q, out, worksp
     k_new, v_new, q = k_new.contiguous(), v_new.contiguous(), q.contiguous()
     if out_dtype is None:
         out_dtype = F32 if out.dtype == torch.float32 else BF16
-    check(lib().anchorkv_decode_step(plan.handle, _ptr(cache), n_appended, _ptr(k_new), _ptr(v_new), _ptr(q),
-                                     _ptr(out), out_dtype, softmax_scale, _ptr(workspace), _stream(stream)))
+    dt = _tdtype(plan.cfg.dtype)
+    _dev(k_new, "k_new", dt, _new_shape(plan))
+    _dev(v_new, "v_new", dt, _new_shape(plan))
+    _dev(q, "q", dt, _q_shape(plan))
+    _dev(out, "out", _tdtype(out_dtype), _q_shape(plan))
+    _dev(cache, "cache", torch.uint8)
+    _dev(workspace, "workspace", torch.uint8)
+    check(lib().anchorkv_decode_step(plan.handle, _ptr(cache), _nbytes(cache), n_appended, _ptr(k_new), _ptr(v_new),
+                                     _nbytes(k_new), _ptr(q), _nbytes(q), _ptr(out), _nbytes(out), out_dtype,
+                                     softmax_scale, _ptr(workspace), _nbytes(workspace), _stream(stream)))
     return out
 
 
@@ -204,8 +263,13 @@ def decode_attn(plan: Plan, cache, q, out, workspace, n_appended: int = 0, out_d
     q = q.contiguous()
     if out_dtype is None:
         out_dtype = F32 if out.dtype == torch.float32 else BF16
-    check(lib().anchorkv_decode_attn(plan.handle, _ptr(cache), n_appended, _ptr(q), _ptr(out), out_dtype,
-                                     softmax_scale, _ptr(workspace), _stream(stream)))
+    _dev(q, "q", _tdtype(plan.cfg.dtype), _q_shape(plan))
+    _dev(out, "out", _tdtype(out_dtype), _q_shape(plan))
+    _dev(cache, "cache", torch.uint8)
+    _dev(workspace, "workspace", torch.uint8)
+    check(lib().anchorkv_decode_attn(plan.handle, _ptr(cache), _nbytes(cache), n_appended, _ptr(q), _nbytes(q),
+                                     _ptr(out), _nbytes(out), out_dtype, softmax_scale, _ptr(workspace),
+                                     _nbytes(workspace), _stream(stream)))
     return out
 
 
@@ -215,7 +279,10 @@ def reconstruct(plan: Plan, cache, request: int, side: int, n_appended: int = 0,
     rows = plan.seq_lens[request] + n_appended
     if out is None:
         out = torch.empty(H, rows, D, dtype=torch.float32, device=cache.device)
-    check(lib().anchorkv_reconstruct(plan.handle, _ptr(cache), n_appended, request, side, _ptr(out), _stream(stream)))
+    _dev(out, "out", torch.float32, (H, rows, D))
+    _dev(cache, "cache", torch.uint8)
+    check(lib().anchorkv_reconstruct(plan.handle, _ptr(cache), _nbytes(cache), n_appended, request, side, _ptr(out),
+                                     _nbytes(out), _stream(stream)))
     return out
 
 
@@ -256,7 +323,7 @@ def export(plan: Plan, cache_host: np.ndarray, request: int, n_appended: int = 0
         stats=np.zeros(6, np.int64))
     ea = ExportArrays(*[out[n].ctypes.data for n, _ in ExportArrays._fields_])
     host = np.ascontiguousarray(cache_host, dtype=np.uint8)
-    check(lib().anchorkv_export(plan.handle, host.ctypes.data, request, n_appended, ctypes.byref(ea)))
+    check(lib().anchorkv_export(plan.handle, host.ctypes.data, host.nbytes, request, n_appended, ctypes.byref(ea)))
     for n in ("tail_a_k", "tail_gamma_k", "tail_a_v", "tail_gamma_v"):
         out[n] = out[n][:, :n_appended]
     return out

@@ -563,10 +563,15 @@ __device__ inline int wg_reserve(int cnt, int32_t* count, int* tmp) {
 // between launches.
 bool prof_events(const char* kernel, hipEvent_t* start, hipEvent_t* stop);
 
+// Fault injection of the error path: true when this launch (and every later
+// one of the same entry-point call) must be skipped.
+bool launch_blocked(const char* kernel);
+
 // Launches kernel<<<grid, block, lds, st>>>(args...), timed when profiled.
 template <typename... KArgs, typename... Args>
 inline void launch(const char* name, void (*kernel)(KArgs...), dim3 grid, dim3 block, uint32_t lds, hipStream_t st,
                    Args... args) {
+  if (launch_blocked(name)) return;
   hipEvent_t e0 = nullptr, e1 = nullptr;
   if (prof_events(name, &e0, &e1))
     hipExtLaunchKernelGGL(kernel, grid, block, lds, st, e0, e1, 0, static_cast<KArgs>(args)...);

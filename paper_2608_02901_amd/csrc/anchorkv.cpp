@@ -3,6 +3,7 @@
 // the batch's sequence lengths), launch sequencing on the caller's stream,
 // error mapping, and the host-side export of a cache blob.
 #include <math.h>
+#include <stdlib.h>
 #include <string.h>
 
 #include <algorithm>
@@ -44,6 +45,45 @@ static thread_local std::string g_last_error;
 static anchorkv_status fail(anchorkv_status s, const std::string& msg) {
   g_last_error = msg;
   return s;
+}
+
+// ------------------------------------------------------------------ fault injection
+// ANCHORKV_FAULT_INJECT=<kernel>: a device entry point that reaches that
+// kernel launches nothing from it on and returns ANCHORKV_ERR_HIP.  The state
+// is per thread and per call (FaultScope).
+namespace {
+thread_local std::string g_fi_target, g_fi_kernel;
+thread_local bool g_fi_tripped = false;
+struct FaultScope {
+  FaultScope() {
+    const char* e = getenv("ANCHORKV_FAULT_INJECT");
+    g_fi_target = e ? e : "";
+    g_fi_tripped = false;
+  }
+  ~FaultScope() { g_fi_target.clear(); }
+  anchorkv_status finish(anchorkv_status s) const {
+    if (s == ANCHORKV_OK && g_fi_tripped)
+      return fail(ANCHORKV_ERR_HIP, "fault injected at kernel " + g_fi_kernel + " (ANCHORKV_FAULT_INJECT)");
+    return s;
+  }
+};
+}  // namespace
+
+bool akv::launch_blocked(const char* kernel) {
+  if (g_fi_tripped) return true;
+  if (!g_fi_target.empty() && g_fi_target == kernel) {
+    g_fi_tripped = true;
+    g_fi_kernel = kernel;
+    return true;
+  }
+  return false;
+}
+
+static anchorkv_status need_bytes(size_t have, size_t want, const char* what) {
+  if (have < want)
+    return fail(ANCHORKV_ERR_BUFFER_TOO_SMALL,
+                std::string(what) + ": " + std::to_string(have) + " bytes, the plan needs " + std::to_string(want));
+  return ANCHORKV_OK;
 }
 
 struct Layout {
@@ -210,6 +250,16 @@ extern "C" anchorkv_status anchorkv_plan_create(const anchorkv_config* cfg, int3
   if (totS * H >= (1ll << 30)) {
     delete p;
     return fail(ANCHORKV_ERR_UNSUPPORTED, "total tokens x heads above 2^30");
+  }
+  // Every prefix sum below must fit the int32 offsets the kernels use.
+  {
+    int64_t kt = 0;
+    for (int b = 0; b < batch; ++b)
+      kt += (int64_t)H * geo.k[b] * ((geo.S[b] + akv::SORT_CHUNK - 1) / akv::SORT_CHUNK + 1);
+    if (kt >= (1ll << 31) - 1) {
+      delete p;
+      return fail(ANCHORKV_ERR_UNSUPPORTED, "anchors x heads x sort chunks above 2^31");
+    }
   }
   for (int b = 0; b < batch; ++b) {
     const int S = geo.S[b], k = geo.k[b];
@@ -455,20 +505,42 @@ static akv::DecWs dws_ptrs(const anchorkv_plan* p, void* base) {
 }
 
 static anchorkv_status hip_status(hipError_t e, const char* what) {
+  if (g_fi_tripped)  // an injected fault: nothing was launched from that kernel on
+    return fail(ANCHORKV_ERR_HIP, "fault injected at kernel " + g_fi_kernel + " (ANCHORKV_FAULT_INJECT)");
   if (e == hipSuccess) return ANCHORKV_OK;
   return fail(ANCHORKV_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
 }
 
-extern "C" anchorkv_status anchorkv_encode(const anchorkv_plan* p, const void* K, const void* V, const void* Q_obs,
-                                           const int32_t* anchor_pos_override, void* cache, void* workspace,
-                                           void* stream) {
+// Bytes the plan needs for each caller buffer.
+static size_t kv_need(const anchorkv_plan* p) { return (size_t)p->geo.prefS[p->geo.B] * p->geo.H * p->geo.D * p->geo.esz; }
+static size_t qobs_need(const anchorkv_plan* p) {
+  return (size_t)p->geo.B * p->geo.Hq * p->geo.W * p->geo.D * p->geo.esz;
+}
+static size_t override_need(const anchorkv_plan* p) { return 4 * (size_t)p->geo.prefK[p->geo.B] * p->geo.H; }
+static size_t new_need(const anchorkv_plan* p) { return (size_t)p->geo.B * p->geo.H * p->geo.D * p->geo.esz; }
+static size_t q_need(const anchorkv_plan* p) { return (size_t)p->geo.B * p->geo.Hq * p->geo.D * p->geo.esz; }
+static size_t out_need(const anchorkv_plan* p, int out_dtype) {
+  return (size_t)p->geo.B * p->geo.Hq * p->geo.D * (out_dtype == ANCHORKV_F32 ? 4 : 2);
+}
+
+extern "C" anchorkv_status anchorkv_encode(const anchorkv_plan* p, const void* K, const void* V, size_t kv_bytes,
+                                           const void* Q_obs, size_t q_obs_bytes, const int32_t* anchor_pos_override,
+                                           size_t override_bytes, void* cache, size_t cache_bytes, void* workspace,
+                                           size_t workspace_bytes, void* stream) {
   if (!p || !K || !V || !Q_obs || !cache || !workspace) return fail(ANCHORKV_ERR_INVALID_ARG, "null argument");
+  anchorkv_status s;
+  if ((s = need_bytes(kv_bytes, kv_need(p), "K / V")) != ANCHORKV_OK) return s;
+  if ((s = need_bytes(q_obs_bytes, qobs_need(p), "Q_obs")) != ANCHORKV_OK) return s;
+  if (anchor_pos_override && (s = need_bytes(override_bytes, override_need(p), "anchor override")) != ANCHORKV_OK)
+    return s;
+  if ((s = need_bytes(cache_bytes, p->cache_bytes, "cache")) != ANCHORKV_OK) return s;
+  if ((s = need_bytes(workspace_bytes, p->ws_bytes, "encode workspace")) != ANCHORKV_OK) return s;
+  const FaultScope fs;
   const hipStream_t st = (hipStream_t)stream;
   const akv::Cache c = cache_ptrs(p, cache);
   const akv::Ws w = ws_ptrs(p, workspace);
   const Geo& g = p->geo;
   (void)hipGetLastError();
-  anchorkv_status s;
   if ((s = hip_status(akv::launch_init(g, c, w, st), "init")) != ANCHORKV_OK) return s;
   if ((s = hip_status(akv::launch_obs64(g, w, K, V, Q_obs, st), "fp64 observation pass")) != ANCHORKV_OK) return s;
   if ((s = hip_status(akv::launch_obs(g, w, K, Q_obs, st), "observation pass")) != ANCHORKV_OK) return s;
@@ -479,61 +551,89 @@ extern "C" anchorkv_status anchorkv_encode(const anchorkv_plan* p, const void* K
   if ((s = hip_status(akv::launch_epilogue(g, w, c, K, V, Q_obs, st), "utilities")) != ANCHORKV_OK) return s;
   if ((s = hip_status(akv::launch_budget(g, w, c, K, V, Q_obs, st), "budget")) != ANCHORKV_OK) return s;
   if ((s = hip_status(akv::launch_layout(g, w, c, K, V, st), "layout")) != ANCHORKV_OK) return s;
-  return ANCHORKV_OK;
+  return fs.finish(ANCHORKV_OK);
 }
 
-extern "C" anchorkv_status anchorkv_append(const anchorkv_plan* p, void* cache, int32_t n_appended, const void* k_new,
-                                           const void* v_new, void* workspace, void* stream) {
+extern "C" anchorkv_status anchorkv_append(const anchorkv_plan* p, void* cache, size_t cache_bytes, int32_t n_appended,
+                                           const void* k_new, const void* v_new, size_t new_bytes, void* workspace,
+                                           size_t workspace_bytes, void* stream) {
   if (!p || !cache || !k_new || !v_new || !workspace) return fail(ANCHORKV_ERR_INVALID_ARG, "null argument");
   if (n_appended < 0) return fail(ANCHORKV_ERR_INVALID_ARG, "n_appended must be >= 0");
   if (n_appended >= p->cfg.max_append) return fail(ANCHORKV_ERR_CAPACITY, "append capacity exhausted");
+  anchorkv_status s;
+  if ((s = need_bytes(cache_bytes, p->cache_bytes, "cache")) != ANCHORKV_OK) return s;
+  if ((s = need_bytes(new_bytes, new_need(p), "k_new / v_new")) != ANCHORKV_OK) return s;
+  if ((s = need_bytes(workspace_bytes, p->dws_bytes, "decode workspace")) != ANCHORKV_OK) return s;
+  const FaultScope fs;
   (void)hipGetLastError();
-  return hip_status(akv::launch_decode(p->geo, cache_ptrs(p, cache), dws_ptrs(p, workspace), nullptr, k_new, v_new,
-                                       nullptr, 0, 0.0f, n_appended, (hipStream_t)stream),
-                    "append");
+  return fs.finish(hip_status(akv::launch_decode(p->geo, cache_ptrs(p, cache), dws_ptrs(p, workspace), nullptr, k_new,
+                                                 v_new, nullptr, 0, 0.0f, n_appended, (hipStream_t)stream),
+                              "append"));
 }
 
-extern "C" anchorkv_status anchorkv_decode_attn(const anchorkv_plan* p, const void* cache, int32_t n_appended,
-                                                const void* q, void* out, int32_t out_dtype, float softmax_scale,
-                                                void* workspace, void* stream) {
+extern "C" anchorkv_status anchorkv_decode_attn(const anchorkv_plan* p, const void* cache, size_t cache_bytes,
+                                                int32_t n_appended, const void* q, size_t q_bytes, void* out,
+                                                size_t out_bytes, int32_t out_dtype, float softmax_scale,
+                                                void* workspace, size_t workspace_bytes, void* stream) {
   if (!p || !cache || !q || !out || !workspace) return fail(ANCHORKV_ERR_INVALID_ARG, "null argument");
   if (n_appended < 0 || n_appended > p->cfg.max_append)
     return fail(ANCHORKV_ERR_INVALID_ARG, "n_appended must be in [0, max_append]");
   if (out_dtype != ANCHORKV_F32 && out_dtype != ANCHORKV_BF16) return fail(ANCHORKV_ERR_INVALID_ARG, "bad out_dtype");
+  anchorkv_status s;
+  if ((s = need_bytes(cache_bytes, p->cache_bytes, "cache")) != ANCHORKV_OK) return s;
+  if ((s = need_bytes(q_bytes, q_need(p), "q")) != ANCHORKV_OK) return s;
+  if ((s = need_bytes(out_bytes, out_need(p, out_dtype), "out")) != ANCHORKV_OK) return s;
+  if ((s = need_bytes(workspace_bytes, p->dws_bytes, "decode workspace")) != ANCHORKV_OK) return s;
   const float scale = softmax_scale > 0.0f ? softmax_scale : 1.0f / sqrtf((float)p->geo.D);
+  const FaultScope fs;
   (void)hipGetLastError();
-  return hip_status(akv::launch_decode(p->geo, cache_ptrs(p, (void*)cache), dws_ptrs(p, workspace), q, nullptr,
-                                       nullptr, out, out_dtype, scale, n_appended, (hipStream_t)stream),
-                    "decode");
+  return fs.finish(hip_status(akv::launch_decode(p->geo, cache_ptrs(p, (void*)cache), dws_ptrs(p, workspace), q,
+                                                 nullptr, nullptr, out, out_dtype, scale, n_appended,
+                                                 (hipStream_t)stream),
+                              "decode"));
 }
 
-extern "C" anchorkv_status anchorkv_decode_step(const anchorkv_plan* p, void* cache, int32_t n_appended,
-                                                const void* k_new, const void* v_new, const void* q, void* out,
-                                                int32_t out_dtype, float softmax_scale, void* workspace,
-                                                void* stream) {
+extern "C" anchorkv_status anchorkv_decode_step(const anchorkv_plan* p, void* cache, size_t cache_bytes,
+                                                int32_t n_appended, const void* k_new, const void* v_new,
+                                                size_t new_bytes, const void* q, size_t q_bytes, void* out,
+                                                size_t out_bytes, int32_t out_dtype, float softmax_scale,
+                                                void* workspace, size_t workspace_bytes, void* stream) {
   if (!p || !cache || !k_new || !v_new || !q || !out || !workspace)
     return fail(ANCHORKV_ERR_INVALID_ARG, "null argument");
   if (n_appended < 0) return fail(ANCHORKV_ERR_INVALID_ARG, "n_appended must be >= 0");
   if (n_appended >= p->cfg.max_append) return fail(ANCHORKV_ERR_CAPACITY, "append capacity exhausted");
   if (out_dtype != ANCHORKV_F32 && out_dtype != ANCHORKV_BF16) return fail(ANCHORKV_ERR_INVALID_ARG, "bad out_dtype");
+  anchorkv_status s;
+  if ((s = need_bytes(cache_bytes, p->cache_bytes, "cache")) != ANCHORKV_OK) return s;
+  if ((s = need_bytes(new_bytes, new_need(p), "k_new / v_new")) != ANCHORKV_OK) return s;
+  if ((s = need_bytes(q_bytes, q_need(p), "q")) != ANCHORKV_OK) return s;
+  if ((s = need_bytes(out_bytes, out_need(p, out_dtype), "out")) != ANCHORKV_OK) return s;
+  if ((s = need_bytes(workspace_bytes, p->dws_bytes, "decode workspace")) != ANCHORKV_OK) return s;
   const float scale = softmax_scale > 0.0f ? softmax_scale : 1.0f / sqrtf((float)p->geo.D);
+  const FaultScope fs;
   (void)hipGetLastError();
-  return hip_status(akv::launch_decode(p->geo, cache_ptrs(p, cache), dws_ptrs(p, workspace), q, k_new, v_new, out,
-                                       out_dtype, scale, n_appended, (hipStream_t)stream),
-                    "decode step");
+  return fs.finish(hip_status(akv::launch_decode(p->geo, cache_ptrs(p, cache), dws_ptrs(p, workspace), q, k_new,
+                                                 v_new, out, out_dtype, scale, n_appended, (hipStream_t)stream),
+                              "decode step"));
 }
 
-extern "C" anchorkv_status anchorkv_reconstruct(const anchorkv_plan* p, const void* cache, int32_t n_appended,
-                                                int32_t request, int32_t side, float* out, void* stream) {
+extern "C" anchorkv_status anchorkv_reconstruct(const anchorkv_plan* p, const void* cache, size_t cache_bytes,
+                                                int32_t n_appended, int32_t request, int32_t side, float* out,
+                                                size_t out_bytes, void* stream) {
   if (!p || !cache || !out) return fail(ANCHORKV_ERR_INVALID_ARG, "null argument");
   if (request < 0 || request >= p->geo.B) return fail(ANCHORKV_ERR_INVALID_ARG, "request out of range");
   if (side != 0 && side != 1) return fail(ANCHORKV_ERR_INVALID_ARG, "side must be 0 (keys) or 1 (values)");
   if (n_appended < 0 || n_appended > p->cfg.max_append)
     return fail(ANCHORKV_ERR_INVALID_ARG, "n_appended must be in [0, max_append]");
+  anchorkv_status s;
+  if ((s = need_bytes(cache_bytes, p->cache_bytes, "cache")) != ANCHORKV_OK) return s;
+  const size_t want = (size_t)p->geo.H * (p->geo.S[request] + n_appended) * p->geo.D * 4;
+  if ((s = need_bytes(out_bytes, want, "out")) != ANCHORKV_OK) return s;
+  const FaultScope fs;
   (void)hipGetLastError();
-  return hip_status(
+  return fs.finish(hip_status(
       akv::launch_reconstruct(p->geo, cache_ptrs(p, (void*)cache), request, side, n_appended, out, (hipStream_t)stream),
-      "reconstruct");
+      "reconstruct"));
 }
 
 static float coef_host(const void* base, size_t i, int dtype) {
@@ -541,9 +641,13 @@ static float coef_host(const void* base, size_t i, int dtype) {
   return ((const float*)base)[i];
 }
 
-extern "C" anchorkv_status anchorkv_export(const anchorkv_plan* p, const void* cache_host, int32_t b,
-                                           int32_t n_appended, anchorkv_export_arrays* o) {
+extern "C" anchorkv_status anchorkv_export(const anchorkv_plan* p, const void* cache_host, size_t cache_bytes,
+                                           int32_t b, int32_t n_appended, anchorkv_export_arrays* o) {
   if (!p || !cache_host || !o) return fail(ANCHORKV_ERR_INVALID_ARG, "null argument");
+  {
+    const anchorkv_status s = need_bytes(cache_bytes, p->cache_bytes, "cache");
+    if (s != ANCHORKV_OK) return s;
+  }
   if (b < 0 || b >= p->geo.B) return fail(ANCHORKV_ERR_INVALID_ARG, "request out of range");
   if (n_appended < 0 || n_appended > p->cfg.max_append)
     return fail(ANCHORKV_ERR_INVALID_ARG, "n_appended must be in [0, max_append]");
@@ -621,6 +725,7 @@ extern "C" const char* anchorkv_status_string(anchorkv_status s) {
     case ANCHORKV_ERR_CAPACITY: return "append capacity exhausted";
     case ANCHORKV_ERR_CORRUPT_CACHE: return "corrupt cache";
     case ANCHORKV_ERR_HIP: return "HIP runtime error";
+    case ANCHORKV_ERR_BUFFER_TOO_SMALL: return "buffer too small";
   }
   return "unknown status";
 }

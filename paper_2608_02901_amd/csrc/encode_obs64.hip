@@ -237,35 +237,46 @@ __global__ __launch_bounds__(256) void k_obs64_reduce(Geo g, Ws w, const void* Q
   const int lane = tid & 63;
   const size_t bhm = (size_t)bh * m;
   double sq = 0.0;
+  // the thread's 8 outputs (2 column groups x 4 register slots), chunks added
+  // in order, 8 chunks x 8 outputs loaded per round
+  double acc[8];
+  const double* op[8];
 #pragma unroll
-  for (int e = 0; e < 2; ++e) {
-    const int blk = 2 * (tid >> 6) + e;
+  for (int q = 0; q < 8; ++q) {
+    const int blk = 2 * (tid >> 6) + (q >> 2), r = q & 3;
+    op[q] = w.o64O + (gc0 * nrb + rb16) * 2048 + (blk * 4 + r) * 64 + lane;
+    acc[q] = 0.0;
+  }
+  const size_t cstride = (size_t)nrb * 2048;
+  for (int c0 = 0; c0 < nch; c0 += 8) {
+    double v[8][8];
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const double* op = w.o64O + (gc0 * nrb + rb16) * 2048 + (blk * 4 + r) * 64 + lane;
-      // chunks added in order, their partial outputs loaded 8 at a time
-      double acc = 0.0;
-      for (int c0 = 0; c0 < nch; c0 += 8) {
-        double v[8];
+    for (int u = 0; u < 8; ++u)
 #pragma unroll
-        for (int u = 0; u < 8; ++u) v[u] = c0 + u < nch ? op[(size_t)(c0 + u) * nrb * 2048] : 0.0;
+      for (int q = 0; q < 8; ++q) v[u][q] = c0 + u < nch ? op[q][(size_t)(c0 + u) * cstride] : 0.0;
 #pragma unroll
-        for (int u = 0; u < 8; ++u)
-          if (c0 + u < nch) acc += v[u] * scl[c0 + u][r16];
+    for (int u = 0; u < 8; ++u)
+      if (c0 + u < nch) {
+        const double sc = scl[c0 + u][r16];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) acc[q] += v[u][q] * sc;
       }
-      const double y = acc / Zsh[r16];
-      const int dim = 8 * ((lane >> 4) + 4 * r) + blk;
-      if (rok) {
-        const size_t o = (bhm + row) * D + dim;
-        w.Y64[o] = y;
-        const float y32 = (float)y;
-        w.Y[o] = y32;
-        const uint16_t hi = f2bf(y32);
-        w.Yhi[o] = hi;
-        w.Ylo[o] = f2bf(y32 - bf2f(hi));
-      }
-      sq += y * y;
+  }
+#pragma unroll
+  for (int q = 0; q < 8; ++q) {
+    const int blk = 2 * (tid >> 6) + (q >> 2), r = q & 3;
+    const double y = acc[q] / Zsh[r16];
+    const int dim = 8 * ((lane >> 4) + 4 * r) + blk;
+    if (rok) {
+      const size_t o = (bhm + row) * D + dim;
+      w.Y64[o] = y;
+      const float y32 = (float)y;
+      w.Y[o] = y32;
+      const uint16_t hi = f2bf(y32);
+      w.Yhi[o] = hi;
+      w.Ylo[o] = f2bf(y32 - bf2f(hi));
     }
+    sq += y * y;
   }
   __syncthreads();
   red[part][r16] = sq;

@@ -226,3 +226,23 @@ def test_budget_cut_inside_exact_utility_ties():
     assert sel[299:329].all() and not sel[329:360].any()
     exp = akv.export(plan, cache.cpu().numpy(), 0, 0)
     assert_request_parity(exp, enc, cfg)
+
+
+def test_fault_injection_mid_encode_then_recovery(monkeypatch):
+    """Error path forced from the host: with ANCHORKV_FAULT_INJECT=k_assign the
+    encode stops before the assignment kernel (nothing after it is enqueued)
+    and returns ANCHORKV_ERR_HIP; the next call without injection encodes the
+    same inputs into the same cache as a clean run."""
+    wl = _wl("fault_inject")
+    print("[edge] fault injection mid-encode", flush=True)
+    layer = synth.make_layer(wl)
+    cfg = make_cfg(wl)
+    plan = N.Plan(cfg, wl.seq_lens)
+    ref, _, _ = gpu_encode(plan, layer)
+    monkeypatch.setenv("ANCHORKV_FAULT_INJECT", "k_assign")
+    with pytest.raises(N.AnchorKVError) as e:
+        gpu_encode(plan, layer)
+    assert e.value.status == N.ERR_HIP and "k_assign" in str(e.value)
+    monkeypatch.delenv("ANCHORKV_FAULT_INJECT")
+    again, _, _ = gpu_encode(plan, layer)
+    assert torch.equal(ref, again)

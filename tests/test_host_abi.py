@@ -118,21 +118,107 @@ def test_buffer_sizes_grow_with_batch():
     assert p1.cache_bytes < 8 * 8192 * 128 * 2 * 2 / 5  # well under the dense layer
 
 
+def _sizes(p):
+    """Bytes the plan needs for each device buffer of the 4096-token 8B plan."""
+    esz = 2
+    H, Hq, D, W = 8, 32, 128, 32
+    S = sum(p.seq_lens)
+    B = len(p.seq_lens)
+    return dict(kv=H * S * D * esz, qobs=B * Hq * W * D * esz, new=B * H * D * esz, q=B * Hq * D * esz,
+                out32=B * Hq * D * 4, cache=p.cache_bytes, ws=p.encode_ws_bytes, dws=p.decode_ws_bytes)
+
+
 def test_entry_points_validate_before_touching_the_gpu():
     L = _lib_or_skip()
     p = N.Plan(_cfg(max_append=4), [4096])
-    assert L.anchorkv_encode(p.handle, None, None, None, None, None, None, None) == N.ERR_INVALID_ARG
-    assert L.anchorkv_append(p.handle, 1, 4, 1, 1, 1, None) == N.ERR_CAPACITY
-    assert L.anchorkv_append(p.handle, 1, -1, 1, 1, 1, None) == N.ERR_INVALID_ARG
-    assert L.anchorkv_append(p.handle, 1, 0, 1, 1, None, None) == N.ERR_INVALID_ARG
-    assert L.anchorkv_decode_step(p.handle, 1, 4, 1, 1, 1, 1, 0, 0.0, 1, None) == N.ERR_CAPACITY
-    assert L.anchorkv_decode_step(p.handle, 1, 0, 1, 1, 1, 1, 7, 0.0, 1, None) == N.ERR_INVALID_ARG
-    assert L.anchorkv_decode_step(p.handle, 1, 0, 1, 1, None, 1, 0, 0.0, 1, None) == N.ERR_INVALID_ARG
-    assert L.anchorkv_decode_attn(p.handle, 1, 5, 1, 1, 0, 0.0, 1, None) == N.ERR_INVALID_ARG
-    assert L.anchorkv_decode_attn(p.handle, 1, 0, 1, 1, 9, 0.0, 1, None) == N.ERR_INVALID_ARG
-    assert L.anchorkv_reconstruct(p.handle, 1, 0, 3, 0, 1, None) == N.ERR_INVALID_ARG
-    assert L.anchorkv_reconstruct(p.handle, 1, 0, 0, 2, 1, None) == N.ERR_INVALID_ARG
+    z = _sizes(p)
+    assert L.anchorkv_encode(p.handle, None, None, 0, None, 0, None, 0, None, 0, None, 0, None) == N.ERR_INVALID_ARG
+    assert L.anchorkv_append(p.handle, 1, z["cache"], 4, 1, 1, z["new"], 1, z["dws"], None) == N.ERR_CAPACITY
+    assert L.anchorkv_append(p.handle, 1, z["cache"], -1, 1, 1, z["new"], 1, z["dws"], None) == N.ERR_INVALID_ARG
+    assert L.anchorkv_append(p.handle, 1, z["cache"], 0, 1, 1, z["new"], None, z["dws"], None) == N.ERR_INVALID_ARG
+    step = lambda n, od, ws: L.anchorkv_decode_step(p.handle, 1, z["cache"], n, 1, 1, z["new"], 1, z["q"], 1,
+                                                   z["out32"], od, 0.0, ws, z["dws"], None)
+    assert step(4, 0, 1) == N.ERR_CAPACITY
+    assert step(0, 7, 1) == N.ERR_INVALID_ARG
+    assert step(0, 0, None) == N.ERR_INVALID_ARG
+    attn = lambda n, od: L.anchorkv_decode_attn(p.handle, 1, z["cache"], n, 1, z["q"], 1, z["out32"], od, 0.0, 1,
+                                               z["dws"], None)
+    assert attn(5, 0) == N.ERR_INVALID_ARG
+    assert attn(0, 9) == N.ERR_INVALID_ARG
+    rec_bytes = 8 * 4096 * 128 * 4
+    assert L.anchorkv_reconstruct(p.handle, 1, z["cache"], 0, 3, 0, 1, rec_bytes, None) == N.ERR_INVALID_ARG
+    assert L.anchorkv_reconstruct(p.handle, 1, z["cache"], 0, 0, 2, 1, rec_bytes, None) == N.ERR_INVALID_ARG
     assert L.anchorkv_status_string(N.ERR_HIP).decode() == "HIP runtime error"
+    assert L.anchorkv_status_string(N.ERR_BUFFER_TOO_SMALL).decode() == "buffer too small"
+
+
+def test_undersized_buffers_are_rejected_before_any_launch():
+    """Each device buffer one byte short of what the plan needs returns
+    ANCHORKV_ERR_BUFFER_TOO_SMALL and names the buffer (no GPU is touched:
+    the checks come before anything is enqueued)."""
+    L = _lib_or_skip()
+    p = N.Plan(_cfg(max_append=4), [4096])
+    z = _sizes(p)
+
+    def enc(**kw):
+        a = dict(kv=z["kv"], qobs=z["qobs"], ov=0, cache=z["cache"], ws=z["ws"], ovp=None)
+        a.update(kw)
+        return L.anchorkv_encode(p.handle, 1, 1, a["kv"], 1, a["qobs"], a["ovp"], a["ov"], 1, a["cache"], 1, a["ws"],
+                                 None)
+
+    cases = [
+        (lambda: enc(kv=z["kv"] - 1), "K / V"),
+        (lambda: enc(qobs=z["qobs"] - 1), "Q_obs"),
+        (lambda: enc(ovp=1, ov=4 * 8 * p.requests[0].anchors - 1), "anchor override"),
+        (lambda: enc(cache=z["cache"] - 1), "cache"),
+        (lambda: enc(ws=z["ws"] - 1), "encode workspace"),
+        (lambda: L.anchorkv_append(p.handle, 1, z["cache"], 0, 1, 1, z["new"] - 1, 1, z["dws"], None),
+         "k_new / v_new"),
+        (lambda: L.anchorkv_append(p.handle, 1, z["cache"], 0, 1, 1, z["new"], 1, z["dws"] - 1, None),
+         "decode workspace"),
+        (lambda: L.anchorkv_decode_attn(p.handle, 1, z["cache"] - 1, 0, 1, z["q"], 1, z["out32"], 0, 0.0, 1,
+                                        z["dws"], None), "cache"),
+        (lambda: L.anchorkv_decode_attn(p.handle, 1, z["cache"], 0, 1, z["q"] - 1, 1, z["out32"], 0, 0.0, 1,
+                                        z["dws"], None), "q"),
+        (lambda: L.anchorkv_decode_attn(p.handle, 1, z["cache"], 0, 1, z["q"], 1, z["out32"] - 1, 0, 0.0, 1,
+                                        z["dws"], None), "out"),
+        (lambda: L.anchorkv_decode_attn(p.handle, 1, z["cache"], 0, 1, z["q"], 1, z["out32"] // 2 - 1, 1, 0.0, 1,
+                                        z["dws"], None), "out"),
+        (lambda: L.anchorkv_decode_step(p.handle, 1, z["cache"], 0, 1, 1, z["new"], 1, z["q"], 1, z["out32"], 0,
+                                        0.0, 1, z["dws"] - 1, None), "decode workspace"),
+        (lambda: L.anchorkv_reconstruct(p.handle, 1, z["cache"], 2, 0, 0, 1, 8 * 4098 * 128 * 4 - 1, None), "out"),
+    ]
+    for call, what in cases:
+        assert call() == N.ERR_BUFFER_TOO_SMALL, what
+        assert N.last_error().startswith(what + ":"), (what, N.last_error())
+    host = np.zeros(p.cache_bytes - 1, np.uint8)
+    ea = N.ExportArrays()
+    assert L.anchorkv_export(p.handle, host.ctypes.data, host.nbytes, 0, 0, ctypes.byref(ea)) == N.ERR_BUFFER_TOO_SMALL
+
+
+def test_plan_rejects_offsets_beyond_int32():
+    """64 requests of 2^22 tokens with 16384 anchors per head: the counting
+    sort's per-chunk anchor tables would pass 2^31 entries; the plan refuses
+    it instead of wrapping its int32 offsets."""
+    _lib_or_skip()
+    cfg = _cfg(num_kv_heads=1, num_q_heads=1, anchor_count=16384, anchor_frac=0.0)
+    with pytest.raises(N.AnchorKVError) as e:
+        N.Plan(cfg, [1 << 22] * 64)
+    assert e.value.status in (N.ERR_UNSUPPORTED,)
+
+
+def test_fault_injection_stops_the_call_before_its_first_kernel(monkeypatch):
+    """ANCHORKV_FAULT_INJECT=k_init: the encode reaches its first kernel and
+    enqueues nothing from there on (the pointers here are not device memory:
+    a launch would be an error), returning ANCHORKV_ERR_HIP with the kernel
+    named; without the variable the plan's validation still passes."""
+    L = _lib_or_skip()
+    p = N.Plan(_cfg(), [4096])
+    z = _sizes(p)
+    monkeypatch.setenv("ANCHORKV_FAULT_INJECT", "k_init")
+    st = L.anchorkv_encode(p.handle, 8, 8, z["kv"], 8, z["qobs"], None, 0, 8, z["cache"], 8, z["ws"], None)
+    assert st == N.ERR_HIP
+    assert "fault injected at kernel k_init" in N.last_error()
 
 
 def test_export_rejects_a_foreign_blob():
