@@ -1,22 +1,25 @@
 """GPU parity at the full sizes of the evaluation workloads, in the launch
 configuration the benchmark uses (``decode_step``, the plan's split length).
 
-* Workloads 1 and 2 fit the oracle whole: everything is compared with the
-  oracle's full compression pass and its fp64 attention.
-* Workloads 3, 4 and 5 are too large for the oracle's assignment of every
-  token.  The oracle runs the steps it can afford on the full inputs (the
-  observation pass and the anchor selection of every head), then samples
-  tokens.  For each sampled token it computes the nearest anchor, gamma,
-  residual codes and utilities, which must match bit for bit or sit on the
-  right side of the pooled budget cut.
-* Decode at those sizes is checked by a property that holds at any size: it
-  equals fp64 softmax attention over the dense reconstruction of the same
-  cache.  That reconstruction is itself bit-exact against the oracle at the
-  sizes the oracle covers.
+* Workloads 1 and 2: the whole compression pass against the oracle's, and
+  the decode output against the oracle's fp64 attention over its own
+  reconstruction.
+* Workload 3 (the 128K layer): the same for all 8 heads, then the benchmark's
+  64 appended tokens (every tail record against the oracle's nearest anchor
+  and coefficient) and the decode outputs of steps 1 and 64 against the
+  oracle's attention over its reconstruction plus the appended tokens.
+* Workload 4 (70B shape, 8 requests): every request, encode and decode.
+* Workload 5 (16 ragged requests): the shortest, the median and the longest.
+* One 540000-token request (265 split records per query head, the merge's
+  second round): decode_step against fp64 attention over the dense
+  reconstruction of the same cache, a property that holds at any size (the
+  reconstruction is itself bit-exact against the oracle wherever compared).
+The oracle's wall time is printed with each comparison.
 """
 from __future__ import annotations
 
 import math
+import time
 
 import numpy as np
 import pytest
@@ -95,54 +98,6 @@ def test_small_workloads_whole_against_oracle(wi):
     assert err <= (1e-4 if wl.dtype == "f32" else 2e-3)
 
 
-def _sampled_request_check(cfg, lay, b, exp, ntok, rng):
-    """Oracle on the full inputs of request b for the observation pass and the
-    anchor sets, then on ntok sampled non-anchor tokens per head."""
-    K = lay.K[b].float().cpu().numpy()
-    V = lay.V[b].float().cpu().numpy()
-    Q = lay.Qobs[b].float().cpu().numpy()
-    H, S, D = K.shape
-    g = Q.shape[0] // H
-    W, k = cfg.window, plan_k(cfg, S)
-    G = cfg.quant_group or D
-    bf16 = cfg.dtype == N.BF16
-    u_sel = {"K": [], "V": []}
-    u_non = {"K": [], "V": []}
-    n_checked = 0
-    for h in range(H):
-        Qg = np.ascontiguousarray(Q[h * g:(h + 1) * g])
-        M, Z, Y = R.obs_head(K[h], V[h], Qg)
-        _, pooled = R.selector_scores(K[h], Qg, M, Z, cfg.kappa)
-        assert selection_gap_ok(pooled, R.n_top(k, W, cfg.rho), SEL_GAP), "near-tie at the selection cut"
-        anc = R.select_anchors(pooled, S, W, k, cfg.rho, cfg.seed, h)
-        np.testing.assert_array_equal(exp["anchors"][h], anc)
-        free = np.setdiff1d(np.arange(S), anc)
-        toks = np.sort(rng.choice(free, size=min(ntok, free.size), replace=False)).astype(np.int32)
-        aK, gK, rK = R.assign_tokens(K[h], anc, bf16, toks)
-        aV, gV, rV = R.assign_tokens(V[h], anc, bf16, toks)
-        np.testing.assert_array_equal(exp["a_k"][h][toks], aK)
-        np.testing.assert_array_equal(exp["a_v"][h][toks], aV)
-        np.testing.assert_array_equal(exp["gamma_k"][h][toks], gK.astype(np.float32))
-        np.testing.assert_array_equal(exp["gamma_v"][h][toks], gV.astype(np.float32))
-        uK, uV = R.utilities(K[h], V[h], Qg, M, Z, Y, toks, rK, rV)
-        for side, u, r in (("K", uK, rK), ("V", uV, rV)):
-            sel = exp["sel_" + side.lower()][h][toks].astype(bool)
-            u_sel[side].append(u[sel])
-            u_non[side].append(u[~sel])
-            for i in np.flatnonzero(sel):
-                codes, scales = R.codec_encode(r[i], G, cfg.scale_mode, cfg.seed)
-                np.testing.assert_array_equal(exp["codes_" + side.lower()][h][toks[i]], codes)
-                np.testing.assert_array_equal(exp["scales_" + side.lower()][h][toks[i]], scales)
-                n_checked += 1
-    # The pooled cut: every selected sample outranks every unselected one.
-    for side in "KV":
-        s = np.concatenate(u_sel[side])
-        n = np.concatenate(u_non[side])
-        if s.size and n.size:
-            assert s.min() >= n.max(), (side, s.min(), n.max())
-    return n_checked
-
-
 def _decode_property(plan, cache, dws, lay, b_list, steps, append):
     """decode_step / decode_attn output equals fp64 attention over the dense
     reconstruction of the same cache (tail tokens included)."""
@@ -165,11 +120,84 @@ def _decode_property(plan, cache, dws, lay, b_list, steps, append):
     return worst
 
 
-def test_workload3_128k_sampled_and_decode_steps():
+def _oracle_whole_request(cfg, lay, b, exp, tag):
+    """The oracle's full compression pass of request b; every exported stream
+    must match it bit for bit (residual sets included)."""
+    t0 = time.time()
+    print(f"[full] {tag}: oracle encode of request {b} (S={lay.K[b].shape[1]}) ...", flush=True)
+    enc = oracle_encode(cfg, _cpu_layer(lay), b)
+    print(f"[full] {tag}: oracle encode took {time.time() - t0:.1f} s on {R.num_threads()} threads; "
+          f"fixup rows {exp['stats'][:2]}, budget bands {exp['stats'][4:6]}", flush=True)
+    S = lay.K[b].shape[1]
+    n_top = R.n_top(plan_k(cfg, S), cfg.window, cfg.rho)
+    for h in range(enc["anchors"].shape[0]):
+        assert selection_gap_ok(enc["pooled"][h], n_top, SEL_GAP), "near-tie at the selection cut"
+    assert_request_parity(exp, enc, cfg)
+    return enc
+
+
+class _CpuLayer:
+    def __init__(self, lay):
+        self.K = [t.cpu() for t in lay.K]
+        self.V = [t.cpu() for t in lay.V]
+        self.Qobs = [t.cpu() for t in lay.Qobs]
+
+
+_cpu_cache = {}
+
+
+def _cpu_layer(lay):
+    key = id(lay)
+    if key not in _cpu_cache:
+        _cpu_cache.clear()
+        _cpu_cache[key] = _CpuLayer(lay)
+    return _cpu_cache[key]
+
+
+def _oracle_decode_check(cfg, lay, b, enc, q, got, tails=None, tag=""):
+    """Decode output of request b against the oracle's fp64 attention over its
+    own dense reconstruction (and the appended tokens, encoded by the oracle
+    against its anchors: fp32(gamma) * anchor, no residual)."""
+    cl = _cpu_layer(lay)
+    K = cl.K[b].float().numpy()
+    V = cl.V[b].float().numpy()
+    G = cfg.quant_group or K.shape[2]
+    Kh = R.reconstruct(K, enc, "K", G, cfg.seed)
+    Vh = R.reconstruct(V, enc, "V", G, cfg.seed)
+    if tails is not None:
+        kt, vt = tails  # [n][H][D] each
+        H = K.shape[0]
+        bf16 = cfg.dtype == N.BF16
+        addK, addV = [], []
+        for h in range(H):
+            anc = enc["anchors"][h]
+            rows = []
+            for X, new in ((K, kt), (V, vt)):
+                A = X[h][anc]
+                a, gm = R.assign_vectors(new[:, h], A, bf16=bf16)
+                rows.append(np.float32(gm)[:, None] * A[a].astype(np.float32))
+            addK.append(rows[0])
+            addV.append(rows[1])
+        Kh = np.concatenate([Kh, np.stack(addK)], axis=1)
+        Vh = np.concatenate([Vh, np.stack(addV)], axis=1)
+    ref = R.attention(Kh, Vh, q)
+    err = float(np.abs(got - ref).max())
+    print(f"[full] {tag}: decode vs oracle attention max|err| {err:.3g}", flush=True)
+    assert err <= 2e-3, err
+    return err
+
+
+def test_workload3_128k_whole_with_64_appends():
+    """The 128K layer against the oracle's whole compression pass (all 8
+    heads), then the 64 generated tokens of the benchmark: every tail record
+    against the oracle's nearest anchor and coefficient, and the decode
+    outputs of steps 1 and 64 against the oracle's attention over its own
+    reconstruction plus the appended tokens."""
     wl = synth.workload(3)
+    NS = 64
     print(f"[full] workload 3 {wl.name}", flush=True)
-    lay = _layer_on_gpu(wl, steps=4)
-    cfg = make_cfg(wl, max_append=64)
+    lay = _layer_on_gpu(wl, steps=NS)
+    cfg = make_cfg(wl, max_append=NS)
     plan = N.Plan(cfg, wl.seq_lens)
     cache, ws, dws = plan.alloc("cuda")
     keep = akv.encode(plan, lay.K[0], lay.V[0], lay.Qobs[0], cache, ws)
@@ -177,25 +205,36 @@ def test_workload3_128k_sampled_and_decode_steps():
     del keep
     assert _header_flags(cache) == 0
     exp = _export(plan, cache, 0)
-    print(f"[full] workload 3: fixup rows {exp['stats'][:2]}, budget bands {exp['stats'][4:6]}", flush=True)
-    n = _sampled_request_check(cfg, lay, 0, exp, 256, np.random.default_rng(30))
-    print(f"[full] workload 3: sampled codes checked {n}", flush=True)
-    err = _decode_property(plan, cache, dws, lay, [0], steps=4, append=True)
-    print(f"[full] workload 3: decode_step vs dense fp64 attention max|err| {err:.3g}", flush=True)
-    assert err <= 2e-3
-    # Appended tokens: the oracle's nearest anchor and gamma against its own anchor set.
-    ex4 = _export(plan, cache, 0, 4)
-    K = lay.K[0].float().cpu().numpy()
-    V = lay.V[0].float().cpu().numpy()
+    enc = _oracle_whole_request(cfg, lay, 0, exp, "workload 3")
+    out = torch.empty(1, wl.Hq, wl.D, dtype=torch.float32, device="cuda")
+    outs = {}
+    for s in range(NS):
+        akv.decode_step(plan, cache, s, lay.k_new[s], lay.v_new[s], lay.q[s], out, dws)
+        if s in (0, NS - 1):
+            torch.cuda.synchronize()
+            outs[s] = out[0].cpu().numpy().copy()
+    torch.cuda.synchronize()
+    ex = _export(plan, cache, 0, NS)
+    kt = lay.k_new[:, 0].float().cpu().numpy()
+    vt = lay.v_new[:, 0].float().cpu().numpy()
+    cl = _cpu_layer(lay)
+    K = cl.K[0].float().numpy()
+    V = cl.V[0].float().numpy()
     for h in range(wl.H):
-        anc = ex4["anchors"][h]
-        for X, new, side in ((K, lay.k_new, "k"), (V, lay.v_new, "v")):
-            a, gm = R.assign_vectors(new[:4, 0, h].float().cpu().numpy(), X[h][anc], bf16=True)
-            np.testing.assert_array_equal(ex4["tail_a_" + side][h], a)
-            np.testing.assert_array_equal(ex4["tail_gamma_" + side][h], gm.astype(np.float32))
+        anc = enc["anchors"][h]
+        for X, new, side in ((K, kt, "k"), (V, vt, "v")):
+            a, gm = R.assign_vectors(new[:, h], X[h][anc], bf16=True)
+            np.testing.assert_array_equal(ex["tail_a_" + side][h], a)
+            np.testing.assert_array_equal(ex["tail_gamma_" + side][h], gm.astype(np.float32))
+    for s, got in outs.items():
+        _oracle_decode_check(cfg, lay, 0, enc, lay.q[s, 0].float().cpu().numpy(), got,
+                             tails=(kt[:s + 1], vt[:s + 1]), tag=f"workload 3 step {s + 1}")
 
 
-def test_workload4_70b_batch8():
+def test_workload4_70b_batch8_whole():
+    """All 8 requests of the 70B-shaped batch against the oracle's whole
+    compression pass, and the batched decode step of every request against
+    the oracle's attention over its reconstruction."""
     wl = synth.workload(4)
     print(f"[full] workload 4 {wl.name}", flush=True)
     lay = _layer_on_gpu(wl)
@@ -206,17 +245,22 @@ def test_workload4_70b_batch8():
     torch.cuda.synchronize()
     del keep
     assert _header_flags(cache) == 0
-    rng = np.random.default_rng(40)
-    for b in (0, 7):
-        exp = _export(plan, cache, b)
-        n = _sampled_request_check(cfg, lay, b, exp, 128, rng)
-        print(f"[full] workload 4 request {b}: sampled codes checked {n}", flush=True)
-    err = _decode_property(plan, cache, dws, lay, [0, 3, 7], steps=1, append=False)
-    print(f"[full] workload 4: decode vs dense fp64 attention max|err| {err:.3g}", flush=True)
-    assert err <= 2e-3
+    out = torch.empty(wl.batch, wl.Hq, wl.D, dtype=torch.float32, device="cuda")
+    akv.decode_attn(plan, cache, lay.q[0], out, dws)
+    torch.cuda.synchronize()
+    got = out.cpu().numpy()
+    host = cache.cpu().numpy()
+    for b in range(wl.batch):
+        exp = akv.export(plan, host, b, 0)
+        enc = _oracle_whole_request(cfg, lay, b, exp, f"workload 4 request {b}")
+        _oracle_decode_check(cfg, lay, b, enc, lay.q[0, b].float().cpu().numpy(), got[b],
+                             tag=f"workload 4 request {b}")
 
 
-def test_workload5_ragged16():
+def test_workload5_ragged16_short_median_long():
+    """The ragged batch of 16: the shortest, the median and the longest
+    request against the oracle's whole compression pass, and their decode
+    outputs against the oracle's attention over its reconstruction."""
     wl = synth.workload(5)
     print(f"[full] workload 5 {wl.name} lens={wl.seq_lens}", flush=True)
     lay = _layer_on_gpu(wl)
@@ -227,16 +271,17 @@ def test_workload5_ragged16():
     torch.cuda.synchronize()
     del keep
     assert _header_flags(cache) == 0
+    out = torch.empty(wl.batch, wl.Hq, wl.D, dtype=torch.float32, device="cuda")
+    akv.decode_attn(plan, cache, lay.q[0], out, dws)
+    torch.cuda.synchronize()
+    got = out.cpu().numpy()
+    host = cache.cpu().numpy()
     order = np.argsort(wl.seq_lens)
-    picks = [int(order[0]), int(order[len(order) // 2])]
-    rng = np.random.default_rng(50)
-    for b in picks:
-        exp = _export(plan, cache, b)
-        n = _sampled_request_check(cfg, lay, b, exp, 128, rng)
-        print(f"[full] workload 5 request {b} (S={wl.seq_lens[b]}): sampled codes checked {n}", flush=True)
-    err = _decode_property(plan, cache, dws, lay, picks + [int(order[-1])], steps=1, append=False)
-    print(f"[full] workload 5: decode vs dense fp64 attention max|err| {err:.3g}", flush=True)
-    assert err <= 2e-3
+    for b in (int(order[0]), int(order[len(order) // 2]), int(order[-1])):
+        exp = akv.export(plan, host, b, 0)
+        tag = f"workload 5 request {b} (S={wl.seq_lens[b]})"
+        enc = _oracle_whole_request(cfg, lay, b, exp, tag)
+        _oracle_decode_check(cfg, lay, b, enc, lay.q[0, b].float().cpu().numpy(), got[b], tag=tag)
 
 
 def test_long_sequence_more_than_256_splits():
