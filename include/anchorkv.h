@@ -190,6 +190,23 @@ anchorkv_status anchorkv_decode_step(const anchorkv_plan* plan, void* cache, siz
                                      size_t q_bytes, void* out, size_t out_bytes, int32_t out_dtype,
                                      float softmax_scale, void* workspace, size_t workspace_bytes, void* stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc):
+ * anchorkv_decode_step without the workspace argument.  Its scratch is a
+ * library-owned static device array of ANCHORKV_NOALLOC_SCRATCH_BYTES per GPU,
+ * held until the process ends; a plan whose decode workspace is larger
+ * returns ANCHORKV_ERR_BUFFER_TOO_SMALL.  The call allocates nothing.  The
+ * stream must belong to the current device.  Every call on one GPU shares
+ * that GPU's array: calls that overlap on it (other streams, other threads)
+ * race, so the caller serializes them.  Nothing in the array has to start at
+ * zero: each call writes all the scratch it reads.  Other arguments and the
+ * result as in anchorkv_decode_step. */
+#define ANCHORKV_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)
+anchorkv_status anchorkv_decode_step_noalloc(const anchorkv_plan* plan, void* cache, size_t cache_bytes,
+                                             int32_t n_appended, const void* k_new, const void* v_new,
+                                             size_t new_bytes, const void* q, size_t q_bytes, void* out,
+                                             size_t out_bytes, int32_t out_dtype, float softmax_scale, void* stream);
+
 /* Dense reconstruction (Eq. reconstruction) of one side (0 = keys, 1 = values)
  * of one request: out is device fp32 [H][S_b + n_appended][D], position order,
  * out_bytes its size. */

@@ -23,8 +23,9 @@ BUDGET_FRACTION, BUDGET_THETA, BUDGET_COUNT = 0, 1, 2
 
 EXPORTED = ["anchorkv_plan_create", "anchorkv_plan_destroy", "anchorkv_cache_bytes", "anchorkv_encode_workspace_bytes",
             "anchorkv_decode_workspace_bytes", "anchorkv_plan_request", "anchorkv_encode", "anchorkv_append",
-            "anchorkv_decode_attn", "anchorkv_decode_step", "anchorkv_reconstruct", "anchorkv_export", "anchorkv_profile_enable",
-            "anchorkv_profile_read", "anchorkv_profile_disable", "anchorkv_status_string", "anchorkv_last_error"]
+            "anchorkv_decode_attn", "anchorkv_decode_step", "anchorkv_decode_step_noalloc", "anchorkv_reconstruct",
+            "anchorkv_export", "anchorkv_profile_enable", "anchorkv_profile_read", "anchorkv_profile_disable",
+            "anchorkv_status_string", "anchorkv_last_error"]
 
 
 class AnchorKVError(RuntimeError):
@@ -88,6 +89,8 @@ def lib():
         L.anchorkv_decode_attn.argtypes = [vp, vp, sz, i32, vp, sz, vp, sz, i32, f32, vp, sz, vp]
         L.anchorkv_decode_step.restype = i32
         L.anchorkv_decode_step.argtypes = [vp, vp, sz, i32, vp, vp, sz, vp, sz, vp, sz, i32, f32, vp, sz, vp]
+        L.anchorkv_decode_step_noalloc.restype = i32
+        L.anchorkv_decode_step_noalloc.argtypes = [vp, vp, sz, i32, vp, vp, sz, vp, sz, vp, sz, i32, f32, vp]
         L.anchorkv_reconstruct.restype = i32
         L.anchorkv_reconstruct.argtypes = [vp, vp, sz, i32, i32, i32, vp, sz, vp]
         L.anchorkv_export.restype = i32
@@ -254,6 +257,26 @@ def decode_step(plan: Plan, cache, n_appended: int, k_new, v_new, q, out, worksp
     check(lib().anchorkv_decode_step(plan.handle, _ptr(cache), _nbytes(cache), n_appended, _ptr(k_new), _ptr(v_new),
                                      _nbytes(k_new), _ptr(q), _nbytes(q), _ptr(out), _nbytes(out), out_dtype,
                                      softmax_scale, _ptr(workspace), _nbytes(workspace), _stream(stream)))
+    return out
+
+
+def decode_step_noalloc(plan: Plan, cache, n_appended: int, k_new, v_new, q, out, out_dtype: Optional[int] = None,
+                        softmax_scale: float = 0.0, stream=None):
+    """decode_step with the library's static per-GPU scratch instead of a
+    caller workspace (the entry point allocates nothing)."""
+    import torch
+    k_new, v_new, q = k_new.contiguous(), v_new.contiguous(), q.contiguous()
+    if out_dtype is None:
+        out_dtype = F32 if out.dtype == torch.float32 else BF16
+    dt = _tdtype(plan.cfg.dtype)
+    _dev(k_new, "k_new", dt, _new_shape(plan))
+    _dev(v_new, "v_new", dt, _new_shape(plan))
+    _dev(q, "q", dt, _q_shape(plan))
+    _dev(out, "out", _tdtype(out_dtype), _q_shape(plan))
+    _dev(cache, "cache", torch.uint8)
+    check(lib().anchorkv_decode_step_noalloc(plan.handle, _ptr(cache), _nbytes(cache), n_appended, _ptr(k_new),
+                                             _ptr(v_new), _nbytes(k_new), _ptr(q), _nbytes(q), _ptr(out),
+                                             _nbytes(out), out_dtype, softmax_scale, _stream(stream)))
     return out
 
 

@@ -617,6 +617,60 @@ extern "C" anchorkv_status anchorkv_decode_step(const anchorkv_plan* p, void* ca
                               "decode step"));
 }
 
+// ------------------------------------------------------------------ no-allocation decode step
+// The scratch of anchorkv_decode_step_noalloc: one static device array per
+// GPU.  In host code `scratch` only names the symbol; its device address is
+// looked up once per device (with that device current) and kept.
+static __device__ __align__(256) unsigned char scratch[ANCHORKV_NOALLOC_SCRATCH_BYTES];
+namespace {
+std::mutex g_scratch_mu;
+constexpr int kMaxDevices = 64;
+void* g_scratch_ptr[kMaxDevices] = {};
+}  // namespace
+
+static anchorkv_status scratch_address(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_status(e, "hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices) return fail(ANCHORKV_ERR_UNSUPPORTED, "device index above 63");
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_status(e, "hipGetSymbolAddress(scratch)");
+    if (!ptr) return fail(ANCHORKV_ERR_HIP, "hipGetSymbolAddress(scratch) returned no address");
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = g_scratch_ptr[dev];
+  return ANCHORKV_OK;
+}
+
+extern "C" anchorkv_status anchorkv_decode_step_noalloc(const anchorkv_plan* p, void* cache, size_t cache_bytes,
+                                                        int32_t n_appended, const void* k_new, const void* v_new,
+                                                        size_t new_bytes, const void* q, size_t q_bytes, void* out,
+                                                        size_t out_bytes, int32_t out_dtype, float softmax_scale,
+                                                        void* stream) {
+  if (!p || !cache || !k_new || !v_new || !q || !out) return fail(ANCHORKV_ERR_INVALID_ARG, "null argument");
+  if (n_appended < 0) return fail(ANCHORKV_ERR_INVALID_ARG, "n_appended must be >= 0");
+  if (n_appended >= p->cfg.max_append) return fail(ANCHORKV_ERR_CAPACITY, "append capacity exhausted");
+  if (out_dtype != ANCHORKV_F32 && out_dtype != ANCHORKV_BF16) return fail(ANCHORKV_ERR_INVALID_ARG, "bad out_dtype");
+  anchorkv_status s;
+  if ((s = need_bytes(cache_bytes, p->cache_bytes, "cache")) != ANCHORKV_OK) return s;
+  if ((s = need_bytes(new_bytes, new_need(p), "k_new / v_new")) != ANCHORKV_OK) return s;
+  if ((s = need_bytes(q_bytes, q_need(p), "q")) != ANCHORKV_OK) return s;
+  if ((s = need_bytes(out_bytes, out_need(p, out_dtype), "out")) != ANCHORKV_OK) return s;
+  if ((s = need_bytes(ANCHORKV_NOALLOC_SCRATCH_BYTES, p->dws_bytes, "static decode scratch")) != ANCHORKV_OK)
+    return s;
+  void* ws = nullptr;
+  if ((s = scratch_address(&ws)) != ANCHORKV_OK) return s;
+  const float scale = softmax_scale > 0.0f ? softmax_scale : 1.0f / sqrtf((float)p->geo.D);
+  const FaultScope fs;
+  (void)hipGetLastError();
+  return fs.finish(hip_status(akv::launch_decode(p->geo, cache_ptrs(p, cache), dws_ptrs(p, ws), q, k_new, v_new, out,
+                                                 out_dtype, scale, n_appended, (hipStream_t)stream),
+                              "decode step (no allocation)"));
+}
+
 extern "C" anchorkv_status anchorkv_reconstruct(const anchorkv_plan* p, const void* cache, size_t cache_bytes,
                                                 int32_t n_appended, int32_t request, int32_t side, float* out,
                                                 size_t out_bytes, void* stream) {

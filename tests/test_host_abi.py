@@ -228,3 +228,17 @@ def test_export_rejects_a_foreign_blob():
     with pytest.raises(N.AnchorKVError) as e:
         N.export(p, junk, 0)
     assert e.value.status == N.ERR_CORRUPT_CACHE
+
+
+def test_noalloc_decode_step_rejects_a_plan_beyond_its_static_scratch():
+    """The no-allocation decode step serves plans whose decode workspace fits
+    its 32 MiB static scratch; 64 ragged 8B requests need about 77 MiB and are
+    refused before anything touches the GPU."""
+    L = _lib_or_skip()
+    import synth
+    wl = synth.workload(5)
+    plan = N.Plan(_cfg(max_append=1), wl.seq_lens * 4)
+    assert plan.decode_ws_bytes > 32 << 20
+    big = 1 << 30
+    st = L.anchorkv_decode_step_noalloc(plan.handle, 1, plan.cache_bytes, 0, 1, 1, big, 1, big, 1, big, 0, 0.0, None)
+    assert st == N.ERR_BUFFER_TOO_SMALL and "static decode scratch" in N.last_error()
