@@ -111,7 +111,7 @@ void akvref_fwht(float* z, int D) {
 #define AKV_LM_L1 1.5104176f
 #define AKV_LM_T 0.9815988f
 
-enum { SCALE_ABSMAX_OUTER = 0, SCALE_ABSMAX_LITERAL = 1, SCALE_RMS = 2 };
+enum { SCALE_ABSMAX_OUTER = 0, SCALE_ABSMAX_LITERAL = 1, SCALE_RMS = 2, SCALE_NAIVE = 3 };
 
 /* Scale of one group of rotated coordinates: the Gaussian standard deviation
  * the codebook is applied at.  The paper names a per-token absmax scale; the
@@ -140,19 +140,40 @@ static float group_scale(const float* z, int G, int mode) {
 
 /* Encode one residual r[D] (fp32): z = FWHT(s * r); per group of G
  * coordinates a scale sigma; code in {0,1,2,3} for levels {-L1,-L0,+L0,+L1};
- * four codes per byte, coordinate j in byte j/4 at bits 2*(j%4)..2*(j%4)+1. */
+ * four codes per byte, coordinate j in byte j/4 at bits 2*(j%4)..2*(j%4)+1.
+ *
+ * SCALE_NAIVE is the ablation of Sec. 4.3 "Component Removal" (iv): 2-bit
+ * quantization without the Hadamard rotation and without the Lloyd-Max
+ * codebook, i.e. z = r and the uniform four-level quantizer of [-A, A]
+ * (A = group absmax): cells of width A/2, levels +-A/4, +-3A/4, so
+ * sigma = A/4 with levels {-3,-1,+1,+3} sigma and threshold 2 sigma. */
 void akvref_codec_encode(const float* r, int D, int G, int mode, uint64_t seed,
                          uint8_t* codes, float* scales) {
   float* s = (float*)malloc(sizeof(float) * D);
   float* z = (float*)malloc(sizeof(float) * D);
   akvref_hadamard_signs(seed, D, s);
-  for (int j = 0; j < D; ++j) z[j] = s[j] * r[j];
-  akvref_fwht(z, D);
+  if (mode == SCALE_NAIVE) {
+    for (int j = 0; j < D; ++j) z[j] = r[j];
+  } else {
+    for (int j = 0; j < D; ++j) z[j] = s[j] * r[j];
+    akvref_fwht(z, D);
+  }
   memset(codes, 0, (size_t)D / 4);
   for (int g0 = 0; g0 < D; g0 += G) {
-    float sigma = group_scale(z + g0, G, mode);
+    float sigma, T;
+    if (mode == SCALE_NAIVE) {
+      float A = 0.0f;
+      for (int j = g0; j < g0 + G; ++j) {
+        float m = fabsf(z[j]);
+        if (m > A) A = m;
+      }
+      sigma = A * 0.25f;
+      T = sigma * 2.0f;
+    } else {
+      sigma = group_scale(z + g0, G, mode);
+      T = sigma * AKV_LM_T;
+    }
     scales[g0 / G] = sigma;
-    float T = sigma * AKV_LM_T;
     for (int j = g0; j < g0 + G; ++j) {
       int outer = fabsf(z[j]) > T;
       int c = (z[j] < 0.0f) ? (outer ? 0 : 1) : (outer ? 3 : 2);
@@ -164,10 +185,19 @@ void akvref_codec_encode(const float* r, int D, int G, int mode, uint64_t seed,
 }
 
 /* Decode: zhat_j = sigma * level(code_j); r~ = s * FWHT(zhat) / D, i.e.
- * U^T applied to the dequantized rotated coordinates (App. A.1, Eq. arc-tuple). */
+ * U^T applied to the dequantized rotated coordinates (App. A.1, Eq. arc-tuple).
+ * SCALE_NAIVE: levels {-3,-1,+1,+3} and no rotation, r~ = zhat. */
 void akvref_codec_decode(const uint8_t* codes, const float* scales, int D, int G,
-                         uint64_t seed, float* rt) {
+                         uint64_t seed, int mode, float* rt) {
   static const float lev[4] = {-AKV_LM_L1, -AKV_LM_L0, AKV_LM_L0, AKV_LM_L1};
+  static const float ulev[4] = {-3.0f, -1.0f, 1.0f, 3.0f};
+  if (mode == SCALE_NAIVE) {
+    for (int j = 0; j < D; ++j) {
+      int c = (codes[j / 4] >> (2 * (j % 4))) & 3;
+      rt[j] = scales[j / G] * ulev[c];
+    }
+    return;
+  }
   float* s = (float*)malloc(sizeof(float) * D);
   akvref_hadamard_signs(seed, D, s);
   for (int j = 0; j < D; ++j) {
@@ -496,6 +526,49 @@ int64_t akvref_budget_select(const double* u, int H, int S, int64_t N, uint8_t* 
   return n;
 }
 
+/* Equal per-head budgets (Sec. 4.3 "Component Removal" (ii), the pooling
+ * across heads dropped): every head selects its own floor(N / H) candidates
+ * of highest key, ties to the lower position.  Returns the number selected. */
+int64_t akvref_budget_select_per_head(const double* u, int H, int S, int64_t N, uint8_t* sel) {
+  int64_t tot = 0;
+  for (int h = 0; h < H; ++h) tot += akvref_budget_select(u + (size_t)h * S, 1, S, N / H, sel + (size_t)h * S);
+  return tot;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Residual ranking (Sec. 3.3 utilities and the alternatives of Sec. 4.3     */
+/* "Residual Ranking").                                                       */
+/* ------------------------------------------------------------------------ */
+
+enum { RANK_UTILITY = 0, RANK_COSINE = 1, RANK_RESNORM = 2, RANK_ATTENTION = 3, RANK_RANDOM = 4 };
+
+/* Ranking key of non-anchor token t of head h on one side (larger = earlier
+ * residual), for the alternatives to the utility:
+ *   COSINE    : 1 - |cos(x_t, abar_a(t))|, the least aligned first (cos from
+ *               sequential fp64 dots; a zero vector counts as orthogonal);
+ *   RESNORM   : ||r_t||^2 of the fp32 residual (sequential fp64 sum);
+ *   ATTENTION : the raw selector score sc(t) (mean attention of the
+ *               observation rows, App. A.2), the same on both sides;
+ *   RANDOM    : a uniform variate in [0, 1) from the counter-based hash
+ *               splitmix64(seed_r ^ (side + 1) << 60 ^ h << 40 ^ t), 53 bits. */
+double akvref_rank_key(int mode, int side, int h, int t, const double* x, const double* abar, int D,
+                       const float* r, double sc_t, uint64_t seed) {
+  if (mode == RANK_COSINE) {
+    double d = dot64(x, abar, D), xx = dot64(x, x, D), nn = dot64(abar, abar, D);
+    double den = sqrt(xx * nn);
+    return den > 0.0 ? 1.0 - fabs(d) / den : 1.0;
+  }
+  if (mode == RANK_RESNORM) {
+    double s = 0.0;
+    for (int j = 0; j < D; ++j) s += (double)r[j] * (double)r[j];
+    return s;
+  }
+  if (mode == RANK_ATTENTION) return sc_t;
+  uint64_t rs = akvref_splitmix64(seed ^ 3ULL);
+  uint64_t key = akvref_splitmix64(rs ^ ((uint64_t)(side + 1) << 60) ^ ((uint64_t)h << 40) ^ (uint64_t)t);
+  return (double)(key >> 11) * 0x1p-53;
+}
+
 /* ------------------------------------------------------------------------ */
 /* Whole compression pass of one request (Algorithm 1).                      */
 /* ------------------------------------------------------------------------ */
@@ -504,6 +577,9 @@ enum { BUDGET_FRACTION = 0, BUDGET_THETA = 1, BUDGET_COUNT = 2 };
 
 /* K, V: [H][S][D]; Qobs: [Hq][W][D] (values exactly representable in the
  * cache dtype).  anchor_override: [H][k] sorted positions or NULL.
+ * rank_mode: RANK_* (the utility is the method; the rest are the ablations
+ * of Sec. 4.3); head_budget: 0 pools the budget over heads (the method), 1
+ * gives every head floor(N / H).
  * Outputs, all per head in position order:
  *   anchors[H][k]; aK, aV [H][S] anchor index; gK, gV [H][S] stored gamma;
  *   uK, uV [H][S] utilities (-1 on anchors); selK, selV [H][S] residual flags;
@@ -512,13 +588,13 @@ enum { BUDGET_FRACTION = 0, BUDGET_THETA = 1, BUDGET_COUNT = 2 };
  * nsel[2] receives the residual counts per side. */
 int akvref_encode(int H, int Hq, int D, int S, int W, int k, float rho, int kappa, int bf16,
                   uint64_t seed, int budget_mode, double budget, int64_t budget_count, int G,
-                  int scale_mode, const double* K, const double* V, const double* Qobs,
-                  const int* anchor_override, int* anchors, int* aK, double* gK, int* aV,
+                  int scale_mode, int rank_mode, int head_budget, const double* K, const double* V,
+                  const double* Qobs, const int* anchor_override, int* anchors, int* aK, double* gK, int* aV,
                   double* gV, double* uK, double* uV, uint8_t* selK, uint8_t* selV,
                   uint8_t* codesK, float* scalesK, uint8_t* codesV, float* scalesV,
                   double* pooled, int64_t* nsel) {
   if (H <= 0 || Hq % H != 0 || D < 4 || (D & (D - 1)) || W < 0 || k < W || k > S ||
-      G <= 0 || D % G || G % 4 || kappa <= 0 || (kappa & 1) == 0)
+      G <= 0 || D % G || G % 4 || kappa <= 0 || (kappa & 1) == 0 || rank_mode < 0 || rank_mode > 4)
     return 1;
   int g = Hq / H, m = W * g, P = S - W;
   size_t SD = (size_t)S * D;
@@ -539,6 +615,7 @@ int akvref_encode(int H, int Hq, int D, int S, int W, int k, float rho, int kapp
     akvref_obs_head(Kh, Vh, Qg, S, D, W, g, M, Zs, Y);
     if (anchor_override) {
       memcpy(anc, anchor_override + (size_t)h * k, sizeof(int) * k);
+      if (rank_mode == RANK_ATTENTION) akvref_selector_scores(Kh, Qg, M, Zs, S, D, W, g, kappa, sc, pl);
     } else {
       akvref_selector_scores(Kh, Qg, M, Zs, S, D, W, g, kappa, sc, pl);
       if (pooled) memcpy(pooled + (size_t)h * P, pl, sizeof(double) * P);
@@ -568,6 +645,21 @@ int akvref_encode(int H, int Hq, int D, int S, int W, int k, float rho, int kapp
       uK[(size_t)h * S + cand_t[i]] = cuk[i];
       uV[(size_t)h * S + cand_t[i]] = cuv[i];
     }
+    if (rank_mode != RANK_UTILITY) {
+      double* ak = (double*)malloc(sizeof(double) * D);
+      double* av = (double*)malloc(sizeof(double) * D);
+      for (int i = 0; i < nc; ++i) {
+        int t = cand_t[i];
+        size_t e = (size_t)h * S + t;
+        memcpy(ak, Kh + (size_t)anc[aK[e]] * D, sizeof(double) * D);
+        memcpy(av, Vh + (size_t)anc[aV[e]] * D, sizeof(double) * D);
+        double sct = t < P ? sc[t] : 0.0;
+        uK[e] = akvref_rank_key(rank_mode, 0, h, t, Kh + (size_t)t * D, ak, D, crk + (size_t)i * D, sct, seed);
+        uV[e] = akvref_rank_key(rank_mode, 1, h, t, Vh + (size_t)t * D, av, D, crv + (size_t)i * D, sct, seed);
+      }
+      free(ak);
+      free(av);
+    }
     free(isanc); free(cand_t); free(crk); free(crv); free(cuk); free(cuv);
   }
   int64_t NK, NV;
@@ -581,8 +673,13 @@ int akvref_encode(int H, int Hq, int D, int S, int W, int k, float rho, int kapp
   } else {
     NK = NV = (int64_t)floor((double)(float)budget * (double)H * (double)S);
   }
-  nsel[0] = akvref_budget_select(uK, H, S, NK, selK);
-  nsel[1] = akvref_budget_select(uV, H, S, NV, selV);
+  if (head_budget) {
+    nsel[0] = akvref_budget_select_per_head(uK, H, S, NK, selK);
+    nsel[1] = akvref_budget_select_per_head(uV, H, S, NV, selV);
+  } else {
+    nsel[0] = akvref_budget_select(uK, H, S, NK, selK);
+    nsel[1] = akvref_budget_select(uV, H, S, NV, selV);
+  }
   int nb = D / 4, ns = D / G;
   memset(codesK, 0, (size_t)H * S * nb);
   memset(codesV, 0, (size_t)H * S * nb);
@@ -606,7 +703,7 @@ int akvref_encode(int H, int Hq, int D, int S, int W, int k, float rho, int kapp
 /* Dense reconstruction of one side of one head, fp32:
  *   anchor positions: the stored anchor vector;
  *   others: p_j = fp32(gamma * abar_j); with a residual, x^_j = fp32(p_j + r~_j). */
-void akvref_reconstruct(const double* X, int S, int D, int G, uint64_t seed, const int* anchors,
+void akvref_reconstruct(const double* X, int S, int D, int G, uint64_t seed, int scale_mode, const int* anchors,
                         int k, const int* a, const double* gm, const uint8_t* sel,
                         const uint8_t* codes, const float* scales, float* out) {
   int* rank = (int*)malloc(sizeof(int) * (size_t)S);
@@ -623,7 +720,7 @@ void akvref_reconstruct(const double* X, int S, int D, int G, uint64_t seed, con
     float g = (float)gm[t];
     for (int j = 0; j < D; ++j) o[j] = g * (float)an[j];
     if (sel[t]) {
-      akvref_codec_decode(codes + (size_t)t * (D / 4), scales + (size_t)t * (D / G), D, G, seed, rt);
+      akvref_codec_decode(codes + (size_t)t * (D / 4), scales + (size_t)t * (D / G), D, G, seed, scale_mode, rt);
       for (int j = 0; j < D; ++j) o[j] = o[j] + rt[j];
     }
   }

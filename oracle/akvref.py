@@ -19,7 +19,8 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "akvref.c")
 _LIB = os.path.join(_HERE, "libakvref.so")
 
-SCALE_ABSMAX_OUTER, SCALE_ABSMAX_LITERAL, SCALE_RMS = 0, 1, 2
+SCALE_ABSMAX_OUTER, SCALE_ABSMAX_LITERAL, SCALE_RMS, SCALE_NAIVE = 0, 1, 2, 3
+RANK_UTILITY, RANK_COSINE, RANK_RESNORM, RANK_ATTENTION, RANK_RANDOM = 0, 1, 2, 3, 4
 BUDGET_FRACTION, BUDGET_THETA, BUDGET_COUNT = 0, 1, 2
 
 
@@ -58,7 +59,7 @@ def _declare(L):
     L.akvref_hadamard_signs.argtypes = [_c_u64, _c_int, _f]
     L.akvref_fwht.argtypes = [_f, _c_int]
     L.akvref_codec_encode.argtypes = [_f, _c_int, _c_int, _c_int, _c_u64, _u8, _f]
-    L.akvref_codec_decode.argtypes = [_u8, _f, _c_int, _c_int, _c_u64, _f]
+    L.akvref_codec_decode.argtypes = [_u8, _f, _c_int, _c_int, _c_u64, _c_int, _f]
     L.akvref_base_bytes.restype = _c_dbl
     L.akvref_base_bytes.argtypes = [_c_int] * 7
     L.akvref_theta_budget.restype = _c_i64
@@ -74,11 +75,16 @@ def _declare(L):
                                    _i, _c_int, _f, _f, _d, _d]
     L.akvref_budget_select.restype = _c_i64
     L.akvref_budget_select.argtypes = [_d, _c_int, _c_int, _c_i64, _u8]
+    L.akvref_budget_select_per_head.restype = _c_i64
+    L.akvref_budget_select_per_head.argtypes = [_d, _c_int, _c_int, _c_i64, _u8]
+    L.akvref_rank_key.restype = _c_dbl
+    L.akvref_rank_key.argtypes = [_c_int, _c_int, _c_int, _c_int, _d, _d, _c_int, _f, _c_dbl, _c_u64]
     L.akvref_encode.restype = _c_int
     L.akvref_encode.argtypes = ([_c_int] * 6 + [_c_flt, _c_int, _c_int, _c_u64, _c_int, _c_dbl, _c_i64,
-                                                _c_int, _c_int, _d, _d, _d, _i, _i, _i, _d, _i, _d, _d, _d,
-                                                _u8, _u8, _u8, _f, _u8, _f, _d, _i64])
-    L.akvref_reconstruct.argtypes = [_d, _c_int, _c_int, _c_int, _c_u64, _i, _c_int, _i, _d, _u8, _u8, _f, _f]
+                                                _c_int, _c_int, _c_int, _c_int, _d, _d, _d, _i, _i, _i, _d, _i, _d,
+                                                _d, _d, _u8, _u8, _u8, _f, _u8, _f, _d, _i64])
+    L.akvref_reconstruct.argtypes = [_d, _c_int, _c_int, _c_int, _c_u64, _c_int, _i, _c_int, _i, _d, _u8, _u8, _f,
+                                     _f]
     L.akvref_attention.argtypes = [_f, _f, _c_int, _c_int, _c_int, _d, _c_int, _c_dbl, _d]
     L.akvref_num_threads.restype = _c_int
 
@@ -126,11 +132,11 @@ def codec_encode(r, G: int, mode: int, seed: int):
     return codes, scales
 
 
-def codec_decode(codes, scales, D: int, G: int, seed: int) -> np.ndarray:
+def codec_decode(codes, scales, D: int, G: int, seed: int, mode: int = SCALE_ABSMAX_OUTER) -> np.ndarray:
     codes = np.ascontiguousarray(codes, np.uint8)
     scales = _f32(scales)
     rt = np.empty(D, np.float32)
-    lib().akvref_codec_decode(_p(codes, _u8), _p(scales, _f), D, G, seed, _p(rt, _f))
+    lib().akvref_codec_decode(_p(codes, _u8), _p(scales, _f), D, G, seed, mode, _p(rt, _f))
     return rt
 
 
@@ -213,18 +219,20 @@ def utilities(Kh, Vh, Qg, M, Z, Y, toks, rK, rV):
     return uK, uV
 
 
-def budget_select(u, N):
+def budget_select(u, N, per_head=False):
     u = _f64(u)
     H, S = u.shape
     sel = np.zeros((H, S), np.uint8)
-    n = lib().akvref_budget_select(_p(u, _d), H, S, N, _p(sel, _u8))
+    fn = lib().akvref_budget_select_per_head if per_head else lib().akvref_budget_select
+    n = fn(_p(u, _d), H, S, N, _p(sel, _u8))
     return sel, int(n)
 
 
 # ----------------------------------------------------------------------------- whole request
 
 def encode(K, V, Qobs, *, W, k, rho=0.7, kappa=7, bf16=True, seed=0, budget_mode=BUDGET_FRACTION,
-           budget=0.05, budget_count=0, G=None, scale_mode=SCALE_ABSMAX_OUTER, anchor_override=None):
+           budget=0.05, budget_count=0, G=None, scale_mode=SCALE_ABSMAX_OUTER, anchor_override=None,
+           rank_mode=RANK_UTILITY, head_budget=0):
     """Algorithm 1 for one request.  K, V: [H][S][D]; Qobs: [Hq][W][D]."""
     K, V, Qobs = _f64(K), _f64(V), _f64(Qobs)
     H, S, D = K.shape
@@ -240,7 +248,7 @@ def encode(K, V, Qobs, *, W, k, rho=0.7, kappa=7, bf16=True, seed=0, budget_mode
     ov = None if anchor_override is None else _i32(anchor_override)
     rc = lib().akvref_encode(
         H, Hq, D, S, W, k, rho, kappa, int(bf16), seed, budget_mode, budget, budget_count, G, scale_mode,
-        _p(K, _d), _p(V, _d), _p(Qobs, _d), _p(ov, _i) if ov is not None else None,
+        rank_mode, int(head_budget), _p(K, _d), _p(V, _d), _p(Qobs, _d), _p(ov, _i) if ov is not None else None,
         _p(out["anchors"], _i), _p(out["aK"], _i), _p(out["gK"], _d), _p(out["aV"], _i), _p(out["gV"], _d),
         _p(out["uK"], _d), _p(out["uV"], _d), _p(out["selK"], _u8), _p(out["selV"], _u8),
         _p(out["codesK"], _u8), _p(out["scalesK"], _f), _p(out["codesV"], _u8), _p(out["scalesV"], _f),
@@ -248,6 +256,7 @@ def encode(K, V, Qobs, *, W, k, rho=0.7, kappa=7, bf16=True, seed=0, budget_mode
     if rc != 0:
         raise ValueError("oracle rejected the configuration")
     out["pooled"] = out["pooled"][:, : S - W]
+    out["scale_mode"] = scale_mode
     return out
 
 
@@ -266,8 +275,8 @@ def reconstruct(X, enc, side: str, G, seed):
         codes = np.ascontiguousarray(enc["codes" + side][h], np.uint8)
         scales = _f32(enc["scales" + side][h])
         o = np.empty((S, D), np.float32)
-        lib().akvref_reconstruct(_p(Xh, _d), S, D, G, seed, _p(anc, _i), k, _p(a, _i), _p(g, _d),
-                                 _p(sel, _u8), _p(codes, _u8), _p(scales, _f), _p(o, _f))
+        lib().akvref_reconstruct(_p(Xh, _d), S, D, G, seed, int(enc.get("scale_mode", 0)), _p(anc, _i), k,
+                                 _p(a, _i), _p(g, _d), _p(sel, _u8), _p(codes, _u8), _p(scales, _f), _p(o, _f))
         out[h] = o
     return out
 
