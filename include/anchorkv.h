@@ -60,12 +60,32 @@ typedef enum { ANCHORKV_F32 = 0, ANCHORKV_BF16 = 1 } anchorkv_dtype;
  * standard deviation the codebook is applied at) has three readings:
  *   OUTER   : sigma = absmax / L1 -- the largest coordinate lands on the outer level;
  *   LITERAL : sigma = absmax;
- *   RMS     : sigma = root mean square of the group's rotated coordinates. */
+ *   RMS     : sigma = root mean square of the group's rotated coordinates.
+ * NAIVE is the ablation of Sec. 4.3 ("Component Removal" (iv)): no Hadamard
+ * rotation and no Lloyd-Max codebook, the uniform four-level quantizer of
+ * [-A, A] (A = group absmax, levels +-A/4, +-3A/4) on the raw residual. */
 typedef enum {
   ANCHORKV_SCALE_ABSMAX_OUTER = 0,
   ANCHORKV_SCALE_ABSMAX_LITERAL = 1,
-  ANCHORKV_SCALE_RMS = 2
+  ANCHORKV_SCALE_RMS = 2,
+  ANCHORKV_SCALE_NAIVE = 3
 } anchorkv_scale_mode;
+
+/* What ranks the candidates for a residual (Sec. 3.3 utilities; the
+ * alternatives are the ablations of Sec. 4.3 "Residual Ranking"):
+ *   UTILITY   : the attention-output-aware utilities of Eq. utilities (the method);
+ *   COSINE    : 1 - |cos(x_t, anchor)|, the least aligned first;
+ *   RESNORM   : the residual's squared norm;
+ *   ATTENTION : the mean attention of the observation rows on the token;
+ *   RANDOM    : a uniform draw (seeded).
+ * Every mode ranks exactly (fp64 keys, ties to the lower head, then position). */
+typedef enum {
+  ANCHORKV_RANK_UTILITY = 0,
+  ANCHORKV_RANK_COSINE = 1,
+  ANCHORKV_RANK_RESNORM = 2,
+  ANCHORKV_RANK_ATTENTION = 3,
+  ANCHORKV_RANK_RANDOM = 4
+} anchorkv_rank_mode;
 
 /* Residual budget per side (Sec. 3.4).
  *   FRACTION : N_side = floor(budget * H * S) per request and side;
@@ -96,7 +116,10 @@ typedef struct anchorkv_config {
   int32_t scale_mode;     /* anchorkv_scale_mode */
   int32_t dtype;          /* anchorkv_dtype of K, V, queries, anchors and coefficients */
   int32_t max_append;     /* capacity for tokens appended after the compression pass */
-  uint64_t seed;          /* seeds the uniform anchor share and the Hadamard sign pattern */
+  int32_t rank_mode;      /* an anchorkv_rank_mode; 0 is the method's utilities */
+  int32_t head_budget;    /* 0: the budget is pooled over heads (the method); 1: every head gets
+                             floor(N_side / H) (Sec. 4.3 ablation; needs batch * H <= 64) */
+  uint64_t seed;          /* seeds the uniform anchor share, the Hadamard signs and the random ranking */
 } anchorkv_config;
 
 /* Derived per-request sizes (host memory). */

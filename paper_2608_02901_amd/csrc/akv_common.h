@@ -27,6 +27,11 @@ struct Geo {
   int dtype;                    // 0 = fp32, 1 = bf16 (inputs, anchors, coefficients)
   int esz;                      // element bytes of the dtype
   int kappa, scale_mode, max_append;
+  int rot;                      // residual codec rotates (Hadamard) before quantizing (0 for the naive codec)
+  float lev0, lev1, thr;        // codec levels (in units of the scale) and threshold
+  int rank_mode;                // residual ranking key (anchorkv_rank_mode)
+  int hdiv;                     // budget lists per request and side: H (equal per-head budgets) or 1
+  unsigned long long seed_rank; // random ranking
   int maxS, maxK;
   unsigned long long seed_anchor, seed_sign;
   unsigned long long sgnbits[2];  // Hadamard sign of coordinate j (bit set = -1), j < 128
@@ -72,6 +77,8 @@ enum : int {
   BST_B = 5,      // bits of max{upper bound : u <= T}  (every exact utility above it is selected)
   BST_NEED = 6    // band members the fp32 order selected (= selections the band must supply)
 };
+// Residual ranking keys (the public anchorkv_rank_mode values).
+enum : int { RANK_UTILITY = 0, RANK_COSINE = 1, RANK_RESNORM = 2, RANK_ATTENTION = 3, RANK_RANDOM = 4 };
 // Cache header flag bits (header[2]).
 enum : uint32_t {
   HDR_BAD_OVERRIDE = 1u,  // anchor override broke its rules

@@ -155,7 +155,11 @@ extern "C" anchorkv_status anchorkv_plan_create(const anchorkv_config* cfg, int3
   const int G = c.quant_group ? c.quant_group : c.head_dim;
   if (G < 4 || G % 4 || c.head_dim % G) return fail(ANCHORKV_ERR_INVALID_ARG, "quant_group must divide head_dim and be a multiple of 4");
   if (G < 32) return fail(ANCHORKV_ERR_UNSUPPORTED, "this build supports quant_group 32, 64 or 128");
-  if (c.scale_mode < 0 || c.scale_mode > 2) return fail(ANCHORKV_ERR_INVALID_ARG, "bad scale_mode");
+  if (c.scale_mode < 0 || c.scale_mode > 3) return fail(ANCHORKV_ERR_INVALID_ARG, "bad scale_mode");
+  if (c.rank_mode < 0 || c.rank_mode > 4) return fail(ANCHORKV_ERR_INVALID_ARG, "bad rank_mode");
+  if (c.head_budget != 0 && c.head_budget != 1) return fail(ANCHORKV_ERR_INVALID_ARG, "head_budget must be 0 or 1");
+  if (c.head_budget && (int64_t)batch * c.num_kv_heads > AKV_MAXB)
+    return fail(ANCHORKV_ERR_UNSUPPORTED, "equal per-head budgets need batch * num_kv_heads <= 64");
   if (c.budget_mode < 0 || c.budget_mode > 2) return fail(ANCHORKV_ERR_INVALID_ARG, "bad budget_mode");
   if (!(c.budget >= 0.0f) || (c.budget_mode != ANCHORKV_BUDGET_COUNT && c.budget > 1.0f))
     return fail(ANCHORKV_ERR_INVALID_ARG, "budget must be in [0, 1]");
@@ -184,6 +188,16 @@ extern "C" anchorkv_status anchorkv_plan_create(const anchorkv_config* cfg, int3
   geo.esz = c.dtype == ANCHORKV_BF16 ? 2 : 4;
   geo.kappa = c.kappa;
   geo.scale_mode = c.scale_mode;
+  // Codec levels and threshold in units of the stored scale: the Lloyd-Max
+  // pair for the rotated codec, the uniform grid {1, 3} (threshold 2) for the
+  // naive one, whose scale is a quarter of the group absmax.
+  geo.rot = c.scale_mode != ANCHORKV_SCALE_NAIVE;
+  geo.lev0 = geo.rot ? AKV_L0 : 1.0f;
+  geo.lev1 = geo.rot ? AKV_L1 : 3.0f;
+  geo.thr = geo.rot ? AKV_T : 2.0f;
+  geo.rank_mode = c.rank_mode;
+  geo.hdiv = c.head_budget ? c.num_kv_heads : 1;
+  geo.seed_rank = mix64(c.seed ^ 3ull);
   geo.max_append = c.max_append;
   geo.seed_anchor = mix64(c.seed ^ 1ull);
   geo.seed_sign = mix64(c.seed ^ 2ull);
@@ -231,6 +245,10 @@ extern "C" anchorkv_status anchorkv_plan_create(const anchorkv_config* cfg, int3
     }
     if (NK > ncand) NK = ncand;
     if (NV > ncand) NV = ncand;
+    if (c.head_budget) {  // every head takes floor(N_side / H)
+      NK = NK / H * H;
+      NV = NV / H * H;
+    }
     anchorkv_request_info ri;
     ri.seq_len = S;
     ri.anchors = k;
@@ -268,7 +286,7 @@ extern "C" anchorkv_status anchorkv_plan_create(const anchorkv_config* cfg, int3
     geo.prefW[b + 1] = geo.prefW[b] + (S + 63) / 64;
     geo.prefC[b + 1] = geo.prefC[b] + (S + akv::OBS_CHUNK - 1) / akv::OBS_CHUNK;
     geo.prefKT[b + 1] = geo.prefKT[b] + H * k * ((S + akv::SORT_CHUNK - 1) / akv::SORT_CHUNK + 1);
-    geo.prefBC[b + 1] = geo.prefBC[b] + (H * S + kBudgetChunk - 1) / kBudgetChunk;
+    geo.prefBC[b + 1] = geo.prefBC[b] + geo.hdiv * ((H / geo.hdiv * S + kBudgetChunk - 1) / kBudgetChunk);
     geo.prefKp[b + 1] = geo.prefKp[b] + ((k + 3) & ~3);
     geo.prefAB[b + 1] = geo.prefAB[b] + (k + 255) / 256;
     geo.prefNK[b + 1] = geo.prefNK[b] + (int)p->req[b].residuals_k;
@@ -373,13 +391,16 @@ extern "C" anchorkv_status anchorkv_plan_create(const anchorkv_config* cfg, int3
   p->w_uU = Wl.add(4 * 2 * TS);
   p->w_sel = Wl.add(2 * TS);
   p->w_srec = Wl.add(16 * TW * 64);
-  p->w_bhist = Wl.add(4 * 2 * 4096 * batch);
-  p->w_bstate = Wl.add(4 * 2 * akv::BST_N * batch);
-  p->w_bandpos = Wl.add(4 * 2 * (size_t)akv::BAND_CAP * batch);
-  p->w_bandu = Wl.add(8 * 2 * (size_t)akv::BAND_CAP * batch);
-  p->w_brank = Wl.add(4 * 2 * (size_t)akv::BAND_CAP * batch);
-  p->w_bcval = Wl.add(4 * 2 * (size_t)32768 * batch);
-  p->w_bcpos = Wl.add(4 * 2 * (size_t)32768 * batch);
+  // budget lists: one per request and side, or one per request, head and
+  // side with equal per-head budgets
+  const size_t nlist = (size_t)batch * geo.hdiv;
+  p->w_bhist = Wl.add(4 * 2 * 4096 * nlist);
+  p->w_bstate = Wl.add(4 * 2 * akv::BST_N * nlist);
+  p->w_bandpos = Wl.add(4 * 2 * (size_t)akv::BAND_CAP * nlist);
+  p->w_bandu = Wl.add(8 * 2 * (size_t)akv::BAND_CAP * nlist);
+  p->w_brank = Wl.add(4 * 2 * (size_t)akv::BAND_CAP * nlist);
+  p->w_bcval = Wl.add(4 * 2 * (size_t)32768 * nlist);
+  p->w_bcpos = Wl.add(4 * 2 * (size_t)32768 * nlist);
   p->w_tiecnt = Wl.add(4 * 2 * (size_t)geo.prefBC[batch]);
   p->w_shist = Wl.add(4 * (size_t)geo.prefKT[batch]);
   p->w_wcnt = Wl.add(4 * 2 * TW);
@@ -901,14 +922,15 @@ __global__ void k_init(Geo g, Cache c, Ws w) {
   if (i < 2 * g.H * g.B) w.fixcount[i] = 0;
   if (i < akv::SS_N * g.H * g.B) w.sstate[i] = 0;
   if (i < 4096 * g.H * g.B) w.sghist[i] = 0u;
-  if (i < 2 * 4096 * g.B) w.bhist[i] = 0u;
-  if (i < 2 * akv::BST_N * g.B) w.bstate[i] = (i % akv::BST_N) == akv::BST_A ? 0x7F800000 : 0;
+  const int nl = g.B * g.hdiv;
+  if (i < 2 * 4096 * nl) w.bhist[i] = 0u;
+  if (i < 2 * akv::BST_N * nl) w.bstate[i] = (i % akv::BST_N) == akv::BST_A ? 0x7F800000 : 0;
 }
 hipError_t launch_init(const Geo& g, const Cache& c, const Ws& w, hipStream_t st) {
   int n = 4 * g.B > 2 * g.H * g.B ? 4 * g.B : 2 * g.H * g.B;
   if (4096 * g.H * g.B > n) n = 4096 * g.H * g.B;
-  if (2 * 4096 * g.B > n) n = 2 * 4096 * g.B;
-  if (2 * akv::BST_N * g.B > n) n = 2 * akv::BST_N * g.B;
+  if (2 * 4096 * g.B * g.hdiv > n) n = 2 * 4096 * g.B * g.hdiv;
+  if (2 * akv::BST_N * g.B * g.hdiv > n) n = 2 * akv::BST_N * g.B * g.hdiv;
   launch("k_init", k_init, dim3((n + 255) / 256), dim3(256), 0, st, g, c, w);
   return hipGetLastError();
 }

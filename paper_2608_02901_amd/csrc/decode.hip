@@ -38,18 +38,13 @@ namespace akv {
 
 constexpr int PS = 4 + AKV_D;  // split record: max, sum, 2 pad, output[D]
 
-__device__ inline float level(int code) {
-  // 0 -> -L1, 1 -> -L0, 2 -> +L0, 3 -> +L1
-  const float mag = (code == 0 || code == 3) ? AKV_L1 : AKV_L0;
+__device__ inline float level(const Geo& g, int code) {
+  // 0 -> -l1, 1 -> -l0, 2 -> +l0, 3 -> +l1 (the Lloyd-Max pair, or 1 and 3
+  // for the naive uniform codec)
+  const float mag = (code == 0 || code == 3) ? g.lev1 : g.lev0;
   return code < 2 ? -mag : mag;
 }
 
-// sigma * level(code) from the group's four precomputed values.
-__device__ inline float scaled_level(int code, float n1, float n0, float p0, float p1) {
-  const float lo = (code & 1) ? n0 : n1;
-  const float hi = (code & 1) ? p1 : p0;
-  return (code & 2) ? hi : lo;
-}
 
 // Merge of two (best, second best, index of best) summaries of screening
 // scores; ties of the best go to the lower anchor index.
@@ -402,7 +397,9 @@ __global__ __launch_bounds__(256) void k_dec_front(Geo g, Cache c, DecWs dw, con
   __syncthreads();
   const int lo = bhr[0], hi = bhr[1];
   const uint32_t cw[4] = {ch4.x, ch4.y, ch4.z, ch4.w};
-  const float qscale = sl2 * (1.0f / (float)D);
+  // the rotated codec's residual dot is q_rot . zhat / D; the naive codec's
+  // is q . zhat (no rotation)
+  const float qscale = g.rot ? sl2 * (1.0f / (float)D) : sl2;
   const float s0v = sign_bit(g.sgnbits, 2 * lane), s1v = sign_bit(g.sgnbits, 2 * lane + 1);
   float dot[GQ];
 #pragma unroll
@@ -415,14 +412,18 @@ __global__ __launch_bounds__(256) void k_dec_front(Geo g, Cache c, DecWs dw, con
       float z0, z1;
       if (qpre && b2 == bq) {
         const E* qp = qraw + ((size_t)h2 * GQ + jj) * D;
-        z0 = s0v * Elem<DT>::get(qp, 2 * lane);
-        z1 = s1v * Elem<DT>::get(qp, 2 * lane + 1);
+        z0 = Elem<DT>::get(qp, 2 * lane);
+        z1 = Elem<DT>::get(qp, 2 * lane + 1);
       } else {
         const E* qp = (const E*)q + ((size_t)b2 * g.Hq + (size_t)h2 * GQ + jj) * D;
-        z0 = s0v * Elem<DT>::get(qp, 2 * lane);
-        z1 = s1v * Elem<DT>::get(qp, 2 * lane + 1);
+        z0 = Elem<DT>::get(qp, 2 * lane);
+        z1 = Elem<DT>::get(qp, 2 * lane + 1);
       }
-      fwht_wave_dpp(z0, z1, lane);
+      if (g.rot) {
+        z0 *= s0v;
+        z1 *= s1v;
+        fwht_wave_dpp(z0, z1, lane);
+      }
       float* qt = qs + (f / GQ) * D * GQ;
       qt[(2 * lane) * GQ + jj] = z0 * qscale;
       qt[(2 * lane + 1) * GQ + jj] = z1 * qscale;
@@ -438,7 +439,7 @@ __global__ __launch_bounds__(256) void k_dec_front(Geo g, Cache c, DecWs dw, con
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
         const int nib = n0 + u;
-        const float la = level(nib & 3), lb = level(nib >> 2);
+        const float la = level(g, nib & 3), lb = level(g, nib >> 2);
         float tv[GQ];
 #pragma unroll
         for (int jj = 0; jj < GQ; ++jj) tv[jj] = fmaf(lb, qb[jj], la * qa[jj]);
@@ -816,7 +817,7 @@ __global__ __launch_bounds__(256) void k_dec_stream(Geo g, Cache c, DecWs dw, in
   const int ws0 = s0 + wave * LW, ws1 = min(s1, ws0 + LW);
   if (ws0 < ws1) {
     for (int i = lane; i < SW_ACH * GQ; i += 64) (&W.wacc[0][0])[i] = 0.0f;
-    if (lane < 16) W.lvl[lane] = make_float2(level(lane & 3), level(lane >> 2));
+    if (lane < 16) W.lvl[lane] = make_float2(level(g, lane & 3), level(g, lane >> 2));
 
     // ---- round 1: records and flag words of this wave's slots.  Every
     // lane reads raw words (a lane past the split end re-reads the wave's
@@ -1150,8 +1151,15 @@ __global__ __launch_bounds__(256) void k_dec_stream(Geo g, Cache c, DecWs dw, in
       y1 = fmaf(f, yp[w][jj][2 * lane + 1], y1);
       l = fmaf(f, wl[w][jj], l);
     }
-    fwht_wave_dpp(z0, z1, lane);
-    const float o0 = y0 + s0v * (z0 * invD), o1 = y1 + s1v * (z1 * invD);
+    float o0, o1;
+    if (g.rot) {
+      fwht_wave_dpp(z0, z1, lane);
+      o0 = y0 + s0v * (z0 * invD);
+      o1 = y1 + s1v * (z1 * invD);
+    } else {
+      o0 = y0 + z0;
+      o1 = y1 + z1;
+    }
     float* pr = dw.part + ((size_t)g.prefSp[b] * Hq + (size_t)(h * GQ + jj) * (nsp + 1) + sp) * PS;
     if (lane == 0) {
       pr[0] = M;
@@ -1268,13 +1276,15 @@ __global__ __launch_bounds__(256) void k_reconstruct(Geo g, Cache c, int b, int 
     const uint8_t* cd = (side ? c.codesV : c.codesK) + (size_t)slot * (D / 4);
     const float sg = (side ? c.scalesV : c.scalesK)[(size_t)slot * (D / G) + (2 * lane) / G];
     const int nib = (cd[lane / 2] >> (4 * (lane & 1))) & 15;
-    float z0 = sg * level(nib & 3), z1 = sg * level(nib >> 2);
-    fwht_wave(z0, z1, lane);
-    const float invD = 1.0f / (float)D;
-    const float r0 = (z0 * invD) * hsign(g.seed_sign, 2 * lane);
-    const float r1 = (z1 * invD) * hsign(g.seed_sign, 2 * lane + 1);
-    x0 = x0 + r0;
-    x1 = x1 + r1;
+    float z0 = sg * level(g, nib & 3), z1 = sg * level(g, nib >> 2);
+    if (g.rot) {
+      fwht_wave(z0, z1, lane);
+      const float invD = 1.0f / (float)D;
+      z0 = (z0 * invD) * hsign(g.seed_sign, 2 * lane);
+      z1 = (z1 * invD) * hsign(g.seed_sign, 2 * lane + 1);
+    }
+    x0 = x0 + z0;
+    x1 = x1 + z1;
   }
   float* o = out + ((size_t)h * rows + t) * D;
   o[2 * lane] = x0;

@@ -39,53 +39,177 @@
 //                flattened index ascending) order;
 //   k_bsel     : re-marks the band: ranks below `need` are selected.
 // A band above BAND_CAP keeps the fp32 marks and raises HDR_BAND_OVERFLOW.
+//
+// Ranking keys other than the utility (the residual-ranking ablations of
+// Sec. 4.3) go through the same cut: k_rankkeys replaces u, uL, uU by the
+// key's fp32 rounding and an interval that holds its exact fp64 value, and
+// k_brescore computes the exact fp64 key of the band members.  With equal
+// per-head budgets (the head-pooling ablation of Sec. 4.3) every (request,
+// head, side) is a list of its own, ranked in position order.
 #include "akv_common.h"
 
 namespace akv {
 
 constexpr int BCHUNK = 4096;
-constexpr int BCMAX = 32768;  // first-digit candidates kept per request and side
+constexpr int BCMAX = 32768;  // first-digit candidates kept per list and side
 
-__device__ inline int nside(const Geo& g, int b, int side) {
-  return side ? g.prefNV[b + 1] - g.prefNV[b] : g.prefNK[b + 1] - g.prefNK[b];
+// Budget list L: request L / hdiv; heads [h0, h0 + hp) of it, hp = H / hdiv
+// (all heads with pooled budgets, one head with equal per-head budgets).
+// Its elements are the flattened (h - h0, t) positions, n = hp * S of them,
+// at offset `off` of a side's per-position arrays.
+struct BList {
+  int b, hp, h0, S, n, nch;
+  size_t off;
+};
+__device__ inline BList blist(const Geo& g, int L) {
+  BList q;
+  q.b = L / g.hdiv;
+  q.hp = g.H / g.hdiv;
+  q.h0 = (L % g.hdiv) * q.hp;
+  q.S = g.S[q.b];
+  q.n = q.hp * q.S;
+  q.nch = (q.n + BCHUNK - 1) / BCHUNK;
+  q.off = (size_t)g.prefS[q.b] * g.H + (size_t)q.h0 * q.S;
+  return q;
+}
+__device__ inline int nside(const Geo& g, const BList& q, int side) {
+  const int b = q.b;
+  return (side ? g.prefNV[b + 1] - g.prefNV[b] : g.prefNK[b + 1] - g.prefNK[b]) / g.hdiv;
 }
 // 0: radix select, 1: take every candidate, 2: take none.
-__device__ inline int bmode(const Geo& g, int b, int side) {
-  const int N = nside(g, b, side);
-  const int ncand = g.H * (g.S[b] - g.k[b]);
+__device__ inline int bmode(const Geo& g, const BList& q, int side) {
+  const int N = nside(g, q, side);
+  const int ncand = q.hp * (q.S - g.k[q.b]);
   return N <= 0 ? 2 : (N >= ncand ? 1 : 0);
 }
+// Threshold-tie counts of the list's chunks.
+__device__ inline int32_t* btie(const Geo& g, const Ws& w, int L, const BList& q, int side) {
+  return w.tiecnt + 2 * g.prefBC[q.b] + (2 * (L % g.hdiv) + side) * q.nch;
+}
 
-__device__ inline int locate_b(const Geo& g, int& idx) {
-  for (int b = 0; b < g.B; ++b) {
-    int n = 2 * ((g.H * g.S[b] + BCHUNK - 1) / BCHUNK);
-    if (idx < n) return b;
+// Workgroup idx -> list (chunks of both sides of every list in turn).
+__device__ inline int locate_l(const Geo& g, int& idx) {
+  const int nl = g.B * g.hdiv;
+  for (int L = 0; L < nl; ++L) {
+    const int n = 2 * (((g.H / g.hdiv) * g.S[L / g.hdiv] + BCHUNK - 1) / BCHUNK);
+    if (idx < n) return L;
     idx -= n;
   }
   return -1;
 }
 
-__device__ inline const float* butil(const Geo& g, const Ws& w, int b, int side) {
-  return w.u + (size_t)side * g.H * g.prefS[g.B] + (size_t)g.prefS[b] * g.H;
+__device__ inline size_t bbase(const Geo& g, const BList& q, int side) {
+  return (size_t)side * g.H * g.prefS[g.B] + q.off;
+}
+
+// ------------------------------------------------------------------ rank keys
+// Exact fp64 keys of the ranking ablations, as the oracle defines them:
+//   COSINE  : 1 - |d| / sqrt(xx nn) with d, xx, nn sequential fp64 dots of
+//             the token and its anchor (1 when a norm is zero);
+//   RESNORM : sequential fp64 sum of the squared fp32 residual
+//             r = x - fp32(gamma a);
+//   RANDOM  : 53 bits of splitmix64(seed ^ (side + 1) << 60 ^ h << 40 ^ t).
+// Products of two fp32 (or bf16) values are exact in fp64, so a fused
+// multiply-add accumulates exactly as a product followed by an add.
+template <int DT>
+__device__ double rank_key64(const Geo& g, int side, int h, int t, const typename Elem<DT>::T* x,
+                             const typename Elem<DT>::T* a, float gm) {
+  if (g.rank_mode == RANK_RANDOM) {
+    const unsigned long long key =
+        splitmix64(g.seed_rank ^ ((unsigned long long)(side + 1) << 60) ^ ((unsigned long long)h << 40) ^
+                   (unsigned long long)t);
+    return (double)(key >> 11) * 0x1p-53;
+  }
+  constexpr int PER = 16 / sizeof(typename Elem<DT>::T);
+  double d = 0.0, xx = 0.0, nn = 0.0;
+  for (int c = 0; c < AKV_D / PER; ++c) {
+    const uint4 xv = ((const uint4*)x)[c], av = ((const uint4*)a)[c];
+#pragma unroll
+    for (int e = 0; e < PER; ++e) {
+      const float xf = Elem<DT>::get(&xv, e), af = Elem<DT>::get(&av, e);
+      if (g.rank_mode == RANK_COSINE) {
+        d = fma((double)xf, (double)af, d);
+        xx = fma((double)xf, (double)xf, xx);
+        nn = fma((double)af, (double)af, nn);
+      } else {
+        const float p = gm * af;
+        const float r = xf - p;
+        d = fma((double)r, (double)r, d);
+      }
+    }
+  }
+  if (g.rank_mode != RANK_COSINE) return d;
+  const double den = __dsqrt_rn(xx * nn);
+  return den > 0.0 ? 1.0 - fabs(d) / den : 1.0;
+}
+
+// Relative and absolute slack of the fp32 selector score against its fp64
+// value (logit error of fp32 MFMA dots, fp32 exp and sums; the absolute part
+// covers terms that underflow in fp32).
+constexpr float ATT_REL = 1e-2f;
+constexpr float ATT_ABS = 1e-30f;
+
+// Replaces the utilities of the non-anchor positions (u >= 0) by the key of
+// the configured ranking: its fp32 rounding and an fp32 interval around the
+// exact value.  Thread = position, grid = (request, head, 256 positions).
+template <int DT>
+__global__ __launch_bounds__(256) void k_rankkeys(Geo g, Ws w, Cache c, const void* Kin, const void* Vin) {
+  using E = typename Elem<DT>::T;
+  int idx = blockIdx.x, b = 0;
+  for (; b < g.B; ++b) {
+    const int n = g.H * ((g.S[b] + 255) / 256);
+    if (idx < n) break;
+    idx -= n;
+  }
+  const int S = g.S[b], k = g.k[b], P = S - g.W;
+  const int nc = (S + 255) / 256, h = idx / nc, t = (idx % nc) * 256 + threadIdx.x;
+  if (t >= S) return;
+  const size_t TS = (size_t)g.prefS[g.B] * g.H;
+  const size_t po = (size_t)g.prefS[b] * g.H + (size_t)h * S;
+  const size_t ko = (size_t)g.prefK[b] * g.H + (size_t)h * k;
+  for (int side = 0; side < 2; ++side) {
+    const size_t e = side * TS + po + t;
+    if (!(w.u[e] >= 0.0f)) continue;  // anchor
+    float u, lo, hi;
+    if (g.rank_mode == RANK_ATTENTION) {
+      const float sc = t < P ? w.sc[po + t] : 0.0f;
+      u = sc;
+      lo = fmaxf(sc * (1.0f - ATT_REL) - ATT_ABS, 0.0f);
+      hi = sc * (1.0f + ATT_REL) + ATT_ABS;
+      if (t >= P) lo = hi = 0.0f;
+    } else {
+      const int a = min(max(w.apos[e], 0), k - 1);
+      const E* x = (const E*)(side ? Vin : Kin) + (po + t) * AKV_D;
+      const E* ar = (const E*)(side ? c.ancV : c.ancK) + (ko + a) * AKV_D;
+      const double key = rank_key64<DT>(g, side, h, t, x, ar, w.gpos[e]);
+      u = __double2float_rn(key);
+      lo = __double2float_rd(key);
+      hi = __double2float_ru(key);
+    }
+    w.u[e] = u;
+    w.uL[e] = lo;
+    w.uU[e] = hi;
+  }
 }
 
 __global__ __launch_bounds__(256) void k_bhist(Geo g, Ws w) {
   __shared__ uint32_t hist[SEL_NBIN];
   int idx = blockIdx.x;
-  const int b = locate_b(g, idx);
+  const int L = locate_l(g, idx);
   const int side = idx & 1, ch = idx >> 1;
-  if (bmode(g, b, side) != 0) return;
+  const BList q = blist(g, L);
+  if (bmode(g, q, side) != 0) return;
   for (int i = threadIdx.x; i < SEL_NBIN; i += blockDim.x) hist[i] = 0;
   __syncthreads();
-  const int n = g.H * g.S[b];
-  const float* u = butil(g, w, b, side);
+  const int n = q.n;
+  const float* u = w.u + bbase(g, q, side);
   const int e0 = ch * BCHUNK, e1 = min(n, e0 + BCHUNK);
   for (int e = e0 + threadIdx.x; e < e1; e += blockDim.x) {
     const float v = u[e];
     if (v >= 0.0f) atomicAdd(&hist[__float_as_uint(v) >> 20], 1u);
   }
   __syncthreads();
-  uint32_t* gh = w.bhist + (size_t)(b * 2 + side) * SEL_NBIN;
+  uint32_t* gh = w.bhist + (size_t)(L * 2 + side) * SEL_NBIN;
   for (int i = threadIdx.x; i < SEL_NBIN; i += blockDim.x)
     if (hist[i]) atomicAdd(&gh[i], hist[i]);
 }
@@ -95,17 +219,18 @@ __global__ __launch_bounds__(256) void k_bcand(Geo g, Ws w) {
   __shared__ int tmp[8], pick[2];
   static_assert(BCHUNK % 256 == 0, "whole rounds of 256 elements per chunk");
   int idx = blockIdx.x;
-  const int b = locate_b(g, idx);
+  const int L = locate_l(g, idx);
   const int side = idx & 1, ch = idx >> 1;
-  if (bmode(g, b, side) != 0) return;
-  const int bs = b * 2 + side;
+  const BList q = blist(g, L);
+  if (bmode(g, q, side) != 0) return;
+  const int bs = L * 2 + side;
   const uint32_t* gh = w.bhist + (size_t)bs * SEL_NBIN;
   for (int i = threadIdx.x; i < SEL_NBIN; i += blockDim.x) hist[i] = gh[i];
   __syncthreads();
-  digit_pick(hist, SEL_NBIN, nside(g, b, side), true, tmp, pick);
+  digit_pick(hist, SEL_NBIN, nside(g, q, side), true, tmp, pick);
   const uint32_t bin1 = (uint32_t)pick[0];
-  const int n = g.H * g.S[b];
-  const float* u = butil(g, w, b, side);
+  const int n = q.n;
+  const float* u = w.u + bbase(g, q, side);
   float* cv = w.bcval + (size_t)bs * BCMAX;
   int32_t* cp = w.bcpos + (size_t)bs * BCMAX;
   const int e0 = ch * BCHUNK, e1 = min(n, e0 + BCHUNK);
@@ -134,13 +259,14 @@ __global__ __launch_bounds__(256) void k_bcand(Geo g, Ws w) {
 __global__ __launch_bounds__(1024) void k_bcut(Geo g, Ws w, Cache c) {
   __shared__ uint32_t hist[SEL_NBIN];
   __shared__ int tmp[20], pick[2];
-  const int bs = blockIdx.x, b = bs >> 1, side = bs & 1;
-  const int n = g.H * g.S[b];
-  const int nch = (n + BCHUNK - 1) / BCHUNK;
-  int32_t* tc = w.tiecnt + 2 * g.prefBC[b] + side * nch;
+  const int bs = blockIdx.x, L = bs >> 1, side = bs & 1;
+  const BList q = blist(g, L);
+  const int n = q.n;
+  const int nch = q.nch;
+  int32_t* tc = btie(g, w, L, q, side);
   int32_t* st = w.bstate + bs * BST_N;
-  if (bmode(g, b, side) != 0) return;
-  const int N = nside(g, b, side);
+  if (bmode(g, q, side) != 0) return;
+  const int N = nside(g, q, side);
   const uint32_t* gh = w.bhist + (size_t)bs * SEL_NBIN;
   for (int i = threadIdx.x; i < SEL_NBIN; i += blockDim.x) hist[i] = gh[i];
   __syncthreads();
@@ -158,7 +284,7 @@ __global__ __launch_bounds__(1024) void k_bcut(Geo g, Ws w, Cache c) {
   const int nc = st[0];
   const float* cv = w.bcval + (size_t)bs * BCMAX;
   const int32_t* cp = w.bcpos + (size_t)bs * BCMAX;
-  const float* u = butil(g, w, b, side);
+  const float* u = w.u + bbase(g, q, side);
   // Anchors carry -1 (sign bit set): they never match a prefix of a
   // non-negative utility.
   for (int pass = 0; pass < 2; ++pass) {
@@ -218,13 +344,14 @@ __global__ __launch_bounds__(1024) void k_bcut(Geo g, Ws w, Cache c) {
 __global__ __launch_bounds__(256) void k_bbound(Geo g, Ws w) {
   __shared__ unsigned red[2][4];
   int idx = blockIdx.x;
-  const int b = locate_b(g, idx);
+  const int L = locate_l(g, idx);
   const int side = idx & 1, ch = idx >> 1;
-  if (bmode(g, b, side) != 0) return;
-  const int bs = b * 2 + side;
+  const BList q = blist(g, L);
+  if (bmode(g, q, side) != 0) return;
+  const int bs = L * 2 + side;
   const uint32_t T = (uint32_t)w.bstate[bs * BST_N + BST_T];
-  const int n = g.H * g.S[b];
-  const size_t base = (size_t)side * g.H * g.prefS[g.B] + (size_t)g.prefS[b] * g.H;
+  const int n = q.n;
+  const size_t base = bbase(g, q, side);
   const int e0 = ch * BCHUNK, e1 = min(n, e0 + BCHUNK);
   unsigned amin = 0x7F800000u, bmax = 0u;
   for (int e = e0 + threadIdx.x; e < e1; e += blockDim.x) {
@@ -259,18 +386,18 @@ __global__ __launch_bounds__(256) void k_bmark(Geo g, Ws w) {
   __shared__ int wtot[4];
   __shared__ int tmp[8];
   int idx = blockIdx.x;
-  const int b = locate_b(g, idx);
+  const int L = locate_l(g, idx);
   const int side = idx & 1, ch = idx >> 1;
-  const int bs = b * 2 + side;
+  const BList q = blist(g, L);
+  const int bs = L * 2 + side;
   int32_t* st = w.bstate + bs * BST_N;
-  const int mode = bmode(g, b, side);
+  const int mode = bmode(g, q, side);
   const uint32_t T = (uint32_t)st[BST_T];
   const int need = st[BST_REMAIN];
   const uint32_t A = (uint32_t)st[BST_A], Bb = (uint32_t)st[BST_B];
-  const int n = g.H * g.S[b];
-  const int nch = (n + BCHUNK - 1) / BCHUNK;
-  const int32_t* tc = w.tiecnt + 2 * g.prefBC[b] + side * nch;
-  const size_t base = (size_t)side * g.H * g.prefS[g.B] + (size_t)g.prefS[b] * g.H;
+  const int n = q.n;
+  const int32_t* tc = btie(g, w, L, q, side);
+  const size_t base = bbase(g, q, side);
   const float* u = w.u + base;
   uint8_t* sel = w.sel + base;
   const int e0 = ch * BCHUNK, e1 = min(n, e0 + BCHUNK);
@@ -344,7 +471,9 @@ __global__ __launch_bounds__(256) void k_bmark(Geo g, Ws w) {
 // ...) the sequential fp64 dots l = q_w.k_t / sqrt(D), alpha = exp(l - M_w) /
 // Z_w, and for keys q_w.r and ||v_t - y_w||^2, for values ||r||^2; the row
 // terms alpha^2 (q.r)^2 / D ||v - y||^2 (or alpha^2 ||r||^2) summed in row
-// order and divided by m.
+// order and divided by m.  The ATTENTION ranking sums alpha itself (the raw
+// selector score, 0 inside the window); the other ablation keys come from
+// rank_key64 on one lane.
 template <int DT>
 __global__ __launch_bounds__(256) void k_brescore(Geo g, Ws w, Cache c, const void* Kin, const void* Vin,
                                                   const void* Qin) {
@@ -358,16 +487,18 @@ __global__ __launch_bounds__(256) void k_brescore(Geo g, Ws w, Cache c, const vo
   const size_t TS = (size_t)g.prefS[g.B] * g.H;
   const double sqd = sqrt((double)D);
   int base = 0;  // members of the earlier lists
-  for (int bs = 0; bs < 2 * g.B; ++bs) {
-    const int b = bs >> 1, side = bs & 1;
+  for (int bs = 0; bs < 2 * g.B * g.hdiv; ++bs) {
+    const int L = bs >> 1, side = bs & 1;
+    const BList bl = blist(g, L);
+    const int b = bl.b;
     const int nl = w.bstate[bs * BST_N + BST_NBAND];
-    const int n = (bmode(g, b, side) == 0 && nl <= BAND_CAP) ? nl : 0;
+    const int n = (bmode(g, bl, side) == 0 && nl <= BAND_CAP) ? nl : 0;
     int i0 = gw - base;
     if (i0 < 0) i0 += ((-i0 + nw - 1) / nw) * nw;
     for (int i = i0; i < n; i += nw) {
       const int S = g.S[b], k = g.k[b];
       const int f = w.bandpos[(size_t)bs * BAND_CAP + i];
-      const int h = f / S, t = f % S;
+      const int h = bl.h0 + f / S, t = f % S;
       const size_t po = (size_t)g.prefS[b] * g.H + (size_t)h * S;
       const size_t ko = (size_t)g.prefK[b] * g.H + (size_t)h * k;
       const size_t xo = (po + t) * D;
@@ -377,6 +508,11 @@ __global__ __launch_bounds__(256) void k_brescore(Geo g, Ws w, Cache c, const vo
       const E* ar = (const E*)(side ? c.ancV : c.ancK) + (ko + a) * D;
       const E* kr = (const E*)Kin + xo;
       const E* vr = (const E*)Vin + xo;
+      const bool att = g.rank_mode == RANK_ATTENTION;
+      if ((g.rank_mode != RANK_UTILITY && !att) || (att && t >= S - g.W)) {  // uniform per wave
+        if (lane == 0) w.bandu[(size_t)bs * BAND_CAP + i] = att ? 0.0 : rank_key64<DT>(g, side, h, t, xr, ar, gm);
+        continue;
+      }
       for (int j = lane; j < D; j += 64) {
         const float p = gm * Elem<DT>::get(ar, j);
         rs[wave][j] = Elem<DT>::get(xr, j) - p;
@@ -412,7 +548,9 @@ __global__ __launch_bounds__(256) void k_brescore(Geo g, Ws w, Cache c, const vo
         const double al = exp(l - w.M64[bh * m + wr]) / w.Z64[bh * m + wr];
         const double a2 = al * al;
         double term;
-        if (side == 0) {
+        if (att) {
+          term = al;
+        } else if (side == 0) {
           const double4* y4 = (const double4*)(w.Y64 + (bh * m + wr) * D);
           double vy = 0.0;
           double4 yc = y4[0];
@@ -457,10 +595,11 @@ __global__ __launch_bounds__(RANK_T) void k_brank(Geo g, Ws w) {
   __shared__ double su[RANK_T];
   __shared__ int sp[RANK_T];
   int tile0 = 0;
-  for (int bs = 0; bs < 2 * g.B; ++bs) {
-    const int b = bs >> 1, side = bs & 1;
+  for (int bs = 0; bs < 2 * g.B * g.hdiv; ++bs) {
+    const int side = bs & 1;
+    const BList bl = blist(g, bs >> 1);
     const int nl = w.bstate[bs * BST_N + BST_NBAND];
-    const int n = (bmode(g, b, side) == 0 && nl <= BAND_CAP) ? nl : 0;
+    const int n = (bmode(g, bl, side) == 0 && nl <= BAND_CAP) ? nl : 0;
     const int nt = (n + RANK_T - 1) / RANK_T;
     const int32_t* bp = w.bandpos + (size_t)bs * BAND_CAP;
     const double* bu = w.bandu + (size_t)bs * BAND_CAP;
@@ -489,27 +628,36 @@ __global__ __launch_bounds__(RANK_T) void k_brank(Geo g, Ws w) {
 }
 
 __global__ __launch_bounds__(256) void k_bsel(Geo g, Ws w, Cache c) {
-  const int bs = blockIdx.y, b = bs >> 1, side = bs & 1;
-  if (bmode(g, b, side) != 0) return;
+  const int bs = blockIdx.y, side = bs & 1;
+  const BList bl = blist(g, bs >> 1);
+  if (bmode(g, bl, side) != 0) return;
   const int n = w.bstate[bs * BST_N + BST_NBAND];
   if (blockIdx.x == 0 && threadIdx.x == 0) {
-    c.stats[b * 4 + 2 + side] = n;  // band size, reported by the export
+    atomicAdd(&c.stats[bl.b * 4 + 2 + side], n);  // band size (summed over heads), reported by the export
     if (n > BAND_CAP) atomicOr(&c.header[2], HDR_BAND_OVERFLOW);
   }
   if (n > BAND_CAP) return;
   const int need = w.bstate[bs * BST_N + BST_NEED];
-  uint8_t* sel = w.sel + (size_t)side * g.H * g.prefS[g.B] + (size_t)g.prefS[b] * g.H;
+  uint8_t* sel = w.sel + bbase(g, bl, side);
   for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x)
     sel[w.bandpos[(size_t)bs * BAND_CAP + i]] = w.brank[(size_t)bs * BAND_CAP + i] < need ? 1 : 0;
 }
 
 hipError_t launch_budget(const Geo& g, const Ws& w, const Cache& c, const void* K, const void* V, const void* Q,
                          hipStream_t st) {
-  int nblk = 0;
-  for (int b = 0; b < g.B; ++b) nblk += 2 * ((g.H * g.S[b] + BCHUNK - 1) / BCHUNK);
+  int nblk = 0, nkey = 0;
+  const int nl = g.B * g.hdiv;
+  for (int L = 0; L < nl; ++L) nblk += 2 * (((g.H / g.hdiv) * g.S[L / g.hdiv] + BCHUNK - 1) / BCHUNK);
+  for (int b = 0; b < g.B; ++b) nkey += g.H * ((g.S[b] + 255) / 256);
+  if (g.rank_mode != RANK_UTILITY) {
+    if (g.dtype == 1)
+      launch("k_rankkeys", k_rankkeys<1>, dim3(nkey), dim3(256), 0, st, g, w, c, K, V);
+    else
+      launch("k_rankkeys", k_rankkeys<0>, dim3(nkey), dim3(256), 0, st, g, w, c, K, V);
+  }
   launch("k_bhist", k_bhist, dim3(nblk), dim3(256), 0, st, g, w);
   launch("k_bcand", k_bcand, dim3(nblk), dim3(256), 0, st, g, w);
-  launch("k_bcut", k_bcut, dim3(g.B * 2), dim3(1024), 0, st, g, w, c);
+  launch("k_bcut", k_bcut, dim3(nl * 2), dim3(1024), 0, st, g, w, c);
   launch("k_bbound", k_bbound, dim3(nblk), dim3(256), 0, st, g, w);
   launch("k_bmark", k_bmark, dim3(nblk), dim3(256), 0, st, g, w);
   if (g.dtype == 1)
@@ -517,7 +665,7 @@ hipError_t launch_budget(const Geo& g, const Ws& w, const Cache& c, const void* 
   else
     launch("k_brescore", k_brescore<0>, dim3(1024), dim3(256), 0, st, g, w, c, K, V, Q);
   launch("k_brank", k_brank, dim3(2048), dim3(RANK_T), 0, st, g, w);
-  launch("k_bsel", k_bsel, dim3(64, g.B * 2), dim3(256), 0, st, g, w, c);
+  launch("k_bsel", k_bsel, dim3(64, nl * 2), dim3(256), 0, st, g, w, c);
   return hipGetLastError();
 }
 

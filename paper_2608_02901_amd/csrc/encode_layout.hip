@@ -405,8 +405,12 @@ __global__ __launch_bounds__(256) void k_codec(Geo g, Ws w, Cache c, const void*
       if (bit[q] < 0) break;
       const float p0 = gq[q] * a0[q], p1 = gq[q] * a1[q];
       const float r0 = x0[q] - p0, r1 = x1[q] - p1;
-      float z0 = s0 * r0, z1 = s1 * r1;
-      fwht_wave_dpp(z0, z1, lane);
+      float z0 = r0, z1 = r1;
+      if (g.rot) {  // randomized Hadamard rotation (uniform branch)
+        z0 = s0 * r0;
+        z1 = s1 * r1;
+        fwht_wave_dpp(z0, z1, lane);
+      }
       // Group scale (G coordinates = G/2 lanes).
       const int gl = G / 2;
       float sigma;
@@ -426,9 +430,9 @@ __global__ __launch_bounds__(256) void k_codec(Geo g, Ws w, Cache c, const void*
       } else {
         float am = fmaxf(fabsf(z0), fabsf(z1));
         for (int o = 1; o < gl; o <<= 1) am = fmaxf(am, __shfl_xor(am, o, 64));
-        sigma = g.scale_mode == 1 ? am : am / AKV_L1;
+        sigma = g.scale_mode == 1 ? am : (g.scale_mode == 3 ? am * 0.25f : am / AKV_L1);
       }
-      const float T = sigma * AKV_T;
+      const float T = sigma * g.thr;
       const int c0 = z0 < 0.0f ? (fabsf(z0) > T ? 0 : 1) : (fabsf(z0) > T ? 3 : 2);
       const int c1 = z1 < 0.0f ? (fabsf(z1) > T ? 0 : 1) : (fabsf(z1) > T ? 3 : 2);
       const int nib = c0 | (c1 << 2);

@@ -46,7 +46,8 @@ def oracle_encode(cfg, layer, b, anchor_override=None):
     return R.encode(K, V, Q, W=cfg.window, k=k, rho=float(np.float32(cfg.rho)), kappa=cfg.kappa,
                     bf16=cfg.dtype == N.BF16, seed=cfg.seed, budget_mode=cfg.budget_mode,
                     budget=float(np.float32(cfg.budget)), budget_count=cfg.budget_count, G=G,
-                    scale_mode=cfg.scale_mode, anchor_override=anchor_override)
+                    scale_mode=cfg.scale_mode, anchor_override=anchor_override, rank_mode=cfg.rank_mode,
+                    head_budget=cfg.head_budget)
 
 
 def plan_k(cfg, S):

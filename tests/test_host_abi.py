@@ -61,6 +61,10 @@ def _cfg(**kw):
     (dict(anchor_count=16, anchor_frac=0.0), N.ERR_INVALID_ARG),  # k < W
     (dict(window=64, num_q_heads=64), N.ERR_UNSUPPORTED),         # m = 512
     (dict(dtype=7), N.ERR_INVALID_ARG),
+    (dict(scale_mode=4), N.ERR_INVALID_ARG),
+    (dict(rank_mode=5), N.ERR_INVALID_ARG),
+    (dict(rank_mode=-1), N.ERR_INVALID_ARG),
+    (dict(head_budget=2), N.ERR_INVALID_ARG),
 ])
 def test_plan_rejects_bad_configs(kw, status):
     _lib_or_skip()
@@ -108,6 +112,22 @@ def test_budget_caps_at_candidate_count():
     p = N.Plan(_cfg(budget_mode=N.BUDGET_COUNT, budget_count=10 ** 9), [1000])
     ri = p.requests[0]
     assert ri.residuals_k == 8 * (1000 - ri.anchors)
+
+
+def test_equal_per_head_budgets_in_the_plan():
+    """Equal per-head budgets (Sec. 4.3 ablation): every head gets floor(N / H)
+    of the pooled count, so the request holds H * floor(N / H) per side; the
+    per-(request, head) budget lists are limited to 64."""
+    _lib_or_skip()
+    pooled = N.Plan(_cfg(), [5000]).requests[0]
+    per = N.Plan(_cfg(head_budget=1), [5000]).requests[0]
+    assert per.residuals_k == pooled.residuals_k // 8 * 8 and per.residuals_v == pooled.residuals_v // 8 * 8
+    N.Plan(_cfg(head_budget=1), [4096] * 8)  # 64 lists
+    with pytest.raises(N.AnchorKVError) as e:
+        N.Plan(_cfg(head_budget=1), [4096] * 9)
+    assert e.value.status == N.ERR_UNSUPPORTED
+    for mode in (N.RANK_COSINE, N.RANK_RESNORM, N.RANK_ATTENTION, N.RANK_RANDOM):
+        assert N.Plan(_cfg(rank_mode=mode), [5000]).requests[0].residuals_k == pooled.residuals_k
 
 
 def test_buffer_sizes_grow_with_batch():
