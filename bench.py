@@ -152,6 +152,108 @@ def cpu_baseline(wl, seed, Ss=32768, nsteps=8):
                 encode_s=round(t_enc, 3))
 
 
+def fidelity(args):
+    """Attention-output fidelity of the method and its ablations at the paper's
+    operating point (App. D; Sec. 4.3): W = 32, k = S/128, rho = 0.7,
+    kappa = 7, residual count from the byte budget at theta = 0.05 (20x),
+    bf16.  For every variant and every (layer, query head, decode query) cell:
+    cos(y, y_hat) between decode attention over the compressed cache and
+    exact fp32 attention over the original keys and values.  Two query
+    regimes: the workload's N(0, I) queries, and focused queries aimed at a
+    few context tokens (observation queries foreshadowing the decode ones).
+    Also the share of each KV head in the pooled residual budget (App. D,
+    "where the residual budget goes").  Prints one JSON line."""
+    import numpy as np
+    import torch
+
+    import paper_2608_02901_amd as akv
+    import synth
+    from paper_2608_02901_amd import _native as N
+
+    torch.cuda.set_device(0)
+    S, nq, nl = args.fid_len, args.fid_queries, args.fid_layers
+    wl = synth.Workload("llama8b-fidelity", H=8, Hq=32, D=128, seq_lens=[S], dtype="bf16",
+                        anchor_count=S // 128, n_centers=512, steps=nq, seed=7)
+    theta = 0.05
+    base = dict(num_kv_heads=wl.H, num_q_heads=wl.Hq, head_dim=wl.D, window=32, anchor_count=S // 128, rho=0.7,
+                kappa=7, budget_mode=N.BUDGET_THETA, budget=theta, dtype=N.BF16, seed=wl.seed)
+
+    def residuals(**kw):
+        ri = N.Plan(N.Config.make(**dict(base, **kw)), [S]).requests[0]
+        return ri.residuals_k + ri.residuals_v
+
+    # "no residuals": the largest anchor count whose fixed bytes still fit the
+    # byte budget, and no residual
+    lo, hi = S // 128, min(S, 16384)
+    while lo < hi:
+        mid = (lo + hi + 1) // 2
+        if residuals(anchor_count=mid) >= 1:
+            lo = mid
+        else:
+            hi = mid - 1
+    k_nores = lo
+    variants = {
+        "anchorkv": {},
+        "rank_cosine": dict(rank_mode=N.RANK_COSINE),
+        "rank_resnorm": dict(rank_mode=N.RANK_RESNORM),
+        "rank_attention": dict(rank_mode=N.RANK_ATTENTION),
+        "rank_random": dict(rank_mode=N.RANK_RANDOM),
+        "attention_only_anchors": dict(rho=1.0),
+        "equal_head_budgets": dict(head_budget=1),
+        "no_residuals": dict(anchor_count=k_nores, budget_mode=N.BUDGET_COUNT, budget_count=0),
+        "naive_2bit": dict(scale_mode=N.SCALE_NAIVE),
+    }
+    plans = {name: N.Plan(N.Config.make(**dict(base, **kw)), [S]) for name, kw in variants.items()}
+    ri = plans["anchorkv"].requests[0]
+    log(f"fidelity: S={S} k={ri.anchors} N_K={ri.residuals_k} N_V={ri.residuals_v} "
+        f"no-residual k={k_nores} layers={nl} queries={nq}")
+    cos = {r: {v: [] for v in variants} for r in ("iid", "focused")}
+    share = []
+    g = wl.Hq // wl.H
+    for l in range(nl):
+        lay = synth.make_layer(wl, device="cuda", seed=wl.seed + 100 * l, steps=nq)
+        KfT, Vf = lay.K[0].float().transpose(1, 2).contiguous(), lay.V[0].float()
+        Qf, qf = synth.focused_queries(wl, lay.K, nq, seed=wl.seed + 100 * l + 1)
+        for regime, Qobs, q in (("iid", lay.Qobs[0], lay.q), ("focused", Qf[0], qf)):
+            # exact attention in fp32: [steps][Hq][D]
+            qq = q[:, 0].float().reshape(nq, wl.H, g, wl.D).permute(1, 0, 2, 3).reshape(wl.H, nq * g, wl.D)
+            logit = torch.matmul(qq.contiguous(), KfT) / math.sqrt(wl.D)
+            ref = torch.matmul(torch.softmax(logit, dim=-1), Vf)
+            ref = ref.reshape(wl.H, nq, g, wl.D).permute(1, 0, 2, 3).reshape(nq, wl.Hq, wl.D)
+            del logit
+            for name, plan in plans.items():
+                cache, ws, dws = plan.alloc("cuda")
+                akv.encode(plan, [lay.K[0]], [lay.V[0]], [Qobs.contiguous()], cache, ws)
+                out = torch.empty(1, wl.Hq, wl.D, dtype=torch.float32, device="cuda")
+                for s in range(nq):
+                    akv.decode_attn(plan, cache, q[s], out, dws)
+                    c = torch.nn.functional.cosine_similarity(out[0].double(), ref[s].double(), dim=-1)
+                    cos[regime][name].append(c.cpu().numpy())
+                if name == "anchorkv" and regime == "focused":
+                    ex = akv.export(plan, cache.cpu().numpy(), 0, 0)
+                    sh = [ex["sel_" + sd].reshape(wl.H, -1).sum(1) for sd in "kv"]
+                    share.append([(x / max(int(x.sum()), 1)).round(4).tolist() for x in sh])
+                del cache, ws, dws
+        log(f"fidelity layer {l} done")
+        del lay, KfT, Vf
+
+    def summary(c):
+        c = np.concatenate(c)
+        return {"cells": int(c.size), "frac_cos_below_0.9": round(float((c < 0.9).mean()), 5),
+                "frac_cos_below_0.99": round(float((c < 0.99).mean()), 5),
+                "cos_p01": round(float(np.quantile(c, 0.01)), 6), "cos_p10": round(float(np.quantile(c, 0.1)), 6),
+                "cos_p50": round(float(np.quantile(c, 0.5)), 6), "mean_1_minus_cos": float(f"{(1 - c).mean():.4g}")}
+
+    M_full = 2 * S * wl.H * wl.D * 2
+    res = {"report": "fidelity", "workload": wl.name, "seq_len": S, "layers": nl, "decode_queries": nq,
+           "theta": theta, "anchors": ri.anchors, "residuals_k": ri.residuals_k, "residuals_v": ri.residuals_v,
+           "cache_bytes": plans["anchorkv"].cache_bytes, "dense_bytes": M_full,
+           "no_residual_anchors": k_nores,
+           "cos": {r: {v: summary(c) for v, c in d.items()} for r, d in cos.items()},
+           "residual_share_per_kv_head_focused": share}
+    print(json.dumps(res), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -160,12 +262,20 @@ def main():
     ap.add_argument("--layers", type=int, default=32)
     ap.add_argument("--decode-steps", type=int, default=64)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--fidelity", action="store_true",
+                    help="attention-output fidelity report of the method and its ablations instead of the benchmark")
+    ap.add_argument("--fid-len", type=int, default=32768)
+    ap.add_argument("--fid-layers", type=int, default=4)
+    ap.add_argument("--fid-queries", type=int, default=8)
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py measures one GPU: this build is a single-GPU hot path (no collectives); "
               "run with --gpus 1", file=sys.stderr)
         sys.exit(2)
+    if args.fidelity:
+        fidelity(args)
+        return
 
     import numpy as np
     import torch

@@ -154,3 +154,35 @@ def make_layer(wl: Workload, device="cpu", seed: Optional[int] = None, steps: Op
                 v_new[:, b, h] = (cv[pick] + wl.sigma * torch.randn(steps, wl.D, generator=gen,
                                                                      device=device)).to(dt)
     return Layer(K, V, Q, q, k_new, v_new)
+
+
+def focused_queries(wl: Workload, K: List[torch.Tensor], steps: int, n_focus: int = 8, tau: float = 0.4,
+                    noise: float = 0.3, seed: int = 0):
+    """Observation and decode queries that attend to a few tokens, as a model's
+    queries attend to what the context is about: per request and KV head,
+    n_focus positions before the window are drawn; every query row is
+    tau * sqrt(D) * (a focus key / its norm) + N(0, noise^2 I), observation row
+    (j, i) of query head j using focus (i + j) mod n_focus and decode step s
+    focus (s + j) mod n_focus, so the window's queries foreshadow the decode
+    queries.  Returns (Qobs per request [Hq][W][D], q [steps][batch][Hq][D]) in
+    the workload dtype, on K's device."""
+    device = K[0].device
+    gen = _gen(device, seed)
+    dt = wl.torch_dtype()
+    g = wl.Hq // wl.H
+    Qs = []
+    q = torch.empty(steps, wl.batch, wl.Hq, wl.D, device=device, dtype=dt)
+    for b, S in enumerate(wl.seq_lens):
+        Qb = torch.empty(wl.Hq, wl.window, wl.D, device=device, dtype=dt)
+        for h in range(wl.H):
+            pos = torch.randint(0, S - wl.window, (n_focus,), generator=gen, device=device)
+            f = K[b][h, pos].float()
+            f = f / f.norm(dim=1, keepdim=True).clamp_min(1e-30) * (tau * math.sqrt(wl.D))
+            for jj in range(g):
+                j = h * g + jj
+                rows = f[(torch.arange(wl.window, device=device) + jj) % n_focus]
+                Qb[j] = (rows + noise * torch.randn(wl.window, wl.D, generator=gen, device=device)).to(dt)
+                rows = f[(torch.arange(steps, device=device) + jj) % n_focus]
+                q[:, b, j] = (rows + noise * torch.randn(steps, wl.D, generator=gen, device=device)).to(dt)
+        Qs.append(Qb)
+    return Qs, q
