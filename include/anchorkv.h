@@ -100,6 +100,13 @@ typedef enum {
   ANCHORKV_BUDGET_COUNT = 2
 } anchorkv_budget_mode;
 
+/* What an appended (generated) token stores (App. E "Generated Tokens"):
+ *   ENCODED : its nearest anchor and coefficient on both sides, no residual
+ *             (8 bytes per KV head at bf16), assigned against the current anchors;
+ *   DENSE   : its key and value exactly, in the cache dtype (the paper's choice:
+ *             generated tokens join the exact window and are never compressed). */
+typedef enum { ANCHORKV_APPEND_ENCODED = 0, ANCHORKV_APPEND_DENSE = 1 } anchorkv_append_mode;
+
 typedef struct anchorkv_config {
   int32_t num_kv_heads;   /* H */
   int32_t num_q_heads;    /* Hq, a multiple of H */
@@ -119,6 +126,7 @@ typedef struct anchorkv_config {
   int32_t rank_mode;      /* an anchorkv_rank_mode; 0 is the method's utilities */
   int32_t head_budget;    /* 0: the budget is pooled over heads (the method); 1: every head gets
                              floor(N_side / H) (Sec. 4.3 ablation; needs batch * H <= 64) */
+  int32_t append_mode;    /* an anchorkv_append_mode */
   uint64_t seed;          /* seeds the uniform anchor share, the Hadamard signs and the random ranking */
 } anchorkv_config;
 
@@ -173,10 +181,11 @@ anchorkv_status anchorkv_encode(const anchorkv_plan* plan, const void* K, const 
                                 size_t workspace_bytes, void* stream);
 
 /* Appends one generated token per request and KV head (config max_append
- * slots).  The token is encoded against the request's existing anchors (its
- * nearest anchor and coefficient, Eqs. nearest-anchor and projection, with the
- * same certified argmax and canonical coefficient as the compression pass) and
- * stores no residual.  n_appended: tokens already appended to this cache
+ * slots).  ENCODED append mode: the token is encoded against the request's
+ * existing anchors (its nearest anchor and coefficient, Eqs. nearest-anchor
+ * and projection, with the same certified argmax and canonical coefficient as
+ * the compression pass) and stores no residual.  DENSE append mode: the key
+ * and value are stored exactly (App. E "Generated Tokens").  n_appended: tokens already appended to this cache
  * (host-tracked), must be < max_append, else ANCHORKV_ERR_CAPACITY.
  * k_new, v_new: device [batch][H][D], dtype, new_bytes the size of each.
  * workspace: device, workspace_bytes >= anchorkv_decode_workspace_bytes(plan),
@@ -243,7 +252,7 @@ anchorkv_status anchorkv_reconstruct(const anchorkv_plan* plan, const void* cach
  *   anchors [H][k] int32; a_X [H][S] int32 anchor index; gamma_X [H][S] fp32
  *   stored coefficient; sel_X [H][S] uint8 residual flag; codes_X [H][S][D/4];
  *   scales_X [H][S][D/G] (zero where no residual); tail_a_X, tail_gamma_X
- *   [H][n_appended]; stats[6]: tokens resolved by the exact fp64 path of the
+ *   [H][n_appended] (-1 and 0 in DENSE append mode); stats[6]: tokens resolved by the exact fp64 path of the
  *   certified argmax, keys then values, then N_K, N_V, then the candidates
  *   whose utility bounds straddled the residual budget's cut and were re-scored
  *   in fp64, keys then values. */

@@ -7,5 +7,5 @@ include/anchorkv.h); this package only binds it.  Build it with
 """
 from ._native import (BF16, BUDGET_COUNT, BUDGET_FRACTION, BUDGET_THETA, F32, SCALE_ABSMAX_LITERAL,  # noqa: F401
                       SCALE_ABSMAX_OUTER, SCALE_RMS, SCALE_NAIVE, RANK_UTILITY, RANK_COSINE, RANK_RESNORM,
-                      RANK_ATTENTION, RANK_RANDOM, AnchorKVError, Config, Plan, append, decode_attn, decode_step,
+                      RANK_ATTENTION, RANK_RANDOM, APPEND_ENCODED, APPEND_DENSE, AnchorKVError, Config, Plan, append, decode_attn, decode_step,
                       decode_step_noalloc, encode, export, last_error, lib, reconstruct, LIB_PATH)

@@ -20,6 +20,7 @@ OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_CAPACITY, ERR_CORRUPT_CACHE, ERR_HIP, 
 F32, BF16 = 0, 1
 SCALE_ABSMAX_OUTER, SCALE_ABSMAX_LITERAL, SCALE_RMS, SCALE_NAIVE = 0, 1, 2, 3
 RANK_UTILITY, RANK_COSINE, RANK_RESNORM, RANK_ATTENTION, RANK_RANDOM = 0, 1, 2, 3, 4
+APPEND_ENCODED, APPEND_DENSE = 0, 1
 BUDGET_FRACTION, BUDGET_THETA, BUDGET_COUNT = 0, 1, 2
 
 EXPORTED = ["anchorkv_plan_create", "anchorkv_plan_destroy", "anchorkv_cache_bytes", "anchorkv_encode_workspace_bytes",
@@ -41,14 +42,17 @@ class Config(ctypes.Structure):
                 ("rho", ctypes.c_float), ("kappa", ctypes.c_int32), ("budget_mode", ctypes.c_int32),
                 ("budget", ctypes.c_float), ("budget_count", ctypes.c_int64), ("quant_group", ctypes.c_int32),
                 ("scale_mode", ctypes.c_int32), ("dtype", ctypes.c_int32), ("max_append", ctypes.c_int32),
-                ("rank_mode", ctypes.c_int32), ("head_budget", ctypes.c_int32), ("seed", ctypes.c_uint64)]
+                ("rank_mode", ctypes.c_int32), ("head_budget", ctypes.c_int32), ("append_mode", ctypes.c_int32),
+                ("seed", ctypes.c_uint64)]
 
     @classmethod
     def make(cls, *, num_kv_heads, num_q_heads, head_dim=128, window=32, anchor_count=0, anchor_frac=0.0,
              rho=0.7, kappa=7, budget_mode=BUDGET_FRACTION, budget=0.05, budget_count=0, quant_group=0,
-             scale_mode=SCALE_ABSMAX_OUTER, dtype=BF16, max_append=0, rank_mode=RANK_UTILITY, head_budget=0, seed=0):
+             scale_mode=SCALE_ABSMAX_OUTER, dtype=BF16, max_append=0, rank_mode=RANK_UTILITY, head_budget=0,
+             append_mode=APPEND_ENCODED, seed=0):
         return cls(num_kv_heads, num_q_heads, head_dim, window, anchor_count, anchor_frac, rho, kappa, budget_mode,
-                   budget, budget_count, quant_group, scale_mode, dtype, max_append, rank_mode, head_budget, seed)
+                   budget, budget_count, quant_group, scale_mode, dtype, max_append, rank_mode, head_budget,
+                   append_mode, seed)
 
 
 class RequestInfo(ctypes.Structure):

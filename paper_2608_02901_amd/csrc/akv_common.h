@@ -31,6 +31,7 @@ struct Geo {
   float lev0, lev1, thr;        // codec levels (in units of the scale) and threshold
   int rank_mode;                // residual ranking key (anchorkv_rank_mode)
   int hdiv;                     // budget lists per request and side: H (equal per-head budgets) or 1
+  int dense_tail;               // appended tokens are stored exactly (1) or encoded (0)
   unsigned long long seed_rank; // random ranking
   int maxS, maxK;
   unsigned long long seed_anchor, seed_sign;
@@ -130,6 +131,8 @@ struct Cache {
   uint16_t* tidxV;
   void* tgK;
   void* tgV;
+  void* tkd;            // [b][h][max_append][D] dtype, appended keys stored exactly (dense tail)
+  void* tvd;            // [b][h][max_append][D] appended values
   int32_t* stats;       // [b][4]
 };
 

@@ -103,7 +103,7 @@ struct anchorkv_plan {
   std::vector<anchorkv_request_info> req;
   // cache blob offsets
   size_t c_header, c_anc_pos, c_ancK, c_ancV, c_nrmK, c_nrmV, c_invK, c_invV, c_idxK, c_idxV, c_gK, c_gV, c_pos,
-      c_maskK, c_maskV, c_pcK, c_pcV, c_codesK, c_codesV, c_scalesK, c_scalesV, c_tidxK, c_tidxV, c_tgK, c_tgV,
+      c_maskK, c_maskV, c_pcK, c_pcV, c_codesK, c_codesV, c_scalesK, c_scalesV, c_tidxK, c_tidxV, c_tgK, c_tgV, c_tkd, c_tvd,
       c_stats;
   size_t cache_bytes;
   // encode workspace offsets
@@ -158,6 +158,8 @@ extern "C" anchorkv_status anchorkv_plan_create(const anchorkv_config* cfg, int3
   if (c.scale_mode < 0 || c.scale_mode > 3) return fail(ANCHORKV_ERR_INVALID_ARG, "bad scale_mode");
   if (c.rank_mode < 0 || c.rank_mode > 4) return fail(ANCHORKV_ERR_INVALID_ARG, "bad rank_mode");
   if (c.head_budget != 0 && c.head_budget != 1) return fail(ANCHORKV_ERR_INVALID_ARG, "head_budget must be 0 or 1");
+  if (c.append_mode != ANCHORKV_APPEND_ENCODED && c.append_mode != ANCHORKV_APPEND_DENSE)
+    return fail(ANCHORKV_ERR_INVALID_ARG, "bad append_mode");
   if (c.head_budget && (int64_t)batch * c.num_kv_heads > AKV_MAXB)
     return fail(ANCHORKV_ERR_UNSUPPORTED, "equal per-head budgets need batch * num_kv_heads <= 64");
   if (c.budget_mode < 0 || c.budget_mode > 2) return fail(ANCHORKV_ERR_INVALID_ARG, "bad budget_mode");
@@ -198,6 +200,7 @@ extern "C" anchorkv_status anchorkv_plan_create(const anchorkv_config* cfg, int3
   geo.rank_mode = c.rank_mode;
   geo.hdiv = c.head_budget ? c.num_kv_heads : 1;
   geo.seed_rank = mix64(c.seed ^ 3ull);
+  geo.dense_tail = c.append_mode == ANCHORKV_APPEND_DENSE;
   geo.max_append = c.max_append;
   geo.seed_anchor = mix64(c.seed ^ 1ull);
   geo.seed_sign = mix64(c.seed ^ 2ull);
@@ -350,6 +353,9 @@ extern "C" anchorkv_status anchorkv_plan_create(const anchorkv_config* cfg, int3
   p->c_tidxV = L.add(2 * batch * H * cap);
   p->c_tgK = L.add(esz * batch * H * cap);
   p->c_tgV = L.add(esz * batch * H * cap);
+  const size_t dcap = geo.dense_tail ? (size_t)cap : 0;
+  p->c_tkd = L.add(esz * batch * H * dcap * D);
+  p->c_tvd = L.add(esz * batch * H * dcap * D);
   p->c_stats = L.add(4 * 4 * batch);
   p->cache_bytes = L.total;
 
@@ -461,6 +467,8 @@ static akv::Cache cache_ptrs(const anchorkv_plan* p, void* base) {
   c.tidxV = at<uint16_t>(base, p->c_tidxV);
   c.tgK = at<void>(base, p->c_tgK);
   c.tgV = at<void>(base, p->c_tgV);
+  c.tkd = at<void>(base, p->c_tkd);
+  c.tvd = at<void>(base, p->c_tvd);
   c.stats = at<int32_t>(base, p->c_stats);
   return c;
 }
@@ -777,8 +785,9 @@ extern "C" anchorkv_status anchorkv_export(const anchorkv_plan* p, const void* c
     for (int h = 0; h < H; ++h)
       for (int n = 0; n < n_appended; ++n) {
         const size_t ti = ((size_t)b * H + h) * g.max_append + n;
-        if (ta) ta[(size_t)h * n_appended + n] = tidx[ti];
-        if (tg) tg[(size_t)h * n_appended + n] = coef_host(tgm, ti, g.dtype);
+        // a dense tail stores the tokens themselves: no anchor, no coefficient
+        if (ta) ta[(size_t)h * n_appended + n] = g.dense_tail ? -1 : tidx[ti];
+        if (tg) tg[(size_t)h * n_appended + n] = g.dense_tail ? 0.0f : coef_host(tgm, ti, g.dtype);
       }
   }
   if (o->stats) {

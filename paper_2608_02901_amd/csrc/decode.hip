@@ -712,6 +712,144 @@ __device__ void tail_block(const Geo& g, const Cache& c, const DecWs& dw, int bh
   }
 }
 
+// The appended tokens of one (request, KV head) when they are stored exactly
+// (App. E "Generated Tokens"): one more split record per query head of the
+// group with the exact logits sl2 q_j . k_n (fp32, sequential over the
+// coordinates) and the exact values.  When this step appends (kin !=
+// nullptr), the token is written to tail slot n_app and attended straight
+// from kin / vin.
+template <int DT, int GQ>
+__device__ void tail_dense(const Geo& g, const Cache& c, const DecWs& dw, int bh, int n_app, const void* kin,
+                           const void* vin, const void* q, float sl2, unsigned char* pool) {
+  using E = typename Elem<DT>::T;
+  constexpr int D = AKV_D, TCH = 256;
+  __shared__ float red[4][GQ];
+  float(*qs)[D] = (float(*)[D])pool;
+  float(*tl)[GQ] = (float(*)[GQ])(pool + GQ * D * 4);
+  float(*acc)[D] = (float(*)[D])(pool + GQ * D * 4 + TCH * GQ * 4);
+  const int b = bh / g.H, h = bh % g.H;
+  const int S = g.S[b];
+  const int nsp = (S + g.dsplit - 1) / g.dsplit;
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const bool app = kin != nullptr;
+  const int ntail = n_app + (app ? 1 : 0);
+  const size_t tb = ((size_t)b * g.H + h) * g.max_append;
+  const E* TK = (const E*)c.tkd + tb * D;
+  const E* TV = (const E*)c.tvd + tb * D;
+  const E* kn = app ? (const E*)kin + ((size_t)b * g.H + h) * D : nullptr;
+  const E* vn = app ? (const E*)vin + ((size_t)b * g.H + h) * D : nullptr;
+  if (app && tid < D) {
+    Elem<DT>::put(c.tkd, (tb + n_app) * D + tid, Elem<DT>::get(kn, tid));
+    Elem<DT>::put(c.tvd, (tb + n_app) * D + tid, Elem<DT>::get(vn, tid));
+  }
+  const E* qg = (const E*)q + ((size_t)b * g.Hq + (size_t)h * GQ) * D;
+  for (int i = tid; i < GQ * D; i += 256) qs[i / D][i % D] = Elem<DT>::get(qg, i);
+  __syncthreads();
+  auto logits = [&](int n, float* l) {
+    const E* kr = (app && n == n_app) ? kn : TK + (size_t)n * D;
+#pragma unroll
+    for (int jj = 0; jj < GQ; ++jj) l[jj] = 0.0f;
+    for (int d = 0; d < D; ++d) {
+      const float kd = Elem<DT>::get(kr, d);
+#pragma unroll
+      for (int jj = 0; jj < GQ; ++jj) l[jj] = fmaf(qs[jj][d], kd, l[jj]);
+    }
+#pragma unroll
+    for (int jj = 0; jj < GQ; ++jj) l[jj] *= sl2;
+  };
+  float mloc[GQ];
+#pragma unroll
+  for (int jj = 0; jj < GQ; ++jj) mloc[jj] = -INFINITY;
+  for (int n = tid; n < ntail; n += 256) {
+    float l[GQ];
+    logits(n, l);
+#pragma unroll
+    for (int jj = 0; jj < GQ; ++jj) mloc[jj] = fmaxf(mloc[jj], l[jj]);
+  }
+#pragma unroll
+  for (int jj = 0; jj < GQ; ++jj) {
+    const float v = wave_max_dpp(mloc[jj]);
+    if (lane == 0) red[wave][jj] = v;
+  }
+  __syncthreads();
+  float M[GQ], lsum[GQ];
+#pragma unroll
+  for (int jj = 0; jj < GQ; ++jj) {
+    M[jj] = fmaxf(fmaxf(red[0][jj], red[1][jj]), fmaxf(red[2][jj], red[3][jj]));
+    lsum[jj] = 0.0f;
+  }
+  const int cq = tid & 31, sg = tid >> 5;
+  float o[GQ][4];
+#pragma unroll
+  for (int jj = 0; jj < GQ; ++jj) o[jj][0] = o[jj][1] = o[jj][2] = o[jj][3] = 0.0f;
+  for (int c0 = 0; c0 < ntail; c0 += TCH) {
+    const int n = c0 + tid;
+    __syncthreads();
+    if (n < ntail) {
+      float l[GQ];
+      logits(n, l);
+#pragma unroll
+      for (int jj = 0; jj < GQ; ++jj) {
+        const float p = __builtin_amdgcn_exp2f(l[jj] - M[jj]);
+        lsum[jj] += p;
+        tl[tid][jj] = p;
+      }
+    }
+    __syncthreads();
+    const int cn = min(TCH, ntail - c0);
+    for (int u = sg; u < cn; u += 8) {
+      const int nn = c0 + u;
+      const E* row = ((app && nn == n_app) ? vn : TV + (size_t)nn * D) + 4 * cq;
+      float v[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) v[i] = Elem<DT>::get(row, i);
+#pragma unroll
+      for (int jj = 0; jj < GQ; ++jj) {
+        const float w = tl[u][jj];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) o[jj][i] = fmaf(w, v[i], o[jj][i]);
+      }
+    }
+  }
+#pragma unroll
+  for (int jj = 0; jj < GQ; ++jj) {
+    const float v = wave_sum_dpp(lsum[jj]);
+    __syncthreads();
+    if (lane == 0) red[wave][jj] = v;
+    __syncthreads();
+    lsum[jj] = (red[0][jj] + red[1][jj]) + (red[2][jj] + red[3][jj]);
+  }
+  const int Hq = g.Hq;
+#pragma unroll
+  for (int jj = 0; jj < GQ; ++jj) {
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < 4; ++i) acc[sg][4 * cq + i] = o[jj][i];
+    __syncthreads();
+    float* pr = dw.part + ((size_t)g.prefSp[b] * Hq + (size_t)(h * GQ + jj) * (nsp + 1) + nsp) * PS;
+    if (tid < D) {
+      float y = 0.0f;
+#pragma unroll
+      for (int qq = 0; qq < 8; ++qq) y += acc[qq][tid];
+      pr[4 + tid] = y;
+    }
+    if (tid == 0) {
+      pr[0] = ntail > 0 ? M[jj] : -INFINITY;
+      pr[1] = lsum[jj];
+    }
+  }
+}
+
+// Append only, dense tail: copies the new key and value of every (request,
+// KV head) into tail slot n_app.  Grid: B * H workgroups of D threads.
+template <int DT>
+__global__ __launch_bounds__(AKV_D) void k_app_dense(Geo g, Cache c, int n_app, const void* kin, const void* vin) {
+  const size_t bh = blockIdx.x, d = threadIdx.x;
+  const size_t ti = (bh * g.max_append + n_app) * AKV_D + d;
+  Elem<DT>::put(c.tkd, ti, Elem<DT>::get(kin, bh * AKV_D + d));
+  Elem<DT>::put(c.tvd, ti, Elem<DT>::get(vin, bh * AKV_D + d));
+}
+
 // ------------------------------------------------------------------ stream
 // R uint16 values starting at p (R * 2 bytes, 8-byte aligned).
 template <int R>
@@ -774,19 +912,23 @@ __device__ inline void wave_lds_sync() {
 // applied once per query head.
 template <int DT, int GQ, int R>
 __global__ __launch_bounds__(256) void k_dec_stream(Geo g, Cache c, DecWs dw, int nst, int n_app, const void* kin,
-                                                    const void* vin) {
+                                                    const void* vin, const void* q, float sl2) {
   using E = typename Elem<DT>::T;
   using WL = StreamWaveLds<DT, GQ>;
   constexpr int D = AKV_D, LW = 64 * R, L = 4 * LW, PER = 16 / sizeof(E);
   constexpr int NAVW = SW_AST * D / PER / 64;  // 16-byte anchor-row chunks per lane
   constexpr int ZY_B = 2 * 4 * GQ * D * 4;
   constexpr int WL_B = 4 * (int)sizeof(WL);
-  constexpr int TAIL_B = 256 * GQ * 4 + 256 * 4 + 8 * D * 4;
+  constexpr int TAIL_E = 256 * GQ * 4 + 256 * 4 + 8 * D * 4, TAIL_D = GQ * D * 4 + 256 * GQ * 4 + 8 * D * 4;
+  constexpr int TAIL_B = TAIL_E > TAIL_D ? TAIL_E : TAIL_D;
   constexpr int POOL_B = (WL_B > ZY_B ? WL_B : ZY_B) > TAIL_B ? (WL_B > ZY_B ? WL_B : ZY_B) : TAIL_B;
   __shared__ __align__(16) unsigned char pool[POOL_B];
   __shared__ float wm[4][GQ], wl[4][GQ];
   if ((int)blockIdx.x >= nst) {
-    tail_block<DT, GQ>(g, c, dw, (int)blockIdx.x - nst, n_app, kin, vin, pool);
+    if (g.dense_tail)
+      tail_dense<DT, GQ>(g, c, dw, (int)blockIdx.x - nst, n_app, kin, vin, q, sl2, pool);
+    else
+      tail_block<DT, GQ>(g, c, dw, (int)blockIdx.x - nst, n_app, kin, vin, pool);
     return;
   }
   // Logical block id: consecutive ids (the splits of one head) share an XCD.
@@ -1266,6 +1408,13 @@ __global__ __launch_bounds__(256) void k_reconstruct(Geo g, Cache c, int b, int 
     slot = (side ? c.pcV : c.pcK)[wo] + __popcll(wm & ((1ull << (i & 63)) - 1ull));
   } else {
     const size_t ti = ((size_t)b * g.H + h) * g.max_append + (i - S);
+    if (g.dense_tail) {  // stored exactly
+      const void* X = side ? c.tvd : c.tkd;
+      float* o = out + ((size_t)h * rows + i) * D;
+      o[2 * lane] = Elem<DT>::get(X, ti * D + 2 * lane);
+      o[2 * lane + 1] = Elem<DT>::get(X, ti * D + 2 * lane + 1);
+      return;
+    }
     t = i;
     a = min((int)(side ? c.tidxV : c.tidxK)[ti], k - 1);
     gb = Elem<DT>::get(side ? c.tgV : c.tgK, ti);
@@ -1296,10 +1445,17 @@ template <int DT, int GQ>
 static void launch_steps(const Geo& g, const Cache& c, const DecWs& dw, const void* q, const void* kn,
                          const void* vn, void* out, int out_dtype, float scale, int n_app, bool attn, bool app,
                          hipStream_t st) {
+  // A dense tail needs no anchor screening for the appended token: the tail
+  // workgroups store it (or k_app_dense, for an append alone).
+  const bool screen = app && !g.dense_tail;
+  if (!attn && !screen) {
+    launch("k_app_dense", k_app_dense<DT>, dim3(g.B * g.H), dim3(AKV_D), 0, st, g, c, n_app, kn, vn);
+    return;
+  }
   const int nAK = g.H * g.prefAB[g.B];
-  const int nAV = app ? nAK : 0;
+  const int nAV = screen ? nAK : 0;
   const int nR = attn ? (g.prefNK[g.B] + RK_PER_BLOCK - 1) / RK_PER_BLOCK : 0;
-  const int flags = (attn ? 1 : 0) | (app ? 2 : 0);
+  const int flags = (attn ? 1 : 0) | (screen ? 2 : 0);
   const float sl2 = scale * 1.4426950408889634f;
   launch("k_dec_front", k_dec_front<DT, GQ>, dim3(nAK + nAV + nR), dim3(256), 0, st, g, c, dw, q, kn, vn, flags, nAK, nAV, sl2);
   if (!attn) {
@@ -1311,9 +1467,11 @@ static void launch_steps(const Geo& g, const Cache& c, const DecWs& dw, const vo
   for (int b = 0; b < g.B; ++b) nst += g.H * ((g.S[b] + L - 1) / L);
   const int ntb = g.B * g.H;  // tail workgroups
   if (L == 2048) {
-    launch("k_dec_stream", k_dec_stream<DT, GQ, 8>, dim3(nst + ntb), dim3(256), 0, st, g, c, dw, nst, n_app, kn, vn);
+    launch("k_dec_stream", k_dec_stream<DT, GQ, 8>, dim3(nst + ntb), dim3(256), 0, st, g, c, dw, nst, n_app, kn, vn, q,
+           sl2);
   } else {
-    launch("k_dec_stream", k_dec_stream<DT, GQ, 4>, dim3(nst + ntb), dim3(256), 0, st, g, c, dw, nst, n_app, kn, vn);
+    launch("k_dec_stream", k_dec_stream<DT, GQ, 4>, dim3(nst + ntb), dim3(256), 0, st, g, c, dw, nst, n_app, kn, vn, q,
+           sl2);
   }
   launch("k_dec_merge", k_dec_merge<DT, GQ>, dim3(g.B * g.Hq), dim3(256), 0, st, g, dw, out, out_dtype);
 }

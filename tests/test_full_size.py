@@ -10,6 +10,9 @@ configuration the benchmark uses (``decode_step``, the plan's split length).
   oracle's attention over its reconstruction plus the appended tokens.
 * Workload 4 (70B shape, 8 requests): every request, encode and decode.
 * Workload 5 (16 ragged requests): the shortest, the median and the longest.
+* The paper's operating point (8B layer at 32K, k = S/128, theta = 0.05 from
+  the byte budget, i.e. 20x): the residual count of the worked example and the
+  whole request against the oracle, encode and decode.
 * One 540000-token request (265 split records per query head, the merge's
   second round): decode_step against fp64 attention over the dense
   reconstruction of the same cache, a property that holds at any size (the
@@ -185,6 +188,37 @@ def _oracle_decode_check(cfg, lay, b, enc, q, got, tails=None, tag=""):
     print(f"[full] {tag}: decode vs oracle attention max|err| {err:.3g}", flush=True)
     assert err <= 2e-3, err
     return err
+
+
+def test_paper_operating_point_theta_20x():
+    """App. A.1 worked example at full size: S = 32768, H = 8, D = 128, W = 32,
+    k = S/128 = 256 and theta = 0.05 give N = 91,056 residuals (Eq.
+    byte-budget), split N_K = floor(N/2), N_V = N - N_K; the compression pass
+    at that budget matches the oracle's bit for bit and decode matches its
+    attention."""
+    S = 32768
+    wl = synth.Workload("llama8b-32K-theta0.05", H=8, Hq=32, D=128, seq_lens=[S], dtype="bf16",
+                        anchor_count=S // 128, n_centers=512, steps=2, seed=5)
+    cfg = make_cfg(wl, budget_mode=N.BUDGET_THETA, budget=0.05)
+    plan = N.Plan(cfg, wl.seq_lens)
+    ri = plan.requests[0]
+    n = R.theta_budget(S, 8, 128, 32, 256, 128, float(np.float32(0.05)))
+    assert abs(n - 91056) <= 1  # the fp32 rounding of theta may move the floor by one
+    assert (ri.residuals_k, ri.residuals_v) == (n // 2, n - n // 2)
+    print(f"[full] operating point: k={ri.anchors} N_K={ri.residuals_k} N_V={ri.residuals_v} "
+          f"cache {plan.cache_bytes / 1e6:.2f} MB vs dense {2 * S * 8 * 128 * 2 / 1e6:.1f} MB", flush=True)
+    lay = _layer_on_gpu(wl, steps=2)
+    cache, ws, dws = gpu_encode(plan, lay)
+    assert _header_flags(cache) == 0
+    exp = _export(plan, cache, 0)
+    enc = _oracle_whole_request(cfg, lay, 0, exp, "operating point")
+    assert int(exp["sel_k"].sum()) == ri.residuals_k and int(exp["sel_v"].sum()) == ri.residuals_v
+    for s in range(2):
+        out = torch.empty(1, wl.Hq, wl.D, dtype=torch.float32, device="cuda")
+        akv.decode_attn(plan, cache, lay.q[s], out, dws)
+        torch.cuda.synchronize()
+        _oracle_decode_check(cfg, lay, 0, enc, lay.q[s, 0].float().cpu().numpy(), out[0].cpu().numpy(),
+                             tag=f"operating point step {s}")
 
 
 def test_workload3_128k_whole_with_64_appends():

@@ -130,6 +130,21 @@ def test_equal_per_head_budgets_in_the_plan():
         assert N.Plan(_cfg(rank_mode=mode), [5000]).requests[0].residuals_k == pooled.residuals_k
 
 
+def test_dense_tail_cache_bytes():
+    """DENSE append mode (App. E "Generated Tokens"): the exact tail costs
+    2 * H * D * element bytes per appended token and request on top of the
+    same compressed prefix."""
+    _lib_or_skip()
+    lens, cap = [900, 1700], 5
+    enc = N.Plan(_cfg(max_append=cap), lens)
+    dense = N.Plan(_cfg(max_append=cap, append_mode=N.APPEND_DENSE), lens)
+    extra = dense.cache_bytes - enc.cache_bytes
+    need = len(lens) * 2 * 8 * cap * 128 * 2
+    assert need <= extra <= need + 2 * 256  # two more arrays, each 256-byte aligned
+    with pytest.raises(N.AnchorKVError):
+        N.Plan(_cfg(append_mode=2), lens)
+
+
 def test_buffer_sizes_grow_with_batch():
     _lib_or_skip()
     p1 = N.Plan(_cfg(), [8192])
