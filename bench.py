@@ -143,13 +143,47 @@ def cpu_baseline(wl, seed, Ss=32768, nsteps=8):
     t_dec = (time.perf_counter() - t0) / nsteps
     nk, nv = int(enc["nsel"][0]), int(enc["nsel"][1])
     H, D = wl.H, wl.D
-    byts = (H * Ss * 8 + 2 * H * math.ceil(Ss / 64) * 12 + (nk + nv) * (D // 4 + 4) + 2 * H * k * D * 2
-            + wl.Hq * D * 4)
-    return dict(value=round(byts / t_dec / 1e9, 4), unit="GB/s", cores=R.num_threads(), kind="oracle",
+
+    def dbytes(S_, k_, n_):
+        return (H * S_ * 8 + 2 * H * math.ceil(S_ / 64) * 12 + n_ * (D // 4 + 4) + 2 * H * k_ * D * 2
+                + wl.Hq * D * 4)
+
+    byts = dbytes(Ss, k, nk + nv)
+    threads = R.num_threads()
+    # the same oracle on one thread, on a quarter of the sample (one decode step)
+    S1 = Ss // 4
+    k1 = sub.k_of(S1)
+    R.set_threads(1)
+    try:
+        t0 = time.perf_counter()
+        enc1 = R.encode(K[:, :S1], V[:, :S1], Q, W=32, k=k1, bf16=True, seed=seed,
+                        budget=float(np.float32(wl.budget)), G=wl.D)
+        t_enc1 = time.perf_counter() - t0
+        t0 = time.perf_counter()
+        R.attention(R.reconstruct(K[:, :S1], enc1, "K", wl.D, seed), R.reconstruct(V[:, :S1], enc1, "V", wl.D, seed),
+                    layer.q[0, 0].float().numpy())
+        t_dec1 = time.perf_counter() - t0
+    finally:
+        R.set_threads(threads)
+    n1 = int(enc1["nsel"][0]) + int(enc1["nsel"][1])
+    cpu_model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    cpu_model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return dict(value=round(byts / t_dec / 1e9, 4), unit="GB/s", cores=threads, kind="oracle",
                 sample=f"first {Ss} positions of one 8B layer (H={H}, Hq={wl.Hq}, bf16, k={k}): oracle encode "
                        f"{t_enc:.2f} s, then {nsteps} oracle decode steps at {t_dec:.3f} s each",
                 encode_mtok_s=round(Ss / t_enc / 1e6, 6), decode_s_per_step=round(t_dec, 4),
-                encode_s=round(t_enc, 3))
+                encode_s=round(t_enc, 3), cpu_model=cpu_model, host_cpus=os.cpu_count(),
+                single_thread={"value": round(dbytes(S1, k1, n1) / t_dec1 / 1e9, 4), "unit": "GB/s", "cores": 1,
+                               "encode_mtok_s": round(S1 / t_enc1 / 1e6, 6), "decode_s_per_step": round(t_dec1, 4),
+                               "sample": f"first {S1} positions of the same layer (k={k1}): one oracle encode, "
+                                         f"one decode step"})
 
 
 def fidelity(args):
@@ -337,7 +371,7 @@ def main():
     # Kernel durations: HIP events around the first launches of each named
     # kernel inside the timed region (a bounded number, so that the event
     # records barely touch the timed step).
-    kernels = ["k_dec_stream", "k_dec_front", "k_dec_merge", "k_assign"]
+    kernels = ["k_dec_stream", "k_dec_front", "k_dec_merge", "k_assign", "k_obs64", "k_epilogue"]
     timer = N.KernelTimer(kernels, max_launches=256)
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
     torch.cuda.synchronize()

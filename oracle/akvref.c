@@ -767,3 +767,13 @@ int akvref_num_threads(void) {
   return 1;
 #endif
 }
+
+/* Threads of the parallel loops from now on (timing only; results do not
+ * depend on it). */
+void akvref_set_threads(int n) {
+#ifdef _OPENMP
+  if (n > 0) omp_set_num_threads(n);
+#else
+  (void)n;
+#endif
+}

@@ -87,6 +87,7 @@ def _declare(L):
                                      _f]
     L.akvref_attention.argtypes = [_f, _f, _c_int, _c_int, _c_int, _d, _c_int, _c_dbl, _d]
     L.akvref_num_threads.restype = _c_int
+    L.akvref_set_threads.argtypes = [_c_int]
 
 
 def _p(a, t):
@@ -294,3 +295,8 @@ def attention(Kt, Vt, q, scale=None):
 
 def num_threads() -> int:
     return int(lib().akvref_num_threads())
+
+
+def set_threads(n: int) -> None:
+    """Threads of the oracle's parallel loops (timing only)."""
+    lib().akvref_set_threads(int(n))
