@@ -30,9 +30,16 @@
  *              centred zero-padded numpy convolution at kappa = 1..9),
  *              utilities (numpy brute force over m = 6 observation rows, each
  *              with its own causal softmax and y_w; finite-difference test of
- *              the two-channel expansion, Eq. channels).  Planted mistakes in
- *              a copy of this file (off-centre or renormalised pool, one-row
- *              sums, offset-major rows, alpha for alpha^2) fail these pins.
+ *              the two-channel expansion, Eq. channels), positional rotation
+ *              (the rotary table against numpy's cos and sin, the rotation as
+ *              a complex product, worked unit vectors, relative-position
+ *              invariance; the rotated pass's selector, utilities and
+ *              attention against numpy over explicitly rotated keys; zero
+ *              frequencies reduce it to the unrotated pass bit for bit).
+ *              Planted mistakes in a copy of this file (off-centre or
+ *              renormalised pool, one-row sums, offset-major rows, alpha for
+ *              alpha^2, reversed rotation, unrotated observation keys or key
+ *              residuals, mirrored positions) fail these pins.
  *   parity unpinned beyond self-consistency: the absmax scale readings of the
  *              codec (Sec. 3.1 / App. A.1 leave the scale rule ambiguous).
  */
@@ -98,6 +105,60 @@ void akvref_fwht(float* z, int D) {
         z[i] = a + b;
         z[i + h] = a - b;
       }
+}
+
+/* ------------------------------------------------------------------------ */
+/* Rotary position embedding (Sec. 3.2: keys are projected before the        */
+/* rotation, anchors are scored with rotated keys, and the stored keys are   */
+/* rotated at decoding; App. E "Implementation").                            */
+/* ------------------------------------------------------------------------ */
+
+/* Cosines and sines of the rotation R_t of positions t = 0 .. npos-1 in the
+ * rotate-half pairing of Llama-family models: coordinate pair (f, f + D/2),
+ * f < D/2, turns by the angle t * inv_freq[f].  Both are fp32, the roundings
+ * of the fp64 cos and sin of the fp64 angle (t exact, inv_freq[f] an fp32
+ * value), as a model's rotary table holds them: cs[t][f][0] = cos,
+ * cs[t][f][1] = sin. */
+void akvref_rope_table(const float* inv_freq, int D, int npos, float* cs) {
+  int F = D / 2;
+  for (int t = 0; t < npos; ++t)
+    for (int f = 0; f < F; ++f) {
+      double ang = (double)t * (double)inv_freq[f];
+      cs[((size_t)t * F + f) * 2] = (float)cos(ang);
+      cs[((size_t)t * F + f) * 2 + 1] = (float)sin(ang);
+    }
+}
+
+/* out = R_t x in fp64 from position t's fp32 cosines and sines (cs_t, D
+ * values): (x_f, x_{f+D/2}) -> (c x_f - s x_{f+D/2}, s x_f + c x_{f+D/2}).
+ * A product of an fp32 factor and an fp32 or bf16 coordinate is exact in
+ * fp64, so each output coordinate is rounded once. */
+void akvref_rope_rotate(const float* cs_t, const double* x, int D, double* out) {
+  int F = D / 2;
+  for (int f = 0; f < F; ++f) {
+    double c = cs_t[2 * f], s = cs_t[2 * f + 1];
+    double a = x[f], b = x[f + F];
+    out[f] = c * a - s * b;
+    out[f + F] = s * a + c * b;
+  }
+}
+
+/* Rotated keys of one head as attention sees them: R_t K_t for every
+ * position, rounded to fp32 and, for a bf16 cache, on to bf16 (the dtype of a
+ * model's rotated keys).  They feed the observation pass -- anchor scores,
+ * attention weights and the outputs y_w -- while assignment, projection and
+ * storage use the unrotated keys. */
+void akvref_rope_keys(const double* K, int S, int D, const float* cs, int bf16, double* Kpost) {
+  double* tmp = (double*)malloc(sizeof(double) * D);
+  for (int t = 0; t < S; ++t) {
+    akvref_rope_rotate(cs + (size_t)t * D, K + (size_t)t * D, D, tmp);
+    for (int j = 0; j < D; ++j) {
+      float v = (float)tmp[j];
+      if (bf16) v = bf16_rne(v);
+      Kpost[(size_t)t * D + j] = v;
+    }
+  }
+  free(tmp);
 }
 
 /* ------------------------------------------------------------------------ */
@@ -455,14 +516,16 @@ void akvref_assign_vectors(const double* xs, int n, const double* A, int k, int 
 /* Attention-output-aware utilities (Sec. 3.3, Eq. utilities; App. A.3).      */
 /* ------------------------------------------------------------------------ */
 
-/* Utilities of listed non-anchor tokens of one head (R_t = I: no positional
- * rotation on this path).  rK, rV are the fp32 residuals of those tokens.
- *   uK_t = (1/m) sum_w alpha_wt^2 (q_w . rK_t)^2 / D * ||v_t - y_w||^2
- *   uV_t = (1/m) sum_w alpha_wt^2 ||rV_t||^2 */
-void akvref_utilities(const double* Kh, const double* Vh, const double* Qg, const double* M,
-                      const double* Z, const double* Y, int S, int D, int W, int g,
-                      const int* toks, int ntok, const float* rK, const float* rV, double* uK,
-                      double* uV) {
+/* Utilities of listed non-anchor tokens of one head.  rK, rV are the fp32
+ * residuals of those tokens; Kh holds the keys the observation rows attend to
+ * (rotated when positions are encoded), cs the rotation table or NULL.
+ *   uK_t = (1/m) sum_w alpha_wt^2 (q_w . R_t rK_t)^2 / D * ||v_t - y_w||^2
+ *   uV_t = (1/m) sum_w alpha_wt^2 ||rV_t||^2
+ * R_t r is formed in fp64 (akvref_rope_rotate); without a table R_t = I. */
+static void utilities_impl(const double* Kh, const double* Vh, const double* Qg, const double* M,
+                           const double* Z, const double* Y, int S, int D, int W, int g,
+                           const int* toks, int ntok, const float* rK, const float* rV, const float* cs,
+                           double* uK, double* uV) {
   int m = W * g;
 #pragma omp parallel for schedule(dynamic, 16)
   for (int i = 0; i < ntok; ++i) {
@@ -473,6 +536,10 @@ void akvref_utilities(const double* Kh, const double* Vh, const double* Qg, cons
     for (int j = 0; j < D; ++j) {
       rk[j] = rK[(size_t)i * D + j];
       rv[j] = rV[(size_t)i * D + j];
+    }
+    if (cs) {
+      akvref_rope_rotate(cs + (size_t)t * D, rk, D, dv);
+      memcpy(rk, dv, sizeof(double) * D);
     }
     double rvn = dot64(rv, rv, D);
     double sk = 0.0, sv = 0.0;
@@ -491,6 +558,22 @@ void akvref_utilities(const double* Kh, const double* Vh, const double* Qg, cons
     free(rv);
     free(dv);
   }
+}
+
+void akvref_utilities(const double* Kh, const double* Vh, const double* Qg, const double* M,
+                      const double* Z, const double* Y, int S, int D, int W, int g,
+                      const int* toks, int ntok, const float* rK, const float* rV, double* uK,
+                      double* uV) {
+  utilities_impl(Kh, Vh, Qg, M, Z, Y, S, D, W, g, toks, ntok, rK, rV, NULL, uK, uV);
+}
+
+/* The same with positions encoded: Kh_rot the rotated keys of the head
+ * (akvref_rope_keys), cs the rotation table of its S positions. */
+void akvref_utilities_rope(const double* Kh_rot, const double* Vh, const double* Qg, const double* M,
+                           const double* Z, const double* Y, int S, int D, int W, int g,
+                           const int* toks, int ntok, const float* rK, const float* rV, const float* cs,
+                           double* uK, double* uV) {
+  utilities_impl(Kh_rot, Vh, Qg, M, Z, Y, S, D, W, g, toks, ntok, rK, rV, cs, uK, uV);
 }
 
 /* ------------------------------------------------------------------------ */
@@ -586,13 +669,13 @@ enum { BUDGET_FRACTION = 0, BUDGET_THETA = 1, BUDGET_COUNT = 2 };
  *   codesK, codesV [H][S][D/4]; scalesK, scalesV [H][S][D/G] (zero where the
  *   position stores no residual); pooled [H][S-W] selector scores (may be NULL).
  * nsel[2] receives the residual counts per side. */
-int akvref_encode(int H, int Hq, int D, int S, int W, int k, float rho, int kappa, int bf16,
-                  uint64_t seed, int budget_mode, double budget, int64_t budget_count, int G,
-                  int scale_mode, int rank_mode, int head_budget, const double* K, const double* V,
-                  const double* Qobs, const int* anchor_override, int* anchors, int* aK, double* gK, int* aV,
-                  double* gV, double* uK, double* uV, uint8_t* selK, uint8_t* selV,
-                  uint8_t* codesK, float* scalesK, uint8_t* codesV, float* scalesV,
-                  double* pooled, int64_t* nsel) {
+static int encode_impl(int H, int Hq, int D, int S, int W, int k, float rho, int kappa, int bf16,
+                       uint64_t seed, int budget_mode, double budget, int64_t budget_count, int G,
+                       int scale_mode, int rank_mode, int head_budget, const double* K, const double* V,
+                       const double* Qobs, const int* anchor_override, const float* inv_freq, int* anchors,
+                       int* aK, double* gK, int* aV, double* gV, double* uK, double* uV, uint8_t* selK,
+                       uint8_t* selV, uint8_t* codesK, float* scalesK, uint8_t* codesV, float* scalesV,
+                       double* pooled, int64_t* nsel) {
   if (H <= 0 || Hq % H != 0 || D < 4 || (D & (D - 1)) || W < 0 || k < W || k > S ||
       G <= 0 || D % G || G % 4 || kappa <= 0 || (kappa & 1) == 0 || rank_mode < 0 || rank_mode > 4)
     return 1;
@@ -607,17 +690,31 @@ int akvref_encode(int H, int Hq, int D, int S, int W, int k, float rho, int kapp
   double* Y = (double*)malloc(sizeof(double) * (size_t)(m > 0 ? m : 1) * D);
   double* sc = (double*)malloc(sizeof(double) * (size_t)(P > 0 ? P : 1));
   double* pl = (double*)malloc(sizeof(double) * (size_t)(P > 0 ? P : 1));
+  /* With positions encoded, the observation pass runs on the rotated keys
+   * (Sec. 3.2: anchor scoring uses post-rotation keys). */
+  float* cs = NULL;
+  double* Krot = NULL;
+  if (inv_freq) {
+    cs = (float*)malloc(sizeof(float) * (size_t)S * D);
+    Krot = (double*)malloc(sizeof(double) * SD);
+    akvref_rope_table(inv_freq, D, S, cs);
+  }
   for (int h = 0; h < H; ++h) {
     const double* Kh = K + (size_t)h * SD;
     const double* Vh = V + (size_t)h * SD;
     const double* Qg = Qobs + (size_t)h * g * W * D;
     int* anc = anchors + (size_t)h * k;
-    akvref_obs_head(Kh, Vh, Qg, S, D, W, g, M, Zs, Y);
+    const double* Ko = Kh;
+    if (inv_freq) {
+      akvref_rope_keys(Kh, S, D, cs, bf16, Krot);
+      Ko = Krot;
+    }
+    akvref_obs_head(Ko, Vh, Qg, S, D, W, g, M, Zs, Y);
     if (anchor_override) {
       memcpy(anc, anchor_override + (size_t)h * k, sizeof(int) * k);
-      if (rank_mode == RANK_ATTENTION) akvref_selector_scores(Kh, Qg, M, Zs, S, D, W, g, kappa, sc, pl);
+      if (rank_mode == RANK_ATTENTION) akvref_selector_scores(Ko, Qg, M, Zs, S, D, W, g, kappa, sc, pl);
     } else {
-      akvref_selector_scores(Kh, Qg, M, Zs, S, D, W, g, kappa, sc, pl);
+      akvref_selector_scores(Ko, Qg, M, Zs, S, D, W, g, kappa, sc, pl);
       if (pooled) memcpy(pooled + (size_t)h * P, pl, sizeof(double) * P);
       akvref_select_anchors(pl, S, W, k, rho, seed, h, anc);
     }
@@ -639,7 +736,7 @@ int akvref_encode(int H, int Hq, int D, int S, int W, int k, float rho, int kapp
       memcpy(crk + (size_t)i * D, rKh + (size_t)cand_t[i] * D, sizeof(float) * D);
       memcpy(crv + (size_t)i * D, rVh + (size_t)cand_t[i] * D, sizeof(float) * D);
     }
-    akvref_utilities(Kh, Vh, Qg, M, Zs, Y, S, D, W, g, cand_t, nc, crk, crv, cuk, cuv);
+    utilities_impl(Ko, Vh, Qg, M, Zs, Y, S, D, W, g, cand_t, nc, crk, crv, cs, cuk, cuv);
     for (int t = 0; t < S; ++t) { uK[(size_t)h * S + t] = -1.0; uV[(size_t)h * S + t] = -1.0; }
     for (int i = 0; i < nc; ++i) {
       uK[(size_t)h * S + cand_t[i]] = cuk[i];
@@ -692,7 +789,39 @@ int akvref_encode(int H, int Hq, int D, int S, int W, int k, float rho, int kapp
       if (selV[e]) akvref_codec_encode(rV + e * D, D, G, scale_mode, seed, codesV + e * nb, scalesV + e * ns);
     }
   free(rK); free(rV); free(all); free(M); free(Zs); free(Y); free(sc); free(pl);
+  free(cs); free(Krot);
   return 0;
+}
+
+int akvref_encode(int H, int Hq, int D, int S, int W, int k, float rho, int kappa, int bf16,
+                  uint64_t seed, int budget_mode, double budget, int64_t budget_count, int G,
+                  int scale_mode, int rank_mode, int head_budget, const double* K, const double* V,
+                  const double* Qobs, const int* anchor_override, int* anchors, int* aK, double* gK, int* aV,
+                  double* gV, double* uK, double* uV, uint8_t* selK, uint8_t* selV,
+                  uint8_t* codesK, float* scalesK, uint8_t* codesV, float* scalesV,
+                  double* pooled, int64_t* nsel) {
+  return encode_impl(H, Hq, D, S, W, k, rho, kappa, bf16, seed, budget_mode, budget, budget_count, G, scale_mode,
+                     rank_mode, head_budget, K, V, Qobs, anchor_override, NULL, anchors, aK, gK, aV, gV, uK, uV,
+                     selK, selV, codesK, scalesK, codesV, scalesV, pooled, nsel);
+}
+
+/* The compression pass with positions encoded (Sec. 3.2 "RoPE"): K holds the
+ * keys before the rotation (position t of request's prompt is t) and
+ * inv_freq[D/2] the rotation's frequencies.  Anchor selection, the attention
+ * weights and y_w use the rotated keys, u^K uses R_t r^K_t (Eq. utilities);
+ * assignment, coefficients, residuals and codes are those of the unrotated
+ * keys, which is what the cache stores.  Same outputs as akvref_encode. */
+int akvref_encode_rope(int H, int Hq, int D, int S, int W, int k, float rho, int kappa, int bf16,
+                       uint64_t seed, int budget_mode, double budget, int64_t budget_count, int G,
+                       int scale_mode, int rank_mode, int head_budget, const double* K, const double* V,
+                       const double* Qobs, const int* anchor_override, const float* inv_freq, int* anchors,
+                       int* aK, double* gK, int* aV, double* gV, double* uK, double* uV, uint8_t* selK,
+                       uint8_t* selV, uint8_t* codesK, float* scalesK, uint8_t* codesV, float* scalesV,
+                       double* pooled, int64_t* nsel) {
+  if (!inv_freq) return 1;
+  return encode_impl(H, Hq, D, S, W, k, rho, kappa, bf16, seed, budget_mode, budget, budget_count, G, scale_mode,
+                     rank_mode, head_budget, K, V, Qobs, anchor_override, inv_freq, anchors, aK, gK, aV, gV, uK,
+                     uV, selK, selV, codesK, scalesK, codesV, scalesV, pooled, nsel);
 }
 
 /* ------------------------------------------------------------------------ */
@@ -757,6 +886,42 @@ void akvref_attention(const float* Kt, const float* Vt, int H, int T, int D, con
     }
     free(l);
     free(kk);
+  }
+}
+
+/* Attention with positions encoded: entry t of every head sits at position
+ * t (prompt positions, then appended tokens) and its key enters the logit
+ * rotated, dot64(q, R_t k_t) * scale with R_t k_t in fp64 from the table cs
+ * of T positions; values are not rotated.  Otherwise as akvref_attention. */
+void akvref_attention_rope(const float* Kt, const float* Vt, int H, int T, int D, const double* q,
+                           int Hq, double scale, const float* cs, double* out) {
+  int g = Hq / H;
+#pragma omp parallel for schedule(static)
+  for (int j = 0; j < Hq; ++j) {
+    int h = j / g;
+    double* l = (double*)malloc(sizeof(double) * (size_t)T);
+    double* kk = (double*)malloc(sizeof(double) * D);
+    double* kr = (double*)malloc(sizeof(double) * D);
+    double mx = -INFINITY;
+    for (int t = 0; t < T; ++t) {
+      const float* k0 = Kt + ((size_t)h * T + t) * D;
+      for (int c = 0; c < D; ++c) kk[c] = k0[c];
+      akvref_rope_rotate(cs + (size_t)t * D, kk, D, kr);
+      l[t] = dot64(q + (size_t)j * D, kr, D) * scale;
+      if (l[t] > mx) mx = l[t];
+    }
+    double z = 0.0;
+    for (int t = 0; t < T; ++t) z += exp(l[t] - mx);
+    double* o = out + (size_t)j * D;
+    for (int c = 0; c < D; ++c) o[c] = 0.0;
+    for (int t = 0; t < T; ++t) {
+      double p = exp(l[t] - mx) / z;
+      const float* vr = Vt + ((size_t)h * T + t) * D;
+      for (int c = 0; c < D; ++c) o[c] += p * vr[c];
+    }
+    free(l);
+    free(kk);
+    free(kr);
   }
 }
 

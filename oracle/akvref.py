@@ -86,6 +86,16 @@ def _declare(L):
     L.akvref_reconstruct.argtypes = [_d, _c_int, _c_int, _c_int, _c_u64, _c_int, _i, _c_int, _i, _d, _u8, _u8, _f,
                                      _f]
     L.akvref_attention.argtypes = [_f, _f, _c_int, _c_int, _c_int, _d, _c_int, _c_dbl, _d]
+    L.akvref_attention_rope.argtypes = [_f, _f, _c_int, _c_int, _c_int, _d, _c_int, _c_dbl, _f, _d]
+    L.akvref_rope_table.argtypes = [_f, _c_int, _c_int, _f]
+    L.akvref_rope_rotate.argtypes = [_f, _d, _c_int, _d]
+    L.akvref_rope_keys.argtypes = [_d, _c_int, _c_int, _f, _c_int, _d]
+    L.akvref_utilities_rope.argtypes = [_d, _d, _d, _d, _d, _d, _c_int, _c_int, _c_int, _c_int,
+                                        _i, _c_int, _f, _f, _f, _d, _d]
+    L.akvref_encode_rope.restype = _c_int
+    L.akvref_encode_rope.argtypes = ([_c_int] * 6 + [_c_flt, _c_int, _c_int, _c_u64, _c_int, _c_dbl, _c_i64,
+                                                     _c_int, _c_int, _c_int, _c_int, _d, _d, _d, _i, _f, _i, _i,
+                                                     _d, _i, _d, _d, _d, _u8, _u8, _u8, _f, _u8, _f, _d, _i64])
     L.akvref_num_threads.restype = _c_int
     L.akvref_set_threads.argtypes = [_c_int]
 
@@ -149,6 +159,31 @@ def theta_budget(S, H, D, W, k, G, theta, elem_bytes=2, b_gamma=2) -> int:
     return int(lib().akvref_theta_budget(S, H, D, W, k, G, elem_bytes, b_gamma, theta))
 
 
+def rope_table(inv_freq, D: int, npos: int) -> np.ndarray:
+    """fp32 cosines and sines [npos][D/2][2] of the rotation R_t (rotate-half pairs)."""
+    inv_freq = _f32(inv_freq)
+    cs = np.empty((npos, D // 2, 2), np.float32)
+    lib().akvref_rope_table(_p(inv_freq, _f), D, npos, _p(cs, _f))
+    return cs
+
+
+def rope_rotate(cs_t, x) -> np.ndarray:
+    """R_t x in fp64 for one position (cs_t: [D/2][2])."""
+    cs_t, x = _f32(cs_t), _f64(x)
+    out = np.empty_like(x)
+    lib().akvref_rope_rotate(_p(cs_t, _f), _p(x, _d), x.shape[-1], _p(out, _d))
+    return out
+
+
+def rope_keys(Kh, cs, bf16: bool) -> np.ndarray:
+    """Rotated keys of one head [S][D], rounded to the cache dtype."""
+    Kh, cs = _f64(Kh), _f32(cs)
+    S, D = Kh.shape
+    out = np.empty((S, D))
+    lib().akvref_rope_keys(_p(Kh, _d), S, D, _p(cs, _f), int(bf16), _p(out, _d))
+    return out
+
+
 def n_top(k, W, rho) -> int:
     return int(lib().akvref_n_top(k, W, rho))
 
@@ -207,7 +242,9 @@ def assign_vectors(xs, A, bf16: bool):
     return a, g
 
 
-def utilities(Kh, Vh, Qg, M, Z, Y, toks, rK, rV):
+def utilities(Kh, Vh, Qg, M, Z, Y, toks, rK, rV, cs=None):
+    """Eq. utilities; with a rotation table cs, Kh are the rotated keys and
+    u^K uses R_t r^K_t."""
     Kh, Vh, Qg, M, Z, Y = map(_f64, (Kh, Vh, Qg, M, Z, Y))
     S, D = Kh.shape
     g, W, _ = Qg.shape
@@ -215,8 +252,14 @@ def utilities(Kh, Vh, Qg, M, Z, Y, toks, rK, rV):
     rK, rV = _f32(rK), _f32(rV)
     n = toks.shape[0]
     uK, uV = np.empty(n), np.empty(n)
-    lib().akvref_utilities(_p(Kh, _d), _p(Vh, _d), _p(Qg, _d), _p(M, _d), _p(Z, _d), _p(Y, _d), S, D, W, g,
-                           _p(toks, _i), n, _p(rK, _f), _p(rV, _f), _p(uK, _d), _p(uV, _d))
+    if cs is None:
+        lib().akvref_utilities(_p(Kh, _d), _p(Vh, _d), _p(Qg, _d), _p(M, _d), _p(Z, _d), _p(Y, _d), S, D, W, g,
+                               _p(toks, _i), n, _p(rK, _f), _p(rV, _f), _p(uK, _d), _p(uV, _d))
+    else:
+        cs = _f32(cs)
+        lib().akvref_utilities_rope(_p(Kh, _d), _p(Vh, _d), _p(Qg, _d), _p(M, _d), _p(Z, _d), _p(Y, _d), S, D, W,
+                                    g, _p(toks, _i), n, _p(rK, _f), _p(rV, _f), _p(cs, _f), _p(uK, _d),
+                                    _p(uV, _d))
     return uK, uV
 
 
@@ -233,8 +276,10 @@ def budget_select(u, N, per_head=False):
 
 def encode(K, V, Qobs, *, W, k, rho=0.7, kappa=7, bf16=True, seed=0, budget_mode=BUDGET_FRACTION,
            budget=0.05, budget_count=0, G=None, scale_mode=SCALE_ABSMAX_OUTER, anchor_override=None,
-           rank_mode=RANK_UTILITY, head_budget=0):
-    """Algorithm 1 for one request.  K, V: [H][S][D]; Qobs: [Hq][W][D]."""
+           rank_mode=RANK_UTILITY, head_budget=0, inv_freq=None):
+    """Algorithm 1 for one request.  K, V: [H][S][D]; Qobs: [Hq][W][D].  With
+    inv_freq ([D/2] rotation frequencies) K holds the unrotated keys and the
+    pass encodes positions as the paper does (Sec. 3.2)."""
     K, V, Qobs = _f64(K), _f64(V), _f64(Qobs)
     H, S, D = K.shape
     Hq = Qobs.shape[0]
@@ -247,10 +292,17 @@ def encode(K, V, Qobs, *, W, k, rho=0.7, kappa=7, bf16=True, seed=0, budget_mode
         codesV=np.empty((H, S, D // 4), np.uint8), scalesV=np.empty((H, S, D // G), np.float32),
         pooled=np.zeros((H, max(S - W, 1))), nsel=np.zeros(2, np.int64))
     ov = None if anchor_override is None else _i32(anchor_override)
-    rc = lib().akvref_encode(
-        H, Hq, D, S, W, k, rho, kappa, int(bf16), seed, budget_mode, budget, budget_count, G, scale_mode,
-        rank_mode, int(head_budget), _p(K, _d), _p(V, _d), _p(Qobs, _d), _p(ov, _i) if ov is not None else None,
-        _p(out["anchors"], _i), _p(out["aK"], _i), _p(out["gK"], _d), _p(out["aV"], _i), _p(out["gV"], _d),
+    head = (H, Hq, D, S, W, k, rho, kappa, int(bf16), seed, budget_mode, budget, budget_count, G, scale_mode,
+            rank_mode, int(head_budget), _p(K, _d), _p(V, _d), _p(Qobs, _d),
+            _p(ov, _i) if ov is not None else None)
+    if inv_freq is None:
+        fn = lib().akvref_encode
+    else:
+        invf = _f32(inv_freq)
+        head = head + (_p(invf, _f),)
+        fn = lib().akvref_encode_rope
+    rc = fn(
+        *head, _p(out["anchors"], _i), _p(out["aK"], _i), _p(out["gK"], _d), _p(out["aV"], _i), _p(out["gV"], _d),
         _p(out["uK"], _d), _p(out["uV"], _d), _p(out["selK"], _u8), _p(out["selV"], _u8),
         _p(out["codesK"], _u8), _p(out["scalesK"], _f), _p(out["codesV"], _u8), _p(out["scalesV"], _f),
         _p(out["pooled"], _d), _p(out["nsel"], _i64))
@@ -282,14 +334,21 @@ def reconstruct(X, enc, side: str, G, seed):
     return out
 
 
-def attention(Kt, Vt, q, scale=None):
-    """Softmax attention in fp64 over dense entries Kt, Vt [H][T][D]; q [Hq][D]."""
+def attention(Kt, Vt, q, scale=None, cs=None):
+    """Softmax attention in fp64 over dense entries Kt, Vt [H][T][D]; q [Hq][D].
+    With a rotation table cs ([>= T][D/2][2]) entry t sits at position t and
+    its key is rotated by R_t."""
     Kt, Vt, q = _f32(Kt), _f32(Vt), _f64(q)
     H, T, D = Kt.shape
     Hq = q.shape[0]
     scale = 1.0 / np.sqrt(D) if scale is None else float(scale)
     out = np.empty((Hq, D))
-    lib().akvref_attention(_p(Kt, _f), _p(Vt, _f), H, T, D, _p(q, _d), Hq, scale, _p(out, _d))
+    if cs is None:
+        lib().akvref_attention(_p(Kt, _f), _p(Vt, _f), H, T, D, _p(q, _d), Hq, scale, _p(out, _d))
+    else:
+        cs = _f32(cs)
+        assert cs.shape[0] >= T
+        lib().akvref_attention_rope(_p(Kt, _f), _p(Vt, _f), H, T, D, _p(q, _d), Hq, scale, _p(cs, _f), _p(out, _d))
     return out
 
 

@@ -186,3 +186,22 @@ def focused_queries(wl: Workload, K: List[torch.Tensor], steps: int, n_focus: in
                 q[:, b, j] = (rows + noise * torch.randn(steps, wl.D, generator=gen, device=device)).to(dt)
         Qs.append(Qb)
     return Qs, q
+
+
+def llama31_inv_freq(D: int = 128, base: float = 500000.0, factor: float = 8.0, low_freq_factor: float = 1.0,
+                     high_freq_factor: float = 4.0, original_context: int = 8192):
+    """Rotary frequencies of Llama-3.1 (rope_theta 500000 with the model's
+    long-context rescaling of the low frequencies), as fp32 numpy values
+    [D/2].  This is the model's positional encoding, an input of the
+    compression pass when keys are given before the rotation."""
+    import numpy as np
+    inv = 1.0 / (base ** (np.arange(0, D, 2, dtype=np.float64) / D))
+    wavelen = 2.0 * math.pi / inv
+    low_wl = original_context / low_freq_factor
+    high_wl = original_context / high_freq_factor
+    out = np.where(wavelen > low_wl, inv / factor, inv)
+    smooth = (original_context / wavelen - low_freq_factor) / (high_freq_factor - low_freq_factor)
+    smoothed = (1.0 - smooth) * out / factor + smooth * out
+    medium = (wavelen >= high_wl) & (wavelen <= low_wl)
+    out = np.where(medium, smoothed, out)
+    return out.astype(np.float32)
