@@ -288,6 +288,60 @@ def fidelity(args):
     print(json.dumps(res), flush=True)
 
 
+def rope_leg(args, akv, N, torch, synth, wl, layers, packed, caches, ws, out, steps=8):
+    """The same layers with their keys taken as the keys before RoPE and
+    Llama-3.1's rotary frequencies (Sec. 3.2; App. E): every layer's
+    compression pass, then `steps` decode steps (append + attention) over all
+    layers, timed apart from the main workload.  The caches of the main leg
+    are reused as storage."""
+    freq = synth.llama31_inv_freq(wl.D)
+    cfg = N.Config.make(num_kv_heads=wl.H, num_q_heads=wl.Hq, head_dim=wl.D, window=wl.window,
+                        anchor_frac=wl.anchor_frac, rho=0.7, kappa=7, budget=wl.budget, dtype=N.BF16,
+                        max_append=steps, seed=wl.seed, rope_inv_freq=freq)
+    plan = N.Plan(cfg, wl.seq_lens)
+    L = len(layers)
+    rws = torch.empty(plan.encode_ws_bytes, dtype=torch.uint8, device="cuda")
+    rdws = torch.empty(plan.decode_ws_bytes, dtype=torch.uint8, device="cuda")
+    assert plan.cache_bytes <= caches[0].numel()
+
+    def run(ev=None):
+        if ev:
+            ev[0].record()
+        for l in range(L):
+            K, V, Q = packed[l]
+            akv.encode(plan, K, V, Q, caches[l], rws)
+        if ev:
+            ev[1].record()
+        for s in range(steps):
+            for l in range(L):
+                lay = layers[l]
+                akv.decode_step(plan, caches[l], s, lay.k_new[s], lay.v_new[s], lay.q[s], out, rdws)
+        if ev:
+            ev[2].record()
+
+    run()
+    torch.cuda.synchronize()
+    kernels = ["k_dec_rope_scores", "k_dec_stream", "k_dec_front", "k_dec_merge", "k_rope_prep", "k_epilogue",
+               "k_obs64"]
+    timer = N.KernelTimer(kernels, max_launches=256)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    run(ev)
+    torch.cuda.synchronize()
+    kt = {}
+    for k in kernels:
+        ms, n = timer.read(k)
+        kt[k] = round(ms / max(n, 1) * 1e3, 3)
+    timer.close()
+    enc_ms, dec_ms = ev[0].elapsed_time(ev[1]), ev[1].elapsed_time(ev[2])
+    log(f"rope leg: encode {enc_ms / L:.3f} ms/layer, decode {dec_ms * 1e3 / (steps * L):.2f} us/layer-step")
+    del rws, rdws
+    return {"workload": wl.name + "-rope-llama31", "decode_steps": steps,
+            "decode_us_per_step": round(dec_ms * 1e3 / (steps * L), 3),
+            "encode_ms_per_layer": round(enc_ms / L, 4),
+            "encode_mtok_s": round(L * wl.seq_lens[0] / (enc_ms / 1e3) / 1e6, 3),
+            "kernel_avg_us": kt}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -296,6 +350,7 @@ def main():
     ap.add_argument("--layers", type=int, default=32)
     ap.add_argument("--decode-steps", type=int, default=64)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-rope", action="store_true", help="skip the leg with keys given before RoPE")
     ap.add_argument("--fidelity", action="store_true",
                     help="attention-output fidelity report of the method and its ablations instead of the benchmark")
     ap.add_argument("--fid-len", type=int, default=32768)
@@ -409,6 +464,10 @@ def main():
     ex = akv.export(plan, cache_host, 0, NS)
     fix_k, fix_v = int(ex["stats"][0]), int(ex["stats"][1])
 
+    rope = None
+    if not args.no_rope:
+        rope = rope_leg(args, akv, N, torch, synth, wl, layers, packed, caches, ws, out)
+
     cpu = None
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle on a bounded sample)")
@@ -445,6 +504,7 @@ def main():
                             "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": round(ach_e / BF16_PEAK_TFLOPS, 4),
                             "flops_per_launch": fl},
         "cpu_baseline": cpu,
+        "rope": rope,
     }
     print(json.dumps(res), flush=True)
 

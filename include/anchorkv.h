@@ -128,6 +128,21 @@ typedef struct anchorkv_config {
                              floor(N_side / H) (Sec. 4.3 ablation; needs batch * H <= 64) */
   int32_t append_mode;    /* an anchorkv_append_mode */
   uint64_t seed;          /* seeds the uniform anchor share, the Hadamard signs and the random ranking */
+  /* Rotary position encoding (Sec. 3.2 "RoPE"; App. E "Implementation").
+   * 0: the keys are used as given (no rotation).  1: K (encode) and k_new
+   * (append) hold keys BEFORE the rotation; the token at prompt position t
+   * (appended token n: position S + n) enters attention as R_t k, where R_t
+   * turns each rotate-half coordinate pair (f, f + D/2) by the angle
+   * t * rope_inv_freq[f] (the Llama convention: x cos + rotate_half(x) sin).
+   * The compression pass scores anchors and computes the attention weights
+   * and y_w with the rotated keys, projects and stores the unrotated keys,
+   * and ranks key residuals by q . R_t r (Eq. utilities); decode attention
+   * rotates every stored key at its position.  Q_obs and q are the rotated
+   * queries, as the model produces them.  The encode-side rotation uses the
+   * fp32 roundings of the fp64 cos and sin of the fp64 angle; decode
+   * evaluates them in fp32 within about 1e-6. */
+  int32_t rope;
+  float rope_inv_freq[64]; /* the D/2 frequencies (radians per position); unused entries ignored */
 } anchorkv_config;
 
 /* Derived per-request sizes (host memory). */

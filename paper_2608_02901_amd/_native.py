@@ -43,16 +43,25 @@ class Config(ctypes.Structure):
                 ("budget", ctypes.c_float), ("budget_count", ctypes.c_int64), ("quant_group", ctypes.c_int32),
                 ("scale_mode", ctypes.c_int32), ("dtype", ctypes.c_int32), ("max_append", ctypes.c_int32),
                 ("rank_mode", ctypes.c_int32), ("head_budget", ctypes.c_int32), ("append_mode", ctypes.c_int32),
-                ("seed", ctypes.c_uint64)]
+                ("seed", ctypes.c_uint64), ("rope", ctypes.c_int32), ("rope_inv_freq", ctypes.c_float * 64)]
 
     @classmethod
     def make(cls, *, num_kv_heads, num_q_heads, head_dim=128, window=32, anchor_count=0, anchor_frac=0.0,
              rho=0.7, kappa=7, budget_mode=BUDGET_FRACTION, budget=0.05, budget_count=0, quant_group=0,
              scale_mode=SCALE_ABSMAX_OUTER, dtype=BF16, max_append=0, rank_mode=RANK_UTILITY, head_budget=0,
-             append_mode=APPEND_ENCODED, seed=0):
+             append_mode=APPEND_ENCODED, seed=0, rope_inv_freq=None):
+        """rope_inv_freq: None (keys used as given) or the D/2 rotary
+        frequencies; then K and k_new are the keys before the rotation."""
+        freqs = (ctypes.c_float * 64)()
+        if rope_inv_freq is not None:
+            vals = [float(v) for v in rope_inv_freq]
+            if len(vals) != head_dim // 2:
+                raise ValueError("rope_inv_freq needs head_dim / 2 values")
+            for i, v in enumerate(vals):
+                freqs[i] = v
         return cls(num_kv_heads, num_q_heads, head_dim, window, anchor_count, anchor_frac, rho, kappa, budget_mode,
                    budget, budget_count, quant_group, scale_mode, dtype, max_append, rank_mode, head_budget,
-                   append_mode, seed)
+                   append_mode, seed, 1 if rope_inv_freq is not None else 0, freqs)
 
 
 class RequestInfo(ctypes.Structure):

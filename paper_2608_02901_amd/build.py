@@ -21,7 +21,7 @@ LIBDIR = os.path.join(PKG, "lib")
 LIB = os.path.join(LIBDIR, "libanchorkv.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
-SOURCES = ["anchorkv.cpp", "encode_obs.hip", "encode_obs64.hip", "encode_select.hip", "encode_assign.hip", "encode_epilogue.hip",
+SOURCES = ["anchorkv.cpp", "encode_rope.hip", "encode_obs.hip", "encode_obs64.hip", "encode_select.hip", "encode_assign.hip", "encode_epilogue.hip",
            "encode_budget.hip", "encode_layout.hip", "decode.hip"]
 
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-ffp-contract=off",

@@ -52,6 +52,8 @@ struct Geo {
   int oc64;                  // tokens per fp64 observation chunk
   int mpad;                  // m rounded up to 16 (rows of the fp64 partial outputs)
   int dsplit;                // decode split length (sorted slots per workgroup)
+  int rope;                  // keys are stored before the rotation and rotated at their positions
+  float invf[AKV_D / 2];     // rotation frequencies of the coordinate pairs (f, f + D/2)
 };
 
 // Per-slot arrays (records, position ids) give every head a stride of
@@ -183,6 +185,8 @@ struct Ws {
   int32_t* tiecnt;      // [b][side][nchunk] threshold ties in the earlier chunks
   int32_t* shist;       // [b][h][sort chunks + 1][k_b] per-chunk anchor histograms, then column prefixes; last row: anchor totals
   int32_t* wcnt;        // [side][b][h][ceil(S_b/64)] popcounts for the slot scan
+  void* krot;           // [b][h][S_b][D] dtype: rotated keys (positions encoded), else unused
+  float* cs;            // [maxS][D/2][2] fp32 cos, sin of the rotation of each position (positions encoded)
 };
 
 struct DecWs {
@@ -191,6 +195,7 @@ struct DecWs {
   float* part;          // [b][Hq][split][4 + D] split record (max, sum, -, -, output[D])
   float* asc;           // [side][b][h][kp_b] screening score of the appended token per anchor
   float4* atop;         // [side][b][h][4 ceil(k_b/256)] top-2 of those scores per 64 anchors
+  float* LK;            // [sorted slot][g] key logits with positions encoded (scaled to base 2)
 };
 
 // ------------------------------------------------------------------ vector types

@@ -20,13 +20,14 @@ namespace akv {
 hipError_t launch_init(const Geo& g, const Cache& c, const Ws& w, hipStream_t st);
 hipError_t launch_obs(const Geo& g, const Ws& w, const void* K, const void* Q, hipStream_t st);
 hipError_t launch_obs64(const Geo& g, const Ws& w, const void* K, const void* V, const void* Q, hipStream_t st);
-hipError_t launch_select(const Geo& g, const Ws& w, const Cache& c, const void* K, const void* V, const void* Q,
-                         const int32_t* ovr, hipStream_t st);
+hipError_t launch_rope(const Geo& g, const Ws& w, const void* K, hipStream_t st);
+hipError_t launch_select(const Geo& g, const Ws& w, const Cache& c, const void* K, const void* Kobs, const void* V,
+                         const void* Q, const int32_t* ovr, hipStream_t st);
 hipError_t launch_assign(const Geo& g, const Ws& w, const Cache& c, const void* K, const void* V, hipStream_t st);
-hipError_t launch_epilogue(const Geo& g, const Ws& w, const Cache& c, const void* K, const void* V, const void* Q,
-                           hipStream_t st);
-hipError_t launch_budget(const Geo& g, const Ws& w, const Cache& c, const void* K, const void* V, const void* Q,
-                         hipStream_t st);
+hipError_t launch_epilogue(const Geo& g, const Ws& w, const Cache& c, const void* K, const void* Kobs, const void* V,
+                           const void* Q, hipStream_t st);
+hipError_t launch_budget(const Geo& g, const Ws& w, const Cache& c, const void* K, const void* Kobs, const void* V,
+                         const void* Q, hipStream_t st);
 hipError_t launch_layout(const Geo& g, const Ws& w, const Cache& c, const void* K, const void* V, hipStream_t st);
 hipError_t launch_decode(const Geo& g, const Cache& c, const DecWs& dw, const void* q, const void* kn,
                          const void* vn, void* out, int out_dtype, float scale, int n_app, hipStream_t st);
@@ -109,10 +110,11 @@ struct anchorkv_plan {
   // encode workspace offsets
   size_t w_o64M, w_o64Z, w_o64O, w_M64, w_Z64, w_Y64, w_Y, w_Yhi, w_Ylo, w_ynorm,
       w_cw, w_qn, w_uL, w_uU, w_bandpos, w_bandu, w_brank, w_sc, w_rank, w_flag, w_sband, w_sbscore, w_sstate, w_sghist, w_scand, w_rkey, w_rpos, w_slcnt, w_QA, w_apos,
-      w_fix, w_fixcount, w_gpos, w_xn2, w_u, w_sel, w_srec, w_bhist, w_bstate, w_bcval, w_bcpos, w_tiecnt, w_shist, w_wcnt;
+      w_fix, w_fixcount, w_gpos, w_xn2, w_u, w_sel, w_srec, w_bhist, w_bstate, w_bcval, w_bcpos, w_tiecnt, w_shist, w_wcnt,
+      w_krot, w_cs;
   size_t ws_bytes;
   // decode workspace offsets
-  size_t d_SK, d_RK, d_part, d_asc, d_atop;
+  size_t d_SK, d_RK, d_part, d_asc, d_atop, d_LK;
   size_t dws_bytes;
 };
 
@@ -171,6 +173,11 @@ extern "C" anchorkv_status anchorkv_plan_create(const anchorkv_config* cfg, int3
   if (c.anchor_count == 0 && !(c.anchor_frac > 0.0f && c.anchor_frac <= 1.0f))
     return fail(ANCHORKV_ERR_INVALID_ARG, "anchor_frac must be in (0, 1] when anchor_count = 0");
   if (c.anchor_count < 0) return fail(ANCHORKV_ERR_INVALID_ARG, "anchor_count must be >= 0");
+  if (c.rope != 0 && c.rope != 1) return fail(ANCHORKV_ERR_INVALID_ARG, "rope must be 0 or 1");
+  if (c.rope)
+    for (int f = 0; f < c.head_dim / 2 && f < 64; ++f)
+      if (!(c.rope_inv_freq[f] >= 0.0f && c.rope_inv_freq[f] <= 1e6f))
+        return fail(ANCHORKV_ERR_INVALID_ARG, "rope_inv_freq must be finite and >= 0");
 
   anchorkv_plan* p = new (std::nothrow) anchorkv_plan();
   if (!p) return fail(ANCHORKV_ERR_INVALID_ARG, "out of host memory");
@@ -204,6 +211,8 @@ extern "C" anchorkv_status anchorkv_plan_create(const anchorkv_config* cfg, int3
   geo.max_append = c.max_append;
   geo.seed_anchor = mix64(c.seed ^ 1ull);
   geo.seed_sign = mix64(c.seed ^ 2ull);
+  geo.rope = c.rope;
+  for (int f = 0; f < D / 2; ++f) geo.invf[f] = c.rope ? c.rope_inv_freq[f] : 0.0f;
   geo.sgnbits[0] = geo.sgnbits[1] = 0;
   for (int j = 0; j < D; ++j)
     if (mix64(geo.seed_sign ^ (uint64_t)j) >> 63) geo.sgnbits[j >> 6] |= 1ull << (j & 63);
@@ -410,6 +419,8 @@ extern "C" anchorkv_status anchorkv_plan_create(const anchorkv_config* cfg, int3
   p->w_tiecnt = Wl.add(4 * 2 * (size_t)geo.prefBC[batch]);
   p->w_shist = Wl.add(4 * (size_t)geo.prefKT[batch]);
   p->w_wcnt = Wl.add(4 * 2 * TW);
+  p->w_krot = Wl.add(c.rope ? esz * TS * D : 0);
+  p->w_cs = Wl.add(c.rope ? 4 * (size_t)geo.maxS * D : 0);
   p->ws_bytes = Wl.total;
 
   Layout Dl;
@@ -418,6 +429,7 @@ extern "C" anchorkv_status anchorkv_plan_create(const anchorkv_config* cfg, int3
   p->d_part = Dl.add(4 * (size_t)geo.prefSp[batch] * geo.Hq * (4 + D));
   p->d_asc = Dl.add(4 * 2 * (size_t)geo.prefKp[batch] * H);
   p->d_atop = Dl.add(16 * 2 * 4 * (size_t)geo.prefAB[batch] * H);
+  p->d_LK = Dl.add(c.rope ? 4 * TSP * g : 0);
   p->dws_bytes = Dl.total;
   *out = p;
   return ANCHORKV_OK;
@@ -520,6 +532,8 @@ static akv::Ws ws_ptrs(const anchorkv_plan* p, void* base) {
   w.tiecnt = at<int32_t>(base, p->w_tiecnt);
   w.shist = at<int32_t>(base, p->w_shist);
   w.wcnt = at<int32_t>(base, p->w_wcnt);
+  w.krot = at<void>(base, p->w_krot);
+  w.cs = at<float>(base, p->w_cs);
   return w;
 }
 
@@ -530,6 +544,7 @@ static akv::DecWs dws_ptrs(const anchorkv_plan* p, void* base) {
   d.part = at<float>(base, p->d_part);
   d.asc = at<float>(base, p->d_asc);
   d.atop = at<float4>(base, p->d_atop);
+  d.LK = at<float>(base, p->d_LK);
   return d;
 }
 
@@ -571,14 +586,22 @@ extern "C" anchorkv_status anchorkv_encode(const anchorkv_plan* p, const void* K
   const Geo& g = p->geo;
   (void)hipGetLastError();
   if ((s = hip_status(akv::launch_init(g, c, w, st), "init")) != ANCHORKV_OK) return s;
-  if ((s = hip_status(akv::launch_obs64(g, w, K, V, Q_obs, st), "fp64 observation pass")) != ANCHORKV_OK) return s;
-  if ((s = hip_status(akv::launch_obs(g, w, K, Q_obs, st), "observation pass")) != ANCHORKV_OK) return s;
-  if ((s = hip_status(akv::launch_select(g, w, c, K, V, Q_obs, anchor_pos_override, st), "anchor selection")) !=
+  // With positions encoded the observation pass, the selection band and the
+  // attention weights of the utilities read the rotated keys; assignment,
+  // anchors, coefficients and residuals read the keys as given.
+  const void* Kobs = K;
+  if (g.rope) {
+    if ((s = hip_status(akv::launch_rope(g, w, K, st), "rotation")) != ANCHORKV_OK) return s;
+    Kobs = w.krot;
+  }
+  if ((s = hip_status(akv::launch_obs64(g, w, Kobs, V, Q_obs, st), "fp64 observation pass")) != ANCHORKV_OK) return s;
+  if ((s = hip_status(akv::launch_obs(g, w, Kobs, Q_obs, st), "observation pass")) != ANCHORKV_OK) return s;
+  if ((s = hip_status(akv::launch_select(g, w, c, K, Kobs, V, Q_obs, anchor_pos_override, st), "anchor selection")) !=
       ANCHORKV_OK)
     return s;
   if ((s = hip_status(akv::launch_assign(g, w, c, K, V, st), "assignment")) != ANCHORKV_OK) return s;
-  if ((s = hip_status(akv::launch_epilogue(g, w, c, K, V, Q_obs, st), "utilities")) != ANCHORKV_OK) return s;
-  if ((s = hip_status(akv::launch_budget(g, w, c, K, V, Q_obs, st), "budget")) != ANCHORKV_OK) return s;
+  if ((s = hip_status(akv::launch_epilogue(g, w, c, K, Kobs, V, Q_obs, st), "utilities")) != ANCHORKV_OK) return s;
+  if ((s = hip_status(akv::launch_budget(g, w, c, K, Kobs, V, Q_obs, st), "budget")) != ANCHORKV_OK) return s;
   if ((s = hip_status(akv::launch_layout(g, w, c, K, V, st), "layout")) != ANCHORKV_OK) return s;
   return fs.finish(ANCHORKV_OK);
 }

@@ -46,6 +46,64 @@ __device__ inline float level(const Geo& g, int code) {
 }
 
 
+// ------------------------------------------------------------------ positions
+// x - floor(x) for the finite, non-negative angles (in revolutions) below:
+// v_fract_f64 itself, without the compiler's guard for inputs just below an
+// integer (a result of 1.0 turns by a whole revolution, the same rotation).
+__device__ inline double fract64(double x) {
+  double r;
+  asm("v_fract_f64 %0, %1" : "=v"(r) : "v"(x));
+  return r;
+}
+
+// Keys are stored before the rotation when positions are encoded (Sec. 3.2
+// "RoPE"); decode rotates each key at its position (App. E
+// "Implementation").  The rotation of position p turns the coordinate pair
+// (f, f + D/2) by p * inv_freq[f].  Its cosine and sine are evaluated in
+// fp32 from the angle in revolutions, reduced in fp64 (p * inv_freq / 2 pi,
+// fractional part, centred to [-1/2, 1/2)) and passed to the hardware sine
+// and cosine, which take revolutions: within about 1e-6 of the fp32 table
+// of the compression pass, well inside attention's tolerance.
+__device__ inline void rope_cs(float invf, int p, float& c, float& s) {
+  const float r = (float)fract64((double)p * ((double)invf * 0.15915494309189535));
+  c = __builtin_amdgcn_cosf(r);
+  s = __builtin_amdgcn_sinf(r);
+}
+
+// Base-2 logits sl2 * q_j . R_p x of tail tokens n0 .. n1-1 into dst[n - n0][j]:
+// one wave per token (tokens wave, wave + 4, ...), lane f takes the pair
+// (f, f + 64) of x = fp32(gm a) (row and gm from row_of(n), p from pos_of(n))
+// and the GQ staged queries (qs: [j][D] fp32), then a wave sum per query.
+// Whole workgroup of 256 threads; dst is LDS, complete after the call.
+template <int DT, int GQ, typename RowOf, typename PosOf>
+__device__ inline void rope_tail_logits(const float* qs, const float* invs, RowOf row_of, PosOf pos_of, float sl2,
+                                        float (*dst)[GQ], int n0, int n1) {
+  using E = typename Elem<DT>::T;
+  constexpr int F = AKV_D / 2;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  float qa[GQ], qb[GQ];
+#pragma unroll
+  for (int jj = 0; jj < GQ; ++jj) {
+    qa[jj] = qs[jj * AKV_D + lane];
+    qb[jj] = qs[jj * AKV_D + lane + F];
+  }
+  const float invf = invs[lane];
+  for (int n = n0 + wave; n < n1; n += 4) {
+    float gm;
+    const E* row = row_of(n, gm);
+    const float a = gm * Elem<DT>::get(row, lane), bb = gm * Elem<DT>::get(row, lane + F);
+    float c, s;
+    rope_cs(invf, pos_of(n), c, s);
+    const float k0 = fmaf(c, a, -(s * bb)), k1 = fmaf(s, a, c * bb);
+#pragma unroll
+    for (int jj = 0; jj < GQ; ++jj) {
+      const float t = wave_sum_dpp(fmaf(qa[jj], k0, qb[jj] * k1));
+      if (lane == 0) dst[n - n0][jj] = t * sl2;
+    }
+  }
+  __syncthreads();
+}
+
 // Merge of two (best, second best, index of best) summaries of screening
 // scores; ties of the best go to the lower anchor index.
 __device__ inline void top2_merge(float& b1, float& b2, int& i1, float c1, float c2, int j1) {
@@ -586,7 +644,7 @@ __global__ __launch_bounds__(256) void k_app_finish(Geo g, Cache c, DecWs dw, in
 // gamma^V abar^V_{a^V}.  Runs beside the split workgroups of the stream pass.
 template <int DT, int GQ>
 __device__ void tail_block(const Geo& g, const Cache& c, const DecWs& dw, int bh, int n_app, const void* kin,
-                           const void* vin, unsigned char* pool) {
+                           const void* vin, const void* q, float sl2, unsigned char* pool) {
   using E = typename Elem<DT>::T;
   constexpr int D = AKV_D, TCH = 256;
   __shared__ int t_idx[2];
@@ -597,6 +655,10 @@ __device__ void tail_block(const Geo& g, const Cache& c, const DecWs& dw, int bh
   float(*tl)[GQ] = (float(*)[GQ])pool;
   int* tav = (int*)(pool + TCH * GQ * 4);
   float(*acc)[D] = (float(*)[D])(pool + TCH * GQ * 4 + TCH * 4);
+  // positions encoded: the queries, the frequencies and a chunk's logits
+  float* qsr = (float*)(pool + TCH * GQ * 4 + TCH * 4 + 8 * D * 4);
+  float* invs = qsr + GQ * D;
+  float(*tlg)[GQ] = (float(*)[GQ])(invs + D / 2);
   const int b = bh / g.H, h = bh % g.H;
   const int S = g.S[b], k = g.k[b], kp = (k + 3) & ~3;
   const int nsp = (S + g.dsplit - 1) / g.dsplit;
@@ -608,6 +670,12 @@ __device__ void tail_block(const Geo& g, const Cache& c, const DecWs& dw, int bh
   const float* SKh = dw.SK + ((size_t)g.prefKp[b] * g.H + (size_t)h * kp) * GQ;
   const E* AVg = (const E*)c.ancV + ko * D;
   const size_t tb = ((size_t)b * g.H + h) * g.max_append;
+  if (g.rope) {
+    const typename Elem<DT>::T* qg = (const typename Elem<DT>::T*)q + ((size_t)b * g.Hq + (size_t)h * GQ) * D;
+    for (int i = tid; i < GQ * D; i += 256) qsr[i] = Elem<DT>::get(qg, i);
+    if (tid < D / 2) invs[tid] = g.invf[tid];
+    __syncthreads();
+  }
   auto rec = [&](int n, int& ak, float& gk, int& av, float& gv) {
     if (app && n == n_app) {
       ak = t_idx[0];
@@ -621,18 +689,49 @@ __device__ void tail_block(const Geo& g, const Cache& c, const DecWs& dw, int bh
       gv = Elem<DT>::get(c.tgV, tb + n);
     }
   };
+  // With positions encoded the logits q . R_{S+n} (gamma abar_a) of a chunk
+  // of 256 tail tokens are formed first (one wave per token) into tlg.
+  auto rope_chunk = [&](int c0) {
+    rope_tail_logits<DT, GQ>(
+        qsr, invs,
+        [&](int n, float& gmo) {
+          int ak, av;
+          float gk, gv;
+          rec(n, ak, gk, av, gv);
+          gmo = gk;
+          return (const E*)c.ancK + (ko + ak) * D;
+        },
+        [&](int n) { return S + n; }, sl2, tlg, c0, min(ntail, c0 + TCH));
+  };
+  // Base-2 logit of tail token n (chunk c0): gamma S_K[a], or from tlg.
+  auto tlogit = [&](int n, int c0, int ak, float gk, float* l) {
+    if (g.rope) {
+#pragma unroll
+      for (int jj = 0; jj < GQ; ++jj) l[jj] = tlg[n - c0][jj];
+    } else {
+      float sk[GQ];
+      load_g<GQ>(SKh + (size_t)ak * GQ, sk);
+#pragma unroll
+      for (int jj = 0; jj < GQ; ++jj) l[jj] = gk * sk[jj];
+    }
+  };
   // Maxima over the whole tail (log2-domain logits).
   float mloc[GQ];
 #pragma unroll
   for (int jj = 0; jj < GQ; ++jj) mloc[jj] = -INFINITY;
-  for (int n = tid; n < ntail; n += 256) {
-    int ak, av;
-    float gk, gv;
-    rec(n, ak, gk, av, gv);
-    float sk[GQ];
-    load_g<GQ>(SKh + (size_t)ak * GQ, sk);
+  for (int c0 = 0; c0 < ntail; c0 += TCH) {
+    if (g.rope) rope_chunk(c0);
+    const int n = c0 + tid;
+    if (n < ntail) {
+      int ak, av;
+      float gk, gv;
+      rec(n, ak, gk, av, gv);
+      float sk[GQ];
+      tlogit(n, c0, ak, gk, sk);
 #pragma unroll
-    for (int jj = 0; jj < GQ; ++jj) mloc[jj] = fmaxf(mloc[jj], gk * sk[jj]);
+      for (int jj = 0; jj < GQ; ++jj) mloc[jj] = fmaxf(mloc[jj], sk[jj]);
+    }
+    if (g.rope) __syncthreads();  // tlg is refilled by the next chunk
   }
 #pragma unroll
   for (int jj = 0; jj < GQ; ++jj) {
@@ -654,15 +753,16 @@ __device__ void tail_block(const Geo& g, const Cache& c, const DecWs& dw, int bh
   for (int c0 = 0; c0 < ntail; c0 += TCH) {
     const int n = c0 + tid;
     __syncthreads();
+    if (g.rope) rope_chunk(c0);
     if (n < ntail) {
       int ak, av;
       float gk, gv;
       rec(n, ak, gk, av, gv);
       float sk[GQ];
-      load_g<GQ>(SKh + (size_t)ak * GQ, sk);
+      tlogit(n, c0, ak, gk, sk);
 #pragma unroll
       for (int jj = 0; jj < GQ; ++jj) {
-        const float p = __builtin_amdgcn_exp2f(gk * sk[jj] - M[jj]);
+        const float p = __builtin_amdgcn_exp2f(sk[jj] - M[jj]);
         lsum[jj] += p;
         tl[tid][jj] = p * gv;
       }
@@ -727,6 +827,8 @@ __device__ void tail_dense(const Geo& g, const Cache& c, const DecWs& dw, int bh
   float(*qs)[D] = (float(*)[D])pool;
   float(*tl)[GQ] = (float(*)[GQ])(pool + GQ * D * 4);
   float(*acc)[D] = (float(*)[D])(pool + GQ * D * 4 + TCH * GQ * 4);
+  float* invs = (float*)(pool + GQ * D * 4 + TCH * GQ * 4 + 8 * D * 4);  // positions encoded
+  float(*tlg)[GQ] = (float(*)[GQ])(invs + D / 2);                          // a chunk's rotated logits
   const int b = bh / g.H, h = bh % g.H;
   const int S = g.S[b];
   const int nsp = (S + g.dsplit - 1) / g.dsplit;
@@ -744,9 +846,27 @@ __device__ void tail_dense(const Geo& g, const Cache& c, const DecWs& dw, int bh
   }
   const E* qg = (const E*)q + ((size_t)b * g.Hq + (size_t)h * GQ) * D;
   for (int i = tid; i < GQ * D; i += 256) qs[i / D][i % D] = Elem<DT>::get(qg, i);
+  if (tid < D / 2) invs[tid] = g.invf[tid];
   __syncthreads();
-  auto logits = [&](int n, float* l) {
+  // With positions encoded the stored keys are unrotated: the logits
+  // q . R_{S+n} k_n of a chunk of 256 tokens are formed first (one wave per
+  // token) into tlg.
+  auto rope_chunk = [&](int c0) {
+    rope_tail_logits<DT, GQ>(
+        &qs[0][0], invs,
+        [&](int n, float& gmo) {
+          gmo = 1.0f;
+          return (app && n == n_app) ? kn : TK + (size_t)n * D;
+        },
+        [&](int n) { return S + n; }, sl2, tlg, c0, min(ntail, c0 + TCH));
+  };
+  auto logits = [&](int n, int c0, float* l) {
     const E* kr = (app && n == n_app) ? kn : TK + (size_t)n * D;
+    if (g.rope) {
+#pragma unroll
+      for (int jj = 0; jj < GQ; ++jj) l[jj] = tlg[n - c0][jj];
+      return;
+    }
 #pragma unroll
     for (int jj = 0; jj < GQ; ++jj) l[jj] = 0.0f;
     for (int d = 0; d < D; ++d) {
@@ -760,11 +880,16 @@ __device__ void tail_dense(const Geo& g, const Cache& c, const DecWs& dw, int bh
   float mloc[GQ];
 #pragma unroll
   for (int jj = 0; jj < GQ; ++jj) mloc[jj] = -INFINITY;
-  for (int n = tid; n < ntail; n += 256) {
-    float l[GQ];
-    logits(n, l);
+  for (int c0 = 0; c0 < ntail; c0 += TCH) {
+    if (g.rope) rope_chunk(c0);
+    const int n = c0 + tid;
+    if (n < ntail) {
+      float l[GQ];
+      logits(n, c0, l);
 #pragma unroll
-    for (int jj = 0; jj < GQ; ++jj) mloc[jj] = fmaxf(mloc[jj], l[jj]);
+      for (int jj = 0; jj < GQ; ++jj) mloc[jj] = fmaxf(mloc[jj], l[jj]);
+    }
+    if (g.rope) __syncthreads();  // tlg is refilled by the next chunk
   }
 #pragma unroll
   for (int jj = 0; jj < GQ; ++jj) {
@@ -785,9 +910,10 @@ __device__ void tail_dense(const Geo& g, const Cache& c, const DecWs& dw, int bh
   for (int c0 = 0; c0 < ntail; c0 += TCH) {
     const int n = c0 + tid;
     __syncthreads();
+    if (g.rope) rope_chunk(c0);
     if (n < ntail) {
       float l[GQ];
-      logits(n, l);
+      logits(n, c0, l);
 #pragma unroll
       for (int jj = 0; jj < GQ; ++jj) {
         const float p = __builtin_amdgcn_exp2f(l[jj] - M[jj]);
@@ -848,6 +974,225 @@ __global__ __launch_bounds__(AKV_D) void k_app_dense(Geo g, Cache c, int n_app, 
   const size_t ti = (bh * g.max_append + n_app) * AKV_D + d;
   Elem<DT>::put(c.tkd, ti, Elem<DT>::get(kin, bh * AKV_D + d));
   Elem<DT>::put(c.tvd, ti, Elem<DT>::get(vin, bh * AKV_D + d));
+}
+
+// Two fp32 values rounded to bf16 (round to nearest even) and packed, low first.
+__device__ inline uint32_t pk_bf16(float a, float b) {
+  typedef __attribute__((ext_vector_type(2))) float f2;
+  typedef __attribute__((ext_vector_type(2))) __bf16 b2;
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f2){a, b}, b2));
+}
+
+// Key logits of every stored slot with positions encoded: LK[slot][j] =
+// sl2 * q_j . R_p x^_p, p the slot's position and x^ = gamma abar (+ the
+// dequantized residual r~ for a slot in R_K) the unrotated reconstruction of
+// Eq. (reconstruction); R_p is linear, so the anchor part and the residual
+// part are rotated and contracted separately.  One wave per 64 slots (one
+// mask word):
+//  - residuals first, one at a time (about 3 per word at a 5 % budget): lane l
+//    holds coordinates 2l, 2l+1 of z^, the inverse Hadamard transform runs on
+//    DPP lane moves, lanes l and l ^ 32 exchange the halves of each
+//    rotate-half pair, and q_j . R_p r~ is a wave sum, kept in LDS per slot;
+//  - then four 16-slot MFMA tiles of gamma abar: lane l holds coordinates
+//    32 ks + 8 (l / 16) + e (ks < 4, e < 8) of slot l % 16, which pairs
+//    coordinate f with f + 64 inside the lane; the rotated rows are contracted
+//    with the g queries (bf16: hi and lo parts on v_mfma_f32_16x16x32_bf16;
+//    fp32: v_mfma_f32_16x16x4f32 in the same coordinate order).
+template <int DT, int GQ>
+__global__ __launch_bounds__(256) void k_dec_rope_scores(Geo g, Cache c, DecWs dw, const void* q, float sl2) {
+  using E = typename Elem<DT>::T;
+  constexpr int D = AKV_D, F = AKV_D / 2;
+  __shared__ float invs[F];
+  __shared__ float rl[4][64][GQ];  // per wave: residual logit terms of its 64 slots
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  if (tid < F) invs[tid] = g.invf[tid];
+  for (int i = lane; i < 64 * GQ; i += 64) (&rl[wave][0][0])[i] = 0.0f;
+  __syncthreads();
+  // Consecutive logical blocks (the words of one head) share an XCD, so a
+  // head's anchor rows stay in that XCD's L2.
+  int blk = blockIdx.x;
+  const int n8 = gridDim.x & ~7;
+  if (blk < n8) blk = (blk & 7) * (n8 >> 3) + (blk >> 3);
+  int gw = blk * 4 + wave;  // global mask word
+  int b = 0;
+  for (; b < g.B; ++b) {
+    const int n = g.H * ((g.S[b] + 63) / 64);
+    if (gw < n) break;
+    gw -= n;
+  }
+  if (b >= g.B) return;
+  const int S = g.S[b], k = g.k[b], nw = (S + 63) / 64;
+  const int h = gw / nw, wi = gw % nw;
+  const size_t so = slot_base(g, b, h) + (size_t)wi * 64;
+  const size_t wo = (size_t)g.prefW[b] * g.H + (size_t)h * nw + wi;
+  const size_t ko = (size_t)g.prefK[b] * g.H + (size_t)h * k;
+  const E* qg = (const E*)q + ((size_t)b * g.Hq + (size_t)h * GQ) * D;
+  const uint2 mw2 = *(const uint2*)&c.maskK[wo];
+  const unsigned long long mword = ((unsigned long long)__builtin_amdgcn_readfirstlane(mw2.y) << 32) |
+                                   (unsigned)__builtin_amdgcn_readfirstlane(mw2.x);  // wave-uniform
+
+  // ---- key residuals of the word: q_j . R_p r~
+  if (mword) {
+    const int pc0 = __builtin_amdgcn_readfirstlane(c.pcK[wo]);
+    float q0[GQ], q1[GQ];
+#pragma unroll
+    for (int jj = 0; jj < GQ; ++jj) {
+      q0[jj] = Elem<DT>::get(qg, (size_t)jj * D + 2 * lane);
+      q1[jj] = Elem<DT>::get(qg, (size_t)jj * D + 2 * lane + 1);
+    }
+    const float if0 = invs[(2 * lane) & (F - 1)], if1 = invs[(2 * lane + 1) & (F - 1)];
+    const float sg0 = sign_bit(g.sgnbits, 2 * lane), sg1 = sign_bit(g.sgnbits, 2 * lane + 1);
+    const float invD = 1.0f / (float)D;
+    const bool lo_half = lane < 32;
+    unsigned long long m = mword;
+    int rank = 0;
+    while (m) {
+      const int bit = __builtin_ctzll(m);
+      m &= m - 1ull;
+      const int slot = pc0 + rank++;
+      const int p = c.pos[so + bit];
+      const int nib = (c.codesK[(size_t)slot * (D / 4) + (lane >> 1)] >> (4 * (lane & 1))) & 15;
+      const float sc = c.scalesK[(size_t)slot * (D / g.G) + (2 * lane) / g.G];
+      float z0 = sc * level(g, nib & 3), z1 = sc * level(g, nib >> 2);
+      if (g.rot) {
+        fwht_wave_dpp(z0, z1, lane);
+        z0 = (z0 * invD) * sg0;
+        z1 = (z1 * invD) * sg1;
+      }
+      const float o0 = lane_xor<32>(z0), o1 = lane_xor<32>(z1);
+      float c0, s0, c1, s1;
+      rope_cs(if0, p, c0, s0);
+      rope_cs(if1, p, c1, s1);
+      // (r_f, r_{f+64}) -> (c r_f - s r_{f+64}, s r_f + c r_{f+64})
+      const float r0 = lo_half ? fmaf(c0, z0, -(s0 * o0)) : fmaf(s0, o0, c0 * z0);
+      const float r1 = lo_half ? fmaf(c1, z1, -(s1 * o1)) : fmaf(s1, o1, c1 * z1);
+#pragma unroll
+      for (int jj = 0; jj < GQ; ++jj) {
+        const float t = wave_sum_dpp(fmaf(q0[jj], r0, q1[jj] * r1));
+        if (lane == 0) rl[wave][bit][jj] = t;
+      }
+    }
+    // the tiles below read these terms from other lanes of this wave
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  }
+
+  // ---- anchor parts: four 16-slot MFMA tiles
+  const int i = lane & 15, kq = lane >> 4, col = i;
+  // frequencies of the lane's 16 pairs, in revolutions per position
+  double cf[2][8];
+#pragma unroll
+  for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) cf[ks][e] = (double)invs[32 * ks + 8 * kq + e] * 0.15915494309189535;
+  // queries as the B operand: lane supplies q_col[32 ks + 8 kq + e]
+  const bool qv = col < GQ;
+  const E* qp = qg + (size_t)(qv ? col : 0) * D;
+  bf16x8 bq[DT == 1 ? 4 : 1];
+  float qf[DT == 1 ? 1 : 4][8];
+  if constexpr (DT == 1) {
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+      const uint4 v = qv ? *(const uint4*)((const uint16_t*)qp + 32 * ks + 8 * kq) : make_uint4(0, 0, 0, 0);
+      bq[ks] = __builtin_bit_cast(bf16x8, v);
+    }
+  } else {
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) qf[ks][e] = qv ? Elem<DT>::get(qp, 32 * ks + 8 * kq + e) : 0.0f;
+  }
+  // records and anchor row chunks of one tile (loading the next tile's while
+  // processing the current one measured slower: 89 against 78 us per 128K
+  // layer-step, at three instead of four waves per SIMD)
+  constexpr int NCH = DT == 1 ? 4 : 8;  // 16-byte chunks of the lane's 32 coordinates
+  uint4 nxt[NCH];
+  float ngm = 0.0f;
+  int np = 0;
+  auto fetch = [&](int tile) {
+    const bool valid = wi * 64 + tile * 16 + i < S;
+    const size_t sl = so + tile * 16 + i;
+    const int a = valid ? min((int)c.idxK[sl], k - 1) : 0;
+    ngm = valid ? Elem<DT>::get(c.gK, sl) : 0.0f;
+    np = valid ? c.pos[sl] : 0;
+    const E* ar = (const E*)c.ancK + (ko + a) * D;
+#pragma unroll
+    for (int u = 0; u < NCH; ++u) {
+      const int ks = DT == 1 ? u : u >> 1;
+      nxt[u] = *(const uint4*)(ar + 32 * ks + 8 * kq + (DT == 1 ? 0 : 4 * (u & 1)));
+    }
+  };
+  for (int tile = 0; tile < 4; ++tile) {
+    fetch(tile);
+    uint4 cur[NCH];
+#pragma unroll
+    for (int u = 0; u < NCH; ++u) cur[u] = nxt[u];
+    const float gm = ngm;
+    const int p = np;
+    float x[4][8];
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+      if constexpr (DT == 1) {
+        const uint4 v = cur[ks];
+        const uint32_t w4[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          x[ks][2 * u] = gm * __uint_as_float(w4[u] << 16);
+          x[ks][2 * u + 1] = gm * __uint_as_float(w4[u] & 0xffff0000u);
+        }
+      } else {
+        const uint4 v0 = cur[2 * ks], v1 = cur[2 * ks + 1];
+        const float t8[8] = {__uint_as_float(v0.x), __uint_as_float(v0.y), __uint_as_float(v0.z),
+                             __uint_as_float(v0.w), __uint_as_float(v1.x), __uint_as_float(v1.y),
+                             __uint_as_float(v1.z), __uint_as_float(v1.w)};
+#pragma unroll
+        for (int e = 0; e < 8; ++e) x[ks][e] = gm * t8[e];
+      }
+    }
+    // rotation of the pairs (f, f + 64) held as (x[ks][e], x[ks + 2][e])
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        // revolutions in [0, 1): inside the hardware sine's input range
+        const float r = (float)fract64((double)p * cf[ks][e]);
+        const float cc = __builtin_amdgcn_cosf(r), ss = __builtin_amdgcn_sinf(r);
+        const float u = x[ks][e], v = x[ks + 2][e];
+        x[ks][e] = fmaf(cc, u, -(ss * v));
+        x[ks + 2][e] = fmaf(ss, u, cc * v);
+      }
+    f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
+    if constexpr (DT == 1) {
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) {
+        uint32_t hw[4], lw[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const float a0 = x[ks][2 * u], a1 = x[ks][2 * u + 1];
+          hw[u] = pk_bf16(a0, a1);
+          lw[u] = pk_bf16(a0 - __uint_as_float(hw[u] << 16), a1 - __uint_as_float(hw[u] & 0xffff0000u));
+        }
+        const bf16x8 ah = __builtin_bit_cast(bf16x8, make_uint4(hw[0], hw[1], hw[2], hw[3]));
+        const bf16x8 al = __builtin_bit_cast(bf16x8, make_uint4(lw[0], lw[1], lw[2], lw[3]));
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, bq[ks], acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al, bq[ks], acc, 0, 0, 0);
+      }
+    } else {
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(x[ks][e], qf[ks][e], acc, 0, 0, 0);
+    }
+    // lane holds rows 4 kq + r (slots) of column col (query head)
+    if (qv) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int row = tile * 16 + 4 * kq + r;
+        if (wi * 64 + row < S) dw.LK[(so + row) * GQ + col] = (acc[r] + rl[wave][row][col]) * sl2;
+      }
+    }
+  }
 }
 
 // ------------------------------------------------------------------ stream
@@ -919,7 +1264,8 @@ __global__ __launch_bounds__(256) void k_dec_stream(Geo g, Cache c, DecWs dw, in
   constexpr int NAVW = SW_AST * D / PER / 64;  // 16-byte anchor-row chunks per lane
   constexpr int ZY_B = 2 * 4 * GQ * D * 4;
   constexpr int WL_B = 4 * (int)sizeof(WL);
-  constexpr int TAIL_E = 256 * GQ * 4 + 256 * 4 + 8 * D * 4, TAIL_D = GQ * D * 4 + 256 * GQ * 4 + 8 * D * 4;
+  constexpr int TAIL_E = 256 * GQ * 4 + 256 * 4 + 8 * D * 4 + GQ * D * 4 + D * 2 + 256 * GQ * 4,
+                TAIL_D = GQ * D * 4 + 256 * GQ * 4 + 8 * D * 4 + D * 2 + 256 * GQ * 4;
   constexpr int TAIL_B = TAIL_E > TAIL_D ? TAIL_E : TAIL_D;
   constexpr int POOL_B = (WL_B > ZY_B ? WL_B : ZY_B) > TAIL_B ? (WL_B > ZY_B ? WL_B : ZY_B) : TAIL_B;
   __shared__ __align__(16) unsigned char pool[POOL_B];
@@ -928,7 +1274,7 @@ __global__ __launch_bounds__(256) void k_dec_stream(Geo g, Cache c, DecWs dw, in
     if (g.dense_tail)
       tail_dense<DT, GQ>(g, c, dw, (int)blockIdx.x - nst, n_app, kin, vin, q, sl2, pool);
     else
-      tail_block<DT, GQ>(g, c, dw, (int)blockIdx.x - nst, n_app, kin, vin, pool);
+      tail_block<DT, GQ>(g, c, dw, (int)blockIdx.x - nst, n_app, kin, vin, q, sl2, pool);
     return;
   }
   // Logical block id: consecutive ids (the splits of one head) share an XCD.
@@ -972,6 +1318,11 @@ __global__ __launch_bounds__(256) void k_dec_stream(Geo g, Cache c, DecWs dw, in
     float gk[R], gv[R];
     unsigned long long wk, wv;
     int pck, pcv;
+    float lg[R][GQ];
+    if (g.rope) {  // positions encoded: the slots' whole key logits (residuals included), by slot index
+#pragma unroll
+      for (int r = 0; r < R; ++r) load_g<GQ>(dw.LK + (so + i0c + r) * GQ, lg[r]);
+    }
     {
       constexpr int NU = R / 4;                       // uint2 words per index array
       constexpr int NG = DT == 1 ? R / 4 : R / 2;     // uint2 words per coefficient array
@@ -1048,9 +1399,14 @@ __global__ __launch_bounds__(256) void k_dec_stream(Geo g, Cache c, DecWs dw, in
     const int nrange = a_hi - a_lo + 1, nstage = min(nrange, SW_AST), nvres = pv_hi - pv_lo;
 
     // ---- round 2: anchor scores, key-residual terms, anchor rows, first value residuals.
-    float lg[R][GQ], rk[R][GQ];
+    float rk[R][GQ];
 #pragma unroll
     for (int r = 0; r < R; ++r) {
+      if (g.rope) {  // the logits were loaded with the records
+#pragma unroll
+        for (int jj = 0; jj < GQ; ++jj) rk[r][jj] = 0.0f;
+        continue;
+      }
       load_g<GQ>(SKh + (size_t)min((int)ik[r], k - 1) * GQ, lg[r]);
       if ((bk >> r) & 1u) {
         load_g<GQ>(dw.RK + (size_t)(pck + __popc(bk & ((1u << r) - 1u))) * GQ, rk[r]);
@@ -1096,10 +1452,12 @@ __global__ __launch_bounds__(256) void k_dec_stream(Geo g, Cache c, DecWs dw, in
     load_vchunk(0, vc0, vc1, vsv);
 
     // ---- logits (base 2) and this wave's softmax statistics.
+    if (!g.rope) {
 #pragma unroll
-    for (int r = 0; r < R; ++r)
+      for (int r = 0; r < R; ++r)
 #pragma unroll
-      for (int jj = 0; jj < GQ; ++jj) lg[r][jj] = fmaf(gk[r], lg[r][jj], rk[r][jj]);
+        for (int jj = 0; jj < GQ; ++jj) lg[r][jj] = fmaf(gk[r], lg[r][jj], rk[r][jj]);
+    }
 #pragma unroll
     for (int jj = 0; jj < GQ; ++jj) {
       float v = -INFINITY;
@@ -1452,15 +1810,25 @@ static void launch_steps(const Geo& g, const Cache& c, const DecWs& dw, const vo
     launch("k_app_dense", k_app_dense<DT>, dim3(g.B * g.H), dim3(AKV_D), 0, st, g, c, n_app, kn, vn);
     return;
   }
-  const int nAK = g.H * g.prefAB[g.B];
-  const int nAV = screen ? nAK : 0;
-  const int nR = attn ? (g.prefNK[g.B] + RK_PER_BLOCK - 1) / RK_PER_BLOCK : 0;
-  const int flags = (attn ? 1 : 0) | (screen ? 2 : 0);
+  // With positions encoded the anchor scores and key-residual terms are
+  // replaced by the per-slot logits of k_dec_rope_scores; the front kernel
+  // then only screens an appended token.
+  const bool sk = attn && !g.rope;
+  const int nAK = (sk || screen) ? g.H * g.prefAB[g.B] : 0;
+  const int nAV = screen ? g.H * g.prefAB[g.B] : 0;
+  const int nR = sk ? (g.prefNK[g.B] + RK_PER_BLOCK - 1) / RK_PER_BLOCK : 0;
+  const int flags = (sk ? 1 : 0) | (screen ? 2 : 0);
   const float sl2 = scale * 1.4426950408889634f;
-  launch("k_dec_front", k_dec_front<DT, GQ>, dim3(nAK + nAV + nR), dim3(256), 0, st, g, c, dw, q, kn, vn, flags, nAK, nAV, sl2);
+  if (nAK + nAV + nR > 0)
+    launch("k_dec_front", k_dec_front<DT, GQ>, dim3(nAK + nAV + nR), dim3(256), 0, st, g, c, dw, q, kn, vn, flags, nAK,
+           nAV, sl2);
   if (!attn) {
     launch("k_app_finish", k_app_finish<DT>, dim3(g.B * g.H), dim3(256), 0, st, g, c, dw, n_app, kn, vn);
     return;
+  }
+  if (g.rope) {
+    const int nwords = g.H * g.prefW[g.B];
+    launch("k_dec_rope_scores", k_dec_rope_scores<DT, GQ>, dim3((nwords + 3) / 4), dim3(256), 0, st, g, c, dw, q, sl2);
   }
   const int L = g.dsplit;
   int nst = 0;

@@ -475,10 +475,11 @@ __global__ __launch_bounds__(256) void k_bmark(Geo g, Ws w) {
 // selector score, 0 inside the window); the other ablation keys come from
 // rank_key64 on one lane.
 template <int DT>
-__global__ __launch_bounds__(256) void k_brescore(Geo g, Ws w, Cache c, const void* Kin, const void* Vin,
-                                                  const void* Qin) {
+__global__ __launch_bounds__(256) void k_brescore(Geo g, Ws w, Cache c, const void* Kin, const void* Kobs,
+                                                  const void* Vin, const void* Qin) {
   using E = typename Elem<DT>::T;
   __shared__ float xs[4][AKV_D], vs[4][AKV_D], rs[4][AKV_D];
+  __shared__ double rr[4][AKV_D];  // R_t r_K in fp64 (positions encoded)
   __shared__ double terms[4][256];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int nw = gridDim.x * 4;
@@ -506,7 +507,7 @@ __global__ __launch_bounds__(256) void k_brescore(Geo g, Ws w, Cache c, const vo
       const float gm = w.gpos[side * TS + po + t];
       const E* xr = (const E*)(side ? Vin : Kin) + xo;
       const E* ar = (const E*)(side ? c.ancV : c.ancK) + (ko + a) * D;
-      const E* kr = (const E*)Kin + xo;
+      const E* kr = (const E*)Kobs + xo;  // the keys of the logits (rotated when positions are encoded)
       const E* vr = (const E*)Vin + xo;
       const bool att = g.rank_mode == RANK_ATTENTION;
       if ((g.rank_mode != RANK_UTILITY && !att) || (att && t >= S - g.W)) {  // uniform per wave
@@ -521,6 +522,18 @@ __global__ __launch_bounds__(256) void k_brescore(Geo g, Ws w, Cache c, const vo
       }
       __builtin_amdgcn_wave_barrier();
       __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+      const bool rot = g.rope && side == 0;
+      if (rot) {
+        // (c r_f - s r_{f+D/2}, s r_f + c r_{f+D/2}) in fp64: exact products
+        // of fp32 factors, one rounding per coordinate, as the oracle forms it
+        const int f = lane;
+        const float2 cv = *(const float2*)&w.cs[(size_t)t * D + 2 * f];
+        const double cd = cv.x, sd = cv.y, a = rs[wave][f], bb = rs[wave][f + D / 2];
+        rr[wave][f] = cd * a - sd * bb;
+        rr[wave][f + D / 2] = sd * a + cd * bb;
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+      }
       double rvn = 0.0;
       if (side == 1)
         for (int j = 0; j < D; ++j) rvn += (double)rs[wave][j] * (double)rs[wave][j];
@@ -540,7 +553,7 @@ __global__ __launch_bounds__(256) void k_brescore(Geo g, Ws w, Cache c, const vo
           for (int e = 0; e < PER; ++e) {
             const double qe = (double)Elem<DT>::get(&cur, e);
             l += qe * (double)xs[wave][c4 * PER + e];
-            qr += qe * (double)rs[wave][c4 * PER + e];
+            qr += qe * (rot ? rr[wave][c4 * PER + e] : (double)rs[wave][c4 * PER + e]);
           }
           cur = nxt;
         }
@@ -643,8 +656,8 @@ __global__ __launch_bounds__(256) void k_bsel(Geo g, Ws w, Cache c) {
     sel[w.bandpos[(size_t)bs * BAND_CAP + i]] = w.brank[(size_t)bs * BAND_CAP + i] < need ? 1 : 0;
 }
 
-hipError_t launch_budget(const Geo& g, const Ws& w, const Cache& c, const void* K, const void* V, const void* Q,
-                         hipStream_t st) {
+hipError_t launch_budget(const Geo& g, const Ws& w, const Cache& c, const void* K, const void* Kobs, const void* V,
+                         const void* Q, hipStream_t st) {
   int nblk = 0, nkey = 0;
   const int nl = g.B * g.hdiv;
   for (int L = 0; L < nl; ++L) nblk += 2 * (((g.H / g.hdiv) * g.S[L / g.hdiv] + BCHUNK - 1) / BCHUNK);
@@ -661,9 +674,9 @@ hipError_t launch_budget(const Geo& g, const Ws& w, const Cache& c, const void* 
   launch("k_bbound", k_bbound, dim3(nblk), dim3(256), 0, st, g, w);
   launch("k_bmark", k_bmark, dim3(nblk), dim3(256), 0, st, g, w);
   if (g.dtype == 1)
-    launch("k_brescore", k_brescore<1>, dim3(1024), dim3(256), 0, st, g, w, c, K, V, Q);
+    launch("k_brescore", k_brescore<1>, dim3(1024), dim3(256), 0, st, g, w, c, K, Kobs, V, Q);
   else
-    launch("k_brescore", k_brescore<0>, dim3(1024), dim3(256), 0, st, g, w, c, K, V, Q);
+    launch("k_brescore", k_brescore<0>, dim3(1024), dim3(256), 0, st, g, w, c, K, Kobs, V, Q);
   launch("k_brank", k_brank, dim3(2048), dim3(RANK_T), 0, st, g, w);
   launch("k_bsel", k_bsel, dim3(64, nl * 2), dim3(256), 0, st, g, w, c);
   return hipGetLastError();

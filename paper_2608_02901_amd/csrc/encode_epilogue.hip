@@ -10,12 +10,16 @@
 // bound decides the rounded value when its whole error interval rounds alike
 // (nearly always); otherwise the sequential fp64 sum is formed.
 //
-// Utilities (fp32, no positional rotation on this path, R_t = I):
-//   uK_t = (1/m) sum_w alpha_wt^2 (q_w . rK_t)^2 / D * ||v_t - y_w||^2
+// Utilities (fp32):
+//   uK_t = (1/m) sum_w alpha_wt^2 (q_w . R_t rK_t)^2 / D * ||v_t - y_w||^2
 //   uV_t = (1/m) sum_w alpha_wt^2 ||rV_t||^2
-// with q_w . rK_t = q_w . k_t - gamma_t (q_w . abar_a(t)) (the second term from
-// the QA table), ||v_t - y_w||^2 = ||v_t||^2 - 2 v_t . y_w + ||y_w||^2 and the
-// logits and v_t . y_w on MFMA; anchors get u = -1 and never compete.
+// with ||v_t - y_w||^2 = ||v_t||^2 - 2 v_t . y_w + ||y_w||^2 and the logits and
+// v_t . y_w on MFMA; anchors get u = -1 and never compete.  Without positions
+// (R_t = I) q_w . rK_t = q_w . k_t - gamma_t (q_w . abar_a(t)), the second term
+// from the QA table.  With positions encoded (RP) the logits come from the
+// rotated keys and q_w . R_t rK_t from a second contraction over the tile of
+// rotated residuals R_t (k_t - fp32(gamma abar)), split into bf16 hi + lo parts
+// for a bf16 cache.
 //
 // Schedule: first the 2 x EPI_TOK coefficient chains of the workgroup's
 // tokens (four per thread, spread over all waves), then the utilities tile by
@@ -37,9 +41,9 @@ __device__ __attribute__((noinline)) double dot64_rows(const typename Elem<DT>::
   return dot64_seq<DT, true>(x, a, AKV_D);
 }
 
-template <int DT, int R>
-__global__ __launch_bounds__(256, R == 1 ? 2 : 1) void k_epilogue(Geo g, Ws w, Cache c, const void* Kin, const void* Vin,
-                                                  const void* Qin) {
+template <int DT, int R, bool RP>
+__global__ __launch_bounds__(256, R == 1 ? 2 : 1) void k_epilogue(Geo g, Ws w, Cache c, const void* Kin,
+                                                                  const void* Kobs, const void* Vin, const void* Qin) {
   using E = typename Elem<DT>::T;
   using M = MF<DT>;
   constexpr int LD = AKV_D + (DT ? 8 : 4);
@@ -50,6 +54,9 @@ __global__ __launch_bounds__(256, R == 1 ? 2 : 1) void k_epilogue(Geo g, Ws w, C
   constexpr int NT = EPI_TOK / 32;
   __shared__ __align__(16) E KT[32 * LD];
   __shared__ __align__(16) E VT[32 * LD];
+  // rotated key residuals of the tile (RP): fp32, or bf16 hi and lo parts
+  __shared__ __align__(16) E RTh[RP ? 32 * LD : 1];
+  __shared__ __align__(16) E RTl[RP && DT == 1 ? 32 * LD : 1];
   __shared__ float gK_s[EPI_TOK], rv2_s[EPI_TOK], vn_s[EPI_TOK], rk2_s[EPI_TOK];
   __shared__ int aK_s[EPI_TOK];
   // Row sums per token: each wave leaves its partials of a tile in tpart
@@ -71,6 +78,7 @@ __global__ __launch_bounds__(256, R == 1 ? 2 : 1) void k_epilogue(Geo g, Ws w, C
   const size_t xoff = ((size_t)g.prefS[b] * g.H + (size_t)h * S) * D;
   const E* Kx = (const E*)Kin + xoff;
   const E* Vx = (const E*)Vin + xoff;
+  const E* Ko = (const E*)(RP ? Kobs : Kin) + xoff;  // keys of the logits
   const size_t po = (size_t)g.prefS[b] * g.H + (size_t)h * S;
   const size_t TS = (size_t)g.prefS[g.B] * g.H;  // per-side stride of the position arrays
   const size_t ko = (size_t)g.prefK[b] * g.H + (size_t)h * k;
@@ -231,7 +239,7 @@ __global__ __launch_bounds__(256, R == 1 ? 2 : 1) void k_epilogue(Geo g, Ws w, C
       kpre[i] = make_uint4(0, 0, 0, 0);
       vpre[i] = make_uint4(0, 0, 0, 0);
       if (t0 + r < S) {
-        kpre[i] = *(const uint4*)(Kx + (size_t)(t0 + r) * D + col);
+        kpre[i] = *(const uint4*)(Ko + (size_t)(t0 + r) * D + col);
         vpre[i] = *(const uint4*)(Vx + (size_t)(t0 + r) * D + col);
       }
     }
@@ -255,6 +263,61 @@ __global__ __launch_bounds__(256, R == 1 ? 2 : 1) void k_epilogue(Geo g, Ws w, C
       *(uint4*)(&KT[r * LD + col]) = kpre[i];
       *(uint4*)(&VT[r * LD + col]) = vpre[i];
     }
+    if constexpr (RP) {
+      // Rotated key residuals: thread = (token tid / 8, pairs 8 (tid % 8) ..
+      // +7).  r = x - fp32(gamma abar) (the residual the codec sees), then
+      // (c r_f - s r_{f+64}, s r_f + c r_{f+64}) in fp32; zero for anchors and
+      // rows past S.
+      const int rr = threadIdx.x >> 3, f0 = 8 * (threadIdx.x & 7);
+      const int tl = 32 * it + rr, t = t0 + rr;
+      const int ak = aK_s[tl];
+      float xr[16], ar[16];
+#pragma unroll
+      for (int i = 0; i < 16; ++i) xr[i] = ar[i] = 0.0f;
+      float2 csv[8];
+      if (ak >= 0) {
+        const E* xrow = Kx + (size_t)t * D;
+        const E* arow = (const E*)c.ancK + (ko + ak) * D;
+#pragma unroll
+        for (int hf = 0; hf < 2; ++hf)
+#pragma unroll
+          for (int i = 0; i < 8; i += PER) {
+            const uint4 xv4 = *(const uint4*)(xrow + f0 + 64 * hf + i);
+            const uint4 av4 = *(const uint4*)(arow + f0 + 64 * hf + i);
+#pragma unroll
+            for (int e = 0; e < PER && i + e < 8; ++e) {
+              xr[8 * hf + i + e] = Elem<DT>::get(&xv4, e);
+              ar[8 * hf + i + e] = Elem<DT>::get(&av4, e);
+            }
+          }
+#pragma unroll
+        for (int i = 0; i < 8; i += 2) {
+          const float4 cv = *(const float4*)&w.cs[(size_t)t * D + 2 * (f0 + i)];
+          csv[i] = make_float2(cv.x, cv.y);
+          csv[i + 1] = make_float2(cv.z, cv.w);
+        }
+      } else {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) csv[i] = make_float2(0.0f, 0.0f);
+      }
+      const float gk = gK_s[tl];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const float r0 = xr[i] - gk * ar[i], r1 = xr[8 + i] - gk * ar[8 + i];
+        const float o0 = fmaf(csv[i].x, r0, -(csv[i].y * r1));
+        const float o1 = fmaf(csv[i].y, r0, csv[i].x * r1);
+        if constexpr (DT == 1) {
+          const uint16_t h0 = f2bf(o0), h1 = f2bf(o1);
+          RTh[rr * LD + f0 + i] = h0;
+          RTh[rr * LD + f0 + 64 + i] = h1;
+          RTl[rr * LD + f0 + i] = f2bf(o0 - bf2f(h0));
+          RTl[rr * LD + f0 + 64 + i] = f2bf(o1 - bf2f(h1));
+        } else {
+          RTh[rr * LD + f0 + i] = o0;
+          RTh[rr * LD + f0 + 64 + i] = o1;
+        }
+      }
+    }
     __syncthreads();
     if (it + 1 < ntl) fetch(t0 + 32);
     const int tl = 32 * it + (lane & 31);
@@ -269,27 +332,34 @@ __global__ __launch_bounds__(256, R == 1 ? 2 : 1) void k_epilogue(Geo g, Ws w, C
     for (int r = 0; r < R; ++r) {
       const int rb = wave + 4 * r;
       if (rb >= nrb) break;
-      float qv[16];
+      float qv[RP ? 1 : 16];
+      if constexpr (!RP) {
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int w0 = rb * 32 + j * 8 + (lane >> 5) * 4;
-        if ((m & 3) == 0) {
-          const float4 q4 = *(const float4*)(qa + min(w0, m - 4));
-          qv[4 * j] = q4.x; qv[4 * j + 1] = q4.y; qv[4 * j + 2] = q4.z; qv[4 * j + 3] = q4.w;
-        } else {
+        for (int j = 0; j < 4; ++j) {
+          const int w0 = rb * 32 + j * 8 + (lane >> 5) * 4;
+          if ((m & 3) == 0) {
+            const float4 q4 = *(const float4*)(qa + min(w0, m - 4));
+            qv[4 * j] = q4.x; qv[4 * j + 1] = q4.y; qv[4 * j + 2] = q4.z; qv[4 * j + 3] = q4.w;
+          } else {
 #pragma unroll
-          for (int i = 0; i < 4; ++i) qv[4 * j + i] = qa[min(w0 + i, m - 1)];
+            for (int i = 0; i < 4; ++i) qv[4 * j + i] = qa[min(w0 + i, m - 1)];
+          }
         }
       }
-      f32x16 accL = {}, accY = {};
+      f32x16 accL = {}, accY = {}, accR = {};
 #pragma unroll
       for (int s = 0; s < NKS; ++s) {
         const int k0 = kofs(M::KS, s, lane);
         const auto kb = M::load_lds(&KT[(lane & 31) * LD], k0);
         const auto vb = M::load_lds(&VT[(lane & 31) * LD], k0);
-        accL = M::mma(M::load_lds(&QS[(min(rb * 32 + (lane & 31), m - 1)) * LD], k0), kb, accL);
+        const auto qf = M::load_lds(&QS[(min(rb * 32 + (lane & 31), m - 1)) * LD], k0);
+        accL = M::mma(qf, kb, accL);
         accY = M::mma(yh[r][s], vb, accY);
         if constexpr (DT == 1) accY = M::mma(yl[r][s], vb, accY);
+        if constexpr (RP) {
+          accR = M::mma(qf, M::load_lds(&RTh[(lane & 31) * LD], k0), accR);
+          if constexpr (DT == 1) accR = M::mma(qf, M::load_lds(&RTl[(lane & 31) * LD], k0), accR);
+        }
       }
       if (ak >= 0) {
 #pragma unroll
@@ -304,7 +374,9 @@ __global__ __launch_bounds__(256, R == 1 ? 2 : 1) void k_epilogue(Geo g, Ws w, C
             const float l = accL[e];
             const float al = __builtin_amdgcn_exp2f(fmaf(l, isl, -cq[i]));
             const float a2 = al * al;
-            const float qr = fmaf(-gk, qv[e], l);
+            float qr;
+            if constexpr (RP) qr = accR[e];
+            else qr = fmaf(-gk, qv[e], l);
             // ||v - y||^2 >= 0: the cancellation form can dip below zero
             // when y nearly equals v; the bounds below cover the clamp.
             const float vv = fmaxf(fmaf(-2.0f, accY[e], vn + yq[i]), 0.0f);
@@ -366,7 +438,10 @@ __global__ __launch_bounds__(256, R == 1 ? 2 : 1) void k_epilogue(Geo g, Ws w, C
         uk = sk / ((float)m * (float)D);
         uv = rv2_s[tl] * sv / (float)m;
         // token quantities (upper bounds of the norms)
-        const float kn = sqrtf(w.xn2[po + t] * (1.0f + 300.0f * U)) * (1.0f + 2.0f * U);
+        // the logits' keys: the token, or its rotation rounded to the dtype
+        // (|R_t k| = |k| up to the fp32 table, then one fp32 and one bf16 rounding)
+        const float kn = sqrtf(w.xn2[po + t] * (1.0f + 300.0f * U)) * (1.0f + 2.0f * U) *
+                         (RP ? (DT == 1 ? 1.0079f : 1.0001f) : 1.0f);
         const float vn2 = vn_s[tl] * (1.0f + 300.0f * U);
         const float vnm = sqrtf(vn2) * (1.0f + 2.0f * U);
         const float gk = fabsf(gK_s[tl]);
@@ -375,7 +450,15 @@ __global__ __launch_bounds__(256, R == 1 ? 2 : 1) void k_epilogue(Geo g, Ws w, C
         const float qk = qmax * kn * isl1;
         const float eta = 0.6931472f * (C1 * qk + U * (3.0f * qk + 2.0f * cmax)) + 4.0f * U;
         const float ea = eta * (1.0f + eta) * 1.0001f;
-        const float e = qmax * (kn + gk * an) * (C1 + 4.0f * U) * 1.0001f;
+        // |qr32 - q.R_t r| <= e.  Without positions: the logit and QA-table
+        // MFMA errors and the residual's rounding.  With positions: the
+        // rotation's two fp32 roundings per coordinate (2u |r|), the hi/lo
+        // split (2^-18 |r|), the MFMA over the hi and lo chains (2 C1, or C1
+        // for fp32) and, for an fp32 cache, the difference of the fused and
+        // the canonical residual (2u |gamma| |a|).
+        const float e = RP ? qmax * (rkn + (DT == 1 ? 0.0f : 2.1f * U * gk * an)) *
+                                 (2.0002f * U + (DT == 1 ? 3.82e-6f + 2.0079f * C1 : C1) + 1e-15f) * 1.0001f
+                           : qmax * (kn + gk * an) * (C1 + 4.0f * U) * 1.0001f;
         const float dvv = (258.0f * U * vn2 + 4.0f * U * ymax2 + 9.3e-5f * vnm * ymax) * 1.0001f;
         const float V2 = (vnm + ymax) * (vnm + ymax) * 1.0001f + dvv;
         const float qr1 = qmax * rkn + e;
@@ -417,29 +500,38 @@ __global__ __launch_bounds__(256, R == 1 ? 2 : 1) void k_epilogue(Geo g, Ws w, C
   }
 }
 
-hipError_t launch_epilogue(const Geo& g, const Ws& w, const Cache& c, const void* K, const void* V, const void* Q,
-                           hipStream_t st) {
-  int nblk = 0;
-  for (int b = 0; b < g.B; ++b) nblk += g.H * ((g.S[b] + EPI_TOK - 1) / EPI_TOK);
-  const bool r2 = g.m > 128;  // 4 waves x 2 row blocks of 32 for up to 256 rows
-  const uint32_t qlds = (uint32_t)g.m * (AKV_D + (g.dtype == 1 ? 8 : 4)) * (g.dtype == 1 ? 2 : 4);
+template <int DT, int R, bool RP>
+static hipError_t launch_epi_t(const Geo& g, const Ws& w, const Cache& c, const void* K, const void* Kobs,
+                               const void* V, const void* Q, int nblk, uint32_t qlds, hipStream_t st) {
   // With 256 observation rows the staged rows and the kernel's static arrays
   // pass 64 KiB; the kernel then asks for the larger LDS allocation gfx950
   // offers.
   if (qlds > 32768) {
-    const void* f = g.dtype == 1 ? (r2 ? (const void*)k_epilogue<1, 2> : (const void*)k_epilogue<1, 1>)
-                                 : (r2 ? (const void*)k_epilogue<0, 2> : (const void*)k_epilogue<0, 1>);
-    const hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, (int)qlds);
+    const hipError_t e =
+        hipFuncSetAttribute((const void*)k_epilogue<DT, R, RP>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)qlds);
     if (e != hipSuccess) return e;
   }
-  if (g.dtype == 1) {
-    if (r2) launch("k_epilogue", k_epilogue<1, 2>, dim3(nblk), dim3(256), qlds, st, g, w, c, K, V, Q);
-    else launch("k_epilogue", k_epilogue<1, 1>, dim3(nblk), dim3(256), qlds, st, g, w, c, K, V, Q);
-  } else {
-    if (r2) launch("k_epilogue", k_epilogue<0, 2>, dim3(nblk), dim3(256), qlds, st, g, w, c, K, V, Q);
-    else launch("k_epilogue", k_epilogue<0, 1>, dim3(nblk), dim3(256), qlds, st, g, w, c, K, V, Q);
-  }
+  launch("k_epilogue", k_epilogue<DT, R, RP>, dim3(nblk), dim3(256), qlds, st, g, w, c, K, Kobs, V, Q);
   return hipGetLastError();
+}
+
+hipError_t launch_epilogue(const Geo& g, const Ws& w, const Cache& c, const void* K, const void* Kobs, const void* V,
+                           const void* Q, hipStream_t st) {
+  int nblk = 0;
+  for (int b = 0; b < g.B; ++b) nblk += g.H * ((g.S[b] + EPI_TOK - 1) / EPI_TOK);
+  const bool r2 = g.m > 128;  // 4 waves x 2 row blocks of 32 for up to 256 rows
+  const uint32_t qlds = (uint32_t)g.m * (AKV_D + (g.dtype == 1 ? 8 : 4)) * (g.dtype == 1 ? 2 : 4);
+  const bool rp = g.rope != 0;
+  if (g.dtype == 1) {
+    if (rp) return r2 ? launch_epi_t<1, 2, true>(g, w, c, K, Kobs, V, Q, nblk, qlds, st)
+                      : launch_epi_t<1, 1, true>(g, w, c, K, Kobs, V, Q, nblk, qlds, st);
+    return r2 ? launch_epi_t<1, 2, false>(g, w, c, K, Kobs, V, Q, nblk, qlds, st)
+              : launch_epi_t<1, 1, false>(g, w, c, K, Kobs, V, Q, nblk, qlds, st);
+  }
+  if (rp) return r2 ? launch_epi_t<0, 2, true>(g, w, c, K, Kobs, V, Q, nblk, qlds, st)
+                    : launch_epi_t<0, 1, true>(g, w, c, K, Kobs, V, Q, nblk, qlds, st);
+  return r2 ? launch_epi_t<0, 2, false>(g, w, c, K, Kobs, V, Q, nblk, qlds, st)
+            : launch_epi_t<0, 1, false>(g, w, c, K, Kobs, V, Q, nblk, qlds, st);
 }
 
 }  // namespace akv

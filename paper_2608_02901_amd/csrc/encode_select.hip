@@ -643,8 +643,8 @@ __global__ __launch_bounds__(256) void k_anchor_prep(Geo g, Ws w, Cache c, const
   }
 }
 
-hipError_t launch_select(const Geo& g, const Ws& w, const Cache& c, const void* K, const void* V, const void* Q,
-                         const int32_t* ovr, hipStream_t st) {
+hipError_t launch_select(const Geo& g, const Ws& w, const Cache& c, const void* K, const void* Kobs, const void* V,
+                         const void* Q, const int32_t* ovr, hipStream_t st) {
   int nblk = 0, nsel = 0;
   for (int b = 0; b < g.B; ++b) {
     nblk += g.H * ((g.k[b] + 63) / 64);
@@ -657,8 +657,8 @@ hipError_t launch_select(const Geo& g, const Ws& w, const Cache& c, const void* 
   } else {
     launch("k_sel_cand", k_sel_cand, dim3(nsel), dim3(256), 0, st, g, w);
     launch("k_sel_class", k_sel_class, dim3(nsel), dim3(256), 0, st, g, w);
-    if (g.dtype == 1) launch("k_sel_band", k_sel_band<1>, dim3(nbh * SEL_BAND_MAX), dim3(256), 0, st, g, w, K, Q);
-    else launch("k_sel_band", k_sel_band<0>, dim3(nbh * SEL_BAND_MAX), dim3(256), 0, st, g, w, K, Q);
+    if (g.dtype == 1) launch("k_sel_band", k_sel_band<1>, dim3(nbh * SEL_BAND_MAX), dim3(256), 0, st, g, w, Kobs, Q);
+    else launch("k_sel_band", k_sel_band<0>, dim3(nbh * SEL_BAND_MAX), dim3(256), 0, st, g, w, Kobs, Q);
     launch("k_sel_rhist", k_sel_rhist, dim3(nsel), dim3(256), 0, st, g, w, c);
     launch("k_sel_rcand", k_sel_rcand, dim3(nsel), dim3(256), 0, st, g, w);
     launch("k_sel_list", k_sel_list, dim3(nsel), dim3(256), 0, st, g, w, c);

@@ -36,6 +36,13 @@ def gpu_encode(plan, layer, override=None):
     return cache, ws, dws
 
 
+def rope_freqs(cfg):
+    """The rotary frequencies of a config, or None without positions."""
+    if not cfg.rope:
+        return None
+    return np.array(cfg.rope_inv_freq[: cfg.head_dim // 2], np.float32)
+
+
 def oracle_encode(cfg, layer, b, anchor_override=None):
     K = layer.K[b].float().numpy()
     V = layer.V[b].float().numpy()
@@ -47,7 +54,7 @@ def oracle_encode(cfg, layer, b, anchor_override=None):
                     bf16=cfg.dtype == N.BF16, seed=cfg.seed, budget_mode=cfg.budget_mode,
                     budget=float(np.float32(cfg.budget)), budget_count=cfg.budget_count, G=G,
                     scale_mode=cfg.scale_mode, anchor_override=anchor_override, rank_mode=cfg.rank_mode,
-                    head_budget=cfg.head_budget)
+                    head_budget=cfg.head_budget, inv_freq=rope_freqs(cfg))
 
 
 def plan_k(cfg, S):

@@ -157,7 +157,7 @@ def _cpu_layer(lay):
     return _cpu_cache[key]
 
 
-def _oracle_decode_check(cfg, lay, b, enc, q, got, tails=None, tag=""):
+def _oracle_decode_check(cfg, lay, b, enc, q, got, tails=None, tag="", cs=None):
     """Decode output of request b against the oracle's fp64 attention over its
     own dense reconstruction (and the appended tokens, encoded by the oracle
     against its anchors: fp32(gamma) * anchor, no residual)."""
@@ -183,7 +183,7 @@ def _oracle_decode_check(cfg, lay, b, enc, q, got, tails=None, tag=""):
             addV.append(rows[1])
         Kh = np.concatenate([Kh, np.stack(addK)], axis=1)
         Vh = np.concatenate([Vh, np.stack(addV)], axis=1)
-    ref = R.attention(Kh, Vh, q)
+    ref = R.attention(Kh, Vh, q, cs=None if cs is None else cs[: Kh.shape[1]])
     err = float(np.abs(got - ref).max())
     print(f"[full] {tag}: decode vs oracle attention max|err| {err:.3g}", flush=True)
     assert err <= 2e-3, err
@@ -263,6 +263,42 @@ def test_workload3_128k_whole_with_64_appends():
     for s, got in outs.items():
         _oracle_decode_check(cfg, lay, 0, enc, lay.q[s, 0].float().cpu().numpy(), got,
                              tails=(kt[:s + 1], vt[:s + 1]), tag=f"workload 3 step {s + 1}")
+
+
+def test_workload3_128k_rope_whole_with_appends():
+    """The 128K layer with keys given before RoPE and Llama-3.1's rotary
+    frequencies (Sec. 3.2): the whole compression pass against the oracle's
+    (anchors scored with the rotated keys, residuals ranked with R_t r), then
+    8 generated tokens through decode_step, whose outputs at steps 1 and 8
+    match the oracle's attention with every key rotated at its position."""
+    wl = synth.workload(3)
+    NS = 8
+    freq = synth.llama31_inv_freq(wl.D)
+    print(f"[full] workload 3 with RoPE {wl.name}", flush=True)
+    lay = _layer_on_gpu(wl, steps=NS)
+    cfg = make_cfg(wl, max_append=NS, rope_inv_freq=freq)
+    plan = N.Plan(cfg, wl.seq_lens)
+    cache, ws, dws = plan.alloc("cuda")
+    keep = akv.encode(plan, lay.K[0], lay.V[0], lay.Qobs[0], cache, ws)
+    torch.cuda.synchronize()
+    del keep
+    assert _header_flags(cache) == 0
+    exp = _export(plan, cache, 0)
+    enc = _oracle_whole_request(cfg, lay, 0, exp, "workload 3 RoPE")
+    out = torch.empty(1, wl.Hq, wl.D, dtype=torch.float32, device="cuda")
+    outs = {}
+    for s in range(NS):
+        akv.decode_step(plan, cache, s, lay.k_new[s], lay.v_new[s], lay.q[s], out, dws)
+        if s in (0, NS - 1):
+            torch.cuda.synchronize()
+            outs[s] = out[0].cpu().numpy().copy()
+    torch.cuda.synchronize()
+    kt = lay.k_new[:, 0].float().cpu().numpy()
+    vt = lay.v_new[:, 0].float().cpu().numpy()
+    cs = R.rope_table(freq, wl.D, wl.seq_lens[0] + NS)
+    for s, got in outs.items():
+        _oracle_decode_check(cfg, lay, 0, enc, lay.q[s, 0].float().cpu().numpy(), got,
+                             tails=(kt[:s + 1], vt[:s + 1]), tag=f"workload 3 RoPE step {s + 1}", cs=cs)
 
 
 def test_workload4_70b_batch8_whole():
