@@ -70,7 +70,14 @@ __global__ __launch_bounds__(256, R == 1 ? 2 : 1) void k_epilogue(Geo g, Ws w, C
   extern __shared__ __align__(16) char qlds_raw[];  // the m observation rows, row stride LD
   E* QS = (E*)qlds_raw;
 
+  // Consecutive logical blocks (the chunks of one head) share an XCD, so the
+  // head's anchor rows, gathered by every token's coefficient chain, stay in
+  // that XCD's L2.
   int idx = blockIdx.x;
+  {
+    const int n8 = gridDim.x & ~7;
+    if (idx < n8) idx = (idx & 7) * (n8 >> 3) + (idx >> 3);
+  }
   const int b = locate(g, EPI_TOK, 1, idx);
   const int S = g.S[b], k = g.k[b], D = AKV_D, m = g.m;
   const int nchunk = (S + EPI_TOK - 1) / EPI_TOK;

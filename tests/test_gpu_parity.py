@@ -215,3 +215,43 @@ def test_encode_is_deterministic():
     c1, _, _ = gpu_encode(plan, layer)
     c2, _, _ = gpu_encode(plan, layer)
     assert torch.equal(c1, c2)
+
+
+def test_repeated_steps_share_one_workspace():
+    """Twenty decode calls in a row on one decode workspace, each with its own
+    queries and every other one appending: nothing one call leaves in the
+    workspace leaks into the next, so every output matches the oracle's
+    attention over the tokens appended so far."""
+    wl = _small("repeat", seq_lens=[1600], steps=20, append=True, seed=51)
+    layer = synth.make_layer(wl)
+    cfg = make_cfg(wl)
+    plan = N.Plan(cfg, wl.seq_lens)
+    cache, ws, dws = gpu_encode(plan, layer)
+    enc = oracle_encode(cfg, layer, 0)
+    Kh = _oracle_dense(cfg, layer, 0, enc, "K")
+    Vh = _oracle_dense(cfg, layer, 0, enc, "V")
+    Kx, Vx = layer.K[0].float().numpy(), layer.V[0].float().numpy()
+    tk, tv = [], []
+    n_app = 0
+    for s in range(wl.steps):
+        out = torch.empty(1, wl.Hq, wl.D, dtype=torch.float32, device="cuda")
+        if s % 2:
+            akv.decode_step(plan, cache, n_app, layer.k_new[s].cuda(), layer.v_new[s].cuda(), layer.q[s].cuda(), out,
+                            dws)
+            rows_k, rows_v = [], []
+            for h in range(wl.H):
+                anc = enc["anchors"][h]
+                for X, new, rows in ((Kx, layer.k_new, rows_k), (Vx, layer.v_new, rows_v)):
+                    a, g = R.assign_vectors(new[s, 0, h:h + 1].float().numpy(), X[h][anc], bf16=True)
+                    rows.append((X[h][anc[a[0]]].astype(np.float32) * np.float32(g[0])).astype(np.float32))
+            tk.append(np.stack(rows_k))
+            tv.append(np.stack(rows_v))
+            n_app += 1
+        else:
+            akv.decode_attn(plan, cache, layer.q[s].cuda(), out, dws, n_appended=n_app)
+        torch.cuda.synchronize()
+        Kt = np.concatenate([Kh] + ([np.stack(tk, 1)] if tk else []), 1)
+        Vt = np.concatenate([Vh] + ([np.stack(tv, 1)] if tv else []), 1)
+        ref = R.attention(Kt, Vt, layer.q[s, 0].float().numpy())
+        err = np.abs(out[0].cpu().numpy() - ref).max()
+        assert np.isfinite(out.cpu().numpy()).all() and err <= 2e-3, (s, err)
