@@ -294,6 +294,7 @@ def rope_leg(args, akv, N, torch, synth, wl, layers, packed, caches, ws, out, st
     compression pass, then `steps` decode steps (append + attention) over all
     layers, timed apart from the main workload.  The caches of the main leg
     are reused as storage."""
+    steps = min(steps, layers[0].k_new.shape[0])
     freq = synth.llama31_inv_freq(wl.D)
     cfg = N.Config.make(num_kv_heads=wl.H, num_q_heads=wl.Hq, head_dim=wl.D, window=wl.window,
                         anchor_frac=wl.anchor_frac, rho=0.7, kappa=7, budget=wl.budget, dtype=N.BF16,
