@@ -6,9 +6,11 @@
 // Coefficient (bit-exact with the CPU oracle): d = sequential fp64 dot of the
 // token and its anchor, gamma = d / ||a||^2 in fp64, rounded to fp32 and, for
 // a bf16 cache, to bf16 (round to nearest even).  Anchor positions keep
-// gamma = 1.  For a bf16 cache an fp32 estimate of d with a proven error
-// bound decides the rounded value when its whole error interval rounds alike
-// (nearly always); otherwise the sequential fp64 sum is formed.
+// gamma = 1.  An estimate of d with a proven error bound (an fp32 sum of the
+// exact bf16 products for a bf16 cache, an fp64 sum of the exact fp32
+// products for an fp32 cache, in a lane tree) decides the rounded value when
+// its whole error interval rounds alike (nearly always); otherwise the
+// sequential fp64 sum is formed.
 //
 // Utilities (fp32):
 //   uK_t = (1/m) sum_w alpha_wt^2 (q_w . R_t rK_t)^2 / D * ||v_t - y_w||^2
@@ -22,11 +24,14 @@
 // for a bf16 cache.
 //
 // Schedule: first the 2 x EPI_TOK coefficient chains of the workgroup's
-// tokens (four per thread, spread over all waves), then the utilities tile by
-// tile (32 tokens), with the observation rows staged in LDS once, each wave's
-// y fragments in registers and its rows' softmax constants in LDS for all
-// tiles, and the next tile's keys and values loaded while the current tile is
-// processed.
+// tokens, 32 tokens per step, each chain's row split over a group of lanes
+// (16-byte chunks, so that a wave's loads cover whole rows), then the
+// utilities tile by tile (32 tokens), with the observation rows staged in LDS
+// once, each wave's y fragments in registers and its rows' softmax constants
+// in LDS for all tiles.  In both phases the next step's rows are loaded while
+// the current one is processed; the loads are issued by every lane alike
+// (rows past the workgroup's last token repeat that token's row), so that the
+// waits for the current rows leave them in flight.
 #include "akv_common.h"
 
 namespace akv {
@@ -34,11 +39,94 @@ namespace akv {
 constexpr int EPI_TOK = 512;  // tokens per workgroup: 16 tiles of 32
 
 // The canonical sequential fp64 dot of a token row and an anchor row, read
-// from memory: the rare fallback of the certified coefficient, kept out of
-// line so that it holds no registers in the caller.
+// from memory (fp64 fused multiply-add on the exact products, j = 0..D-1): the
+// rare fallback of the certified coefficient, one 16-byte chunk per step so
+// that it holds few registers in the caller.
+// 16 bytes of row data as a native vector: copies of it stay in registers
+// (the struct form of uint4 is copied through memory when a copy is not
+// guarded by a branch).
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+
+// Element e of a 16-byte chunk of cache-dtype values, as fp32.
 template <int DT>
-__device__ __attribute__((noinline)) double dot64_rows(const typename Elem<DT>::T* x, const typename Elem<DT>::T* a) {
-  return dot64_seq<DT, true>(x, a, AKV_D);
+__device__ inline float chunk_elem(const u32x4& v, int e) {
+  if constexpr (DT == 1) return __uint_as_float((e & 1) ? (v[e >> 1] & 0xFFFF0000u) : (v[e >> 1] << 16));
+  else return __uint_as_float(v[e]);
+}
+
+template <int DT>
+__device__ inline double dot64_rows(const typename Elem<DT>::T* x, const typename Elem<DT>::T* a) {
+  constexpr int PER = 16 / sizeof(typename Elem<DT>::T);
+  double s = 0.0;
+#pragma unroll 1
+  for (int j = 0; j < AKV_D; j += PER) {
+    const uint4 xv = *(const uint4*)(x + j), av = *(const uint4*)(a + j);
+#pragma unroll
+    for (int e = 0; e < PER; ++e) s = fma((double)Elem<DT>::get(&xv, e), (double)Elem<DT>::get(&av, e), s);
+  }
+  return s;
+}
+
+// Lane exchange of a 64-bit value (two 32-bit moves).
+template <int M>
+__device__ inline double lane_xor_d(double v) {
+  const unsigned long long u = __builtin_bit_cast(unsigned long long, v);
+  const int lo = __builtin_bit_cast(int, lane_xor<M>(__builtin_bit_cast(float, (int)(unsigned)u)));
+  const int hi = __builtin_bit_cast(int, lane_xor<M>(__builtin_bit_cast(float, (int)(unsigned)(u >> 32))));
+  return __builtin_bit_cast(double, (unsigned long long)(unsigned)lo | ((unsigned long long)(unsigned)hi << 32));
+}
+template <int M>
+__device__ inline float lane_xor_v(float v) { return lane_xor<M>(v); }
+template <int M>
+__device__ inline double lane_xor_v(double v) { return lane_xor_d<M>(v); }
+
+// Reduce-scatter of NC chains over a group of G lanes (G a power of two,
+// NC <= G): on entry v[c] is this lane's partial of chain c; on exit v[0]
+// holds, in lane j of the group, the whole sum of chain rev(j mod NC) (the
+// bit-reversed index).  At each level a lane keeps half of its chains and adds
+// its partner's half; the remaining levels add whole sums.  Every addition
+// pairs a lane's value with its partner's, and fp addition commutes, so all
+// lanes that hold a chain hold the same bits; the summation tree has depth
+// log2(G) above the lanes' own partial sums.
+template <int M, int CNT, int NC, typename T>
+__device__ inline void rs_level(T (&v)[NC], int lane) {
+  const bool hi = lane & M;
+#pragma unroll
+  for (int q = 0; q < CNT / 2; ++q) {
+    const T keep = hi ? v[q + CNT / 2] : v[q];
+    const T send = hi ? v[q] : v[q + CNT / 2];
+    v[q] = keep + lane_xor_v<M>(send);
+  }
+}
+template <int G, int NC, typename T>
+__device__ inline void group_reduce_scatter(T (&v)[NC], int lane) {
+  static_assert(NC == 4 || NC == 8, "two or four rows per lane, two sides each");
+  rs_level<1, NC>(v, lane);
+  rs_level<2, NC / 2>(v, lane);
+  if constexpr (NC == 8) rs_level<4, 2>(v, lane);
+  if constexpr (NC < 8 && G > 4) v[0] += lane_xor_v<4>(v[0]);
+  if constexpr (G > 8) v[0] += lane_xor_v<8>(v[0]);
+  if constexpr (G > 16) v[0] += lane_xor_v<16>(v[0]);
+}
+template <int NC>
+__device__ constexpr int chain_of(int j) {  // chain held by lane j after the reduce-scatter
+  return NC == 4 ? (((j & 1) << 1) | ((j >> 1) & 1)) : (((j & 1) << 2) | (j & 2) | ((j >> 2) & 1));
+}
+// Chain C's value from the lane of this lane's NC-block that holds it.
+template <int NC, int C>
+__device__ inline float chain_bcast(float v, int lane) {
+  constexpr int src = chain_of<NC>(C);  // the bit reversal is its own inverse
+  if constexpr (NC == 4) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), src * 0x55, 0xF, 0xF, false));
+  } else {
+    return __shfl(v, (lane & ~(NC - 1)) | src, 64);
+  }
+}
+
+template <int NC, int C = 0>
+__device__ inline void chain_bcast_all(float (&gc)[NC], float v, int lane) {
+  gc[C] = chain_bcast<NC, C>(v, lane);
+  if constexpr (C + 1 < NC) chain_bcast_all<NC, C + 1>(gc, v, lane);
 }
 
 template <int DT, int R, bool RP>
@@ -57,8 +145,12 @@ __global__ __launch_bounds__(256, R == 1 ? 2 : 1) void k_epilogue(Geo g, Ws w, C
   // rotated key residuals of the tile (RP): fp32, or bf16 hi and lo parts
   __shared__ __align__(16) E RTh[RP ? 32 * LD : 1];
   __shared__ __align__(16) E RTl[RP && DT == 1 ? 32 * LD : 1];
-  __shared__ float gK_s[EPI_TOK], rv2_s[EPI_TOK], vn_s[EPI_TOK], rk2_s[EPI_TOK];
-  __shared__ int aK_s[EPI_TOK];
+  constexpr int NC = 2 * RPT;  // coefficient chains per lane group: RPT rows x (K, V)
+  // Per token and side: the anchor row to gather (0 for an invalid
+  // assignment) and flags.
+  constexpr int F_IDX = 0x0FFFFFFF, F_BAD = 1 << 28, F_PAST = 1 << 29, F_ANC = 1 << 30;
+  __shared__ int fa_s[2][EPI_TOK];
+  __shared__ float gK_s[EPI_TOK], gV_s[EPI_TOK], rv2_s[EPI_TOK], vn_s[EPI_TOK], rk2_s[EPI_TOK];
   // Row sums per token: each wave leaves its partials of a tile in tpart
   // (double-buffered by tile parity); 32 threads add the four waves' partials
   // in a fixed order into sumK (sum a2 vv qr^2), sumV (sum a2) and sumQ
@@ -97,101 +189,157 @@ __global__ __launch_bounds__(256, R == 1 ? 2 : 1) void k_epilogue(Geo g, Ws w, C
     *(uint4*)(&QS[r * LD + col]) = *(const uint4*)(Q + (size_t)r * D + col);
   }
 
-  // ---- coefficients: thread = token tb + tid + 256 p (p < EPI_TOK / 256),
-  // both sides.  A token with
-  // an invalid assignment raises the error bit and uses anchor 0; the
-  // K side marks utility candidates (non-anchors), the V side also leaves
-  // ||rV||^2 and ||v||^2 (the latter from the assignment pass).
+  for (int tl = threadIdx.x; tl < EPI_TOK; tl += 256) {
+    const int t = tb + tl;
+    int fk = F_PAST, fv = F_PAST;
+    if (t < S) {
+      const int anc = w.rank[po + t] >= 0 ? F_ANC : 0;
+      const int apk = w.apos[po + t], apv = w.apos[TS + po + t];
+      fk = anc | ((apk < 0 || apk >= k) ? F_BAD : apk);
+      fv = anc | ((apv < 0 || apv >= k) ? F_BAD : apv);
+    }
+    fa_s[0][tl] = fk;
+    fa_s[1][tl] = fv;
+  }
+  __syncthreads();
+  const int ntl = min(NT, (S - tb + 31) / 32);
+  const int tlast = min(tb + EPI_TOK, S) - 1;  // the workgroup's last token
+
+  // ---- coefficients, 32 tokens per step.  Lane gj of a CPR-lane group holds
+  // elements PER gj .. PER gj + PER - 1 of rows tid / CPR + (256 / CPR) i of
+  // the step (i < RPT) and of their anchors; chain c = 2 i + side is the dot
+  // of row i's token and its anchor on that side, summed over the group by
+  // the reduce-scatter.  Each lane certifies chain cc and the group shares
+  // the coefficients.  The next step's rows are loaded while the current one
+  // is processed.
   {
-#pragma unroll 1
-  for (int pp = 0; pp < EPI_TOK / 256; ++pp) {
-    const int tl = threadIdx.x + 256 * pp, t = tb + tl;
-    const bool in = t < S;
-    const int tc = in ? t : S - 1;
-    const int rk = w.rank[po + tc];
-#pragma unroll 1
-    for (int side = 0; side < 2; ++side) {
-      const int ap = w.apos[side * TS + po + tc];
-      const bool bad = ap < 0 || ap >= k;
-      const int a = bad ? 0 : ap;
-      const E* xrow = (side ? Vx : Kx) + (size_t)tc * D;
-      const E* arow = (const E*)(side ? c.ancV : c.ancK) + (ko + a) * D;
-      const double n = (side ? c.nrmV : c.nrmK)[ko + a];
-      uint4 xv[CPR], av[CPR];
+    const int gj = threadIdx.x % CPR;
+    const int cc = chain_of<NC>(gj % NC);  // certified chain: row cc >> 1, side cc & 1
+    struct Rows {
+      u32x4 x[2][RPT], a[2][RPT];
+      float x2;
+      double n;
+    };
+    // Every lane issues the same loads (rows past the workgroup's last token
+    // read that token's row; chains of tokens past S or of anchors are
+    // discarded), so that the wait for one step's rows leaves the next step's
+    // loads in flight.
+    auto load = [&](Rows& q, int t0) {
 #pragma unroll
-      for (int i = 0; i < CPR; ++i) {
-        const uint4 x4 = *(const uint4*)(xrow + i * PER);
-        const uint4 a4 = *(const uint4*)(arow + i * PER);
-        xv[i] = make_uint4(x4.x, x4.y, x4.z, x4.w);
-        av[i] = make_uint4(a4.x, a4.y, a4.z, a4.w);
+      for (int i = 0; i < RPT; ++i) {
+        const int t = min(t0 + threadIdx.x / CPR + (256 / CPR) * i, tlast), col = gj * PER;
+        const int fk = fa_s[0][t - tb], fv = fa_s[1][t - tb];
+        q.x[0][i] = *(const u32x4*)(Kx + (size_t)t * D + col);
+        q.x[1][i] = *(const u32x4*)(Vx + (size_t)t * D + col);
+        q.a[0][i] = *(const u32x4*)((const E*)c.ancK + (ko + (fk & F_IDX)) * D + col);
+        q.a[1][i] = *(const u32x4*)((const E*)c.ancV + (ko + (fv & F_IDX)) * D + col);
       }
-      const E* xe = (const E*)xv;
-      const E* ae = (const E*)av;
-      float gb = 1.0f;
-      if (in && rk < 0) {
-        if (bad) atomicOr(&c.header[2], 4u);
-        bool done = false;
-        if constexpr (DT == 1) {
-          // Certified shortcut for a bf16 cache.  Four interleaved fp32 FMA
-          // chains over the exact bf16 products give d32 with |d32 - d| <=
-          // 35 u (1 + 35 u) sum|x_j a_j| <= 36 u sqrt(xx n) (u = 2^-24; 32
-          // steps per chain and three combining adds; xx is the token's fp32
-          // sum of squares, within 130 u of the exact one), and the
-          // sequential fp64 sum lies within 2^-44 sqrt(xx n) of d.  The
-          // stored value bf16(fp32(fl64(d / n))) is monotone in d, so when
-          // both ends of the interval round to the same bits, those are the
-          // canonical bits; otherwise the sequential fp64 chain decides.
-          float e0 = 0.0f, e1 = 0.0f, e2 = 0.0f, e3 = 0.0f;
+      const int side = cc & 1, t = min(t0 + threadIdx.x / CPR + (256 / CPR) * (cc >> 1), tlast);
+      q.x2 = w.xn2[side * TS + po + t];
+      q.n = (side ? c.nrmV : c.nrmK)[ko + (fa_s[side][t - tb] & F_IDX)];
+    };
+    auto chains = [&](const Rows& q, int it) {
+      using P = typename std::conditional<DT == 1, float, double>::type;
+      float xs[NC][PER], as[NC][PER];
 #pragma unroll
-          for (int j = 0; j < AKV_D; j += 4) {
-            e0 = fmaf(Elem<DT>::get(xe, j), Elem<DT>::get(ae, j), e0);
-            e1 = fmaf(Elem<DT>::get(xe, j + 1), Elem<DT>::get(ae, j + 1), e1);
-            e2 = fmaf(Elem<DT>::get(xe, j + 2), Elem<DT>::get(ae, j + 2), e2);
-            e3 = fmaf(Elem<DT>::get(xe, j + 3), Elem<DT>::get(ae, j + 3), e3);
-          }
-          const float f32 = (e0 + e1) + (e2 + e3);
-          const double d32 = (double)f32;
-          if (n > 0.0 && __builtin_isfinite(f32)) {
-            // + 128 * 2^-126 for products flushed to zero below the fp32
-            // normal range
-            const double E = 2.1482e-6 * sqrt((double)w.xn2[side * TS + po + tc] * n) + 3e-36;
-            const float lo = Elem<DT>::round_coef((float)((d32 - E) / n));
-            const float hi = Elem<DT>::round_coef((float)((d32 + E) / n));
-            if (__float_as_uint(lo) == __float_as_uint(hi)) {
-              gb = lo;
-              done = true;
-            }
-          } else if (!(n > 0.0)) {
-            gb = 0.0f;  // canonical gamma of a zero anchor
+      for (int i = 0; i < RPT; ++i)
+#pragma unroll
+        for (int e = 0; e < PER; ++e) {
+          xs[2 * i][e] = chunk_elem<DT>(q.x[0][i], e);
+          xs[2 * i + 1][e] = chunk_elem<DT>(q.x[1][i], e);
+          as[2 * i][e] = chunk_elem<DT>(q.a[0][i], e);
+          as[2 * i + 1][e] = chunk_elem<DT>(q.a[1][i], e);
+        }
+      P dp[NC];
+#pragma unroll
+      for (int j = 0; j < NC; ++j) {
+        dp[j] = (P)0;
+#pragma unroll
+        for (int e = 0; e < PER; ++e) {
+          if constexpr (DT == 1) dp[j] = fmaf(xs[j][e], as[j][e], dp[j]);
+          else dp[j] = fma((double)xs[j][e], (double)as[j][e], dp[j]);
+        }
+      }
+      group_reduce_scatter<CPR>(dp, lane);
+      const int side = cc & 1, tl = 32 * it + threadIdx.x / CPR + (256 / CPR) * (cc >> 1), t = tb + tl;
+      const int fa = fa_s[side][tl];
+      const bool cand = !(fa & (F_PAST | F_ANC));
+      float gb = 1.0f;
+      if (cand) {
+        // Certified coefficient.  The lanes' products are exact (bf16 in
+        // fp32, fp32 in fp64) up to fp32 underflow (at most D 2^-126 in all);
+        // the group sum has a summation tree of depth PER + log2(CPR) <= 12,
+        // so its error is at most 12 u (1 + 12 u) sum|x_j a_j| (u = 2^-24 for
+        // fp32, 2^-53 for fp64), and the canonical sequential fp64 sum lies
+        // within 128 * 2^-53 (1 + 2^-46) sum|x_j a_j| of the exact dot.
+        // sum|x_j a_j| <= sqrt(xx n), with xx the token's fp32 squared norm
+        // (within 130 u of the exact one above fp32 underflow, which leaves at
+        // most D 2^-126 < 2e-36) and n the anchor's fp64 one.  Eb below bounds
+        // the distance of the canonical dot from the estimate; the stored
+        // value round(fp32(fl64(d / n))) is monotone in d, so when both ends
+        // of [est - Eb, est + Eb] give the same bits those are the canonical
+        // bits; otherwise the sequential fp64 chain decides.
+        const double n = q.n, est = (double)dp[0];
+        bool done = false;
+        if (n > 0.0 && __builtin_isfinite(est)) {
+          const double rxn = sqrt(((double)q.x2 + 2e-36) * n);
+          const double Eb = DT == 1 ? 2.1482e-6 * rxn + 3e-36 : 1.6e-14 * rxn;
+          const float lo = Elem<DT>::round_coef((float)((est - Eb) / n));
+          const float hi = Elem<DT>::round_coef((float)((est + Eb) / n));
+          if (__float_as_uint(lo) == __float_as_uint(hi)) {
+            gb = lo;
             done = true;
           }
+        } else if (!(n > 0.0)) {
+          gb = 0.0f;  // canonical gamma of a zero anchor
+          done = true;
         }
         if (!done) {
-          const double d = DT == 1 ? dot64_rows<DT>(xrow, arow) : dot64_seq<DT, true>(xe, ae, D);
-          const double g64 = n > 0.0 ? d / n : 0.0;
-          gb = Elem<DT>::round_coef((float)g64);
+          const E* xrow = (side ? Vx : Kx) + (size_t)t * D;
+          const E* arow = (const E*)(side ? c.ancV : c.ancK) + (ko + (fa & F_IDX)) * D;
+          const double d = dot64_rows<DT>(xrow, arow);
+          gb = Elem<DT>::round_coef((float)(n > 0.0 ? d / n : 0.0));
         }
       }
-      if (in) w.gpos[side * TS + po + t] = gb;
-      // ||r||^2 of the side's fp32 residual (the key side bounds q.r_K, the
-      // value side is the value utility's factor)
-      float rs = 0.0f;
+      float gc[NC];
+      chain_bcast_all(gc, gb, lane);
+      // ||r||^2 of each chain's fp32 residual (the key side bounds q.r_K,
+      // the value side is the value utility's factor)
+      float rs[NC];
 #pragma unroll
-      for (int j = 0; j < AKV_D; ++j) {
-        const float r = fmaf(-gb, Elem<DT>::get(ae, j), Elem<DT>::get(xe, j));
-        rs = fmaf(r, r, rs);
+      for (int j = 0; j < NC; ++j) {
+        rs[j] = 0.0f;
+#pragma unroll
+        for (int e = 0; e < PER; ++e) {
+          const float r = fmaf(-gc[j], as[j][e], xs[j][e]);
+          rs[j] = fmaf(r, r, rs[j]);
+        }
       }
-      rs = (in && rk < 0) ? rs : 0.0f;
-      if (side == 0) {
-        gK_s[tl] = in ? gb : 0.0f;
-        aK_s[tl] = (in && rk < 0) ? a : -1;  // -1: no utility (anchor or past S)
-        rk2_s[tl] = rs;
-      } else {
-        vn_s[tl] = w.xn2[TS + po + tc];
-        rv2_s[tl] = rs;
+      group_reduce_scatter<CPR>(rs, lane);
+      if (gj < NC) {  // one lane per chain
+        const bool in = t < S;
+        if (in) w.gpos[side * TS + po + t] = gb;
+        if (cand && (fa & F_BAD)) atomicOr(&c.header[2], 4u);
+        const float rsv = cand ? rs[0] : 0.0f;
+        if (side == 0) {
+          gK_s[tl] = in ? gb : 0.0f;
+          rk2_s[tl] = rsv;
+        } else {
+          gV_s[tl] = in ? gb : 0.0f;
+          rv2_s[tl] = rsv;
+          vn_s[tl] = in ? q.x2 : 0.0f;
+        }
       }
+    };
+    Rows q0, q1;
+    load(q0, tb);
+#pragma unroll 1
+    for (int it = 0; it < ntl; it += 2) {
+      load(q1, tb + 32 * (it + 1));
+      chains(q0, it);
+      load(q0, tb + 32 * (it + 2));
+      if (it + 1 < ntl) chains(q1, it + 1);
     }
-  }
   }
 
   // ---- utilities.  Wave rows: row block rb = wave + 4 r; lane l supplies
@@ -237,21 +385,19 @@ __global__ __launch_bounds__(256, R == 1 ? 2 : 1) void k_epilogue(Geo g, Ws w, C
       }
     }
   }
-  // Next tile's keys and values, 16-byte chunks (rows past S are zero).
-  uint4 kpre[RPT], vpre[RPT];
+  // Next tile's keys and values, 16-byte chunks.  Every lane issues the same
+  // loads (rows past the workgroup's last token read that token's row; their
+  // columns are never used), so the waits of the current tile leave them in
+  // flight.
+  u32x4 kpre[RPT], vpre[RPT];
   auto fetch = [&](int t0) {
 #pragma unroll
     for (int i = 0; i < RPT; ++i) {
-      const int ch = threadIdx.x + 256 * i, r = ch / CPR, col = (ch % CPR) * PER;
-      kpre[i] = make_uint4(0, 0, 0, 0);
-      vpre[i] = make_uint4(0, 0, 0, 0);
-      if (t0 + r < S) {
-        kpre[i] = *(const uint4*)(Ko + (size_t)(t0 + r) * D + col);
-        vpre[i] = *(const uint4*)(Vx + (size_t)(t0 + r) * D + col);
-      }
+      const int ch = threadIdx.x + 256 * i, r = min(t0 + ch / CPR, tlast), col = (ch % CPR) * PER;
+      kpre[i] = *(const u32x4*)(Ko + (size_t)r * D + col);
+      vpre[i] = *(const u32x4*)(Vx + (size_t)r * D + col);
     }
   };
-  const int ntl = min(NT, (S - tb + 31) / 32);
   fetch(tb);
   auto fold = [&](int tt) {  // tile tt's partials into the per-token sums
     const int tl = 32 * tt + threadIdx.x;
@@ -267,8 +413,8 @@ __global__ __launch_bounds__(256, R == 1 ? 2 : 1) void k_epilogue(Geo g, Ws w, C
 #pragma unroll
     for (int i = 0; i < RPT; ++i) {
       const int ch = threadIdx.x + 256 * i, r = ch / CPR, col = (ch % CPR) * PER;
-      *(uint4*)(&KT[r * LD + col]) = kpre[i];
-      *(uint4*)(&VT[r * LD + col]) = vpre[i];
+      *(u32x4*)(&KT[r * LD + col]) = kpre[i];
+      *(u32x4*)(&VT[r * LD + col]) = vpre[i];
     }
     if constexpr (RP) {
       // Rotated key residuals: thread = (token tid / 8, pairs 8 (tid % 8) ..
@@ -277,7 +423,8 @@ __global__ __launch_bounds__(256, R == 1 ? 2 : 1) void k_epilogue(Geo g, Ws w, C
       // rows past S.
       const int rr = threadIdx.x >> 3, f0 = 8 * (threadIdx.x & 7);
       const int tl = 32 * it + rr, t = t0 + rr;
-      const int ak = aK_s[tl];
+      const int fk0 = fa_s[0][tl];
+      const int ak = (fk0 & (F_PAST | F_ANC)) ? -1 : (fk0 & F_IDX);
       float xr[16], ar[16];
 #pragma unroll
       for (int i = 0; i < 16; ++i) xr[i] = ar[i] = 0.0f;
@@ -326,33 +473,40 @@ __global__ __launch_bounds__(256, R == 1 ? 2 : 1) void k_epilogue(Geo g, Ws w, C
       }
     }
     __syncthreads();
-    if (it + 1 < ntl) fetch(t0 + 32);
     const int tl = 32 * it + (lane & 31);
-    const int ak = aK_s[tl];
+    const int fk0 = fa_s[0][tl];
+    const int ak = (fk0 & (F_PAST | F_ANC)) ? -1 : (fk0 & F_IDX);  // -1: no utility
     const float gk = gK_s[tl], vn = vn_s[tl];
     // The token's QA row (rows of accumulator entries 4j .. 4j+3 are
-    // consecutive) is read before the contraction, for every token (anchor 0
-    // stands in for an anchor position), so its latency overlaps the MFMAs.
+    // consecutive) is read before the next tile's rows are requested, for
+    // every token (anchor 0 stands in for an anchor position), so that its
+    // wait leaves those in flight and its latency overlaps the MFMAs.
     const float* qa = QA + (size_t)max(ak, 0) * m;
-    float tk = 0.0f, tv = 0.0f, tq = 0.0f;
+    float qv[R][RP ? 1 : 16];
+    if constexpr (!RP) {
 #pragma unroll
-    for (int r = 0; r < R; ++r) {
-      const int rb = wave + 4 * r;
-      if (rb >= nrb) break;
-      float qv[RP ? 1 : 16];
-      if constexpr (!RP) {
+      for (int r = 0; r < R; ++r) {
+        const int rb = wave + 4 * r;
+        if (rb >= nrb) break;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           const int w0 = rb * 32 + j * 8 + (lane >> 5) * 4;
           if ((m & 3) == 0) {
             const float4 q4 = *(const float4*)(qa + min(w0, m - 4));
-            qv[4 * j] = q4.x; qv[4 * j + 1] = q4.y; qv[4 * j + 2] = q4.z; qv[4 * j + 3] = q4.w;
+            qv[r][4 * j] = q4.x; qv[r][4 * j + 1] = q4.y; qv[r][4 * j + 2] = q4.z; qv[r][4 * j + 3] = q4.w;
           } else {
 #pragma unroll
-            for (int i = 0; i < 4; ++i) qv[4 * j + i] = qa[min(w0 + i, m - 1)];
+            for (int i = 0; i < 4; ++i) qv[r][4 * j + i] = qa[min(w0 + i, m - 1)];
           }
         }
       }
+    }
+    fetch(t0 + 32);
+    float tk = 0.0f, tv = 0.0f, tq = 0.0f;
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      const int rb = wave + 4 * r;
+      if (rb >= nrb) break;
       f32x16 accL = {}, accY = {}, accR = {};
 #pragma unroll
       for (int s = 0; s < NKS; ++s) {
@@ -383,7 +537,7 @@ __global__ __launch_bounds__(256, R == 1 ? 2 : 1) void k_epilogue(Geo g, Ws w, C
             const float a2 = al * al;
             float qr;
             if constexpr (RP) qr = accR[e];
-            else qr = fmaf(-gk, qv[e], l);
+            else qr = fmaf(-gk, qv[r][e], l);
             // ||v - y||^2 >= 0: the cancellation form can dip below zero
             // when y nearly equals v; the bounds below cover the clamp.
             const float vv = fmaxf(fmaf(-2.0f, accY[e], vn + yq[i]), 0.0f);
@@ -439,7 +593,8 @@ __global__ __launch_bounds__(256, R == 1 ? 2 : 1) void k_epilogue(Geo g, Ws w, C
       const int t = tb + tl;
       if (t >= S) continue;
       float uk = -1.0f, uv = -1.0f, ukl = -1.0f, uku = -1.0f, uvl = -1.0f, uvu = -1.0f;
-      const int ak = aK_s[tl];
+      const int fk0 = fa_s[0][tl];
+      const int ak = (fk0 & (F_PAST | F_ANC)) ? -1 : (fk0 & F_IDX);
       if (ak >= 0) {
         const float sk = sumK[tl], sv = sumV[tl], sq = sumQ[tl];
         uk = sk / ((float)m * (float)D);
@@ -488,9 +643,9 @@ __global__ __launch_bounds__(256, R == 1 ? 2 : 1) void k_epilogue(Geo g, Ws w, C
         // value side: ||r_V||^2 (fp32 sum of squares of the fp32 residual; for
         // an fp32 cache the residual's product rounding differs from the
         // canonical form by <= 2u |gamma| |a| per coordinate)
-        const int av = w.apos[TS + po + t];
-        const float gv = fabsf(w.gpos[TS + po + t]);
-        const float anv = (av >= 0 && av < k) ? (float)sqrt((c.nrmV)[ko + av]) * (1.0f + 2.0f * U) : 0.0f;
+        const int fv = fa_s[1][tl];
+        const float gv = fabsf(gV_s[tl]);
+        const float anv = (fv & F_BAD) ? 0.0f : (float)sqrt((c.nrmV)[ko + (fv & F_IDX)]) * (1.0f + 2.0f * U);
         const float rv2 = rv2_s[tl];
         const float drv = 300.0f * U * rv2 + (DT == 1 ? 0.0f : 4.1f * U * sqrtf(rv2) * gv * anv * 1.01f);
         const float ufV = fmaxf(2.4e-38f, 2.4e-38f * (rv2 + drv + 1.0f));
