@@ -117,25 +117,46 @@ def test_assignment_exact_ties_and_zero_tokens(dtype):
     assert np.abs(out[0].cpu().numpy() - ref).max() <= (1e-4 if dtype == "f32" else 2e-3)
 
 
-def test_coefficient_rounding_boundaries():
-    """Stored coefficients at and next to bf16 rounding boundaries (Sec. 3.1
-    Eq. projection; the coefficient is rounded to the cache dtype): with the
-    anchor a = (1, ..., 1), tokens 1 + e_0/2 and 1 + 3 e_0/2 give gamma =
-    1 + 2^-8 and 1 + 3 * 2^-8, exact ties between bf16 neighbours (to even:
-    1 and 1 + 2^-6), which the kernel's certified fp32 estimate cannot decide,
-    so the sequential fp64 sum does; tokens with one more coordinate at
-    1 +- 2^-7 sit 2^-14 from a tie and are decided by the estimate."""
-    wl = _wl("gamma_ties", seq_lens=[600], anchor_count=64, anchor_frac=0.0, n_outlier=0)
-    print("[edge] coefficient rounding boundaries", flush=True)
+# Per cache dtype: (c0 values, c1 values, expected stored coefficients).  With
+# the anchor a = (1, ..., 1) (||a||^2 = D = 128), a token (c0, c1, 1, ..., 1)
+# has gamma = (126 + c0 + c1) / 128.
+_GAMMA_TIES = {
+    # bf16: c0 = 1.5 and 2.5 give gamma = 1 + 2^-8 and 1 + 3 * 2^-8, exact ties
+    # between bf16 neighbours (to even: 1 and 1 + 2^-6); c1 = 1 +- 2^-7 moves
+    # gamma 2^-14 above or below the tie.
+    "bf16": ((1.5, 2.5), (1.0, 1.0078125, 0.9921875),
+             [1.0, 1.0078125, 1.0, 1.015625, 1.015625, 1.0078125]),
+    # fp32: c0 = 1 + 2^-17 and 1 + 3 * 2^-17 give gamma = 1 + 2^-24 and
+    # 1 + 3 * 2^-24, exact ties between fp32 neighbours (to even: 1 and
+    # 1 + 2^-22); c1 = 1 +- 2^-20 moves gamma 2^-27 above or below the tie.
+    "f32": ((1.0 + 2.0 ** -17, 1.0 + 3 * 2.0 ** -17), (1.0, 1.0 + 2.0 ** -20, 1.0 - 2.0 ** -20),
+            [1.0, 1.0 + 2.0 ** -23, 1.0, 1.0 + 2.0 ** -22, 1.0 + 2.0 ** -22, 1.0 + 2.0 ** -23]),
+}
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_coefficient_rounding_boundaries(dtype):
+    """Stored coefficients at and next to rounding boundaries of the cache
+    dtype (Sec. 3.1 Eq. projection; the coefficient is rounded to the cache
+    dtype).  Exact ties between neighbours cannot be decided by the kernel's
+    certified estimate (an fp32 sum of the exact bf16 products, or an fp64
+    sum of the exact fp32 products), so the sequential fp64 sum decides them
+    (round to nearest, ties to even); tokens next to a tie are decided by the
+    estimate."""
+    c0s, c1s, want = _GAMMA_TIES[dtype]
+    wl = _wl("gamma_ties_" + dtype, dtype=dtype, seq_lens=[600], anchor_count=64, anchor_frac=0.0, n_outlier=0)
+    print(f"[edge] coefficient rounding boundaries {dtype}", flush=True)
     layer = synth.make_layer(wl)
     S, W = wl.seq_lens[0], wl.window
-    one = torch.ones(wl.D, dtype=torch.bfloat16)
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    one = torch.ones(wl.D, dtype=tdt)
     rows = []
-    for c0 in (1.5, 2.5):
-        for c1 in (1.0, 1.0078125, 0.9921875):
+    for c0 in c0s:
+        for c1 in c1s:
             r = one.clone()
             r[0] = c0
             r[1] = c1
+            assert float(r[0]) == c0 and float(r[1]) == c1  # representable in the dtype
             rows.append(r)
     for X in (layer.K[0], layer.V[0]):
         for h in range(wl.H):
@@ -154,9 +175,6 @@ def test_coefficient_rounding_boundaries():
     for side in ("k", "v"):
         a, gm = exp["a_" + side], exp["gamma_" + side]
         assert (a[:, 100:124] == 0).all()
-        # (c0, c1) = (1.5, 1), (1.5, 1 + 2^-7), (1.5, 1 - 2^-7), then c0 = 2.5:
-        # exact ties to even, then 2^-14 above and below the tie
-        want = [1.0, 1.0078125, 1.0, 1.015625, 1.015625, 1.0078125]
         got = [float(gm[0, 100 + 4 * i]) for i in range(6)]
         assert got == want, (side, got)
 
