@@ -140,10 +140,10 @@ struct Cache {
 
 // Encode scratch.
 struct Ws {
-  double* o64M;         // [b][h][chunk64][mpad] fp64 pass: chunk row max of the logits
-  double* o64Z;         // [b][h][chunk64][mpad] chunk sum of exp(l - chunk max)
+  double* o64M;         // [b][h][chunk64][mpad] fp64 pass: chunk row reference of the logits (<= 20 below their max)
+  double* o64Z;         // [b][h][chunk64][mpad] chunk sum of exp(l - chunk reference)
   double* o64O;         // [b][h][chunk64][mpad/16][8][4][64] chunk outputs (unnormalized, lane order)
-  double* M64;          // [b][h][m] row max of the fp64 logits
+  double* M64;          // [b][h][m] row reference M_w of the fp64 logits (at most 20 below their max)
   double* Z64;          // [b][h][m] sum_t exp(l_wt - M_w)
   double* Y64;          // [b][h][m][D] y_w in fp64
   float* Y;             // [b][h][m][D] fp32 rounding of y_w

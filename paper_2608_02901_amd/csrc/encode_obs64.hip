@@ -1,9 +1,10 @@
 // fp64 observation attention of the compression pass: for every KV head the
 // m = W * (Hq/H) observation rows (the queries of the last W positions,
 // causal inside the window; Sec. 3.2, App. A.2) attend to all positions, and
-// this pass returns per row the logit max M_w, Z_w = sum_t exp(l_wt - M_w) and
-// y_w = sum_t alpha_wt v_t in fp64 (Sec. 3.3 Eq. utilities uses alpha_wt and
-// y_w).  The utility epilogue reads them to bound its fp32 utilities, the
+// this pass returns per row a reference M_w of the logits (at most 20 below
+// their maximum), Z_w = sum_t exp(l_wt - M_w) and y_w = sum_t alpha_wt v_t in
+// fp64, alpha_wt = exp(l_wt - M_w) / Z_w (Sec. 3.3 Eq. utilities uses alpha_wt
+// and y_w; the softmax does not depend on the reference).  The utility epilogue reads them to bound its fp32 utilities, the
 // residual budget re-scores the candidates at its cut with them, and the
 // anchor selection re-scores its near-ties with M_w and Z_w.
 //
@@ -26,7 +27,10 @@ typedef __attribute__((ext_vector_type(4))) double f64x4;
 
 constexpr int O64_KT = 32;          // keys per LDS tile (two MFMA key tiles)
 constexpr int O64_MAXCH = 256;      // most chunks per head (the reduce keeps their scales in LDS)
-constexpr double O64_NEG = -1e300;  // running-max sentinel (finite: exp of differences stays defined)
+constexpr double O64_NEG = -1e300;  // reference sentinel (finite: exp of differences stays defined)
+// A row's reference lags its running maximum by at most this much (logit
+// units), so p = exp(l - reference) <= exp(20).
+constexpr double O64_SLACK = 20.0;
 
 template <int DT>
 __device__ inline double e2d(const void* p, int i) {
@@ -99,7 +103,7 @@ __global__ __launch_bounds__(256) void k_obs64(Geo g, Ws w, const void* Kin, con
     }
   };
 
-  double mrow = O64_NEG, zl = 0.0;  // running max of the row (same on its 4 lanes), lane-partial sum
+  double mrow = O64_NEG, zl = 0.0;  // reference of the row (same on its 4 lanes), lane-partial sum
   f64x4 O[8];
 #pragma unroll
   for (int blk = 0; blk < 8; ++blk) O[blk] = f64x4{0.0, 0.0, 0.0, 0.0};
@@ -147,18 +151,23 @@ __global__ __launch_bounds__(256) void k_obs64(Geo g, Ws w, const void* Kin, con
       }
       tmax = fmax(tmax, __shfl_xor(tmax, 16, 64));
       tmax = fmax(tmax, __shfl_xor(tmax, 32, 64));
-      const double nm = fmax(mrow, tmax);
-      if (__ballot(nm > mrow)) {  // some row's max moved: rescale (factor 1 on the others)
-        const double scl = exp(mrow - nm);
+      // The row's reference mrow moves only when a logit exceeds it by more
+      // than O64_SLACK (then to the running maximum, rescaling the sums), so
+      // the rescale of the eight accumulators is rare: every p stays below
+      // exp(O64_SLACK), far inside fp64 (and fp32) range.
+      const bool up = tmax > mrow + O64_SLACK;
+      if (__ballot(up)) {  // some row's reference moves (factor 1 on the others)
+        const double nr = up ? tmax : mrow;
+        const double scl = exp(mrow - nr);
         zl *= scl;
 #pragma unroll
         for (int blk = 0; blk < 8; ++blk) O[blk] *= scl;
+        mrow = nr;
       }
-      mrow = nm;
       double p[4];
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        p[r] = ok[r] ? exp(lg[r] - nm) : 0.0;
+        p[r] = ok[r] ? exp(lg[r] - mrow) : 0.0;
         zl += p[r];
       }
       // ---- values: MFMA r contracts the keys 16u + kq + 4r (k = kq); lane l
@@ -190,7 +199,7 @@ __global__ __launch_bounds__(256) void k_obs64(Geo g, Ws w, const void* Kin, con
     for (int r = 0; r < 4; ++r) op[(blk * 4 + r) * 64 + lane] = O[blk][r];
 }
 
-// One workgroup per (request, head, 16 rows): M_w = max of the chunk maxima,
+// One workgroup per (request, head, 16 rows): M_w = max of the chunk references,
 // Z_w = sum_c Z_c exp(M_c - M_w), y_w = sum_c O_c exp(M_c - M_w) / Z_w (chunks
 // in order), then the fp32 forms: y rounded and its bf16 hi/lo split, ||y||^2,
 // (M + ln Z) log2(e) and ||q_w||.
