@@ -3,8 +3,8 @@
 // (the queries of the last W positions, causal inside the window) attend to
 // all positions, and k_obs_pass takes fp32 MFMA logits q_w.k_t / sqrt(D),
 // alpha = exp(l - M_w) / Z_w with the row statistics of the fp64 pass
-// (encode_obs64.hip, which runs first) and the SnapKV column score
-// sc(t) = (1/m) sum_w alpha_wt.
+// (encode_obs64.hip, which runs first; as c_w = (M_w + ln Z_w) log2(e)) and
+// the SnapKV column score sc(t) = (1/m) sum_w alpha_wt.
 #include "akv_common.h"
 
 namespace akv {
@@ -82,25 +82,27 @@ __global__ __launch_bounds__(256) void k_obs_pass(Geo g, Ws w, const void* Kin, 
   const size_t xoff = ((size_t)g.prefS[b] * g.H + (size_t)h * S) * D;
   const E* X = (const E*)Kin + xoff;
   const E* Q = qrows<DT>(g, Qin, b, h);
-  const double* M64 = w.M64 + (size_t)(b * g.H + h) * m;
-  const double* Z64 = w.Z64 + (size_t)(b * g.H + h) * m;
+  const float* cw = w.cw + (size_t)(b * g.H + h) * m;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int nrb = (m + 31) / 32;
-  const float isd = 1.0f / sqrtf((float)D);
-  // The lane's row of each row block: query fragments, row max, 1/Z and
-  // causal limit stay in registers; the next key tile is loaded while the
-  // current one is used.
+  // alpha = exp(l / sqrt(D) - M_w) / Z_w is taken as exp2(l log2(e) / sqrt(D)
+  // - c_w) with c_w = (M_w + ln Z_w) log2(e) from the fp64 row statistics
+  // (one fused multiply-add and one exp2 per pair); rows past m get
+  // c_w = +inf, hence alpha = 0.
+  const float isl = 1.4426950408889634f / sqrtf((float)D);
+  // The lane's row of each row block: query fragments, c_w and causal limit
+  // stay in registers; the next key tile is loaded while the current one is
+  // used.
   constexpr int NKS = AKV_D / M::KS;
   typename M::frag qf[R][NKS];
-  float rmax[R], riz[R];
+  float cwr[R];
   int lim[R];
 #pragma unroll
   for (int r = 0; r < R; ++r) {
     const int wr = (wave + 4 * r) * 32 + (lane & 31);
     const int arow = min(wr, m - 1);
     lim[r] = obs_limit(wr, m, P, g.W);
-    rmax[r] = (float)M64[arow];
-    riz[r] = (float)(1.0 / Z64[arow]);
+    cwr[r] = wr < m ? cw[arow] : INFINITY;
 #pragma unroll
     for (int s = 0; s < NKS; ++s) qf[r][s] = M::load(Q + (size_t)arow * D, kofs(M::KS, s, lane));
   }
@@ -136,11 +138,17 @@ __global__ __launch_bounds__(256) void k_obs_pass(Geo g, Ws w, const void* Kin, 
         auto kb = M::load_lds(&KT[cb][(lane & 31) * LD], kofs(M::KS, s, lane));
         acc = M::mma(kb, qf[r][s], acc);
       }
-      // alpha of the lane's row and tokens t0 + crow(e, lane).
+      // alpha of the lane's row and tokens t0 + crow(e, lane); a tile before
+      // the window (every row attends to all of it) needs no causal mask.
+      if (t0 + 32 <= P) {
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const float a = __expf(acc[e] * isd - rmax[r]) * riz[r];
-        cs[e] += t0 + crow(e, lane) <= lim[r] ? a : 0.0f;
+        for (int e = 0; e < 16; ++e) cs[e] += __builtin_amdgcn_exp2f(fmaf(acc[e], isl, -cwr[r]));
+      } else {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const float a = __builtin_amdgcn_exp2f(fmaf(acc[e], isl, -cwr[r]));
+          cs[e] += t0 + crow(e, lane) <= lim[r] ? a : 0.0f;
+        }
       }
     }
     // Column sums over the wave's rows: the 16 lanes of a DPP row, then the
