@@ -149,7 +149,7 @@ struct Ws {
   float* Y;             // [b][h][m][D] fp32 rounding of y_w
   uint16_t* Yhi;        // [b][h][m][D] bf16 split of Y: Y ~ hi + lo
   uint16_t* Ylo;
-  float* ynorm;         // [b][h][m] ||y_w||^2 (fp32 rounding of the fp64 sum)
+  double* ynp;          // [b][h][m][4] fp64 partial sums of y_w^2 over the four quarters of the dimensions
   float* cw;            // [b][h][m] (M_w + ln Z_w) log2(e), fp32
   float* qn;            // [b][h][m] ||q_w||, rounded up
   float* sc;            // [b][h][S_b] selector score, then pooled score

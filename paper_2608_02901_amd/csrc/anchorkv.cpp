@@ -108,7 +108,7 @@ struct anchorkv_plan {
       c_stats;
   size_t cache_bytes;
   // encode workspace offsets
-  size_t w_o64M, w_o64Z, w_o64O, w_M64, w_Z64, w_Y64, w_Y, w_Yhi, w_Ylo, w_ynorm,
+  size_t w_o64M, w_o64Z, w_o64O, w_M64, w_Z64, w_Y64, w_Y, w_Yhi, w_Ylo, w_ynp,
       w_cw, w_qn, w_uL, w_uU, w_bandpos, w_bandu, w_brank, w_sc, w_rank, w_flag, w_sband, w_sbscore, w_sstate, w_sghist, w_scand, w_rkey, w_rpos, w_slcnt, w_QA, w_apos,
       w_fix, w_fixcount, w_gpos, w_xn2, w_u, w_sel, w_srec, w_bhist, w_bstate, w_bcval, w_bcpos, w_tiecnt, w_shist, w_wcnt,
       w_krot, w_cs;
@@ -383,7 +383,7 @@ extern "C" anchorkv_status anchorkv_plan_create(const anchorkv_config* cfg, int3
   p->w_Y = Wl.add(4 * batch * H * m * D);
   p->w_Yhi = Wl.add(2 * batch * H * m * D);
   p->w_Ylo = Wl.add(2 * batch * H * m * D);
-  p->w_ynorm = Wl.add(4 * batch * H * m);
+  p->w_ynp = Wl.add(8 * 4 * batch * H * m);
   p->w_sc = Wl.add(4 * TS);
   p->w_rank = Wl.add(4 * TS);
   p->w_flag = Wl.add(TS);
@@ -498,7 +498,7 @@ static akv::Ws ws_ptrs(const anchorkv_plan* p, void* base) {
   w.Y = at<float>(base, p->w_Y);
   w.Yhi = at<uint16_t>(base, p->w_Yhi);
   w.Ylo = at<uint16_t>(base, p->w_Ylo);
-  w.ynorm = at<float>(base, p->w_ynorm);
+  w.ynp = at<double>(base, p->w_ynp);
   w.sc = at<float>(base, p->w_sc);
   w.rank = at<int32_t>(base, p->w_rank);
   w.flag = at<uint8_t>(base, p->w_flag);

@@ -350,7 +350,7 @@ __global__ __launch_bounds__(256, R == 1 ? 2 : 1) void k_epilogue(Geo g, Ws w, C
   const float isl = LOG2E / sqrtf((float)D);  // logit scale in base 2
   const float* cw = w.cw + (size_t)(b * g.H + h) * m;
   const float* qn = w.qn + (size_t)(b * g.H + h) * m;
-  const float* yn = w.ynorm + (size_t)(b * g.H + h) * m;
+  const double* ynp = w.ynp + (size_t)(b * g.H + h) * m * 4;  // quarters of ||y_w||^2
   const float* QA = w.QA + ko * m;
   // alpha = exp(l / sqrt(D) - M_w) / Z_w is taken as exp2(l log2(e) / sqrt(D)
   // - c_w) with c_w = (M_w + ln Z_w) log2(e) from the fp64 row statistics;
@@ -360,11 +360,13 @@ __global__ __launch_bounds__(256, R == 1 ? 2 : 1) void k_epilogue(Geo g, Ws w, C
   if (threadIdx.x < 3) hmax[threadIdx.x] = 0u;
   __syncthreads();
   for (int wr = threadIdx.x; wr < nrb * 32; wr += 256) {
+    // ||y_w||^2: the fp32 rounding of the fp64 sum of the four quarters
+    const float yn = wr < m ? (float)((ynp[4 * wr] + ynp[4 * wr + 1]) + (ynp[4 * wr + 2] + ynp[4 * wr + 3])) : 0.0f;
     CVS[wr] = wr < m ? cw[wr] : 1e30f;
-    YVS[wr] = wr < m ? yn[wr] : 0.0f;
+    YVS[wr] = yn;
     if (wr < m) {
       atomicMax(&hmax[0], __float_as_uint(qn[wr]));
-      atomicMax(&hmax[1], __float_as_uint(yn[wr]));
+      atomicMax(&hmax[1], __float_as_uint(yn));
       atomicMax(&hmax[2], __float_as_uint(fabsf(cw[wr])));
     }
   }

@@ -199,10 +199,12 @@ __global__ __launch_bounds__(256) void k_obs64(Geo g, Ws w, const void* Kin, con
     for (int r = 0; r < 4; ++r) op[(blk * 4 + r) * 64 + lane] = O[blk][r];
 }
 
-// One workgroup per (request, head, 16 rows): M_w = max of the chunk references,
-// Z_w = sum_c Z_c exp(M_c - M_w), y_w = sum_c O_c exp(M_c - M_w) / Z_w (chunks
-// in order), then the fp32 forms: y rounded and its bf16 hi/lo split, ||y||^2,
-// (M + ln Z) log2(e) and ||q_w||.
+// One workgroup per (request, head, 16 rows, quarter of the dimensions):
+// M_w = max of the chunk references, Z_w = sum_c Z_c exp(M_c - M_w) (every
+// quarter forms them alike), y_w = sum_c O_c exp(M_c - M_w) / Z_w over the
+// quarter's 32 dimensions (chunks in order), then the fp32 forms: y rounded
+// and its bf16 hi/lo split, and the quarter's fp64 partial of ||y_w||^2.  The
+// first quarter also writes M_w, Z_w, (M + ln Z) log2(e) and ||q_w||.
 template <int DT>
 __global__ __launch_bounds__(256) void k_obs64_reduce(Geo g, Ws w, const void* Qin) {
   using E = typename Elem<DT>::T;
@@ -210,7 +212,8 @@ __global__ __launch_bounds__(256) void k_obs64_reduce(Geo g, Ws w, const void* Q
   __shared__ double red[16][16];
   __shared__ double Msh[16], Zsh[16];
   const int nrb = g.mpad / 16;
-  const int bh = blockIdx.x / nrb, rb16 = blockIdx.x % nrb, b = bh / g.H, h = bh % g.H;
+  const int qd = blockIdx.x & 3, blk16 = blockIdx.x >> 2;
+  const int bh = blk16 / nrb, rb16 = blk16 % nrb, b = bh / g.H, h = bh % g.H;
   const int m = g.m, D = AKV_D;
   const int nch = (g.S[b] + g.oc64 - 1) / g.oc64;
   const size_t gc0 = (size_t)g.prefC64[b] * g.H + (size_t)h * nch;
@@ -242,38 +245,38 @@ __global__ __launch_bounds__(256) void k_obs64_reduce(Geo g, Ws w, const void* Q
     Zsh[tid] = Z;
   }
   __syncthreads();
-  // Outputs: the thread's lane slot in the chunk layout, 8 elements of row r16.
+  // Outputs: in the chunk layout, register slot (blk * 4 + r) of lane l holds
+  // dimension 8 (l / 16 + 4 r) + blk of row l % 16; the quarter qd takes
+  // blk = 2 qd, 2 qd + 1 (512 contiguous values per chunk), two per thread.
   const int lane = tid & 63;
   const size_t bhm = (size_t)bh * m;
-  double sq = 0.0;
-  // the thread's 8 outputs (2 column groups x 4 register slots), chunks added
-  // in order, 8 chunks x 8 outputs loaded per round
-  double acc[8];
-  const double* op[8];
+  double acc[2];
+  const double* op[2];
 #pragma unroll
-  for (int q = 0; q < 8; ++q) {
-    const int blk = 2 * (tid >> 6) + (q >> 2), r = q & 3;
-    op[q] = w.o64O + (gc0 * nrb + rb16) * 2048 + (blk * 4 + r) * 64 + lane;
+  for (int q = 0; q < 2; ++q) {
+    const int slot = 8 * qd + 4 * q + (tid >> 6);  // blk * 4 + r
+    op[q] = w.o64O + (gc0 * nrb + rb16) * 2048 + slot * 64 + lane;
     acc[q] = 0.0;
   }
   const size_t cstride = (size_t)nrb * 2048;
-  for (int c0 = 0; c0 < nch; c0 += 8) {
-    double v[8][8];
+  for (int c0 = 0; c0 < nch; c0 += 16) {
+    double v[16][2];
 #pragma unroll
-    for (int u = 0; u < 8; ++u)
+    for (int u = 0; u < 16; ++u)
 #pragma unroll
-      for (int q = 0; q < 8; ++q) v[u][q] = c0 + u < nch ? op[q][(size_t)(c0 + u) * cstride] : 0.0;
+      for (int q = 0; q < 2; ++q) v[u][q] = c0 + u < nch ? op[q][(size_t)(c0 + u) * cstride] : 0.0;
 #pragma unroll
-    for (int u = 0; u < 8; ++u)
+    for (int u = 0; u < 16; ++u)
       if (c0 + u < nch) {
         const double sc = scl[c0 + u][r16];
 #pragma unroll
-        for (int q = 0; q < 8; ++q) acc[q] += v[u][q] * sc;
+        for (int q = 0; q < 2; ++q) acc[q] += v[u][q] * sc;
       }
   }
+  double sq = 0.0;
 #pragma unroll
-  for (int q = 0; q < 8; ++q) {
-    const int blk = 2 * (tid >> 6) + (q >> 2), r = q & 3;
+  for (int q = 0; q < 2; ++q) {
+    const int slot = 8 * qd + 4 * q + (tid >> 6), blk = slot >> 2, r = slot & 3;
     const double y = acc[q] / Zsh[r16];
     const int dim = 8 * ((lane >> 4) + 4 * r) + blk;
     if (rok) {
@@ -293,18 +296,28 @@ __global__ __launch_bounds__(256) void k_obs64_reduce(Geo g, Ws w, const void* Q
   if (tid < 16 && rok) {
     double t = 0.0;
     for (int p = 0; p < 16; ++p) t += red[p][tid];
-    const int rw = rb16 * 16 + tid;
-    w.ynorm[bhm + rw] = (float)t;
-    w.M64[bhm + rw] = Msh[tid];
-    w.Z64[bhm + rw] = Zsh[tid];
-    w.cw[bhm + rw] = (float)((Msh[tid] + log(Zsh[tid])) * 1.4426950408889634);
-    const E* q = (const E*)Qin + ((size_t)b * g.Hq + (size_t)h * g.g) * g.W * D + (size_t)rw * D;
+    w.ynp[(bhm + rb16 * 16 + tid) * 4 + qd] = t;
+  }
+  if (qd == 0) {
+    // ||q_w||: 16 threads per row, 8 coordinates each, then a fixed-order sum
+    __syncthreads();
+    const E* q = (const E*)Qin + ((size_t)b * g.Hq + (size_t)h * g.g) * g.W * D + (size_t)min(row, m - 1) * D;
     double qq = 0.0;
-    for (int j = 0; j < D; ++j) {
+    for (int j = 8 * part; j < 8 * part + 8; ++j) {
       const double x = e2d<DT>(q, j);
       qq += x * x;
     }
-    w.qn[bhm + rw] = (float)(sqrt(qq) * (1.0 + 1e-6));
+    red[part][r16] = qq;
+    __syncthreads();
+    if (tid < 16 && rok) {
+      double t = 0.0;
+      for (int p = 0; p < 16; ++p) t += red[p][tid];
+      const int rw = rb16 * 16 + tid;
+      w.M64[bhm + rw] = Msh[tid];
+      w.Z64[bhm + rw] = Zsh[tid];
+      w.cw[bhm + rw] = (float)((Msh[tid] + log(Zsh[tid])) * 1.4426950408889634);
+      w.qn[bhm + rw] = (float)(sqrt(t) * (1.0 + 1e-6));
+    }
   }
 }
 
@@ -312,7 +325,7 @@ hipError_t launch_obs64(const Geo& g, const Ws& w, const void* K, const void* V,
   const int nrg = (g.m + 63) / 64;
   int nblk = 0;
   for (int b = 0; b < g.B; ++b) nblk += g.H * nrg * ((g.S[b] + g.oc64 - 1) / g.oc64);
-  const int nred = g.B * g.H * (g.mpad / 16);
+  const int nred = g.B * g.H * (g.mpad / 16) * 4;
   if (g.dtype == 1) {
     launch("k_obs64", k_obs64<1>, dim3(nblk), dim3(256), 0, st, g, w, K, V, Q);
     launch("k_obs64_reduce", k_obs64_reduce<1>, dim3(nred), dim3(256), 0, st, g, w, Q);
