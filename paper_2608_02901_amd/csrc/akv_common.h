@@ -145,11 +145,12 @@ struct Ws {
   double* o64O;         // [b][h][chunk64][mpad/16][8][4][64] chunk outputs (unnormalized, lane order)
   double* M64;          // [b][h][m] row reference M_w of the fp64 logits (at most 20 below their max)
   double* Z64;          // [b][h][m] sum_t exp(l_wt - M_w)
-  double* Y64;          // [b][h][m][D] y_w in fp64
+  double* Y64;          // [b][h][D/2][m][2] y_w in fp64: dimension pairs, rows innermost
   float* Y;             // [b][h][m][D] fp32 rounding of y_w
   uint16_t* Yhi;        // [b][h][m][D] bf16 split of Y: Y ~ hi + lo
   uint16_t* Ylo;
   double* ynp;          // [b][h][m][4] fp64 partial sums of y_w^2 over the four quarters of the dimensions
+  void* qt;             // [b][h][D esz / 16][m] 16-byte chunks of the observation rows q_w, rows innermost
   float* cw;            // [b][h][m] (M_w + ln Z_w) log2(e), fp32
   float* qn;            // [b][h][m] ||q_w||, rounded up
   float* sc;            // [b][h][S_b] selector score, then pooled score
@@ -232,6 +233,19 @@ template <> struct Elem<1> {
   __device__ static void put(void* p, size_t i, float v) { ((uint16_t*)p)[i] = f2bf(v); }
   __device__ static float round_coef(float g) { return bf2f(f2bf(g)); }
 };
+
+// 16 bytes of row data as a native vector: copies of it stay in registers
+// (the struct form of uint4 is copied through memory when a copy is not
+// guarded by a branch, and an array of it indexed through a pointer is kept
+// in scratch).
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+
+// Element e of a 16-byte chunk of cache-dtype values, as fp32.
+template <int DT>
+__device__ inline float chunk_elem(const u32x4& v, int e) {
+  if constexpr (DT == 1) return __uint_as_float((e & 1) ? (v[e >> 1] & 0xFFFF0000u) : (v[e >> 1] << 16));
+  else return __uint_as_float(v[e]);
+}
 
 // MFMA traits: A[m][k] (anchors/rows), B[k][n] (tokens/columns), C 32x32.
 // Lane l supplies A[l%32][kofs..] and B[kofs..][l%32]; the accumulator entry

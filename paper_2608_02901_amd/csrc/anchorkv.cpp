@@ -27,7 +27,7 @@ hipError_t launch_assign(const Geo& g, const Ws& w, const Cache& c, const void* 
 hipError_t launch_epilogue(const Geo& g, const Ws& w, const Cache& c, const void* K, const void* Kobs, const void* V,
                            const void* Q, hipStream_t st);
 hipError_t launch_budget(const Geo& g, const Ws& w, const Cache& c, const void* K, const void* Kobs, const void* V,
-                         const void* Q, hipStream_t st);
+                         hipStream_t st);
 hipError_t launch_layout(const Geo& g, const Ws& w, const Cache& c, const void* K, const void* V, hipStream_t st);
 hipError_t launch_decode(const Geo& g, const Cache& c, const DecWs& dw, const void* q, const void* kn,
                          const void* vn, void* out, int out_dtype, float scale, int n_app, hipStream_t st);
@@ -108,7 +108,7 @@ struct anchorkv_plan {
       c_stats;
   size_t cache_bytes;
   // encode workspace offsets
-  size_t w_o64M, w_o64Z, w_o64O, w_M64, w_Z64, w_Y64, w_Y, w_Yhi, w_Ylo, w_ynp,
+  size_t w_o64M, w_o64Z, w_o64O, w_M64, w_Z64, w_Y64, w_Y, w_Yhi, w_Ylo, w_ynp, w_qt,
       w_cw, w_qn, w_uL, w_uU, w_bandpos, w_bandu, w_brank, w_sc, w_rank, w_flag, w_sband, w_sbscore, w_sstate, w_sghist, w_scand, w_rkey, w_rpos, w_slcnt, w_QA, w_apos,
       w_fix, w_fixcount, w_gpos, w_xn2, w_u, w_sel, w_srec, w_bhist, w_bstate, w_bcval, w_bcpos, w_tiecnt, w_shist, w_wcnt,
       w_krot, w_cs;
@@ -384,6 +384,7 @@ extern "C" anchorkv_status anchorkv_plan_create(const anchorkv_config* cfg, int3
   p->w_Yhi = Wl.add(2 * batch * H * m * D);
   p->w_Ylo = Wl.add(2 * batch * H * m * D);
   p->w_ynp = Wl.add(8 * 4 * batch * H * m);
+  p->w_qt = Wl.add(esz * batch * H * m * D);
   p->w_sc = Wl.add(4 * TS);
   p->w_rank = Wl.add(4 * TS);
   p->w_flag = Wl.add(TS);
@@ -499,6 +500,7 @@ static akv::Ws ws_ptrs(const anchorkv_plan* p, void* base) {
   w.Yhi = at<uint16_t>(base, p->w_Yhi);
   w.Ylo = at<uint16_t>(base, p->w_Ylo);
   w.ynp = at<double>(base, p->w_ynp);
+  w.qt = at<uint8_t>(base, p->w_qt);
   w.sc = at<float>(base, p->w_sc);
   w.rank = at<int32_t>(base, p->w_rank);
   w.flag = at<uint8_t>(base, p->w_flag);
@@ -601,7 +603,7 @@ extern "C" anchorkv_status anchorkv_encode(const anchorkv_plan* p, const void* K
     return s;
   if ((s = hip_status(akv::launch_assign(g, w, c, K, V, st), "assignment")) != ANCHORKV_OK) return s;
   if ((s = hip_status(akv::launch_epilogue(g, w, c, K, Kobs, V, Q_obs, st), "utilities")) != ANCHORKV_OK) return s;
-  if ((s = hip_status(akv::launch_budget(g, w, c, K, Kobs, V, Q_obs, st), "budget")) != ANCHORKV_OK) return s;
+  if ((s = hip_status(akv::launch_budget(g, w, c, K, Kobs, V, st), "budget")) != ANCHORKV_OK) return s;
   if ((s = hip_status(akv::launch_layout(g, w, c, K, V, st), "layout")) != ANCHORKV_OK) return s;
   return fs.finish(ANCHORKV_OK);
 }

@@ -465,6 +465,35 @@ __global__ __launch_bounds__(256) void k_bmark(Geo g, Ws w) {
   if (lane == 0 && ns) atomicAdd(&st[BST_NEED], ns);
 }
 
+// Sequential fp64 dots of a query row (16-byte chunks, chunk c at q4[c m]) with the
+// member's key row x and, when R is set, its residual r (both fp64 in LDS):
+// l = sum_j q_j x_j and qr = sum_j q_j r_j, products rounded, then added in
+// j order.  The row is loaded 16 chunks at a time (the whole bf16 row, half
+// an fp32 row) before any is consumed; the scheduling fences keep each
+// chunk's LDS operands from being read ahead of earlier chunks' work.
+template <int DT, bool R>
+__device__ inline void qrow_dots(const u32x4* q4, int m, const double* xd, const double* rr, double& l, double& qr) {
+  constexpr int PER = 16 / sizeof(typename Elem<DT>::T), NC = AKV_D / PER, QB = 16;
+#pragma unroll 1
+  for (int c0 = 0; c0 < NC; c0 += QB) {
+    u32x4 qc[QB];
+#pragma unroll
+    for (int u = 0; u < QB; ++u) qc[u] = q4[(size_t)(c0 + u) * m];
+#pragma unroll
+    for (int u = 0; u < QB; ++u) {
+      __builtin_amdgcn_sched_barrier(0);
+      asm volatile("" : "+v"(qc[u]));  // unpack this chunk here, not all at once
+#pragma unroll
+      for (int e = 0; e < PER; ++e) {
+        const double qe = (double)chunk_elem<DT>(qc[u], e);
+        l += qe * xd[(c0 + u) * PER + e];
+        if constexpr (R) qr += qe * rr[(c0 + u) * PER + e];
+      }
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  }
+}
+
 // fp64 utility of every listed band member, one wave per member, computed as
 // the oracle computes it (Sec. 3.3 Eq. utilities): the stored coefficient's
 // residual r = x - fp32(gamma a) in fp32; per observation row w (lane w, w + 64,
@@ -476,10 +505,13 @@ __global__ __launch_bounds__(256) void k_bmark(Geo g, Ws w) {
 // rank_key64 on one lane.
 template <int DT>
 __global__ __launch_bounds__(256) void k_brescore(Geo g, Ws w, Cache c, const void* Kin, const void* Kobs,
-                                                  const void* Vin, const void* Qin) {
+                                                  const void* Vin) {
   using E = typename Elem<DT>::T;
-  __shared__ float xs[4][AKV_D], vs[4][AKV_D], rs[4][AKV_D];
-  __shared__ double rr[4][AKV_D];  // R_t r_K in fp64 (positions encoded)
+  // the member's rows widened to fp64 once (exact), so the per-row loops
+  // below convert only the query elements
+  __shared__ float rs[4][AKV_D];
+  __shared__ double xd[4][AKV_D], vd[4][AKV_D];
+  __shared__ double rr[4][AKV_D];  // r, or R_t r_K when positions are encoded
   __shared__ double terms[4][256];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int nw = gridDim.x * 4;
@@ -516,9 +548,11 @@ __global__ __launch_bounds__(256) void k_brescore(Geo g, Ws w, Cache c, const vo
       }
       for (int j = lane; j < D; j += 64) {
         const float p = gm * Elem<DT>::get(ar, j);
-        rs[wave][j] = Elem<DT>::get(xr, j) - p;
-        xs[wave][j] = Elem<DT>::get(kr, j);
-        vs[wave][j] = Elem<DT>::get(vr, j);
+        const float r = Elem<DT>::get(xr, j) - p;
+        rs[wave][j] = r;
+        rr[wave][j] = r;
+        xd[wave][j] = Elem<DT>::get(kr, j);
+        vd[wave][j] = Elem<DT>::get(vr, j);
       }
       __builtin_amdgcn_wave_barrier();
       __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
@@ -536,27 +570,16 @@ __global__ __launch_bounds__(256) void k_brescore(Geo g, Ws w, Cache c, const vo
       }
       double rvn = 0.0;
       if (side == 1)
-        for (int j = 0; j < D; ++j) rvn += (double)rs[wave][j] * (double)rs[wave][j];
+        for (int j = 0; j < D; ++j) rvn += rr[wave][j] * rr[wave][j];
       const size_t bh = (size_t)b * g.H + h;
-      const E* Q = (const E*)Qin + ((size_t)b * g.Hq + (size_t)h * g.g) * g.W * D;
-      constexpr int PER = 16 / sizeof(E);
-      constexpr int NC = AKV_D / PER;
       for (int wr = lane; wr < m; wr += 64) {
-        // q.k and q.r_K in one pass over the lane's query row, 16 bytes at a
-        // time with the next chunk's load in flight (sequential sums)
-        const uint4* q4 = (const uint4*)(Q + (size_t)wr * D);
+        // q.k (and q.r_K for keys) over the lane's query row
+        const u32x4* q4 = (const u32x4*)w.qt + bh * m * (AKV_D * sizeof(E) / 16) + wr;
         double l = 0.0, qr = 0.0;
-        uint4 cur = q4[0];
-        for (int c4 = 0; c4 < NC; ++c4) {
-          const uint4 nxt = q4[min(c4 + 1, NC - 1)];
-#pragma unroll
-          for (int e = 0; e < PER; ++e) {
-            const double qe = (double)Elem<DT>::get(&cur, e);
-            l += qe * (double)xs[wave][c4 * PER + e];
-            qr += qe * (rot ? rr[wave][c4 * PER + e] : (double)rs[wave][c4 * PER + e]);
-          }
-          cur = nxt;
-        }
+        if (side == 0 && !att)
+          qrow_dots<DT, true>(q4, m, xd[wave], rr[wave], l, qr);
+        else
+          qrow_dots<DT, false>(q4, m, xd[wave], rr[wave], l, qr);
         l = l / sqd;
         const double al = exp(l - w.M64[bh * m + wr]) / w.Z64[bh * m + wr];
         const double a2 = al * al;
@@ -564,18 +587,27 @@ __global__ __launch_bounds__(256) void k_brescore(Geo g, Ws w, Cache c, const vo
         if (att) {
           term = al;
         } else if (side == 0) {
-          const double4* y4 = (const double4*)(w.Y64 + (bh * m + wr) * D);
+          // ||v_t - y_w||^2 (sequential); y_w is stored in dimension pairs
+          // with the rows innermost, so that one load of the wave reads 64
+          // rows' pair p as 1 KB of contiguous memory.  Sixteen pairs are
+          // loaded before any is consumed.
+          const double2* y2 = (const double2*)(w.Y64 + bh * m * D) + wr;
           double vy = 0.0;
-          double4 yc = y4[0];
-          for (int c4 = 0; c4 < AKV_D / 4; ++c4) {
-            const double4 yn = y4[min(c4 + 1, AKV_D / 4 - 1)];
-            const double ye[4] = {yc.x, yc.y, yc.z, yc.w};
+          constexpr int YB = 16;
+#pragma unroll 1
+          for (int p0 = 0; p0 < AKV_D / 2; p0 += YB) {
+            double2 yc[YB];
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              const double dv = (double)vs[wave][4 * c4 + e] - ye[e];
-              vy += dv * dv;
+            for (int u = 0; u < YB; ++u) yc[u] = y2[(size_t)(p0 + u) * m];
+#pragma unroll
+            for (int u = 0; u < YB; ++u) {
+              __builtin_amdgcn_sched_barrier(0);
+              const double d0 = vd[wave][2 * (p0 + u)] - yc[u].x;
+              vy += d0 * d0;
+              const double d1 = vd[wave][2 * (p0 + u) + 1] - yc[u].y;
+              vy += d1 * d1;
             }
-            yc = yn;
+            __builtin_amdgcn_sched_barrier(0);
           }
           term = a2 * (qr * qr / D) * vy;
         } else {
@@ -586,8 +618,16 @@ __global__ __launch_bounds__(256) void k_brescore(Geo g, Ws w, Cache c, const vo
       __builtin_amdgcn_wave_barrier();
       __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
       if (lane == 0) {
+        // row order, the terms read 16 at a time
         double su = 0.0;
-        for (int wr = 0; wr < m; ++wr) su += terms[wave][wr];
+        for (int w0 = 0; w0 < m; w0 += 16) {
+          double tv[16];
+#pragma unroll
+          for (int u = 0; u < 16; ++u) tv[u] = terms[wave][w0 + u];
+#pragma unroll
+          for (int u = 0; u < 16; ++u)
+            if (w0 + u < m) su += tv[u];
+        }
         w.bandu[(size_t)bs * BAND_CAP + i] = su / m;
       }
       __builtin_amdgcn_wave_barrier();
@@ -657,7 +697,7 @@ __global__ __launch_bounds__(256) void k_bsel(Geo g, Ws w, Cache c) {
 }
 
 hipError_t launch_budget(const Geo& g, const Ws& w, const Cache& c, const void* K, const void* Kobs, const void* V,
-                         const void* Q, hipStream_t st) {
+                         hipStream_t st) {
   int nblk = 0, nkey = 0;
   const int nl = g.B * g.hdiv;
   for (int L = 0; L < nl; ++L) nblk += 2 * (((g.H / g.hdiv) * g.S[L / g.hdiv] + BCHUNK - 1) / BCHUNK);
@@ -674,9 +714,9 @@ hipError_t launch_budget(const Geo& g, const Ws& w, const Cache& c, const void* 
   launch("k_bbound", k_bbound, dim3(nblk), dim3(256), 0, st, g, w);
   launch("k_bmark", k_bmark, dim3(nblk), dim3(256), 0, st, g, w);
   if (g.dtype == 1)
-    launch("k_brescore", k_brescore<1>, dim3(1024), dim3(256), 0, st, g, w, c, K, Kobs, V, Q);
+    launch("k_brescore", k_brescore<1>, dim3(1024), dim3(256), 0, st, g, w, c, K, Kobs, V);
   else
-    launch("k_brescore", k_brescore<0>, dim3(1024), dim3(256), 0, st, g, w, c, K, Kobs, V, Q);
+    launch("k_brescore", k_brescore<0>, dim3(1024), dim3(256), 0, st, g, w, c, K, Kobs, V);
   launch("k_brank", k_brank, dim3(2048), dim3(RANK_T), 0, st, g, w);
   launch("k_bsel", k_bsel, dim3(64, nl * 2), dim3(256), 0, st, g, w, c);
   return hipGetLastError();

@@ -42,18 +42,6 @@ constexpr int EPI_TOK = 512;  // tokens per workgroup: 16 tiles of 32
 // from memory (fp64 fused multiply-add on the exact products, j = 0..D-1): the
 // rare fallback of the certified coefficient, one 16-byte chunk per step so
 // that it holds few registers in the caller.
-// 16 bytes of row data as a native vector: copies of it stay in registers
-// (the struct form of uint4 is copied through memory when a copy is not
-// guarded by a branch).
-typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
-
-// Element e of a 16-byte chunk of cache-dtype values, as fp32.
-template <int DT>
-__device__ inline float chunk_elem(const u32x4& v, int e) {
-  if constexpr (DT == 1) return __uint_as_float((e & 1) ? (v[e >> 1] & 0xFFFF0000u) : (v[e >> 1] << 16));
-  else return __uint_as_float(v[e]);
-}
-
 template <int DT>
 __device__ inline double dot64_rows(const typename Elem<DT>::T* x, const typename Elem<DT>::T* a) {
   constexpr int PER = 16 / sizeof(typename Elem<DT>::T);

@@ -204,7 +204,8 @@ __global__ __launch_bounds__(256) void k_obs64(Geo g, Ws w, const void* Kin, con
 // quarter forms them alike), y_w = sum_c O_c exp(M_c - M_w) / Z_w over the
 // quarter's 32 dimensions (chunks in order), then the fp32 forms: y rounded
 // and its bf16 hi/lo split, and the quarter's fp64 partial of ||y_w||^2.  The
-// first quarter also writes M_w, Z_w, (M + ln Z) log2(e) and ||q_w||.
+// first quarter also writes M_w, Z_w, (M + ln Z) log2(e), ||q_w|| and the
+// chunk-transposed copy of q_w (qt) that the band re-scoring reads.
 template <int DT>
 __global__ __launch_bounds__(256) void k_obs64_reduce(Geo g, Ws w, const void* Qin) {
   using E = typename Elem<DT>::T;
@@ -281,7 +282,7 @@ __global__ __launch_bounds__(256) void k_obs64_reduce(Geo g, Ws w, const void* Q
     const int dim = 8 * ((lane >> 4) + 4 * r) + blk;
     if (rok) {
       const size_t o = (bhm + row) * D + dim;
-      w.Y64[o] = y;
+      w.Y64[(bhm * D + (size_t)(dim >> 1) * m * 2) + row * 2 + (dim & 1)] = y;
       const float y32 = (float)y;
       w.Y[o] = y32;
       const uint16_t hi = f2bf(y32);
@@ -307,6 +308,14 @@ __global__ __launch_bounds__(256) void k_obs64_reduce(Geo g, Ws w, const void* Q
       const double x = e2d<DT>(q, j);
       qq += x * x;
     }
+    // the same 8 coordinates: one 16-byte chunk (bf16) or two (fp32)
+    constexpr int CPT = sizeof(E) / 2, NCH = AKV_D * sizeof(E) / 16;
+    if (rok)
+#pragma unroll
+      for (int u = 0; u < CPT; ++u) {
+        const int c = part * CPT + u;
+        ((u32x4*)w.qt)[((size_t)bh * NCH + c) * m + row] = ((const u32x4*)q)[c];
+      }
     red[part][r16] = qq;
     __syncthreads();
     if (tid < 16 && rok) {
