@@ -32,8 +32,11 @@ FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-ffp-contract=o
 
 # Per-source additions: the assignment kernels keep their MFMA accumulators in
 # VGPRs (the epilogue reads every accumulator entry), and their scores are
-# finite, so max/min need no NaN canonicalisation.
-EXTRA = {"encode_assign.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form", "-fno-honor-nans"]}
+# finite, so max/min need no NaN canonicalisation.  The fp64 observation pass
+# keeps its accumulators in VGPRs too (its softmax reads every logit, and the
+# copies out of accumulation registers cost as much as a tenth of its loop).
+EXTRA = {"encode_assign.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form", "-fno-honor-nans"],
+         "encode_obs64.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
 
 
 def _compile(src: str) -> str:

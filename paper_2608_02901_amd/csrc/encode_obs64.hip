@@ -13,7 +13,11 @@
 //                    softmax over the chunk on v_mfma_f64_16x16x4_f64:
 //                    S^T = K Q^T per 16-key tile (A = keys, B = queries), then
 //                    O^T += V^T P^T (A = values, B = the probabilities, which
-//                    the S^T accumulators already hold in the B layout);
+//                    the S^T accumulators already hold in the B layout).
+//                    The key and value tiles sit in LDS in fp32 (one
+//                    conversion to fp64 per operand), the query fragment in
+//                    fp32 registers, the accumulators in VGPRs, and the
+//                    softmax uses a table-driven exp (exp_tab);
 //   k_obs64_reduce : merges the chunk statistics and outputs of 16 rows and
 //                    derives the fp32 forms the epilogue uses.
 //
@@ -38,6 +42,39 @@ __device__ inline double e2d(const void* p, int i) {
   else return (double)((const float*)p)[i];
 }
 
+// exp(x) in fp64 for -inf < x <= 20, within a few ulp: x is clamped below at
+// -745 (the result underflows to zero there), then split as x = n ln2/64 + r
+// with n = round(64 x / ln2) and |r| <= ln2/128 (Cody-Waite: ln2/64 in a
+// 29-bit head, exact times any |n| < 2^24, and a tail), so that
+// exp(x) = 2^(n >> 6) * 2^((n & 63)/64) * e^r, e^r by its degree-6 Taylor
+// polynomial (truncation below 1e-19 relative) and 2^(j/64) from a table of
+// 64 values.  About half the instructions of the library exp, which also
+// guards the overflow range that the softmax here never reaches.
+__device__ inline double exp_tab(double x, const double* tab) {
+  constexpr double L64E = 92.332482616893656;                 // 64 / ln2
+  constexpr double LN2H = 0.010830424696905538;               // ln2/64, head (0x3f862e42ff000000)
+  constexpr double LN2L = -6.563929801064195e-13;             // ln2/64 - head
+  x = fmax(x, -745.0);
+  const double n = __builtin_rint(x * L64E);
+  double r = fma(-n, LN2H, x);
+  r = fma(-n, LN2L, r);
+  const int ni = (int)n;
+  double p = 1.0 / 720;
+  p = fma(p, r, 1.0 / 120);
+  p = fma(p, r, 1.0 / 24);
+  p = fma(p, r, 1.0 / 6);
+  p = fma(p, r, 0.5);
+  p = fma(p, r, 1.0);
+  p = fma(p, r, 1.0);
+  return ldexp(tab[ni & 63] * p, ni >> 6);
+}
+
+// Four bf16 values (two packed words) as fp32.
+__device__ inline float4 bf16x4_f(unsigned a, unsigned b) {
+  return float4{__uint_as_float(a << 16), __uint_as_float(a & 0xFFFF0000u), __uint_as_float(b << 16),
+                __uint_as_float(b & 0xFFFF0000u)};
+}
+
 __device__ inline f64x4 mfma64(double a, double b, f64x4 c) {
   return __builtin_amdgcn_mfma_f64_16x16x4f64(a, b, c, 0, 0, 0);
 }
@@ -46,11 +83,15 @@ template <int DT>
 __global__ __launch_bounds__(256) void k_obs64(Geo g, Ws w, const void* Kin, const void* Vin, const void* Qin) {
   using E = typename Elem<DT>::T;
   constexpr int PER = 16 / sizeof(E);      // elements per 16-byte chunk
-  constexpr int LDK = AKV_D + PER;         // LDS row stride in elements (one chunk of padding)
+  constexpr int LDK = AKV_D + 4;           // LDS row stride in floats (16 bytes of padding)
   constexpr int CPR = AKV_D / PER;         // chunks per row
   constexpr int NLD = O64_KT * CPR / 256;  // chunks per thread per tile and side
-  __shared__ __align__(16) E KT[2][O64_KT * LDK];
-  __shared__ __align__(16) E VT[2][O64_KT * LDK];
+  // key and value tiles in fp32 (bf16 widened once per tile, exactly), so
+  // that the contractions convert each element with one instruction
+  __shared__ __align__(16) float KT[2][O64_KT * LDK];
+  __shared__ __align__(16) float VT[2][O64_KT * LDK];
+  __shared__ double etab[64];  // 2^(j/64), the table of exp_tab
+  if (threadIdx.x < 64) etab[threadIdx.x] = exp2(threadIdx.x / 64.0);
   const int nrg = (g.m + 63) / 64;
   int idx = blockIdx.x;
   int b = 0;
@@ -76,11 +117,21 @@ __global__ __launch_bounds__(256) void k_obs64(Geo g, Ws w, const void* Kin, con
 
   // Query fragment of the lane: Q[row][32 kq + s], s = 0..31 (the contraction
   // index d = 32 (l/16) + s, the same bijection on both operands).
-  uint4 qraw[32 / PER];
+  float qf[32];
   {
     const E* qr = Q + (size_t)min(row, m - 1) * D + 32 * kq;
 #pragma unroll
-    for (int c = 0; c < 32 / PER; ++c) qraw[c] = *(const uint4*)(qr + c * PER);
+    for (int c = 0; c < 32 / PER; ++c) {
+      const uint4 v = *(const uint4*)(qr + c * PER);
+      if constexpr (DT == 1) {
+        const float4 a = bf16x4_f(v.x, v.y), bq = bf16x4_f(v.z, v.w);
+        qf[8 * c] = a.x; qf[8 * c + 1] = a.y; qf[8 * c + 2] = a.z; qf[8 * c + 3] = a.w;
+        qf[8 * c + 4] = bq.x; qf[8 * c + 5] = bq.y; qf[8 * c + 6] = bq.z; qf[8 * c + 7] = bq.w;
+      } else {
+        qf[4 * c] = __uint_as_float(v.x); qf[4 * c + 1] = __uint_as_float(v.y);
+        qf[4 * c + 2] = __uint_as_float(v.z); qf[4 * c + 3] = __uint_as_float(v.w);
+      }
+    }
   }
 
   const int tb = ch * g.oc64, te = min(S, tb + g.oc64);
@@ -98,8 +149,16 @@ __global__ __launch_bounds__(256) void k_obs64(Geo g, Ws w, const void* Kin, con
 #pragma unroll
     for (int i = 0; i < NLD; ++i) {
       const int c = threadIdx.x + 256 * i, r = c / CPR, col = (c % CPR) * PER;
-      *(uint4*)&KT[buf][r * LDK + col] = kpre[i];
-      *(uint4*)&VT[buf][r * LDK + col] = vpre[i];
+      if constexpr (DT == 1) {
+        const uint4 k = kpre[i], v = vpre[i];
+        *(float4*)&KT[buf][r * LDK + col] = bf16x4_f(k.x, k.y);
+        *(float4*)&KT[buf][r * LDK + col + 4] = bf16x4_f(k.z, k.w);
+        *(float4*)&VT[buf][r * LDK + col] = bf16x4_f(v.x, v.y);
+        *(float4*)&VT[buf][r * LDK + col + 4] = bf16x4_f(v.z, v.w);
+      } else {
+        *(uint4*)&KT[buf][r * LDK + col] = kpre[i];
+        *(uint4*)&VT[buf][r * LDK + col] = vpre[i];
+      }
     }
   };
 
@@ -123,21 +182,25 @@ __global__ __launch_bounds__(256) void k_obs64(Geo g, Ws w, const void* Kin, con
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
       // ---- logits: register r of acc is key t0 + 16u + kq + 4r against row l%16
-      uint4 kraw[32 / PER];
-      const E* kr = &KT[cb][(16 * u + (lane & 15)) * LDK + 32 * kq];
+      const float* kr = &KT[cb][(16 * u + (lane & 15)) * LDK + 32 * kq];
+      // The query fragment stays in fp32: widening it to fp64 once outside
+      // the loop would hold 32 more registers for the whole chunk.
 #pragma unroll
-      for (int c = 0; c < 32 / PER; ++c) kraw[c] = *(const uint4*)(kr + c * PER);
-      // The query fragment stays packed: converting it once outside the loop
-      // would hold 64 more registers for the whole chunk.
-#pragma unroll
-      for (int c = 0; c < 32 / PER; ++c)
-        asm volatile("" : "+v"(qraw[c].x), "+v"(qraw[c].y), "+v"(qraw[c].z), "+v"(qraw[c].w));
+      for (int s = 0; s < 32; ++s) asm volatile("" : "+v"(qf[s]));
       // two independent accumulation chains (even and odd s)
       f64x4 acc = {0.0, 0.0, 0.0, 0.0}, acc1 = {0.0, 0.0, 0.0, 0.0};
+      // the key fragment in two halves of 16 floats (fewer registers live)
 #pragma unroll
-      for (int s = 0; s < 32; s += 2) {
-        acc = mfma64(e2d<DT>(kraw, s), e2d<DT>(qraw, s), acc);
-        acc1 = mfma64(e2d<DT>(kraw, s + 1), e2d<DT>(qraw, s + 1), acc1);
+      for (int hf = 0; hf < 2; ++hf) {
+        float4 kraw[4];
+#pragma unroll
+        for (int c = 0; c < 4; ++c) kraw[c] = *(const float4*)(kr + 16 * hf + 4 * c);
+#pragma unroll
+        for (int s = 0; s < 16; s += 2) {
+          acc = mfma64((double)((const float*)kraw)[s], (double)qf[16 * hf + s], acc);
+          acc1 = mfma64((double)((const float*)kraw)[s + 1], (double)qf[16 * hf + s + 1], acc1);
+        }
+        __builtin_amdgcn_sched_barrier(0);
       }
       acc += acc1;
       double lg[4];
@@ -167,7 +230,8 @@ __global__ __launch_bounds__(256) void k_obs64(Geo g, Ws w, const void* Kin, con
       double p[4];
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        p[r] = ok[r] ? exp(lg[r] - mrow) : 0.0;
+        const double e = exp_tab(lg[r] - mrow, etab);
+        p[r] = ok[r] ? e : 0.0;
         zl += p[r];
       }
       // ---- values: MFMA r contracts the keys 16u + kq + 4r (k = kq); lane l
@@ -175,12 +239,11 @@ __global__ __launch_bounds__(256) void k_obs64(Geo g, Ws w, const void* Kin, con
       // register r' of O[blk] is O^T[dim 8 (l/16 + 4 r') + blk][row l%16].
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const E* vr = &VT[cb][(16 * u + kq + 4 * r) * LDK + 8 * (lane & 15)];
-        uint4 vraw[8 / PER];
+        const float* vr = &VT[cb][(16 * u + kq + 4 * r) * LDK + 8 * (lane & 15)];
+        const float4 v0 = *(const float4*)vr, v1 = *(const float4*)(vr + 4);
+        const float vf[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
 #pragma unroll
-        for (int c = 0; c < 8 / PER; ++c) vraw[c] = *(const uint4*)(vr + c * PER);
-#pragma unroll
-        for (int blk = 0; blk < 8; ++blk) O[blk] = mfma64(e2d<DT>(vraw, blk), p[r], O[blk]);
+        for (int blk = 0; blk < 8; ++blk) O[blk] = mfma64((double)vf[blk], p[r], O[blk]);
       }
     }
   }
