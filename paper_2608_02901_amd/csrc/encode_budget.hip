@@ -324,13 +324,24 @@ __global__ __launch_bounds__(1024) void k_bcut(Geo g, Ws w, Cache c) {
         if (__float_as_uint(u[e]) == prefix) atomicAdd(&hist[e / BCHUNK - c0], 1u);
     }
     __syncthreads();
-    if (threadIdx.x == 0) {
-      for (int i = c0; i < c1; ++i) {
-        const int v = (int)hist[i - c0];
-        tc[i] = carry;
-        carry += v;
+    // exclusive scan of the round's counts: each thread takes `per`
+    // consecutive chunks
+    const int ncc = c1 - c0, per = (ncc + (int)blockDim.x - 1) / (int)blockDim.x;
+    int loc = 0;
+    for (int i = 0; i < per; ++i) {
+      const int ci = (int)threadIdx.x * per + i;
+      if (ci < ncc) loc += (int)hist[ci];
+    }
+    int tot;
+    int run = carry + block_excl_scan(loc, tmp, tot);
+    for (int i = 0; i < per; ++i) {
+      const int ci = (int)threadIdx.x * per + i;
+      if (ci < ncc) {
+        tc[c0 + ci] = run;
+        run += (int)hist[ci];
       }
     }
+    carry += tot;
     __syncthreads();
   }
   if (threadIdx.x == 0) {
@@ -354,12 +365,24 @@ __global__ __launch_bounds__(256) void k_bbound(Geo g, Ws w) {
   const size_t base = bbase(g, q, side);
   const int e0 = ch * BCHUNK, e1 = min(n, e0 + BCHUNK);
   unsigned amin = 0x7F800000u, bmax = 0u;
-  for (int e = e0 + threadIdx.x; e < e1; e += blockDim.x) {
-    const float v = w.u[base + e];
-    if (!(v >= 0.0f)) continue;
-    const uint32_t vb = __float_as_uint(v);
-    if (vb >= T) amin = min(amin, __float_as_uint(w.uL[base + e]));
-    if (vb <= T) bmax = max(bmax, __float_as_uint(w.uU[base + e]));
+  // the chunk's 16 elements per thread: estimates and both bounds are loaded
+  // before any is compared (positions past the list end are skipped)
+  constexpr int per = BCHUNK / 256;
+  float v[per];
+  unsigned lb[per], ub[per];
+#pragma unroll
+  for (int j = 0; j < per; ++j) {
+    const int e = min(e0 + j * 256 + (int)threadIdx.x, e1 - 1);
+    v[j] = w.u[base + e];
+    lb[j] = __float_as_uint(w.uL[base + e]);
+    ub[j] = __float_as_uint(w.uU[base + e]);
+  }
+#pragma unroll
+  for (int j = 0; j < per; ++j) {
+    if (!(e0 + j * 256 + (int)threadIdx.x < e1 && v[j] >= 0.0f)) continue;
+    const uint32_t vb = __float_as_uint(v[j]);
+    if (vb >= T) amin = min(amin, lb[j]);
+    if (vb <= T) bmax = max(bmax, ub[j]);
   }
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) {
@@ -468,12 +491,13 @@ __global__ __launch_bounds__(256) void k_bmark(Geo g, Ws w) {
 // Sequential fp64 dots of a query row (16-byte chunks, chunk c at q4[c m]) with the
 // member's key row x and, when R is set, its residual r (both fp64 in LDS):
 // l = sum_j q_j x_j and qr = sum_j q_j r_j, products rounded, then added in
-// j order.  The row is loaded 16 chunks at a time (the whole bf16 row, half
-// an fp32 row) before any is consumed; the scheduling fences keep each
+// j order.  The row is loaded 8 chunks at a time (half a bf16 row) before
+// any is consumed (with 16 the kernel needs more than 168 registers and fits
+// two waves per SIMD instead of three); the scheduling fences keep each
 // chunk's LDS operands from being read ahead of earlier chunks' work.
 template <int DT, bool R>
 __device__ inline void qrow_dots(const u32x4* q4, int m, const double* xd, const double* rr, double& l, double& qr) {
-  constexpr int PER = 16 / sizeof(typename Elem<DT>::T), NC = AKV_D / PER, QB = 16;
+  constexpr int PER = 16 / sizeof(typename Elem<DT>::T), NC = AKV_D / PER, QB = 8;
 #pragma unroll 1
   for (int c0 = 0; c0 < NC; c0 += QB) {
     u32x4 qc[QB];
@@ -671,8 +695,20 @@ __global__ __launch_bounds__(RANK_T) void k_brank(Geo g, Ws w) {
         const double ui = bu[i];
         const int pi = bp[i];
         const int nj = min(RANK_T, n - tj * RANK_T);
+        // eight members per step, read before any is compared, no branches
         int r = 0;
-        for (int jj = 0; jj < nj; ++jj) r += (su[jj] > ui || (su[jj] == ui && sp[jj] < pi)) ? 1 : 0;
+        for (int j0 = 0; j0 < nj; j0 += 8) {
+          double uj[8];
+          int pj[8];
+#pragma unroll
+          for (int u = 0; u < 8; ++u) {
+            uj[u] = su[j0 + u];
+            pj[u] = sp[j0 + u];
+          }
+#pragma unroll
+          for (int u = 0; u < 8; ++u)
+            r += (j0 + u < nj) & ((uj[u] > ui) | ((uj[u] == ui) & (pj[u] < pi)));
+        }
         if (r) atomicAdd(&br[i], r);
       }
     }
