@@ -497,6 +497,24 @@ __device__ inline int block_excl_scan(int v, int* tmp /* >= 16 ints */, int& tot
   return r;
 }
 
+// Workgroup copy of n (>= 1) elements from global memory to LDS.  A strided
+// loop of single copies waits for every load before its store (the trip count
+// is not known at compile time, so nothing is unrolled); here each thread
+// issues eight loads (indices clamped to the last element) before it stores
+// any, so eight elements cost one memory round trip.
+template <typename T>
+__device__ inline void stage_lds(T* dst, const T* src, int n) {
+  const int nt = blockDim.x;
+  for (int i0 = threadIdx.x; i0 < n; i0 += 8 * nt) {
+    T v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v[u] = src[min(i0 + u * nt, n - 1)];
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      if (i0 + u * nt < n) dst[i0 + u * nt] = v[u];
+  }
+}
+
 // Radix digit search over a 4096-bin histogram: the bin where the running
 // count (from the top when `desc`, else from the bottom) reaches `need`.
 // Writes (bin, count before it) to out[0..1], or (-1, 0) when the total is

@@ -225,7 +225,7 @@ __global__ __launch_bounds__(256) void k_bcand(Geo g, Ws w) {
   if (bmode(g, q, side) != 0) return;
   const int bs = L * 2 + side;
   const uint32_t* gh = w.bhist + (size_t)bs * SEL_NBIN;
-  for (int i = threadIdx.x; i < SEL_NBIN; i += blockDim.x) hist[i] = gh[i];
+  stage_lds(hist, gh, SEL_NBIN);
   __syncthreads();
   digit_pick(hist, SEL_NBIN, nside(g, q, side), true, tmp, pick);
   const uint32_t bin1 = (uint32_t)pick[0];
@@ -268,7 +268,7 @@ __global__ __launch_bounds__(1024) void k_bcut(Geo g, Ws w, Cache c) {
   if (bmode(g, q, side) != 0) return;
   const int N = nside(g, q, side);
   const uint32_t* gh = w.bhist + (size_t)bs * SEL_NBIN;
-  for (int i = threadIdx.x; i < SEL_NBIN; i += blockDim.x) hist[i] = gh[i];
+  stage_lds(hist, gh, SEL_NBIN);
   __syncthreads();
   digit_pick(hist, SEL_NBIN, N, true, tmp, pick);
   if (pick[0] < 0) {  // fewer candidates than N: cannot happen with N < candidates

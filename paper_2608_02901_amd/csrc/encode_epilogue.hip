@@ -172,9 +172,20 @@ __global__ __launch_bounds__(256, R == 1 ? 2 : 1) void k_epilogue(Geo g, Ws w, C
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
 
   const E* Q = (const E*)Qin + ((size_t)b * g.Hq + (size_t)h * g.g) * g.W * D;
-  for (int ch = threadIdx.x; ch < m * CPR; ch += 256) {
-    const int r = ch / CPR, col = (ch % CPR) * PER;
-    *(uint4*)(&QS[r * LD + col]) = *(const uint4*)(Q + (size_t)r * D + col);
+  // the observation rows into LDS (row stride LD), eight 16-byte loads in
+  // flight per thread before any is stored
+  for (int c0 = threadIdx.x; c0 < m * CPR; c0 += 8 * 256) {
+    u32x4 qv[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int ch = min(c0 + 256 * u, m * CPR - 1);
+      qv[u] = *(const u32x4*)(Q + (size_t)(ch / CPR) * D + (ch % CPR) * PER);
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int ch = c0 + 256 * u;
+      if (ch < m * CPR) *(u32x4*)(&QS[(ch / CPR) * LD + (ch % CPR) * PER]) = qv[u];
+    }
   }
 
   for (int tl = threadIdx.x; tl < EPI_TOK; tl += 256) {

@@ -78,8 +78,7 @@ __global__ __launch_bounds__(256) void k_sel_band(Geo g, Ws w, const void* Kin, 
   const bool kst = (size_t)nk * AKV_D * sizeof(E) <= SEL_KLDS;
   E* qs = (E*)qlds;
   E* ks = (E*)klds;
-  if (qst)
-    for (int c = tid; c < m * NCH; c += nt) ((uint4*)qs)[c] = ((const uint4*)Q)[c];
+  if (qst) stage_lds((uint4*)qs, (const uint4*)Q, m * NCH);
   if (kst)
     for (int c = tid; c < nk * NCH; c += nt) {
       const int u = min(max(t + c / NCH - half, 0), P - 1);
@@ -113,8 +112,15 @@ __global__ __launch_bounds__(256) void k_sel_band(Geo g, Ws w, const void* Kin, 
   part[tid] = acc;
   __syncthreads();
   if (tid == 0) {
+    // in thread order, the partials read 16 at a time (nt is a multiple of 16)
     double tot = 0.0;
-    for (int r = 0; r < nt; ++r) tot += part[r];
+    for (int r0 = 0; r0 < nt; r0 += 16) {
+      double pv[16];
+#pragma unroll
+      for (int u = 0; u < 16; ++u) pv[u] = part[r0 + u];
+#pragma unroll
+      for (int u = 0; u < 16; ++u) tot += pv[u];
+    }
     w.sbscore[(size_t)bh * SEL_BAND_MAX + i] = tot / (double)m / (double)g.kappa;
   }
 }
@@ -158,7 +164,7 @@ __device__ inline int wave_append(bool take, int32_t* count) {
 // The bin of a head's summed histogram where the running count (from the
 // top when `desc`) reaches `need`, and the count before it; whole workgroup.
 __device__ inline void pick_global(const uint32_t* gh, uint32_t* hist, int need, bool desc, int* tmp, int* pick) {
-  for (int i = threadIdx.x; i < SEL_NBIN; i += blockDim.x) hist[i] = gh[i];
+  stage_lds(hist, gh, SEL_NBIN);
   __syncthreads();
   digit_pick(hist, SEL_NBIN, need, desc, tmp, pick);
 }
@@ -182,10 +188,18 @@ __global__ __launch_bounds__(256) void k_sel_pool(Geo g, Ws w, int override_anch
   const int half = g.kappa / 2;
   const float* sc = w.sc + q.so;
   float* pooled = w.u + q.so;  // the utility buffer is free until the epilogue
+  // the slice's scores and halo, eight loads in flight per thread (indices
+  // clamped into the head's row; positions outside [0, P) read as 0)
   const int ntile = q.t1 - q.t0 + 2 * half;
-  for (int j = tid; j < ntile; j += nt) {
-    const int u = q.t0 - half + j;
-    stile[j] = (u >= 0 && u < q.P) ? sc[u] : 0.0f;
+  for (int j0 = tid; j0 < ntile; j0 += 8 * nt) {
+    float v[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = sc[min(max(q.t0 - half + j0 + e * nt, 0), max(q.P - 1, 0))];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int j = j0 + e * nt, u = q.t0 - half + j;
+      if (j < ntile) stile[j] = (u >= 0 && u < q.P) ? v[e] : 0.0f;
+    }
   }
   for (int i = tid; i < SEL_NBIN; i += nt) hist[i] = 0;
   __syncthreads();
