@@ -204,10 +204,13 @@ __global__ __launch_bounds__(256) void k_bhist(Geo g, Ws w) {
   const int n = q.n;
   const float* u = w.u + bbase(g, q, side);
   const int e0 = ch * BCHUNK, e1 = min(n, e0 + BCHUNK);
-  for (int e = e0 + threadIdx.x; e < e1; e += blockDim.x) {
-    const float v = u[e];
-    if (v >= 0.0f) atomicAdd(&hist[__float_as_uint(v) >> 20], 1u);
-  }
+  constexpr int per = BCHUNK / 256;  // all loads issued before any is counted
+  float v[per];
+#pragma unroll
+  for (int j = 0; j < per; ++j) v[j] = u[min(e0 + j * 256 + (int)threadIdx.x, e1 - 1)];
+#pragma unroll
+  for (int j = 0; j < per; ++j)
+    if (e0 + j * 256 + (int)threadIdx.x < e1 && v[j] >= 0.0f) atomicAdd(&hist[__float_as_uint(v[j]) >> 20], 1u);
   __syncthreads();
   uint32_t* gh = w.bhist + (size_t)(L * 2 + side) * SEL_NBIN;
   for (int i = threadIdx.x; i < SEL_NBIN; i += blockDim.x)
@@ -408,6 +411,11 @@ __global__ __launch_bounds__(256) void k_bbound(Geo g, Ws w) {
 __global__ __launch_bounds__(256) void k_bmark(Geo g, Ws w) {
   __shared__ int wtot[4];
   __shared__ int tmp[8];
+  // the chunk's estimates and bounds, read coalesced and then taken by each
+  // thread as 16 consecutive elements; the marks go back the same way
+  __shared__ __align__(16) float s_u[BCHUNK];
+  __shared__ __align__(16) uint32_t s_lb[BCHUNK], s_ub[BCHUNK];
+  __shared__ __align__(16) uint8_t s_sel[BCHUNK];
   int idx = blockIdx.x;
   const int L = locate_l(g, idx);
   const int side = idx & 1, ch = idx >> 1;
@@ -420,6 +428,7 @@ __global__ __launch_bounds__(256) void k_bmark(Geo g, Ws w) {
   const uint32_t A = (uint32_t)st[BST_A], Bb = (uint32_t)st[BST_B];
   const int n = q.n;
   const int32_t* tc = btie(g, w, L, q, side);
+  const int tie0 = mode == 0 ? tc[ch] : 0;  // threshold ties in the earlier chunks
   const size_t base = bbase(g, q, side);
   const float* u = w.u + base;
   uint8_t* sel = w.sel + base;
@@ -427,9 +436,37 @@ __global__ __launch_bounds__(256) void k_bmark(Geo g, Ws w) {
   // Each thread owns 16 consecutive elements; ranks of ties follow (h, t) order.
   constexpr int per = BCHUNK / 256;
   const int lo = e0 + threadIdx.x * per;
-  float v[per];
+  {
+    float cu[per];
+    uint32_t cl[per], ch2[per];
 #pragma unroll
-  for (int j = 0; j < per; ++j) v[j] = lo + j < e1 ? u[lo + j] : -1.0f;
+    for (int j = 0; j < per; ++j) {
+      const int e = min(e0 + j * 256 + (int)threadIdx.x, e1 - 1);
+      cu[j] = u[e];
+      cl[j] = mode == 0 ? __float_as_uint(w.uL[base + e]) : 0u;
+      ch2[j] = mode == 0 ? __float_as_uint(w.uU[base + e]) : 0u;
+    }
+#pragma unroll
+    for (int j = 0; j < per; ++j) {
+      const int i = j * 256 + threadIdx.x;
+      const bool in = e0 + i < e1;
+      s_u[i] = in ? cu[j] : -1.0f;
+      s_lb[i] = cl[j];
+      s_ub[i] = ch2[j];
+    }
+  }
+  __syncthreads();
+  float v[per];
+  uint32_t lbv[per], ubv[per];
+#pragma unroll
+  for (int j = 0; j < per; j += 4) {
+    const int i = threadIdx.x * per + j;
+    const float4 a4 = *(const float4*)&s_u[i];
+    const uint4 l4 = *(const uint4*)&s_lb[i], h4 = *(const uint4*)&s_ub[i];
+    v[j] = a4.x; v[j + 1] = a4.y; v[j + 2] = a4.z; v[j + 3] = a4.w;
+    lbv[j] = l4.x; lbv[j + 1] = l4.y; lbv[j + 2] = l4.z; lbv[j + 3] = l4.w;
+    ubv[j] = h4.x; ubv[j + 1] = h4.y; ubv[j + 2] = h4.z; ubv[j + 3] = h4.w;
+  }
   int eq = 0;
   if (mode == 0)
 #pragma unroll
@@ -442,15 +479,14 @@ __global__ __launch_bounds__(256) void k_bmark(Geo g, Ws w) {
   }
   if (lane == 63) wtot[wave] = x;
   __syncthreads();
-  int before = x - eq + (mode == 0 ? tc[ch] : 0);
+  int before = x - eq + tie0;
   for (int i = 0; i < wave; ++i) before += wtot[i];
   unsigned bandbits = 0;  // element j of the thread is a band member
   int nb = 0, nsel = 0;
 #pragma unroll
   for (int j = 0; j < per; ++j) {
-    if (lo + j >= e1) break;
     uint8_t s = 0;
-    if (v[j] >= 0.0f) {
+    if (lo + j < e1 && v[j] >= 0.0f) {  // (v is -1 past the list end as well)
       if (mode == 1) {
         s = 1;
       } else if (mode == 0) {
@@ -461,15 +497,20 @@ __global__ __launch_bounds__(256) void k_bmark(Geo g, Ws w) {
           s = before < need;
           ++before;
         }
-        const uint32_t lb = __float_as_uint(w.uL[base + lo + j]), ub = __float_as_uint(w.uU[base + lo + j]);
-        if (!(lb > Bb) && !(ub < A)) {
+        if (!(lbv[j] > Bb) && !(ubv[j] < A)) {
           bandbits |= 1u << j;
           ++nb;
           nsel += s;
         }
       }
     }
-    sel[lo + j] = s;
+    s_sel[threadIdx.x * per + j] = s;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < per; ++j) {
+    const int i = j * 256 + threadIdx.x;
+    if (e0 + i < e1) sel[e0 + i] = s_sel[i];
   }
   if (mode != 0) return;  // uniform per workgroup
   // List the band members (one slot reservation per workgroup).

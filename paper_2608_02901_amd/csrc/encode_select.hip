@@ -356,7 +356,15 @@ __global__ __launch_bounds__(256) void k_sel_rhist(Geo g, Ws w, Cache c) {
       sflag[t - q.t0] = f;
     }
   } else {
-    for (int t = q.t0 + tid; t < q.t1; t += nt) sflag[t - q.t0] = flag[t];
+    if (q.t1 > q.t0) {  // the slice's flags, all loaded before any is stored
+      constexpr int NJ = SEL_SLICE / 256;
+      uint8_t fv[NJ];
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) fv[j] = flag[min(q.t0 + j * 256 + tid, q.t1 - 1)];
+#pragma unroll
+      for (int j = 0; j < NJ; ++j)
+        if (q.t0 + j * 256 + tid < q.t1) sflag[j * 256 + tid] = fv[j];
+    }
     if (nb > 0) {
       const int need = ntop - st[SS_NABOVE];
       const int32_t* band = w.sband + (size_t)q.bh * SEL_BAND_MAX;
@@ -448,8 +456,10 @@ __global__ __launch_bounds__(256) void k_sel_rcand(Geo g, Ws w) {
 // scan of the per-wave counts); then the window.  The slice holding
 // position P - 1 (or the first slice when P = 0) checks the total.
 __global__ __launch_bounds__(256) void k_sel_list(Geo g, Ws w, Cache c) {
+  constexpr int NJ = SEL_SLICE / 256;  // positions per thread of the slice
   __shared__ uint32_t hist[SEL_NBIN];
-  __shared__ int tmp[8], pick[2], wc[4], wpre[5], basev, extra;
+  __shared__ unsigned long long skey[SEL_CAND];  // the bin's keys, staged for the ranking
+  __shared__ int tmp[8], pick[2], wc[NJ][4], wpre[NJ][4], wtot, basev, extra;
   const SelSlice q = sel_slice(g);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int W = g.W, k = g.k[q.b];
@@ -469,10 +479,13 @@ __global__ __launch_bounds__(256) void k_sel_list(Geo g, Ws w, Cache c) {
     const unsigned long long* ckey = w.rkey + (size_t)q.bh * SEL_CAND;
     const int32_t* cpos = w.rpos + (size_t)q.bh * SEL_CAND;
     if (nc <= SEL_CAND) {
+      if (nc > 0) stage_lds(skey, ckey, nc);
+      __syncthreads();
       int ex = 0;
       for (int i = tid; i < nc; i += blockDim.x) {
+        const unsigned long long ki = skey[i];
         int r = 0;
-        for (int j = 0; j < nc; ++j) r += ckey[j] < ckey[i];
+        for (int j = 0; j < nc; ++j) r += skey[j] < ki;
         if (r < need) {
           const int t = cpos[i];
           if (t < q.t0) ++ex;
@@ -529,29 +542,41 @@ __global__ __launch_bounds__(256) void k_sel_list(Geo g, Ws w, Cache c) {
   }
   __syncthreads();
   int base = basev + extra;
-  for (int t0 = q.t0; t0 < q.t1; t0 += blockDim.x) {
-    const int t = t0 + tid;
-    const bool f = t < q.t1 && flag[t] != 0;
-    const unsigned long long bal = __ballot(f);
-    if (lane == 0) wc[wave] = __popcll(bal);
-    __syncthreads();
-    if (tid == 0) {
-      int s = 0;
+  // The slice's flags, all loaded before any is used (one round trip), then
+  // the ranks of the flagged positions in position order: wave ballots per
+  // round of 256 positions and one scan over (round, wave).
+  uint8_t fl[NJ];
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) fl[j] = flag[min(q.t0 + j * 256 + tid, max(q.t1 - 1, 0))];
+  unsigned long long bal[NJ];
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) {
+    const int t = q.t0 + j * 256 + tid;
+    bal[j] = __ballot(t < q.t1 && fl[j] != 0);
+    if (lane == 0) wc[j][wave] = __popcll(bal[j]);
+  }
+  __syncthreads();
+  if (tid == 0) {
+    int s = 0;
+    for (int j = 0; j < NJ; ++j)
       for (int i = 0; i < 4; ++i) {
-        wpre[i] = s;
-        s += wc[i];
+        wpre[j][i] = s;
+        s += wc[j][i];
       }
-      wpre[4] = s;
-    }
-    __syncthreads();
-    const int r = base + wpre[wave] + __popcll(bal & ((1ull << lane) - 1ull));
+    wtot = s;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) {
+    const int t = q.t0 + j * 256 + tid;
+    const bool f = t < q.t1 && fl[j] != 0;
+    const int r = base + wpre[j][wave] + __popcll(bal[j] & ((1ull << lane) - 1ull));
     if (f && r < k - W) {
       anc[r] = t;
       rank[t] = r;
     }
-    base += wpre[4];
-    __syncthreads();
   }
+  base += wtot;
   const bool tail = q.P > 0 ? (q.t0 <= q.P - 1 && q.P - 1 < q.t0 + SEL_SLICE) : q.sl == 0;
   if (tail) {
     if (tid == 0 && base + W != k) atomicOr(&c.header[2], 2u);
