@@ -371,7 +371,7 @@ __global__ __launch_bounds__(256) void k_codec(Geo g, Ws w, Cache c, const void*
   const E* A = (const E*)(side ? c.ancV : c.ancK) + ko * D;
   uint8_t* codes = side ? c.codesV : c.codesK;
   float* scales = side ? c.scalesV : c.scalesK;
-  const float s0 = hsign(g.seed_sign, 2 * lane), s1 = hsign(g.seed_sign, 2 * lane + 1);
+  const float s0 = sign_bit(g.sgnbits, 2 * lane), s1 = sign_bit(g.sgnbits, 2 * lane + 1);
   // Position, anchor and coefficient of every slot of the word, one lane each
   // (clamped: padding slots of the last word hold no record and no flag).
   const int tj = min((int)(rec.x & 0x3FFFFFFFu), S - 1);
