@@ -63,7 +63,7 @@ __device__ __host__ inline size_t slot_base(const Geo& g, int b, int h) {
   return ((size_t)g.prefW[b] * g.H + (size_t)h * ((g.S[b] + 63) / 64)) * 64;
 }
 
-constexpr int OBS_CHUNK = 2048;   // tokens per observation-pass workgroup
+constexpr int OBS_CHUNK = 1024;   // tokens per observation-pass workgroup (1024 WGs per 128K layer: 4 waves per SIMD)
 constexpr int SEL_BAND_MAX = 256; // largest band re-scored in fp64 at the selection cut
 constexpr int SORT_CHUNK = 2048;  // tokens per counting-sort chunk
 constexpr int SEL_SLICE = 4096;   // positions per workgroup of the selection passes
