@@ -263,8 +263,10 @@ __device__ inline int wave_incl_scan_i(int v, int lane) {
   return v;
 }
 
+constexpr int FIX_NW = 8;  // waves per k_fixup workgroup (interleaved anchor tiles)
+
 template <int DT>
-__global__ __launch_bounds__(256) void k_fixup(Geo g, Ws w, Cache c, const void* Kin, const void* Vin) {
+__global__ __launch_bounds__(64 * FIX_NW) void k_fixup(Geo g, Ws w, Cache c, const void* Kin, const void* Vin) {
   using E = typename Elem<DT>::T;
   using M = MF<DT>;
   constexpr int NKS = AKV_D / M::KS;
@@ -342,9 +344,9 @@ __global__ __launch_bounds__(256) void k_fixup(Geo g, Ws w, Cache c, const void*
     const float eps = score_eps(ss, D) + tag_eps(b1);
     const float bnd = b1 - 2.0f * eps - b1 * 9.094947e-13f;
 
-    // Band collection: wave w takes anchor tiles w, w+4, ... (rows of the tile
-    // on M, tokens on N), prefetching two tiles ahead together with the
-    // inverse norms of the lane's 16 rows (rows past k read 0: score 0).
+    // Band collection: wave w takes anchor tiles w, w + FIX_NW, ... (rows of
+    // the tile on M, tokens on N), prefetching two tiles ahead together with
+    // the inverse norms of the lane's 16 rows (rows past k read 0: score 0).
     typename M::frag f0[NKS], f1[NKS];
     float i0[16], i1[16];
     auto fetch = [&](typename M::frag (&f)[NKS], float (&iv)[16], int a0) {
@@ -370,22 +372,23 @@ __global__ __launch_bounds__(256) void k_fixup(Geo g, Ws w, Cache c, const void*
         }
       }
     };
+    constexpr int TS = 32 * FIX_NW;  // anchors between a wave's consecutive tiles
     int a0 = wave * 32;
     if (a0 < k) fetch(f0, i0, a0);
-    if (a0 + 128 < k) fetch(f1, i1, a0 + 128);
-    for (; a0 < k; a0 += 256) {
+    if (a0 + TS < k) fetch(f1, i1, a0 + TS);
+    for (; a0 < k; a0 += 2 * TS) {
       tile(f0, i0, a0);
-      if (a0 + 256 < k) fetch(f0, i0, a0 + 256);
-      if (a0 + 128 >= k) break;
-      tile(f1, i1, a0 + 128);
-      if (a0 + 384 < k) fetch(f1, i1, a0 + 384);
+      if (a0 + 2 * TS < k) fetch(f0, i0, a0 + 2 * TS);
+      if (a0 + TS >= k) break;
+      tile(f1, i1, a0 + TS);
+      if (a0 + 3 * TS < k) fetch(f1, i1, a0 + 3 * TS);
     }
     __syncthreads();
 
     // Canonical fp64 scores of the band members (one thread per member).
     {
       const int pn = threadIdx.x / FIX_SLOTS, pj = threadIdx.x % FIX_SLOTS;
-      const int cn = ccnt[pn];
+      const int cn = pn < nr ? ccnt[pn] : 0;
       if (pn < nr && cn <= FIX_SLOTS && pj < cn) {
         const int a = cidx[pn][pj];
         const int tp = w.fixt[lo + r0 + pn];
@@ -451,10 +454,10 @@ hipError_t launch_assign(const Geo& g, const Ws& w, const Cache& c, const void* 
   for (int b = 0; b < g.B; ++b) nblk += g.H * ((g.S[b] + ASSIGN_TOK - 1) / ASSIGN_TOK) * 2;
   if (g.dtype == 1) {
     launch("k_assign", k_assign<1>, dim3(nblk), dim3(256), 0, st, g, w, c, K, V);
-    launch("k_fixup", k_fixup<1>, dim3(512), dim3(256), 0, st, g, w, c, K, V);
+    launch("k_fixup", k_fixup<1>, dim3(512), dim3(64 * FIX_NW), 0, st, g, w, c, K, V);
   } else {
     launch("k_assign", k_assign<0>, dim3(nblk), dim3(256), 0, st, g, w, c, K, V);
-    launch("k_fixup", k_fixup<0>, dim3(512), dim3(256), 0, st, g, w, c, K, V);
+    launch("k_fixup", k_fixup<0>, dim3(512), dim3(64 * FIX_NW), 0, st, g, w, c, K, V);
   }
   return hipGetLastError();
 }
