@@ -262,7 +262,8 @@ __global__ __launch_bounds__(256) void k_obs64(Geo g, Ws w, const void* Kin, con
     for (int r = 0; r < 4; ++r) op[(blk * 4 + r) * 64 + lane] = O[blk][r];
 }
 
-// One workgroup per (request, head, 16 rows, quarter of the dimensions):
+// One workgroup of 512 threads per (request, head, 16 rows, quarter of the
+// dimensions), one output per thread:
 // M_w = max of the chunk references, Z_w = sum_c Z_c exp(M_c - M_w) (every
 // quarter forms them alike), y_w = sum_c O_c exp(M_c - M_w) / Z_w over the
 // quarter's 32 dimensions (chunks in order), then the fp32 forms: y rounded
@@ -270,11 +271,12 @@ __global__ __launch_bounds__(256) void k_obs64(Geo g, Ws w, const void* Kin, con
 // first quarter also writes M_w, Z_w, (M + ln Z) log2(e), ||q_w|| and the
 // chunk-transposed copy of q_w (qt) that the band re-scoring reads.
 template <int DT>
-__global__ __launch_bounds__(256) void k_obs64_reduce(Geo g, Ws w, const void* Qin) {
+__global__ __launch_bounds__(512) void k_obs64_reduce(Geo g, Ws w, const void* Qin) {
   using E = typename Elem<DT>::T;
   __shared__ double scl[O64_MAXCH][16];
   __shared__ double red[16][16];
   __shared__ double Msh[16], Zsh[16];
+  __shared__ double ysq[256];  // y^2 of the upper half's outputs
   const int nrb = g.mpad / 16;
   const int qd = blockIdx.x & 3, blk16 = blockIdx.x >> 2;
   const int bh = blk16 / nrb, rb16 = blk16 % nrb, b = bh / g.H, h = bh % g.H;
@@ -284,10 +286,11 @@ __global__ __launch_bounds__(256) void k_obs64_reduce(Geo g, Ws w, const void* Q
   const int tid = threadIdx.x, r16 = tid & 15, part = tid >> 4;
   const int row = rb16 * 16 + r16;
   const bool rok = row < m;
+  const bool low = tid < 256;  // the row statistics use the first 256 threads
   double mx = O64_NEG;
-  if (rok)
+  if (low && rok)
     for (int c = part; c < nch; c += 16) mx = fmax(mx, w.o64M[(gc0 + c) * g.mpad + row]);
-  red[part][r16] = mx;
+  if (low) red[part][r16] = mx;
   __syncthreads();
   if (tid < 16) {
     double M = red[0][tid];
@@ -296,12 +299,13 @@ __global__ __launch_bounds__(256) void k_obs64_reduce(Geo g, Ws w, const void* Q
   }
   __syncthreads();
   double za = 0.0;
-  for (int c = part; c < nch; c += 16) {
-    const double s = rok ? exp(w.o64M[(gc0 + c) * g.mpad + row] - Msh[r16]) : 0.0;
-    scl[c][r16] = s;
-    za += rok ? w.o64Z[(gc0 + c) * g.mpad + row] * s : 0.0;
-  }
-  red[part][r16] = za;
+  if (low)
+    for (int c = part; c < nch; c += 16) {
+      const double s = rok ? exp(w.o64M[(gc0 + c) * g.mpad + row] - Msh[r16]) : 0.0;
+      scl[c][r16] = s;
+      za += rok ? w.o64Z[(gc0 + c) * g.mpad + row] * s : 0.0;
+    }
+  if (low) red[part][r16] = za;
   __syncthreads();
   if (tid < 16) {
     double Z = 0.0;
@@ -311,37 +315,25 @@ __global__ __launch_bounds__(256) void k_obs64_reduce(Geo g, Ws w, const void* Q
   __syncthreads();
   // Outputs: in the chunk layout, register slot (blk * 4 + r) of lane l holds
   // dimension 8 (l / 16 + 4 r) + blk of row l % 16; the quarter qd takes
-  // blk = 2 qd, 2 qd + 1 (512 contiguous values per chunk), two per thread.
+  // blk = 2 qd, 2 qd + 1 (512 contiguous values per chunk), one per thread
+  // (threads t and t + 256 hold the two blocks).
   const int lane = tid & 63;
   const size_t bhm = (size_t)bh * m;
-  double acc[2];
-  const double* op[2];
-#pragma unroll
-  for (int q = 0; q < 2; ++q) {
-    const int slot = 8 * qd + 4 * q + (tid >> 6);  // blk * 4 + r
-    op[q] = w.o64O + (gc0 * nrb + rb16) * 2048 + slot * 64 + lane;
-    acc[q] = 0.0;
-  }
+  const int slot = 8 * qd + (tid >> 6);  // blk * 4 + r
+  const double* op = w.o64O + (gc0 * nrb + rb16) * 2048 + slot * 64 + lane;
+  double acc = 0.0;
   const size_t cstride = (size_t)nrb * 2048;
   for (int c0 = 0; c0 < nch; c0 += 16) {
-    double v[16][2];
+    double v[16];
+#pragma unroll
+    for (int u = 0; u < 16; ++u) v[u] = c0 + u < nch ? op[(size_t)(c0 + u) * cstride] : 0.0;
 #pragma unroll
     for (int u = 0; u < 16; ++u)
-#pragma unroll
-      for (int q = 0; q < 2; ++q) v[u][q] = c0 + u < nch ? op[q][(size_t)(c0 + u) * cstride] : 0.0;
-#pragma unroll
-    for (int u = 0; u < 16; ++u)
-      if (c0 + u < nch) {
-        const double sc = scl[c0 + u][r16];
-#pragma unroll
-        for (int q = 0; q < 2; ++q) acc[q] += v[u][q] * sc;
-      }
+      if (c0 + u < nch) acc += v[u] * scl[c0 + u][r16];
   }
-  double sq = 0.0;
-#pragma unroll
-  for (int q = 0; q < 2; ++q) {
-    const int slot = 8 * qd + 4 * q + (tid >> 6), blk = slot >> 2, r = slot & 3;
-    const double y = acc[q] / Zsh[r16];
+  {
+    const int blk = slot >> 2, r = slot & 3;
+    const double y = acc / Zsh[r16];
     const int dim = 8 * ((lane >> 4) + 4 * r) + blk;
     if (rok) {
       const size_t o = (bhm + row) * D + dim;
@@ -352,10 +344,12 @@ __global__ __launch_bounds__(256) void k_obs64_reduce(Geo g, Ws w, const void* Q
       w.Yhi[o] = hi;
       w.Ylo[o] = f2bf(y32 - bf2f(hi));
     }
-    sq += y * y;
+    acc = y * y;
   }
+  // per thread of the lower half: y^2 of its block, then that of its partner
+  if (!low) ysq[tid - 256] = acc;
   __syncthreads();
-  red[part][r16] = sq;
+  if (low) red[part][r16] = acc + ysq[tid];
   __syncthreads();
   if (tid < 16 && rok) {
     double t = 0.0;
@@ -363,23 +357,26 @@ __global__ __launch_bounds__(256) void k_obs64_reduce(Geo g, Ws w, const void* Q
     w.ynp[(bhm + rb16 * 16 + tid) * 4 + qd] = t;
   }
   if (qd == 0) {
-    // ||q_w||: 16 threads per row, 8 coordinates each, then a fixed-order sum
+    // ||q_w||: 16 threads per row (the lower half), 8 coordinates each, then
+    // a fixed-order sum
     __syncthreads();
     const E* q = (const E*)Qin + ((size_t)b * g.Hq + (size_t)h * g.g) * g.W * D + (size_t)min(row, m - 1) * D;
-    double qq = 0.0;
-    for (int j = 8 * part; j < 8 * part + 8; ++j) {
-      const double x = e2d<DT>(q, j);
-      qq += x * x;
-    }
-    // the same 8 coordinates: one 16-byte chunk (bf16) or two (fp32)
-    constexpr int CPT = sizeof(E) / 2, NCH = AKV_D * sizeof(E) / 16;
-    if (rok)
-#pragma unroll
-      for (int u = 0; u < CPT; ++u) {
-        const int c = part * CPT + u;
-        ((u32x4*)w.qt)[((size_t)bh * NCH + c) * m + row] = ((const u32x4*)q)[c];
+    if (low) {
+      double qq = 0.0;
+      for (int j = 8 * part; j < 8 * part + 8; ++j) {
+        const double x = e2d<DT>(q, j);
+        qq += x * x;
       }
-    red[part][r16] = qq;
+      // the same 8 coordinates: one 16-byte chunk (bf16) or two (fp32)
+      constexpr int CPT = sizeof(E) / 2, NCH = AKV_D * sizeof(E) / 16;
+      if (rok)
+#pragma unroll
+        for (int u = 0; u < CPT; ++u) {
+          const int c = part * CPT + u;
+          ((u32x4*)w.qt)[((size_t)bh * NCH + c) * m + row] = ((const u32x4*)q)[c];
+        }
+      red[part][r16] = qq;
+    }
     __syncthreads();
     if (tid < 16 && rok) {
       double t = 0.0;
@@ -400,10 +397,10 @@ hipError_t launch_obs64(const Geo& g, const Ws& w, const void* K, const void* V,
   const int nred = g.B * g.H * (g.mpad / 16) * 4;
   if (g.dtype == 1) {
     launch("k_obs64", k_obs64<1>, dim3(nblk), dim3(256), 0, st, g, w, K, V, Q);
-    launch("k_obs64_reduce", k_obs64_reduce<1>, dim3(nred), dim3(256), 0, st, g, w, Q);
+    launch("k_obs64_reduce", k_obs64_reduce<1>, dim3(nred), dim3(512), 0, st, g, w, Q);
   } else {
     launch("k_obs64", k_obs64<0>, dim3(nblk), dim3(256), 0, st, g, w, K, V, Q);
-    launch("k_obs64_reduce", k_obs64_reduce<0>, dim3(nred), dim3(256), 0, st, g, w, Q);
+    launch("k_obs64_reduce", k_obs64_reduce<0>, dim3(nred), dim3(512), 0, st, g, w, Q);
   }
   return hipGetLastError();
 }
