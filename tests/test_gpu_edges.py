@@ -37,6 +37,11 @@ EDGES = {
     "gqa8_group32": (_wl("gqa8_group32", Hq=16, quant_group=32), {}),
     "almost_all_anchors": (_wl("almost_all_anchors", seq_lens=[300], anchor_count=290, anchor_frac=0.0), {}),
     "f32_gqa1": (_wl("f32_gqa1", H=2, Hq=2, dtype="f32", n_outlier=0), {}),
+    # observation row counts that are not a multiple of 16 (padded row blocks
+    # of the observation passes, ragged lanes of the band re-score)
+    "rows15": (_wl("rows15", H=2, Hq=2, window=15), {}),
+    "rows20_gqa4": (_wl("rows20_gqa4", H=2, Hq=8, window=5), {}),
+    "f32_rows7": (_wl("f32_rows7", H=2, Hq=2, window=7, dtype="f32", n_outlier=0), {}),
 }
 
 
